@@ -1,0 +1,137 @@
+"""ctypes binding for the WHTMix CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+The oracle (``whtmix_oracle.c``) is a plain double-precision statement of the
+Walsh-Hadamard token mixer of section III-B (eqs. (2)-(3)).  Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+this module.  The product path (``paper_2607_25234_amd``) never imports it.
+
+``build()`` compiles the C source with gcc into ``liboracle.so`` beside it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "whtmix_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(src: str = SRC, out: str = LIB, extra_flags: tuple = ()) -> str:
+    """Compile the oracle with gcc (OpenMP, no fast-math, no FP contraction)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+           *extra_flags, src, "-o", out + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def load(path: str = LIB):
+    """Load a compiled oracle library (building the default one if absent)."""
+    global _lib
+    if path == LIB and _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        if path != LIB:
+            raise FileNotFoundError(path)
+        build()
+    lib = ctypes.CDLL(path)
+    dp = ctypes.POINTER(ctypes.c_double)
+    L = ctypes.c_long
+    lib.oracle_whtmix.argtypes = [dp, dp, dp, L, L, L]
+    lib.oracle_whtmix.restype = ctypes.c_int
+    lib.oracle_whtmix_separable.argtypes = [dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_separable.restype = ctypes.c_int
+    lib.oracle_fwht.argtypes = [dp, L]
+    lib.oracle_fwht.restype = ctypes.c_int
+    if path == LIB:
+        _lib = lib
+    return lib
+
+
+def _dptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _as_f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+class Oracle:
+    """Thin wrapper over one compiled oracle library (default: liboracle.so)."""
+
+    def __init__(self, path: str = LIB):
+        self.lib = load(path)
+
+    def whtmix(self, x, g) -> np.ndarray:
+        """Y[b] = H_N (G o (H_N X[b] H_C)) H_C in float64.
+
+        x: [B, N, C] or [N, C]; g: [N, C].  Returns float64 of x's shape."""
+        x64 = _as_f64(x)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64 = x64[None]
+        B, N, C = x64.shape
+        g64 = _as_f64(g)
+        if g64.shape != (N, C):
+            raise ValueError(f"gain shape {g64.shape} != {(N, C)}")
+        y = np.empty_like(x64)
+        rc = self.lib.oracle_whtmix(_dptr(x64), _dptr(g64), _dptr(y), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix rejected shape {(B, N, C)}")
+        return y[0] if squeeze else y
+
+    def whtmix_separable(self, x, g_t, g_c) -> np.ndarray:
+        """The paper's eq. (2) then eq. (3) with log-domain gains g_t[N], g_c[C]."""
+        x64 = _as_f64(x)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64 = x64[None]
+        B, N, C = x64.shape
+        gt = _as_f64(g_t).reshape(-1)
+        gc = _as_f64(g_c).reshape(-1)
+        if gt.shape != (N,) or gc.shape != (C,):
+            raise ValueError("g_t must have N entries and g_c C entries")
+        y = np.empty_like(x64)
+        rc = self.lib.oracle_whtmix_separable(_dptr(x64), _dptr(gt), _dptr(gc),
+                                              _dptr(y), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_separable rejected {(B, N, C)}")
+        return y[0] if squeeze else y
+
+    def fwht(self, v) -> np.ndarray:
+        """Unnormalised Sylvester butterfly of a 1-D vector (H_n v, +/-1 H)."""
+        v64 = _as_f64(v).copy()
+        if v64.ndim != 1:
+            raise ValueError("fwht takes a 1-D vector")
+        rc = self.lib.oracle_fwht(_dptr(v64), v64.shape[0])
+        if rc != 0:
+            raise ValueError("length must be a power of two")
+        return v64
+
+
+_default = None
+
+
+def default() -> Oracle:
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default
+
+
+def whtmix(x, g) -> np.ndarray:
+    return default().whtmix(x, g)
+
+
+def whtmix_separable(x, g_t, g_c) -> np.ndarray:
+    return default().whtmix_separable(x, g_t, g_c)
+
+
+def fwht(v) -> np.ndarray:
+    return default().fwht(v)

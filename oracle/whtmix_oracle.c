@@ -1,0 +1,150 @@
+/*
+ * WHTMix CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, double-precision statement of the Walsh-Hadamard token mixer
+ * (Method, section III-B, eqs. (2)-(3)).  Only the test suite, the smoke check
+ * and the CPU-baseline leg of the benchmark may load this library; the product
+ * path (the HIP library) never calls it, and the two share no code, headers or
+ * build steps.
+ *
+ * What the paper fixes:
+ *   - H is the orthonormal Walsh-Hadamard transform: the Sylvester-Hadamard
+ *     matrix divided by sqrt(n), n a power of two, applied by an O(n log n)
+ *     butterfly (section III-B, first paragraph).
+ *   - Sylvester order is natural Hadamard order: H_1 = [1],
+ *     H_2n = [[H_n, H_n], [H_n, -H_n]], so entry (i, j) is
+ *     (-1)^popcount(i & j) / sqrt(n).  No bit reversal is involved.
+ *   - Channel mixing (eq. 2) acts along each token row of X in R^{N x C};
+ *     token mixing (eq. 3) acts along each channel column.
+ *   - Both transforms are orthonormal and H^{-1} = H (H is symmetric and
+ *     orthogonal), so the "inverse" transform is the same butterfly.
+ *
+ * The mixer computed here (joint-gain form):
+ *     Y[b] = H_N (G o (H_N X[b] H_C)) H_C,   b = 0 .. B-1,
+ * with G[N, C] a per-frequency gain shared by all batch slices and "o" the
+ * element-wise product.  The paper's own parametrisation, log-domain gains
+ * g_c (length C) and g_t (length N) applied by eq. (2) then eq. (3), is
+ * oracle_whtmix_separable(); it equals the joint form with
+ * G[n][c] = exp(g_t[n]) * exp(g_c[c]) (rank one).
+ *
+ * Layout: x, y are [B][N][C] row-major (C fastest), g is [N][C] row-major.
+ * Every per-vector operation runs in a fixed order, so the output is bitwise
+ * independent of the OpenMP thread count.
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Unnormalised Sylvester butterfly, in place, on the n values v[0], v[s],
+ * v[2s], ...: after the loop v holds H_n v with H_n the +/-1 Sylvester matrix
+ * (section III-B).  Each stage pairs index j with j + h inside blocks of 2h
+ * and replaces (a, b) by (a + b, a - b). */
+static void fwht_strided(double *v, long n, long s)
+{
+    for (long h = 1; h < n; h *= 2) {
+        for (long i = 0; i < n; i += 2 * h) {
+            for (long j = i; j < i + h; ++j) {
+                double a = v[j * s];
+                double b = v[(j + h) * s];
+                v[j * s] = a + b;
+                v[(j + h) * s] = a - b;
+            }
+        }
+    }
+}
+
+/* Orthonormal transform: the butterfly followed by the 1/sqrt(n) factor that
+ * makes H orthonormal (section III-B). */
+static void wht_orthonormal(double *v, long n, long s)
+{
+    fwht_strided(v, n, s);
+    double f = 1.0 / sqrt((double)n);
+    for (long j = 0; j < n; ++j)
+        v[j * s] *= f;
+}
+
+/* Z <- Z H_C: transform every token row along the channel axis. */
+static void channel_transform(double *z, long N, long C)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; ++n)
+        wht_orthonormal(z + n * C, C, 1);
+}
+
+/* Z <- H_N Z: transform every channel column along the token axis. */
+static void token_transform(double *z, long N, long C)
+{
+#pragma omp parallel for schedule(static)
+    for (long c = 0; c < C; ++c)
+        wht_orthonormal(z + c, N, C);
+}
+
+static int is_pow2(long n) { return n >= 1 && (n & (n - 1)) == 0; }
+
+/* Joint-gain mixer, Y[b] = H_N (G o (H_N X[b] H_C)) H_C.
+ * Returns 0 on success, -1 on a bad argument (null pointer, B < 0, N or C not
+ * a power of two). */
+int oracle_whtmix(const double *x, const double *g, double *y,
+                  long B, long N, long C)
+{
+    if (!x || !g || !y || B < 0 || !is_pow2(N) || !is_pow2(C))
+        return -1;
+    const long L = N * C;
+    for (long b = 0; b < B; ++b) {
+        double *z = y + b * L;
+        if (z != x + b * L)
+            memcpy(z, x + b * L, (size_t)L * sizeof(double));
+        /* forward: T = H_N X H_C */
+        channel_transform(z, N, C);
+        token_transform(z, N, C);
+        /* per-frequency gain */
+        for (long i = 0; i < L; ++i)
+            z[i] *= g[i];
+        /* inverse (H^{-1} = H): Y = H_N T H_C */
+        token_transform(z, N, C);
+        channel_transform(z, N, C);
+    }
+    return 0;
+}
+
+/* The paper's literal parametrisation, eq. (2) then eq. (3):
+ *   Z <- H_C^{-1}( exp(g_c) o H_C(Z) )   along channels, per token row,
+ *   Z <- H_N^{-1}( exp(g_t) o H_N(Z) )   along tokens, per channel column,
+ * with g_c (length C) and g_t (length N) log-domain gains.  Same return
+ * convention as oracle_whtmix(). */
+int oracle_whtmix_separable(const double *x, const double *g_t,
+                            const double *g_c, double *y,
+                            long B, long N, long C)
+{
+    if (!x || !g_t || !g_c || !y || B < 0 || !is_pow2(N) || !is_pow2(C))
+        return -1;
+    const long L = N * C;
+    for (long b = 0; b < B; ++b) {
+        double *z = y + b * L;
+        if (z != x + b * L)
+            memcpy(z, x + b * L, (size_t)L * sizeof(double));
+        /* eq. (2): channel mixing */
+        channel_transform(z, N, C);
+        for (long n = 0; n < N; ++n)
+            for (long c = 0; c < C; ++c)
+                z[n * C + c] *= exp(g_c[c]);
+        channel_transform(z, N, C);
+        /* eq. (3): token mixing */
+        token_transform(z, N, C);
+        for (long n = 0; n < N; ++n)
+            for (long c = 0; c < C; ++c)
+                z[n * C + c] *= exp(g_t[n]);
+        token_transform(z, N, C);
+    }
+    return 0;
+}
+
+/* Bare unnormalised butterfly over a contiguous vector, exported so that the
+ * tests can pin the transform itself against a dense Sylvester matrix. */
+int oracle_fwht(double *v, long n)
+{
+    if (!v || !is_pow2(n))
+        return -1;
+    fwht_strided(v, n, 1);
+    return 0;
+}

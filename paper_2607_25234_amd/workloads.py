@@ -1,0 +1,120 @@
+"""Seeded synthetic WHTMix inputs (shapes and distributions only, no mixer arithmetic).
+
+Both sides of every parity check draw their inputs here: the HIP path receives
+them as device tensors, the CPU oracle as float64 arrays.  Nothing in this
+module computes any part of the mixer.
+
+Workloads (X: [B, N, C] tokens x channels, G: [N, C] float32 gain):
+
+* ``image1k_f32``     B=1,  N=1024   (32x32 grid, row-major),       C=64,  fp32
+* ``stereo16k_f32``   B=2,  N=16384  (two 64x128 view grids),       C=128, fp32
+* ``stereo64k_bf16``  B=4,  N=65536  (two 128x256 view grids),      C=128, bf16
+* ``text4k_f32``      B=32, N=4096   (embedded integer tokens),     C=64,  fp32
+* ``stereo256k_bf16`` B=1,  N=262144 (two 256x512 view grids),      C=256, bf16
+
+The stereo workloads stand in for the CNN-plus-positional-encoding features of
+the stereo backbone (section III-A: N = 2 (H/8)(W/8) joint tokens of the left
+and right views), the 1k and 4k ones for the byte-level image and text
+sequence-classification tasks (section IV-D).  No dataset item is reproduced:
+X ~ N(0, 1) (or embeddings of uniform random integer tokens through a
+N(0, 0.02) table for the text workload) and G ~ U(0.5, 1.5), drawn with numpy's
+PCG64 generator seeded per workload, in the order X then G (text workload:
+table, tokens, G).  bf16 workloads round X to bf16 with round-to-nearest-even
+before either side sees it, so both sides receive identical values.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    N: int
+    C: int
+    dtype: str          # "f32" or "bf16": the element type of X and Y
+    seed: int
+    x_dist: str = "normal"   # "normal" or "embed"
+    note: str = ""
+
+    @property
+    def elements(self) -> int:
+        return self.B * self.N * self.C
+
+    @property
+    def io_bytes(self) -> int:
+        """Ideal HBM bytes of one call: read X, read G once, write Y."""
+        s = 4 if self.dtype == "f32" else 2
+        return self.elements * 2 * s + 4 * self.N * self.C
+
+
+WORKLOADS = {
+    w.name: w
+    for w in [
+        Workload("image1k_f32", 1, 1024, 64, "f32", 1, "normal",
+                 "32x32 feature grid, row-major"),
+        Workload("stereo16k_f32", 2, 16384, 128, "f32", 2, "normal",
+                 "two 64x128 view grids concatenated along tokens"),
+        Workload("stereo64k_bf16", 4, 65536, 128, "bf16", 3, "normal",
+                 "two 128x256 view grids concatenated, bf16 in/out"),
+        Workload("text4k_f32", 32, 4096, 64, "f32", 4, "embed",
+                 "uniform integer tokens in [0,256) through a N(0,0.02) table"),
+        Workload("stereo256k_bf16", 1, 262144, 256, "bf16", 5, "normal",
+                 "two 256x512 view grids concatenated, bf16 in/out"),
+    ]
+}
+
+# The workload the benchmark times (the N=65536, C=128 bf16 configuration).
+BENCH_WORKLOAD = "stereo64k_bf16"
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bf16 (ties to even), kept as float32."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
+    out = r.view(np.float32).copy()
+    nan = np.isnan(x)
+    if nan.any():
+        out[nan] = np.float32("nan")
+    return out
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """The uint16 bf16 bit patterns of float32 values that are exactly bf16."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    if np.any(u & 0xFFFF):
+        raise ValueError("values are not exactly representable in bf16")
+    return (u >> 16).astype(np.uint16)
+
+
+def draw(B: int, N: int, C: int, dtype: str = "f32", seed: int = 0,
+         x_dist: str = "normal", gain_lo: float = 0.5, gain_hi: float = 1.5):
+    """Return (x, g): x float32 [B, N, C] (bf16-rounded if dtype == "bf16"),
+    g float32 [N, C] ~ U(gain_lo, gain_hi)."""
+    rng = np.random.default_rng(seed)
+    if x_dist == "normal":
+        x = rng.standard_normal((B, N, C)).astype(np.float32)
+    elif x_dist == "embed":
+        table = (0.02 * rng.standard_normal((256, C))).astype(np.float32)
+        tokens = rng.integers(0, 256, size=(B, N))
+        x = table[tokens]
+    else:
+        raise ValueError(f"unknown x distribution {x_dist!r}")
+    g = rng.uniform(gain_lo, gain_hi, size=(N, C)).astype(np.float32)
+    if dtype == "bf16":
+        x = round_to_bf16(x)
+    elif dtype != "f32":
+        raise ValueError(f"unknown dtype {dtype!r}")
+    return np.ascontiguousarray(x), np.ascontiguousarray(g)
+
+
+def inputs(w: Workload | str):
+    """Inputs of a named workload, as (x float32 [B,N,C], g float32 [N,C])."""
+    if isinstance(w, str):
+        w = WORKLOADS[w]
+    return draw(w.B, w.N, w.C, w.dtype, w.seed, w.x_dist)

@@ -1,0 +1,258 @@
+"""Checks that pin the CPU oracle to facts fixed outside the oracle itself.
+
+Each ``pin_*`` function takes an ``oracle.oracle.Oracle`` and raises
+AssertionError when the oracle disagrees with the paper or with mathematics
+that does not depend on the oracle's code:
+
+* a library Sylvester construction (``scipy.linalg.hadamard``) and the closed
+  form (-1)^popcount(i & j) of the matrix entries (section III-B);
+* dense matrix products of the mixer's definition;
+* the dyadic (XOR) convolution form of the mixer, by brute force;
+* hand-worked examples under ``tests/golden/``;
+* invariants: unit gain is the identity (the zero-initialised log gain of
+  section III-B), energy preservation of orthonormal transforms, one-hot gains
+  selecting a single Walsh basis image, linearity, self-adjointness, batch
+  independence;
+* the paper's separable form (eq. (2) then eq. (3)) equals the joint gain
+  form with a rank-one G.
+
+The same functions run against the real oracle (``test_oracle_pins.py``) and
+against deliberately broken copies of it (``test_oracle_mutants.py``), which
+shows that a plausible mistake anywhere in the oracle fails at least one pin.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import scipy.linalg
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+SHAPES_SMALL = [(1, 1), (2, 1), (1, 2), (2, 2), (4, 8), (8, 4), (16, 16),
+                (2, 64), (64, 2), (32, 8), (1, 32), (128, 1)]
+
+
+def _rel(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = max(np.max(np.abs(b)), 1e-300)
+    return float(np.max(np.abs(a - b)) / den) if a.size else 0.0
+
+
+def _popcount(v: int) -> int:
+    return bin(v).count("1")
+
+
+def _walsh(n: int, k: int) -> np.ndarray:
+    """Row k of the orthonormal Sylvester matrix, by the closed form."""
+    return np.array([(-1.0) ** _popcount(k & i) for i in range(n)]) / np.sqrt(n)
+
+
+def _hadamard_orth(n: int) -> np.ndarray:
+    return scipy.linalg.hadamard(n).astype(np.float64) / np.sqrt(n)
+
+
+# --------------------------------------------------------------------------
+def pin_sylvester_closed_form(o) -> None:
+    """scipy's Sylvester construction has entries (-1)^popcount(i & j): the
+    natural (Hadamard) ordering that section III-B names."""
+    for n in [1, 2, 4, 8, 16, 64]:
+        H = scipy.linalg.hadamard(n)
+        ref = np.array([[(-1) ** _popcount(i & j) for j in range(n)]
+                        for i in range(n)])
+        assert np.array_equal(H, ref), n
+
+
+def pin_butterfly_matches_dense(o) -> None:
+    """The oracle's butterfly equals the dense +/-1 Sylvester product."""
+    rng = np.random.default_rng(100)
+    for k in range(0, 10):
+        n = 1 << k
+        v = rng.standard_normal(n)
+        got = o.fwht(v)
+        ref = scipy.linalg.hadamard(n).astype(np.float64) @ v
+        assert _rel(got, ref) < 1e-13, (n, _rel(got, ref))
+
+
+def pin_dense_product(o) -> None:
+    """Y = H_N (G o (H_N X H_C)) H_C with explicit orthonormal matrices."""
+    rng = np.random.default_rng(101)
+    for (N, C) in SHAPES_SMALL + [(64, 64), (256, 16)]:
+        x = rng.standard_normal((N, C))
+        g = rng.uniform(0.5, 1.5, (N, C))
+        Hn, Hc = _hadamard_orth(N), _hadamard_orth(C)
+        ref = Hn @ (g * (Hn @ x @ Hc)) @ Hc
+        got = o.whtmix(x, g)
+        assert got.shape == (N, C)
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+
+
+def pin_dyadic_convolution(o) -> None:
+    """Brute force: Y[n,c] = sum_{m,d} K[n^m, c^d] X[m,d] with
+    K[i,j] = (1/(N C)) sum_{k,l} G[k,l] (-1)^(popcount(i&k) + popcount(j&l)).
+    (Expanding the definition entry-wise and using
+    (-1)^popcount(n&k) (-1)^popcount(m&k) = (-1)^popcount((n^m)&k).)"""
+    rng = np.random.default_rng(102)
+    for (N, C) in [(1, 1), (2, 1), (1, 4), (4, 2), (2, 8), (8, 8), (16, 4)]:
+        x = rng.standard_normal((N, C))
+        g = rng.uniform(-1.0, 2.0, (N, C))
+        K = np.zeros((N, C))
+        for i in range(N):
+            for j in range(C):
+                s = 0.0
+                for k in range(N):
+                    for l in range(C):
+                        sgn = -1.0 if (_popcount(i & k) + _popcount(j & l)) & 1 else 1.0
+                        s += sgn * g[k, l]
+                K[i, j] = s / (N * C)
+        ref = np.zeros((N, C))
+        for n in range(N):
+            for c in range(C):
+                s = 0.0
+                for m in range(N):
+                    for d in range(C):
+                        s += K[n ^ m, c ^ d] * x[m, d]
+                ref[n, c] = s
+        got = o.whtmix(x, g)
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+
+
+def pin_golden_hand_examples(o) -> None:
+    """Hand-worked values (tests/golden/hand_examples.json)."""
+    with open(os.path.join(GOLDEN, "hand_examples.json")) as f:
+        data = json.load(f)
+    for case in data["cases"]:
+        got = o.whtmix(np.array(case["x"]), np.array(case["g"]))
+        ref = np.array(case["y"])
+        assert np.allclose(got, ref, rtol=0, atol=1e-13), (case["name"], got, ref)
+
+
+def pin_unit_gain_identity(o) -> None:
+    """Zero log gain = unit gain (section III-B): G = 1 returns X, because H is
+    orthonormal and involutory."""
+    rng = np.random.default_rng(103)
+    for (N, C) in SHAPES_SMALL + [(1024, 64), (4096, 2)]:
+        x = rng.standard_normal((2, N, C))
+        got = o.whtmix(x, np.ones((N, C)))
+        assert _rel(got, x) < 1e-13, ((N, C), _rel(got, x))
+
+
+def pin_energy(o) -> None:
+    """Orthonormal transforms preserve energy (section III-B, magnitude
+    preserving): a +/-1 gain keeps ||Y|| = ||X||; any gain keeps
+    min|G| ||X|| <= ||Y|| <= max|G| ||X||."""
+    rng = np.random.default_rng(104)
+    for (N, C) in [(8, 4), (64, 32), (256, 8), (2, 1)]:
+        x = rng.standard_normal((N, C))
+        s = rng.choice([-1.0, 1.0], size=(N, C))
+        y = o.whtmix(x, s)
+        assert abs(np.linalg.norm(y) / np.linalg.norm(x) - 1) < 1e-13
+        g = rng.uniform(0.25, 3.0, (N, C))
+        y = o.whtmix(x, g)
+        nx, ny = np.linalg.norm(x), np.linalg.norm(y)
+        assert g.min() * nx * (1 - 1e-12) <= ny <= g.max() * nx * (1 + 1e-12)
+
+
+def pin_one_hot_gain(o) -> None:
+    """A gain that keeps only frequency (k, j) projects X onto the single Walsh
+    basis image B = h_k h_j^T: Y = <X, B> B.  X = B is kept whole by that gain
+    and removed by any other one-hot gain."""
+    rng = np.random.default_rng(105)
+    for (N, C) in [(8, 4), (4, 16), (16, 2), (1, 8), (32, 1)]:
+        x = rng.standard_normal((N, C))
+        for (k, j) in [(0, 0), (N - 1, C - 1), (N // 2, C // 3), (1 % N, 0)]:
+            B = np.outer(_walsh(N, k), _walsh(C, j))
+            g = np.zeros((N, C))
+            g[k, j] = 1.0
+            got = o.whtmix(x, g)
+            ref = np.sum(x * B) * B
+            assert _rel(got, ref) < 1e-12, ((N, C, k, j), _rel(got, ref))
+            kept = o.whtmix(B, g)
+            assert _rel(kept, B) < 1e-12
+            k2, j2 = (k + 1) % N, (j + 1) % C
+            if (k2, j2) != (k, j):
+                g2 = np.zeros((N, C))
+                g2[k2, j2] = 1.0
+                assert np.max(np.abs(o.whtmix(B, g2))) < 1e-13
+
+
+def pin_separable_form(o) -> None:
+    """The paper's eq. (2) then eq. (3) with log gains equals, with dense
+    matrices, H_N D_t H_N X H_C D_c H_C, and equals the joint form with the
+    rank-one gain exp(g_t) exp(g_c)^T."""
+    rng = np.random.default_rng(106)
+    for (N, C) in [(8, 4), (2, 32), (64, 8), (1, 4), (4, 1)]:
+        x = rng.standard_normal((3, N, C))
+        gt = rng.normal(0, 0.5, N)
+        gc = rng.normal(0, 0.5, C)
+        Hn, Hc = _hadamard_orth(N), _hadamard_orth(C)
+        Dt, Dc = np.diag(np.exp(gt)), np.diag(np.exp(gc))
+        ref = np.stack([Hn @ Dt @ Hn @ xb @ Hc @ Dc @ Hc for xb in x])
+        got = o.whtmix_separable(x, gt, gc)
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+        joint = o.whtmix(x, np.outer(np.exp(gt), np.exp(gc)))
+        assert _rel(joint, ref) < 1e-12, ((N, C), _rel(joint, ref))
+
+
+def pin_flat_1d_equivalence(o) -> None:
+    """H_N kron H_C = H_{N C} in Sylvester order, so the mixer is also
+    (1/(N C)) H (g o H x) on the flattened row-major slice of length N C.
+    (Checked with the dense 1-D matrix; this is the fact the GPU's bit-group
+    passes rely on.)"""
+    rng = np.random.default_rng(107)
+    for (N, C) in [(4, 8), (16, 4), (2, 2), (8, 32)]:
+        x = rng.standard_normal((N, C))
+        g = rng.uniform(0.5, 1.5, (N, C))
+        H = scipy.linalg.hadamard(N * C).astype(np.float64)
+        ref = (H @ (g.reshape(-1) * (H @ x.reshape(-1)))) / (N * C)
+        got = o.whtmix(x, g).reshape(-1)
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+
+
+def pin_structure(o) -> None:
+    """Linearity in X, linearity in G, self-adjointness <f(X1),X2> = <X1,f(X2)>
+    (H and diag(G) are symmetric), and batch independence / equivariance."""
+    rng = np.random.default_rng(108)
+    N, C = 16, 8
+    g = rng.uniform(-1, 2, (N, C))
+    x1, x2 = rng.standard_normal((2, N, C))
+    a, b = 1.7, -0.3
+    f = lambda x, gg=g: o.whtmix(x, gg)
+    assert _rel(f(a * x1 + b * x2), a * f(x1) + b * f(x2)) < 1e-12
+    assert _rel(o.whtmix(x1, 2.5 * g), 2.5 * f(x1)) < 1e-12
+    lhs, rhs = np.sum(f(x1) * x2), np.sum(x1 * f(x2))
+    assert abs(lhs - rhs) < 1e-12 * max(1.0, abs(lhs))
+    xb = rng.standard_normal((5, N, C))
+    yb = o.whtmix(xb, g)
+    for i in range(5):
+        assert np.array_equal(yb[i], o.whtmix(xb[i], g)), i
+    perm = [3, 0, 4, 1, 2]
+    assert np.array_equal(o.whtmix(xb[perm], g), yb[perm])
+
+
+def pin_rejects_bad_shapes(o) -> None:
+    """The transform is defined for power-of-two lengths only (section III-B)."""
+    for (N, C) in [(3, 4), (4, 6), (12, 1)]:
+        try:
+            o.whtmix(np.zeros((N, C)), np.ones((N, C)))
+        except ValueError:
+            continue
+        raise AssertionError(f"accepted non-power-of-two shape {(N, C)}")
+
+
+ALL_PINS = [
+    pin_sylvester_closed_form,
+    pin_butterfly_matches_dense,
+    pin_dense_product,
+    pin_dyadic_convolution,
+    pin_golden_hand_examples,
+    pin_unit_gain_identity,
+    pin_energy,
+    pin_one_hot_gain,
+    pin_separable_form,
+    pin_flat_1d_equivalence,
+    pin_structure,
+    pin_rejects_bad_shapes,
+]

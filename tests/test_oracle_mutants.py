@@ -1,0 +1,85 @@
+"""Plant plausible mistakes in copies of the oracle and check the pins catch them.
+
+Each mutant is a one-place textual edit of ``oracle/whtmix_oracle.c``,
+compiled with gcc into a temporary library (CPU only; the real oracle is never
+modified).  A pin set that let any of these through would not be strong
+enough to trust the oracle.
+"""
+import os
+
+import pytest
+
+from oracle import oracle as oracle_mod
+from tests import pins
+
+MUTANTS = {
+    # butterfly: wrong sign on the difference output
+    "butterfly_sign": ("v[(j + h) * s] = a - b;", "v[(j + h) * s] = b - a;"),
+    # butterfly: last stage dropped
+    "butterfly_last_stage": ("for (long h = 1; h < n; h *= 2)",
+                             "for (long h = 1; h < n / 2; h *= 2)"),
+    # butterfly: one pair per block skipped
+    "butterfly_pair_skipped": ("for (long j = i; j < i + h; ++j)",
+                               "for (long j = i + (h > 1); j < i + h; ++j)"),
+    # normalisation 1/n instead of 1/sqrt(n)
+    "normalisation": ("double f = 1.0 / sqrt((double)n);",
+                      "double f = 1.0 / (double)n;"),
+    # token transform left unnormalised
+    "token_unnormalised": ("wht_orthonormal(z + c, N, C);",
+                           "fwht_strided(z + c, N, C);"),
+    # token transform applied along the wrong stride (transposed operand)
+    "token_stride": ("wht_orthonormal(z + c, N, C);",
+                     "wht_orthonormal(z + c * N, N, 1);"),
+    # gain read transposed, G[c][n] instead of G[n][c]
+    "gain_transposed": ("z[i] *= g[i];", "z[i] *= g[(i % C) * N + i / C];"),
+    # forward token transform dropped
+    "forward_token_dropped": (
+        "        channel_transform(z, N, C);\n        token_transform(z, N, C);\n"
+        "        /* per-frequency gain */",
+        "        channel_transform(z, N, C);\n        /* per-frequency gain */"),
+    # batch slice offset wrong
+    "batch_offset": ("double *z = y + b * L;\n        if (z != x + b * L)\n"
+                     "            memcpy(z, x + b * L, (size_t)L * sizeof(double));\n"
+                     "        /* forward",
+                     "double *z = y + b * L;\n        if (z != x + b * N)\n"
+                     "            memcpy(z, x + b * N, (size_t)L * sizeof(double));\n"
+                     "        /* forward"),
+    # separable form: log gains used without exponentiation
+    "separable_no_exp": ("z[n * C + c] *= exp(g_c[c]);", "z[n * C + c] *= g_c[c];"),
+    # separable form: token gain indexed by channel
+    "separable_gain_index": ("z[n * C + c] *= exp(g_t[n]);",
+                             "z[n * C + c] *= exp(g_t[c % N]);"),
+}
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(oracle_mod.SRC) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, source, tmp_path):
+    old, new = MUTANTS[name]
+    assert source.count(old) == 1, f"mutation site for {name} not unique"
+    src = tmp_path / f"{name}.c"
+    src.write_text(source.replace(old, new))
+    lib = oracle_mod.build(str(src), str(tmp_path / f"{name}.so"))
+    mutant = oracle_mod.Oracle(lib)
+    caught = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(mutant)
+        except (AssertionError, ValueError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin caught mutant {name}"
+
+
+def test_unmutated_copy_passes(source, tmp_path):
+    """The mutation harness itself: an unmodified copy passes every pin."""
+    src = tmp_path / "same.c"
+    src.write_text(source)
+    mutant = oracle_mod.Oracle(oracle_mod.build(str(src), str(tmp_path / "same.so")))
+    for pin in pins.ALL_PINS:
+        pin(mutant)
+    assert os.path.exists(tmp_path / "same.so")
