@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""WHTMix forward throughput on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one whtmix_forward call (every kernel of the plan) over one batch of
+the workload (default: stereo64k_bf16, B=4, N=65536, C=128, bf16 in/out,
+float32 gain and arithmetic).  Inputs are resident in HBM before timing.
+Steps rotate over several input/output sets whose total footprint is at
+least twice the 256 MB Infinity Cache, so every step reads x and G from HBM.
+
+Prints one JSON line: GB/s of ideal traffic (read x + read G once + write y)
+per second of wall time over K steps, tokens/s, the fraction of the 8 TB/s
+HBM peak, a roofline record for the longest kernel (its average duration
+from HIP events recorded on the launch stream during the timed steps), and
+the CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak, GB/s
+METRIC = "WHTMix forward GB/s and tokens/s at 1 MI355X; % of HBM roofline"
+MALL_BYTES = 256 * 1024 * 1024
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2607_25234_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_names(plan: str) -> list[str]:
+    return {"three_pass": ["outer_fwd", "middle", "outer_inv"],
+            "fused": ["fused"], "small": ["small"]}[plan]
+
+
+def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int) -> list[int]:
+    """Bytes each kernel of the plan must move by its definition."""
+    L = N * C
+    if plan in ("fused", "small"):
+        return [B * L * 2 * s + 4 * L]
+    return [B * L * (s + 4),           # read x, write float32 workspace
+            B * L * 8 + 4 * L,         # read + write workspace, read G once
+            B * L * (4 + s)]           # read workspace, write y
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    if data.get("source_hash") != kernel_source_hash():
+        return None
+    entry = data.get("workloads", {}).get(workload, {}).get(kernel)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
+class HipEvents:
+    """HIP events through the runtime torch already loaded (same soname)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.events = []
+
+    def create(self) -> int:
+        ev = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        self.events.append(ev.value)
+        return ev.value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def destroy(self):
+        for ev in self.events:
+            self.hip.hipEventDestroy(ev)
+        self.events = []
+
+
+def cpu_baseline(w, x_slice, g, seconds: float) -> dict:
+    """The float64 CPU oracle, as it stands, on one batch slice, repeated until
+    about `seconds` of work; scaled to whole-workload GB/s."""
+    from oracle import oracle as oracle_mod
+    orc = oracle_mod.Oracle()
+    runs, t_total = 0, 0.0
+    while runs == 0 or (t_total < seconds and runs < 50):
+        t0 = time.perf_counter()
+        orc.whtmix(x_slice, g)
+        t_total += time.perf_counter() - t0
+        runs += 1
+    t_slice = t_total / runs
+    t_workload = t_slice * w.B
+    return {
+        "value": w.io_bytes / t_workload / 1e9,
+        "unit": "GB/s",
+        "tokens_per_s": w.B * w.N / t_workload,
+        "cores": orc.threads(),
+        "kind": "oracle",
+        "sample": (f"{runs} run(s) of one of the {w.B} batch slices ({w.N}x{w.C}), "
+                   f"{t_total:.1f} s total, float64 C oracle with OpenMP; rate scaled "
+                   f"to the whole {w.B}-slice workload"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--plan", default="auto")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="input/output sets rotated over the steps (0 = auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the WHTMix path here is built and "
+              "timed on a single MI355X (batch slices would shard across GPUs with "
+              "no communication; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_25234_amd import whtmix, workloads
+
+    name = args.workload or workloads.BENCH_WORKLOAD
+    w = workloads.WORKLOADS[name]
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        return 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    whtmix.lib()
+    s = 2 if w.dtype == "bf16" else 4
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dt_code = whtmix.DTYPE_BF16 if w.dtype == "bf16" else whtmix.DTYPE_F32
+    plan = whtmix.plan_describe(w.B, w.N, w.C, w.dtype, args.plan)
+    set_bytes = w.io_bytes
+    nsets = args.sets or max(1, min(8, -(-2 * MALL_BYTES // set_bytes) + 1))
+    log(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}; plan {plan}; {nsets} input sets")
+
+    sets = []
+    for i in range(nsets):
+        if i == 0:
+            x, g = workloads.inputs(w)
+        else:
+            x, g = workloads.draw(w.B, w.N, w.C, w.dtype, w.seed + 1000 * i, w.x_dist)
+        xd = torch.from_numpy(x).to(dev).to(tdt)
+        gd = torch.from_numpy(g).to(dev)
+        yd = torch.empty_like(xd)
+        sets.append((xd, gd, yd))
+        if i == 0:
+            x0_slice, g0 = x[0].copy(), g.copy()
+        del x, g
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    sptr = stream.cuda_stream
+    hip = HipEvents()
+    nk = plan["kernels"]
+    names = kernel_names(plan["plan"])
+
+    def step(i, events=None):
+        xd, gd, yd = sets[i % nsets]
+        st = whtmix.forward_raw(xd.data_ptr(), gd.data_ptr(), yd.data_ptr(), w.B, w.N, w.C,
+                                dt_code, sptr, args.plan, events)
+        if st != whtmix.SUCCESS:
+            raise whtmix.WhtmixError(st, "whtmix_forward")
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[hip.create() for _ in range(nk + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()            # barrier (one rank) + device sync
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    per_kernel = [float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs]))
+                  for j in range(nk)]
+    gpu_span_ms = hip.elapsed_ms(evs[0][0], evs[-1][-1])
+    hip.destroy()
+
+    ms_per_step = wall * 1e3 / args.steps
+    gbs = w.io_bytes / (ms_per_step * 1e-3) / 1e9
+    tokens = w.B * w.N / (ms_per_step * 1e-3)
+    alg = algorithmic_bytes(plan["plan"], w.B, w.N, w.C, s)
+    dom = int(np.argmax(per_kernel))
+    achieved = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9
+    traffic = load_traffic(names[dom], name)
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": name, "B": w.B, "N": w.N, "C": w.C,
+                   "io_dtype": w.dtype, "gain_dtype": "f32", "plan": plan["plan"],
+                   "input_sets": nsets},
+        "tokens_per_s": round(tokens, 1),
+        "hbm_peak_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "gpu_event_ms_per_step": round(gpu_span_ms / args.steps, 5),
+        "kernels": [{"name": n, "avg_ms": round(t, 5), "alg_bytes": b,
+                     "alg_GBs": round(b / (t * 1e-3) / 1e9, 1)}
+                    for n, t, b in zip(names, per_kernel, alg)],
+        "roofline": {"bound": "hbm", "kernel": names[dom],
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on one batch slice ...")
+        out["cpu_baseline"] = cpu_baseline(w, x0_slice, g0, args.cpu_seconds)
+        out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 4)
+        out["cpu_baseline"]["tokens_per_s"] = round(out["cpu_baseline"]["tokens_per_s"], 1)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

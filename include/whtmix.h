@@ -1,0 +1,157 @@
+/*
+ * whtmix.h -- C ABI of the MI355X (gfx950) WHTMix token mixer.
+ *
+ * The mixer is the Walsh-Hadamard token mixer of "WHTMix: Efficient Stereo
+ * Depth Estimation via Walsh-Hadamard Token Mixing", section III-B, eqs.
+ * (2)-(3), in its joint per-frequency-gain form:
+ *
+ *     Y[b] = H_N (G o (H_N X[b] H_C)) H_C,      b = 0 .. B-1
+ *
+ *   X[b], Y[b]  N x C (tokens x channels), row-major, channels fastest;
+ *   H_n         the orthonormal Sylvester-ordered Walsh-Hadamard matrix,
+ *               entry (i, j) = (-1)^popcount(i & j) / sqrt(n), n = 2^k;
+ *               H_n is symmetric and orthogonal, so H_n^{-1} = H_n;
+ *   G           N x C float32 per-frequency gain shared by every slice b
+ *               ("o" is the element-wise product).
+ *
+ * The paper's own gains are log-domain vectors g_c (length C) and g_t
+ * (length N) applied by eq. (2) then eq. (3); that is this operation with
+ * G[n][c] = exp(g_t[n]) * exp(g_c[c]).  Exponentiating is the caller's job.
+ *
+ * All computation runs in hand-written HIP kernels on the GPU.  Arithmetic is
+ * float32 (bf16 inputs are widened exactly, bf16 outputs are rounded to
+ * nearest even once at the end); the four orthonormal 1/sqrt factors are
+ * applied together as the exact power of two 1/(N*C) at the gain multiply.
+ *
+ * Threading and streams: every entry point is safe to call from several host
+ * threads.  Work is enqueued on the caller's stream and the call returns
+ * without waiting for it.  The library keeps one float32 workspace of
+ * B*N*C*4 bytes per (device, stream) for shapes that need more than one pass;
+ * it is allocated (or grown) on the first call that needs it, which therefore
+ * synchronises that stream and is not safe inside HIP graph capture.
+ */
+#ifndef WHTMIX_H
+#define WHTMIX_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define WHTMIX_API __attribute__((visibility("default")))
+#else
+#define WHTMIX_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of x and y (the gain is always float32). */
+typedef enum whtmix_dtype {
+    WHTMIX_DTYPE_F32 = 0,
+    WHTMIX_DTYPE_BF16 = 1
+} whtmix_dtype;
+
+/* Return codes.  Every argument check runs on the host before any HIP call;
+ * a rejected call enqueues nothing and writes nothing. */
+typedef enum whtmix_status {
+    WHTMIX_SUCCESS = 0,
+    WHTMIX_ERROR_INVALID_VALUE = 1,    /* null pointer, B < 0, partial x/y
+                                          overlap, gain overlapping y,
+                                          bad option values */
+    WHTMIX_ERROR_NOT_POWER_OF_TWO = 2, /* N or C not a power of two >= 1 */
+    WHTMIX_ERROR_UNSUPPORTED_DTYPE = 3,
+    WHTMIX_ERROR_MISALIGNED = 4,       /* x, y or gain not 16-byte aligned */
+    WHTMIX_ERROR_OUT_OF_MEMORY = 5,    /* workspace allocation failed */
+    WHTMIX_ERROR_HIP = 6,              /* HIP runtime / launch error; text in
+                                          whtmix_last_error() */
+    WHTMIX_ERROR_TOO_LARGE = 7         /* N*C > 2^30 or sizes overflow */
+} whtmix_status;
+
+/* Execution plans.  AUTO picks by the slice size L = N*C:
+ *   L <= 2^10          one small workgroup per slice, all stages in LDS;
+ *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass;
+ *   L >= 2^16          THREE_PASS: forward over the low bits of the flat
+ *                      index, then forward over the high bits + gain +
+ *                      inverse over the high bits, then inverse over the low
+ *                      bits, exchanging through the workspace.
+ * THREE_PASS may also be forced for 2^12 <= L <= 2^15 (tests compare it with
+ * FUSED on the same shapes). */
+typedef enum whtmix_plan {
+    WHTMIX_PLAN_AUTO = 0,
+    WHTMIX_PLAN_SMALL = 1,
+    WHTMIX_PLAN_FUSED = 2,
+    WHTMIX_PLAN_THREE_PASS = 3
+} whtmix_plan;
+
+typedef struct whtmix_options {
+    int plan;          /* whtmix_plan; WHTMIX_PLAN_AUTO = 0 */
+    /* Optional hipEvent_t handles (NULL to skip).  events[0] is recorded on
+     * the stream before the first kernel and events[i] after the i-th kernel
+     * of the plan (at most 3 kernels).  Used for per-kernel timing. */
+    void *events[4];
+} whtmix_options;
+
+/* Describes how a shape would run (no GPU work, no allocation). */
+typedef struct whtmix_plan_info {
+    int plan;             /* resolved whtmix_plan (never AUTO) */
+    int kernels;          /* kernels launched per call (1 or 3) */
+    int log2_slice;       /* K = log2(N*C) */
+    int outer_bits;       /* THREE_PASS: flat-index bits of the outer passes */
+    int run_bits;         /* THREE_PASS: log2 of the contiguous run carried
+                             by the middle pass */
+    int64_t workspace_bytes; /* float32 workspace this call needs */
+} whtmix_plan_info;
+
+/*
+ * whtmix_forward -- y[b] = H_N (G o (H_N x[b] H_C)) H_C for b in [0, B).
+ *
+ *   x      device pointer, [B][N][C] contiguous elements of `dtype`
+ *          (read only).  May equal y exactly (in place); any other overlap
+ *          with y is rejected.
+ *   gain   device pointer, [N][C] contiguous float32, shared by all b; must
+ *          not overlap y.
+ *   y      device pointer, [B][N][C] contiguous elements of `dtype` (written).
+ *   B      number of independent slices; B == 0 is a no-op (pointers are not
+ *          inspected).
+ *   N, C   tokens and channels; each a power of two >= 1, N*C <= 2^30.
+ *   dtype  whtmix_dtype of x and y.
+ *   stream hipStream_t to enqueue on (NULL = the null stream).
+ *
+ * The caller owns x, gain and y and keeps them alive until the stream work
+ * is done.  Pointers must be 16-byte aligned.  Returns a whtmix_status.
+ * Kernel faults surface asynchronously through the stream like any HIP op.
+ */
+WHTMIX_API int whtmix_forward(const void *x, const float *gain, void *y,
+                   int64_t B, int64_t N, int64_t C, int dtype, void *stream);
+
+/* As whtmix_forward, with options (NULL = defaults). */
+WHTMIX_API int whtmix_forward_ex(const void *x, const float *gain, void *y,
+                      int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                      const whtmix_options *options);
+
+/* Fills *info with the plan whtmix_forward_ex would use.  Validates the
+ * shape, dtype and options exactly as the forward call does (pointers are
+ * not needed).  Returns a whtmix_status. */
+WHTMIX_API int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
+                         const whtmix_options *options,
+                         whtmix_plan_info *info);
+
+/* Static description of a status code (never NULL). */
+WHTMIX_API const char *whtmix_status_string(int status);
+
+/* Text of the last WHTMIX_ERROR_HIP / OUT_OF_MEMORY on the calling thread
+ * ("" if none). */
+WHTMIX_API const char *whtmix_last_error(void);
+
+/* Synchronises every stream that owns a workspace and frees all workspaces.
+ * Returns a whtmix_status. */
+WHTMIX_API int whtmix_release_workspaces(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+WHTMIX_API int whtmix_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WHTMIX_H */

@@ -49,6 +49,8 @@ def load(path: str = LIB):
     lib.oracle_whtmix_separable.restype = ctypes.c_int
     lib.oracle_fwht.argtypes = [dp, L]
     lib.oracle_fwht.restype = ctypes.c_int
+    lib.oracle_threads.argtypes = []
+    lib.oracle_threads.restype = ctypes.c_int
     if path == LIB:
         _lib = lib
     return lib
@@ -113,6 +115,10 @@ class Oracle:
         if rc != 0:
             raise ValueError("length must be a power of two")
         return v64
+
+    def threads(self) -> int:
+        """OpenMP threads the oracle's parallel loops use."""
+        return int(self.lib.oracle_threads())
 
 
 _default = None

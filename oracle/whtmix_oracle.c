@@ -32,6 +32,7 @@
  * independent of the OpenMP thread count.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -147,4 +148,10 @@ int oracle_fwht(double *v, long n)
         return -1;
     fwht_strided(v, n, 1);
     return 0;
+}
+
+/* Number of OpenMP threads a parallel region of the oracle uses. */
+int oracle_threads(void)
+{
+    return omp_get_max_threads();
 }

@@ -1,0 +1,253 @@
+// C entry points of the WHTMix library: argument checks, plan choice,
+// per-(device, stream) workspace, status text.  Declared in include/whtmix.h.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+
+#include "whtmix.h"
+#include "whtmix_launch.h"
+#include "whtmix_plan.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+struct Workspace {
+    float *ptr = nullptr;
+    int64_t bytes = 0;
+};
+
+// Keyed by (device, stream).  The mutex is held from workspace lookup until
+// the kernels that use the workspace are enqueued, so a concurrent call that
+// grows (frees and reallocates) the same stream's workspace cannot free it
+// between lookup and launch.
+std::mutex g_ws_mutex;
+std::map<std::pair<int, void *>, Workspace> g_ws;
+
+bool is_pow2(int64_t v) { return v >= 1 && (v & (v - 1)) == 0; }
+
+int log2_exact(int64_t v)
+{
+    int k = 0;
+    while ((int64_t(1) << k) < v) ++k;
+    return k;
+}
+
+bool overlaps(uintptr_t a, uint64_t na, uintptr_t b, uint64_t nb)
+{
+    return a < b + nb && b < a + na;
+}
+
+struct Checked {
+    int K = 0;
+    int plan = whtmix::PLAN_AUTO;
+    int kernels = 0;
+    whtmix::Split split{0, 0, 0};
+    int64_t ws_bytes = 0;
+    int elt = 4;
+};
+
+// Shape, dtype and option checks shared by forward and describe.
+int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options *opt,
+                Checked *out)
+{
+    if (dtype != WHTMIX_DTYPE_F32 && dtype != WHTMIX_DTYPE_BF16)
+        return WHTMIX_ERROR_UNSUPPORTED_DTYPE;
+    if (B < 0)
+        return WHTMIX_ERROR_INVALID_VALUE;
+    if (!is_pow2(N) || !is_pow2(C))
+        return WHTMIX_ERROR_NOT_POWER_OF_TWO;
+    const int K = log2_exact(N) + log2_exact(C);
+    if (K > whtmix::kMaxLog2Slice)
+        return WHTMIX_ERROR_TOO_LARGE;
+    const int64_t L = int64_t(1) << K;
+    // Work-items per launch are B*L/32 (tiled plans) or B*256 (small plan);
+    // both must fit the 32-bit grid size.
+    if (B > (int64_t(1) << 37) / L)
+        return WHTMIX_ERROR_TOO_LARGE;
+    if (K <= whtmix::kMaxSmall && B >= (int64_t(1) << 24))
+        return WHTMIX_ERROR_TOO_LARGE;
+    int plan = opt ? opt->plan : whtmix::PLAN_AUTO;
+    switch (plan) {
+    case whtmix::PLAN_AUTO:
+        plan = K <= whtmix::kMaxSmall ? whtmix::PLAN_SMALL
+               : K <= whtmix::kMaxTile ? whtmix::PLAN_FUSED
+                                       : whtmix::PLAN_THREE_PASS;
+        break;
+    case whtmix::PLAN_SMALL:
+        if (K > whtmix::kMaxSmall) return WHTMIX_ERROR_INVALID_VALUE;
+        break;
+    case whtmix::PLAN_FUSED:
+        if (K < whtmix::kMinTile || K > whtmix::kMaxTile) return WHTMIX_ERROR_INVALID_VALUE;
+        break;
+    case whtmix::PLAN_THREE_PASS:
+        if (K < whtmix::kMinTile + 1) return WHTMIX_ERROR_INVALID_VALUE;
+        break;
+    default:
+        return WHTMIX_ERROR_INVALID_VALUE;
+    }
+    out->K = K;
+    out->plan = plan;
+    out->elt = dtype == WHTMIX_DTYPE_BF16 ? 2 : 4;
+    out->kernels = plan == whtmix::PLAN_THREE_PASS ? 3 : 1;
+    if (plan == whtmix::PLAN_THREE_PASS) {
+        out->split = whtmix::three_pass_split(K);
+        out->ws_bytes = B * L * 4;
+    }
+    return WHTMIX_SUCCESS;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? WHTMIX_ERROR_OUT_OF_MEMORY : WHTMIX_ERROR_HIP;
+}
+
+// Returns a workspace of at least `bytes` for (current device, stream).
+// Caller holds g_ws_mutex.
+int get_workspace(void *stream, int64_t bytes, float **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Workspace &w = g_ws[{dev, stream}];
+    if (w.bytes < bytes) {
+        if (w.ptr) {
+            // Work already enqueued on this stream may still read the old
+            // buffer; let it finish before freeing.
+            e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+            if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+            e = hipFree(w.ptr);
+            w.ptr = nullptr;
+            w.bytes = 0;
+            if (e != hipSuccess) return hip_fail(e, "hipFree");
+        }
+        void *p = nullptr;
+        e = hipMalloc(&p, (size_t)bytes);
+        if (e != hipSuccess) {
+            g_last_error = std::string("hipMalloc of workspace (") + std::to_string(bytes) +
+                           " bytes): " + hipGetErrorString(e);
+            (void)hipGetLastError();
+            return WHTMIX_ERROR_OUT_OF_MEMORY;
+        }
+        w.ptr = static_cast<float *>(p);
+        w.bytes = bytes;
+    }
+    *out = w.ptr;
+    return WHTMIX_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
+                         const whtmix_options *options, whtmix_plan_info *info)
+{
+    if (!info) return WHTMIX_ERROR_INVALID_VALUE;
+    Checked c;
+    int st = check_shape(B, N, C, dtype, options, &c);
+    if (st != WHTMIX_SUCCESS) return st;
+    info->plan = c.plan;
+    info->kernels = c.kernels;
+    info->log2_slice = c.K;
+    info->outer_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.A : 0;
+    info->run_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.R : 0;
+    info->workspace_bytes = c.ws_bytes;
+    return WHTMIX_SUCCESS;
+}
+
+int whtmix_forward_ex(const void *x, const float *gain, void *y, int64_t B, int64_t N,
+                      int64_t C, int dtype, void *stream, const whtmix_options *options)
+{
+    Checked c;
+    int st = check_shape(B, N, C, dtype, options, &c);
+    if (st != WHTMIX_SUCCESS) return st;
+    if (B == 0) return WHTMIX_SUCCESS;
+    if (!x || !gain || !y) return WHTMIX_ERROR_INVALID_VALUE;
+    const uintptr_t px = reinterpret_cast<uintptr_t>(x);
+    const uintptr_t py = reinterpret_cast<uintptr_t>(y);
+    const uintptr_t pg = reinterpret_cast<uintptr_t>(gain);
+    if ((px | py | pg) & 15u) return WHTMIX_ERROR_MISALIGNED;
+    const uint64_t L = uint64_t(1) << c.K;
+    const uint64_t xy_bytes = (uint64_t)B * L * (uint64_t)c.elt;
+    if (px != py && overlaps(px, xy_bytes, py, xy_bytes)) return WHTMIX_ERROR_INVALID_VALUE;
+    if (overlaps(pg, L * 4, py, xy_bytes)) return WHTMIX_ERROR_INVALID_VALUE;
+
+    whtmix::LaunchArgs a{};
+    a.x = x;
+    a.gain = gain;
+    a.y = y;
+    a.B = B;
+    a.K = c.K;
+    a.dtype = dtype;
+    a.plan = c.plan;
+    a.stream = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < 4; ++i)
+        a.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
+
+    if (c.plan == whtmix::PLAN_THREE_PASS) {
+        std::lock_guard<std::mutex> lock(g_ws_mutex);
+        st = get_workspace(stream, c.ws_bytes, &a.ws);
+        if (st != WHTMIX_SUCCESS) return st;
+        hipError_t e = whtmix::launch(a);
+        if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        return WHTMIX_SUCCESS;
+    }
+    hipError_t e = whtmix::launch(a);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return WHTMIX_SUCCESS;
+}
+
+int whtmix_forward(const void *x, const float *gain, void *y, int64_t B, int64_t N, int64_t C,
+                   int dtype, void *stream)
+{
+    return whtmix_forward_ex(x, gain, y, B, N, C, dtype, stream, nullptr);
+}
+
+const char *whtmix_status_string(int status)
+{
+    switch (status) {
+    case WHTMIX_SUCCESS: return "success";
+    case WHTMIX_ERROR_INVALID_VALUE: return "invalid value";
+    case WHTMIX_ERROR_NOT_POWER_OF_TWO: return "N and C must be powers of two >= 1";
+    case WHTMIX_ERROR_UNSUPPORTED_DTYPE: return "unsupported dtype";
+    case WHTMIX_ERROR_MISALIGNED: return "x, y and gain must be 16-byte aligned";
+    case WHTMIX_ERROR_OUT_OF_MEMORY: return "workspace allocation failed";
+    case WHTMIX_ERROR_HIP: return "HIP runtime error";
+    case WHTMIX_ERROR_TOO_LARGE: return "shape too large (N*C <= 2^30, B*N*C <= 2^37)";
+    default: return "unknown status";
+    }
+}
+
+const char *whtmix_last_error(void) { return g_last_error.c_str(); }
+
+int whtmix_release_workspaces(void)
+{
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    int st = WHTMIX_SUCCESS;
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) cur = -1;
+    for (auto &kv : g_ws) {
+        Workspace &w = kv.second;
+        if (!w.ptr) continue;
+        if (hipSetDevice(kv.first.first) != hipSuccess ||
+            hipStreamSynchronize(static_cast<hipStream_t>(kv.first.second)) != hipSuccess ||
+            hipFree(w.ptr) != hipSuccess)
+            st = WHTMIX_ERROR_HIP;
+        w.ptr = nullptr;
+        w.bytes = 0;
+    }
+    g_ws.clear();
+    if (cur >= 0) (void)hipSetDevice(cur);
+    return st;
+}
+
+int whtmix_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,404 @@
+// WHTMix forward kernels for gfx950 (MI355X).
+//
+// One slice of the mixer (section III-B, eqs. (2)-(3), joint gain G[N][C]) is
+//     y = (1/L) H_L (g o H_L x),   L = N*C = 2^K,
+// on the flattened row-major index f = n*C + c (whtmix_plan.h explains why).
+// The Walsh-Hadamard transform is add/subtract work: no multiplies except the
+// single gain product, and it is bound by memory traffic and VALU issue, not
+// by matrix throughput, so there is no MFMA here.
+//
+// Tile machinery.  A workgroup owns a tile of 2^M elements (11 <= M <= 15)
+// with tile-local index t.  Each of its 2^(M-5) threads holds 32 values in
+// registers.  A "layout S" gives thread tau the 32 values whose t has
+// register index k in bits [S, S+5) and tau in the remaining bits:
+//     t = (tau mod 2^S) | (k << S) | ((tau >> S) << (S + 5)).
+// In a layout, a butterfly over t-bit S+j is a register butterfly over bit j
+// of k.  The tile's bits are transformed in groups of up to five: the top
+// group [M-5, M) straight from the global load (lanes run over the low t
+// bits, so loads coalesce), then groups [W, W+5), [W+5, W+10), ... from the
+// bottom, each reached by writing the tile to LDS in the old layout and
+// reading it back in the new one.  LDS addresses are padded by one word per
+// 32 (p = t + t/32), which keeps every layout's reads and writes free of
+// bank conflicts and keeps each register's LDS address a constant offset from
+// a per-thread base.
+//
+// Kernels (MODE):
+//   FUSED     whole slice in one tile: forward over all bits, gain, inverse.
+//   OUTER_FWD contiguous 2^A chunk of x: forward over its A bits, stored to
+//             the workspace in runs of 2^R so each middle tile is contiguous.
+//   MIDDLE    one 2^HB x 2^R workspace tile: forward over the HB high bits,
+//             gain, inverse over the HB bits (R low bits carried along).
+//   OUTER_INV mirror of OUTER_FWD: inverse over the A low bits, store y.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "whtmix_launch.h"
+#include "whtmix_plan.h"
+
+namespace whtmix {
+namespace {
+
+constexpr int VB = 5;        // log2(values per thread)
+constexpr int V = 1 << VB;   // values per thread
+
+enum Mode { OUTER_FWD = 0, MIDDLE = 1, OUTER_INV = 2, FUSED = 3 };
+
+// ---------------------------------------------------------------- elements
+__device__ __forceinline__ float load_elt(const float *p) { return *p; }
+__device__ __forceinline__ float load_elt(const __bf16 *p) { return (float)*p; }
+__device__ __forceinline__ void store_elt(float *p, float v) { *p = v; }
+// RNE rounding (v_cvt_pk_bf16_f32 on gfx950)
+__device__ __forceinline__ void store_elt(__bf16 *p, float v) { *p = (__bf16)v; }
+
+// ---------------------------------------------------------------- layouts
+template <int S>
+__device__ __forceinline__ uint32_t layout_base(uint32_t tau)
+{
+    return (tau & ((1u << S) - 1u)) | ((tau >> S) << (S + VB));
+}
+
+__host__ __device__ constexpr uint32_t pad(uint32_t t) { return t + (t >> 5); }
+
+// Tile bits [WT, M) are transformed; [0, WT) are carried untouched.
+template <int M, int WT>
+struct Groups {
+    static constexpr int TOP = M - VB;
+    // first register bit of the top group that is a transformed tile bit
+    static constexpr int JT = WT > TOP ? WT - TOP : 0;
+    static constexpr int NBOT = TOP > WT ? (TOP - WT + VB - 1) / VB : 0;
+    static constexpr int S(int i) { return WT + VB * i; }
+    static constexpr int NB(int i) { return (TOP - S(i)) < VB ? (TOP - S(i)) : VB; }
+    static constexpr int SL = NBOT > 0 ? WT + VB * (NBOT - 1) : TOP;
+};
+
+// Butterflies over register bits [J0, J1): (a, b) -> (a + b, a - b).
+template <int J0, int J1>
+__device__ __forceinline__ void butterflies(float (&v)[V])
+{
+#pragma unroll
+    for (int j = J0; j < J1; ++j) {
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            if (!(k & (1 << j))) {
+                const float a = v[k];
+                const float b = v[k | (1 << j)];
+                v[k] = a + b;
+                v[k | (1 << j)] = a - b;
+            }
+        }
+    }
+}
+
+// Re-lay the tile from layout SA to layout SB through LDS.
+template <int SA, int SB>
+__device__ __forceinline__ void exchange(float *lds, float (&v)[V], uint32_t tau)
+{
+    const uint32_t pa = pad(layout_base<SA>(tau));
+    const uint32_t pb = pad(layout_base<SB>(tau));
+    __syncthreads();   // earlier reads of this LDS tile are complete
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pa + pad((uint32_t)k << SA)] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] = lds[pb + pad((uint32_t)k << SB)];
+}
+
+// Forward bottom groups I, I+1, ... starting from layout SPREV.
+template <int M, int WT, int I, int SPREV>
+__device__ __forceinline__ void forward_groups(float *lds, float (&v)[V], uint32_t tau)
+{
+    using G = Groups<M, WT>;
+    if constexpr (I < G::NBOT) {
+        constexpr int S = G::S(I);
+        exchange<SPREV, S>(lds, v, tau);
+        butterflies<0, G::NB(I)>(v);
+        forward_groups<M, WT, I + 1, S>(lds, v, tau);
+    }
+}
+
+// Inverse bottom groups I, I-1, ..., 0 (data in group I's layout), ending in
+// the top layout.
+template <int M, int WT, int I>
+__device__ __forceinline__ void inverse_groups(float *lds, float (&v)[V], uint32_t tau)
+{
+    using G = Groups<M, WT>;
+    if constexpr (I >= 0) {
+        constexpr int S = G::S(I);
+        constexpr int SNEXT = I == 0 ? G::TOP : G::S(I - 1);
+        butterflies<0, G::NB(I)>(v);
+        exchange<S, SNEXT>(lds, v, tau);
+        inverse_groups<M, WT, I - 1>(lds, v, tau);
+    }
+}
+
+// ---------------------------------------------------------------- address maps
+// Each map sends tile-local t to an element offset from the tile's base by
+// moving bit fields, so map(a | b) = map(a) + map(b) for disjoint a, b: the
+// per-register offsets map(k << S) are compile-time constants.
+struct ContigMap {
+    __host__ __device__ static constexpr uint32_t at(uint32_t t) { return t; }
+};
+// Outer-pass chunk index lo (A bits) -> workspace: runs of 2^R elements, run
+// number lo >> R strided by a whole middle tile (2^(HB+R)).
+template <int HB, int R>
+struct RunMap {
+    __host__ __device__ static constexpr uint32_t at(uint32_t t)
+    {
+        return ((t >> R) << (HB + R)) | (t & ((1u << R) - 1u));
+    }
+};
+// Middle tile index (hi << R | run) -> flat slice index hi * 2^A + run.
+template <int A, int R>
+struct GainMap {
+    __host__ __device__ static constexpr uint32_t at(uint32_t t)
+    {
+        return ((t >> R) << A) | (t & ((1u << R) - 1u));
+    }
+};
+
+template <int S, class Map, typename T>
+__device__ __forceinline__ void load_layout(float (&v)[V], const T *base, uint32_t tau)
+{
+    const T *p = base + Map::at(layout_base<S>(tau));
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] = load_elt(p + Map::at((uint32_t)k << S));
+}
+
+template <int S, class Map, typename T>
+__device__ __forceinline__ void store_layout(const float (&v)[V], T *base, uint32_t tau)
+{
+    T *p = base + Map::at(layout_base<S>(tau));
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        store_elt(p + Map::at((uint32_t)k << S), v[k]);
+}
+
+// v *= gain * 2^-K, in layout S.
+template <int S, class Map, int K>
+__device__ __forceinline__ void apply_gain(float (&v)[V], const float *g, uint32_t tau)
+{
+    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
+    const float *p = g + Map::at(layout_base<S>(tau));
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] *= p[Map::at((uint32_t)k << S)] * scale;
+}
+
+// ---------------------------------------------------------------- kernels
+// FUSED: tile = whole slice (M = K), one workgroup per slice b.
+template <int K, typename T>
+__global__ void __launch_bounds__(1 << (K - VB))
+fused_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict__ y)
+{
+    using G = Groups<K, 0>;
+    __shared__ float lds[pad(1u << K)];
+    const uint32_t tau = threadIdx.x;
+    const size_t base = (size_t)blockIdx.x << K;
+    float v[V];
+    load_layout<G::TOP, ContigMap>(v, x + base, tau);
+    butterflies<G::JT, VB>(v);
+    forward_groups<K, 0, 0, G::TOP>(lds, v, tau);
+    apply_gain<G::SL, ContigMap, K>(v, g, tau);
+    if constexpr (G::NBOT > 0)
+        inverse_groups<K, 0, G::NBOT - 1>(lds, v, tau);
+    butterflies<G::JT, VB>(v);
+    store_layout<G::TOP, ContigMap>(v, y + base, tau);
+}
+
+// OUTER_FWD: block = b * 2^HB + hi; chunk x[b][hi * 2^A ...] -> workspace.
+template <int A, int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (A - VB))
+outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws)
+{
+    using G = Groups<A, 0>;
+    __shared__ float lds[pad(1u << A)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = blockIdx.x;
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const size_t slice = b << (A + HB);
+    float v[V];
+    load_layout<G::TOP, ContigMap>(v, x + slice + ((size_t)hi << A), tau);
+    butterflies<0, VB>(v);
+    forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
+    store_layout<G::SL, RunMap<HB, R>>(v, ws + slice + ((size_t)hi << R), tau);
+}
+
+// MIDDLE: logical tile = run * B + b (the B slices sharing a gain tile are
+// adjacent); workgroups are renumbered so adjacent logical tiles land on the
+// same XCD (blocks are dealt round-robin over the 8 XCDs) and share its L2.
+template <int A, int HB, int R>
+__global__ void __launch_bounds__(1 << (HB + R - VB))
+middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nslices)
+{
+    constexpr int M = HB + R;
+    using G = Groups<M, R>;
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t nblk = gridDim.x;
+    uint32_t logical = blockIdx.x;
+    if ((nblk & 7u) == 0)
+        logical = (blockIdx.x & 7u) * (nblk >> 3) + (blockIdx.x >> 3);
+    const uint32_t run = logical / nslices;
+    const size_t b = logical - run * nslices;
+    float *tile = ws + (b << (A + HB)) + ((size_t)run << M);
+    float v[V];
+    load_layout<G::TOP, ContigMap>(v, tile, tau);
+    butterflies<G::JT, VB>(v);
+    forward_groups<M, R, 0, G::TOP>(lds, v, tau);
+    apply_gain<G::SL, GainMap<A, R>, A + HB>(v, g + ((size_t)run << R), tau);
+    if constexpr (G::NBOT > 0)
+        inverse_groups<M, R, G::NBOT - 1>(lds, v, tau);
+    butterflies<G::JT, VB>(v);
+    store_layout<G::TOP, ContigMap>(v, tile, tau);
+}
+
+// OUTER_INV: mirror of OUTER_FWD.
+template <int A, int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (A - VB))
+outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y)
+{
+    using G = Groups<A, 0>;
+    __shared__ float lds[pad(1u << A)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = blockIdx.x;
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const size_t slice = b << (A + HB);
+    float v[V];
+    load_layout<G::SL, RunMap<HB, R>>(v, ws + slice + ((size_t)hi << R), tau);
+    inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
+    butterflies<0, VB>(v);
+    store_layout<G::TOP, ContigMap>(v, y + slice + ((size_t)hi << A), tau);
+}
+
+// SMALL: L = 2^K <= 2^10; one 256-thread workgroup per slice, every stage on
+// the LDS copy.
+template <typename T>
+__global__ void __launch_bounds__(256)
+small_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict__ y, int K)
+{
+    __shared__ float s[1 << kMaxSmall];
+    const int L = 1 << K;
+    const size_t base = (size_t)blockIdx.x << K;
+    const float scale = 1.0f / (float)L;
+    for (int i = threadIdx.x; i < L; i += blockDim.x)
+        s[i] = load_elt(x + base + i);
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int h = 1; h < L; h <<= 1) {
+            __syncthreads();
+            for (int p = threadIdx.x; p < L / 2; p += blockDim.x) {
+                const int i = ((p / h) * 2 * h) + (p % h);
+                const float a = s[i], c = s[i + h];
+                s[i] = a + c;
+                s[i + h] = a - c;
+            }
+        }
+        __syncthreads();
+        if (pass == 0)
+            for (int i = threadIdx.x; i < L; i += blockDim.x)
+                s[i] *= g[i] * scale;
+    }
+    for (int i = threadIdx.x; i < L; i += blockDim.x)
+        store_elt(y + base + i, s[i]);
+}
+
+// ---------------------------------------------------------------- launchers
+inline hipError_t record(hipEvent_t ev, hipStream_t st)
+{
+    return ev ? hipEventRecord(ev, st) : hipSuccess;
+}
+
+template <int K, typename T>
+hipError_t launch_fused(const T *x, const float *g, T *y, int64_t B, hipStream_t st,
+                        hipEvent_t const *ev)
+{
+    hipError_t e = record(ev[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((fused_kernel<K, T>), dim3((uint32_t)B), dim3(1u << (K - VB)), 0, st,
+                       x, g, y);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return record(ev[1], st);
+}
+
+template <int K, typename T>
+hipError_t launch_three_pass(const T *x, const float *g, T *y, float *ws, int64_t B,
+                             hipStream_t st, hipEvent_t const *ev)
+{
+    constexpr Split sp = three_pass_split(K);
+    constexpr int A = sp.A, HB = sp.HB, R = sp.R;
+    static_assert(A >= kMinTile && A <= kMaxTile, "outer tile size");
+    static_assert(HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
+    static_assert(HB >= 1 && R >= 0 && R <= A, "split");
+    hipError_t e = record(ev[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(B << HB)),
+                       dim3(1u << (A - VB)), 0, st, x, ws);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(ev[1], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((middle_kernel<A, HB, R>), dim3((uint32_t)(B << (A - R))),
+                       dim3(1u << (HB + R - VB)), 0, st, ws, g, (uint32_t)B);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(ev[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(B << HB)),
+                       dim3(1u << (A - VB)), 0, st, ws, y);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(ev[3], st);
+}
+
+template <typename T>
+hipError_t launch_small(const T *x, const float *g, T *y, int64_t B, int K, hipStream_t st,
+                        hipEvent_t const *ev)
+{
+    hipError_t e = record(ev[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((small_kernel<T>), dim3((uint32_t)B), dim3(256), 0, st, x, g, y, K);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(ev[1], st);
+}
+
+template <typename T>
+hipError_t dispatch(const LaunchArgs &a)
+{
+    const T *x = static_cast<const T *>(a.x);
+    T *y = static_cast<T *>(a.y);
+    const int K = a.K;
+    if (a.plan == PLAN_SMALL)
+        return launch_small<T>(x, a.gain, y, a.B, K, a.stream, a.events);
+    if (a.plan == PLAN_FUSED) {
+        switch (K) {
+#define WHTMIX_FUSED_CASE(k) \
+    case k: return launch_fused<k, T>(x, a.gain, y, a.B, a.stream, a.events);
+            WHTMIX_FUSED_CASE(11) WHTMIX_FUSED_CASE(12) WHTMIX_FUSED_CASE(13)
+            WHTMIX_FUSED_CASE(14) WHTMIX_FUSED_CASE(15)
+#undef WHTMIX_FUSED_CASE
+        default: return hipErrorInvalidValue;
+        }
+    }
+    switch (K) {
+#define WHTMIX_3P_CASE(k) \
+    case k: return launch_three_pass<k, T>(x, a.gain, y, a.ws, a.B, a.stream, a.events);
+        WHTMIX_3P_CASE(12) WHTMIX_3P_CASE(13) WHTMIX_3P_CASE(14) WHTMIX_3P_CASE(15)
+        WHTMIX_3P_CASE(16) WHTMIX_3P_CASE(17) WHTMIX_3P_CASE(18) WHTMIX_3P_CASE(19)
+        WHTMIX_3P_CASE(20) WHTMIX_3P_CASE(21) WHTMIX_3P_CASE(22) WHTMIX_3P_CASE(23)
+        WHTMIX_3P_CASE(24) WHTMIX_3P_CASE(25) WHTMIX_3P_CASE(26) WHTMIX_3P_CASE(27)
+        WHTMIX_3P_CASE(28) WHTMIX_3P_CASE(29) WHTMIX_3P_CASE(30)
+#undef WHTMIX_3P_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch(const LaunchArgs &a)
+{
+    if (a.dtype == DTYPE_BF16)
+        return dispatch<__bf16>(a);
+    return dispatch<float>(a);
+}
+
+}  // namespace whtmix

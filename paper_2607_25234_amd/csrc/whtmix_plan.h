@@ -1,0 +1,53 @@
+// Plan table shared by the host entry points and the kernel launchers.
+//
+// The mixer of one slice is, on the flattened row-major index f = n*C + c of
+// length L = N*C = 2^K, y = (1/L) H_L (g o H_L x) with H_L the +/-1 Sylvester
+// matrix: H_N (x) H_C = H_{N*C} in Sylvester order, so the channel and token
+// transforms of section III-B (eqs. (2)-(3)) together are one Walsh-Hadamard
+// transform over all K bits of f, and the four 1/sqrt factors multiply to 1/L.
+// Sylvester butterflies over disjoint bit groups commute and need no twiddle
+// factors, so any split of the K bits into passes is exact.
+#pragma once
+
+namespace whtmix {
+
+enum PlanKind { PLAN_AUTO = 0, PLAN_SMALL = 1, PLAN_FUSED = 2, PLAN_THREE_PASS = 3 };
+
+constexpr int kMaxLog2Slice = 30;   // N*C <= 2^30
+constexpr int kMaxSmall = 10;       // SMALL: L <= 2^10
+constexpr int kMinTile = 11;        // tiles hold 2^11 .. 2^15 elements
+constexpr int kMaxTile = 15;
+
+// THREE_PASS split for slice bits K:
+//   outer passes: contiguous chunks of 2^A elements (all A low bits of f);
+//   middle pass : the HB = K - A high bits, for a run of 2^R contiguous low
+//                 elements carried along (R bits untransformed), so one middle
+//                 tile holds 2^(HB + R) elements.
+struct Split {
+    int A, HB, R;
+};
+
+constexpr int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// Automatic split for K >= 16: balance the outer and middle tile sizes and
+// carry runs of 32 floats (128 bytes) where the tile limits allow.
+constexpr Split auto_split(int K)
+{
+    int A = clampi((K + 6) / 2, kMinTile, kMaxTile);
+    int HB = K - A;
+    int R = clampi(5, kMinTile - HB, kMaxTile - HB);
+    return Split{A, HB, R};
+}
+
+// Forced THREE_PASS for 12 <= K <= 15 (the shapes FUSED would take).
+constexpr Split forced_split(int K)
+{
+    return Split{kMinTile, K - kMinTile, 2 * kMinTile - K};
+}
+
+constexpr Split three_pass_split(int K)
+{
+    return K >= 16 ? auto_split(K) : forced_split(K);
+}
+
+}  // namespace whtmix

@@ -1,0 +1,173 @@
+"""Python binding of the WHTMix C ABI (include/whtmix.h).
+
+Argument marshalling only: every step of the mixer runs in the HIP kernels of
+``libwhtmix.so``.  PyTorch supplies device memory and the current stream.
+There is no fallback: if the library is missing, importing the functions
+that need it raises.
+
+    y = forward(x, gain)          # x [B, N, C] (or [N, C]) f32/bf16, gain [N, C] f32
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libwhtmix.so")
+
+SUCCESS = 0
+DTYPE_F32, DTYPE_BF16 = 0, 1
+PLANS = {"auto": 0, "small": 1, "fused": 2, "three_pass": 3}
+PLAN_NAMES = {v: k for k, v in PLANS.items()}
+
+# Every symbol include/whtmix.h declares.
+EXPORTS = (
+    "whtmix_forward",
+    "whtmix_forward_ex",
+    "whtmix_plan_describe",
+    "whtmix_status_string",
+    "whtmix_last_error",
+    "whtmix_release_workspaces",
+    "whtmix_version",
+)
+
+
+class WhtmixError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})"
+                         + (f" [{last_error()}]" if last_error() else ""))
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("plan", ctypes.c_int), ("events", ctypes.c_void_p * 4)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("plan", ctypes.c_int), ("kernels", ctypes.c_int),
+                ("log2_slice", ctypes.c_int), ("outer_bits", ctypes.c_int),
+                ("run_bits", ctypes.c_int), ("workspace_bytes", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libwhtmix.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2607_25234_amd.build` (there is no fallback)")
+        try:
+            # Load torch's HIP runtime first so that the library binds to the
+            # same runtime instance (same soname) as the tensors and streams.
+            import torch  # noqa: F401
+        except ImportError:
+            pass
+        L = ctypes.CDLL(LIB_PATH)
+        i64, vp = ctypes.c_int64, ctypes.c_void_p
+        L.whtmix_forward.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
+        L.whtmix_forward.restype = ctypes.c_int
+        L.whtmix_forward_ex.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
+                                        ctypes.POINTER(Options)]
+        L.whtmix_forward_ex.restype = ctypes.c_int
+        L.whtmix_plan_describe.argtypes = [i64, i64, i64, ctypes.c_int,
+                                           ctypes.POINTER(Options), ctypes.POINTER(PlanInfo)]
+        L.whtmix_plan_describe.restype = ctypes.c_int
+        L.whtmix_status_string.argtypes = [ctypes.c_int]
+        L.whtmix_status_string.restype = ctypes.c_char_p
+        L.whtmix_last_error.argtypes = []
+        L.whtmix_last_error.restype = ctypes.c_char_p
+        L.whtmix_release_workspaces.argtypes = []
+        L.whtmix_release_workspaces.restype = ctypes.c_int
+        L.whtmix_version.argtypes = []
+        L.whtmix_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().whtmix_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().whtmix_last_error().decode()
+
+
+def _options(plan: str | int = "auto", events=None) -> Options:
+    o = Options()
+    o.plan = PLANS[plan] if isinstance(plan, str) else int(plan)
+    for i, ev in enumerate(events or ()):
+        o.events[i] = ev
+    return o
+
+
+def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = "auto") -> dict:
+    """How a shape would run; raises WhtmixError on an invalid shape."""
+    info = PlanInfo()
+    opt = _options(plan)
+    st = lib().whtmix_plan_describe(B, N, C, DTYPE_BF16 if dtype == "bf16" else DTYPE_F32,
+                                    ctypes.byref(opt), ctypes.byref(info))
+    if st != SUCCESS:
+        raise WhtmixError(st, "whtmix_plan_describe")
+    return {"plan": PLAN_NAMES[info.plan], "kernels": info.kernels,
+            "log2_slice": info.log2_slice, "outer_bits": info.outer_bits,
+            "run_bits": info.run_bits, "workspace_bytes": info.workspace_bytes}
+
+
+def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
+                dtype: int, stream: int, plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_forward_ex with integer pointers; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream,
+                                   ctypes.byref(opt))
+
+
+def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=None):
+    """y[b] = H_N (G o (H_N x[b] H_C)) H_C on the GPU (section III-B, eqs. (2)-(3)).
+
+    x: torch tensor [B, N, C] or [N, C], float32 or bfloat16, on a ROCm device.
+    gain: float32 [N, C] on the same device.  out: optional tensor like x
+    (may be x itself for in-place).  stream: a torch.cuda.Stream (default:
+    the current stream)."""
+    import torch
+
+    if x.device.type != "cuda" or gain.device != x.device:
+        raise ValueError("x and gain must be on the same GPU device")
+    if x.dtype == torch.float32:
+        dt = DTYPE_F32
+    elif x.dtype == torch.bfloat16:
+        dt = DTYPE_BF16
+    else:
+        raise TypeError(f"x must be float32 or bfloat16, got {x.dtype}")
+    if gain.dtype != torch.float32:
+        raise TypeError("gain must be float32")
+    squeeze = x.dim() == 2
+    xx = x.unsqueeze(0) if squeeze else x
+    if xx.dim() != 3:
+        raise ValueError("x must be [B, N, C] or [N, C]")
+    B, N, C = xx.shape
+    if tuple(gain.shape) != (N, C):
+        raise ValueError(f"gain shape {tuple(gain.shape)} != {(N, C)}")
+    if not xx.is_contiguous() or not gain.is_contiguous():
+        raise ValueError("x and gain must be contiguous")
+    if out is None:
+        out = torch.empty_like(x)
+    elif out.shape != x.shape or out.dtype != x.dtype or not out.is_contiguous() \
+            or out.device != x.device:
+        raise ValueError("out must be a contiguous tensor like x")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = forward_raw(xx.data_ptr(), gain.data_ptr(), out.data_ptr(), B, N, C, dt,
+                             st.cuda_stream, plan, events)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_forward")
+    return out
+
+
+def release_workspaces() -> None:
+    st = lib().whtmix_release_workspaces()
+    if st != SUCCESS:
+        raise WhtmixError(st, "whtmix_release_workspaces")

@@ -17,9 +17,9 @@ the stereo backbone (section III-A: N = 2 (H/8)(W/8) joint tokens of the left
 and right views), the 1k and 4k ones for the byte-level image and text
 sequence-classification tasks (section IV-D).  No dataset item is reproduced:
 X ~ N(0, 1) (or embeddings of uniform random integer tokens through a
-N(0, 0.02) table for the text workload) and G ~ U(0.5, 1.5), drawn with numpy's
-PCG64 generator seeded per workload, in the order X then G (text workload:
-table, tokens, G).  bf16 workloads round X to bf16 with round-to-nearest-even
+N(0, 0.02) table for the text workload) and G ~ U(0.5, 1.5), drawn in float32 with
+numpy's PCG64 generator seeded per workload, in the order X then G (text
+workload: table, tokens, G).  bf16 workloads round X to bf16 with round-to-nearest-even
 before either side sees it, so both sides receive identical values.
 """
 from __future__ import annotations
@@ -71,16 +71,26 @@ WORKLOADS = {
 BENCH_WORKLOAD = "stereo64k_bf16"
 
 
-def round_to_bf16(x: np.ndarray) -> np.ndarray:
+def round_to_bf16(x: np.ndarray, inplace: bool = False) -> np.ndarray:
     """Round float32 values to the nearest bf16 (ties to even), kept as float32."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
-    out = r.view(np.float32).copy()
-    nan = np.isnan(x)
-    if nan.any():
-        out[nan] = np.float32("nan")
+    out = x if inplace else np.array(x, dtype=np.float32, copy=True, order="C")
+    if out.dtype != np.float32 or not out.flags.c_contiguous:
+        raise ValueError("round_to_bf16 works on contiguous float32 arrays")
+    flat = out.reshape(-1)
+    u = flat.view(np.uint32)
+    step = 1 << 20
+    lsb = np.empty(min(step, u.size), dtype=np.uint32)
+    for i in range(0, u.size, step):
+        seg = u[i:i + step]
+        t = lsb[:seg.size]
+        nan = np.isnan(flat[i:i + step])
+        np.right_shift(seg, 16, out=t)
+        np.bitwise_and(t, 1, out=t)
+        seg += t          # finite values: u + lsb + 0x7FFF stays below 2^32
+        seg += 0x7FFF
+        seg &= 0xFFFF0000
+        if nan.any():
+            flat[i:i + step][nan] = np.float32("nan")
     return out
 
 
@@ -98,16 +108,18 @@ def draw(B: int, N: int, C: int, dtype: str = "f32", seed: int = 0,
     g float32 [N, C] ~ U(gain_lo, gain_hi)."""
     rng = np.random.default_rng(seed)
     if x_dist == "normal":
-        x = rng.standard_normal((B, N, C)).astype(np.float32)
+        x = rng.standard_normal((B, N, C), dtype=np.float32)
     elif x_dist == "embed":
-        table = (0.02 * rng.standard_normal((256, C))).astype(np.float32)
+        table = np.float32(0.02) * rng.standard_normal((256, C), dtype=np.float32)
         tokens = rng.integers(0, 256, size=(B, N))
         x = table[tokens]
     else:
         raise ValueError(f"unknown x distribution {x_dist!r}")
-    g = rng.uniform(gain_lo, gain_hi, size=(N, C)).astype(np.float32)
+    g = rng.random((N, C), dtype=np.float32)
+    g *= np.float32(gain_hi - gain_lo)
+    g += np.float32(gain_lo)
     if dtype == "bf16":
-        x = round_to_bf16(x)
+        x = round_to_bf16(x, inplace=True)
     elif dtype != "f32":
         raise ValueError(f"unknown dtype {dtype!r}")
     return np.ascontiguousarray(x), np.ascontiguousarray(g)

@@ -1,0 +1,54 @@
+"""Helpers shared by the GPU tests (not collected by pytest)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def device():
+    import pytest
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU test run without a visible GPU")
+    return torch.device("cuda:0")
+
+
+def to_device(x: np.ndarray, dtype: str, dev):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def to_host(t) -> np.ndarray:
+    import torch
+    return t.detach().to(torch.float32).cpu().numpy()
+
+
+def run_gpu(x: np.ndarray, g: np.ndarray, dtype: str, dev, plan="auto") -> np.ndarray:
+    import torch
+    from paper_2607_25234_amd import whtmix
+    xd = to_device(x, dtype, dev)
+    gd = torch.from_numpy(np.ascontiguousarray(g, dtype=np.float32)).to(dev)
+    y = whtmix.forward(xd, gd, plan=plan)
+    torch.cuda.synchronize(dev)
+    return to_host(y)
+
+
+def errors(y: np.ndarray, ref: np.ndarray) -> tuple[float, float]:
+    """(normwise max relative error, rms relative error)."""
+    y = np.asarray(y, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0, 0.0
+    den = max(float(np.max(np.abs(ref))), 1e-300)
+    d = y - ref
+    rms_den = max(float(np.sqrt(np.mean(ref * ref))), 1e-300)
+    return float(np.max(np.abs(d)) / den), float(np.sqrt(np.mean(d * d)) / rms_den)

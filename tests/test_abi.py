@@ -1,0 +1,124 @@
+"""The C ABI on the host: the library loads, exports what include/whtmix.h
+declares, and rejects bad arguments before any HIP call (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_25234_amd import whtmix
+from paper_2607_25234_amd import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "whtmix.h")
+
+ALIGNED = 0x10000          # fake device addresses: never dereferenced, every
+ALIGNED2 = 0x40000000      # call below is rejected or is a no-op on the host
+
+
+def header_symbols():
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"WHTMIX_API\s+[\w\s\*]*?\b(whtmix_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert header_symbols() == sorted(whtmix.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = whtmix.lib()
+    for name in header_symbols():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_library_exports_nothing_else():
+    """Only the C API is visible (internal C++ symbols are hidden)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", whtmix.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    text_syms = sorted(l.split()[-1] for l in out.splitlines() if " T " in l)
+    assert text_syms == sorted(header_symbols())
+
+
+def test_version_and_status_strings():
+    assert whtmix.lib().whtmix_version() == 100
+    for st in range(8):
+        assert whtmix.status_string(st)
+    assert whtmix.status_string(99) == "unknown status"
+
+
+def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
+    return whtmix.forward_raw(x, g, y, B, N, C, dtype, 0, plan)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(dtype=2), 3),
+    (dict(dtype=-1), 3),
+    (dict(B=-1), 1),
+    (dict(N=3), 2),
+    (dict(C=0), 2),
+    (dict(N=0), 2),
+    (dict(N=-4), 2),
+    (dict(N=1 << 16, C=1 << 15), 7),          # N*C = 2^31 > 2^30
+    (dict(B=1 << 30, N=1 << 10, C=1 << 10), 7),  # B*N*C beyond the grid limit
+    (dict(x=0), 1),
+    (dict(g=0), 1),
+    (dict(y=0), 1),
+    (dict(x=ALIGNED + 4, y=ALIGNED2 * 2), 4),
+    (dict(g=ALIGNED2 + 8), 4),
+    (dict(y=ALIGNED + 4 * 64), 1),            # partial overlap of x and y
+    (dict(g=ALIGNED + 16, y=ALIGNED), 1),     # gain inside y
+    (dict(plan=9), 1),
+    (dict(plan=1, N=64, C=64), 1),            # SMALL needs N*C <= 2^10
+    (dict(plan=2, N=8, C=8), 1),              # FUSED needs 2^11..2^15
+    (dict(plan=2, N=1024, C=64), 1),
+    (dict(plan=3, N=32, C=64), 1),            # THREE_PASS needs >= 2^12
+])
+def test_rejected_before_any_hip_call(kwargs, status):
+    assert call(**kwargs) == status
+
+
+def test_empty_batch_is_a_no_op():
+    assert whtmix.forward_raw(0, 0, 0, 0, 64, 64, 0, 0) == 0
+    assert whtmix.forward_raw(0, 0, 0, 0, 1 << 20, 1 << 7, 1, 0) == 0
+
+
+def test_plan_table():
+    d = whtmix.plan_describe(1, 1, 1)
+    assert d["plan"] == "small" and d["kernels"] == 1 and d["workspace_bytes"] == 0
+    assert whtmix.plan_describe(3, 32, 32)["plan"] == "small"
+    assert whtmix.plan_describe(3, 32, 64)["plan"] == "fused"
+    assert whtmix.plan_describe(3, 256, 128)["plan"] == "fused"
+    d = whtmix.plan_describe(3, 512, 128, "bf16")
+    assert d["plan"] == "three_pass" and d["kernels"] == 3
+    assert d["workspace_bytes"] == 3 * 512 * 128 * 4
+    d = whtmix.plan_describe(2, 64, 64, plan="three_pass")
+    assert d["plan"] == "three_pass" and d["outer_bits"] == 11
+    for w in workloads.WORKLOADS.values():
+        d = whtmix.plan_describe(w.B, w.N, w.C, w.dtype)
+        K = d["log2_slice"]
+        assert 1 << K == w.N * w.C
+        if K >= 16:
+            A, R = d["outer_bits"], d["run_bits"]
+            assert d["plan"] == "three_pass"
+            assert 11 <= A <= 15 and 11 <= K - A + R <= 15 and R <= A
+
+
+def test_every_three_pass_split_fits_the_tiles():
+    for K in range(12, 31):
+        N = 1 << (K // 2)
+        C = 1 << (K - K // 2)
+        d = whtmix.plan_describe(1, N, C, plan="three_pass")
+        A, R = d["outer_bits"], d["run_bits"]
+        assert 11 <= A <= 15, K
+        assert 1 <= K - A and 11 <= K - A + R <= 15 and 0 <= R <= A, K
+
+
+def test_python_forward_rejects_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 64, 64)
+    g = torch.ones(64, 64)
+    with pytest.raises(ValueError):
+        whtmix.forward(x, g)

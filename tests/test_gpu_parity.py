@@ -1,0 +1,224 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Both sides receive the same seeded inputs (paper_2607_25234_amd.workloads);
+the oracle computes in float64.  The bar is the normwise maximum relative
+error max|y - r| / max|r| over the whole output: <= 1e-5 for float32 I/O and
+<= 2e-2 for bf16 I/O with float32 arithmetic.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as oracle_mod
+from paper_2607_25234_amd import whtmix, workloads
+from tests.gpu_util import TOL, device, errors, run_gpu, say, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle_mod.Oracle()
+
+
+def check(name, y, ref, dtype):
+    err, rms = errors(y, ref)
+    say(f"  {name}: normwise-max {err:.3e} rms {rms:.3e} (tol {TOL[dtype]:g})")
+    assert y.shape == ref.shape
+    assert np.all(np.isfinite(y))
+    assert err <= TOL[dtype], (name, err)
+    return err
+
+
+@pytest.mark.parametrize("name", list(workloads.WORKLOADS))
+def test_workload_parity(name, dev, orc):
+    """Every workload at full size, in the plan the benchmark runs."""
+    w = workloads.WORKLOADS[name]
+    say(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}")
+    x, g = workloads.inputs(w)
+    y = run_gpu(x, g, w.dtype, dev)
+    ref = orc.whtmix(x, g)
+    check(name, y, ref, w.dtype)
+
+
+SHAPES = [
+    # (B, N, C) -- K = log2(N*C) from 0 (degenerate) to 20, square and
+    # skewed, every plan and every three-pass split shape class
+    (1, 1, 1), (3, 1, 1), (2, 2, 1), (1, 1, 2), (2, 4, 8), (1, 16, 1),
+    (5, 32, 32), (2, 1, 1024), (1, 1024, 1),
+    (3, 64, 32), (1, 2048, 1), (2, 1, 2048), (2, 128, 32), (4, 64, 128),
+    (1, 8192, 2), (2, 512, 64), (3, 256, 128),
+    (1, 1024, 64), (2, 65536, 1), (1, 1, 65536), (2, 512, 256),
+    (1, 4096, 64), (3, 1024, 256), (1, 16384, 64), (2, 4096, 512),
+    (1, 8192, 128),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_shapes(shape, dtype, dev, orc):
+    B, N, C = shape
+    x, g = workloads.draw(B, N, C, dtype, seed=11 + N + 3 * C + B)
+    plan = whtmix.plan_describe(B, N, C, dtype)["plan"]
+    say(f"shape {shape} {dtype} plan={plan}")
+    y = run_gpu(x, g, dtype, dev)
+    check(f"{shape}", y, orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("K", [12, 13, 14, 15])
+def test_three_pass_matches_fused(K, dev, orc):
+    """Slices that fit one workgroup, forced through the three-pass plan too."""
+    N, C = 1 << (K - 6), 64
+    x, g = workloads.draw(3, N, C, "f32", seed=K)
+    say(f"K={K}: fused vs three_pass")
+    ref = orc.whtmix(x, g)
+    y_f = run_gpu(x, g, "f32", dev, plan="fused")
+    y_3 = run_gpu(x, g, "f32", dev, plan="three_pass")
+    check("fused", y_f, ref, "f32")
+    check("three_pass", y_3, ref, "f32")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32, 16), (2, 64, 64), (2, 4096, 64)])
+def test_in_place(shape, dtype, dev, orc):
+    import torch
+    B, N, C = shape
+    x, g = workloads.draw(B, N, C, dtype, seed=5)
+    xd = to_device(x, dtype, dev)
+    gd = torch.from_numpy(g).to(dev)
+    out = whtmix.forward(xd, gd, out=xd)
+    torch.cuda.synchronize()
+    assert out.data_ptr() == xd.data_ptr()
+    check(f"in-place {shape}", to_host(xd), orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 32, 32), (2, 128, 64), (4, 65536, 128)])
+def test_unit_gain_is_identity(shape, dtype, dev):
+    """G = 1 (the paper's zero-initialised log gain) returns x; for bf16 the
+    float32 result is within far less than half a bf16 ulp of x, so the
+    rounded output is x exactly."""
+    B, N, C = shape
+    x, _ = workloads.draw(B, N, C, dtype, seed=21)
+    y = run_gpu(x, np.ones((N, C), np.float32), dtype, dev)
+    if dtype == "bf16":
+        assert np.array_equal(y, x)
+    else:
+        assert errors(y, x)[0] < 1e-6
+
+
+def test_deterministic_and_batch_independent(dev):
+    import torch
+    x, g = workloads.draw(4, 4096, 64, "f32", seed=3)
+    xd = to_device(x, "f32", dev)
+    gd = torch.from_numpy(g).to(dev)
+    y1 = to_host(whtmix.forward(xd, gd))
+    y2 = to_host(whtmix.forward(xd, gd))
+    assert np.array_equal(y1, y2)
+    for b in [0, 3]:
+        yb = to_host(whtmix.forward(xd[b:b + 1].contiguous(), gd))
+        assert np.array_equal(yb[0], y1[b])
+
+
+def test_bf16_round_to_nearest_even(dev):
+    """N = C = 1 reduces the mixer to y = g x: products placed exactly on bf16
+    halfway points must round to the even neighbour."""
+    import torch
+    xs = np.array([1.0, 1.0, -1.0, 2.0, 1.0], np.float32)
+    gs = np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 2 ** -8, 1 + 2 ** -9, 1 + 2 ** -8 + 2 ** -20],
+                  np.float32)
+    want = [1.0, 1 + 2 ** -6, -1.0, 2.0, 1 + 2 ** -7]
+    for xv, gv, wv in zip(xs, gs, want):
+        y = run_gpu(np.array([[[xv]]]), np.array([[gv]]), "bf16", dev)
+        assert float(y.reshape(-1)[0]) == wv, (xv, gv, y, wv)
+    del torch
+
+
+def test_device_pointer_checks(dev):
+    import torch
+    x = torch.zeros(2, 64, 64, device=dev)
+    g = torch.ones(64, 64, device=dev)
+    y = torch.zeros(2, 64, 64, device=dev)
+    s = torch.cuda.current_stream().cuda_stream
+    assert whtmix.forward_raw(x.data_ptr() + 4, g.data_ptr(), y.data_ptr(), 1, 64, 64, 0, s) == 4
+    assert whtmix.forward_raw(x.data_ptr(), g.data_ptr(), x.data_ptr() + 1024, 1, 64, 64, 0, s) == 1
+    assert whtmix.forward_raw(x.data_ptr(), y.data_ptr(), y.data_ptr(), 1, 64, 64, 0, s) == 1
+    assert whtmix.forward_raw(x.data_ptr(), g.data_ptr(), y.data_ptr(), 0, 64, 64, 0, s) == 0
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(y).item() == 0
+
+
+def test_workspace_growth_and_streams(dev, orc):
+    """Growing the per-stream workspace, then shrinking the shape, on two
+    streams whose work overlaps."""
+    import torch
+    cases = [(1, 4096, 64), (2, 16384, 128), (1, 2048, 64)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for i, (B, N, C) in enumerate(cases):
+        x, g = workloads.draw(B, N, C, "f32", seed=40 + i)
+        x2, g2 = workloads.draw(B, N, C, "f32", seed=50 + i)
+        xd, gd = to_device(x, "f32", dev), torch.from_numpy(g).to(dev)
+        xd2, gd2 = to_device(x2, "f32", dev), torch.from_numpy(g2).to(dev)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            y1 = whtmix.forward(xd, gd)
+        with torch.cuda.stream(s2):
+            y2 = whtmix.forward(xd2, gd2)
+        torch.cuda.synchronize()
+        check(f"stream1 {(B, N, C)}", to_host(y1), orc.whtmix(x, g), "f32")
+        check(f"stream2 {(B, N, C)}", to_host(y2), orc.whtmix(x2, g2), "f32")
+
+
+@pytest.mark.parametrize("shape", [(1, 1 << 22, 256), (2, 1 << 20, 256)])
+def test_large_slices_by_properties(shape, dev):
+    """Up to the largest slice (N*C = 2^30), where the float64 oracle would be
+    slow: unit gain returns x, a +/-1 gain preserves energy, and a one-hot
+    gain at (2^p, 2^q) projects x on the Walsh image s_n s_c / sqrt(N C)
+    with s_n = (-1)^(bit p of n), s_c = (-1)^(bit q of c)."""
+    import torch
+    B, N, C = shape
+    say(f"large {shape}")
+    gen = torch.Generator(device=dev).manual_seed(7)
+    x = torch.randn(B, N, C, device=dev, generator=gen)
+    ones = torch.ones(N, C, device=dev)
+    y = whtmix.forward(x, ones)
+    err = ((y - x).abs().max() / x.abs().max()).item()
+    say(f"  unit gain err {err:.3e}")
+    assert err < 1e-5
+    del y
+    sign = torch.where(torch.rand(N, C, device=dev, generator=gen) < 0.5, -1.0, 1.0)
+    y = whtmix.forward(x, sign)
+    r = (torch.linalg.vector_norm(y.double()) / torch.linalg.vector_norm(x.double())).item()
+    say(f"  energy ratio {r:.9f}")
+    assert abs(r - 1) < 1e-5
+    del y, sign
+    p, q = 17, 3
+    n = torch.arange(N, device=dev)
+    c = torch.arange(C, device=dev)
+    sn = (1 - 2 * ((n >> p) & 1)).double()
+    sc = (1 - 2 * ((c >> q) & 1)).double()
+    g = torch.zeros(N, C, device=dev)
+    g[1 << p, 1 << q] = 1.0
+    y = whtmix.forward(x, g)
+    scale = 1.0 / np.sqrt(float(N) * C)
+    rows = 1 << 18
+    for b in range(B):
+        coef = 0.0
+        for r0 in range(0, N, rows):
+            xb = x[b, r0:r0 + rows].double()
+            coef += float(torch.mv(xb.t().contiguous(), sn[r0:r0 + rows]).dot(sc))
+        # error scale: the coefficient <x, B> has standard deviation rms(x)
+        # (B has unit norm), so judge against max(|<x, B>|, rms(x))
+        xrms = float(x[b].double().pow(2).mean().sqrt())
+        amp = max(abs(coef) * scale, xrms) * scale
+        worst = 0.0
+        for r0 in range(0, N, rows):
+            ref = (coef * scale * scale) * sn[r0:r0 + rows, None] * sc[None, :]
+            worst = max(worst, (y[b, r0:r0 + rows].double() - ref).abs().max().item())
+        say(f"  one-hot slice {b} err {worst / amp:.3e}")
+        assert worst / amp < 1e-5
+    torch.cuda.synchronize()

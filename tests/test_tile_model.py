@@ -1,0 +1,290 @@
+"""CPU model of the HIP kernels' tile index maps (no GPU).
+
+Re-states, in numpy, the index arithmetic of csrc/whtmix_kernels.hip (layouts,
+LDS padding, bit groups, workspace run map, gain map, block decoding) and the
+plan table of csrc/whtmix_plan.h, then checks for every plan shape:
+
+* every global load/store and every LDS access stays inside its buffer;
+* each kernel reads and writes every element of its tile exactly once, and
+  the tiles of a launch partition the buffer;
+* executing the modelled schedule (butterflies, exchanges, gain) on data
+  reproduces the CPU oracle -- i.e. the bit-group plan transforms every bit
+  of the flattened index exactly once in each direction.
+
+The model is test code only; nothing in the product path uses it.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as oracle_mod
+
+VB, V = 5, 32
+
+
+def pad(t):
+    return t + (t >> 5)
+
+
+def layout_base(S, tau):
+    return (tau & ((1 << S) - 1)) | ((tau >> S) << (S + VB))
+
+
+def layout_index(S, tau):
+    """[P, 32] tile indices of every thread's registers in layout S."""
+    k = np.arange(V)[None, :]
+    return layout_base(S, tau)[:, None] | (k << S)
+
+
+class Groups:
+    def __init__(self, M, WT):
+        self.M, self.WT = M, WT
+        self.TOP = M - VB
+        self.JT = WT - self.TOP if WT > self.TOP else 0
+        self.NBOT = (self.TOP - WT + VB - 1) // VB if self.TOP > WT else 0
+        self.SL = WT + VB * (self.NBOT - 1) if self.NBOT > 0 else self.TOP
+
+    def S(self, i):
+        return self.WT + VB * i
+
+    def NB(self, i):
+        return min(VB, self.TOP - self.S(i))
+
+
+def clampi(v, lo, hi):
+    return max(lo, min(hi, v))
+
+
+def three_pass_split(K):
+    if K >= 16:
+        A = clampi((K + 6) // 2, 11, 15)
+        HB = K - A
+        R = clampi(5, 11 - HB, 15 - HB)
+        return A, HB, R
+    return 11, K - 11, 22 - K
+
+
+def butterflies(v, j0, j1):
+    for j in range(j0, j1):
+        h = 1 << j
+        for k in range(V):
+            if not k & h:
+                a, b = v[:, k].copy(), v[:, k | h].copy()
+                v[:, k], v[:, k | h] = a + b, a - b
+
+
+class Tile:
+    """One workgroup: P threads x 32 registers, plus an LDS array."""
+
+    def __init__(self, M, WT):
+        self.g = Groups(M, WT)
+        self.P = 1 << (M - VB)
+        self.tau = np.arange(self.P)
+        self.lds = np.full(pad(1 << M), np.nan)
+        self.lds_touched = np.zeros(pad(1 << M), bool)
+
+    def idx(self, S):
+        return layout_index(S, self.tau)
+
+    def exchange(self, v, SA, SB):
+        ia, ib = pad(self.idx(SA)), pad(self.idx(SB))
+        assert ia.max() < self.lds.size and ib.max() < self.lds.size
+        assert len(np.unique(ia)) == ia.size and len(np.unique(ib)) == ib.size
+        self.lds[:] = np.nan
+        self.lds[ia] = v
+        self.lds_touched[ia] = True
+        out = self.lds[ib]
+        assert not np.isnan(out).any(), "read an LDS word no thread wrote"
+        return out
+
+    def forward_groups(self, v, SPREV):
+        g = self.g
+        for i in range(g.NBOT):
+            v = self.exchange(v, SPREV, g.S(i))
+            butterflies(v, 0, g.NB(i))
+            SPREV = g.S(i)
+        return v
+
+    def inverse_groups(self, v):
+        g = self.g
+        for i in range(g.NBOT - 1, -1, -1):
+            butterflies(v, 0, g.NB(i))
+            snext = g.TOP if i == 0 else g.S(i - 1)
+            v = self.exchange(v, g.S(i), snext)
+        return v
+
+
+def contig_map(t, **_):
+    return t
+
+
+def run_map(t, HB, R):
+    return ((t >> R) << (HB + R)) | (t & ((1 << R) - 1))
+
+
+def gain_map(t, A, R):
+    return ((t >> R) << A) | (t & ((1 << R) - 1))
+
+
+class Access:
+    """Records every element offset read or written in a buffer."""
+
+    def __init__(self, size):
+        self.size = size
+        self.count = np.zeros(size, np.int64)
+
+    def at(self, offs):
+        assert offs.min() >= 0 and offs.max() < self.size, "out of bounds"
+        np.add.at(self.count, offs.reshape(-1), 1)
+        return offs
+
+
+def simulate_three_pass(x, g, K, split):
+    """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel."""
+    B = x.shape[0]
+    L = 1 << K
+    A, HB, R = split
+    xs = x.reshape(B, L)
+    ws = np.full(B * L, np.nan)
+    y = np.full(B * L, np.nan)
+    gf = g.reshape(L)
+    acc = {k: Access(B * L) for k in ("x", "ws_w1", "ws_r2", "ws_w2", "ws_r3", "y")}
+    acc_g = Access(L)
+    # outer forward: block = b * 2^HB + hi
+    for blk in range(B << HB):
+        b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        T = Tile(A, 0)
+        base = b * L + (hi << A)
+        v = xs.reshape(-1)[acc["x"].at(base + contig_map(T.idx(T.g.TOP)))].copy()
+        butterflies(v, 0, VB)
+        v = T.forward_groups(v, T.g.TOP)
+        wbase = b * L + (hi << R)
+        ws[acc["ws_w1"].at(wbase + run_map(T.idx(T.g.SL), HB, R))] = v
+    # middle: logical tile = run * B + b, XCD renumbering of blocks
+    M = HB + R
+    nblk = B << (A - R)
+    for blk in range(nblk):
+        logical = (blk & 7) * (nblk >> 3) + (blk >> 3) if nblk % 8 == 0 else blk
+        run, b = logical // B, logical % B
+        T = Tile(M, R)
+        base = b * (1 << (A + HB)) + (run << M)
+        v = ws[acc["ws_r2"].at(base + T.idx(T.g.TOP))].copy()
+        butterflies(v, T.g.JT, VB)
+        v = T.forward_groups(v, T.g.TOP)
+        goff = acc_g.at((run << R) + gain_map(T.idx(T.g.SL), A, R))
+        v = v * (gf[goff] * (1.0 / L))
+        if T.g.NBOT > 0:
+            v = T.inverse_groups(v)
+        butterflies(v, T.g.JT, VB)
+        ws[acc["ws_w2"].at(base + T.idx(T.g.TOP))] = v
+    # outer inverse
+    for blk in range(B << HB):
+        b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        T = Tile(A, 0)
+        wbase = b * L + (hi << R)
+        v = ws[acc["ws_r3"].at(wbase + run_map(T.idx(T.g.SL), HB, R))].copy()
+        v = T.inverse_groups(v)
+        butterflies(v, 0, VB)
+        y[acc["y"].at(b * L + (hi << A) + contig_map(T.idx(T.g.TOP)))] = v
+    for k, a in acc.items():
+        assert np.all(a.count == 1), f"{k}: elements not touched exactly once"
+    assert np.all(acc_g.count == B), "each gain element read once per slice"
+    return y.reshape(x.shape)
+
+
+def simulate_fused(x, g, K):
+    B = x.shape[0]
+    L = 1 << K
+    xs = x.reshape(B * L)
+    y = np.full(B * L, np.nan)
+    acc_x, acc_y, acc_g = Access(B * L), Access(B * L), Access(L)
+    for b in range(B):
+        T = Tile(K, 0)
+        v = xs[acc_x.at(b * L + T.idx(T.g.TOP))].copy()
+        butterflies(v, T.g.JT, VB)
+        v = T.forward_groups(v, T.g.TOP)
+        v = v * (g.reshape(L)[acc_g.at(T.idx(T.g.SL))] * (1.0 / L))
+        if T.g.NBOT > 0:
+            v = T.inverse_groups(v)
+        butterflies(v, T.g.JT, VB)
+        y[acc_y.at(b * L + T.idx(T.g.TOP))] = v
+    assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
+    assert np.all(acc_g.count == B)
+    return y.reshape(x.shape)
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle_mod.Oracle()
+
+
+@pytest.mark.parametrize("K", [11, 12, 13, 14, 15])
+def test_fused_schedule(K, orc):
+    rng = np.random.default_rng(K)
+    N, C = 1 << (K - K // 2), 1 << (K // 2)
+    x = rng.standard_normal((2, N, C))
+    g = rng.uniform(0.5, 1.5, (N, C))
+    y = simulate_fused(x, g, K)
+    ref = orc.whtmix(x, g)
+    assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("K", list(range(12, 19)))
+def test_three_pass_schedule(K, orc):
+    """Executed schedule for the forced (12..15) and automatic (16..18) splits;
+    B = 3 also exercises a middle grid that is not a multiple of 8."""
+    rng = np.random.default_rng(100 + K)
+    N, C = 1 << (K - 6), 64
+    for B in (3, 8):
+        x = rng.standard_normal((B, N, C))
+        g = rng.uniform(0.5, 1.5, (N, C))
+        y = simulate_three_pass(x, g, K, three_pass_split(K))
+        ref = orc.whtmix(x, g)
+        assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref)), (K, B)
+
+
+@pytest.mark.parametrize("K", list(range(12, 31)))
+def test_three_pass_maps_in_bounds(K):
+    """Index-only check for every split up to N*C = 2^30: one representative
+    block per kernel at the first, last and a middle block index, for B = 3."""
+    A, HB, R = three_pass_split(K)
+    L = 1 << K
+    B = 3
+    Mm = HB + R
+    assert 11 <= A <= 15 and 11 <= Mm <= 15 and 0 <= R <= A and HB >= 1
+    To = Tile(A, 0)
+    Tm = Tile(Mm, R)
+    # groups transform every tile bit in [WT, M) exactly once
+    for T in (To, Tm):
+        g = T.g
+        bits = list(range(g.TOP + g.JT, g.M))
+        for i in range(g.NBOT):
+            bits += list(range(g.S(i), g.S(i) + g.NB(i)))
+        assert sorted(bits) == list(range(g.WT, g.M)), (K, T.g.M)
+        if g.NBOT:
+            assert g.S(g.NBOT - 1) + VB <= g.M
+    # the outer passes' last layout keeps 32 consecutive lanes on consecutive
+    # elements (coalesced workspace runs)
+    assert To.g.SL == 5
+    for blk in (0, (B << HB) // 2, (B << HB) - 1):
+        b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        o = b * L + (hi << A) + To.idx(To.g.TOP)
+        assert o.min() >= 0 and o.max() < B * L
+        w = b * L + (hi << R) + run_map(To.idx(To.g.SL), HB, R)
+        assert w.min() >= 0 and w.max() < B * L
+        assert len(np.unique(w)) == w.size
+    nblk = B << (A - R)
+    for blk in (0, nblk // 2, nblk - 1):
+        logical = (blk & 7) * (nblk >> 3) + (blk >> 3) if nblk % 8 == 0 else blk
+        run, b = logical // B, logical % B
+        base = b * (1 << (A + HB)) + (run << Mm)
+        t = Tm.idx(Tm.g.TOP)
+        assert base + t.min() >= 0 and base + t.max() < B * L
+        goff = (run << R) + gain_map(Tm.idx(Tm.g.SL), A, R)
+        assert goff.min() >= 0 and goff.max() < L
+    assert pad((1 << 15) - 1) < 160 * 1024 // 4   # LDS fits in 160 KiB
+
+
+def test_middle_renumbering_is_a_permutation():
+    for nblk in (8, 16, 24, 4096, 3 * 8):
+        seen = sorted((blk & 7) * (nblk >> 3) + (blk >> 3) for blk in range(nblk))
+        assert seen == list(range(nblk))
