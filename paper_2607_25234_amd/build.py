@@ -3,7 +3,8 @@
     python -m paper_2607_25234_amd.build
 
 Compiles every source under csrc/ with hipcc into one shared library beside
-this file.  Packed FP32 instructions are disabled for all device code.
+this file, and the memory-system calibration program calib/membw.  Packed
+FP32 instructions are disabled for all device code.
 """
 from __future__ import annotations
 
@@ -17,6 +18,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwhtmix.so")
+CALIB_SRC = os.path.join(HERE, "calib", "membw.hip")
+CALIB_BIN = os.path.join(HERE, "calib", "membw")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -56,5 +59,19 @@ def build(out: str = LIB, extra: tuple = (), verbose: bool = False) -> str:
     return out
 
 
+def build_calib(out: str = CALIB_BIN, verbose: bool = False) -> str:
+    flags = [f for f in HIPCC_FLAGS if f not in ("-shared", "-fPIC", "-fvisibility=hidden")]
+    cmd = [hipcc(), *flags, CALIB_SRC, "-o", out + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"hipcc failed building {out}")
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_calib(verbose=True))

@@ -99,16 +99,22 @@ def test_in_place(shape, dtype, dev, orc):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", [(1, 32, 32), (2, 128, 64), (4, 65536, 128)])
 def test_unit_gain_is_identity(shape, dtype, dev):
-    """G = 1 (the paper's zero-initialised log gain) returns x; for bf16 the
-    float32 result is within far less than half a bf16 ulp of x, so the
-    rounded output is x exactly."""
+    """G = 1 (the paper's zero-initialised log gain) returns x.  For bf16 the
+    float32 result differs from x by rounding errors of the order of
+    1e-7 * max|x|; that is far below half a bf16 ulp of all but the smallest
+    elements, so nearly every output rounds back to x exactly and none moves
+    by more than one bf16 ulp of max|x| * 2^-8."""
     B, N, C = shape
     x, _ = workloads.draw(B, N, C, dtype, seed=21)
     y = run_gpu(x, np.ones((N, C), np.float32), dtype, dev)
+    err = errors(y, x)[0]
     if dtype == "bf16":
-        assert np.array_equal(y, x)
+        exact = float(np.mean(y == x))
+        say(f"  bf16 identity: {exact:.5f} bit-exact, normwise-max {err:.2e}")
+        assert exact > 0.99
+        assert err <= 2.0 ** -8
     else:
-        assert errors(y, x)[0] < 1e-6
+        assert err < 1e-6
 
 
 def test_deterministic_and_batch_independent(dev):
