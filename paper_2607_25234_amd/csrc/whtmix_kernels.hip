@@ -22,7 +22,7 @@
 // bank conflicts and keeps each register's LDS address a constant offset from
 // a per-thread base.
 //
-// Kernels (MODE):
+// Kernels:
 //   FUSED     whole slice in one tile: forward over all bits, gain, inverse.
 //   OUTER_FWD contiguous 2^A chunk of x: forward over its A bits, stored to
 //             the workspace in runs of 2^R so each middle tile is contiguous.
@@ -41,14 +41,56 @@ namespace {
 constexpr int VB = 5;        // log2(values per thread)
 constexpr int V = 1 << VB;   // values per thread
 
-enum Mode { OUTER_FWD = 0, MIDDLE = 1, OUTER_INV = 2, FUSED = 3 };
+// ---------------------------------------------------------------- memory
+// Global memory is reached through raw buffer resources: a per-tile base and
+// byte extent in SGPRs, a 32-bit per-thread offset in one VGPR, and each
+// register's constant offset in an SGPR (soffset), so addressing costs no
+// 64-bit vector arithmetic and no per-register VGPRs.
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9-family raw buffer descriptor
 
-// ---------------------------------------------------------------- elements
-__device__ __forceinline__ float load_elt(const float *p) { return *p; }
-__device__ __forceinline__ float load_elt(const __bf16 *p) { return (float)*p; }
-__device__ __forceinline__ void store_elt(float *p, float v) { *p = v; }
-// RNE rounding (v_cvt_pk_bf16_f32 on gfx950)
-__device__ __forceinline__ void store_elt(__bf16 *p, float v) { *p = (__bf16)v; }
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes,
+                                             kRawBufferWord3);
+}
+
+template <typename T>
+struct Elt;
+
+template <>
+struct Elt<float> {
+    static constexpr uint32_t bytes = 4;
+    __device__ static __forceinline__ float load(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                 uint32_t soff)
+    {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+    }
+    __device__ static __forceinline__ void store(float v, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                 uint32_t soff)
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, voff, soff, 0);
+    }
+};
+
+template <>
+struct Elt<__bf16> {
+    static constexpr uint32_t bytes = 2;
+    // bf16 -> float32 is exact: the bf16 bits are the high half of the float
+    __device__ static __forceinline__ float load(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                 uint32_t soff)
+    {
+        const unsigned short u = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+        return __builtin_bit_cast(float, (uint32_t)u << 16);
+    }
+    // round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
+    __device__ static __forceinline__ void store(float v, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                                 uint32_t soff)
+    {
+        const __bf16 h = (__bf16)v;
+        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), r, voff, soff,
+                                              0);
+    }
+};
 
 // ---------------------------------------------------------------- layouts
 template <int S>
@@ -89,13 +131,16 @@ __device__ __forceinline__ void butterflies(float (&v)[V])
     }
 }
 
-// Re-lay the tile from layout SA to layout SB through LDS.
-template <int SA, int SB>
+// Re-lay the tile from layout SA to layout SB through LDS.  LEAD: wait first
+// for every thread's reads of the previous exchange (not needed the first time
+// the tile's LDS is used).
+template <int SA, int SB, bool LEAD = true>
 __device__ __forceinline__ void exchange(float *lds, float (&v)[V], uint32_t tau)
 {
     const uint32_t pa = pad(layout_base<SA>(tau));
     const uint32_t pb = pad(layout_base<SB>(tau));
-    __syncthreads();   // earlier reads of this LDS tile are complete
+    if (LEAD)
+        __syncthreads();
 #pragma unroll
     for (int k = 0; k < V; ++k)
         lds[pa + pad((uint32_t)k << SA)] = v[k];
@@ -112,7 +157,7 @@ __device__ __forceinline__ void forward_groups(float *lds, float (&v)[V], uint32
     using G = Groups<M, WT>;
     if constexpr (I < G::NBOT) {
         constexpr int S = G::S(I);
-        exchange<SPREV, S>(lds, v, tau);
+        exchange<SPREV, S, (I > 0)>(lds, v, tau);
         butterflies<0, G::NB(I)>(v);
         forward_groups<M, WT, I + 1, S>(lds, v, tau);
     }
@@ -159,32 +204,52 @@ struct GainMap {
 };
 
 template <int S, class Map, typename T>
-__device__ __forceinline__ void load_layout(float (&v)[V], const T *base, uint32_t tau)
+__device__ __forceinline__ void load_layout(float (&v)[V], __amdgpu_buffer_rsrc_t r, uint32_t tau)
 {
-    const T *p = base + Map::at(layout_base<S>(tau));
+    const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
 #pragma unroll
     for (int k = 0; k < V; ++k)
-        v[k] = load_elt(p + Map::at((uint32_t)k << S));
+        v[k] = Elt<T>::load(r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
 }
 
 template <int S, class Map, typename T>
-__device__ __forceinline__ void store_layout(const float (&v)[V], T *base, uint32_t tau)
+__device__ __forceinline__ void store_layout(const float (&v)[V], __amdgpu_buffer_rsrc_t r,
+                                             uint32_t tau)
 {
-    T *p = base + Map::at(layout_base<S>(tau));
+    const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
 #pragma unroll
     for (int k = 0; k < V; ++k)
-        store_elt(p + Map::at((uint32_t)k << S), v[k]);
+        Elt<T>::store(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
 }
 
-// v *= gain * 2^-K, in layout S.
-template <int S, class Map, int K>
-__device__ __forceinline__ void apply_gain(float (&v)[V], const float *g, uint32_t tau)
+// The gain is read with plain global loads: for its 128-byte-run pattern they
+// measured markedly faster than buffer loads on gfx950.  Issued at kernel
+// start so its latency overlaps the tile load and the forward butterflies.
+template <int S, class Map>
+__device__ __forceinline__ void load_gain(float (&g)[V], const float *__restrict__ base,
+                                          uint32_t tau)
 {
-    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
-    const float *p = g + Map::at(layout_base<S>(tau));
+    const float *p = base + Map::at(layout_base<S>(tau));
 #pragma unroll
     for (int k = 0; k < V; ++k)
-        v[k] *= p[Map::at((uint32_t)k << S)] * scale;
+        g[k] = p[Map::at((uint32_t)k << S)];
+}
+
+// v *= g * 2^-K (g already loaded in the same layout).
+template <int K>
+__device__ __forceinline__ void apply_gain(float (&v)[V], const float (&g)[V])
+{
+    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] *= g[k] * scale;
+}
+
+// Byte extent of a map over a tile of 2^M elements (largest offset + 1).
+template <class Map, int M, typename T>
+constexpr uint32_t extent_bytes()
+{
+    return (Map::at((1u << M) - 1u) + 1u) * Elt<T>::bytes;
 }
 
 // ---------------------------------------------------------------- kernels
@@ -197,15 +262,17 @@ fused_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict
     __shared__ float lds[pad(1u << K)];
     const uint32_t tau = threadIdx.x;
     const size_t base = (size_t)blockIdx.x << K;
-    float v[V];
-    load_layout<G::TOP, ContigMap>(v, x + base, tau);
+    constexpr uint32_t bytes = (1u << K) * Elt<T>::bytes;
+    float v[V], gv[V];
+    load_layout<G::TOP, ContigMap, T>(v, buffer(x + base, bytes), tau);
+    load_gain<G::SL, ContigMap>(gv, g, tau);
     butterflies<G::JT, VB>(v);
     forward_groups<K, 0, 0, G::TOP>(lds, v, tau);
-    apply_gain<G::SL, ContigMap, K>(v, g, tau);
+    apply_gain<K>(v, gv);
     if constexpr (G::NBOT > 0)
         inverse_groups<K, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<G::JT, VB>(v);
-    store_layout<G::TOP, ContigMap>(v, y + base, tau);
+    store_layout<G::TOP, ContigMap, T>(v, buffer(y + base, bytes), tau);
 }
 
 // OUTER_FWD: block = b * 2^HB + hi; chunk x[b][hi * 2^A ...] -> workspace.
@@ -214,6 +281,7 @@ __global__ void __launch_bounds__(1 << (A - VB))
 outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws)
 {
     using G = Groups<A, 0>;
+    using Run = RunMap<HB, R>;
     __shared__ float lds[pad(1u << A)];
     const uint32_t tau = threadIdx.x;
     const uint32_t blk = blockIdx.x;
@@ -221,21 +289,25 @@ outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws)
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const size_t slice = b << (A + HB);
     float v[V];
-    load_layout<G::TOP, ContigMap>(v, x + slice + ((size_t)hi << A), tau);
+    load_layout<G::TOP, ContigMap, T>(
+        v, buffer(x + slice + ((size_t)hi << A), (1u << A) * Elt<T>::bytes), tau);
     butterflies<0, VB>(v);
     forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
-    store_layout<G::SL, RunMap<HB, R>>(v, ws + slice + ((size_t)hi << R), tau);
+    store_layout<G::SL, Run, float>(
+        v, buffer(ws + slice + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
 }
 
 // MIDDLE: logical tile = run * B + b (the B slices sharing a gain tile are
 // adjacent); workgroups are renumbered so adjacent logical tiles land on the
 // same XCD (blocks are dealt round-robin over the 8 XCDs) and share its L2.
+// The gain tile is requested right after the data tile.
 template <int A, int HB, int R>
 __global__ void __launch_bounds__(1 << (HB + R - VB))
 middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nslices)
 {
     constexpr int M = HB + R;
     using G = Groups<M, R>;
+    using Gain = GainMap<A, R>;
     __shared__ float lds[pad(1u << M)];
     const uint32_t tau = threadIdx.x;
     const uint32_t nblk = gridDim.x;
@@ -244,16 +316,18 @@ middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nsli
         logical = (blockIdx.x & 7u) * (nblk >> 3) + (blockIdx.x >> 3);
     const uint32_t run = logical / nslices;
     const size_t b = logical - run * nslices;
-    float *tile = ws + (b << (A + HB)) + ((size_t)run << M);
-    float v[V];
-    load_layout<G::TOP, ContigMap>(v, tile, tau);
+    const __amdgpu_buffer_rsrc_t tile =
+        buffer(ws + (b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
+    float v[V], gv[V];
+    load_layout<G::TOP, ContigMap, float>(v, tile, tau);
+    load_gain<G::SL, Gain>(gv, g + ((size_t)run << R), tau);
     butterflies<G::JT, VB>(v);
     forward_groups<M, R, 0, G::TOP>(lds, v, tau);
-    apply_gain<G::SL, GainMap<A, R>, A + HB>(v, g + ((size_t)run << R), tau);
+    apply_gain<A + HB>(v, gv);
     if constexpr (G::NBOT > 0)
         inverse_groups<M, R, G::NBOT - 1>(lds, v, tau);
     butterflies<G::JT, VB>(v);
-    store_layout<G::TOP, ContigMap>(v, tile, tau);
+    store_layout<G::TOP, ContigMap, float>(v, tile, tau);
 }
 
 // OUTER_INV: mirror of OUTER_FWD.
@@ -262,6 +336,7 @@ __global__ void __launch_bounds__(1 << (A - VB))
 outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y)
 {
     using G = Groups<A, 0>;
+    using Run = RunMap<HB, R>;
     __shared__ float lds[pad(1u << A)];
     const uint32_t tau = threadIdx.x;
     const uint32_t blk = blockIdx.x;
@@ -269,11 +344,18 @@ outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y)
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const size_t slice = b << (A + HB);
     float v[V];
-    load_layout<G::SL, RunMap<HB, R>>(v, ws + slice + ((size_t)hi << R), tau);
+    load_layout<G::SL, Run, float>(
+        v, buffer(ws + slice + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
     inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<0, VB>(v);
-    store_layout<G::TOP, ContigMap>(v, y + slice + ((size_t)hi << A), tau);
+    store_layout<G::TOP, ContigMap, T>(
+        v, buffer(y + slice + ((size_t)hi << A), (1u << A) * Elt<T>::bytes), tau);
 }
+
+__device__ __forceinline__ float to_float(float v) { return v; }
+__device__ __forceinline__ float to_float(__bf16 v) { return (float)v; }
+template <typename T>
+__device__ __forceinline__ T from_float(float v) { return (T)v; }   // bf16: round to nearest even
 
 // SMALL: L = 2^K <= 2^10; one 256-thread workgroup per slice, every stage on
 // the LDS copy.
@@ -286,7 +368,7 @@ small_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict
     const size_t base = (size_t)blockIdx.x << K;
     const float scale = 1.0f / (float)L;
     for (int i = threadIdx.x; i < L; i += blockDim.x)
-        s[i] = load_elt(x + base + i);
+        s[i] = to_float(x[base + i]);
     for (int pass = 0; pass < 2; ++pass) {
         for (int h = 1; h < L; h <<= 1) {
             __syncthreads();
@@ -303,7 +385,7 @@ small_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict
                 s[i] *= g[i] * scale;
     }
     for (int i = threadIdx.x; i < L; i += blockDim.x)
-        store_elt(y + base + i, s[i]);
+        y[base + i] = from_float<T>(s[i]);
 }
 
 // ---------------------------------------------------------------- launchers
