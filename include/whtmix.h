@@ -11,12 +11,18 @@
  *   H_n         the orthonormal Sylvester-ordered Walsh-Hadamard matrix,
  *               entry (i, j) = (-1)^popcount(i & j) / sqrt(n), n = 2^k;
  *               H_n is symmetric and orthogonal, so H_n^{-1} = H_n;
- *   G           N x C float32 per-frequency gain shared by every slice b
+ *   G           N_pad x C float32 per-frequency gain shared by every slice b
  *               ("o" is the element-wise product).
  *
+ * C must be a power of two.  N may be any count >= 1: as the paper does, the
+ * token axis is zero-padded to N_pad = 2^ceil(log2 N) before H_N (the padded
+ * rows of X are zeros), the mixer runs on the N_pad x C slice, and Y keeps its
+ * first N rows.  For a power-of-two N, N_pad = N.
+ *
  * The paper's own gains are log-domain vectors g_c (length C) and g_t
- * (length N) applied by eq. (2) then eq. (3); that is this operation with
- * G[n][c] = exp(g_t[n]) * exp(g_c[c]).  Exponentiating is the caller's job.
+ * (length N_pad) applied by eq. (2) then eq. (3); that is this operation with
+ * G[n][c] = exp(g_t[n]) * exp(g_c[c]), and whtmix_forward_separable() computes
+ * it from the log gains directly.
  *
  * All computation runs in hand-written HIP kernels on the GPU.  Arithmetic is
  * float32 (bf16 inputs are widened exactly, bf16 outputs are rounded to
@@ -55,19 +61,19 @@ typedef enum whtmix_dtype {
  * a rejected call enqueues nothing and writes nothing. */
 typedef enum whtmix_status {
     WHTMIX_SUCCESS = 0,
-    WHTMIX_ERROR_INVALID_VALUE = 1,    /* null pointer, B < 0, partial x/y
-                                          overlap, gain overlapping y,
+    WHTMIX_ERROR_INVALID_VALUE = 1,    /* null pointer, B < 0, N < 1, partial
+                                          x/y overlap, a gain overlapping y,
                                           bad option values */
-    WHTMIX_ERROR_NOT_POWER_OF_TWO = 2, /* N or C not a power of two >= 1 */
+    WHTMIX_ERROR_NOT_POWER_OF_TWO = 2, /* C not a power of two >= 1 */
     WHTMIX_ERROR_UNSUPPORTED_DTYPE = 3,
     WHTMIX_ERROR_MISALIGNED = 4,       /* x, y or gain not 16-byte aligned */
     WHTMIX_ERROR_OUT_OF_MEMORY = 5,    /* workspace allocation failed */
     WHTMIX_ERROR_HIP = 6,              /* HIP runtime / launch error; text in
                                           whtmix_last_error() */
-    WHTMIX_ERROR_TOO_LARGE = 7         /* N*C > 2^30 or sizes overflow */
+    WHTMIX_ERROR_TOO_LARGE = 7         /* N_pad*C > 2^30 or sizes overflow */
 } whtmix_status;
 
-/* Execution plans.  AUTO picks by the slice size L = N*C:
+/* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
  *   L <= 2^10          one small workgroup per slice, all stages in LDS;
  *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass;
  *   L >= 2^16          THREE_PASS: forward over the low bits of the flat
@@ -100,20 +106,22 @@ typedef struct whtmix_plan_info {
     int run_bits;         /* THREE_PASS: log2 of the contiguous run carried
                              by the middle pass */
     int64_t workspace_bytes; /* float32 workspace this call needs */
+    int64_t padded_tokens;   /* N_pad */
 } whtmix_plan_info;
 
 /*
- * whtmix_forward -- y[b] = H_N (G o (H_N x[b] H_C)) H_C for b in [0, B).
+ * whtmix_forward -- y[b] = H_N (G o (H_N x[b] H_C)) H_C for b in [0, B)
+ * (section III-B, eqs. (2)-(3), joint gain).
  *
  *   x      device pointer, [B][N][C] contiguous elements of `dtype`
  *          (read only).  May equal y exactly (in place); any other overlap
  *          with y is rejected.
- *   gain   device pointer, [N][C] contiguous float32, shared by all b; must
- *          not overlap y.
+ *   gain   device pointer, [N_pad][C] contiguous float32 (linear gains),
+ *          shared by all b; must not overlap y.
  *   y      device pointer, [B][N][C] contiguous elements of `dtype` (written).
  *   B      number of independent slices; B == 0 is a no-op (pointers are not
  *          inspected).
- *   N, C   tokens and channels; each a power of two >= 1, N*C <= 2^30.
+ *   N, C   tokens (>= 1) and channels (a power of two >= 1), N_pad*C <= 2^30.
  *   dtype  whtmix_dtype of x and y.
  *   stream hipStream_t to enqueue on (NULL = the null stream).
  *
@@ -128,6 +136,25 @@ WHTMIX_API int whtmix_forward(const void *x, const float *gain, void *y,
 WHTMIX_API int whtmix_forward_ex(const void *x, const float *gain, void *y,
                       int64_t B, int64_t N, int64_t C, int dtype, void *stream,
                       const whtmix_options *options);
+
+/*
+ * whtmix_forward_separable -- the paper's parametrisation, eq. (2) then
+ * eq. (3):  Z <- H_C^{-1}(exp(g_c) o H_C Z) along channels, then
+ *           Z <- H_N^{-1}(exp(g_t) o H_N Z) along tokens,
+ * i.e. whtmix_forward with G[n][c] = exp(g_t[n]) * exp(g_c[c]).  The gain of
+ * each frequency is formed on the device as exp(g_t[n] + g_c[c]), so the
+ * only gain traffic is the two small vectors.
+ *
+ *   log_gain_tokens    device pointer, [N_pad] float32 log gains g_t
+ *   log_gain_channels  device pointer, [C] float32 log gains g_c
+ * Both are 16-byte aligned and must not overlap y (zero log gains, the
+ * paper's initialisation, give Y = X).  Other arguments, options and return
+ * codes as whtmix_forward_ex (options may be NULL).
+ */
+WHTMIX_API int whtmix_forward_separable(const void *x, const float *log_gain_tokens,
+                             const float *log_gain_channels, void *y,
+                             int64_t B, int64_t N, int64_t C, int dtype,
+                             void *stream, const whtmix_options *options);
 
 /* Fills *info with the plan whtmix_forward_ex would use.  Validates the
  * shape, dtype and options exactly as the forward call does (pointers are

@@ -56,6 +56,14 @@ def load(path: str = LIB):
     return lib
 
 
+def padded(n: int) -> int:
+    """P: the token count rounded up to a power of two (zero padding)."""
+    p = 1
+    while p < n:
+        p *= 2
+    return p
+
+
 def _dptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
 
@@ -73,15 +81,16 @@ class Oracle:
     def whtmix(self, x, g) -> np.ndarray:
         """Y[b] = H_N (G o (H_N X[b] H_C)) H_C in float64.
 
-        x: [B, N, C] or [N, C]; g: [N, C].  Returns float64 of x's shape."""
+        x: [B, N, C] or [N, C]; g: [P, C] with P = N rounded up to a power of
+        two (the token axis is zero-padded).  Returns float64 of x's shape."""
         x64 = _as_f64(x)
         squeeze = x64.ndim == 2
         if squeeze:
             x64 = x64[None]
         B, N, C = x64.shape
         g64 = _as_f64(g)
-        if g64.shape != (N, C):
-            raise ValueError(f"gain shape {g64.shape} != {(N, C)}")
+        if g64.shape != (padded(N), C):
+            raise ValueError(f"gain shape {g64.shape} != {(padded(N), C)}")
         y = np.empty_like(x64)
         rc = self.lib.oracle_whtmix(_dptr(x64), _dptr(g64), _dptr(y), B, N, C)
         if rc != 0:
@@ -89,7 +98,7 @@ class Oracle:
         return y[0] if squeeze else y
 
     def whtmix_separable(self, x, g_t, g_c) -> np.ndarray:
-        """The paper's eq. (2) then eq. (3) with log-domain gains g_t[N], g_c[C]."""
+        """The paper's eq. (2) then eq. (3) with log-domain gains g_t[P], g_c[C]."""
         x64 = _as_f64(x)
         squeeze = x64.ndim == 2
         if squeeze:
@@ -97,8 +106,8 @@ class Oracle:
         B, N, C = x64.shape
         gt = _as_f64(g_t).reshape(-1)
         gc = _as_f64(g_c).reshape(-1)
-        if gt.shape != (N,) or gc.shape != (C,):
-            raise ValueError("g_t must have N entries and g_c C entries")
+        if gt.shape != (padded(N),) or gc.shape != (C,):
+            raise ValueError("g_t must have P entries and g_c C entries")
         y = np.empty_like(x64)
         rc = self.lib.oracle_whtmix_separable(_dptr(x64), _dptr(gt), _dptr(gc),
                                               _dptr(y), B, N, C)

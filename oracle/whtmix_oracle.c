@@ -27,7 +27,12 @@
  * oracle_whtmix_separable(); it equals the joint form with
  * G[n][c] = exp(g_t[n]) * exp(g_c[c]) (rank one).
  *
- * Layout: x, y are [B][N][C] row-major (C fastest), g is [N][C] row-major.
+ * Token padding: C must be a power of two; N may be any count >= 1.  As in
+ * section III-B, the token axis is zero-padded to P = 2^ceil(log2 N) rows
+ * before the transforms; the mixer runs on the P x C slice and the first N
+ * rows are kept.  The gains then cover P token frequencies.
+ *
+ * Layout: x, y are [B][N][C] row-major (C fastest), g is [P][C] row-major.
  * Every per-vector operation runs in a fixed order, so the output is bitwise
  * independent of the OpenMP thread count.
  */
@@ -82,61 +87,83 @@ static void token_transform(double *z, long N, long C)
 
 static int is_pow2(long n) { return n >= 1 && (n & (n - 1)) == 0; }
 
-/* Joint-gain mixer, Y[b] = H_N (G o (H_N X[b] H_C)) H_C.
- * Returns 0 on success, -1 on a bad argument (null pointer, B < 0, N or C not
- * a power of two). */
+/* Smallest power of two >= n: the padded token count. */
+static long padded(long n)
+{
+    long p = 1;
+    while (p < n)
+        p *= 2;
+    return p;
+}
+
+/* z <- x[b] followed by P - N zero rows (the zero-padded token axis). */
+static void load_padded(double *z, const double *xb, long N, long P, long C)
+{
+    memcpy(z, xb, (size_t)(N * C) * sizeof(double));
+    memset(z + N * C, 0, (size_t)((P - N) * C) * sizeof(double));
+}
+
+/* Joint-gain mixer, Y[b] = first N rows of H_P (G o (H_P Xpad[b] H_C)) H_C.
+ * g is [P][C].  Returns 0 on success, -1 on a bad argument (null pointer,
+ * B < 0, N < 1, C not a power of two, allocation failure). */
 int oracle_whtmix(const double *x, const double *g, double *y,
                   long B, long N, long C)
 {
-    if (!x || !g || !y || B < 0 || !is_pow2(N) || !is_pow2(C))
+    if (!x || !g || !y || B < 0 || N < 1 || !is_pow2(C))
         return -1;
-    const long L = N * C;
+    const long P = padded(N);
+    double *z = malloc((size_t)(P * C) * sizeof(double));
+    if (!z)
+        return -1;
     for (long b = 0; b < B; ++b) {
-        double *z = y + b * L;
-        if (z != x + b * L)
-            memcpy(z, x + b * L, (size_t)L * sizeof(double));
-        /* forward: T = H_N X H_C */
-        channel_transform(z, N, C);
-        token_transform(z, N, C);
+        load_padded(z, x + b * N * C, N, P, C);
+        /* forward: T = H_P Z H_C */
+        channel_transform(z, P, C);
+        token_transform(z, P, C);
         /* per-frequency gain */
-        for (long i = 0; i < L; ++i)
+        for (long i = 0; i < P * C; ++i)
             z[i] *= g[i];
-        /* inverse (H^{-1} = H): Y = H_N T H_C */
-        token_transform(z, N, C);
-        channel_transform(z, N, C);
+        /* inverse (H^{-1} = H): Y = H_P T H_C */
+        token_transform(z, P, C);
+        channel_transform(z, P, C);
+        memcpy(y + b * N * C, z, (size_t)(N * C) * sizeof(double));
     }
+    free(z);
     return 0;
 }
 
 /* The paper's literal parametrisation, eq. (2) then eq. (3):
  *   Z <- H_C^{-1}( exp(g_c) o H_C(Z) )   along channels, per token row,
- *   Z <- H_N^{-1}( exp(g_t) o H_N(Z) )   along tokens, per channel column,
- * with g_c (length C) and g_t (length N) log-domain gains.  Same return
+ *   Z <- H_P^{-1}( exp(g_t) o H_P(Z) )   along tokens, per channel column,
+ * with g_c (length C) and g_t (length P) log-domain gains.  Same return
  * convention as oracle_whtmix(). */
 int oracle_whtmix_separable(const double *x, const double *g_t,
                             const double *g_c, double *y,
                             long B, long N, long C)
 {
-    if (!x || !g_t || !g_c || !y || B < 0 || !is_pow2(N) || !is_pow2(C))
+    if (!x || !g_t || !g_c || !y || B < 0 || N < 1 || !is_pow2(C))
         return -1;
-    const long L = N * C;
+    const long P = padded(N);
+    double *z = malloc((size_t)(P * C) * sizeof(double));
+    if (!z)
+        return -1;
     for (long b = 0; b < B; ++b) {
-        double *z = y + b * L;
-        if (z != x + b * L)
-            memcpy(z, x + b * L, (size_t)L * sizeof(double));
+        load_padded(z, x + b * N * C, N, P, C);
         /* eq. (2): channel mixing */
-        channel_transform(z, N, C);
-        for (long n = 0; n < N; ++n)
+        channel_transform(z, P, C);
+        for (long n = 0; n < P; ++n)
             for (long c = 0; c < C; ++c)
                 z[n * C + c] *= exp(g_c[c]);
-        channel_transform(z, N, C);
+        channel_transform(z, P, C);
         /* eq. (3): token mixing */
-        token_transform(z, N, C);
-        for (long n = 0; n < N; ++n)
+        token_transform(z, P, C);
+        for (long n = 0; n < P; ++n)
             for (long c = 0; c < C; ++c)
                 z[n * C + c] *= exp(g_t[n]);
-        token_transform(z, N, C);
+        token_transform(z, P, C);
+        memcpy(y + b * N * C, z, (size_t)(N * C) * sizeof(double));
     }
+    free(z);
     return 0;
 }
 

@@ -45,6 +45,7 @@ bool overlaps(uintptr_t a, uint64_t na, uintptr_t b, uint64_t nb)
 
 struct Checked {
     int K = 0;
+    int64_t n_pad = 0;
     int plan = whtmix::PLAN_AUTO;
     int kernels = 0;
     whtmix::Split split{0, 0, 0};
@@ -58,11 +59,15 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
 {
     if (dtype != WHTMIX_DTYPE_F32 && dtype != WHTMIX_DTYPE_BF16)
         return WHTMIX_ERROR_UNSUPPORTED_DTYPE;
-    if (B < 0)
+    if (B < 0 || N < 1)
         return WHTMIX_ERROR_INVALID_VALUE;
-    if (!is_pow2(N) || !is_pow2(C))
+    if (!is_pow2(C))
         return WHTMIX_ERROR_NOT_POWER_OF_TWO;
-    const int K = log2_exact(N) + log2_exact(C);
+    if (N > (int64_t(1) << whtmix::kMaxLog2Slice))
+        return WHTMIX_ERROR_TOO_LARGE;
+    // The token axis is zero-padded to the next power of two (section III-B).
+    const int nbits = log2_exact(N);
+    const int K = nbits + log2_exact(C);
     if (K > whtmix::kMaxLog2Slice)
         return WHTMIX_ERROR_TOO_LARGE;
     const int64_t L = int64_t(1) << K;
@@ -92,6 +97,7 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         return WHTMIX_ERROR_INVALID_VALUE;
     }
     out->K = K;
+    out->n_pad = int64_t(1) << nbits;
     out->plan = plan;
     out->elt = dtype == WHTMIX_DTYPE_BF16 ? 2 : 4;
     out->kernels = plan == whtmix::PLAN_THREE_PASS ? 3 : 1;
@@ -159,32 +165,50 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->outer_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.A : 0;
     info->run_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.R : 0;
     info->workspace_bytes = c.ws_bytes;
+    info->padded_tokens = c.n_pad;
     return WHTMIX_SUCCESS;
 }
 
-int whtmix_forward_ex(const void *x, const float *gain, void *y, int64_t B, int64_t N,
-                      int64_t C, int dtype, void *stream, const whtmix_options *options)
+}  // extern "C"
+
+namespace {
+
+int forward_impl(const void *x, int gain_kind, const float *gain, const float *gain_t,
+                 const float *gain_c, void *y, int64_t B, int64_t N, int64_t C, int dtype,
+                 void *stream, const whtmix_options *options)
 {
     Checked c;
     int st = check_shape(B, N, C, dtype, options, &c);
     if (st != WHTMIX_SUCCESS) return st;
     if (B == 0) return WHTMIX_SUCCESS;
-    if (!x || !gain || !y) return WHTMIX_ERROR_INVALID_VALUE;
+    const bool full = gain_kind == whtmix::GAIN_FULL;
+    if (!x || !y || (full ? !gain : (!gain_t || !gain_c))) return WHTMIX_ERROR_INVALID_VALUE;
     const uintptr_t px = reinterpret_cast<uintptr_t>(x);
     const uintptr_t py = reinterpret_cast<uintptr_t>(y);
-    const uintptr_t pg = reinterpret_cast<uintptr_t>(gain);
-    if ((px | py | pg) & 15u) return WHTMIX_ERROR_MISALIGNED;
-    const uint64_t L = uint64_t(1) << c.K;
-    const uint64_t xy_bytes = (uint64_t)B * L * (uint64_t)c.elt;
+    const uintptr_t pg = reinterpret_cast<uintptr_t>(full ? gain : gain_t);
+    const uintptr_t pc = reinterpret_cast<uintptr_t>(full ? gain : gain_c);
+    if ((px | py | pg | pc) & 15u) return WHTMIX_ERROR_MISALIGNED;
+    const uint64_t xy_bytes = (uint64_t)B * (uint64_t)N * (uint64_t)C * (uint64_t)c.elt;
     if (px != py && overlaps(px, xy_bytes, py, xy_bytes)) return WHTMIX_ERROR_INVALID_VALUE;
-    if (overlaps(pg, L * 4, py, xy_bytes)) return WHTMIX_ERROR_INVALID_VALUE;
+    if (full) {
+        if (overlaps(pg, (uint64_t)c.n_pad * C * 4, py, xy_bytes))
+            return WHTMIX_ERROR_INVALID_VALUE;
+    } else if (overlaps(pg, (uint64_t)c.n_pad * 4, py, xy_bytes) ||
+               overlaps(pc, (uint64_t)C * 4, py, xy_bytes)) {
+        return WHTMIX_ERROR_INVALID_VALUE;
+    }
 
     whtmix::LaunchArgs a{};
     a.x = x;
-    a.gain = gain;
     a.y = y;
+    a.gain_kind = gain_kind;
+    a.gain = gain;
+    a.gain_t = gain_t;
+    a.gain_c = gain_c;
+    a.cbits = log2_exact(C);
     a.B = B;
     a.K = c.K;
+    a.nvalid = (uint32_t)(N * C);
     a.dtype = dtype;
     a.plan = c.plan;
     a.stream = static_cast<hipStream_t>(stream);
@@ -204,6 +228,25 @@ int whtmix_forward_ex(const void *x, const float *gain, void *y, int64_t B, int6
     return WHTMIX_SUCCESS;
 }
 
+}  // namespace
+
+extern "C" {
+
+int whtmix_forward_ex(const void *x, const float *gain, void *y, int64_t B, int64_t N,
+                      int64_t C, int dtype, void *stream, const whtmix_options *options)
+{
+    return forward_impl(x, whtmix::GAIN_FULL, gain, nullptr, nullptr, y, B, N, C, dtype, stream,
+                        options);
+}
+
+int whtmix_forward_separable(const void *x, const float *log_gain_tokens,
+                             const float *log_gain_channels, void *y, int64_t B, int64_t N,
+                             int64_t C, int dtype, void *stream, const whtmix_options *options)
+{
+    return forward_impl(x, whtmix::GAIN_LOG_SEPARABLE, nullptr, log_gain_tokens,
+                        log_gain_channels, y, B, N, C, dtype, stream, options);
+}
+
 int whtmix_forward(const void *x, const float *gain, void *y, int64_t B, int64_t N, int64_t C,
                    int dtype, void *stream)
 {
@@ -215,12 +258,13 @@ const char *whtmix_status_string(int status)
     switch (status) {
     case WHTMIX_SUCCESS: return "success";
     case WHTMIX_ERROR_INVALID_VALUE: return "invalid value";
-    case WHTMIX_ERROR_NOT_POWER_OF_TWO: return "N and C must be powers of two >= 1";
+    case WHTMIX_ERROR_NOT_POWER_OF_TWO: return "C must be a power of two >= 1";
     case WHTMIX_ERROR_UNSUPPORTED_DTYPE: return "unsupported dtype";
     case WHTMIX_ERROR_MISALIGNED: return "x, y and gain must be 16-byte aligned";
     case WHTMIX_ERROR_OUT_OF_MEMORY: return "workspace allocation failed";
     case WHTMIX_ERROR_HIP: return "HIP runtime error";
-    case WHTMIX_ERROR_TOO_LARGE: return "shape too large (N*C <= 2^30, B*N*C <= 2^37)";
+    case WHTMIX_ERROR_TOO_LARGE:
+        return "shape too large (N_pad*C <= 2^30, B*N_pad*C <= 2^37)";
     default: return "unknown status";
     }
 }
@@ -248,6 +292,6 @@ int whtmix_release_workspaces(void)
     return st;
 }
 
-int whtmix_version(void) { return 100; }
+int whtmix_version(void) { return 10100; }
 
 }  // extern "C"

@@ -222,20 +222,108 @@ __device__ __forceinline__ void store_layout(const float (&v)[V], __amdgpu_buffe
         Elt<T>::store(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
 }
 
-// The gain is read with plain global loads: for its 128-byte-run pattern they
-// measured markedly faster than buffer loads on gfx950.  Issued at kernel
-// start so its latency overlaps the tile load and the forward butterflies.
-template <int S, class Map>
-__device__ __forceinline__ void load_gain(float (&g)[V], const float *__restrict__ base,
-                                          uint32_t tau)
+// Masked forms for the one tile of a zero-padded slice that straddles the
+// last real token: elements with tile index >= valid read as 0 and are not
+// stored.  Tiles wholly inside the slice take the unmasked forms; tiles wholly
+// in the padding skip their loads.  (The choice is uniform per workgroup.)
+template <int S, class Map, typename T>
+__device__ __forceinline__ void load_layout_masked(float (&v)[V], __amdgpu_buffer_rsrc_t r,
+                                                   uint32_t tau, uint32_t valid)
 {
-    const float *p = base + Map::at(layout_base<S>(tau));
+    const uint32_t tb = layout_base<S>(tau);
+    const uint32_t voff = Map::at(tb) * Elt<T>::bytes;
 #pragma unroll
-    for (int k = 0; k < V; ++k)
-        g[k] = p[Map::at((uint32_t)k << S)];
+    for (int k = 0; k < V; ++k) {
+        const uint32_t t = tb | ((uint32_t)k << S);
+        v[k] = t < valid ? Elt<T>::load(r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes)
+                         : 0.0f;
+    }
 }
 
-// v *= g * 2^-K (g already loaded in the same layout).
+template <int S, class Map, typename T>
+__device__ __forceinline__ void store_layout_masked(const float (&v)[V],
+                                                    __amdgpu_buffer_rsrc_t r, uint32_t tau,
+                                                    uint32_t valid)
+{
+    const uint32_t tb = layout_base<S>(tau);
+    const uint32_t voff = Map::at(tb) * Elt<T>::bytes;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        const uint32_t t = tb | ((uint32_t)k << S);
+        if (t < valid)
+            Elt<T>::store(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
+    }
+}
+
+// A contiguous tile of 2^M elements of x (type T) with `valid` real elements.
+template <int S, int M, typename T>
+__device__ __forceinline__ void load_tile(float (&v)[V], const T *base, uint32_t valid,
+                                          uint32_t tau)
+{
+    if (valid >= (1u << M)) {
+        load_layout<S, ContigMap, T>(v, buffer(base, (1u << M) * Elt<T>::bytes), tau);
+    } else if (valid == 0) {
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            v[k] = 0.0f;
+    } else {
+        load_layout_masked<S, ContigMap, T>(v, buffer(base, valid * Elt<T>::bytes), tau, valid);
+    }
+}
+
+template <int S, int M, typename T>
+__device__ __forceinline__ void store_tile(const float (&v)[V], T *base, uint32_t valid,
+                                           uint32_t tau)
+{
+    if (valid >= (1u << M))
+        store_layout<S, ContigMap, T>(v, buffer(base, (1u << M) * Elt<T>::bytes), tau);
+    else if (valid > 0)
+        store_layout_masked<S, ContigMap, T>(v, buffer(base, valid * Elt<T>::bytes), tau, valid);
+}
+
+// ---------------------------------------------------------------- gains
+// f is the flat index n*C + c of the (padded) slice.  The gain is read with
+// plain global loads: for its 128-byte-run pattern they measured markedly
+// faster than buffer loads on gfx950.  It is requested right after the data
+// tile so its latency overlaps the forward butterflies.
+
+// Joint per-frequency gain G[N_pad][C] (linear).
+struct FullGain {
+    const float *g;
+    template <int S, class Map>
+    __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
+    {
+        const float *p = g + f0 + Map::at(layout_base<S>(tau));
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            gv[k] = p[Map::at((uint32_t)k << S)];
+    }
+    __device__ __forceinline__ float at(uint32_t f) const { return g[f]; }
+};
+
+// The paper's parametrisation (eqs. (2)-(3)): log-domain gains g_t[N_pad]
+// over token frequencies and g_c[C] over channel frequencies; the gain of
+// frequency (n, c) is exp(g_t[n]) * exp(g_c[c]), computed as one exp of the
+// sum.
+struct LogSeparableGain {
+    const float *gt;
+    const float *gc;
+    uint32_t cbits;   // log2(C)
+    __device__ __forceinline__ float at(uint32_t f) const
+    {
+        return expf(gt[f >> cbits] + gc[f & ((1u << cbits) - 1u)]);
+    }
+    template <int S, class Map>
+    __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
+    {
+        const uint32_t fb = f0 + Map::at(layout_base<S>(tau));
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            gv[k] = at(fb + Map::at((uint32_t)k << S));
+    }
+};
+
+// v *= gain * 2^-K (gain already gathered in the same layout).
 template <int K>
 __device__ __forceinline__ void apply_gain(float (&v)[V], const float (&g)[V])
 {
@@ -253,32 +341,42 @@ constexpr uint32_t extent_bytes()
 }
 
 // ---------------------------------------------------------------- kernels
+// x and y hold `nvalid` = N*C elements per slice (N real tokens); the
+// transform runs over the zero-padded slice of 2^K = N_pad*C elements.
+
 // FUSED: tile = whole slice (M = K), one workgroup per slice b.
-template <int K, typename T>
+template <int K, typename T, class Gain>
 __global__ void __launch_bounds__(1 << (K - VB))
-fused_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict__ y)
+fused_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, uint32_t nvalid)
 {
     using G = Groups<K, 0>;
     __shared__ float lds[pad(1u << K)];
     const uint32_t tau = threadIdx.x;
-    const size_t base = (size_t)blockIdx.x << K;
-    constexpr uint32_t bytes = (1u << K) * Elt<T>::bytes;
+    const size_t base = (size_t)blockIdx.x * nvalid;
     float v[V], gv[V];
-    load_layout<G::TOP, ContigMap, T>(v, buffer(x + base, bytes), tau);
-    load_gain<G::SL, ContigMap>(gv, g, tau);
+    load_tile<G::TOP, K, T>(v, x + base, nvalid, tau);
+    gain.template load<G::SL, ContigMap>(gv, 0, tau);
     butterflies<G::JT, VB>(v);
     forward_groups<K, 0, 0, G::TOP>(lds, v, tau);
     apply_gain<K>(v, gv);
     if constexpr (G::NBOT > 0)
         inverse_groups<K, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<G::JT, VB>(v);
-    store_layout<G::TOP, ContigMap, T>(v, buffer(y + base, bytes), tau);
+    store_tile<G::TOP, K, T>(v, y + base, nvalid, tau);
+}
+
+// Number of real elements in the outer tile hi of a slice.
+template <int A>
+__device__ __forceinline__ uint32_t tile_valid(uint32_t nvalid, uint32_t hi)
+{
+    const uint32_t start = hi << A;
+    return nvalid <= start ? 0u : min(nvalid - start, 1u << A);
 }
 
 // OUTER_FWD: block = b * 2^HB + hi; chunk x[b][hi * 2^A ...] -> workspace.
 template <int A, int HB, int R, typename T>
 __global__ void __launch_bounds__(1 << (A - VB))
-outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws)
+outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
 {
     using G = Groups<A, 0>;
     using Run = RunMap<HB, R>;
@@ -287,27 +385,24 @@ outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws)
     const uint32_t blk = blockIdx.x;
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
-    const size_t slice = b << (A + HB);
     float v[V];
-    load_layout<G::TOP, ContigMap, T>(
-        v, buffer(x + slice + ((size_t)hi << A), (1u << A) * Elt<T>::bytes), tau);
+    load_tile<G::TOP, A, T>(v, x + b * nvalid + ((size_t)hi << A), tile_valid<A>(nvalid, hi),
+                            tau);
     butterflies<0, VB>(v);
     forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
     store_layout<G::SL, Run, float>(
-        v, buffer(ws + slice + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
 }
 
 // MIDDLE: logical tile = run * B + b (the B slices sharing a gain tile are
 // adjacent); workgroups are renumbered so adjacent logical tiles land on the
 // same XCD (blocks are dealt round-robin over the 8 XCDs) and share its L2.
-// The gain tile is requested right after the data tile.
-template <int A, int HB, int R>
+template <int A, int HB, int R, class Gain>
 __global__ void __launch_bounds__(1 << (HB + R - VB))
-middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nslices)
+middle_kernel(float *__restrict__ ws, Gain gain, uint32_t nslices)
 {
     constexpr int M = HB + R;
     using G = Groups<M, R>;
-    using Gain = GainMap<A, R>;
     __shared__ float lds[pad(1u << M)];
     const uint32_t tau = threadIdx.x;
     const uint32_t nblk = gridDim.x;
@@ -320,7 +415,7 @@ middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nsli
         buffer(ws + (b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
     float v[V], gv[V];
     load_layout<G::TOP, ContigMap, float>(v, tile, tau);
-    load_gain<G::SL, Gain>(gv, g + ((size_t)run << R), tau);
+    gain.template load<G::SL, GainMap<A, R>>(gv, run << R, tau);
     butterflies<G::JT, VB>(v);
     forward_groups<M, R, 0, G::TOP>(lds, v, tau);
     apply_gain<A + HB>(v, gv);
@@ -333,7 +428,7 @@ middle_kernel(float *__restrict__ ws, const float *__restrict__ g, uint32_t nsli
 // OUTER_INV: mirror of OUTER_FWD.
 template <int A, int HB, int R, typename T>
 __global__ void __launch_bounds__(1 << (A - VB))
-outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y)
+outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
 {
     using G = Groups<A, 0>;
     using Run = RunMap<HB, R>;
@@ -342,14 +437,15 @@ outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y)
     const uint32_t blk = blockIdx.x;
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
-    const size_t slice = b << (A + HB);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    if (valid == 0)
+        return;   // wholly padding: nothing to store (uniform per workgroup)
     float v[V];
     load_layout<G::SL, Run, float>(
-        v, buffer(ws + slice + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
     inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<0, VB>(v);
-    store_layout<G::TOP, ContigMap, T>(
-        v, buffer(y + slice + ((size_t)hi << A), (1u << A) * Elt<T>::bytes), tau);
+    store_tile<G::TOP, A, T>(v, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
 __device__ __forceinline__ float to_float(float v) { return v; }
@@ -357,18 +453,18 @@ __device__ __forceinline__ float to_float(__bf16 v) { return (float)v; }
 template <typename T>
 __device__ __forceinline__ T from_float(float v) { return (T)v; }   // bf16: round to nearest even
 
-// SMALL: L = 2^K <= 2^10; one 256-thread workgroup per slice, every stage on
-// the LDS copy.
-template <typename T>
+// SMALL: 2^K <= 2^10; one 256-thread workgroup per slice, every stage on the
+// LDS copy.
+template <typename T, class Gain>
 __global__ void __launch_bounds__(256)
-small_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict__ y, int K)
+small_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, int K, uint32_t nvalid)
 {
     __shared__ float s[1 << kMaxSmall];
     const int L = 1 << K;
-    const size_t base = (size_t)blockIdx.x << K;
+    const size_t base = (size_t)blockIdx.x * nvalid;
     const float scale = 1.0f / (float)L;
     for (int i = threadIdx.x; i < L; i += blockDim.x)
-        s[i] = to_float(x[base + i]);
+        s[i] = (uint32_t)i < nvalid ? to_float(x[base + i]) : 0.0f;
     for (int pass = 0; pass < 2; ++pass) {
         for (int h = 1; h < L; h <<= 1) {
             __syncthreads();
@@ -382,9 +478,9 @@ small_kernel(const T *__restrict__ x, const float *__restrict__ g, T *__restrict
         __syncthreads();
         if (pass == 0)
             for (int i = threadIdx.x; i < L; i += blockDim.x)
-                s[i] *= g[i] * scale;
+                s[i] *= gain.at((uint32_t)i) * scale;
     }
-    for (int i = threadIdx.x; i < L; i += blockDim.x)
+    for (int i = threadIdx.x; i < (int)nvalid; i += blockDim.x)
         y[base + i] = from_float<T>(s[i]);
 }
 
@@ -394,76 +490,73 @@ inline hipError_t record(hipEvent_t ev, hipStream_t st)
     return ev ? hipEventRecord(ev, st) : hipSuccess;
 }
 
-template <int K, typename T>
-hipError_t launch_fused(const T *x, const float *g, T *y, int64_t B, hipStream_t st,
-                        hipEvent_t const *ev)
+template <int K, typename T, class Gain>
+hipError_t launch_fused(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
-    hipError_t e = record(ev[0], st);
+    hipError_t e = record(a.events[0], a.stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((fused_kernel<K, T>), dim3((uint32_t)B), dim3(1u << (K - VB)), 0, st,
-                       x, g, y);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return record(ev[1], st);
+    hipLaunchKernelGGL((fused_kernel<K, T, Gain>), dim3((uint32_t)a.B), dim3(1u << (K - VB)), 0,
+                       a.stream, x, y, gain, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(a.events[1], a.stream);
 }
 
-template <int K, typename T>
-hipError_t launch_three_pass(const T *x, const float *g, T *y, float *ws, int64_t B,
-                             hipStream_t st, hipEvent_t const *ev)
+template <int K, typename T, class Gain>
+hipError_t launch_three_pass(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
     constexpr Split sp = three_pass_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
     static_assert(A >= kMinTile && A <= kMaxTile, "outer tile size");
     static_assert(HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
     static_assert(HB >= 1 && R >= 0 && R <= A, "split");
-    hipError_t e = record(ev[0], st);
+    const hipStream_t st = a.stream;
+    hipError_t e = record(a.events[0], st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(B << HB)),
-                       dim3(1u << (A - VB)), 0, st, x, ws);
+    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, x, a.ws, a.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = record(ev[1], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((middle_kernel<A, HB, R>), dim3((uint32_t)(B << (A - R))),
-                       dim3(1u << (HB + R - VB)), 0, st, ws, g, (uint32_t)B);
+    if ((e = record(a.events[1], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((middle_kernel<A, HB, R, Gain>), dim3((uint32_t)(a.B << (A - R))),
+                       dim3(1u << (HB + R - VB)), 0, st, a.ws, gain, (uint32_t)a.B);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = record(ev[2], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(B << HB)),
-                       dim3(1u << (A - VB)), 0, st, ws, y);
+    if ((e = record(a.events[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, a.ws, y, a.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return record(ev[3], st);
+    return record(a.events[3], st);
 }
 
-template <typename T>
-hipError_t launch_small(const T *x, const float *g, T *y, int64_t B, int K, hipStream_t st,
-                        hipEvent_t const *ev)
+template <typename T, class Gain>
+hipError_t launch_small(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
-    hipError_t e = record(ev[0], st);
+    hipError_t e = record(a.events[0], a.stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((small_kernel<T>), dim3((uint32_t)B), dim3(256), 0, st, x, g, y, K);
+    hipLaunchKernelGGL((small_kernel<T, Gain>), dim3((uint32_t)a.B), dim3(256), 0, a.stream, x, y,
+                       gain, a.K, a.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return record(ev[1], st);
+    return record(a.events[1], a.stream);
 }
 
-template <typename T>
-hipError_t dispatch(const LaunchArgs &a)
+template <typename T, class Gain>
+hipError_t dispatch(const LaunchArgs &a, Gain gain)
 {
     const T *x = static_cast<const T *>(a.x);
     T *y = static_cast<T *>(a.y);
-    const int K = a.K;
     if (a.plan == PLAN_SMALL)
-        return launch_small<T>(x, a.gain, y, a.B, K, a.stream, a.events);
+        return launch_small<T, Gain>(x, y, gain, a);
     if (a.plan == PLAN_FUSED) {
-        switch (K) {
+        switch (a.K) {
 #define WHTMIX_FUSED_CASE(k) \
-    case k: return launch_fused<k, T>(x, a.gain, y, a.B, a.stream, a.events);
+    case k: return launch_fused<k, T, Gain>(x, y, gain, a);
             WHTMIX_FUSED_CASE(11) WHTMIX_FUSED_CASE(12) WHTMIX_FUSED_CASE(13)
             WHTMIX_FUSED_CASE(14) WHTMIX_FUSED_CASE(15)
 #undef WHTMIX_FUSED_CASE
         default: return hipErrorInvalidValue;
         }
     }
-    switch (K) {
+    switch (a.K) {
 #define WHTMIX_3P_CASE(k) \
-    case k: return launch_three_pass<k, T>(x, a.gain, y, a.ws, a.B, a.stream, a.events);
+    case k: return launch_three_pass<k, T, Gain>(x, y, gain, a);
         WHTMIX_3P_CASE(12) WHTMIX_3P_CASE(13) WHTMIX_3P_CASE(14) WHTMIX_3P_CASE(15)
         WHTMIX_3P_CASE(16) WHTMIX_3P_CASE(17) WHTMIX_3P_CASE(18) WHTMIX_3P_CASE(19)
         WHTMIX_3P_CASE(20) WHTMIX_3P_CASE(21) WHTMIX_3P_CASE(22) WHTMIX_3P_CASE(23)
@@ -474,13 +567,21 @@ hipError_t dispatch(const LaunchArgs &a)
     }
 }
 
+template <typename T>
+hipError_t dispatch_gain(const LaunchArgs &a)
+{
+    if (a.gain_kind == GAIN_LOG_SEPARABLE)
+        return dispatch<T>(a, LogSeparableGain{a.gain_t, a.gain_c, (uint32_t)a.cbits});
+    return dispatch<T>(a, FullGain{a.gain});
+}
+
 }  // namespace
 
 hipError_t launch(const LaunchArgs &a)
 {
     if (a.dtype == DTYPE_BF16)
-        return dispatch<__bf16>(a);
-    return dispatch<float>(a);
+        return dispatch_gain<__bf16>(a);
+    return dispatch_gain<float>(a);
 }
 
 }  // namespace whtmix

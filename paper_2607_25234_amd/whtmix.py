@@ -24,6 +24,7 @@ PLAN_NAMES = {v: k for k, v in PLANS.items()}
 EXPORTS = (
     "whtmix_forward",
     "whtmix_forward_ex",
+    "whtmix_forward_separable",
     "whtmix_plan_describe",
     "whtmix_status_string",
     "whtmix_last_error",
@@ -46,7 +47,8 @@ class Options(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("plan", ctypes.c_int), ("kernels", ctypes.c_int),
                 ("log2_slice", ctypes.c_int), ("outer_bits", ctypes.c_int),
-                ("run_bits", ctypes.c_int), ("workspace_bytes", ctypes.c_int64)]
+                ("run_bits", ctypes.c_int), ("workspace_bytes", ctypes.c_int64),
+                ("padded_tokens", ctypes.c_int64)]
 
 
 _lib = None
@@ -73,6 +75,9 @@ def lib():
         L.whtmix_forward_ex.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                         ctypes.POINTER(Options)]
         L.whtmix_forward_ex.restype = ctypes.c_int
+        L.whtmix_forward_separable.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
+                                               ctypes.POINTER(Options)]
+        L.whtmix_forward_separable.restype = ctypes.c_int
         L.whtmix_plan_describe.argtypes = [i64, i64, i64, ctypes.c_int,
                                            ctypes.POINTER(Options), ctypes.POINTER(PlanInfo)]
         L.whtmix_plan_describe.restype = ctypes.c_int
@@ -114,7 +119,8 @@ def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = 
         raise WhtmixError(st, "whtmix_plan_describe")
     return {"plan": PLAN_NAMES[info.plan], "kernels": info.kernels,
             "log2_slice": info.log2_slice, "outer_bits": info.outer_bits,
-            "run_bits": info.run_bits, "workspace_bytes": info.workspace_bytes}
+            "run_bits": info.run_bits, "workspace_bytes": info.workspace_bytes,
+            "padded_tokens": info.padded_tokens}
 
 
 def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
@@ -125,45 +131,92 @@ def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
                                    ctypes.byref(opt))
 
 
-def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=None):
-    """y[b] = H_N (G o (H_N x[b] H_C)) H_C on the GPU (section III-B, eqs. (2)-(3)).
+def padded_tokens(N: int) -> int:
+    """N_pad: the token axis is zero-padded to the next power of two."""
+    return 1 << max(0, (int(N) - 1).bit_length())
 
-    x: torch tensor [B, N, C] or [N, C], float32 or bfloat16, on a ROCm device.
-    gain: float32 [N, C] on the same device.  out: optional tensor like x
-    (may be x itself for in-place).  stream: a torch.cuda.Stream (default:
-    the current stream)."""
+
+def forward_separable_raw(x_ptr: int, gt_ptr: int, gc_ptr: int, y_ptr: int, B: int, N: int,
+                          C: int, dtype: int, stream: int, plan: str | int = "auto",
+                          events=None) -> int:
+    """Direct call of whtmix_forward_separable; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_forward_separable(x_ptr, gt_ptr, gc_ptr, y_ptr, B, N, C, dtype, stream,
+                                          ctypes.byref(opt))
+
+
+def _check(x, out):
     import torch
 
-    if x.device.type != "cuda" or gain.device != x.device:
-        raise ValueError("x and gain must be on the same GPU device")
+    if x.device.type != "cuda":
+        raise ValueError("x must be on a GPU device")
     if x.dtype == torch.float32:
         dt = DTYPE_F32
     elif x.dtype == torch.bfloat16:
         dt = DTYPE_BF16
     else:
         raise TypeError(f"x must be float32 or bfloat16, got {x.dtype}")
-    if gain.dtype != torch.float32:
-        raise TypeError("gain must be float32")
-    squeeze = x.dim() == 2
-    xx = x.unsqueeze(0) if squeeze else x
+    xx = x.unsqueeze(0) if x.dim() == 2 else x
     if xx.dim() != 3:
         raise ValueError("x must be [B, N, C] or [N, C]")
-    B, N, C = xx.shape
-    if tuple(gain.shape) != (N, C):
-        raise ValueError(f"gain shape {tuple(gain.shape)} != {(N, C)}")
-    if not xx.is_contiguous() or not gain.is_contiguous():
-        raise ValueError("x and gain must be contiguous")
+    if not xx.is_contiguous():
+        raise ValueError("x must be contiguous")
     if out is None:
         out = torch.empty_like(x)
     elif out.shape != x.shape or out.dtype != x.dtype or not out.is_contiguous() \
             or out.device != x.device:
         raise ValueError("out must be a contiguous tensor like x")
+    return xx, dt, out
+
+
+def _gain(t, shape, x, what):
+    import torch
+
+    if t.device != x.device or t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous float32 tensor on x's device")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} shape {tuple(t.shape)} != {tuple(shape)}")
+
+
+def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=None):
+    """y[b] = H_N (G o (H_N x[b] H_C)) H_C on the GPU (section III-B, eqs. (2)-(3)).
+
+    x: torch tensor [B, N, C] or [N, C], float32 or bfloat16, on a ROCm device.
+    gain: float32 [N_pad, C] (N_pad = N rounded up to a power of two; the token
+    axis is zero-padded) on the same device.  out: optional tensor like x (may
+    be x itself for in-place).  stream: a torch.cuda.Stream (default: the
+    current stream)."""
+    import torch
+
+    xx, dt, out = _check(x, out)
+    B, N, C = xx.shape
+    _gain(gain, (padded_tokens(N), C), x, "gain")
     st = stream if stream is not None else torch.cuda.current_stream(x.device)
     with torch.cuda.device(x.device):
         status = forward_raw(xx.data_ptr(), gain.data_ptr(), out.data_ptr(), B, N, C, dt,
                              st.cuda_stream, plan, events)
     if status != SUCCESS:
         raise WhtmixError(status, "whtmix_forward")
+    return out
+
+
+def forward_separable(x, log_gain_tokens, log_gain_channels, out=None,
+                      plan: str | int = "auto", stream=None, events=None):
+    """The paper's parametrisation (eq. (2) then eq. (3)) with log-domain gains:
+    log_gain_tokens float32 [N_pad], log_gain_channels float32 [C]."""
+    import torch
+
+    xx, dt, out = _check(x, out)
+    B, N, C = xx.shape
+    _gain(log_gain_tokens, (padded_tokens(N),), x, "log_gain_tokens")
+    _gain(log_gain_channels, (C,), x, "log_gain_channels")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = forward_separable_raw(xx.data_ptr(), log_gain_tokens.data_ptr(),
+                                       log_gain_channels.data_ptr(), out.data_ptr(), B, N, C,
+                                       dt, st.cuda_stream, plan, events)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_forward_separable")
     return out
 
 

@@ -125,6 +125,15 @@ def draw(B: int, N: int, C: int, dtype: str = "f32", seed: int = 0,
     return np.ascontiguousarray(x), np.ascontiguousarray(g)
 
 
+def draw_log_gains(P: int, C: int, seed: int):
+    """Seeded log-domain gains for the separable form: g_t[P], g_c[C], each
+    ~ N(0, 0.3^2), float32 (the paper initialises them at zero)."""
+    rng = np.random.default_rng(seed)
+    gt = np.float32(0.3) * rng.standard_normal(P, dtype=np.float32)
+    gc = np.float32(0.3) * rng.standard_normal(C, dtype=np.float32)
+    return gt, gc
+
+
 def inputs(w: Workload | str):
     """Inputs of a named workload, as (x float32 [B,N,C], g float32 [N,C])."""
     if isinstance(w, str):

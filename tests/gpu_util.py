@@ -52,3 +52,16 @@ def errors(y: np.ndarray, ref: np.ndarray) -> tuple[float, float]:
     d = y - ref
     rms_den = max(float(np.sqrt(np.mean(ref * ref))), 1e-300)
     return float(np.max(np.abs(d)) / den), float(np.sqrt(np.mean(d * d)) / rms_den)
+
+
+def run_gpu_separable(x: np.ndarray, gt: np.ndarray, gc: np.ndarray, dtype: str, dev,
+                      plan="auto") -> np.ndarray:
+    import torch
+    from paper_2607_25234_amd import whtmix
+    xd = to_device(x, dtype, dev)
+    gtd = torch.from_numpy(np.ascontiguousarray(gt, dtype=np.float32)).to(dev)
+    gcd = torch.from_numpy(np.ascontiguousarray(gc, dtype=np.float32)).to(dev)
+    y = whtmix.forward_separable(xd, gtd, gcd, plan=plan)
+    torch.cuda.synchronize(dev)
+    return to_host(y)
+

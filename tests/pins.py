@@ -14,7 +14,9 @@ that does not depend on the oracle's code:
   selecting a single Walsh basis image, linearity, self-adjointness, batch
   independence;
 * the paper's separable form (eq. (2) then eq. (3)) equals the joint gain
-  form with a rank-one G.
+  form with a rank-one G;
+* zero padding of the token axis (section III-B) against dense products of
+  explicitly padded matrices.
 
 The same functions run against the real oracle (``test_oracle_pins.py``) and
 against deliberately broken copies of it (``test_oracle_mutants.py``), which
@@ -232,14 +234,50 @@ def pin_structure(o) -> None:
     assert np.array_equal(o.whtmix(xb[perm], g), yb[perm])
 
 
+def _pad_rows(x, P):
+    return np.concatenate([x, np.zeros((P - x.shape[0],) + x.shape[1:])], axis=0)
+
+
+def pin_padding_dense(o) -> None:
+    """Section III-B zero-pads the token axis to the next power of two before
+    H_N: with dense matrices, Y = first N rows of
+    H_P (G o (H_P [X; 0] H_C)) H_C, and likewise for the separable form."""
+    rng = np.random.default_rng(109)
+    for (N, C) in [(3, 4), (5, 2), (6, 8), (7, 1), (9, 4), (12, 16), (100, 2), (33, 32)]:
+        P = 1 << (N - 1).bit_length()
+        x = rng.standard_normal((2, N, C))
+        g = rng.uniform(0.5, 1.5, (P, C))
+        Hp, Hc = _hadamard_orth(P), _hadamard_orth(C)
+        ref = np.stack([(Hp @ (g * (Hp @ _pad_rows(xb, P) @ Hc)) @ Hc)[:N] for xb in x])
+        got = o.whtmix(x, g)
+        assert got.shape == x.shape
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+        gt, gc = rng.normal(0, 0.5, P), rng.normal(0, 0.5, C)
+        Dt, Dc = np.diag(np.exp(gt)), np.diag(np.exp(gc))
+        ref = np.stack([(Hp @ Dt @ Hp @ _pad_rows(xb, P) @ Hc @ Dc @ Hc)[:N] for xb in x])
+        got = o.whtmix_separable(x, gt, gc)
+        assert _rel(got, ref) < 1e-12, ((N, C), _rel(got, ref))
+
+
+def pin_padding_unit_gain(o) -> None:
+    """Padding rows are zeros, so a unit gain still returns X exactly."""
+    rng = np.random.default_rng(110)
+    for (N, C) in [(3, 1), (17, 8), (1000, 4), (9216 // 8, 8)]:
+        P = 1 << (N - 1).bit_length()
+        x = rng.standard_normal((2, N, C))
+        assert _rel(o.whtmix(x, np.ones((P, C))), x) < 1e-13, (N, C)
+        assert _rel(o.whtmix_separable(x, np.zeros(P), np.zeros(C)), x) < 1e-13, (N, C)
+
+
 def pin_rejects_bad_shapes(o) -> None:
-    """The transform is defined for power-of-two lengths only (section III-B)."""
-    for (N, C) in [(3, 4), (4, 6), (12, 1)]:
+    """The channel transform needs a power-of-two C (section III-B pads only
+    the token axis); a token count must be at least 1."""
+    for (N, C) in [(4, 3), (4, 6), (12, 12)]:
         try:
-            o.whtmix(np.zeros((N, C)), np.ones((N, C)))
+            o.whtmix(np.zeros((N, C)), np.ones((1 << (N - 1).bit_length(), C)))
         except ValueError:
             continue
-        raise AssertionError(f"accepted non-power-of-two shape {(N, C)}")
+        raise AssertionError(f"accepted non-power-of-two C {(N, C)}")
 
 
 ALL_PINS = [
@@ -254,5 +292,7 @@ ALL_PINS = [
     pin_separable_form,
     pin_flat_1d_equivalence,
     pin_structure,
+    pin_padding_dense,
+    pin_padding_unit_gain,
     pin_rejects_bad_shapes,
 ]

@@ -43,7 +43,7 @@ def test_library_exports_nothing_else():
 
 
 def test_version_and_status_strings():
-    assert whtmix.lib().whtmix_version() == 100
+    assert whtmix.lib().whtmix_version() == 10100
     for st in range(8):
         assert whtmix.status_string(st)
     assert whtmix.status_string(99) == "unknown status"
@@ -57,11 +57,13 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(dtype=2), 3),
     (dict(dtype=-1), 3),
     (dict(B=-1), 1),
-    (dict(N=3), 2),
+    (dict(C=3), 2),
     (dict(C=0), 2),
-    (dict(N=0), 2),
-    (dict(N=-4), 2),
+    (dict(C=96), 2),
+    (dict(N=0), 1),
+    (dict(N=-4), 1),
     (dict(N=1 << 16, C=1 << 15), 7),          # N*C = 2^31 > 2^30
+    (dict(N=(1 << 24) + 1, C=64), 7),         # N pads to 2^25: 2^31 > 2^30
     (dict(B=1 << 30, N=1 << 10, C=1 << 10), 7),  # B*N*C beyond the grid limit
     (dict(x=0), 1),
     (dict(g=0), 1),
@@ -78,6 +80,33 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
     assert call(**kwargs) == status
+
+
+def sep(x=ALIGNED, gt=ALIGNED2, gc=ALIGNED2 + 4096, y=ALIGNED, B=1, N=64, C=64, dtype=0):
+    return whtmix.forward_separable_raw(x, gt, gc, y, B, N, C, dtype, 0)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(gt=0), 1),
+    (dict(gc=0), 1),
+    (dict(gc=ALIGNED2 + 4), 4),
+    (dict(gt=ALIGNED + 64), 1),               # token gains inside y
+    (dict(gc=ALIGNED + 64 * 64 * 4 - 16), 1),  # channel gains overlap y's end
+    (dict(C=12), 2),
+    (dict(dtype=5), 3),
+])
+def test_separable_rejected_before_any_hip_call(kwargs, status):
+    assert sep(**kwargs) == status
+
+
+def test_padded_plans():
+    """Non-power-of-two token counts are zero-padded (section III-B)."""
+    for N, C, P in [(3, 4, 4), (5, 1, 8), (9216, 64, 16384), (25600, 64, 32768),
+                    (50176, 64, 65536), (1, 1, 1)]:
+        d = whtmix.plan_describe(2, N, C)
+        assert d["padded_tokens"] == P == whtmix.padded_tokens(N)
+        assert 1 << d["log2_slice"] == P * C
+    assert whtmix.plan_describe(2, 9216, 64)["workspace_bytes"] == 2 * 16384 * 64 * 4
 
 
 def test_empty_batch_is_a_no_op():

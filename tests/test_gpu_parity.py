@@ -10,7 +10,10 @@ import pytest
 
 from oracle import oracle as oracle_mod
 from paper_2607_25234_amd import whtmix, workloads
-from tests.gpu_util import TOL, device, errors, run_gpu, say, to_device, to_host
+from tests.gpu_util import (TOL, device, errors, run_gpu, run_gpu_separable, say, to_device,
+                            to_host)
+
+log_gains = workloads.draw_log_gains
 
 pytestmark = pytest.mark.gpu
 
@@ -67,6 +70,69 @@ def test_shapes(shape, dtype, dev, orc):
     say(f"shape {shape} {dtype} plan={plan}")
     y = run_gpu(x, g, dtype, dev)
     check(f"{shape}", y, orc.whtmix(x, g), dtype)
+
+
+# Token counts that are not powers of two (zero padding, section III-B),
+# including the paper's stereo joint token counts 9216, 25600 and 50176
+# (384x768, 640x1280 and 896x1792 images).
+PADDED = [(1, 3, 4), (2, 5, 8), (1, 100, 8), (3, 1000, 16), (2, 130, 128), (2, 9216, 64),
+          (1, 25600, 64), (1, 50176, 64), (2, 36864, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", PADDED, ids=lambda s: "x".join(map(str, s)))
+def test_padded_tokens(shape, dtype, dev, orc):
+    B, N, C = shape
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=300 + N)
+    _, g = workloads.draw(1, P, C, "f32", seed=301 + N)
+    plan = whtmix.plan_describe(B, N, C, dtype)["plan"]
+    say(f"padded {shape} -> P={P} {dtype} plan={plan}")
+    ref = orc.whtmix(x, g)
+    check(f"{shape}", run_gpu(x, g, dtype, dev), ref, dtype)
+    if plan == "fused":
+        check(f"{shape} three_pass", run_gpu(x, g, dtype, dev, plan="three_pass"), ref, dtype)
+
+
+SEPARABLE = [(1, 1, 1), (2, 32, 32), (3, 64, 128), (2, 4096, 64), (1, 9216, 64),
+             (2, 16384, 128), (1, 1000, 16)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SEPARABLE, ids=lambda s: "x".join(map(str, s)))
+def test_separable_gains(shape, dtype, dev, orc):
+    """The paper's parametrisation: eq. (2) then eq. (3) with log gains."""
+    B, N, C = shape
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=400 + N)
+    gt, gc = log_gains(P, C, seed=401 + N)
+    plan = whtmix.plan_describe(B, N, C, dtype)["plan"]
+    say(f"separable {shape} {dtype} plan={plan}")
+    check(f"separable {shape}", run_gpu_separable(x, gt, gc, dtype, dev),
+          orc.whtmix_separable(x, gt, gc), dtype)
+
+
+def test_separable_workload(dev, orc):
+    """The benchmarked workload shape with the paper's log gains."""
+    w = workloads.WORKLOADS[workloads.BENCH_WORKLOAD]
+    x, _ = workloads.inputs(w)
+    gt, gc = log_gains(w.N, w.C, seed=77)
+    check("separable stereo64k_bf16", run_gpu_separable(x, gt, gc, w.dtype, dev),
+          orc.whtmix_separable(x, gt, gc), w.dtype)
+
+
+def test_separable_zero_log_gain_and_joint_equivalence(dev):
+    """Zero log gains (the paper's initialisation) give Y = X, and the
+    separable entry point matches the joint one with G = exp(g_t) exp(g_c)^T."""
+    B, N, C = 2, 4096, 64
+    x, _ = workloads.draw(B, N, C, "f32", seed=5)
+    y0 = run_gpu_separable(x, np.zeros(N, np.float32), np.zeros(C, np.float32), "f32", dev)
+    assert errors(y0, x)[0] < 1e-6
+    gt, gc = log_gains(N, C, seed=6)
+    G = (np.exp(gt.astype(np.float64))[:, None] * np.exp(gc.astype(np.float64))[None, :])
+    yj = run_gpu(x, G.astype(np.float32), "f32", dev)
+    ys = run_gpu_separable(x, gt, gc, "f32", dev)
+    assert errors(ys, yj)[0] < 2e-6
 
 
 @pytest.mark.parametrize("K", [12, 13, 14, 15])

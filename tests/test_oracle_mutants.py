@@ -31,19 +31,22 @@ MUTANTS = {
     "token_stride": ("wht_orthonormal(z + c, N, C);",
                      "wht_orthonormal(z + c * N, N, 1);"),
     # gain read transposed, G[c][n] instead of G[n][c]
-    "gain_transposed": ("z[i] *= g[i];", "z[i] *= g[(i % C) * N + i / C];"),
+    "gain_transposed": ("z[i] *= g[i];", "z[i] *= g[(i % C) * P + i / C];"),
     # forward token transform dropped
     "forward_token_dropped": (
-        "        channel_transform(z, N, C);\n        token_transform(z, N, C);\n"
+        "        channel_transform(z, P, C);\n        token_transform(z, P, C);\n"
         "        /* per-frequency gain */",
-        "        channel_transform(z, N, C);\n        /* per-frequency gain */"),
+        "        channel_transform(z, P, C);\n        /* per-frequency gain */"),
     # batch slice offset wrong
-    "batch_offset": ("double *z = y + b * L;\n        if (z != x + b * L)\n"
-                     "            memcpy(z, x + b * L, (size_t)L * sizeof(double));\n"
-                     "        /* forward",
-                     "double *z = y + b * L;\n        if (z != x + b * N)\n"
-                     "            memcpy(z, x + b * N, (size_t)L * sizeof(double));\n"
-                     "        /* forward"),
+    "batch_offset": ("load_padded(z, x + b * N * C, N, P, C);\n        /* forward",
+                     "load_padded(z, x + b * C, N, P, C);\n        /* forward"),
+    # token axis extended periodically instead of zero-padded
+    "padding_not_zero": (
+        "memset(z + N * C, 0, (size_t)((P - N) * C) * sizeof(double));",
+        "for (long i = N * C; i < P * C; ++i) z[i] = xb[i % (N * C)];"),
+    # the wrong N rows kept after the padded transform
+    "crop_offset": ("channel_transform(z, P, C);\n        memcpy(y + b * N * C, z, ",
+                    "channel_transform(z, P, C);\n        memcpy(y + b * N * C, z + (P - N) * C, "),
     # separable form: log gains used without exponentiation
     "separable_no_exp": ("z[n * C + c] *= exp(g_c[c]);", "z[n * C + c] *= g_c[c];"),
     # separable form: token gain indexed by channel

@@ -133,28 +133,41 @@ class Access:
         self.count = np.zeros(size, np.int64)
 
     def at(self, offs):
+        if offs.size == 0:
+            return offs
         assert offs.min() >= 0 and offs.max() < self.size, "out of bounds"
         np.add.at(self.count, offs.reshape(-1), 1)
         return offs
 
 
+def tile_valid(nvalid, hi, A):
+    start = hi << A
+    return 0 if nvalid <= start else min(nvalid - start, 1 << A)
+
+
 def simulate_three_pass(x, g, K, split):
-    """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel."""
+    """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel.  x holds
+    N <= 2^K / C real tokens per slice (zero padding of the token axis)."""
     B = x.shape[0]
     L = 1 << K
+    nvalid = x.shape[1] * x.shape[2]
     A, HB, R = split
-    xs = x.reshape(B, L)
+    xs = x.reshape(B * nvalid)
     ws = np.full(B * L, np.nan)
-    y = np.full(B * L, np.nan)
+    y = np.full(B * nvalid, np.nan)
     gf = g.reshape(L)
-    acc = {k: Access(B * L) for k in ("x", "ws_w1", "ws_r2", "ws_w2", "ws_r3", "y")}
+    acc = {k: Access(B * L) for k in ("ws_w1", "ws_r2", "ws_w2")}
+    acc_x, acc_y, acc_r3 = Access(B * nvalid), Access(B * nvalid), Access(B * L)
     acc_g = Access(L)
     # outer forward: block = b * 2^HB + hi
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
         T = Tile(A, 0)
-        base = b * L + (hi << A)
-        v = xs.reshape(-1)[acc["x"].at(base + contig_map(T.idx(T.g.TOP)))].copy()
+        valid = tile_valid(nvalid, hi, A)
+        t = T.idx(T.g.TOP)
+        v = np.zeros(t.shape)
+        m = t < valid
+        v[m] = xs[acc_x.at(b * nvalid + (hi << A) + t[m])]
         butterflies(v, 0, VB)
         v = T.forward_groups(v, T.g.TOP)
         wbase = b * L + (hi << R)
@@ -179,14 +192,21 @@ def simulate_three_pass(x, g, K, split):
     # outer inverse
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        valid = tile_valid(nvalid, hi, A)
+        if valid == 0:
+            continue
         T = Tile(A, 0)
         wbase = b * L + (hi << R)
-        v = ws[acc["ws_r3"].at(wbase + run_map(T.idx(T.g.SL), HB, R))].copy()
+        v = ws[acc_r3.at(wbase + run_map(T.idx(T.g.SL), HB, R))].copy()
         v = T.inverse_groups(v)
         butterflies(v, 0, VB)
-        y[acc["y"].at(b * L + (hi << A) + contig_map(T.idx(T.g.TOP)))] = v
+        t = T.idx(T.g.TOP)
+        m = t < valid
+        y[acc_y.at(b * nvalid + (hi << A) + t[m])] = v[m]
     for k, a in acc.items():
         assert np.all(a.count == 1), f"{k}: elements not touched exactly once"
+    assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
+    assert np.all(acc_r3.count <= 1)
     assert np.all(acc_g.count == B), "each gain element read once per slice"
     return y.reshape(x.shape)
 
@@ -194,19 +214,23 @@ def simulate_three_pass(x, g, K, split):
 def simulate_fused(x, g, K):
     B = x.shape[0]
     L = 1 << K
-    xs = x.reshape(B * L)
-    y = np.full(B * L, np.nan)
-    acc_x, acc_y, acc_g = Access(B * L), Access(B * L), Access(L)
+    nvalid = x.shape[1] * x.shape[2]
+    xs = x.reshape(B * nvalid)
+    y = np.full(B * nvalid, np.nan)
+    acc_x, acc_y, acc_g = Access(B * nvalid), Access(B * nvalid), Access(L)
     for b in range(B):
         T = Tile(K, 0)
-        v = xs[acc_x.at(b * L + T.idx(T.g.TOP))].copy()
+        t = T.idx(T.g.TOP)
+        m = t < nvalid
+        v = np.zeros(t.shape)
+        v[m] = xs[acc_x.at(b * nvalid + t[m])]
         butterflies(v, T.g.JT, VB)
         v = T.forward_groups(v, T.g.TOP)
         v = v * (g.reshape(L)[acc_g.at(T.idx(T.g.SL))] * (1.0 / L))
         if T.g.NBOT > 0:
             v = T.inverse_groups(v)
         butterflies(v, T.g.JT, VB)
-        y[acc_y.at(b * L + T.idx(T.g.TOP))] = v
+        y[acc_y.at(b * nvalid + t[m])] = v[m]
     assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
     assert np.all(acc_g.count == B)
     return y.reshape(x.shape)
@@ -282,6 +306,24 @@ def test_three_pass_maps_in_bounds(K):
         goff = (run << R) + gain_map(Tm.idx(Tm.g.SL), A, R)
         assert goff.min() >= 0 and goff.max() < L
     assert pad((1 << 15) - 1) < 160 * 1024 // 4   # LDS fits in 160 KiB
+
+
+@pytest.mark.parametrize("N,C", [(1000, 2), (33, 64), (100, 64), (130, 128), (257, 64)])
+def test_padded_schedules(N, C, orc):
+    """Token counts that are not powers of two: the padded slice of
+    P = 2^ceil(log2 N) rows, with the tiles straddling or beyond row N masked."""
+    rng = np.random.default_rng(N + C)
+    P = 1 << (N - 1).bit_length()
+    K = (P * C).bit_length() - 1
+    x = rng.standard_normal((3, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    ref = orc.whtmix(x, g)
+    if K <= 15:
+        y = simulate_fused(x, g, K)
+        assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
+    if K >= 12:
+        y = simulate_three_pass(x, g, K, three_pass_split(K))
+        assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
 
 
 def test_middle_renumbering_is_a_permutation():
