@@ -49,6 +49,10 @@ def load(path: str = LIB):
     lib.oracle_whtmix_separable.restype = ctypes.c_int
     lib.oracle_fwht.argtypes = [dp, L]
     lib.oracle_fwht.restype = ctypes.c_int
+    lib.oracle_whtmix_grad.argtypes = [dp, dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_grad.restype = ctypes.c_int
+    lib.oracle_whtmix_grad_separable.argtypes = [dp, dp, dp, dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_grad_separable.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     if path == LIB:
@@ -114,6 +118,50 @@ class Oracle:
         if rc != 0:
             raise ValueError(f"oracle_whtmix_separable rejected {(B, N, C)}")
         return y[0] if squeeze else y
+
+    def whtmix_grad(self, x, dy, g):
+        """(dX, dG) for upstream gradient dy through the joint-gain mixer:
+        dX = the mixer applied to dy, dG = sum_b (H X_b H) o (H dY_b H)."""
+        x64, dy64 = _as_f64(x), _as_f64(dy)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64, dy64 = x64[None], dy64[None]
+        B, N, C = x64.shape
+        if dy64.shape != x64.shape:
+            raise ValueError("dy must have x's shape")
+        g64 = _as_f64(g)
+        if g64.shape != (padded(N), C):
+            raise ValueError(f"gain shape {g64.shape} != {(padded(N), C)}")
+        dx = np.empty_like(x64)
+        dg = np.empty_like(g64)
+        rc = self.lib.oracle_whtmix_grad(_dptr(x64), _dptr(dy64), _dptr(g64), _dptr(dx),
+                                         _dptr(dg), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_grad rejected shape {(B, N, C)}")
+        return (dx[0] if squeeze else dx), dg
+
+    def whtmix_grad_separable(self, x, dy, g_t, g_c):
+        """(dX, dg_t, dg_c) for upstream gradient dy through eq. (2)-(3)."""
+        x64, dy64 = _as_f64(x), _as_f64(dy)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64, dy64 = x64[None], dy64[None]
+        B, N, C = x64.shape
+        if dy64.shape != x64.shape:
+            raise ValueError("dy must have x's shape")
+        gt = _as_f64(g_t).reshape(-1)
+        gc = _as_f64(g_c).reshape(-1)
+        if gt.shape != (padded(N),) or gc.shape != (C,):
+            raise ValueError("g_t must have P entries and g_c C entries")
+        dx = np.empty_like(x64)
+        dgt = np.empty_like(gt)
+        dgc = np.empty_like(gc)
+        rc = self.lib.oracle_whtmix_grad_separable(_dptr(x64), _dptr(dy64), _dptr(gt),
+                                                   _dptr(gc), _dptr(dx), _dptr(dgt),
+                                                   _dptr(dgc), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_grad_separable rejected {(B, N, C)}")
+        return (dx[0] if squeeze else dx), dgt, dgc
 
     def fwht(self, v) -> np.ndarray:
         """Unnormalised Sylvester butterfly of a 1-D vector (H_n v, +/-1 H)."""

@@ -167,6 +167,98 @@ int oracle_whtmix_separable(const double *x, const double *g_t,
     return 0;
 }
 
+/* Gradients through the joint-gain mixer (the paper trains the gains,
+ * section IV-A).  For a loss with upstream gradient dY = dL/dY, and
+ *     T_x[b]  = H_P Xpad[b] H_C,   T_dy[b] = H_P dYpad[b] H_C
+ * (orthonormal transforms of the zero-padded slices):
+ *     dX[b] = first N rows of H_P (G o T_dy[b]) H_C
+ *             (the mixer is self-adjoint: H symmetric, G diagonal),
+ *     dG    = sum over b of T_x[b] o T_dy[b].
+ * dx or dg may be NULL to skip that output.  Same return convention as
+ * oracle_whtmix(). */
+int oracle_whtmix_grad(const double *x, const double *dy, const double *g,
+                       double *dx, double *dg, long B, long N, long C)
+{
+    if (!x || !dy || !g || B < 0 || N < 1 || !is_pow2(C))
+        return -1;
+    if (dx && oracle_whtmix(dy, g, dx, B, N, C) != 0)
+        return -1;
+    if (!dg)
+        return 0;
+    const long P = padded(N);
+    double *tx = malloc((size_t)(P * C) * sizeof(double));
+    double *td = malloc((size_t)(P * C) * sizeof(double));
+    if (!tx || !td) {
+        free(tx);
+        free(td);
+        return -1;
+    }
+    memset(dg, 0, (size_t)(P * C) * sizeof(double));
+    for (long b = 0; b < B; ++b) {
+        load_padded(tx, x + b * N * C, N, P, C);
+        channel_transform(tx, P, C);
+        token_transform(tx, P, C);
+        load_padded(td, dy + b * N * C, N, P, C);
+        channel_transform(td, P, C);
+        token_transform(td, P, C);
+        for (long i = 0; i < P * C; ++i)
+            dg[i] += tx[i] * td[i];
+    }
+    free(tx);
+    free(td);
+    return 0;
+}
+
+/* Gradients through the separable form (eqs. (2)-(3)), whose joint gain is
+ * G[n][c] = exp(g_t[n]) exp(g_c[c]):
+ *     dX         as oracle_whtmix_grad with that G,
+ *     dg_t[n]  = sum over c of dG[n][c] G[n][c],
+ *     dg_c[c]  = sum over n of dG[n][c] G[n][c]   (chain rule through exp).
+ * Any of dx, dg_t, dg_c may be NULL (dg_t and dg_c together). */
+int oracle_whtmix_grad_separable(const double *x, const double *dy,
+                                 const double *g_t, const double *g_c,
+                                 double *dx, double *dg_t, double *dg_c,
+                                 long B, long N, long C)
+{
+    if (!x || !dy || !g_t || !g_c || B < 0 || N < 1 || !is_pow2(C))
+        return -1;
+    if (dx && oracle_whtmix_separable(dy, g_t, g_c, dx, B, N, C) != 0)
+        return -1;
+    if (!dg_t || !dg_c)
+        return 0;
+    const long P = padded(N);
+    double *G = malloc((size_t)(P * C) * sizeof(double));
+    double *dG = malloc((size_t)(P * C) * sizeof(double));
+    if (!G || !dG) {
+        free(G);
+        free(dG);
+        return -1;
+    }
+    for (long n = 0; n < P; ++n)
+        for (long c = 0; c < C; ++c)
+            G[n * C + c] = exp(g_t[n]) * exp(g_c[c]);
+    if (oracle_whtmix_grad(x, dy, G, NULL, dG, B, N, C) != 0) {
+        free(G);
+        free(dG);
+        return -1;
+    }
+    for (long n = 0; n < P; ++n) {
+        double s = 0.0;
+        for (long c = 0; c < C; ++c)
+            s += dG[n * C + c] * G[n * C + c];
+        dg_t[n] = s;
+    }
+    for (long c = 0; c < C; ++c) {
+        double s = 0.0;
+        for (long n = 0; n < P; ++n)
+            s += dG[n * C + c] * G[n * C + c];
+        dg_c[c] = s;
+    }
+    free(G);
+    free(dG);
+    return 0;
+}
+
 /* Bare unnormalised butterfly over a contiguous vector, exported so that the
  * tests can pin the transform itself against a dense Sylvester matrix. */
 int oracle_fwht(double *v, long n)

@@ -16,7 +16,9 @@ that does not depend on the oracle's code:
 * the paper's separable form (eq. (2) then eq. (3)) equals the joint gain
   form with a rank-one G;
 * zero padding of the token axis (section III-B) against dense products of
-  explicitly padded matrices.
+  explicitly padded matrices;
+* the backward pass (dX, dG and the separable log-gain gradients) against
+  dense products and against finite differences of the forward mixer.
 
 The same functions run against the real oracle (``test_oracle_pins.py``) and
 against deliberately broken copies of it (``test_oracle_mutants.py``), which
@@ -269,6 +271,69 @@ def pin_padding_unit_gain(o) -> None:
         assert _rel(o.whtmix_separable(x, np.zeros(P), np.zeros(C)), x) < 1e-13, (N, C)
 
 
+def pin_grad_dense(o) -> None:
+    """Backward with dense matrices: dX = first N rows of
+    H_P (G o (H_P [dY; 0] H_C)) H_C and dG = sum_b T_x[b] o T_dy[b] with
+    T = H_P [.; 0] H_C; separable log gains by the chain rule through exp."""
+    rng = np.random.default_rng(111)
+    for (N, C, B) in [(4, 8, 3), (3, 4, 2), (16, 2, 1), (1, 8, 2), (6, 1, 2)]:
+        P = 1 << (N - 1).bit_length()
+        Hp, Hc = _hadamard_orth(P), _hadamard_orth(C)
+        x = rng.standard_normal((B, N, C))
+        dy = rng.standard_normal((B, N, C))
+        g = rng.uniform(0.5, 1.5, (P, C))
+        T = lambda a: Hp @ _pad_rows(a, P) @ Hc
+        dx_ref = np.stack([(Hp @ (g * T(d)) @ Hc)[:N] for d in dy])
+        dg_ref = sum(T(xb) * T(db) for xb, db in zip(x, dy))
+        dx, dg = o.whtmix_grad(x, dy, g)
+        assert _rel(dx, dx_ref) < 1e-12 and _rel(dg, dg_ref) < 1e-12, (N, C)
+        gt, gc = rng.normal(0, 0.4, P), rng.normal(0, 0.4, C)
+        G = np.outer(np.exp(gt), np.exp(gc))
+        dG = sum(T(xb) * T(db) for xb, db in zip(x, dy))
+        dx_ref = np.stack([(Hp @ (G * T(d)) @ Hc)[:N] for d in dy])
+        dx, dgt, dgc = o.whtmix_grad_separable(x, dy, gt, gc)
+        assert _rel(dx, dx_ref) < 1e-12, (N, C)
+        assert _rel(dgt, (dG * G).sum(axis=1)) < 1e-12 and _rel(dgc, (dG * G).sum(axis=0)) < 1e-12
+
+
+def pin_grad_finite_differences(o) -> None:
+    """The loss L = sum_b <Y_b, W_b> is linear in G and in X, so central
+    differences of the forward mixer give dG and dX up to rounding; in the
+    log gains it is smooth, checked with a small step."""
+    rng = np.random.default_rng(112)
+    B, N, C = 2, 5, 4
+    P = 8
+    x = rng.standard_normal((B, N, C))
+    w = rng.standard_normal((B, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    dx, dg = o.whtmix_grad(x, w, g)
+    loss = lambda xx, gg: float(np.sum(o.whtmix(xx, gg) * w))
+    for (i, j) in [(0, 0), (3, 2), (7, 3), (5, 1)]:
+        e = np.zeros((P, C))
+        e[i, j] = 1.0
+        fd = (loss(x, g + 0.5 * e) - loss(x, g - 0.5 * e)) / 1.0
+        assert abs(fd - dg[i, j]) < 1e-12 * max(1.0, abs(fd)), (i, j)
+    for (b, n, c) in [(0, 0, 0), (1, 4, 3), (0, 2, 1)]:
+        e = np.zeros((B, N, C))
+        e[b, n, c] = 1.0
+        fd = (loss(x + 0.5 * e, g) - loss(x - 0.5 * e, g)) / 1.0
+        assert abs(fd - dx[b, n, c]) < 1e-12 * max(1.0, abs(fd)), (b, n, c)
+    gt, gc = rng.normal(0, 0.3, P), rng.normal(0, 0.3, C)
+    _, dgt, dgc = o.whtmix_grad_separable(x, w, gt, gc)
+    sloss = lambda a, b_: float(np.sum(o.whtmix_separable(x, a, b_) * w))
+    h = 1e-5
+    for n in [0, 3, 7]:
+        e = np.zeros(P)
+        e[n] = h
+        fd = (sloss(gt + e, gc) - sloss(gt - e, gc)) / (2 * h)
+        assert abs(fd - dgt[n]) < 1e-7 * max(1.0, abs(fd)), n
+    for c in [0, 2]:
+        e = np.zeros(C)
+        e[c] = h
+        fd = (sloss(gt, gc + e) - sloss(gt, gc - e)) / (2 * h)
+        assert abs(fd - dgc[c]) < 1e-7 * max(1.0, abs(fd)), c
+
+
 def pin_rejects_bad_shapes(o) -> None:
     """The channel transform needs a power-of-two C (section III-B pads only
     the token axis); a token count must be at least 1."""
@@ -294,5 +359,7 @@ ALL_PINS = [
     pin_structure,
     pin_padding_dense,
     pin_padding_unit_gain,
+    pin_grad_dense,
+    pin_grad_finite_differences,
     pin_rejects_bad_shapes,
 ]

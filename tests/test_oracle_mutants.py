@@ -47,6 +47,14 @@ MUTANTS = {
     # the wrong N rows kept after the padded transform
     "crop_offset": ("channel_transform(z, P, C);\n        memcpy(y + b * N * C, z, ",
                     "channel_transform(z, P, C);\n        memcpy(y + b * N * C, z + (P - N) * C, "),
+    # gradient: dG accumulated from the wrong operand
+    "grad_operand": ("dg[i] += tx[i] * td[i];", "dg[i] += tx[i] * tx[i];"),
+    # gradient: dY transformed over channels only
+    "grad_dy_token_dropped": ("        channel_transform(td, P, C);\n        token_transform(td, P, C);",
+                              "        channel_transform(td, P, C);"),
+    # separable gradient: chain rule through exp forgotten
+    "grad_separable_chain": ("            s += dG[n * C + c] * G[n * C + c];\n        dg_t[n] = s;",
+                             "            s += dG[n * C + c];\n        dg_t[n] = s;"),
     # separable form: log gains used without exponentiation
     "separable_no_exp": ("z[n * C + c] *= exp(g_c[c]);", "z[n * C + c] *= g_c[c];"),
     # separable form: token gain indexed by channel
