@@ -156,6 +156,47 @@ WHTMIX_API int whtmix_forward_separable(const void *x, const float *log_gain_tok
                              int64_t B, int64_t N, int64_t C, int dtype,
                              void *stream, const whtmix_options *options);
 
+/*
+ * whtmix_backward -- gradients through whtmix_forward for an upstream
+ * gradient dy = dL/dy (the paper trains the gains, section IV-A).  With the
+ * orthonormal transforms T(v) = H_Npad vpad H_C of zero-padded slices:
+ *     dx[b] = H_N (G o T(dy[b])) H_C, first N rows (the mixer is
+ *             self-adjoint, so this is whtmix_forward applied to dy);
+ *     dgain = sum over b of T(x[b]) o T(dy[b])        ([N_pad][C] float32).
+ *
+ *   x, dy  device pointers, [B][N][C] elements of `dtype` (x is not read when
+ *          dgain is NULL).
+ *   gain   [N_pad][C] float32, as passed to the forward call.
+ *   dx     [B][N][C] of `dtype`, or NULL to skip; may be dy itself.
+ *   dgain  [N_pad][C] float32, overwritten (not accumulated), or NULL to skip.
+ * At least one of dx, dgain must be non-NULL.  No output may overlap an
+ * input or another output (except dx == dy).  With B == 0 dgain is filled
+ * with zeros.  The gain gradient is summed over the batch in a fixed order,
+ * so results are bitwise reproducible.  The call uses a float32 workspace of
+ * up to 2*B*N_pad*C (+ partial sums) floats; other conventions and options as
+ * whtmix_forward_ex (events: [0] before, [1] after the gain gradient, [2]
+ * after dx).
+ */
+WHTMIX_API int whtmix_backward(const void *x, const void *dy, const float *gain,
+                    void *dx, float *dgain, int64_t B, int64_t N, int64_t C,
+                    int dtype, void *stream, const whtmix_options *options);
+
+/*
+ * whtmix_backward_separable -- gradients through whtmix_forward_separable:
+ *     dx                as whtmix_backward with G[n][c] = exp(g_t[n] + g_c[c]),
+ *     d_log_gain_tokens[n]   = sum over c of dG[n][c] G[n][c]   ([N_pad]),
+ *     d_log_gain_channels[c] = sum over n of dG[n][c] G[n][c]   ([C]),
+ * (the chain rule through exp).  The two log-gain gradients are both NULL or
+ * both non-NULL; everything else as whtmix_backward.
+ */
+WHTMIX_API int whtmix_backward_separable(const void *x, const void *dy,
+                              const float *log_gain_tokens,
+                              const float *log_gain_channels, void *dx,
+                              float *d_log_gain_tokens,
+                              float *d_log_gain_channels, int64_t B,
+                              int64_t N, int64_t C, int dtype, void *stream,
+                              const whtmix_options *options);
+
 /* Fills *info with the plan whtmix_forward_ex would use.  Validates the
  * shape, dtype and options exactly as the forward call does (pointers are
  * not needed).  Returns a whtmix_status. */

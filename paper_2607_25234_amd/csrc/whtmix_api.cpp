@@ -247,6 +247,115 @@ int whtmix_forward_separable(const void *x, const float *log_gain_tokens,
                         log_gain_channels, y, B, N, C, dtype, stream, options);
 }
 
+}  // extern "C"
+
+namespace {
+
+struct Span {
+    uintptr_t p;
+    uint64_t n;
+};
+
+bool spans_overlap(Span a, Span b) { return a.p && b.p && overlaps(a.p, a.n, b.p, b.n); }
+
+int backward_impl(const void *x, const void *dy, int gain_kind, const float *gain,
+                  const float *gain_t, const float *gain_c, void *dx, float *dgain, float *dgt,
+                  float *dgc, int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                  const whtmix_options *options)
+{
+    Checked c;
+    int st = check_shape(B, N, C, dtype, options, &c);
+    if (st != WHTMIX_SUCCESS) return st;
+    const bool sep = gain_kind == whtmix::GAIN_LOG_SEPARABLE;
+    const bool want_dg = sep ? (dgt != nullptr || dgc != nullptr) : dgain != nullptr;
+    if (sep && (dgt == nullptr) != (dgc == nullptr)) return WHTMIX_ERROR_INVALID_VALUE;
+    if (!want_dg && !dx) return WHTMIX_ERROR_INVALID_VALUE;
+    if (sep ? (!gain_t || !gain_c) : !gain) return WHTMIX_ERROR_INVALID_VALUE;
+    if (B > 0 && (!dy || (want_dg && !x))) return WHTMIX_ERROR_INVALID_VALUE;
+    const uint64_t xy = (uint64_t)B * (uint64_t)N * (uint64_t)C * (uint64_t)c.elt;
+    const uint64_t P = (uint64_t)c.n_pad;
+    Span sx{B > 0 && want_dg ? reinterpret_cast<uintptr_t>(x) : 0, xy};
+    Span sdy{B > 0 ? reinterpret_cast<uintptr_t>(dy) : 0, xy};
+    Span sdx{B > 0 ? reinterpret_cast<uintptr_t>(dx) : 0, xy};
+    Span sg{reinterpret_cast<uintptr_t>(sep ? gain_t : gain), sep ? P * 4 : P * C * 4};
+    Span sgc{reinterpret_cast<uintptr_t>(sep ? gain_c : nullptr), (uint64_t)C * 4};
+    Span sdg{reinterpret_cast<uintptr_t>(dgain), P * C * 4};
+    Span sdgt{reinterpret_cast<uintptr_t>(dgt), P * 4};
+    Span sdgc{reinterpret_cast<uintptr_t>(dgc), (uint64_t)C * 4};
+    const Span inputs[] = {sx, sdy, sg, sgc};
+    const Span outputs[] = {sdx, sdg, sdgt, sdgc};
+    for (const Span &s : inputs)
+        if (s.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    for (const Span &s : outputs)
+        if (s.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    // No output may overlap an input or another output, except that dx may
+    // be dy itself (the gain gradient is computed before dx is written).
+    for (int i = 0; i < 4; ++i) {
+        const Span &o = outputs[i];
+        if (!o.p) continue;
+        for (int j = 0; j < 4; ++j) {
+            if (i == 0 && j == 1 && o.p == inputs[j].p) continue;
+            if (spans_overlap(o, inputs[j])) return WHTMIX_ERROR_INVALID_VALUE;
+        }
+        for (int j = 0; j < 4; ++j)
+            if (j != i && spans_overlap(o, outputs[j])) return WHTMIX_ERROR_INVALID_VALUE;
+    }
+    if (B == 0 && !want_dg) return WHTMIX_SUCCESS;
+
+    whtmix::BackwardArgs a{};
+    a.x = x;
+    a.dy = dy;
+    a.dx = B > 0 ? dx : nullptr;
+    a.gain_kind = gain_kind;
+    a.gain = gain;
+    a.gain_t = gain_t;
+    a.gain_c = gain_c;
+    a.dgain = dgain;
+    a.dgt = dgt;
+    a.dgc = dgc;
+    a.cbits = log2_exact(C);
+    a.B = B;
+    a.K = c.K;
+    a.nvalid = (uint32_t)(N * C);
+    a.dtype = dtype;
+    a.plan = c.plan;
+    a.stream = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < 4; ++i)
+        a.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
+    const whtmix::BackwardLayout lay = whtmix::backward_layout(c.plan, c.K, B, C, sep);
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    if (lay.floats > 0) {
+        st = get_workspace(stream, (int64_t)(lay.floats * 4), &a.ws);
+        if (st != WHTMIX_SUCCESS) return st;
+    }
+    hipError_t e = whtmix::launch_backward(a);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return WHTMIX_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+int whtmix_backward(const void *x, const void *dy, const float *gain, void *dx, float *dgain,
+                    int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                    const whtmix_options *options)
+{
+    return backward_impl(x, dy, whtmix::GAIN_FULL, gain, nullptr, nullptr, dx, dgain, nullptr,
+                         nullptr, B, N, C, dtype, stream, options);
+}
+
+int whtmix_backward_separable(const void *x, const void *dy, const float *log_gain_tokens,
+                              const float *log_gain_channels, void *dx,
+                              float *d_log_gain_tokens, float *d_log_gain_channels, int64_t B,
+                              int64_t N, int64_t C, int dtype, void *stream,
+                              const whtmix_options *options)
+{
+    return backward_impl(x, dy, whtmix::GAIN_LOG_SEPARABLE, nullptr, log_gain_tokens,
+                         log_gain_channels, dx, nullptr, d_log_gain_tokens, d_log_gain_channels,
+                         B, N, C, dtype, stream, options);
+}
+
 int whtmix_forward(const void *x, const float *gain, void *y, int64_t B, int64_t N, int64_t C,
                    int dtype, void *stream)
 {

@@ -1,0 +1,421 @@
+// WHTMix backward kernels for gfx950 (MI355X).
+//
+// The paper trains the mixer's gains (section IV-A).  For a loss with upstream
+// gradient dY, on the zero-padded flat slice of L = 2^K elements with the
+// orthonormal transform T = L^-1/2 H_L:
+//     dX = the mixer applied to dY        (self-adjoint: H symmetric, G
+//                                          diagonal) -- the forward kernels;
+//     dG = sum over b of T(x_b) o T(dy_b) (in the transform domain).
+// dG needs forward-only transforms of x and dy and a product summed over the
+// batch.  The batch is split into chunks; each workgroup accumulates its
+// chunk in registers and a fixed-order pass adds the chunks, so results do not
+// depend on scheduling (no atomics).
+//
+// For the separable log gains G[n][c] = exp(g_t[n] + g_c[c]):
+//     dg_t[n] = sum over c of dG[n][c] G[n][c],  dg_c[c] = sum over n of the same.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "whtmix_launch.h"
+#include "whtmix_plan.h"
+#include "whtmix_tile.h"
+
+namespace whtmix {
+namespace {
+
+using namespace tile;
+
+// Three-pass dG.  After OUTER_FWD of x and of dy over the A low bits, one
+// workgroup owns one workspace run (2^HB x 2^R elements) for a chunk of
+// slices: forward over the HB high bits for both operands, multiply,
+// accumulate; then 2^-K times the sum is stored at the run's positions of G.
+template <int A, int HB, int R>
+__global__ void __launch_bounds__(1 << (HB + R - VB))
+grad_middle_kernel(const float *__restrict__ wsx, const float *__restrict__ wsd,
+                   float *__restrict__ out, uint32_t nslices, uint32_t per_chunk)
+{
+    constexpr int M = HB + R;
+    using G = Groups<M, R>;
+    using Gain = GainMap<A, R>;
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t run = blockIdx.x & ((1u << (A - R)) - 1u);
+    const uint32_t chunk = blockIdx.x >> (A - R);
+    const uint32_t b0 = chunk * per_chunk;
+    const uint32_t b1 = min(b0 + per_chunk, nslices);
+    float acc[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        acc[k] = 0.0f;
+    for (uint32_t b = b0; b < b1; ++b) {   // uniform over the workgroup
+        const size_t off = ((size_t)b << (A + HB)) + ((size_t)run << M);
+        float vx[V], vd[V];
+        load_layout<G::TOP, ContigMap, float>(vx, buffer(wsx + off, (1u << M) * 4u), tau);
+        load_layout<G::TOP, ContigMap, float>(vd, buffer(wsd + off, (1u << M) * 4u), tau);
+        butterflies<G::JT, VB>(vx);
+        butterflies<G::JT, VB>(vd);
+        forward_groups<M, R, 0, G::TOP, true>(lds, vx, tau);
+        forward_groups<M, R, 0, G::TOP, true>(lds, vd, tau);
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            acc[k] = fmaf(vx[k], vd[k], acc[k]);
+    }
+    constexpr float scale = 1.0f / (float)(1u << (A + HB));
+    float *o = out + ((size_t)chunk << (A + HB)) + ((size_t)run << R) +
+               Gain::at(layout_base<G::SL>(tau));
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        o[Gain::at((uint32_t)k << G::SL)] = acc[k] * scale;
+}
+
+// Fused dG (2^11 <= L <= 2^15): one workgroup per chunk of slices, each
+// slice transformed whole.
+template <int K, typename T>
+__global__ void __launch_bounds__(1 << (K - VB))
+grad_fused_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ out,
+                  uint32_t nslices, uint32_t per_chunk, uint32_t nvalid)
+{
+    using G = Groups<K, 0>;
+    __shared__ float lds[pad(1u << K)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t chunk = blockIdx.x;
+    const uint32_t b0 = chunk * per_chunk;
+    const uint32_t b1 = min(b0 + per_chunk, nslices);
+    float acc[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        acc[k] = 0.0f;
+    for (uint32_t b = b0; b < b1; ++b) {
+        float vx[V], vd[V];
+        load_tile<G::TOP, K, T>(vx, x + (size_t)b * nvalid, nvalid, tau);
+        load_tile<G::TOP, K, T>(vd, dy + (size_t)b * nvalid, nvalid, tau);
+        butterflies<G::JT, VB>(vx);
+        butterflies<G::JT, VB>(vd);
+        forward_groups<K, 0, 0, G::TOP, true>(lds, vx, tau);
+        forward_groups<K, 0, 0, G::TOP, true>(lds, vd, tau);
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            acc[k] = fmaf(vx[k], vd[k], acc[k]);
+    }
+    constexpr float scale = 1.0f / (float)(1u << K);
+    float *o = out + ((size_t)chunk << K) + layout_base<G::SL>(tau);
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        o[(uint32_t)k << G::SL] = acc[k] * scale;
+}
+
+// In-place unnormalised butterfly of the L values in LDS (all threads).
+__device__ void lds_fwht(float *s, int L)
+{
+    for (int h = 1; h < L; h <<= 1) {
+        __syncthreads();
+        for (int p = threadIdx.x; p < L / 2; p += blockDim.x) {
+            const int i = ((p / h) * 2 * h) + (p % h);
+            const float a = s[i], c = s[i + h];
+            s[i] = a + c;
+            s[i + h] = a - c;
+        }
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ float widen(float v) { return v; }
+__device__ __forceinline__ float widen(__bf16 v) { return (float)v; }
+
+// Small dG (L <= 2^10): one 256-thread workgroup per chunk, stages in LDS.
+template <typename T>
+__global__ void __launch_bounds__(256)
+grad_small_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ out,
+                  int K, uint32_t nslices, uint32_t per_chunk, uint32_t nvalid)
+{
+    __shared__ float sx[1 << kMaxSmall], sd[1 << kMaxSmall], acc[1 << kMaxSmall];
+    const int L = 1 << K;
+    const uint32_t chunk = blockIdx.x;
+    const uint32_t b0 = chunk * per_chunk;
+    const uint32_t b1 = min(b0 + per_chunk, nslices);
+    for (int i = threadIdx.x; i < L; i += blockDim.x)
+        acc[i] = 0.0f;
+    for (uint32_t b = b0; b < b1; ++b) {
+        __syncthreads();
+        const size_t base = (size_t)b * nvalid;
+        for (int i = threadIdx.x; i < L; i += blockDim.x) {
+            sx[i] = (uint32_t)i < nvalid ? widen(x[base + i]) : 0.0f;
+            sd[i] = (uint32_t)i < nvalid ? widen(dy[base + i]) : 0.0f;
+        }
+        lds_fwht(sx, L);
+        lds_fwht(sd, L);
+        for (int i = threadIdx.x; i < L; i += blockDim.x)
+            acc[i] = fmaf(sx[i], sd[i], acc[i]);
+    }
+    __syncthreads();
+    const float scale = 1.0f / (float)L;
+    for (int i = threadIdx.x; i < L; i += blockDim.x)
+        out[((size_t)chunk << K) + i] = acc[i] * scale;
+}
+
+// out[f] = sum over chunks of part[chunk][f], in chunk order.
+__global__ void __launch_bounds__(256)
+sum_chunks_kernel(const float *__restrict__ part, float *__restrict__ out, uint64_t L,
+                  uint32_t nchunks)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t f = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; f < L; f += stride) {
+        float s = 0.0f;
+        for (uint32_t c = 0; c < nchunks; ++c)
+            s += part[c * L + f];
+        out[f] = s;
+    }
+}
+
+__global__ void __launch_bounds__(256)
+fill_zero_kernel(float *__restrict__ out, uint64_t n)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n; i += stride)
+        out[i] = 0.0f;
+}
+
+// dg_t[n] = sum_c dG[n][c] exp(g_t[n] + g_c[c]); one wavefront per row n.
+__global__ void __launch_bounds__(256)
+sep_rows_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
+                const float *__restrict__ gc, float *__restrict__ dgt, uint32_t P, uint32_t cbits)
+{
+    const uint32_t C = 1u << cbits;
+    const uint32_t row = blockIdx.x * 4u + (threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63u;
+    if (row >= P)
+        return;   // whole wavefront (no barriers in this kernel)
+    const float g = gt[row];
+    const float *d = dG + (size_t)row * C;
+    float s = 0.0f;
+    for (uint32_t c = lane; c < C; c += 64)
+        s = fmaf(d[c], expf(g + gc[c]), s);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        s += __shfl_down(s, off, 64);
+    if (lane == 0)
+        dgt[row] = s;
+}
+
+// Column partial sums over a block of rows: part[blk][c] =
+// sum over rows r in the block of dG[r][c] exp(g_t[r] + g_c[c]).
+__global__ void __launch_bounds__(256)
+sep_cols_partial_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
+                        const float *__restrict__ gc, float *__restrict__ part, uint32_t P,
+                        uint32_t cbits, uint32_t rows_per_block)
+{
+    const uint32_t C = 1u << cbits;
+    const uint32_t r0 = blockIdx.x * rows_per_block;
+    const uint32_t r1 = min(r0 + rows_per_block, P);
+    for (uint32_t c = threadIdx.x; c < C; c += blockDim.x) {
+        const float g = gc[c];
+        float s = 0.0f;
+        for (uint32_t r = r0; r < r1; ++r)
+            s = fmaf(dG[(size_t)r * C + c], expf(gt[r] + g), s);
+        part[(size_t)blockIdx.x * C + c] = s;
+    }
+}
+
+__global__ void __launch_bounds__(256)
+sep_cols_final_kernel(const float *__restrict__ part, float *__restrict__ dgc, uint32_t nblk,
+                      uint32_t C)
+{
+    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C)
+        return;
+    float s = 0.0f;
+    for (uint32_t b = 0; b < nblk; ++b)
+        s += part[(size_t)b * C + c];
+    dgc[c] = s;
+}
+
+inline hipError_t record(hipEvent_t ev, hipStream_t st)
+{
+    return ev ? hipEventRecord(ev, st) : hipSuccess;
+}
+
+inline uint32_t grid_for(uint64_t n)
+{
+    const uint64_t g = (n + 255) / 256;
+    return (uint32_t)(g < 4096 ? (g ? g : 1) : 4096);
+}
+
+// dG (2^-K-scaled sum over the batch) into `dst` ([2^K] floats).
+template <int K, typename T>
+hipError_t grad_three_pass(const T *x, const T *dy, float *dst, const BackwardArgs &a,
+                           const BackwardLayout &lay)
+{
+    constexpr Split sp = three_pass_split(K);
+    constexpr int A = sp.A, HB = sp.HB, R = sp.R;
+    const hipStream_t st = a.stream;
+    float *wsx = a.ws + lay.wsx;
+    float *wsd = a.ws + lay.wsd;
+    hipError_t e;
+    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, x, wsx, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, dy, wsd, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
+    hipLaunchKernelGGL((grad_middle_kernel<A, HB, R>), dim3(lay.nchunks << (A - R)),
+                       dim3(1u << (HB + R - VB)), 0, st, wsx, wsd, o, (uint32_t)a.B,
+                       lay.per_chunk);
+    return hipGetLastError();
+}
+
+template <int K, typename T>
+hipError_t grad_fused(const T *x, const T *dy, float *dst, const BackwardArgs &a,
+                      const BackwardLayout &lay)
+{
+    float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
+    hipLaunchKernelGGL((grad_fused_kernel<K, T>), dim3(lay.nchunks), dim3(1u << (K - VB)), 0,
+                       a.stream, x, dy, o, (uint32_t)a.B, lay.per_chunk, a.nvalid);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t grad_dispatch(const BackwardArgs &a, const BackwardLayout &lay, float *dst)
+{
+    const T *x = static_cast<const T *>(a.x);
+    const T *dy = static_cast<const T *>(a.dy);
+    hipError_t e = hipSuccess;
+    if (a.plan == PLAN_SMALL) {
+        float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
+        hipLaunchKernelGGL((grad_small_kernel<T>), dim3(lay.nchunks), dim3(256), 0, a.stream, x,
+                           dy, o, a.K, (uint32_t)a.B, lay.per_chunk, a.nvalid);
+        e = hipGetLastError();
+    } else if (a.plan == PLAN_FUSED) {
+        switch (a.K) {
+#define WHTMIX_GF_CASE(k) \
+    case k: e = grad_fused<k, T>(x, dy, dst, a, lay); break;
+            WHTMIX_GF_CASE(11) WHTMIX_GF_CASE(12) WHTMIX_GF_CASE(13) WHTMIX_GF_CASE(14)
+            WHTMIX_GF_CASE(15)
+#undef WHTMIX_GF_CASE
+        default: return hipErrorInvalidValue;
+        }
+    } else {
+        switch (a.K) {
+#define WHTMIX_G3_CASE(k) \
+    case k: e = grad_three_pass<k, T>(x, dy, dst, a, lay); break;
+            WHTMIX_G3_CASE(12) WHTMIX_G3_CASE(13) WHTMIX_G3_CASE(14) WHTMIX_G3_CASE(15)
+            WHTMIX_G3_CASE(16) WHTMIX_G3_CASE(17) WHTMIX_G3_CASE(18) WHTMIX_G3_CASE(19)
+            WHTMIX_G3_CASE(20) WHTMIX_G3_CASE(21) WHTMIX_G3_CASE(22) WHTMIX_G3_CASE(23)
+            WHTMIX_G3_CASE(24) WHTMIX_G3_CASE(25) WHTMIX_G3_CASE(26) WHTMIX_G3_CASE(27)
+            WHTMIX_G3_CASE(28) WHTMIX_G3_CASE(29) WHTMIX_G3_CASE(30)
+#undef WHTMIX_G3_CASE
+        default: return hipErrorInvalidValue;
+        }
+    }
+    if (e != hipSuccess || lay.nchunks <= 1) return e;
+    const uint64_t L = uint64_t(1) << a.K;
+    hipLaunchKernelGGL(sum_chunks_kernel, dim3(grid_for(L)), dim3(256), 0, a.stream,
+                       a.ws + lay.part, dst, L, lay.nchunks);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separable)
+{
+    BackwardLayout lay{};
+    const uint64_t L = uint64_t(1) << K;
+    uint64_t cursor = 0;
+    if (plan == PLAN_THREE_PASS) {
+        lay.wsx = cursor;
+        cursor += (uint64_t)B * L;
+        lay.wsd = cursor;
+        cursor += (uint64_t)B * L;
+    }
+    uint64_t want;
+    if (plan == PLAN_THREE_PASS) {
+        const Split sp = three_pass_split(K);
+        const uint64_t runs = uint64_t(1) << (sp.A - sp.R);
+        want = (1024 + runs - 1) / runs;
+    } else {
+        want = plan == PLAN_FUSED ? 1024 : 2048;
+    }
+    uint64_t nch = B < 1 ? 1 : ((uint64_t)B < want ? (uint64_t)B : want);
+    const uint64_t per = ((uint64_t)B + nch - 1) / nch;
+    nch = B < 1 ? 1 : ((uint64_t)B + per - 1) / per;
+    lay.per_chunk = (uint32_t)(per ? per : 1);
+    lay.nchunks = (uint32_t)nch;
+    if (lay.nchunks > 1) {
+        lay.part = cursor;
+        cursor += (uint64_t)lay.nchunks * L;
+    }
+    if (separable) {
+        const uint64_t P = L / (uint64_t)C;
+        lay.dg = cursor;
+        cursor += L;
+        uint64_t rpb = (P + 4095) / 4096;
+        if (rpb < 64) rpb = 64;
+        lay.rows_per_block = (uint32_t)rpb;
+        lay.col_blocks = (uint32_t)((P + rpb - 1) / rpb);
+        lay.colpart = cursor;
+        cursor += (uint64_t)lay.col_blocks * (uint64_t)C;
+    }
+    // The dX pass runs after dG and reuses the start of the workspace.
+    const uint64_t fwd = plan == PLAN_THREE_PASS ? (uint64_t)B * L : 0;
+    lay.floats = cursor > fwd ? cursor : fwd;
+    return lay;
+}
+
+hipError_t launch_backward(const BackwardArgs &a)
+{
+    const hipStream_t st = a.stream;
+    const bool separable = a.gain_kind == GAIN_LOG_SEPARABLE;
+    const BackwardLayout lay = backward_layout(a.plan, a.K, a.B, int64_t(1) << a.cbits, separable);
+    const uint64_t L = uint64_t(1) << a.K;
+    hipError_t e = record(a.events[0], st);
+    if (e != hipSuccess) return e;
+    const bool want_dg = separable ? (a.dgt != nullptr) : (a.dgain != nullptr);
+    if (want_dg) {
+        float *dst = separable ? a.ws + lay.dg : a.dgain;
+        if (a.B == 0) {
+            hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(L)), dim3(256), 0, st, dst, L);
+            e = hipGetLastError();
+        } else {
+            e = a.dtype == DTYPE_BF16 ? grad_dispatch<__bf16>(a, lay, dst)
+                                      : grad_dispatch<float>(a, lay, dst);
+        }
+        if (e != hipSuccess) return e;
+        if (separable) {
+            const uint32_t P = (uint32_t)(L >> a.cbits);
+            hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
+                               a.gain_c, a.dgt, P, (uint32_t)a.cbits);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hipLaunchKernelGGL(sep_cols_partial_kernel, dim3(lay.col_blocks), dim3(256), 0, st,
+                               dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P, (uint32_t)a.cbits,
+                               lay.rows_per_block);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            const uint32_t C = 1u << a.cbits;
+            hipLaunchKernelGGL(sep_cols_final_kernel, dim3((C + 255) / 256), dim3(256), 0, st,
+                               a.ws + lay.colpart, a.dgc, lay.col_blocks, C);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+    }
+    if ((e = record(a.events[1], st)) != hipSuccess) return e;
+    if (a.dx && a.B > 0) {
+        // dX = the mixer applied to dY, after dG so that dX may be dY itself
+        LaunchArgs f{};
+        f.x = a.dy;
+        f.y = a.dx;
+        f.gain_kind = a.gain_kind;
+        f.gain = a.gain;
+        f.gain_t = a.gain_t;
+        f.gain_c = a.gain_c;
+        f.cbits = a.cbits;
+        f.ws = a.ws;
+        f.B = a.B;
+        f.K = a.K;
+        f.nvalid = a.nvalid;
+        f.dtype = a.dtype;
+        f.plan = a.plan;
+        f.stream = st;
+        if ((e = launch(f)) != hipSuccess) return e;
+    }
+    return record(a.events[2], st);
+}
+
+}  // namespace whtmix

@@ -7,20 +7,8 @@
 // single gain product, and it is bound by memory traffic and VALU issue, not
 // by matrix throughput, so there is no MFMA here.
 //
-// Tile machinery.  A workgroup owns a tile of 2^M elements (11 <= M <= 15)
-// with tile-local index t.  Each of its 2^(M-5) threads holds 32 values in
-// registers.  A "layout S" gives thread tau the 32 values whose t has
-// register index k in bits [S, S+5) and tau in the remaining bits:
-//     t = (tau mod 2^S) | (k << S) | ((tau >> S) << (S + 5)).
-// In a layout, a butterfly over t-bit S+j is a register butterfly over bit j
-// of k.  The tile's bits are transformed in groups of up to five: the top
-// group [M-5, M) straight from the global load (lanes run over the low t
-// bits, so loads coalesce), then groups [W, W+5), [W+5, W+10), ... from the
-// bottom, each reached by writing the tile to LDS in the old layout and
-// reading it back in the new one.  LDS addresses are padded by one word per
-// 32 (p = t + t/32), which keeps every layout's reads and writes free of
-// bank conflicts and keeps each register's LDS address a constant offset from
-// a per-thread base.
+// The tile machinery (layouts, butterflies, LDS exchanges, memory access,
+// gains) is in whtmix_tile.h.
 //
 // Kernels:
 //   FUSED     whole slice in one tile: forward over all bits, gain, inverse.
@@ -34,311 +22,12 @@
 
 #include "whtmix_launch.h"
 #include "whtmix_plan.h"
+#include "whtmix_tile.h"
 
 namespace whtmix {
 namespace {
 
-constexpr int VB = 5;        // log2(values per thread)
-constexpr int V = 1 << VB;   // values per thread
-
-// ---------------------------------------------------------------- memory
-// Global memory is reached through raw buffer resources: a per-tile base and
-// byte extent in SGPRs, a 32-bit per-thread offset in one VGPR, and each
-// register's constant offset in an SGPR (soffset), so addressing costs no
-// 64-bit vector arithmetic and no per-register VGPRs.
-constexpr int kRawBufferWord3 = 0x00020000;   // gfx9-family raw buffer descriptor
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer(const void *base, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes,
-                                             kRawBufferWord3);
-}
-
-template <typename T>
-struct Elt;
-
-template <>
-struct Elt<float> {
-    static constexpr uint32_t bytes = 4;
-    __device__ static __forceinline__ float load(__amdgpu_buffer_rsrc_t r, uint32_t voff,
-                                                 uint32_t soff)
-    {
-        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
-    }
-    __device__ static __forceinline__ void store(float v, __amdgpu_buffer_rsrc_t r, uint32_t voff,
-                                                 uint32_t soff)
-    {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, voff, soff, 0);
-    }
-};
-
-template <>
-struct Elt<__bf16> {
-    static constexpr uint32_t bytes = 2;
-    // bf16 -> float32 is exact: the bf16 bits are the high half of the float
-    __device__ static __forceinline__ float load(__amdgpu_buffer_rsrc_t r, uint32_t voff,
-                                                 uint32_t soff)
-    {
-        const unsigned short u = __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
-        return __builtin_bit_cast(float, (uint32_t)u << 16);
-    }
-    // round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
-    __device__ static __forceinline__ void store(float v, __amdgpu_buffer_rsrc_t r, uint32_t voff,
-                                                 uint32_t soff)
-    {
-        const __bf16 h = (__bf16)v;
-        __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), r, voff, soff,
-                                              0);
-    }
-};
-
-// ---------------------------------------------------------------- layouts
-template <int S>
-__device__ __forceinline__ uint32_t layout_base(uint32_t tau)
-{
-    return (tau & ((1u << S) - 1u)) | ((tau >> S) << (S + VB));
-}
-
-__host__ __device__ constexpr uint32_t pad(uint32_t t) { return t + (t >> 5); }
-
-// Tile bits [WT, M) are transformed; [0, WT) are carried untouched.
-template <int M, int WT>
-struct Groups {
-    static constexpr int TOP = M - VB;
-    // first register bit of the top group that is a transformed tile bit
-    static constexpr int JT = WT > TOP ? WT - TOP : 0;
-    static constexpr int NBOT = TOP > WT ? (TOP - WT + VB - 1) / VB : 0;
-    static constexpr int S(int i) { return WT + VB * i; }
-    static constexpr int NB(int i) { return (TOP - S(i)) < VB ? (TOP - S(i)) : VB; }
-    static constexpr int SL = NBOT > 0 ? WT + VB * (NBOT - 1) : TOP;
-};
-
-// Butterflies over register bits [J0, J1): (a, b) -> (a + b, a - b).
-template <int J0, int J1>
-__device__ __forceinline__ void butterflies(float (&v)[V])
-{
-#pragma unroll
-    for (int j = J0; j < J1; ++j) {
-#pragma unroll
-        for (int k = 0; k < V; ++k) {
-            if (!(k & (1 << j))) {
-                const float a = v[k];
-                const float b = v[k | (1 << j)];
-                v[k] = a + b;
-                v[k | (1 << j)] = a - b;
-            }
-        }
-    }
-}
-
-// Re-lay the tile from layout SA to layout SB through LDS.  LEAD: wait first
-// for every thread's reads of the previous exchange (not needed the first time
-// the tile's LDS is used).
-template <int SA, int SB, bool LEAD = true>
-__device__ __forceinline__ void exchange(float *lds, float (&v)[V], uint32_t tau)
-{
-    const uint32_t pa = pad(layout_base<SA>(tau));
-    const uint32_t pb = pad(layout_base<SB>(tau));
-    if (LEAD)
-        __syncthreads();
-#pragma unroll
-    for (int k = 0; k < V; ++k)
-        lds[pa + pad((uint32_t)k << SA)] = v[k];
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < V; ++k)
-        v[k] = lds[pb + pad((uint32_t)k << SB)];
-}
-
-// Forward bottom groups I, I+1, ... starting from layout SPREV.
-template <int M, int WT, int I, int SPREV>
-__device__ __forceinline__ void forward_groups(float *lds, float (&v)[V], uint32_t tau)
-{
-    using G = Groups<M, WT>;
-    if constexpr (I < G::NBOT) {
-        constexpr int S = G::S(I);
-        exchange<SPREV, S, (I > 0)>(lds, v, tau);
-        butterflies<0, G::NB(I)>(v);
-        forward_groups<M, WT, I + 1, S>(lds, v, tau);
-    }
-}
-
-// Inverse bottom groups I, I-1, ..., 0 (data in group I's layout), ending in
-// the top layout.
-template <int M, int WT, int I>
-__device__ __forceinline__ void inverse_groups(float *lds, float (&v)[V], uint32_t tau)
-{
-    using G = Groups<M, WT>;
-    if constexpr (I >= 0) {
-        constexpr int S = G::S(I);
-        constexpr int SNEXT = I == 0 ? G::TOP : G::S(I - 1);
-        butterflies<0, G::NB(I)>(v);
-        exchange<S, SNEXT>(lds, v, tau);
-        inverse_groups<M, WT, I - 1>(lds, v, tau);
-    }
-}
-
-// ---------------------------------------------------------------- address maps
-// Each map sends tile-local t to an element offset from the tile's base by
-// moving bit fields, so map(a | b) = map(a) + map(b) for disjoint a, b: the
-// per-register offsets map(k << S) are compile-time constants.
-struct ContigMap {
-    __host__ __device__ static constexpr uint32_t at(uint32_t t) { return t; }
-};
-// Outer-pass chunk index lo (A bits) -> workspace: runs of 2^R elements, run
-// number lo >> R strided by a whole middle tile (2^(HB+R)).
-template <int HB, int R>
-struct RunMap {
-    __host__ __device__ static constexpr uint32_t at(uint32_t t)
-    {
-        return ((t >> R) << (HB + R)) | (t & ((1u << R) - 1u));
-    }
-};
-// Middle tile index (hi << R | run) -> flat slice index hi * 2^A + run.
-template <int A, int R>
-struct GainMap {
-    __host__ __device__ static constexpr uint32_t at(uint32_t t)
-    {
-        return ((t >> R) << A) | (t & ((1u << R) - 1u));
-    }
-};
-
-template <int S, class Map, typename T>
-__device__ __forceinline__ void load_layout(float (&v)[V], __amdgpu_buffer_rsrc_t r, uint32_t tau)
-{
-    const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
-#pragma unroll
-    for (int k = 0; k < V; ++k)
-        v[k] = Elt<T>::load(r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
-}
-
-template <int S, class Map, typename T>
-__device__ __forceinline__ void store_layout(const float (&v)[V], __amdgpu_buffer_rsrc_t r,
-                                             uint32_t tau)
-{
-    const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
-#pragma unroll
-    for (int k = 0; k < V; ++k)
-        Elt<T>::store(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
-}
-
-// Masked forms for the one tile of a zero-padded slice that straddles the
-// last real token: elements with tile index >= valid read as 0 and are not
-// stored.  Tiles wholly inside the slice take the unmasked forms; tiles wholly
-// in the padding skip their loads.  (The choice is uniform per workgroup.)
-template <int S, class Map, typename T>
-__device__ __forceinline__ void load_layout_masked(float (&v)[V], __amdgpu_buffer_rsrc_t r,
-                                                   uint32_t tau, uint32_t valid)
-{
-    const uint32_t tb = layout_base<S>(tau);
-    const uint32_t voff = Map::at(tb) * Elt<T>::bytes;
-#pragma unroll
-    for (int k = 0; k < V; ++k) {
-        const uint32_t t = tb | ((uint32_t)k << S);
-        v[k] = t < valid ? Elt<T>::load(r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes)
-                         : 0.0f;
-    }
-}
-
-template <int S, class Map, typename T>
-__device__ __forceinline__ void store_layout_masked(const float (&v)[V],
-                                                    __amdgpu_buffer_rsrc_t r, uint32_t tau,
-                                                    uint32_t valid)
-{
-    const uint32_t tb = layout_base<S>(tau);
-    const uint32_t voff = Map::at(tb) * Elt<T>::bytes;
-#pragma unroll
-    for (int k = 0; k < V; ++k) {
-        const uint32_t t = tb | ((uint32_t)k << S);
-        if (t < valid)
-            Elt<T>::store(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
-    }
-}
-
-// A contiguous tile of 2^M elements of x (type T) with `valid` real elements.
-template <int S, int M, typename T>
-__device__ __forceinline__ void load_tile(float (&v)[V], const T *base, uint32_t valid,
-                                          uint32_t tau)
-{
-    if (valid >= (1u << M)) {
-        load_layout<S, ContigMap, T>(v, buffer(base, (1u << M) * Elt<T>::bytes), tau);
-    } else if (valid == 0) {
-#pragma unroll
-        for (int k = 0; k < V; ++k)
-            v[k] = 0.0f;
-    } else {
-        load_layout_masked<S, ContigMap, T>(v, buffer(base, valid * Elt<T>::bytes), tau, valid);
-    }
-}
-
-template <int S, int M, typename T>
-__device__ __forceinline__ void store_tile(const float (&v)[V], T *base, uint32_t valid,
-                                           uint32_t tau)
-{
-    if (valid >= (1u << M))
-        store_layout<S, ContigMap, T>(v, buffer(base, (1u << M) * Elt<T>::bytes), tau);
-    else if (valid > 0)
-        store_layout_masked<S, ContigMap, T>(v, buffer(base, valid * Elt<T>::bytes), tau, valid);
-}
-
-// ---------------------------------------------------------------- gains
-// f is the flat index n*C + c of the (padded) slice.  The gain is read with
-// plain global loads: for its 128-byte-run pattern they measured markedly
-// faster than buffer loads on gfx950.  It is requested right after the data
-// tile so its latency overlaps the forward butterflies.
-
-// Joint per-frequency gain G[N_pad][C] (linear).
-struct FullGain {
-    const float *g;
-    template <int S, class Map>
-    __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
-    {
-        const float *p = g + f0 + Map::at(layout_base<S>(tau));
-#pragma unroll
-        for (int k = 0; k < V; ++k)
-            gv[k] = p[Map::at((uint32_t)k << S)];
-    }
-    __device__ __forceinline__ float at(uint32_t f) const { return g[f]; }
-};
-
-// The paper's parametrisation (eqs. (2)-(3)): log-domain gains g_t[N_pad]
-// over token frequencies and g_c[C] over channel frequencies; the gain of
-// frequency (n, c) is exp(g_t[n]) * exp(g_c[c]), computed as one exp of the
-// sum.
-struct LogSeparableGain {
-    const float *gt;
-    const float *gc;
-    uint32_t cbits;   // log2(C)
-    __device__ __forceinline__ float at(uint32_t f) const
-    {
-        return expf(gt[f >> cbits] + gc[f & ((1u << cbits) - 1u)]);
-    }
-    template <int S, class Map>
-    __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
-    {
-        const uint32_t fb = f0 + Map::at(layout_base<S>(tau));
-#pragma unroll
-        for (int k = 0; k < V; ++k)
-            gv[k] = at(fb + Map::at((uint32_t)k << S));
-    }
-};
-
-// v *= gain * 2^-K (gain already gathered in the same layout).
-template <int K>
-__device__ __forceinline__ void apply_gain(float (&v)[V], const float (&g)[V])
-{
-    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
-#pragma unroll
-    for (int k = 0; k < V; ++k)
-        v[k] *= g[k] * scale;
-}
-
-// Byte extent of a map over a tile of 2^M elements (largest offset + 1).
-template <class Map, int M, typename T>
-constexpr uint32_t extent_bytes()
-{
-    return (Map::at((1u << M) - 1u) + 1u) * Elt<T>::bytes;
-}
+using namespace tile;
 
 // ---------------------------------------------------------------- kernels
 // x and y hold `nvalid` = N*C elements per slice (N real tokens); the
@@ -363,35 +52,6 @@ fused_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, uint32_t nva
         inverse_groups<K, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<G::JT, VB>(v);
     store_tile<G::TOP, K, T>(v, y + base, nvalid, tau);
-}
-
-// Number of real elements in the outer tile hi of a slice.
-template <int A>
-__device__ __forceinline__ uint32_t tile_valid(uint32_t nvalid, uint32_t hi)
-{
-    const uint32_t start = hi << A;
-    return nvalid <= start ? 0u : min(nvalid - start, 1u << A);
-}
-
-// OUTER_FWD: block = b * 2^HB + hi; chunk x[b][hi * 2^A ...] -> workspace.
-template <int A, int HB, int R, typename T>
-__global__ void __launch_bounds__(1 << (A - VB))
-outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
-{
-    using G = Groups<A, 0>;
-    using Run = RunMap<HB, R>;
-    __shared__ float lds[pad(1u << A)];
-    const uint32_t tau = threadIdx.x;
-    const uint32_t blk = blockIdx.x;
-    const size_t b = blk >> HB;
-    const uint32_t hi = blk & ((1u << HB) - 1u);
-    float v[V];
-    load_tile<G::TOP, A, T>(v, x + b * nvalid + ((size_t)hi << A), tile_valid<A>(nvalid, hi),
-                            tau);
-    butterflies<0, VB>(v);
-    forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
-    store_layout<G::SL, Run, float>(
-        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
 }
 
 // MIDDLE: logical tile = run * B + b (the B slices sharing a gain tile are

@@ -33,4 +33,44 @@ struct LaunchArgs {
 // Enqueues the plan's kernels on a.stream.  Returns the first HIP error.
 hipError_t launch(const LaunchArgs &a);
 
+// A validated backward call.  dX = the mixer applied to dY (may be null);
+// the gain gradient goes to dgain (joint) or dgt/dgc (separable log gains),
+// any of which may be null to skip it.
+struct BackwardArgs {
+    const void *x;
+    const void *dy;
+    void *dx;
+    int gain_kind;          // GainKind
+    const float *gain;
+    const float *gain_t;
+    const float *gain_c;
+    float *dgain;           // [N_pad][C], overwritten
+    float *dgt;             // [N_pad], overwritten
+    float *dgc;             // [C], overwritten
+    int cbits;
+    float *ws;              // backward_layout(...).floats floats
+    int64_t B;
+    int K;
+    uint32_t nvalid;
+    int dtype;
+    int plan;
+    hipStream_t stream;
+    hipEvent_t events[4];   // [0] before, [1] after the gain gradient, [2] after dX
+};
+
+// Workspace plan of a backward call (offsets and sizes in floats).
+struct BackwardLayout {
+    uint64_t wsx, wsd;      // low-bit transforms of x and dy (three-pass)
+    uint64_t part;          // per-chunk partial dG sums (when nchunks > 1)
+    uint64_t dg;            // dG for the separable reductions
+    uint64_t colpart;       // column partial sums (separable)
+    uint32_t nchunks, per_chunk;
+    uint32_t rows_per_block, col_blocks;
+    uint64_t floats;        // total workspace
+};
+
+BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separable);
+
+hipError_t launch_backward(const BackwardArgs &a);
+
 }  // namespace whtmix

@@ -22,6 +22,8 @@ PLAN_NAMES = {v: k for k, v in PLANS.items()}
 
 # Every symbol include/whtmix.h declares.
 EXPORTS = (
+    "whtmix_backward",
+    "whtmix_backward_separable",
     "whtmix_forward",
     "whtmix_forward_ex",
     "whtmix_forward_separable",
@@ -78,6 +80,12 @@ def lib():
         L.whtmix_forward_separable.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                                ctypes.POINTER(Options)]
         L.whtmix_forward_separable.restype = ctypes.c_int
+        L.whtmix_backward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
+                                      ctypes.POINTER(Options)]
+        L.whtmix_backward.restype = ctypes.c_int
+        L.whtmix_backward_separable.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64,
+                                                ctypes.c_int, vp, ctypes.POINTER(Options)]
+        L.whtmix_backward_separable.restype = ctypes.c_int
         L.whtmix_plan_describe.argtypes = [i64, i64, i64, ctypes.c_int,
                                            ctypes.POINTER(Options), ctypes.POINTER(PlanInfo)]
         L.whtmix_plan_describe.restype = ctypes.c_int
@@ -218,6 +226,88 @@ def forward_separable(x, log_gain_tokens, log_gain_channels, out=None,
     if status != SUCCESS:
         raise WhtmixError(status, "whtmix_forward_separable")
     return out
+
+
+def backward_raw(x_ptr, dy_ptr, gain_ptr, dx_ptr, dgain_ptr, B, N, C, dtype, stream,
+                 plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_backward (0 for a skipped output); returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_backward(x_ptr, dy_ptr, gain_ptr, dx_ptr, dgain_ptr, B, N, C, dtype,
+                                 stream, ctypes.byref(opt))
+
+
+def backward_separable_raw(x_ptr, dy_ptr, gt_ptr, gc_ptr, dx_ptr, dgt_ptr, dgc_ptr, B, N, C,
+                           dtype, stream, plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_backward_separable; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_backward_separable(x_ptr, dy_ptr, gt_ptr, gc_ptr, dx_ptr, dgt_ptr,
+                                           dgc_ptr, B, N, C, dtype, stream, ctypes.byref(opt))
+
+
+def _same(a, x, what):
+    if a.shape != x.shape or a.dtype != x.dtype or a.device != x.device or not a.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous tensor like x")
+
+
+def backward(x, dy, gain, want_dx: bool = True, want_dgain: bool = True, dx=None,
+             plan: str | int = "auto", stream=None):
+    """Gradients through forward(x, gain) for the upstream gradient dy:
+    returns (dx, dgain); dx = the mixer applied to dy, dgain [N_pad, C]
+    float32 = sum_b T(x_b) o T(dy_b).  An output not wanted is None."""
+    import torch
+
+    xx, dt, _ = _check(x, x)
+    _same(dy, x, "dy")
+    B, N, C = xx.shape
+    _gain(gain, (padded_tokens(N), C), x, "gain")
+    if want_dx and dx is None:
+        dx = torch.empty_like(dy)
+    if dx is not None:
+        _same(dx, x, "dx")
+    dgain = torch.empty_like(gain) if want_dgain else None
+    if dx is None and dgain is None:
+        raise ValueError("nothing to compute")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = backward_raw(xx.data_ptr(), dy.data_ptr(), gain.data_ptr(),
+                              dx.data_ptr() if dx is not None else 0,
+                              dgain.data_ptr() if dgain is not None else 0, B, N, C, dt,
+                              st.cuda_stream, plan)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_backward")
+    return dx, dgain
+
+
+def backward_separable(x, dy, log_gain_tokens, log_gain_channels, want_dx: bool = True,
+                       want_dgains: bool = True, dx=None, plan: str | int = "auto",
+                       stream=None):
+    """Gradients through forward_separable: returns (dx, d_log_gain_tokens,
+    d_log_gain_channels); outputs not wanted are None."""
+    import torch
+
+    xx, dt, _ = _check(x, x)
+    _same(dy, x, "dy")
+    B, N, C = xx.shape
+    _gain(log_gain_tokens, (padded_tokens(N),), x, "log_gain_tokens")
+    _gain(log_gain_channels, (C,), x, "log_gain_channels")
+    if want_dx and dx is None:
+        dx = torch.empty_like(dy)
+    if dx is not None:
+        _same(dx, x, "dx")
+    dgt = torch.empty_like(log_gain_tokens) if want_dgains else None
+    dgc = torch.empty_like(log_gain_channels) if want_dgains else None
+    if dx is None and dgt is None:
+        raise ValueError("nothing to compute")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = backward_separable_raw(
+            xx.data_ptr(), dy.data_ptr(), log_gain_tokens.data_ptr(),
+            log_gain_channels.data_ptr(), dx.data_ptr() if dx is not None else 0,
+            dgt.data_ptr() if dgt is not None else 0, dgc.data_ptr() if dgc is not None else 0,
+            B, N, C, dt, st.cuda_stream, plan)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_backward_separable")
+    return dx, dgt, dgc
 
 
 def release_workspaces() -> None:

@@ -99,6 +99,41 @@ def test_separable_rejected_before_any_hip_call(kwargs, status):
     assert sep(**kwargs) == status
 
 
+def bwd(x=ALIGNED, dy=ALIGNED * 16, g=ALIGNED2, dx=ALIGNED * 64, dg=ALIGNED2 * 2, B=1, N=64,
+        C=64, dtype=0):
+    return whtmix.backward_raw(x, dy, g, dx, dg, B, N, C, dtype, 0)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(dx=0, dg=0), 1),                    # nothing to compute
+    (dict(dy=0), 1),
+    (dict(x=0), 1),                           # x needed for the gain gradient
+    (dict(g=0), 1),
+    (dict(dx=ALIGNED + 64), 1),               # dx overlaps x
+    (dict(dx=ALIGNED * 16 + 64), 1),          # dx partially overlaps dy
+    (dict(dg=ALIGNED * 16), 1),               # dgain inside dy
+    (dict(dg=ALIGNED2 + 256), 1),             # dgain overlaps the gain
+    (dict(dg=ALIGNED * 64), 1),               # dgain overlaps dx
+    (dict(dx=ALIGNED * 64 + 4), 4),
+    (dict(C=6), 2),
+    (dict(dtype=3), 3),
+])
+def test_backward_rejected_before_any_hip_call(kwargs, status):
+    assert bwd(**kwargs) == status
+
+
+def test_backward_separable_rejected_before_any_hip_call():
+    f = whtmix.backward_separable_raw
+    # one log-gain gradient without the other
+    assert f(ALIGNED, ALIGNED * 16, ALIGNED2, ALIGNED2 + 4096, 0, ALIGNED2 * 2, 0,
+             1, 64, 64, 0, 0) == 1
+    # nothing to compute
+    assert f(ALIGNED, ALIGNED * 16, ALIGNED2, ALIGNED2 + 4096, 0, 0, 0, 1, 64, 64, 0, 0) == 1
+    # token-gain gradient overlapping the channel gains
+    assert f(ALIGNED, ALIGNED * 16, ALIGNED2, ALIGNED2 + 4096, 0, ALIGNED2 + 4096 - 64,
+             ALIGNED2 * 2, 1, 64, 64, 0, 0) == 1
+
+
 def test_padded_plans():
     """Non-power-of-two token counts are zero-padded (section III-B)."""
     for N, C, P in [(3, 4, 4), (5, 1, 8), (9216, 64, 16384), (25600, 64, 32768),

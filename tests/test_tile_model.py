@@ -326,6 +326,112 @@ def test_padded_schedules(N, C, orc):
         assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
 
 
+def model_outer_fwd(x, K, split):
+    """outer_fwd_kernel over a batch: the low-bit transforms in the run layout."""
+    B = x.shape[0]
+    L = 1 << K
+    nvalid = x.shape[1] * x.shape[2]
+    A, HB, R = split
+    xs = x.reshape(B * nvalid)
+    ws = np.full(B * L, np.nan)
+    for blk in range(B << HB):
+        b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        T = Tile(A, 0)
+        valid = tile_valid(nvalid, hi, A)
+        t = T.idx(T.g.TOP)
+        v = np.zeros(t.shape)
+        m = t < valid
+        v[m] = xs[b * nvalid + (hi << A) + t[m]]
+        butterflies(v, 0, VB)
+        v = T.forward_groups(v, T.g.TOP)
+        ws[b * L + (hi << R) + run_map(T.idx(T.g.SL), HB, R)] = v
+    assert not np.isnan(ws).any()
+    return ws
+
+
+def chunking(B, want):
+    nch = min(B, want)
+    per = -(-B // nch)
+    return -(-B // per), per
+
+
+def simulate_grad_three_pass(x, dy, K, split):
+    """Model of the backward dG schedule: outer_fwd of x and dy, then
+    grad_middle_kernel over (chunk, run) blocks, then the chunk sum."""
+    B = x.shape[0]
+    L = 1 << K
+    A, HB, R = split
+    M = HB + R
+    wsx, wsd = model_outer_fwd(x, K, split), model_outer_fwd(dy, K, split)
+    runs = 1 << (A - R)
+    nch, per = chunking(B, -(-1024 // runs))
+    out = Access(nch * L)
+    part = np.full(nch * L, np.nan)
+    for blk in range(nch << (A - R)):
+        run, chunk = blk & (runs - 1), blk >> (A - R)
+        T = Tile(M, R)
+        acc = np.zeros((T.P, V))
+        for b in range(chunk * per, min(chunk * per + per, B)):
+            off = (b << (A + HB)) + (run << M)
+            vx = wsx[off + T.idx(T.g.TOP)].copy()
+            vd = wsd[off + T.idx(T.g.TOP)].copy()
+            butterflies(vx, T.g.JT, VB)
+            butterflies(vd, T.g.JT, VB)
+            vx = T.forward_groups(vx, T.g.TOP)
+            vd = T.forward_groups(vd, T.g.TOP)
+            acc += vx * vd
+        o = out.at((chunk << (A + HB)) + (run << R) + gain_map(T.idx(T.g.SL), A, R))
+        part[o] = acc / L
+    assert np.all(out.count == 1)
+    return part.reshape(nch, L).sum(axis=0)
+
+
+def simulate_grad_fused(x, dy, K):
+    B = x.shape[0]
+    L = 1 << K
+    nvalid = x.shape[1] * x.shape[2]
+    nch, per = chunking(B, 1024)
+    part = np.full(nch * L, np.nan)
+    out = Access(nch * L)
+    xs, ds = x.reshape(-1), dy.reshape(-1)
+    for chunk in range(nch):
+        T = Tile(K, 0)
+        acc = np.zeros((T.P, V))
+        for b in range(chunk * per, min(chunk * per + per, B)):
+            t = T.idx(T.g.TOP)
+            m = t < nvalid
+            vx, vd = np.zeros(t.shape), np.zeros(t.shape)
+            vx[m] = xs[b * nvalid + t[m]]
+            vd[m] = ds[b * nvalid + t[m]]
+            butterflies(vx, T.g.JT, VB)
+            butterflies(vd, T.g.JT, VB)
+            vx = T.forward_groups(vx, T.g.TOP)
+            vd = T.forward_groups(vd, T.g.TOP)
+            acc += vx * vd
+        part[out.at((chunk << K) + T.idx(T.g.SL))] = acc / L
+    assert np.all(out.count == 1)
+    return part.reshape(nch, L).sum(axis=0)
+
+
+@pytest.mark.parametrize("B,N,C", [(3, 64, 64), (5, 1000, 16), (2, 4096, 8), (40, 128, 128),
+                                   (2, 300, 64)])
+def test_grad_schedules(B, N, C, orc):
+    """The backward dG schedules reproduce the oracle's gain gradient."""
+    rng = np.random.default_rng(B * N + C)
+    P = 1 << (N - 1).bit_length()
+    K = (P * C).bit_length() - 1
+    x = rng.standard_normal((B, N, C))
+    dy = rng.standard_normal((B, N, C))
+    _, ref = orc.whtmix_grad(x, dy, np.ones((P, C)))
+    ref = ref.reshape(-1)
+    if K <= 15:
+        got = simulate_grad_fused(x, dy, K)
+        assert np.max(np.abs(got - ref)) < 1e-11 * np.max(np.abs(ref))
+    if K >= 12:
+        got = simulate_grad_three_pass(x, dy, K, three_pass_split(K))
+        assert np.max(np.abs(got - ref)) < 1e-11 * np.max(np.abs(ref))
+
+
 def test_middle_renumbering_is_a_permutation():
     for nblk in (8, 16, 24, 4096, 3 * 8):
         seen = sorted((blk & 7) * (nblk >> 3) + (blk >> 3) for blk in range(nblk))
