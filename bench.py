@@ -5,7 +5,8 @@
 
 A step is one whtmix_forward call (every kernel of the plan) over one batch of
 the workload (default: stereo64k_bf16, B=4, N=65536, C=128, bf16 in/out,
-float32 gain and arithmetic).  Inputs are resident in HBM before timing.
+float32 gain and arithmetic).  --op separable / backward / backward_separable
+time the other entry points the same way.  Inputs are resident in HBM before timing.
 Steps rotate over several input/output sets whose total footprint is at
 least twice the 256 MB Infinity Cache, so every step reads x and G from HBM.
 
@@ -53,14 +54,31 @@ def kernel_names(plan: str) -> list[str]:
             "fused": ["fused"], "small": ["small"]}[plan]
 
 
-def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int) -> list[int]:
-    """Bytes each kernel of the plan must move by its definition."""
+def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) -> list[int]:
+    """Bytes each kernel of the forward plan must move by its definition
+    (N here is the padded token count; gbytes: bytes of the gain read once)."""
     L = N * C
     if plan in ("fused", "small"):
-        return [B * L * 2 * s + 4 * L]
+        return [B * L * 2 * s + gbytes]
     return [B * L * (s + 4),           # read x, write float32 workspace
-            B * L * 8 + 4 * L,         # read + write workspace, read G once
+            B * L * 8 + gbytes,        # read + write workspace, read the gain once
             B * L * (4 + s)]           # read workspace, write y
+
+
+OPS = ("forward", "separable", "backward", "backward_separable")
+
+
+def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
+    """Ideal HBM bytes of one call: every input read once, every output
+    written once (P: padded token count, the gains' extent)."""
+    xy = B * N * C * s
+    if op == "forward":
+        return 2 * xy + 4 * P * C
+    if op == "separable":
+        return 2 * xy + 4 * (P + C)
+    if op == "backward":            # read x, dy, G; write dx, dG
+        return 3 * xy + 8 * P * C
+    return 3 * xy + 8 * (P + C)     # backward_separable
 
 
 def load_traffic(kernel: str, workload: str):
@@ -109,21 +127,28 @@ class HipEvents:
         self.events = []
 
 
-def cpu_baseline(w, x_slice, g, seconds: float) -> dict:
-    """The float64 CPU oracle, as it stands, on one batch slice, repeated until
-    about `seconds` of work; scaled to whole-workload GB/s."""
+def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
+    """The float64 CPU oracle, as it stands, on one batch slice of the same
+    operation, repeated until about `seconds` of work; scaled to the whole
+    workload's ideal bytes."""
     from oracle import oracle as oracle_mod
     orc = oracle_mod.Oracle()
+    x, g, gt, gc, dy = host0
+    call = {
+        "forward": lambda: orc.whtmix(x, g),
+        "separable": lambda: orc.whtmix_separable(x, gt, gc),
+        "backward": lambda: orc.whtmix_grad(x, dy, g),
+        "backward_separable": lambda: orc.whtmix_grad_separable(x, dy, gt, gc),
+    }[op]
     runs, t_total = 0, 0.0
     while runs == 0 or (t_total < seconds and runs < 50):
         t0 = time.perf_counter()
-        orc.whtmix(x_slice, g)
+        call()
         t_total += time.perf_counter() - t0
         runs += 1
-    t_slice = t_total / runs
-    t_workload = t_slice * w.B
+    t_workload = t_total / runs * w.B
     return {
-        "value": w.io_bytes / t_workload / 1e9,
+        "value": io_bytes / t_workload / 1e9,
         "unit": "GB/s",
         "tokens_per_s": w.B * w.N / t_workload,
         "cores": orc.threads(),
@@ -141,6 +166,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--plan", default="auto")
+    ap.add_argument("--op", default="forward", choices=OPS,
+                    help="forward (joint gain, the default), separable (log gains), "
+                         "backward, backward_separable")
     ap.add_argument("--sets", type=int, default=0,
                     help="input/output sets rotated over the steps (0 = auto)")
     ap.add_argument("--event-every", type=int, default=8,
@@ -173,9 +201,12 @@ def main() -> int:
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     dt_code = whtmix.DTYPE_BF16 if w.dtype == "bf16" else whtmix.DTYPE_F32
     plan = whtmix.plan_describe(w.B, w.N, w.C, w.dtype, args.plan)
-    set_bytes = w.io_bytes
-    nsets = args.sets or max(1, min(8, -(-2 * MALL_BYTES // set_bytes) + 1))
-    log(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}; plan {plan}; {nsets} input sets")
+    P = plan["padded_tokens"]
+    op = args.op
+    io_bytes = ideal_bytes(op, w.B, w.N, P, w.C, s)
+    nsets = args.sets or max(1, min(8, -(-2 * MALL_BYTES // io_bytes) + 1))
+    log(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}; op {op}; plan {plan}; "
+        f"{nsets} input sets")
 
     sets = []
     for i in range(nsets):
@@ -183,27 +214,52 @@ def main() -> int:
             x, g = workloads.inputs(w)
         else:
             x, g = workloads.draw(w.B, w.N, w.C, w.dtype, w.seed + 1000 * i, w.x_dist)
-        xd = torch.from_numpy(x).to(dev).to(tdt)
-        gd = torch.from_numpy(g).to(dev)
-        yd = torch.empty_like(xd)
-        sets.append((xd, gd, yd))
+        gt, gc = workloads.draw_log_gains(P, w.C, w.seed + 1000 * i + 1)
+        dy = None
+        if op.startswith("backward"):
+            dy, _ = workloads.draw(w.B, w.N, w.C, w.dtype, w.seed + 1000 * i + 2)
+        t = {"x": torch.from_numpy(x).to(dev).to(tdt), "g": torch.from_numpy(g).to(dev),
+             "gt": torch.from_numpy(gt).to(dev), "gc": torch.from_numpy(gc).to(dev)}
+        t["y"] = torch.empty_like(t["x"])
+        if dy is not None:
+            t["dy"] = torch.from_numpy(dy).to(dev).to(tdt)
+            t["dg"] = torch.empty_like(t["g"])
+            t["dgt"], t["dgc"] = torch.empty_like(t["gt"]), torch.empty_like(t["gc"])
+        sets.append(t)
         if i == 0:
-            x0_slice, g0 = x[0].copy(), g.copy()
+            host0 = (x[0].copy(), g.copy(), gt, gc, None if dy is None else dy[0].copy())
         del x, g
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream(dev)
     sptr = stream.cuda_stream
     hip = HipEvents()
-    nk = plan["kernels"]
-    names = kernel_names(plan["plan"])
+    if op.startswith("backward"):
+        nk, names = 2, ["gain_gradient", "dx"]
+    else:
+        nk, names = plan["kernels"], kernel_names(plan["plan"])
 
     def step(i, events=None):
-        xd, gd, yd = sets[i % nsets]
-        st = whtmix.forward_raw(xd.data_ptr(), gd.data_ptr(), yd.data_ptr(), w.B, w.N, w.C,
-                                dt_code, sptr, args.plan, events)
+        t = sets[i % nsets]
+        B, N, C = w.B, w.N, w.C
+        if op == "forward":
+            st = whtmix.forward_raw(t["x"].data_ptr(), t["g"].data_ptr(), t["y"].data_ptr(),
+                                    B, N, C, dt_code, sptr, args.plan, events)
+        elif op == "separable":
+            st = whtmix.forward_separable_raw(t["x"].data_ptr(), t["gt"].data_ptr(),
+                                              t["gc"].data_ptr(), t["y"].data_ptr(), B, N, C,
+                                              dt_code, sptr, args.plan, events)
+        elif op == "backward":
+            st = whtmix.backward_raw(t["x"].data_ptr(), t["dy"].data_ptr(), t["g"].data_ptr(),
+                                     t["y"].data_ptr(), t["dg"].data_ptr(), B, N, C, dt_code,
+                                     sptr, args.plan, events)
+        else:
+            st = whtmix.backward_separable_raw(
+                t["x"].data_ptr(), t["dy"].data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
+                t["y"].data_ptr(), t["dgt"].data_ptr(), t["dgc"].data_ptr(), B, N, C, dt_code,
+                sptr, args.plan, events)
         if st != whtmix.SUCCESS:
-            raise whtmix.WhtmixError(st, "whtmix_forward")
+            raise whtmix.WhtmixError(st, f"whtmix {op}")
 
     for i in range(args.warmup):
         step(i)
@@ -227,12 +283,19 @@ def main() -> int:
     hip.destroy()
 
     ms_per_step = wall * 1e3 / args.steps
-    gbs = w.io_bytes / (ms_per_step * 1e-3) / 1e9
+    gbs = io_bytes / (ms_per_step * 1e-3) / 1e9
     tokens = w.B * w.N / (ms_per_step * 1e-3)
-    alg = algorithmic_bytes(plan["plan"], w.B, w.N, w.C, s)
+    if op in ("forward", "separable"):
+        gbytes = 4 * P * w.C if op == "forward" else 4 * (P + w.C)
+        alg = algorithmic_bytes(plan["plan"], w.B, P, w.C, s, gbytes)
+    else:
+        # gain-gradient phase: read x and dy, write the gain gradient;
+        # dx phase: the forward mixer applied to dy
+        gb = 4 * P * w.C if op == "backward" else 4 * (P + w.C)
+        alg = [2 * w.B * w.N * w.C * s + gb, 2 * w.B * w.N * w.C * s + gb]
     dom = int(np.argmax(per_kernel))
     achieved = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9
-    traffic = load_traffic(names[dom], name)
+    traffic = load_traffic(names[dom], name) if op == "forward" else None
 
     out = {
         "metric": METRIC,
@@ -247,7 +310,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": name, "B": w.B, "N": w.N, "C": w.C,
+        "config": {"workload": name, "op": op, "B": w.B, "N": w.N, "C": w.C,
                    "io_dtype": w.dtype, "gain_dtype": "f32", "plan": plan["plan"],
                    "input_sets": nsets},
         "tokens_per_s": round(tokens, 1),
@@ -262,7 +325,7 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on one batch slice ...")
-        out["cpu_baseline"] = cpu_baseline(w, x0_slice, g0, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, op, host0, io_bytes, args.cpu_seconds)
         out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 4)
         out["cpu_baseline"]["tokens_per_s"] = round(out["cpu_baseline"]["tokens_per_s"], 1)
     else:

@@ -189,7 +189,7 @@ sep_rows_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
     const float *d = dG + (size_t)row * C;
     float s = 0.0f;
     for (uint32_t c = lane; c < C; c += 64)
-        s = fmaf(d[c], expf(g + gc[c]), s);
+        s = fmaf(d[c], __expf(g + gc[c]), s);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1)
         s += __shfl_down(s, off, 64);
@@ -197,36 +197,71 @@ sep_rows_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
         dgt[row] = s;
 }
 
-// Column partial sums over a block of rows: part[blk][c] =
-// sum over rows r in the block of dG[r][c] exp(g_t[r] + g_c[c]).
+// Sum of the 256 values in red[] (fixed tree order); result in red[0].
+__device__ __forceinline__ void block_sum_256(float *red)
+{
+    for (int w = 128; w > 0; w >>= 1) {
+        __syncthreads();
+        if ((int)threadIdx.x < w)
+            red[threadIdx.x] += red[threadIdx.x + w];
+    }
+    __syncthreads();
+}
+
+// Column partial sums of dG*G over a block of rows.  Block (strip, rblk)
+// covers rows [rblk*RB, ...) and columns [strip*256, ...).  With C <= 256 the
+// 256 threads hold 256/C rows of the C columns per step and their sums per
+// column are added in LDS; with C > 256 each thread owns one column of the
+// strip.  part[rblk][c] receives the block's sums.
 __global__ void __launch_bounds__(256)
 sep_cols_partial_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
                         const float *__restrict__ gc, float *__restrict__ part, uint32_t P,
                         uint32_t cbits, uint32_t rows_per_block)
 {
+    __shared__ float red[256];
     const uint32_t C = 1u << cbits;
+    const uint32_t tid = threadIdx.x;
     const uint32_t r0 = blockIdx.x * rows_per_block;
     const uint32_t r1 = min(r0 + rows_per_block, P);
-    for (uint32_t c = threadIdx.x; c < C; c += blockDim.x) {
-        const float g = gc[c];
-        float s = 0.0f;
-        for (uint32_t r = r0; r < r1; ++r)
-            s = fmaf(dG[(size_t)r * C + c], expf(gt[r] + g), s);
-        part[(size_t)blockIdx.x * C + c] = s;
+    const uint32_t cw = C < 256u ? C : 256u;              // columns per step
+    const uint32_t c = blockIdx.y * 256u + (tid & (cw - 1u));
+    const uint32_t rstep = 256u / cw;
+    float s = 0.0f;
+    if (tid < rstep * cw) {
+        const float gcc = gc[c];
+#pragma unroll 8
+        for (uint32_t r = r0 + tid / cw; r < r1; r += rstep)
+            s = fmaf(dG[(size_t)r * C + c], __expf(gt[r] + gcc), s);
     }
+    red[tid] = s;
+    __syncthreads();
+    if (cw < 256u) {
+        // add the rstep partial sums of each column: threads tid and tid + k*cw
+        for (uint32_t w = 128u; w >= cw; w >>= 1) {
+            if (tid < w)
+                red[tid] += red[tid + w];
+            __syncthreads();
+        }
+    }
+    if (tid < cw)
+        part[(size_t)blockIdx.x * C + c] = red[tid];
 }
 
+// dgc[c] = sum over row blocks of part[b][c]: one block per column, 256-way
+// strided sums then a fixed-order tree.
 __global__ void __launch_bounds__(256)
 sep_cols_final_kernel(const float *__restrict__ part, float *__restrict__ dgc, uint32_t nblk,
                       uint32_t C)
 {
-    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C)
-        return;
+    __shared__ float red[256];
+    const uint32_t c = blockIdx.x;
     float s = 0.0f;
-    for (uint32_t b = 0; b < nblk; ++b)
+    for (uint32_t b = threadIdx.x; b < nblk; b += 256)
         s += part[(size_t)b * C + c];
-    dgc[c] = s;
+    red[threadIdx.x] = s;
+    block_sum_256(red);
+    if (threadIdx.x == 0)
+        dgc[c] = red[0];
 }
 
 inline hipError_t record(hipEvent_t ev, hipStream_t st)
@@ -385,12 +420,13 @@ hipError_t launch_backward(const BackwardArgs &a)
             hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
                                a.gain_c, a.dgt, P, (uint32_t)a.cbits);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            hipLaunchKernelGGL(sep_cols_partial_kernel, dim3(lay.col_blocks), dim3(256), 0, st,
+            const uint32_t C = 1u << a.cbits;
+            hipLaunchKernelGGL(sep_cols_partial_kernel,
+                               dim3(lay.col_blocks, C > 256u ? C / 256u : 1u), dim3(256), 0, st,
                                dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P, (uint32_t)a.cbits,
                                lay.rows_per_block);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            const uint32_t C = 1u << a.cbits;
-            hipLaunchKernelGGL(sep_cols_final_kernel, dim3((C + 255) / 256), dim3(256), 0, st,
+            hipLaunchKernelGGL(sep_cols_final_kernel, dim3(C), dim3(256), 0, st,
                                a.ws + lay.colpart, a.dgc, lay.col_blocks, C);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }

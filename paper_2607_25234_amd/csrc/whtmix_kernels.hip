@@ -94,7 +94,7 @@ outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvali
     using Run = RunMap<HB, R>;
     __shared__ float lds[pad(1u << A)];
     const uint32_t tau = threadIdx.x;
-    const uint32_t blk = blockIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const uint32_t valid = tile_valid<A>(nvalid, hi);

@@ -436,3 +436,26 @@ def test_middle_renumbering_is_a_permutation():
     for nblk in (8, 16, 24, 4096, 3 * 8):
         seen = sorted((blk & 7) * (nblk >> 3) + (blk >> 3) for blk in range(nblk))
         assert seen == list(range(nblk))
+
+
+def outer_block(blk, nblk, R):
+    if R >= 5:
+        return blk
+    g = 1 << (5 - R)
+    if nblk % (8 * g):
+        return blk
+    return (blk & ~(8 * g - 1)) | ((blk & 7) * g) | ((blk >> 3) & (g - 1))
+
+
+@pytest.mark.parametrize("R", [0, 1, 2, 3, 4, 5, 6])
+def test_outer_renumbering(R):
+    """A permutation of the outer grid; with R < 5 the 2^(5-R) blocks that
+    share a 128-byte workspace line sit on one XCD (same block index mod 8)."""
+    for nblk in (2048, 4096, 8 * (1 << max(0, 5 - R)) * 3, 24, 7):
+        m = [outer_block(b, nblk, R) for b in range(nblk)]
+        assert sorted(m) == list(range(nblk))
+        if R < 5 and nblk % (8 << (5 - R)) == 0:
+            g = 1 << (5 - R)
+            inv = {v: b for b, v in enumerate(m)}
+            for hi0 in range(0, nblk, g):
+                assert len({inv[hi0 + j] % 8 for j in range(g)}) == 1
