@@ -53,6 +53,10 @@ def load(path: str = LIB):
     lib.oracle_whtmix_grad.restype = ctypes.c_int
     lib.oracle_whtmix_grad_separable.argtypes = [dp, dp, dp, dp, dp, dp, dp, L, L, L]
     lib.oracle_whtmix_grad_separable.restype = ctypes.c_int
+    lib.oracle_whtmix_module.argtypes = [dp, dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_module.restype = ctypes.c_int
+    lib.oracle_whtmix_module_separable.argtypes = [dp, dp, dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_module_separable.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     if path == LIB:
@@ -162,6 +166,42 @@ class Oracle:
         if rc != 0:
             raise ValueError(f"oracle_whtmix_grad_separable rejected {(B, N, C)}")
         return (dx[0] if squeeze else dx), dgt, dgc
+
+    def whtmix_module(self, x, w_in, g, w_out) -> np.ndarray:
+        """The full block, eqs. (1)-(4): Y = mixer(X W_in) W_out (joint gain)."""
+        x64 = _as_f64(x)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64 = x64[None]
+        B, N, C = x64.shape
+        wi, wo, g64 = _as_f64(w_in), _as_f64(w_out), _as_f64(g)
+        if wi.shape != (C, C) or wo.shape != (C, C) or g64.shape != (padded(N), C):
+            raise ValueError("w_in, w_out must be [C, C] and g [P, C]")
+        y = np.empty_like(x64)
+        rc = self.lib.oracle_whtmix_module(_dptr(x64), _dptr(wi), _dptr(g64), _dptr(wo),
+                                           _dptr(y), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_module rejected {(B, N, C)}")
+        return y[0] if squeeze else y
+
+    def whtmix_module_separable(self, x, w_in, g_t, g_c, w_out) -> np.ndarray:
+        """The full block with the paper's log-domain gains."""
+        x64 = _as_f64(x)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64 = x64[None]
+        B, N, C = x64.shape
+        wi, wo = _as_f64(w_in), _as_f64(w_out)
+        gt, gc = _as_f64(g_t).reshape(-1), _as_f64(g_c).reshape(-1)
+        if wi.shape != (C, C) or wo.shape != (C, C) or gt.shape != (padded(N),) \
+                or gc.shape != (C,):
+            raise ValueError("bad weight or gain shapes")
+        y = np.empty_like(x64)
+        rc = self.lib.oracle_whtmix_module_separable(_dptr(x64), _dptr(wi), _dptr(gt),
+                                                     _dptr(gc), _dptr(wo), _dptr(y), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_module_separable rejected {(B, N, C)}")
+        return y[0] if squeeze else y
 
     def fwht(self, v) -> np.ndarray:
         """Unnormalised Sylvester butterfly of a 1-D vector (H_n v, +/-1 H)."""

@@ -167,6 +167,67 @@ int oracle_whtmix_separable(const double *x, const double *g_t,
     return 0;
 }
 
+/* Z = X W for one slice: Z[n][j] = sum over i of X[n][i] W[i][j] (W is
+ * [C][C] row-major), the projections of eqs. (1) and (4). */
+static void project(const double *x, const double *w, double *z, long N, long C)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; ++n)
+        for (long j = 0; j < C; ++j) {
+            double s = 0.0;
+            for (long i = 0; i < C; ++i)
+                s += x[n * C + i] * w[i * C + j];
+            z[n * C + j] = s;
+        }
+}
+
+/* The full WHTMix block, eqs. (1)-(4): Z = X W_in; the token mixer on Z
+ * (joint gain g [P][C], or separable log gains when g is NULL and g_t, g_c
+ * are given); Y = Z W_out.  Same return convention as oracle_whtmix(). */
+static int module_impl(const double *x, const double *w_in, const double *g,
+                       const double *g_t, const double *g_c,
+                       const double *w_out, double *y, long B, long N, long C)
+{
+    if (!x || !w_in || !w_out || !y || B < 0 || N < 1 || !is_pow2(C))
+        return -1;
+    double *z = malloc((size_t)(N * C) * sizeof(double));
+    double *m = malloc((size_t)(N * C) * sizeof(double));
+    if (!z || !m) {
+        free(z);
+        free(m);
+        return -1;
+    }
+    int rc = 0;
+    for (long b = 0; b < B && rc == 0; ++b) {
+        project(x + b * N * C, w_in, z, N, C);                     /* eq. (1) */
+        rc = g ? oracle_whtmix(z, g, m, 1, N, C)                   /* eqs. (2)-(3) */
+               : oracle_whtmix_separable(z, g_t, g_c, m, 1, N, C);
+        if (rc == 0)
+            project(m, w_out, y + b * N * C, N, C);                /* eq. (4) */
+    }
+    free(z);
+    free(m);
+    return rc;
+}
+
+int oracle_whtmix_module(const double *x, const double *w_in, const double *g,
+                         const double *w_out, double *y, long B, long N, long C)
+{
+    if (!g)
+        return -1;
+    return module_impl(x, w_in, g, NULL, NULL, w_out, y, B, N, C);
+}
+
+int oracle_whtmix_module_separable(const double *x, const double *w_in,
+                                   const double *g_t, const double *g_c,
+                                   const double *w_out, double *y,
+                                   long B, long N, long C)
+{
+    if (!g_t || !g_c)
+        return -1;
+    return module_impl(x, w_in, NULL, g_t, g_c, w_out, y, B, N, C);
+}
+
 /* Gradients through the joint-gain mixer (the paper trains the gains,
  * section IV-A).  For a loss with upstream gradient dY = dL/dY, and
  *     T_x[b]  = H_P Xpad[b] H_C,   T_dy[b] = H_P dYpad[b] H_C

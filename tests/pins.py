@@ -18,7 +18,9 @@ that does not depend on the oracle's code:
 * zero padding of the token axis (section III-B) against dense products of
   explicitly padded matrices;
 * the backward pass (dX, dG and the separable log-gain gradients) against
-  dense products and against finite differences of the forward mixer.
+  dense products and against finite differences of the forward mixer;
+* the full block of eqs. (1)-(4) (projections W_in, W_out around the mixer)
+  against dense products.
 
 The same functions run against the real oracle (``test_oracle_pins.py``) and
 against deliberately broken copies of it (``test_oracle_mutants.py``), which
@@ -334,6 +336,29 @@ def pin_grad_finite_differences(o) -> None:
         assert abs(fd - dgc[c]) < 1e-7 * max(1.0, abs(fd)), c
 
 
+def pin_module_dense(o) -> None:
+    """The full block of eqs. (1)-(4) with dense matrices: the projections are
+    plain matrix products around the (padded) mixer, Y = M(X W_in) W_out,
+    for both gain forms; identity weights reduce it to the mixer."""
+    rng = np.random.default_rng(113)
+    for (B, N, C) in [(2, 8, 4), (1, 5, 8), (3, 16, 16), (2, 3, 2)]:
+        P = 1 << (N - 1).bit_length()
+        Hp, Hc = _hadamard_orth(P), _hadamard_orth(C)
+        x = rng.standard_normal((B, N, C))
+        wi = rng.standard_normal((C, C)) / np.sqrt(C)
+        wo = rng.standard_normal((C, C)) / np.sqrt(C)
+        g = rng.uniform(0.5, 1.5, (P, C))
+        mix = lambda z, G: (Hp @ (G * (Hp @ _pad_rows(z, P) @ Hc)) @ Hc)[:N]
+        ref = np.stack([mix(xb @ wi, g) @ wo for xb in x])
+        assert _rel(o.whtmix_module(x, wi, g, wo), ref) < 1e-12, (B, N, C)
+        gt, gc = rng.normal(0, 0.3, P), rng.normal(0, 0.3, C)
+        G = np.outer(np.exp(gt), np.exp(gc))
+        ref = np.stack([mix(xb @ wi, G) @ wo for xb in x])
+        assert _rel(o.whtmix_module_separable(x, wi, gt, gc, wo), ref) < 1e-12, (B, N, C)
+        eye = np.eye(C)
+        assert _rel(o.whtmix_module(x, eye, g, eye), o.whtmix(x, g)) < 1e-13
+
+
 def pin_rejects_bad_shapes(o) -> None:
     """The channel transform needs a power-of-two C (section III-B pads only
     the token axis); a token count must be at least 1."""
@@ -361,5 +386,6 @@ ALL_PINS = [
     pin_padding_unit_gain,
     pin_grad_dense,
     pin_grad_finite_differences,
+    pin_module_dense,
     pin_rejects_bad_shapes,
 ]

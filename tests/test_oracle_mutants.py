@@ -55,6 +55,12 @@ MUTANTS = {
     # separable gradient: chain rule through exp forgotten
     "grad_separable_chain": ("            s += dG[n * C + c] * G[n * C + c];\n        dg_t[n] = s;",
                              "            s += dG[n * C + c];\n        dg_t[n] = s;"),
+    # projection with the weight transposed
+    "projection_transposed": ("s += x[n * C + i] * w[i * C + j];",
+                              "s += x[n * C + i] * w[j * C + i];"),
+    # W_out applied to the mixer's input instead of its output
+    "projection_order": ("project(m, w_out, y + b * N * C, N, C);",
+                         "project(z, w_out, y + b * N * C, N, C);"),
     # separable form: log gains used without exponentiation
     "separable_no_exp": ("z[n * C + c] *= exp(g_c[c]);", "z[n * C + c] *= g_c[c];"),
     # separable form: token gain indexed by channel
