@@ -168,17 +168,22 @@ int oracle_whtmix_separable(const double *x, const double *g_t,
 }
 
 /* Z = X W for one slice: Z[n][j] = sum over i of X[n][i] W[i][j] (W is
- * [C][C] row-major), the projections of eqs. (1) and (4). */
+ * [C][C] row-major), the projections of eqs. (1) and (4).  Each Z[n][j] is
+ * summed over i in ascending order; the loops run i outside j only so that W
+ * is read along its rows. */
 static void project(const double *x, const double *w, double *z, long N, long C)
 {
 #pragma omp parallel for schedule(static)
-    for (long n = 0; n < N; ++n)
-        for (long j = 0; j < C; ++j) {
-            double s = 0.0;
-            for (long i = 0; i < C; ++i)
-                s += x[n * C + i] * w[i * C + j];
-            z[n * C + j] = s;
+    for (long n = 0; n < N; ++n) {
+        double *zn = z + n * C;
+        for (long j = 0; j < C; ++j)
+            zn[j] = 0.0;
+        for (long i = 0; i < C; ++i) {
+            const double xi = x[n * C + i];
+            for (long j = 0; j < C; ++j)
+                zn[j] += xi * w[i * C + j];
         }
+    }
 }
 
 /* The full WHTMix block, eqs. (1)-(4): Z = X W_in; the token mixer on Z

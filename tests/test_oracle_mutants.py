@@ -56,8 +56,8 @@ MUTANTS = {
     "grad_separable_chain": ("            s += dG[n * C + c] * G[n * C + c];\n        dg_t[n] = s;",
                              "            s += dG[n * C + c];\n        dg_t[n] = s;"),
     # projection with the weight transposed
-    "projection_transposed": ("s += x[n * C + i] * w[i * C + j];",
-                              "s += x[n * C + i] * w[j * C + i];"),
+    "projection_transposed": ("zn[j] += xi * w[i * C + j];",
+                              "zn[j] += xi * w[j * C + i];"),
     # W_out applied to the mixer's input instead of its output
     "projection_order": ("project(m, w_out, y + b * N * C, N, C);",
                          "project(z, w_out, y + b * N * C, N, C);"),
