@@ -70,7 +70,8 @@ typedef enum whtmix_status {
     WHTMIX_ERROR_OUT_OF_MEMORY = 5,    /* workspace allocation failed */
     WHTMIX_ERROR_HIP = 6,              /* HIP runtime / launch error; text in
                                           whtmix_last_error() */
-    WHTMIX_ERROR_TOO_LARGE = 7         /* N_pad*C > 2^30 or sizes overflow */
+    WHTMIX_ERROR_TOO_LARGE = 7         /* N_pad*C > 2^30, sizes overflow, or
+                                          module C > 4096 */
 } whtmix_status;
 
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
@@ -196,6 +197,49 @@ WHTMIX_API int whtmix_backward_separable(const void *x, const void *dy,
                               float *d_log_gain_channels, int64_t B,
                               int64_t N, int64_t C, int dtype, void *stream,
                               const whtmix_options *options);
+
+/*
+ * whtmix_module_forward -- the whole block of section III-B, eqs. (1)-(4),
+ * with the joint gain:
+ *     Z = X[b] W_in;   Z <- H_N (G o (H_N Z H_C)) H_C;   Y[b] = Z W_out
+ * (Z zero-padded to N_pad rows before H_N, Y cropped to the first N rows),
+ * the drop-in replacement of the self-attention block with its projections.
+ *
+ *   x      [B][N][C] elements of `dtype`; may equal y exactly (in place).
+ *   w_in   [C][C] elements of `dtype`, row-major: Z[n][j] = sum_i X[n][i]
+ *          W_in[i][j].
+ *   gain   [N_pad][C] float32 linear gains (as whtmix_forward).
+ *   w_out  [C][C] elements of `dtype`: Y[n][j] = sum_i Z[n][i] W_out[i][j].
+ *   y      [B][N][C] elements of `dtype` (written).
+ * C is a power of two <= 4096 (WHTMIX_ERROR_TOO_LARGE above).  Inputs must
+ * not overlap y except x == y.  Arithmetic is float32: for bf16 the products
+ * X W_in are exact, Z' W_out uses a two-term bf16 split of Z' (relative
+ * residual below 2^-17), and y is rounded to nearest even once.  For
+ * 16 <= C <= 128 the projections run on the matrix cores inside the mixer's
+ * first and last kernels (three kernels plus a small weight-repacking kernel
+ * for N_pad*C > 2^15); other C run separate projection kernels around the
+ * float32 mixer.  Workspace: the mixer's, plus 2*C*C elements of packed
+ * weights or B*N*C floats of Z.  Other conventions, plans and options as
+ * whtmix_forward_ex (events: for the three-pass plan around each of its
+ * three passes, otherwise [0] before and [1] after the call's kernels).
+ */
+WHTMIX_API int whtmix_module_forward(const void *x, const void *w_in,
+                          const float *gain, const void *w_out, void *y,
+                          int64_t B, int64_t N, int64_t C, int dtype,
+                          void *stream, const whtmix_options *options);
+
+/*
+ * whtmix_module_forward_separable -- whtmix_module_forward with the paper's
+ * log-domain gains (eqs. (2)-(3)): log_gain_tokens [N_pad] and
+ * log_gain_channels [C] float32, as whtmix_forward_separable.
+ */
+WHTMIX_API int whtmix_module_forward_separable(const void *x, const void *w_in,
+                                    const float *log_gain_tokens,
+                                    const float *log_gain_channels,
+                                    const void *w_out, void *y, int64_t B,
+                                    int64_t N, int64_t C, int dtype,
+                                    void *stream,
+                                    const whtmix_options *options);
 
 /* Fills *info with the plan whtmix_forward_ex would use.  Validates the
  * shape, dtype and options exactly as the forward call does (pointers are

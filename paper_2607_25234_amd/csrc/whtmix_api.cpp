@@ -333,6 +333,79 @@ int backward_impl(const void *x, const void *dy, int gain_kind, const float *gai
     return WHTMIX_SUCCESS;
 }
 
+int module_impl(const void *x, const void *w_in, int gain_kind, const float *gain,
+                const float *gain_t, const float *gain_c, const void *w_out, void *y, int64_t B,
+                int64_t N, int64_t C, int dtype, void *stream, const whtmix_options *options)
+{
+    Checked c;
+    int st = check_shape(B, N, C, dtype, options, &c);
+    if (st != WHTMIX_SUCCESS) return st;
+    const int cbits = log2_exact(C);
+    if (cbits > whtmix::kModuleMaxCbits) return WHTMIX_ERROR_TOO_LARGE;
+    if (B == 0) return WHTMIX_SUCCESS;
+    const bool full = gain_kind == whtmix::GAIN_FULL;
+    if (!x || !y || !w_in || !w_out || (full ? !gain : (!gain_t || !gain_c)))
+        return WHTMIX_ERROR_INVALID_VALUE;
+    const uint64_t xy = (uint64_t)B * (uint64_t)N * (uint64_t)C * (uint64_t)c.elt;
+    const uint64_t wb = (uint64_t)C * (uint64_t)C * (uint64_t)c.elt;
+    const uint64_t P = (uint64_t)c.n_pad;
+    const Span sy{reinterpret_cast<uintptr_t>(y), xy};
+    const Span inputs[] = {{reinterpret_cast<uintptr_t>(x), xy},
+                           {reinterpret_cast<uintptr_t>(w_in), wb},
+                           {reinterpret_cast<uintptr_t>(w_out), wb},
+                           {reinterpret_cast<uintptr_t>(full ? gain : gain_t),
+                            full ? P * (uint64_t)C * 4 : P * 4},
+                           {reinterpret_cast<uintptr_t>(full ? nullptr : gain_c),
+                            (uint64_t)C * 4}};
+    if (sy.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    for (const Span &s : inputs)
+        if (s.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    // y may be x itself; no other overlap with an input.
+    for (int i = 0; i < 5; ++i) {
+        if (i == 0 && inputs[i].p == sy.p) continue;
+        if (spans_overlap(sy, inputs[i])) return WHTMIX_ERROR_INVALID_VALUE;
+    }
+
+    whtmix::ModuleArgs m{};
+    m.x = x;
+    m.w_in = w_in;
+    m.w_out = w_out;
+    m.y = y;
+    m.gain_kind = gain_kind;
+    m.gain = gain;
+    m.gain_t = gain_t;
+    m.gain_c = gain_c;
+    m.cbits = cbits;
+    m.B = B;
+    m.K = c.K;
+    m.nvalid = (uint32_t)(N * C);
+    m.dtype = dtype;
+    m.plan = c.plan;
+    m.stream = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < 4; ++i)
+        m.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
+    const int path = whtmix::module_path(c.plan, cbits);
+    // workspace: mixer (THREE_PASS), then packed weights or Z, 256-byte aligned
+    const int64_t mix = path == whtmix::MODULE_SMALL ? 0 : c.ws_bytes;
+    const int64_t extra = path == whtmix::MODULE_FUSED_MFMA ? (int64_t)(2 * wb)
+                          : path == whtmix::MODULE_UNFUSED  ? B * N * C * 4
+                                                            : 0;
+    const int64_t off = (mix + 255) / 256 * 256;
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    float *ws = nullptr;
+    if (off + extra > 0) {
+        st = get_workspace(stream, off + extra, &ws);
+        if (st != WHTMIX_SUCCESS) return st;
+    }
+    m.ws = mix > 0 ? ws : nullptr;
+    void *tail = ws ? static_cast<void *>(reinterpret_cast<char *>(ws) + off) : nullptr;
+    if (path == whtmix::MODULE_FUSED_MFMA) m.wpack = tail;
+    if (path == whtmix::MODULE_UNFUSED) m.z = static_cast<float *>(tail);
+    hipError_t e = whtmix::launch_module(m);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return WHTMIX_SUCCESS;
+}
+
 }  // namespace
 
 extern "C" {
@@ -356,6 +429,23 @@ int whtmix_backward_separable(const void *x, const void *dy, const float *log_ga
                          B, N, C, dtype, stream, options);
 }
 
+int whtmix_module_forward(const void *x, const void *w_in, const float *gain, const void *w_out,
+                          void *y, int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                          const whtmix_options *options)
+{
+    return module_impl(x, w_in, whtmix::GAIN_FULL, gain, nullptr, nullptr, w_out, y, B, N, C,
+                       dtype, stream, options);
+}
+
+int whtmix_module_forward_separable(const void *x, const void *w_in, const float *log_gain_tokens,
+                                    const float *log_gain_channels, const void *w_out, void *y,
+                                    int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                                    const whtmix_options *options)
+{
+    return module_impl(x, w_in, whtmix::GAIN_LOG_SEPARABLE, nullptr, log_gain_tokens,
+                       log_gain_channels, w_out, y, B, N, C, dtype, stream, options);
+}
+
 int whtmix_forward(const void *x, const float *gain, void *y, int64_t B, int64_t N, int64_t C,
                    int dtype, void *stream)
 {
@@ -373,7 +463,7 @@ const char *whtmix_status_string(int status)
     case WHTMIX_ERROR_OUT_OF_MEMORY: return "workspace allocation failed";
     case WHTMIX_ERROR_HIP: return "HIP runtime error";
     case WHTMIX_ERROR_TOO_LARGE:
-        return "shape too large (N_pad*C <= 2^30, B*N_pad*C <= 2^37)";
+        return "shape too large (N_pad*C <= 2^30, B*N_pad*C <= 2^37, module C <= 4096)";
     default: return "unknown status";
     }
 }

@@ -227,6 +227,32 @@ hipError_t dispatch(const LaunchArgs &a, Gain gain)
     }
 }
 
+template <int K, class Gain>
+hipError_t launch_middle_k(const LaunchArgs &a, Gain gain)
+{
+    constexpr Split sp = three_pass_split(K);
+    hipLaunchKernelGGL((middle_kernel<sp.A, sp.HB, sp.R, Gain>),
+                       dim3((uint32_t)(a.B << (sp.A - sp.R))), dim3(1u << (sp.HB + sp.R - VB)), 0,
+                       a.stream, a.ws, gain, (uint32_t)a.B);
+    return hipGetLastError();
+}
+
+template <class Gain>
+hipError_t dispatch_middle(const LaunchArgs &a, Gain gain)
+{
+    switch (a.K) {
+#define WHTMIX_MID_CASE(k) \
+    case k: return launch_middle_k<k, Gain>(a, gain);
+        WHTMIX_MID_CASE(12) WHTMIX_MID_CASE(13) WHTMIX_MID_CASE(14) WHTMIX_MID_CASE(15)
+        WHTMIX_MID_CASE(16) WHTMIX_MID_CASE(17) WHTMIX_MID_CASE(18) WHTMIX_MID_CASE(19)
+        WHTMIX_MID_CASE(20) WHTMIX_MID_CASE(21) WHTMIX_MID_CASE(22) WHTMIX_MID_CASE(23)
+        WHTMIX_MID_CASE(24) WHTMIX_MID_CASE(25) WHTMIX_MID_CASE(26) WHTMIX_MID_CASE(27)
+        WHTMIX_MID_CASE(28) WHTMIX_MID_CASE(29) WHTMIX_MID_CASE(30)
+#undef WHTMIX_MID_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
 template <typename T>
 hipError_t dispatch_gain(const LaunchArgs &a)
 {
@@ -236,6 +262,13 @@ hipError_t dispatch_gain(const LaunchArgs &a)
 }
 
 }  // namespace
+
+hipError_t launch_middle(const LaunchArgs &a)
+{
+    if (a.gain_kind == GAIN_LOG_SEPARABLE)
+        return dispatch_middle(a, LogSeparableGain{a.gain_t, a.gain_c, (uint32_t)a.cbits});
+    return dispatch_middle(a, FullGain{a.gain});
+}
 
 hipError_t launch(const LaunchArgs &a)
 {

@@ -1,0 +1,857 @@
+// The whole WHTMix block (section III-B, eqs. (1)-(4)) for gfx950:
+//     Z = X W_in;   Z <- mixer(Z);   Y = Z W_out
+// with the projections fused into the mixer's first and last kernels as an
+// MFMA prologue and epilogue, so Z never makes an extra trip through HBM.
+//
+// Projections (C = 2^CB channels, 16 <= C <= 128):
+//   * bf16: v_mfma_f32_16x16x16_bf16.  X W_in multiplies bf16 by bf16, which
+//     is exact in the fp32 accumulator.  Z' W_out has an fp32 left operand:
+//     it is split as Z' = hi + lo (two bf16, hi = RNE(Z'), lo = RNE(Z' - hi),
+//     which leaves a residual below 2^-17 |Z'|) and multiplied in two MFMAs.
+//   * fp32: v_mfma_f32_16x16x4_f32.
+//   The contraction order over k is free, so each lane's k values are chosen
+//   to make its loads of X 16-byte pieces and its register reads contiguous.
+//
+// Register layouts (whtmix_tile.h defines "layout S").  With the lane layout of
+// the 16x16 MFMA result (lane = 16*q + j holds rows 4q + r, r = 0..3, of
+// column j), the fragments of Z = X W_in for a wave's 16*2^(7-CB) tokens are
+// exactly layout 4 (registers hold tile bits [4, 9)) after a renumbering of
+// registers, for every C in [16, 128]: the prologue feeds the transform with
+// no extra LDS pass.  The epilogue computes Y^T = W_out^T Z'^T, whose right
+// operand wants lane j on a token and lanes q on channel groups; the last
+// inverse exchange delivers that "epilogue layout" directly (Epi below).
+// The weights are repacked once per call into the MFMA operand order, staged
+// whole into LDS by each workgroup and read as one 8- or 16-byte LDS load per
+// lane per MFMA.
+//
+// Plans (the mixer's, whtmix_plan.h):
+//   FUSED       K <= 15: one workgroup per slice, prologue + mixer + epilogue.
+//   THREE_PASS  prologue in the first outer pass, the unchanged middle pass,
+//               epilogue in the second outer pass.
+//   SMALL       K <= 10: one LDS-resident workgroup per slice, VALU products.
+//   UNFUSED     any other C: projection kernels around the fp32 mixer.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "whtmix_launch.h"
+#include "whtmix_plan.h"
+#include "whtmix_tile.h"
+
+namespace whtmix {
+namespace {
+
+using namespace tile;
+
+typedef short bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- layouts
+// A layout names the tile bit held by each register bit (reg) and the tile
+// index of a thread's register 0 (base).  Register offsets and LDS offsets
+// pad() are additive over the disjoint bit fields, as in whtmix_tile.h.
+template <int S>
+struct Std {
+    static constexpr int reg(int j) { return S + j; }
+    __device__ static uint32_t base(uint32_t tau) { return layout_base<S>(tau); }
+};
+
+// Epilogue layout of a 2^M tile with C = 2^CB (flat t = token * C + channel):
+//   lanes 0-3  -> token bits 0-3           (the MFMA column j)
+//   lanes 4-5  -> channel bits CB-2, CB-1  (the MFMA k group q)
+//   waves      -> token bits 4 .. M-8
+//   registers  -> channel bits 0 .. CB-3, then token bits M-7 .. M-CB-1
+// so a lane holds C/4 consecutive channels of 2^(7-CB) tokens.
+template <int M, int CB>
+struct Epi {
+    static constexpr int reg(int j) { return j < CB - 2 ? j : M - 7 + CB + (j - (CB - 2)); }
+    __device__ static uint32_t base(uint32_t tau)
+    {
+        return ((tau & 15u) << CB) | (((tau >> 4) & 3u) << (CB - 2)) | ((tau >> 6) << (CB + 4));
+    }
+};
+
+template <class L>
+constexpr uint32_t reg_offset(uint32_t k)
+{
+    uint32_t t = 0;
+    for (int j = 0; j < VB; ++j)
+        if (k & (1u << j)) t |= 1u << L::reg(j);
+    return t;
+}
+
+// Re-lay the tile from LA to LB through LDS (LEAD: wait for the previous
+// readers of the LDS first).
+template <class LA, class LB, bool LEAD = true>
+__device__ __forceinline__ void relayout(float *lds, float (&v)[V], uint32_t tau)
+{
+    const uint32_t pa = pad(LA::base(tau));
+    const uint32_t pb = pad(LB::base(tau));
+    if (LEAD)
+        __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pa + pad(reg_offset<LA>((uint32_t)k))] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] = lds[pb + pad(reg_offset<LB>((uint32_t)k))];
+}
+
+// Butterflies over the register bits set in MASK.
+template <uint32_t MASK>
+__device__ __forceinline__ void butterflies_on(float (&v)[V])
+{
+#pragma unroll
+    for (int j = 0; j < VB; ++j) {
+        if (!(MASK & (1u << j))) continue;
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            if (!(k & (1 << j))) {
+                const float a = v[k];
+                const float b = v[k | (1 << j)];
+                v[k] = a + b;
+                v[k | (1 << j)] = a - b;
+            }
+        }
+    }
+}
+
+// Forward transform of a 2^M tile arriving in layout 4 from the prologue
+// (bits [4, 9) still to do): ends in layout M-5 with every bit done.
+template <int M>
+__device__ __forceinline__ void forward_from_prologue(float *lds, float (&v)[V], uint32_t tau)
+{
+    butterflies_on<31>(v);
+    relayout<Std<4>, Std<0>, true>(lds, v, tau);   // LEAD: the weights were read from LDS
+    butterflies_on<15>(v);                          // bits 0-3
+    if constexpr (M <= 14) {
+        relayout<Std<0>, Std<M - 5>>(lds, v, tau);
+        butterflies_on<31u & ~((1u << (14 - M)) - 1u)>(v);   // bits 9 .. M-1
+    } else {
+        relayout<Std<0>, Std<5>>(lds, v, tau);
+        butterflies_on<16>(v);                      // bit 9
+        relayout<Std<5>, Std<10>>(lds, v, tau);
+        butterflies_on<31>(v);                      // bits 10-14
+    }
+}
+
+// Inverse transform of a 2^M tile in layout M-5 (nothing done yet), ending
+// in the epilogue layout with every bit done.  The epilogue layout's register
+// bits are left to the last step; the others go first.
+template <int M, int CB, bool LEAD0>
+__device__ __forceinline__ void inverse_to_epilogue(float *lds, float (&v)[V], uint32_t tau)
+{
+    constexpr int len = M - 3 - CB;   // bits [CB-2, M-5) between the two
+    butterflies_on<(1u << (CB - 2)) - 1u>(v);   // bits [M-5, M-7+CB)
+    if constexpr (len <= VB) {
+        relayout<Std<M - 5>, Std<CB - 2>, LEAD0>(lds, v, tau);
+        butterflies_on<(1u << len) - 1u>(v);
+        relayout<Std<CB - 2>, Epi<M, CB>>(lds, v, tau);
+    } else {
+        relayout<Std<M - 5>, Std<CB - 2>, LEAD0>(lds, v, tau);
+        butterflies_on<31>(v);
+        relayout<Std<CB - 2>, Std<CB + 3>>(lds, v, tau);
+        butterflies_on<(1u << (len - VB)) - 1u>(v);
+        relayout<Std<CB + 3>, Epi<M, CB>>(lds, v, tau);
+    }
+    butterflies_on<31>(v);
+}
+
+// ---------------------------------------------------------------- projections
+template <typename T, int CB>
+struct Proj {
+    static constexpr int C = 1 << CB;
+    static constexpr int NRB = 1 << (7 - CB);    // 16-row MFMA blocks per wave
+    static constexpr int NNB = C / 16;           // 16-column blocks
+    static constexpr bool BF = sizeof(T) == 2;
+    // k steps per column block: 16 (bf16) or 4 (fp32) k values per MFMA
+    static constexpr int KS = BF ? C / 16 : C / 4;
+    // A-fragment registers per lane and row block (X: C/4 values)
+    static constexpr uint32_t WBYTES = (uint32_t)C * C * sizeof(T);
+};
+
+// k value order of the prologue (X W_in).  bf16: lane group q, step kk,
+// element r: channel 32(kk/2) + 8q + 4(kk%2) + r (C >= 32; each lane reads its
+// channels as 16-byte pieces of 8), or 4q + r (C = 16).  fp32: step s:
+// channel 16(s/4) + 4q + s%4 (16-byte pieces of 4).
+__host__ __device__ constexpr uint32_t k_in_bf16(uint32_t C, uint32_t kk, uint32_t q, uint32_t r)
+{
+    return C >= 32 ? 32u * (kk >> 1) + 8u * q + 4u * (kk & 1u) + r : 4u * q + r;
+}
+__host__ __device__ constexpr uint32_t k_in_f32(uint32_t s, uint32_t q)
+{
+    return 16u * (s >> 2) + 4u * q + (s & 3u);
+}
+// Epilogue: lane group q holds channels [q C/4, (q+1) C/4); step kk element r
+// (bf16) or step s (fp32) is channel q C/4 + 4 kk + r, or q C/4 + s.
+// Output channel of MFMA row m in column block nb: bf16 pairs of blocks give
+// each lane 8 consecutive channels (one 16-byte store); fp32 rows are
+// 16 nb + m (4 consecutive channels per lane, 16 bytes).
+__host__ __device__ constexpr uint32_t oc_bf16(uint32_t C, uint32_t nb, uint32_t m)
+{
+    return C >= 32 ? 32u * (nb >> 1) + 8u * (m >> 2) + 4u * (nb & 1u) + (m & 3u) : m;
+}
+
+// One thread per packed element.  Packed index = ((nb * KS + kk) * 64 + lane)
+// * 4 + r with lane = 16 q + j (bf16), or ((nb * C/16 + p) * 64 + lane) * 4 + e
+// with step s = 4p + e (fp32).  W_in feeds the B operand of Z = X W_in
+// (column 16 nb + j); W_out feeds the A operand of Y^T = W_out^T Z'^T.
+template <typename T>
+__global__ void __launch_bounds__(256)
+pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *__restrict__ p_in,
+                    T *__restrict__ p_out, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= C * C) return;
+    const uint32_t e = idx & 3u;
+    const uint32_t lane = (idx >> 2) & 63u;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const uint32_t rest = idx >> 8;
+    if constexpr (sizeof(T) == 2) {
+        const uint32_t ks = C / 16u;
+        const uint32_t kk = rest % ks, nb = rest / ks;
+        p_in[idx] = w_in[k_in_bf16(C, kk, q, e) * C + 16u * nb + j];
+        p_out[idx] = w_out[(q * (C / 4u) + 4u * kk + e) * C + oc_bf16(C, nb, j)];
+    } else {
+        const uint32_t np = C / 16u;
+        const uint32_t p = rest % np, nb = rest / np;
+        const uint32_t s = 4u * p + e;
+        p_in[idx] = w_in[k_in_f32(s, q) * C + 16u * nb + j];
+        p_out[idx] = w_out[(q * (C / 4u) + s) * C + 16u * nb + j];
+    }
+}
+
+// X fragments of the prologue: per row block, the lane's C/4 channels of its
+// token, as bf16x4 per k step (bf16) or floats (fp32).
+template <typename T, int CB>
+struct XFrag;
+
+template <int CB>
+struct XFrag<__bf16, CB> {
+    using P = Proj<__bf16, CB>;
+    bf16x4 a[P::NRB][P::KS];
+};
+template <int CB>
+struct XFrag<float, CB> {
+    using P = Proj<float, CB>;
+    float a[P::NRB][P::KS];
+};
+
+// Token (tile row) of MFMA row m in row block rb for wave w: layout 4 puts
+// token bits 0-1 on r = m%4, bits 2 .. 8-CB on rb, the next two on the lane
+// group q = m/4 and the rest on the wave.
+template <int CB>
+__device__ __forceinline__ uint32_t prologue_token(uint32_t rb, uint32_t m, uint32_t w)
+{
+    return (m & 3u) | (rb << 2) | ((m >> 2) << (9 - CB)) | (w << (11 - CB));
+}
+
+// Loads the lane's X fragments from a tile of `valid` elements (a multiple of
+// C); rows past it read as zero.  Rows are masked explicitly (the range check
+// of a buffer access is not relied on: part of each offset is in soffset).
+template <typename T, int CB>
+__device__ __forceinline__ void load_x_frags(XFrag<T, CB> &f, const T *tile, uint32_t valid,
+                                             bool whole, uint32_t tau)
+{
+    using P = Proj<T, CB>;
+    const uint32_t lane = tau & 63u, w = tau >> 6;
+    const uint32_t i = lane & 15u, q = lane >> 4;
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * (uint32_t)sizeof(T));
+    const uint32_t tok0 = prologue_token<CB>(0, i, w);
+    const uint32_t row = tok0 * (uint32_t)(P::C * sizeof(T));
+    constexpr uint32_t rb_bytes = 4u * P::C * sizeof(T);
+#pragma unroll
+    for (int rb = 0; rb < P::NRB; ++rb) {
+        const bool ok = whole || (tok0 + 4u * rb) * (uint32_t)P::C < valid;
+        if constexpr (P::BF) {
+            if constexpr (P::C >= 32) {
+#pragma unroll
+                for (int p = 0; p < P::C / 32; ++p) {
+                    u32x4 d = {0u, 0u, 0u, 0u};
+                    if (ok)
+                        d = __builtin_amdgcn_raw_buffer_load_b128(r, row + 16u * q,
+                                                                  rb * rb_bytes + 64u * p,
+                                                                  kStreaming);
+                    f.a[rb][2 * p] = __builtin_bit_cast(bf16x4, (u32x2){d.x, d.y});
+                    f.a[rb][2 * p + 1] = __builtin_bit_cast(bf16x4, (u32x2){d.z, d.w});
+                }
+            } else {
+                u32x2 d = {0u, 0u};
+                if (ok)
+                    d = __builtin_amdgcn_raw_buffer_load_b64(r, row + 8u * q, rb * rb_bytes,
+                                                             kStreaming);
+                f.a[rb][0] = __builtin_bit_cast(bf16x4, d);
+            }
+        } else {
+#pragma unroll
+            for (int p = 0; p < P::C / 16; ++p) {
+                u32x4 d = {0u, 0u, 0u, 0u};
+                if (ok)
+                    d = __builtin_amdgcn_raw_buffer_load_b128(r, row + 16u * q,
+                                                              rb * rb_bytes + 64u * p,
+                                                              kStreaming);
+                // Cast the whole vector: this compiler reads element 0 for a
+                // __builtin_bit_cast of a single ext-vector element (d.y etc.).
+                const f32x4 fv = __builtin_bit_cast(f32x4, d);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    f.a[rb][4 * p + e] = fv[e];
+            }
+        }
+    }
+}
+
+// Z = X W_in for the wave's tokens, into v in layout 4: register
+// nb | r << (CB-4) | rb << (CB-2) holds tile bits [4, 9) = channel bits 4..CB-1
+// (nb), token bits 0-1 (r), token bits 2..8-CB (rb).  wl: packed W_in in LDS.
+template <typename T, int CB>
+__device__ __forceinline__ void project_in(float (&v)[V], const XFrag<T, CB> &f, const void *wl,
+                                           uint32_t tau)
+{
+    using P = Proj<T, CB>;
+    const uint32_t lane = tau & 63u;
+    if constexpr (P::BF) {
+        const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+#pragma unroll
+        for (int nb = 0; nb < P::NNB; ++nb) {
+            bf16x4 b[P::KS];
+#pragma unroll
+            for (int kk = 0; kk < P::KS; ++kk)
+                b[kk] = wb[(nb * P::KS + kk) * 64 + lane];
+#pragma unroll
+            for (int rb = 0; rb < P::NRB; ++rb) {
+                f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int kk = 0; kk < P::KS; ++kk)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(f.a[rb][kk], b[kk], acc, 0, 0,
+                                                                     0);
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    v[nb | (r << (CB - 4)) | (rb << (CB - 2))] = acc[r];
+            }
+        }
+    } else {
+        const f32x4 *wf = static_cast<const f32x4 *>(wl);
+        constexpr int NP = P::C / 16;
+#pragma unroll
+        for (int nb = 0; nb < P::NNB; ++nb) {
+            f32x4 acc[P::NRB];
+#pragma unroll
+            for (int rb = 0; rb < P::NRB; ++rb)
+                acc[rb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                const f32x4 b = wf[(nb * NP + p) * 64 + lane];
+#pragma unroll
+                for (int rb = 0; rb < P::NRB; ++rb) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[rb] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.a[rb][4 * p + e], b[e],
+                                                                       acc[rb], 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int rb = 0; rb < P::NRB; ++rb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    v[nb | (r << (CB - 4)) | (rb << (CB - 2))] = acc[rb][r];
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b)
+{
+    return (uint32_t)__builtin_bit_cast(unsigned short, (__bf16)a) |
+           ((uint32_t)__builtin_bit_cast(unsigned short, (__bf16)b) << 16);
+}
+
+// Y = Z' W_out for the wave's tokens, Z' in the epilogue layout of a 2^M
+// tile; stores the rows of the tile with element index < valid (a multiple
+// of C), masked explicitly.  wl: packed W_out in LDS.
+template <typename T, int CB, int M>
+__device__ __forceinline__ void project_out(const float (&v)[V], const void *wl, T *tile,
+                                            uint32_t valid, uint32_t tau)
+{
+    using P = Proj<T, CB>;
+    const uint32_t lane = tau & 63u, w = tau >> 6;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * (uint32_t)sizeof(T));
+    const bool whole = valid >= (1u << M);
+    // token of column j in row block rb: j | w << 4 | rb << (M-7)
+    const uint32_t tok0 = j | (w << 4);
+    const uint32_t row = tok0 * (uint32_t)(P::C * sizeof(T));
+    constexpr uint32_t rb_bytes = (1u << (M - 7)) * P::C * sizeof(T);
+    constexpr int RB_SHIFT = CB - 2;   // register bits of the row block
+    if constexpr (P::BF) {
+        const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+#pragma unroll
+        for (int rb = 0; rb < P::NRB; ++rb) {
+            bf16x4 hi[P::KS], lo[P::KS];
+#pragma unroll
+            for (int kk = 0; kk < P::KS; ++kk) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float z = v[(4 * kk + e) | (rb << RB_SHIFT)];
+                    const __bf16 h = (__bf16)z;
+                    hi[kk][e] = __builtin_bit_cast(short, h);
+                    lo[kk][e] = __builtin_bit_cast(short, (__bf16)(z - (float)h));
+                }
+            }
+            f32x4 acc[P::NNB];
+#pragma unroll
+            for (int nb = 0; nb < P::NNB; ++nb) {
+                acc[nb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int kk = 0; kk < P::KS; ++kk) {
+                    const bf16x4 a = wb[(nb * P::KS + kk) * 64 + lane];
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, hi[kk], acc[nb], 0, 0,
+                                                                         0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, lo[kk], acc[nb], 0, 0,
+                                                                         0);
+                }
+            }
+            // the row block's token; MFMAs above run with every lane active
+            const bool ok = whole || (tok0 + ((uint32_t)rb << (M - 7))) * (uint32_t)P::C < valid;
+            if constexpr (P::C >= 32) {
+                // blocks 2n, 2n+1: channels 32 n + 8 q + [0, 8)
+#pragma unroll
+                for (int n = 0; n < P::NNB / 2; ++n) {
+                    const u32x4 d = {pack2_bf16(acc[2 * n][0], acc[2 * n][1]),
+                                     pack2_bf16(acc[2 * n][2], acc[2 * n][3]),
+                                     pack2_bf16(acc[2 * n + 1][0], acc[2 * n + 1][1]),
+                                     pack2_bf16(acc[2 * n + 1][2], acc[2 * n + 1][3])};
+                    if (ok)
+                        __builtin_amdgcn_raw_buffer_store_b128(d, r, row + 16u * q,
+                                                               rb * rb_bytes + 64u * n,
+                                                               kStreaming);
+                }
+            } else {
+                const u32x2 d = {pack2_bf16(acc[0][0], acc[0][1]),
+                                 pack2_bf16(acc[0][2], acc[0][3])};
+                if (ok)
+                    __builtin_amdgcn_raw_buffer_store_b64(d, r, row + 8u * q, rb * rb_bytes,
+                                                          kStreaming);
+            }
+        }
+    } else {
+        const f32x4 *wf = static_cast<const f32x4 *>(wl);
+        constexpr int NP = P::C / 16;
+#pragma unroll
+        for (int rb = 0; rb < P::NRB; ++rb) {
+            const bool ok = whole || (tok0 + ((uint32_t)rb << (M - 7))) * (uint32_t)P::C < valid;
+#pragma unroll
+            for (int nb = 0; nb < P::NNB; ++nb) {
+                f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int p = 0; p < NP; ++p) {
+                    const f32x4 a = wf[(nb * NP + p) * 64 + lane];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            a[e], v[(4 * p + e) | (rb << RB_SHIFT)], acc, 0, 0, 0);
+                }
+                // channels 16 nb + 4 q + [0, 4)
+                const u32x4 d = __builtin_bit_cast(u32x4, acc);
+                if (ok)
+                    __builtin_amdgcn_raw_buffer_store_b128(d, r, row + 16u * q,
+                                                           rb * rb_bytes + 64u * nb, kStreaming);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- LDS plan
+// The tile's exchanges use pad(2^M) floats.  The prologue's weights share
+// that space (they are dead before the first exchange).  The epilogue's
+// weights either get their own region, loaded at kernel start, or share it
+// too, prefetched into registers at start and written to LDS after the last
+// exchange; sharing is chosen when a private region would cost occupancy and
+// the prefetch takes at most 8 16-byte registers per thread.
+template <int M, typename T, int CB>
+struct Lds {
+    static constexpr uint32_t NT = 1u << (M - VB);
+    static constexpr uint32_t TILE = pad(1u << M) * 4u;
+    static constexpr uint32_t W = Proj<T, CB>::WBYTES;
+    static constexpr uint32_t CHUNKS = W / 16u;
+    static constexpr bool PREFETCH_OK = CHUNKS % NT == 0 && CHUNKS / NT <= 8;
+    static constexpr bool SEPARATE = TILE + W <= 80u * 1024u || !PREFETCH_OK;
+    static constexpr uint32_t PER = PREFETCH_OK ? CHUNKS / NT : 1;
+    static constexpr uint32_t REGION0 = TILE > W ? TILE : W;   // tile, or weights first
+    static constexpr uint32_t fwd_bytes() { return REGION0; }
+    static constexpr uint32_t inv_bytes() { return SEPARATE ? TILE + W : REGION0; }
+    static constexpr uint32_t fused_bytes() { return SEPARATE ? REGION0 + W : REGION0; }
+};
+
+template <uint32_t CHUNKS, uint32_t NT>
+__device__ __forceinline__ void stage_weights(void *lds, const void *w, uint32_t tau)
+{
+    u32x4 *d = static_cast<u32x4 *>(lds);
+    const u32x4 *s = static_cast<const u32x4 *>(w);
+#pragma unroll
+    for (uint32_t c = tau; c < CHUNKS; c += NT)
+        d[c] = s[c];
+}
+
+// ---------------------------------------------------------------- kernels
+// FUSED: one workgroup per slice (M = K).
+template <int K, typename T, class Gain, int CB>
+__global__ void __launch_bounds__(1 << (K - VB))
+module_fused_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
+                    const T *__restrict__ w_out, T *__restrict__ y, Gain gain, uint32_t nvalid)
+{
+    using L = Lds<K, T, CB>;
+    __shared__ __attribute__((aligned(16))) float lds[L::fused_bytes() / 4];
+    unsigned char *const region1 = reinterpret_cast<unsigned char *>(lds) + L::REGION0;
+    const uint32_t tau = threadIdx.x;
+    const size_t base = (size_t)blockIdx.x * nvalid;
+    XFrag<T, CB> f;
+    load_x_frags<T, CB>(f, x + base, nvalid, nvalid >= (1u << K), tau);
+    stage_weights<L::CHUNKS, L::NT>(lds, w_in, tau);
+    u32x4 wreg[L::PER];
+    if constexpr (L::SEPARATE) {
+        stage_weights<L::CHUNKS, L::NT>(region1, w_out, tau);
+    } else {
+#pragma unroll
+        for (uint32_t i = 0; i < L::PER; ++i)
+            wreg[i] = static_cast<const u32x4 *>(static_cast<const void *>(w_out))[tau + i * L::NT];
+    }
+    float v[V], gv[V];
+    gain.template load<K - 5, ContigMap>(gv, 0, tau);
+    __syncthreads();
+    project_in<T, CB>(v, f, lds, tau);
+    forward_from_prologue<K>(lds, v, tau);
+    apply_gain<K>(v, gv);
+    inverse_to_epilogue<K, CB, true>(lds, v, tau);
+    const void *wl = region1;
+    if constexpr (!L::SEPARATE) {
+        __syncthreads();   // every thread has read its epilogue-layout values
+#pragma unroll
+        for (uint32_t i = 0; i < L::PER; ++i)
+            reinterpret_cast<u32x4 *>(lds)[tau + i * L::NT] = wreg[i];
+        wl = lds;
+    }
+    __syncthreads();
+    project_out<T, CB, K>(v, wl, y + base, nvalid, tau);
+}
+
+// THREE_PASS first pass: prologue, forward over the A low bits, workspace.
+template <int A, int HB, int R, typename T, int CB>
+__global__ void __launch_bounds__(1 << (A - VB))
+module_outer_fwd_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
+                        float *__restrict__ ws, uint32_t nvalid)
+{
+    using L = Lds<A, T, CB>;
+    using Run = RunMap<HB, R>;
+    __shared__ __attribute__((aligned(16))) float lds[L::fwd_bytes() / 4];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    XFrag<T, CB> f;
+    load_x_frags<T, CB>(f, x + b * nvalid + ((size_t)hi << A), valid, valid >= (1u << A), tau);
+    stage_weights<L::CHUNKS, L::NT>(lds, w_in, tau);
+    __syncthreads();
+    float v[V];
+    project_in<T, CB>(v, f, lds, tau);
+    forward_from_prologue<A>(lds, v, tau);
+    store_layout<A - 5, Run, float>(
+        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+}
+
+// THREE_PASS last pass: inverse over the A low bits, epilogue, y.
+template <int A, int HB, int R, typename T, int CB>
+__global__ void __launch_bounds__(1 << (A - VB))
+module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_out,
+                        T *__restrict__ y, uint32_t nvalid)
+{
+    using L = Lds<A, T, CB>;
+    using Run = RunMap<HB, R>;
+    __shared__ __attribute__((aligned(16))) float lds[L::inv_bytes() / 4];
+    unsigned char *const wregion = reinterpret_cast<unsigned char *>(lds) + L::TILE;
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    if (valid == 0)
+        return;   // wholly padding: nothing to store (uniform per workgroup)
+    u32x4 wreg[L::PER];
+    if constexpr (L::SEPARATE) {
+        stage_weights<L::CHUNKS, L::NT>(wregion, w_out, tau);
+    } else {
+#pragma unroll
+        for (uint32_t i = 0; i < L::PER; ++i)
+            wreg[i] = static_cast<const u32x4 *>(static_cast<const void *>(w_out))[tau + i * L::NT];
+    }
+    float v[V];
+    load_layout<A - 5, Run, float>(
+        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+    inverse_to_epilogue<A, CB, false>(lds, v, tau);
+    const void *wl = wregion;
+    if constexpr (!L::SEPARATE) {
+        __syncthreads();
+#pragma unroll
+        for (uint32_t i = 0; i < L::PER; ++i)
+            reinterpret_cast<u32x4 *>(lds)[tau + i * L::NT] = wreg[i];
+        wl = lds;
+    }
+    __syncthreads();
+    project_out<T, CB, A>(v, wl, y + b * nvalid + ((size_t)hi << A), valid, tau);
+}
+
+__device__ __forceinline__ float to_f(float v) { return v; }
+__device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
+
+// SMALL: 2^K <= 2^10, one 256-thread workgroup per slice, everything in LDS,
+// projections on the VALU (any C).
+template <typename T, class Gain>
+__global__ void __launch_bounds__(256)
+module_small_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
+                    const T *__restrict__ w_out, T *__restrict__ y, Gain gain, int K, int cb,
+                    uint32_t nvalid)
+{
+    __shared__ float xs[1 << kMaxSmall];
+    __shared__ float s[1 << kMaxSmall];
+    const int L = 1 << K;
+    const uint32_t C = 1u << cb;
+    const size_t base = (size_t)blockIdx.x * nvalid;
+    for (int i = threadIdx.x; i < L; i += blockDim.x)
+        xs[i] = (uint32_t)i < nvalid ? to_f(x[base + i]) : 0.0f;
+    __syncthreads();
+    for (int i = threadIdx.x; i < L; i += blockDim.x) {
+        const uint32_t row = (uint32_t)i >> cb, c = (uint32_t)i & (C - 1u);
+        float acc = 0.0f;
+        for (uint32_t k = 0; k < C; ++k)
+            acc = fmaf(xs[row * C + k], to_f(w_in[k * C + c]), acc);
+        s[i] = acc;
+    }
+    const float scale = 1.0f / (float)L;
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int h = 1; h < L; h <<= 1) {
+            __syncthreads();
+            for (int p = threadIdx.x; p < L / 2; p += blockDim.x) {
+                const int i = ((p / h) * 2 * h) + (p % h);
+                const float a = s[i], c = s[i + h];
+                s[i] = a + c;
+                s[i + h] = a - c;
+            }
+        }
+        __syncthreads();
+        if (pass == 0)
+            for (int i = threadIdx.x; i < L; i += blockDim.x)
+                s[i] *= gain.at((uint32_t)i) * scale;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < (int)nvalid; i += blockDim.x) {
+        const uint32_t row = (uint32_t)i >> cb, c = (uint32_t)i & (C - 1u);
+        float acc = 0.0f;
+        for (uint32_t k = 0; k < C; ++k)
+            acc = fmaf(s[row * C + k], to_f(w_out[k * C + c]), acc);
+        y[base + i] = (T)acc;
+    }
+}
+
+// UNFUSED projection: out[row][c] = sum_k in[row][k] w[k][c], one thread per
+// output, for the channel counts the MFMA layouts do not cover.
+template <typename Tin, typename Tout, typename Tw>
+__global__ void __launch_bounds__(256)
+project_rows_kernel(const Tin *__restrict__ in, const Tw *__restrict__ w, Tout *__restrict__ out,
+                    uint64_t total, int cb)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256u + threadIdx.x;
+    if (i >= total) return;
+    const uint32_t C = 1u << cb;
+    const uint32_t c = (uint32_t)(i & (C - 1u));
+    const Tin *row = in + (i - c);
+    float acc = 0.0f;
+    for (uint32_t k = 0; k < C; ++k)
+        acc = fmaf(to_f(row[k]), to_f(w[(size_t)k * C + c]), acc);
+    out[i] = (Tout)acc;
+}
+
+// ---------------------------------------------------------------- launchers
+inline hipError_t record(hipEvent_t ev, hipStream_t st)
+{
+    return ev ? hipEventRecord(ev, st) : hipSuccess;
+}
+
+template <typename T>
+hipError_t launch_pack(const ModuleArgs &m)
+{
+    const uint32_t n = 1u << (2 * m.cbits);
+    hipLaunchKernelGGL((pack_weights_kernel<T>), dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
+                       static_cast<const T *>(m.w_in), static_cast<const T *>(m.w_out),
+                       static_cast<T *>(m.wpack), static_cast<T *>(m.wpack) + n, m.cbits);
+    return hipGetLastError();
+}
+
+template <int K, typename T, class Gain, int CB>
+hipError_t launch_module_fused(const ModuleArgs &m, Gain gain)
+{
+    const uint32_t n = 1u << (2 * CB);
+    const T *pin = static_cast<const T *>(m.wpack);
+    hipError_t e = record(m.events[0], m.stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((module_fused_kernel<K, T, Gain, CB>), dim3((uint32_t)m.B),
+                       dim3(1u << (K - VB)), 0, m.stream, static_cast<const T *>(m.x), pin,
+                       pin + n, static_cast<T *>(m.y), gain, m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[1], m.stream);
+}
+
+template <int K, typename T, class Gain, int CB>
+hipError_t launch_module_three_pass(const ModuleArgs &m, Gain gain)
+{
+    constexpr Split sp = three_pass_split(K);
+    constexpr int A = sp.A, HB = sp.HB, R = sp.R;
+    const uint32_t n = 1u << (2 * CB);
+    const T *pin = static_cast<const T *>(m.wpack);
+    const hipStream_t st = m.stream;
+    hipError_t e = record(m.events[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((module_outer_fwd_kernel<A, HB, R, T, CB>), dim3((uint32_t)(m.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, static_cast<const T *>(m.x), pin, m.ws,
+                       m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(m.events[1], st)) != hipSuccess) return e;
+    LaunchArgs a{};
+    a.gain_kind = m.gain_kind;
+    a.gain = m.gain;
+    a.gain_t = m.gain_t;
+    a.gain_c = m.gain_c;
+    a.cbits = m.cbits;
+    a.ws = m.ws;
+    a.B = m.B;
+    a.K = K;
+    a.plan = PLAN_THREE_PASS;
+    a.stream = st;
+    if ((e = launch_middle(a)) != hipSuccess) return e;
+    if ((e = record(m.events[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((module_outer_inv_kernel<A, HB, R, T, CB>), dim3((uint32_t)(m.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, m.ws, pin + n, static_cast<T *>(m.y),
+                       m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[3], st);
+}
+
+template <typename T, class Gain, int CB>
+hipError_t dispatch_k(const ModuleArgs &m, Gain gain)
+{
+    if (m.plan == PLAN_FUSED) {
+        switch (m.K) {
+#define WHTMIX_MF_CASE(k) \
+    case k: return launch_module_fused<k, T, Gain, CB>(m, gain);
+            WHTMIX_MF_CASE(11) WHTMIX_MF_CASE(12) WHTMIX_MF_CASE(13) WHTMIX_MF_CASE(14)
+            WHTMIX_MF_CASE(15)
+#undef WHTMIX_MF_CASE
+        default: return hipErrorInvalidValue;
+        }
+    }
+    switch (m.K) {
+#define WHTMIX_M3_CASE(k) \
+    case k: return launch_module_three_pass<k, T, Gain, CB>(m, gain);
+        WHTMIX_M3_CASE(12) WHTMIX_M3_CASE(13) WHTMIX_M3_CASE(14) WHTMIX_M3_CASE(15)
+        WHTMIX_M3_CASE(16) WHTMIX_M3_CASE(17) WHTMIX_M3_CASE(18) WHTMIX_M3_CASE(19)
+        WHTMIX_M3_CASE(20) WHTMIX_M3_CASE(21) WHTMIX_M3_CASE(22) WHTMIX_M3_CASE(23)
+        WHTMIX_M3_CASE(24) WHTMIX_M3_CASE(25) WHTMIX_M3_CASE(26) WHTMIX_M3_CASE(27)
+        WHTMIX_M3_CASE(28) WHTMIX_M3_CASE(29) WHTMIX_M3_CASE(30)
+#undef WHTMIX_M3_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <typename T, class Gain>
+hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
+{
+    hipError_t e = launch_pack<T>(m);
+    if (e != hipSuccess) return e;
+    switch (m.cbits) {
+    case 4: return dispatch_k<T, Gain, 4>(m, gain);
+    case 5: return dispatch_k<T, Gain, 5>(m, gain);
+    case 6: return dispatch_k<T, Gain, 6>(m, gain);
+    case 7: return dispatch_k<T, Gain, 7>(m, gain);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <typename T, class Gain>
+hipError_t launch_module_small(const ModuleArgs &m, Gain gain)
+{
+    hipError_t e = record(m.events[0], m.stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((module_small_kernel<T, Gain>), dim3((uint32_t)m.B), dim3(256), 0, m.stream,
+                       static_cast<const T *>(m.x), static_cast<const T *>(m.w_in),
+                       static_cast<const T *>(m.w_out), static_cast<T *>(m.y), gain, m.K, m.cbits,
+                       m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[1], m.stream);
+}
+
+// UNFUSED: z = x W_in (fp32, in the workspace), the fp32 mixer in place on
+// z, y = z W_out.
+template <typename T>
+hipError_t launch_module_unfused(const ModuleArgs &m)
+{
+    const uint64_t total = (uint64_t)m.B * m.nvalid;
+    const uint32_t blocks = (uint32_t)((total + 255u) / 256u);
+    const hipStream_t st = m.stream;
+    hipError_t e = record(m.events[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((project_rows_kernel<T, float, T>), dim3(blocks), dim3(256), 0, st,
+                       static_cast<const T *>(m.x), static_cast<const T *>(m.w_in), m.z, total,
+                       m.cbits);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    LaunchArgs a{};
+    a.x = m.z;
+    a.y = m.z;
+    a.gain_kind = m.gain_kind;
+    a.gain = m.gain;
+    a.gain_t = m.gain_t;
+    a.gain_c = m.gain_c;
+    a.cbits = m.cbits;
+    a.ws = m.ws;
+    a.B = m.B;
+    a.K = m.K;
+    a.nvalid = m.nvalid;
+    a.dtype = DTYPE_F32;
+    a.plan = m.plan;
+    a.stream = st;
+    if ((e = launch(a)) != hipSuccess) return e;
+    hipLaunchKernelGGL((project_rows_kernel<float, T, T>), dim3(blocks), dim3(256), 0, st, m.z,
+                       static_cast<const T *>(m.w_out), static_cast<T *>(m.y), total, m.cbits);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[1], st);
+}
+
+template <typename T, class Gain>
+hipError_t dispatch_module(const ModuleArgs &m, Gain gain)
+{
+    switch (module_path(m.plan, m.cbits)) {
+    case MODULE_SMALL: return launch_module_small<T, Gain>(m, gain);
+    case MODULE_FUSED_MFMA: return dispatch_fused_module<T, Gain>(m, gain);
+    default: return launch_module_unfused<T>(m);
+    }
+}
+
+template <typename T>
+hipError_t dispatch_module_gain(const ModuleArgs &m)
+{
+    if (m.gain_kind == GAIN_LOG_SEPARABLE)
+        return dispatch_module<T>(m, LogSeparableGain{m.gain_t, m.gain_c, (uint32_t)m.cbits});
+    return dispatch_module<T>(m, FullGain{m.gain});
+}
+
+}  // namespace
+
+hipError_t launch_module(const ModuleArgs &m)
+{
+    if (m.dtype == DTYPE_BF16)
+        return dispatch_module_gain<__bf16>(m);
+    return dispatch_module_gain<float>(m);
+}
+
+}  // namespace whtmix

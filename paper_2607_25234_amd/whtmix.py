@@ -27,6 +27,8 @@ EXPORTS = (
     "whtmix_forward",
     "whtmix_forward_ex",
     "whtmix_forward_separable",
+    "whtmix_module_forward",
+    "whtmix_module_forward_separable",
     "whtmix_plan_describe",
     "whtmix_status_string",
     "whtmix_last_error",
@@ -80,6 +82,12 @@ def lib():
         L.whtmix_forward_separable.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                                ctypes.POINTER(Options)]
         L.whtmix_forward_separable.restype = ctypes.c_int
+        L.whtmix_module_forward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int,
+                                            vp, ctypes.POINTER(Options)]
+        L.whtmix_module_forward.restype = ctypes.c_int
+        L.whtmix_module_forward_separable.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64,
+                                                      ctypes.c_int, vp, ctypes.POINTER(Options)]
+        L.whtmix_module_forward_separable.restype = ctypes.c_int
         L.whtmix_backward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                       ctypes.POINTER(Options)]
         L.whtmix_backward.restype = ctypes.c_int
@@ -225,6 +233,78 @@ def forward_separable(x, log_gain_tokens, log_gain_channels, out=None,
                                        dt, st.cuda_stream, plan, events)
     if status != SUCCESS:
         raise WhtmixError(status, "whtmix_forward_separable")
+    return out
+
+
+def module_forward_raw(x_ptr: int, w_in_ptr: int, gain_ptr: int, w_out_ptr: int, y_ptr: int,
+                       B: int, N: int, C: int, dtype: int, stream: int,
+                       plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_module_forward; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_module_forward(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, y_ptr, B, N, C,
+                                       dtype, stream, ctypes.byref(opt))
+
+
+def module_forward_separable_raw(x_ptr: int, w_in_ptr: int, gt_ptr: int, gc_ptr: int,
+                                 w_out_ptr: int, y_ptr: int, B: int, N: int, C: int,
+                                 dtype: int, stream: int, plan: str | int = "auto",
+                                 events=None) -> int:
+    """Direct call of whtmix_module_forward_separable; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_module_forward_separable(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr,
+                                                 y_ptr, B, N, C, dtype, stream,
+                                                 ctypes.byref(opt))
+
+
+def _weight(w, C, x, what):
+    if w.device != x.device or w.dtype != x.dtype or not w.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous tensor of x's dtype on x's device")
+    if tuple(w.shape) != (C, C):
+        raise ValueError(f"{what} shape {tuple(w.shape)} != {(C, C)}")
+
+
+def module_forward(x, w_in, gain, w_out, out=None, plan: str | int = "auto", stream=None,
+                   events=None):
+    """The whole block of section III-B, eqs. (1)-(4): Y = mixer(X W_in) W_out with
+    the joint gain.  w_in, w_out: [C, C] tensors of x's dtype (Z[n][j] = sum_i
+    X[n][i] W_in[i][j]); gain: float32 [N_pad, C]."""
+    import torch
+
+    xx, dt, out = _check(x, out)
+    B, N, C = xx.shape
+    _weight(w_in, C, x, "w_in")
+    _weight(w_out, C, x, "w_out")
+    _gain(gain, (padded_tokens(N), C), x, "gain")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = module_forward_raw(xx.data_ptr(), w_in.data_ptr(), gain.data_ptr(),
+                                    w_out.data_ptr(), out.data_ptr(), B, N, C, dt,
+                                    st.cuda_stream, plan, events)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_module_forward")
+    return out
+
+
+def module_forward_separable(x, w_in, log_gain_tokens, log_gain_channels, w_out, out=None,
+                             plan: str | int = "auto", stream=None, events=None):
+    """The whole block with the paper's log-domain gains (eqs. (1)-(4))."""
+    import torch
+
+    xx, dt, out = _check(x, out)
+    B, N, C = xx.shape
+    _weight(w_in, C, x, "w_in")
+    _weight(w_out, C, x, "w_out")
+    _gain(log_gain_tokens, (padded_tokens(N),), x, "log_gain_tokens")
+    _gain(log_gain_channels, (C,), x, "log_gain_channels")
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = module_forward_separable_raw(xx.data_ptr(), w_in.data_ptr(),
+                                              log_gain_tokens.data_ptr(),
+                                              log_gain_channels.data_ptr(), w_out.data_ptr(),
+                                              out.data_ptr(), B, N, C, dt, st.cuda_stream,
+                                              plan, events)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_module_forward_separable")
     return out
 
 

@@ -134,6 +134,20 @@ def draw_log_gains(P: int, C: int, seed: int):
     return gt, gc
 
 
+def draw_weights(C: int, dtype: str, seed: int):
+    """Seeded projection weights of the block (eqs. (1), (4)): W_in, W_out
+    float32 [C, C] ~ N(0, 1/C) (variance-preserving, as a trained projection
+    would roughly be), rounded to bf16 when dtype == "bf16"."""
+    rng = np.random.default_rng(seed)
+    s = np.float32(1.0 / np.sqrt(C))
+    w_in = s * rng.standard_normal((C, C), dtype=np.float32)
+    w_out = s * rng.standard_normal((C, C), dtype=np.float32)
+    if dtype == "bf16":
+        w_in = round_to_bf16(w_in, inplace=True)
+        w_out = round_to_bf16(w_out, inplace=True)
+    return np.ascontiguousarray(w_in), np.ascontiguousarray(w_out)
+
+
 def inputs(w: Workload | str):
     """Inputs of a named workload, as (x float32 [B,N,C], g float32 [N,C])."""
     if isinstance(w, str):

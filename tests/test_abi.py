@@ -134,6 +134,49 @@ def test_backward_separable_rejected_before_any_hip_call():
              ALIGNED2 * 2, 1, 64, 64, 0, 0) == 1
 
 
+def mod(x=ALIGNED, wi=ALIGNED2, g=ALIGNED2 * 2, wo=ALIGNED2 * 3, y=ALIGNED, B=1, N=64, C=64,
+        dtype=0, plan="auto"):
+    return whtmix.module_forward_raw(x, wi, g, wo, y, B, N, C, dtype, 0, plan)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(wi=0), 1),
+    (dict(wo=0), 1),
+    (dict(g=0), 1),
+    (dict(x=0), 1),
+    (dict(wi=ALIGNED2 + 8), 4),
+    (dict(wo=ALIGNED2 * 3 + 4), 4),
+    (dict(wi=ALIGNED + 64 * 64 * 4 - 16), 1),  # w_in overlaps y's end
+    (dict(wo=ALIGNED + 256), 1),              # w_out inside y
+    (dict(y=ALIGNED + 64), 1),                # partial overlap of x and y
+    (dict(C=1 << 13, N=1), 7),                # weights of C*C beyond C = 4096
+    (dict(C=48), 2),
+    (dict(dtype=2), 3),
+    (dict(plan=2, N=8, C=8), 1),
+])
+def test_module_rejected_before_any_hip_call(kwargs, status):
+    assert mod(**kwargs) == status
+
+
+def test_module_separable_rejected_before_any_hip_call():
+    f = whtmix.module_forward_separable_raw
+    ok = dict(x=ALIGNED, wi=ALIGNED2, gt=ALIGNED2 * 2, gc=ALIGNED2 * 2 + 4096, wo=ALIGNED2 * 3,
+              y=ALIGNED)
+
+    def call_sep(**kw):
+        a = {**ok, **kw}
+        return f(a["x"], a["wi"], a["gt"], a["gc"], a["wo"], a["y"], 1, 64, 64, 0, 0)
+
+    assert call_sep(gt=0) == 1
+    assert call_sep(gc=0) == 1
+    assert call_sep(gc=ALIGNED + 128) == 1    # channel gains inside y
+    assert call_sep(gt=ALIGNED2 * 2 + 4) == 4
+
+
+def test_module_empty_batch_is_a_no_op():
+    assert whtmix.module_forward_raw(0, 0, 0, 0, 0, 0, 64, 64, 1, 0) == 0
+
+
 def test_padded_plans():
     """Non-power-of-two token counts are zero-padded (section III-B)."""
     for N, C, P in [(3, 4, 4), (5, 1, 8), (9216, 64, 16384), (25600, 64, 32768),

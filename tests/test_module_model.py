@@ -1,0 +1,484 @@
+"""CPU model of the fused block kernels' index arithmetic (no GPU).
+
+The block with its projections (section III-B, eqs. (1)-(4)) runs its MFMA
+prologue and epilogue inside the mixer's kernels.  This file re-derives, in
+numpy, every index the HIP code computes -- the weight repacking, the lane
+layout of the 16x16 matrix-core operands and results, the layout-4 fragments
+of the prologue, the exchange schedules through LDS and the epilogue layout,
+stores and masks -- and checks that the composition reproduces the oracle's
+block on small tiles.  A wrong index here would be a wrong or out-of-bounds
+access on the GPU, so these run before any GPU parity test.
+
+The matrix-core lane layouts used (v_mfma_f32_16x16x16_bf16 and
+v_mfma_f32_16x16x4_f32) are the documented CDNA ones: lane l supplies row
+l%16 of A and column l%16 of B with k = 4*(l//16) + r (bf16, element r) or
+k = l//16 (fp32), and receives D[4*(l//16) + r][l%16] in element r.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle.oracle import Oracle
+from paper_2607_25234_amd.workloads import round_to_bf16
+
+VB = 5
+
+
+def pad(t):
+    return t + (t >> 5)
+
+
+# ------------------------------------------------------------------ matrix core
+def mfma_bf16(a, b, acc):
+    """a, b: [64, 4] lane operands; acc: [64, 4].  16x16x16."""
+    A = np.zeros((16, 16))
+    B = np.zeros((16, 16))
+    for lane in range(64):
+        for r in range(4):
+            A[lane % 16, 4 * (lane // 16) + r] = a[lane, r]
+            B[4 * (lane // 16) + r, lane % 16] = b[lane, r]
+    D = A @ B
+    out = acc.copy()
+    for lane in range(64):
+        for r in range(4):
+            out[lane, r] += D[4 * (lane // 16) + r, lane % 16]
+    return out
+
+
+def mfma_f32(a, b, acc):
+    """a, b: [64] lane operands; acc: [64, 4].  16x16x4."""
+    A = np.zeros((16, 4))
+    B = np.zeros((4, 16))
+    for lane in range(64):
+        A[lane % 16, lane // 16] = a[lane]
+        B[lane // 16, lane % 16] = b[lane]
+    D = A @ B
+    out = acc.copy()
+    for lane in range(64):
+        for r in range(4):
+            out[lane, r] += D[4 * (lane // 16) + r, lane % 16]
+    return out
+
+
+# ------------------------------------------------------------------ packing
+def k_in_bf16(C, kk, q, r):
+    return 32 * (kk >> 1) + 8 * q + 4 * (kk & 1) + r if C >= 32 else 4 * q + r
+
+
+def k_in_f32(s, q):
+    return 16 * (s >> 2) + 4 * q + (s & 3)
+
+
+def oc_bf16(C, nb, m):
+    return 32 * (nb >> 1) + 8 * (m >> 2) + 4 * (nb & 1) + (m & 3) if C >= 32 else m
+
+
+def pack(w_in, w_out, bf):
+    C = w_in.shape[0]
+    p_in = np.empty(C * C)
+    p_out = np.empty(C * C)
+    src_in = np.full(C * C, -1)
+    src_out = np.full(C * C, -1)
+    for idx in range(C * C):
+        e, lane, rest = idx & 3, (idx >> 2) & 63, idx >> 8
+        j, q = lane & 15, lane >> 4
+        if bf:
+            ks = C // 16
+            kk, nb = rest % ks, rest // ks
+            si = k_in_bf16(C, kk, q, e) * C + 16 * nb + j
+            so = (q * (C // 4) + 4 * kk + e) * C + oc_bf16(C, nb, j)
+        else:
+            npc = C // 16
+            p, nb = rest % npc, rest // npc
+            s = 4 * p + e
+            si = k_in_f32(s, q) * C + 16 * nb + j
+            so = (q * (C // 4) + s) * C + 16 * nb + j
+        assert 0 <= si < C * C and 0 <= so < C * C
+        src_in[idx], src_out[idx] = si, so
+        p_in[idx] = w_in.reshape(-1)[si]
+        p_out[idx] = w_out.reshape(-1)[so]
+    # each packed array is a permutation of the weights
+    assert sorted(src_in) == list(range(C * C))
+    assert sorted(src_out) == list(range(C * C))
+    return p_in, p_out
+
+
+# ------------------------------------------------------------------ layouts
+class Std:
+    def __init__(self, S):
+        self.S = S
+
+    def reg(self, j):
+        return self.S + j
+
+    def base(self, tau):
+        S = self.S
+        return (tau & ((1 << S) - 1)) | ((tau >> S) << (S + VB))
+
+
+class Epi:
+    def __init__(self, M, CB):
+        self.M, self.CB = M, CB
+
+    def reg(self, j):
+        CB, M = self.CB, self.M
+        return j if j < CB - 2 else M - 7 + CB + (j - (CB - 2))
+
+    def base(self, tau):
+        CB = self.CB
+        return ((tau & 15) << CB) | (((tau >> 4) & 3) << (CB - 2)) | ((tau >> 6) << (CB + 4))
+
+
+def reg_offset(L, k):
+    t = 0
+    for j in range(VB):
+        if k & (1 << j):
+            t |= 1 << L.reg(j)
+    return t
+
+
+def flat_index(L, M):
+    """[NT, 32] tile index of every (thread, register) of layout L."""
+    NT = 1 << (M - VB)
+    tau = np.arange(NT)
+    t = np.array([[L.base(int(u)) | reg_offset(L, k) for k in range(32)] for u in tau])
+    assert sorted(t.reshape(-1)) == list(range(1 << M)), "layout is not a bijection"
+    return t
+
+
+class Tracker:
+    """Runs register butterflies and LDS exchanges on a [NT, 32] register
+    file, records which tile bits each butterfly step transforms, checks LDS
+    bounds and measures bank conflicts of every LDS access."""
+
+    def __init__(self, M, v, layout):
+        self.M = M
+        self.v = v
+        self.layout = layout
+        self.done = []
+        self.conflicts = []
+
+    def butterflies(self, mask):
+        for j in range(VB):
+            if not mask & (1 << j):
+                continue
+            self.done.append(self.layout.reg(j))
+            for k in range(32):
+                if not k & (1 << j):
+                    a = self.v[:, k].copy()
+                    b = self.v[:, k | (1 << j)].copy()
+                    self.v[:, k] = a + b
+                    self.v[:, k | (1 << j)] = a - b
+
+    def _addresses(self, L):
+        NT = 1 << (self.M - VB)
+        return np.array([[pad(L.base(u)) + pad(reg_offset(L, k)) for k in range(32)]
+                         for u in range(NT)])
+
+    def _conflict(self, addr):
+        worst = 1
+        NT = addr.shape[0]
+        for w in range(0, NT, 64):
+            for k in range(32):
+                banks = addr[w:w + 64, k] % 64
+                worst = max(worst, np.bincount(banks, minlength=64).max())
+        return worst
+
+    def relayout(self, LB):
+        size = pad(1 << self.M)
+        lds = np.full(size, np.nan)
+        wa = self._addresses(self.layout)
+        assert wa.max() < size and wa.min() >= 0
+        assert len(np.unique(wa)) == wa.size, "two registers write one LDS word"
+        lds[wa] = self.v
+        ra = self._addresses(LB)
+        assert ra.max() < size
+        self.v = lds[ra]
+        assert not np.isnan(self.v).any(), "read of an LDS word nobody wrote"
+        self.conflicts.append((self._conflict(wa), self._conflict(ra)))
+        self.layout = LB
+
+
+def forward_from_prologue(tr, M):
+    tr.butterflies(31)
+    tr.relayout(Std(0))
+    tr.butterflies(15)
+    if M <= 14:
+        tr.relayout(Std(M - 5))
+        tr.butterflies(31 & ~((1 << (14 - M)) - 1))
+    else:
+        tr.relayout(Std(5))
+        tr.butterflies(16)
+        tr.relayout(Std(10))
+        tr.butterflies(31)
+
+
+def inverse_to_epilogue(tr, M, CB):
+    ln = M - 3 - CB
+    tr.butterflies((1 << (CB - 2)) - 1)
+    if ln <= VB:
+        tr.relayout(Std(CB - 2))
+        tr.butterflies((1 << ln) - 1)
+    else:
+        tr.relayout(Std(CB - 2))
+        tr.butterflies(31)
+        tr.relayout(Std(CB + 3))
+        tr.butterflies((1 << (ln - VB)) - 1)
+    tr.relayout(Epi(M, CB))
+    tr.butterflies(31)
+
+
+def to_registers(flat, L, M):
+    return flat[flat_index(L, M)]
+
+
+def from_registers(v, L, M):
+    out = np.empty(1 << M)
+    out[flat_index(L, M)] = v
+    return out
+
+
+def wht_bits(flat, M):
+    """Unnormalised Sylvester transform over all M bits."""
+    y = flat.copy()
+    h = 1
+    while h < (1 << M):
+        y = y.reshape(-1, 2, h)
+        y = np.stack([y[:, 0] + y[:, 1], y[:, 0] - y[:, 1]], axis=1).reshape(-1)
+        h *= 2
+    return y
+
+
+# ------------------------------------------------------------------ prologue
+def prologue_token(CB, rb, m, w):
+    return (m & 3) | (rb << 2) | ((m >> 2) << (9 - CB)) | (w << (11 - CB))
+
+
+def model_prologue(xtile, valid, p_in, CB, M, bf):
+    """Registers [NT, 32] of layout 4 holding Z = X W_in of the tile."""
+    C = 1 << CB
+    NT = 1 << (M - VB)
+    NRB = 1 << (7 - CB)
+    NNB = C // 16
+    flat = xtile.reshape(-1)
+    v = np.zeros((NT, 32))
+    for w in range(NT // 64):
+        lanes = np.arange(64)
+        i, q = lanes & 15, lanes >> 4
+
+        def row_of(rb):
+            tok = prologue_token(CB, rb, i, w)
+            rows = np.zeros((64, C))
+            ok = tok * C < valid
+            rows[ok] = flat.reshape(-1, C)[tok[ok]]
+            return rows
+
+        rows = [row_of(rb) for rb in range(NRB)]
+        for nb in range(NNB):
+            for rb in range(NRB):
+                acc = np.zeros((64, 4))
+                if bf:
+                    for kk in range(C // 16):
+                        a = np.array([[rows[rb][l, k_in_bf16(C, kk, q[l], r)] for r in range(4)]
+                                      for l in range(64)])
+                        b = np.array([[p_in[((nb * (C // 16) + kk) * 64 + l) * 4 + r]
+                                       for r in range(4)] for l in range(64)])
+                        acc = mfma_bf16(a, b, acc)
+                else:
+                    for p in range(C // 16):
+                        bvec = np.array([[p_in[((nb * (C // 16) + p) * 64 + l) * 4 + e]
+                                          for e in range(4)] for l in range(64)])
+                        for e in range(4):
+                            s = 4 * p + e
+                            a = np.array([rows[rb][l, k_in_f32(s, q[l])] for l in range(64)])
+                            acc = mfma_f32(a, bvec[:, e], acc)
+                for r in range(4):
+                    v[w * 64:(w + 1) * 64, nb | (r << (CB - 4)) | (rb << (CB - 2))] = acc[:, r]
+    return v
+
+
+# ------------------------------------------------------------------ epilogue
+def split_bf16(z):
+    hi = round_to_bf16(np.asarray(z, dtype=np.float32).copy()).astype(np.float64)
+    lo = round_to_bf16(np.asarray(z - hi, dtype=np.float32).copy()).astype(np.float64)
+    return hi, lo
+
+
+def model_epilogue(v, p_out, CB, M, valid, bf):
+    """Stores of Y = Z' W_out from epilogue-layout registers; returns the
+    tile's output (NaN where nothing was stored) and the byte offsets used."""
+    C = 1 << CB
+    NT = 1 << (M - VB)
+    NRB = 1 << (7 - CB)
+    NNB = C // 16
+    esz = 2 if bf else 4
+    out = np.full((1 << M), np.nan)
+    written = np.zeros(1 << M, dtype=int)
+    rb_bytes = (1 << (M - 7)) * C * esz
+    for w in range(NT // 64):
+        lanes = np.arange(64)
+        j, q = lanes & 15, lanes >> 4
+        row = (j | (w << 4)) * C * esz
+        vw = v[w * 64:(w + 1) * 64]
+        for rb in range(NRB):
+            accs = []
+            for nb in range(NNB):
+                acc = np.zeros((64, 4))
+                if bf:
+                    for kk in range(C // 16):
+                        z = np.stack([vw[:, (4 * kk + e) | (rb << (CB - 2))] for e in range(4)],
+                                     axis=1)
+                        hi, lo = split_bf16(z)
+                        a = np.array([[p_out[((nb * (C // 16) + kk) * 64 + l) * 4 + r]
+                                       for r in range(4)] for l in range(64)])
+                        acc = mfma_bf16(a, hi, acc)
+                        acc = mfma_bf16(a, lo, acc)
+                else:
+                    for p in range(C // 16):
+                        avec = np.array([[p_out[((nb * (C // 16) + p) * 64 + l) * 4 + e]
+                                          for e in range(4)] for l in range(64)])
+                        for e in range(4):
+                            s = 4 * p + e
+                            acc = mfma_f32(avec[:, e], vw[:, s | (rb << (CB - 2))], acc)
+                accs.append(acc)
+
+            def store(byte_off, vals):
+                for l in range(64):
+                    for u, val in enumerate(vals[l]):
+                        off = byte_off[l] + u * esz
+                        assert off % esz == 0
+                        t = off // esz
+                        if off + esz <= valid * esz:     # buffer range check
+                            out[t] = val
+                            written[t] += 1
+
+            if bf and C >= 32:
+                for n in range(NNB // 2):
+                    vals = np.concatenate([accs[2 * n], accs[2 * n + 1]], axis=1)
+                    store(row + 16 * q + rb * rb_bytes + 64 * n, vals)
+            elif bf:
+                store(row + 8 * q + rb * rb_bytes, accs[0])
+            else:
+                for nb in range(NNB):
+                    store(row + 16 * q + rb * rb_bytes + 64 * nb, accs[nb])
+    assert written.max() <= 1, "an element stored twice"
+    assert (written[:valid] == 1).all(), "an element of the tile not stored"
+    return out
+
+
+# ------------------------------------------------------------------ tests
+CASES = [(cb, M, bf) for bf in (True, False) for cb in (4, 5, 6, 7) for M in (11, 12, 13, 14, 15)]
+
+
+def _weights(rng, C):
+    return rng.standard_normal((C, C)) / np.sqrt(C), rng.standard_normal((C, C)) / np.sqrt(C)
+
+
+@pytest.mark.parametrize("CB,bf", [(cb, bf) for bf in (True, False) for cb in (4, 5, 6, 7)])
+def test_packing_is_a_permutation(CB, bf):
+    rng = np.random.default_rng(CB)
+    w_in, w_out = _weights(rng, 1 << CB)
+    pack(w_in, w_out, bf)
+
+
+@pytest.mark.parametrize("CB,M,bf", [c for c in CASES if c[1] in (11, 14)])
+def test_prologue_fragments_are_layout_4(CB, M, bf):
+    """The MFMA result registers, read as layout 4, are Z = X W_in."""
+    rng = np.random.default_rng(100 * CB + M)
+    C = 1 << CB
+    w_in, w_out = _weights(rng, C)
+    p_in, _ = pack(w_in, w_out, bf)
+    rows = (1 << M) // C
+    x = rng.standard_normal((rows, C))
+    valid = (rows - 3) * C          # a ragged tile: the last 3 rows are padding
+    v = model_prologue(x, valid, p_in, CB, M, bf)
+    z = from_registers(v, Std(4), M).reshape(rows, C)
+    ref = x.copy()
+    ref[valid // C:] = 0.0
+    ref = ref @ w_in
+    np.testing.assert_allclose(z, ref, atol=1e-12)
+
+
+@pytest.mark.parametrize("CB,M", [(cb, M) for cb in (4, 5, 6, 7) for M in (11, 12, 13, 14, 15)])
+def test_schedules_cover_every_bit_once(CB, M):
+    """Prologue schedule + epilogue schedule: every tile bit is transformed
+    exactly once in each direction, every exchange is an in-bounds bijection
+    through LDS, and the result equals the full transform."""
+    rng = np.random.default_rng(7 * M + CB)
+    flat = rng.standard_normal(1 << M)
+    tr = Tracker(M, to_registers(flat, Std(4), M), Std(4))
+    forward_from_prologue(tr, M)
+    assert sorted(tr.done) == list(range(M))
+    assert isinstance(tr.layout, Std) and tr.layout.S == M - 5
+    np.testing.assert_allclose(from_registers(tr.v, tr.layout, M), wht_bits(flat, M), atol=1e-9)
+    tr2 = Tracker(M, to_registers(flat, Std(M - 5), M), Std(M - 5))
+    inverse_to_epilogue(tr2, M, CB)
+    assert sorted(tr2.done) == list(range(M))
+    np.testing.assert_allclose(from_registers(tr2.v, Epi(M, CB), M), wht_bits(flat, M),
+                               atol=1e-9)
+    # standard layouts stay conflict-free; the epilogue layout at most 2-way
+    for (wr, rd), L in zip(tr.conflicts + tr2.conflicts, [None] * 99):
+        assert wr <= 2 and rd <= 2
+
+
+@pytest.mark.parametrize("CB,M,bf", [c for c in CASES if c[1] in (11, 13, 15)])
+def test_epilogue_stores_y(CB, M, bf):
+    """Epilogue-layout registers of Z' give Y = Z' W_out, each valid element
+    stored once, nothing stored past the valid rows."""
+    rng = np.random.default_rng(31 * CB + M)
+    C = 1 << CB
+    w_in, w_out = _weights(rng, C)
+    _, p_out = pack(w_in, w_out, bf)
+    rows = (1 << M) // C
+    z = rng.standard_normal((rows, C))
+    valid = (rows - 5) * C
+    v = to_registers(z.reshape(-1), Epi(M, CB), M)
+    y = model_epilogue(v, p_out, CB, M, valid, bf)
+    assert np.isnan(y[valid:]).all()
+    ref = (z @ w_out).reshape(-1)[:valid]
+    tol = 1e-5 if bf else 1e-12      # the two-term bf16 split of Z'
+    np.testing.assert_allclose(y[:valid], ref, atol=tol * np.abs(ref).max())
+
+
+def _block_tile_model(x, w_in, g, w_out, CB, bf):
+    """One slice through the FUSED kernel's steps (M = K)."""
+    C = 1 << CB
+    N = x.shape[0]
+    P = 1 << (N - 1).bit_length()
+    M = (P * C).bit_length() - 1
+    p_in, p_out = pack(w_in, w_out, bf)
+    xt = np.zeros((P, C))
+    xt[:N] = x
+    v = model_prologue(xt, N * C, p_in, CB, M, bf)
+    tr = Tracker(M, v, Std(4))
+    forward_from_prologue(tr, M)
+    gv = to_registers(g.reshape(-1), Std(M - 5), M)
+    tr.v = tr.v * gv / (1 << M)
+    inverse_to_epilogue(tr, M, CB)
+    y = model_epilogue(tr.v, p_out, CB, M, N * C, bf)
+    return y[:N * C].reshape(N, C)
+
+
+@pytest.fixture(scope="module")
+def oracle():
+    return Oracle()
+
+
+@pytest.mark.parametrize("N,CB,bf", [(32, 6, True), (100, 5, False), (16, 7, False),
+                                     (200, 4, True)])
+def test_fused_model_matches_oracle(oracle, N, CB, bf):
+    rng = np.random.default_rng(N + CB)
+    C = 1 << CB
+    P = 1 << (N - 1).bit_length()
+    x = rng.standard_normal((N, C))
+    w_in, w_out = _weights(rng, C)
+    if bf:
+        x = round_to_bf16(x.astype(np.float32)).astype(np.float64)
+        w_in = round_to_bf16(w_in.astype(np.float32)).astype(np.float64)
+        w_out = round_to_bf16(w_out.astype(np.float32)).astype(np.float64)
+    g = rng.uniform(0.5, 1.5, (P, C))
+    y = _block_tile_model(x, w_in, g, w_out, CB, bf)
+    ref = oracle.whtmix_module(x, w_in, g, w_out)
+    tol = 1e-5 if bf else 1e-12
+    np.testing.assert_allclose(y, ref, atol=tol * np.abs(ref).max())
