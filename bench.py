@@ -6,7 +6,8 @@
 A step is one whtmix_forward call (every kernel of the plan) over one batch of
 the workload (default: stereo64k_bf16, B=4, N=65536, C=128, bf16 in/out,
 float32 gain and arithmetic).  --op separable / backward / backward_separable
-time the other entry points the same way.  Inputs are resident in HBM before timing.
+/ module / module_separable time the other entry points the same way (module:
+the whole block with its W_in / W_out projections, eqs. (1)-(4)).  Inputs are resident in HBM before timing.
 Steps rotate over several input/output sets whose total footprint is at
 least twice the 256 MB Infinity Cache, so every step reads x and G from HBM.
 
@@ -32,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak, GB/s
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix-core peaks
 METRIC = "WHTMix forward GB/s and tokens/s at 1 MI355X; % of HBM roofline"
 MALL_BYTES = 256 * 1024 * 1024
 
@@ -65,7 +67,32 @@ def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) ->
             B * L * (4 + s)]           # read workspace, write y
 
 
-OPS = ("forward", "separable", "backward", "backward_separable")
+OPS = ("forward", "separable", "backward", "backward_separable", "module", "module_separable")
+
+
+def module_kernels(plan: str, C: int) -> list[str]:
+    """Kernels between the events of a whtmix_module_forward call (the weight
+    repacking kernel runs before the first event)."""
+    if plan == "small":
+        return ["module_small"]
+    if not 16 <= C <= 128:
+        return ["unfused"]
+    return ["module_outer_fwd", "middle", "module_outer_inv"] if plan == "three_pass" \
+        else ["module_fused"]
+
+
+def module_algorithmic(names: list[str], B: int, N: int, P: int, C: int, s: int,
+                       gbytes: int) -> tuple[list[int], list[int]]:
+    """(bytes, MFMA-eligible flops) each kernel of the block must move / do by
+    its definition: x, the workspace, y, the gain and each weight matrix once;
+    2 N C^2 flops per slice and projection over the real rows."""
+    L = P * C
+    wb = C * C * s
+    proj = 2 * B * N * C * C
+    if names == ["module_outer_fwd", "middle", "module_outer_inv"]:
+        return ([B * N * C * s + B * L * 4 + wb, B * L * 8 + gbytes, B * L * 4 + B * N * C * s + wb],
+                [proj, 0, proj])
+    return [2 * B * N * C * s + 2 * wb + gbytes], [2 * proj]
 
 
 def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
@@ -78,7 +105,12 @@ def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
         return 2 * xy + 4 * (P + C)
     if op == "backward":            # read x, dy, G; write dx, dG
         return 3 * xy + 8 * P * C
-    return 3 * xy + 8 * (P + C)     # backward_separable
+    if op == "backward_separable":
+        return 3 * xy + 8 * (P + C)
+    wb = 2 * C * C * s              # module: also read W_in and W_out
+    if op == "module":
+        return 2 * xy + 4 * P * C + wb
+    return 2 * xy + 4 * (P + C) + wb  # module_separable
 
 
 def load_traffic(kernel: str, workload: str):
@@ -133,12 +165,14 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
     workload's ideal bytes."""
     from oracle import oracle as oracle_mod
     orc = oracle_mod.Oracle()
-    x, g, gt, gc, dy = host0
+    x, g, gt, gc, dy, wi, wo = host0
     call = {
         "forward": lambda: orc.whtmix(x, g),
         "separable": lambda: orc.whtmix_separable(x, gt, gc),
         "backward": lambda: orc.whtmix_grad(x, dy, g),
         "backward_separable": lambda: orc.whtmix_grad_separable(x, dy, gt, gc),
+        "module": lambda: orc.whtmix_module(x, wi, g, wo),
+        "module_separable": lambda: orc.whtmix_module_separable(x, wi, gt, gc, wo),
     }[op]
     runs, t_total = 0, 0.0
     while runs == 0 or (t_total < seconds and runs < 50):
@@ -168,7 +202,8 @@ def main() -> int:
     ap.add_argument("--plan", default="auto")
     ap.add_argument("--op", default="forward", choices=OPS,
                     help="forward (joint gain, the default), separable (log gains), "
-                         "backward, backward_separable")
+                         "backward, backward_separable, module (the block with its "
+                         "projections), module_separable")
     ap.add_argument("--sets", type=int, default=0,
                     help="input/output sets rotated over the steps (0 = auto)")
     ap.add_argument("--event-every", type=int, default=8,
@@ -208,6 +243,9 @@ def main() -> int:
     log(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}; op {op}; plan {plan}; "
         f"{nsets} input sets")
 
+    wi_h, wo_h = workloads.draw_weights(w.C, w.dtype, w.seed + 50)
+    w_in = torch.from_numpy(wi_h).to(dev).to(tdt)
+    w_out = torch.from_numpy(wo_h).to(dev).to(tdt)
     sets = []
     for i in range(nsets):
         if i == 0:
@@ -227,7 +265,8 @@ def main() -> int:
             t["dgt"], t["dgc"] = torch.empty_like(t["gt"]), torch.empty_like(t["gc"])
         sets.append(t)
         if i == 0:
-            host0 = (x[0].copy(), g.copy(), gt, gc, None if dy is None else dy[0].copy())
+            host0 = (x[0].copy(), g.copy(), gt, gc, None if dy is None else dy[0].copy(),
+                     wi_h, wo_h)
         del x, g
     torch.cuda.synchronize()
 
@@ -236,6 +275,9 @@ def main() -> int:
     hip = HipEvents()
     if op.startswith("backward"):
         nk, names = 2, ["gain_gradient", "dx"]
+    elif op.startswith("module"):
+        names = module_kernels(plan["plan"], w.C)
+        nk = len(names)
     else:
         nk, names = plan["kernels"], kernel_names(plan["plan"])
 
@@ -253,6 +295,14 @@ def main() -> int:
             st = whtmix.backward_raw(t["x"].data_ptr(), t["dy"].data_ptr(), t["g"].data_ptr(),
                                      t["y"].data_ptr(), t["dg"].data_ptr(), B, N, C, dt_code,
                                      sptr, args.plan, events)
+        elif op == "module":
+            st = whtmix.module_forward_raw(t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(),
+                                           w_out.data_ptr(), t["y"].data_ptr(), B, N, C,
+                                           dt_code, sptr, args.plan, events)
+        elif op == "module_separable":
+            st = whtmix.module_forward_separable_raw(
+                t["x"].data_ptr(), w_in.data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
+                w_out.data_ptr(), t["y"].data_ptr(), B, N, C, dt_code, sptr, args.plan, events)
         else:
             st = whtmix.backward_separable_raw(
                 t["x"].data_ptr(), t["dy"].data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
@@ -285,9 +335,13 @@ def main() -> int:
     ms_per_step = wall * 1e3 / args.steps
     gbs = io_bytes / (ms_per_step * 1e-3) / 1e9
     tokens = w.B * w.N / (ms_per_step * 1e-3)
+    flops = None
     if op in ("forward", "separable"):
         gbytes = 4 * P * w.C if op == "forward" else 4 * (P + w.C)
         alg = algorithmic_bytes(plan["plan"], w.B, P, w.C, s, gbytes)
+    elif op.startswith("module"):
+        gbytes = 4 * P * w.C if op == "module" else 4 * (P + w.C)
+        alg, flops = module_algorithmic(names, w.B, w.N, P, w.C, s, gbytes)
     else:
         # gain-gradient phase: read x and dy, write the gain gradient;
         # dx phase: the forward mixer applied to dy
@@ -319,6 +373,12 @@ def main() -> int:
         "kernels": [{"name": n, "avg_ms": round(t, 5), "alg_bytes": b,
                      "alg_GBs": round(b / (t * 1e-3) / 1e9, 1)}
                     for n, t, b in zip(names, per_kernel, alg)],
+        "matrix_core": None if flops is None else {
+            "alg_TFLOPs_per_kernel": [round(f / (t * 1e-3) / 1e12, 2)
+                                      for f, t in zip(flops, per_kernel)],
+            "peak_TFLOPs": PEAK_MFMA_TFLOPS[w.dtype],
+            "note": "projection flops (2 N C^2 per slice each) over the kernel time; "
+                    "the kernels stay HBM-bound"},
         "roofline": {"bound": "hbm", "kernel": names[dom],
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic},
