@@ -387,9 +387,9 @@ int module_impl(const void *x, const void *w_in, int gain_kind, const float *gai
     const int path = whtmix::module_path(c.plan, cbits);
     // workspace: mixer (THREE_PASS), then packed weights or Z, 256-byte aligned
     const int64_t mix = path == whtmix::MODULE_SMALL ? 0 : c.ws_bytes;
-    const int64_t extra = path == whtmix::MODULE_FUSED_MFMA ? (int64_t)(2 * wb)
-                          : path == whtmix::MODULE_UNFUSED  ? B * N * C * 4
-                                                            : 0;
+    // FUSED_MFMA: the packed weights; UNFUSED: Z, then the packed weights
+    const int64_t zbytes = path == whtmix::MODULE_UNFUSED ? (B * N * C * 4 + 255) / 256 * 256 : 0;
+    const int64_t extra = path == whtmix::MODULE_SMALL ? 0 : zbytes + (int64_t)(2 * wb);
     const int64_t off = (mix + 255) / 256 * 256;
     std::lock_guard<std::mutex> lock(g_ws_mutex);
     float *ws = nullptr;
@@ -400,7 +400,10 @@ int module_impl(const void *x, const void *w_in, int gain_kind, const float *gai
     m.ws = mix > 0 ? ws : nullptr;
     void *tail = ws ? static_cast<void *>(reinterpret_cast<char *>(ws) + off) : nullptr;
     if (path == whtmix::MODULE_FUSED_MFMA) m.wpack = tail;
-    if (path == whtmix::MODULE_UNFUSED) m.z = static_cast<float *>(tail);
+    if (path == whtmix::MODULE_UNFUSED) {
+        m.z = static_cast<float *>(tail);
+        m.wpack = static_cast<char *>(tail) + zbytes;
+    }
     hipError_t e = whtmix::launch_module(m);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return WHTMIX_SUCCESS;

@@ -97,10 +97,9 @@ inline int module_path(int plan, int cbits)
     return MODULE_UNFUSED;
 }
 
-// A validated call of the block.  Workspace (module_ws_bytes): the
-// THREE_PASS workspace `ws` (B * 2^K floats, else none), then `wpack` (the
-// two repacked weight matrices, FUSED_MFMA) or `z` (B * N * C floats,
-// UNFUSED).
+// A validated call of the block.  Workspace: the THREE_PASS workspace `ws`
+// (B * 2^K floats, else none), then for UNFUSED `z` (B * N * C floats), then
+// `wpack` (the two repacked weight matrices; not SMALL).
 struct ModuleArgs {
     const void *x;
     const void *w_in;       // [C][C], dtype of x

@@ -29,7 +29,8 @@
 //   THREE_PASS  prologue in the first outer pass, the unchanged middle pass,
 //               epilogue in the second outer pass.
 //   SMALL       K <= 10: one LDS-resident workgroup per slice, VALU products.
-//   UNFUSED     any other C: projection kernels around the fp32 mixer.
+//   UNFUSED     any other C: projection kernels around the fp32 mixer (on the
+//               matrix cores for C >= 256 where a weight slice fits LDS).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -197,11 +198,12 @@ __host__ __device__ constexpr uint32_t oc_bf16(uint32_t C, uint32_t nb, uint32_t
 // One thread per packed element.  Packed index = ((nb * KS + kk) * 64 + lane)
 // * 4 + r with lane = 16 q + j (bf16), or ((nb * C/16 + p) * 64 + lane) * 4 + e
 // with step s = 4p + e (fp32).  W_in feeds the B operand of Z = X W_in
-// (column 16 nb + j); W_out feeds the A operand of Y^T = W_out^T Z'^T.
+// (column 16 nb + j); W_out feeds the A operand of Y^T = W_out^T Z'^T, or
+// (out_as_in) the B operand of Y = Z' W_out like W_in.
 template <typename T>
 __global__ void __launch_bounds__(256)
 pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *__restrict__ p_in,
-                    T *__restrict__ p_out, int cb)
+                    T *__restrict__ p_out, int cb, int out_as_in)
 {
     const uint32_t C = 1u << cb;
     const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
@@ -213,14 +215,17 @@ pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *
     if constexpr (sizeof(T) == 2) {
         const uint32_t ks = C / 16u;
         const uint32_t kk = rest % ks, nb = rest / ks;
-        p_in[idx] = w_in[k_in_bf16(C, kk, q, e) * C + 16u * nb + j];
-        p_out[idx] = w_out[(q * (C / 4u) + 4u * kk + e) * C + oc_bf16(C, nb, j)];
+        const uint32_t src = k_in_bf16(C, kk, q, e) * C + 16u * nb + j;
+        p_in[idx] = w_in[src];
+        p_out[idx] = out_as_in ? w_out[src]
+                               : w_out[(q * (C / 4u) + 4u * kk + e) * C + oc_bf16(C, nb, j)];
     } else {
         const uint32_t np = C / 16u;
         const uint32_t p = rest % np, nb = rest / np;
         const uint32_t s = 4u * p + e;
-        p_in[idx] = w_in[k_in_f32(s, q) * C + 16u * nb + j];
-        p_out[idx] = w_out[(q * (C / 4u) + s) * C + 16u * nb + j];
+        const uint32_t src = k_in_f32(s, q) * C + 16u * nb + j;
+        p_in[idx] = w_in[src];
+        p_out[idx] = out_as_in ? w_out[src] : w_out[(q * (C / 4u) + s) * C + 16u * nb + j];
     }
 }
 
@@ -673,6 +678,176 @@ project_rows_kernel(const Tin *__restrict__ in, const Tw *__restrict__ w, Tout *
     out[i] = (Tout)acc;
 }
 
+// UNFUSED projection on the matrix cores, out[row][c] = sum_k in[row][k] W[k][c],
+// for C >= 256 (the fused layouts cover 16..128).  W is packed in the
+// prologue's operand order, where the NCOL columns of a slice are contiguous.
+// Workgroup (g, slice) stages its slice into LDS once and loops over blocks of
+// 64 rows, 16 per wave.  Operands as in the prologue: bf16 rows against bf16
+// weights; float rows against bf16 weights split as hi + lo; float against
+// float on the fp32 instruction.
+template <typename Tw, int CB>
+struct ProjCols {
+    static constexpr int C = 1 << CB;
+    static constexpr int raw = 65536 / (C * (int)sizeof(Tw));
+    static constexpr int NCOL = raw > 128 ? 128 : (raw < 16 ? 16 : raw);
+    static constexpr uint32_t WSLICE = (uint32_t)C * NCOL * sizeof(Tw);
+    static constexpr bool OK = WSLICE <= 128u * 1024u && C >= 256;
+};
+
+__device__ __forceinline__ void split_bf16(const f32x4 &z, bf16x4 &hi, bf16x4 &lo)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const __bf16 h = (__bf16)z[e];
+        hi[e] = __builtin_bit_cast(short, h);
+        lo[e] = __builtin_bit_cast(short, (__bf16)(z[e] - (float)h));
+    }
+}
+
+// Operand pieces of the projection kernel: one 16-byte load per lane per
+// piece.  bf16 rows: piece p holds channels 32p + 8q + [0, 8), the k values of
+// steps 2p and 2p+1.  Float rows: piece u holds 4 channels, 32(u/2) + 8q +
+// 4(u%2) + [0, 4) against bf16 weights (step u) or 16u + 4q + [0, 4) against
+// float weights (steps 4u .. 4u+3).  A chunk is 256 channels of a row.
+template <typename Tin, typename Tw>
+struct ProjMode {
+    static constexpr bool BFW = sizeof(Tw) == 2;
+    static constexpr bool BFIN = sizeof(Tin) == 2;
+    static constexpr int NPC = BFIN ? 8 : 16;   // pieces per chunk
+    __device__ static uint32_t channel(uint32_t piece, uint32_t q)
+    {
+        if constexpr (BFIN) return 32u * piece + 8u * q;
+        else if constexpr (BFW) return 32u * (piece >> 1) + 8u * q + 4u * (piece & 1u);
+        else return 16u * piece + 4u * q;
+    }
+};
+
+template <typename Tin, typename Tout, typename Tw, int CB>
+__global__ void __launch_bounds__(256)
+project_mfma_kernel(const Tin *__restrict__ in, const Tw *__restrict__ wpk, Tout *__restrict__ out,
+                    uint32_t rows)
+{
+    using PC = ProjCols<Tw, CB>;
+    using PM = ProjMode<Tin, Tw>;
+    constexpr int C = PC::C;
+    constexpr int NB = PC::NCOL / 16;
+    constexpr int KS = PM::BFW ? C / 16 : C / 4;   // k steps of one column block
+    constexpr int NCH = C / 256;                   // chunks of 256 channels per row
+    constexpr int NPC = PM::NPC;
+    static_assert(PC::OK, "weight slice must fit LDS");
+    static_assert(NCH >= 1, "C >= 256");
+    __shared__ __attribute__((aligned(16))) unsigned char lds[PC::WSLICE];
+    const uint32_t tau = threadIdx.x, lane = tau & 63u, w = tau >> 6;
+    const uint32_t i = lane & 15u, q = lane >> 4;
+    const uint32_t slice = blockIdx.y;
+    // the slice's column blocks are contiguous in the packed matrix
+    stage_weights<PC::WSLICE / 16, 256>(lds, wpk + (size_t)slice * PC::NCOL * C, tau);
+    __syncthreads();
+
+    // step t: row block blockIdx.x + (t / NCH) * gridDim.x, chunk t % NCH
+    const uint32_t nblk = (rows + 63u) / 64u;
+    const uint32_t mine = blockIdx.x < nblk ? (nblk - 1u - blockIdx.x) / gridDim.x + 1u : 0u;
+    const uint32_t T = mine * NCH;
+    auto load = [&](u32x4 (&buf)[NPC], uint32_t t) {
+        const uint32_t blk = blockIdx.x + (t / NCH) * gridDim.x;
+        const uint32_t row = blk * 64u + w * 16u + i;
+        const uint32_t c0 = (t % NCH) * 256u;
+        const Tin *src = in + (size_t)row * C + c0;
+#pragma unroll
+        for (int u = 0; u < NPC; ++u) {
+            buf[u] = (u32x4){0u, 0u, 0u, 0u};
+            if (row < rows)
+                buf[u] = *reinterpret_cast<const u32x4 *>(src + PM::channel(u, q));
+        }
+    };
+    f32x4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+        acc[nb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+    auto compute = [&](const u32x4 (&buf)[NPC], uint32_t t) {
+        const uint32_t ch = t % NCH;
+        if constexpr (PM::BFW && PM::BFIN) {
+            const bf16x4 *wb = reinterpret_cast<const bf16x4 *>(lds);
+#pragma unroll
+            for (int u = 0; u < NPC; ++u) {
+                const uint32_t kk = 2u * (ch * NPC + u);
+                const bf16x4 a0 = __builtin_bit_cast(bf16x4, (u32x2){buf[u].x, buf[u].y});
+                const bf16x4 a1 = __builtin_bit_cast(bf16x4, (u32x2){buf[u].z, buf[u].w});
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                        a0, wb[(nb * KS + kk) * 64 + lane], acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                        a1, wb[(nb * KS + kk + 1) * 64 + lane], acc[nb], 0, 0, 0);
+                }
+                // keep the weight reads of later pieces below this piece's MFMAs
+                // (hoisting them all costs registers and occupancy)
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else if constexpr (PM::BFW) {
+            const bf16x4 *wb = reinterpret_cast<const bf16x4 *>(lds);
+#pragma unroll
+            for (int u = 0; u < NPC; ++u) {
+                const uint32_t kk = ch * NPC + u;
+                bf16x4 hi, lo;
+                split_bf16(__builtin_bit_cast(f32x4, buf[u]), hi, lo);
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const bf16x4 b = wb[(nb * KS + kk) * 64 + lane];
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(hi, b, acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(lo, b, acc[nb], 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            const f32x4 *wf = reinterpret_cast<const f32x4 *>(lds);
+#pragma unroll
+            for (int u = 0; u < NPC; ++u) {
+                const uint32_t p = ch * NPC + u;
+                const f32x4 a = __builtin_bit_cast(f32x4, buf[u]);
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const f32x4 b = wf[(nb * (C / 16) + p) * 64 + lane];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], acc[nb], 0, 0,
+                                                                       0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if (ch == NCH - 1) {
+            // lane 16 q + j holds rows 4q + r of column 16 nb + j
+            const uint32_t blk = blockIdx.x + (t / NCH) * gridDim.x;
+            const uint32_t r0 = blk * 64u + w * 16u;
+            const uint32_t col = slice * PC::NCOL + i;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t row = r0 + 4u * q + r;
+                if (row < rows) {
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+                        out[(size_t)row * C + col + 16u * nb] = (Tout)acc[nb][r];
+                }
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+        }
+    };
+    // two buffers: the next step's pieces load while this step computes
+    u32x4 b0[NPC], b1[NPC];
+    if (T > 0) load(b0, 0);
+    for (uint32_t t = 0; t < T; t += 2) {
+        if (t + 1 < T) load(b1, t + 1);
+        compute(b0, t);
+        if (t + 1 < T) {
+            if (t + 2 < T) load(b0, t + 2);
+            compute(b1, t + 1);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- launchers
 inline hipError_t record(hipEvent_t ev, hipStream_t st)
 {
@@ -680,12 +855,13 @@ inline hipError_t record(hipEvent_t ev, hipStream_t st)
 }
 
 template <typename T>
-hipError_t launch_pack(const ModuleArgs &m)
+hipError_t launch_pack(const ModuleArgs &m, bool out_as_in)
 {
     const uint32_t n = 1u << (2 * m.cbits);
     hipLaunchKernelGGL((pack_weights_kernel<T>), dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
                        static_cast<const T *>(m.w_in), static_cast<const T *>(m.w_out),
-                       static_cast<T *>(m.wpack), static_cast<T *>(m.wpack) + n, m.cbits);
+                       static_cast<T *>(m.wpack), static_cast<T *>(m.wpack) + n, m.cbits,
+                       out_as_in ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -767,7 +943,7 @@ hipError_t dispatch_k(const ModuleArgs &m, Gain gain)
 template <typename T, class Gain>
 hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
 {
-    hipError_t e = launch_pack<T>(m);
+    hipError_t e = launch_pack<T>(m, false);
     if (e != hipSuccess) return e;
     switch (m.cbits) {
     case 4: return dispatch_k<T, Gain, 4>(m, gain);
@@ -792,19 +968,40 @@ hipError_t launch_module_small(const ModuleArgs &m, Gain gain)
 }
 
 // UNFUSED: z = x W_in (fp32, in the workspace), the fp32 mixer in place on
-// z, y = z W_out.
+// z, y = z W_out.  Projections on the matrix cores where a weight slice fits
+// LDS (C >= 256 here), else one thread per output on the VALU.
+template <typename T, int CB>
+hipError_t project_pair_mfma(const ModuleArgs &m, LaunchArgs &mix)
+{
+    using PC = ProjCols<T, CB>;
+    const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> CB);
+    const uint32_t slices = PC::C / PC::NCOL;
+    const uint32_t nblk = (rows + 63u) / 64u;
+    uint32_t gx = 512u / slices;
+    gx = gx < 1u ? 1u : (gx > nblk ? nblk : gx);
+    const dim3 grid(gx, slices);
+    const T *pin = static_cast<const T *>(m.wpack);
+    const T *pout = pin + ((size_t)1 << (2 * CB));
+    const hipStream_t st = m.stream;
+    hipError_t e = launch_pack<T>(m, true);
+    if (e != hipSuccess) return e;
+    if ((e = record(m.events[0], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((project_mfma_kernel<T, float, T, CB>), grid, dim3(256), 0, st,
+                       static_cast<const T *>(m.x), pin, m.z, rows);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch(mix)) != hipSuccess) return e;
+    hipLaunchKernelGGL((project_mfma_kernel<float, T, T, CB>), grid, dim3(256), 0, st, m.z, pout,
+                       static_cast<T *>(m.y), rows);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[1], st);
+}
+
 template <typename T>
 hipError_t launch_module_unfused(const ModuleArgs &m)
 {
     const uint64_t total = (uint64_t)m.B * m.nvalid;
     const uint32_t blocks = (uint32_t)((total + 255u) / 256u);
     const hipStream_t st = m.stream;
-    hipError_t e = record(m.events[0], st);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((project_rows_kernel<T, float, T>), dim3(blocks), dim3(256), 0, st,
-                       static_cast<const T *>(m.x), static_cast<const T *>(m.w_in), m.z, total,
-                       m.cbits);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     LaunchArgs a{};
     a.x = m.z;
     a.y = m.z;
@@ -820,6 +1017,22 @@ hipError_t launch_module_unfused(const ModuleArgs &m)
     a.dtype = DTYPE_F32;
     a.plan = m.plan;
     a.stream = st;
+    switch (m.cbits) {
+#define WHTMIX_PM_CASE(cb) \
+    case cb:               \
+        if constexpr (ProjCols<T, cb>::OK) return project_pair_mfma<T, cb>(m, a); \
+        break;
+        WHTMIX_PM_CASE(8) WHTMIX_PM_CASE(9) WHTMIX_PM_CASE(10) WHTMIX_PM_CASE(11)
+        WHTMIX_PM_CASE(12)
+#undef WHTMIX_PM_CASE
+    default: break;
+    }
+    hipError_t e = record(m.events[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((project_rows_kernel<T, float, T>), dim3(blocks), dim3(256), 0, st,
+                       static_cast<const T *>(m.x), static_cast<const T *>(m.w_in), m.z, total,
+                       m.cbits);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch(a)) != hipSuccess) return e;
     hipLaunchKernelGGL((project_rows_kernel<float, T, T>), dim3(blocks), dim3(256), 0, st, m.z,
                        static_cast<const T *>(m.w_out), static_cast<T *>(m.y), total, m.cbits);

@@ -95,8 +95,10 @@ SHAPES = [
     # THREE_PASS with MFMA projections
     (2, 4096, 16), (1, 3000, 32), (2, 2048, 128), (1, 9216, 64), (1, 8192, 128),
     (1, 1 << 15, 32),
-    # UNFUSED: C outside [16, 128]
-    (2, 512, 8), (1, 64, 256), (1, 1024, 256), (1, 8, 512), (1, 3, 1024),
+    # UNFUSED: C outside [16, 128] (matrix-core projections from C = 256; VALU below 16
+    # and for float32 C = 4096, whose weight slice does not fit LDS)
+    (2, 512, 8), (1, 64, 256), (3, 1000, 256), (1, 8, 512), (1, 3, 1024), (1, 16, 2048),
+    (1, 4, 4096),
 ]
 
 

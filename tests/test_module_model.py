@@ -482,3 +482,81 @@ def test_fused_model_matches_oracle(oracle, N, CB, bf):
     ref = oracle.whtmix_module(x, w_in, g, w_out)
     tol = 1e-5 if bf else 1e-12
     np.testing.assert_allclose(y, ref, atol=tol * np.abs(ref).max())
+
+
+# ------------------------------------------------------------------ UNFUSED MFMA projection
+def model_project(inp, w, bf_w, in_bf, CB):
+    """project_mfma_kernel: column slices of NCOL, 64-row blocks, 16 rows per
+    wave, weights in the prologue's packed order."""
+    C = 1 << CB
+    s = 2 if bf_w else 4
+    NCOL = min(128, max(16, 65536 // (C * s)))
+    NB = NCOL // 16
+    KS = C // 16 if bf_w else C // 4
+    packed, _ = pack(w, w, bf_w)
+    rows = inp.shape[0]
+    out = np.full((rows, C), np.nan)
+    lanes = np.arange(64)
+    i, q = lanes & 15, lanes >> 4
+    for sl in range(C // NCOL):
+        wsl = packed[sl * NCOL * C:(sl + 1) * NCOL * C]
+        for blk in range((rows + 63) // 64):
+            for wv in range(4):
+                r0 = blk * 64 + wv * 16
+                ok = r0 + i < rows
+                A = np.zeros((64, C))
+                A[ok] = inp[(r0 + i)[ok]]
+                acc = [np.zeros((64, 4)) for _ in range(NB)]
+
+                def wfrag(idx0):
+                    return np.array([[wsl[(idx0 * 64 + l) * 4 + r] for r in range(4)]
+                                     for l in range(64)])
+                if bf_w:
+                    for p in range(C // 32):
+                        cols = 32 * p + 8 * q[:, None] + np.arange(8)[None, :]
+                        piece = A[lanes[:, None], cols]
+                        parts = [piece[:, :4], piece[:, 4:]]
+                        for nb in range(NB):
+                            for h in range(2):
+                                b = wfrag(nb * KS + 2 * p + h)
+                                if in_bf:
+                                    acc[nb] = mfma_bf16(parts[h], b, acc[nb])
+                                else:
+                                    hi, lo = split_bf16(parts[h])
+                                    acc[nb] = mfma_bf16(hi, b, acc[nb])
+                                    acc[nb] = mfma_bf16(lo, b, acc[nb])
+                else:
+                    for p in range(C // 16):
+                        cols = 16 * p + 4 * q[:, None] + np.arange(4)[None, :]
+                        a = A[lanes[:, None], cols]
+                        for nb in range(NB):
+                            b = wfrag(nb * (C // 16) + p)
+                            for e in range(4):
+                                acc[nb] = mfma_f32(a[:, e], b[:, e], acc[nb])
+                for r in range(4):
+                    row = r0 + 4 * q + r
+                    for nb in range(NB):
+                        m = row < rows
+                        out[row[m], (sl * NCOL + i + 16 * nb)[m]] = acc[nb][m, r]
+    return out
+
+
+@pytest.mark.parametrize("CB,bf_w,in_bf", [(8, True, True), (8, True, False), (8, False, False),
+                                           (9, True, True), (9, False, False)])
+def test_unfused_projection_model(CB, bf_w, in_bf):
+    rng = np.random.default_rng(CB * 10 + bf_w + 2 * in_bf)
+    C = 1 << CB
+    rows = 83                    # a ragged last block
+    x = rng.standard_normal((rows, C))
+    w = rng.standard_normal((C, C)) / np.sqrt(C)
+    if bf_w:
+        w = round_to_bf16(w.astype(np.float32)).astype(np.float64)
+    if in_bf:
+        x = round_to_bf16(x.astype(np.float32)).astype(np.float64)
+    else:
+        x = x.astype(np.float32).astype(np.float64)
+    y = model_project(x, w, bf_w, in_bf, CB)
+    assert not np.isnan(y).any(), "an output element never stored"
+    ref = x @ w
+    tol = 1e-5 if (bf_w and not in_bf) else 1e-12
+    np.testing.assert_allclose(y, ref, atol=tol * np.abs(ref).max())
