@@ -42,11 +42,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+# Sources the kernels of each path are compiled from: a counter record taken
+# on other sources is not reported.
+FORWARD_SOURCES = ("whtmix_kernels.hip", "whtmix_tile.h", "whtmix_plan.h", "whtmix_launch.h")
+MODULE_SOURCES = FORWARD_SOURCES + ("whtmix_module.hip", "whtmix_module.h")
+
+
+def kernel_source_hash(files=FORWARD_SOURCES) -> str:
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2607_25234_amd", "csrc", "*"))):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode())
+    for name in sorted(files):
+        with open(os.path.join(ROOT, "paper_2607_25234_amd", "csrc", name), "rb") as f:
+            h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
@@ -113,18 +119,23 @@ def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
     return 2 * xy + 4 * (P + C) + wb  # module_separable
 
 
-def load_traffic(kernel: str, workload: str):
+TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def load_traffic(kernel: str, workload: str, op: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
     taken on the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
+    path = TRAFFIC_PATH
+    if not os.path.exists(path) or op not in ("forward", "module"):
         return None
     with open(path) as f:
         data = json.load(f)
-    if data.get("source_hash") != kernel_source_hash():
+    files = FORWARD_SOURCES if op == "forward" else MODULE_SOURCES
+    hashes = data.get("source_hash")
+    if not isinstance(hashes, dict) or hashes.get(op) != kernel_source_hash(files):
         return None
-    entry = data.get("workloads", {}).get(workload, {}).get(kernel)
-    return None if entry is None else entry.get("hbm_bytes_per_launch")
+    entry = data.get("workloads", {}).get(workload, {}).get(op, {}).get(kernel)
+    return None if not isinstance(entry, dict) else entry.get("hbm_bytes_per_launch")
 
 
 class HipEvents:
@@ -349,7 +360,7 @@ def main() -> int:
         alg = [2 * w.B * w.N * w.C * s + gb, 2 * w.B * w.N * w.C * s + gb]
     dom = int(np.argmax(per_kernel))
     achieved = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9
-    traffic = load_traffic(names[dom], name) if op == "forward" else None
+    traffic = load_traffic(names[dom], name, op)
 
     out = {
         "metric": METRIC,

@@ -57,6 +57,10 @@ def load(path: str = LIB):
     lib.oracle_whtmix_module.restype = ctypes.c_int
     lib.oracle_whtmix_module_separable.argtypes = [dp, dp, dp, dp, dp, dp, L, L, L]
     lib.oracle_whtmix_module_separable.restype = ctypes.c_int
+    lib.oracle_whtmix_module_grad.argtypes = [dp, dp, dp, dp, dp, dp, dp, dp, dp, L, L, L]
+    lib.oracle_whtmix_module_grad.restype = ctypes.c_int
+    lib.oracle_whtmix_module_grad_separable.argtypes = [dp] * 11 + [L, L, L]
+    lib.oracle_whtmix_module_grad_separable.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
     if path == LIB:
@@ -202,6 +206,47 @@ class Oracle:
         if rc != 0:
             raise ValueError(f"oracle_whtmix_module_separable rejected {(B, N, C)}")
         return y[0] if squeeze else y
+
+    def _module_grad_args(self, x, w_in, w_out, dy):
+        x64, dy64 = _as_f64(x), _as_f64(dy)
+        squeeze = x64.ndim == 2
+        if squeeze:
+            x64, dy64 = x64[None], dy64[None]
+        B, N, C = x64.shape
+        wi, wo = _as_f64(w_in), _as_f64(w_out)
+        if wi.shape != (C, C) or wo.shape != (C, C) or dy64.shape != x64.shape:
+            raise ValueError("w_in, w_out must be [C, C] and dy like x")
+        return x64, dy64, wi, wo, squeeze, (B, N, C)
+
+    def whtmix_module_grad(self, x, w_in, g, w_out, dy):
+        """(dX, dW_in, dW_out, dG) of the block (joint gain) for upstream dY."""
+        x64, dy64, wi, wo, squeeze, (B, N, C) = self._module_grad_args(x, w_in, w_out, dy)
+        g64 = _as_f64(g)
+        if g64.shape != (padded(N), C):
+            raise ValueError("gain must be [P, C]")
+        dx, dwi, dwo, dg = (np.empty_like(x64), np.empty_like(wi), np.empty_like(wo),
+                            np.empty_like(g64))
+        rc = self.lib.oracle_whtmix_module_grad(_dptr(x64), _dptr(wi), _dptr(g64), _dptr(wo),
+                                                _dptr(dy64), _dptr(dx), _dptr(dwi),
+                                                _dptr(dwo), _dptr(dg), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_module_grad rejected {(B, N, C)}")
+        return (dx[0] if squeeze else dx), dwi, dwo, dg
+
+    def whtmix_module_grad_separable(self, x, w_in, g_t, g_c, w_out, dy):
+        """(dX, dW_in, dW_out, dg_t, dg_c) of the block with log gains."""
+        x64, dy64, wi, wo, squeeze, (B, N, C) = self._module_grad_args(x, w_in, w_out, dy)
+        gt, gc = _as_f64(g_t).reshape(-1), _as_f64(g_c).reshape(-1)
+        if gt.shape != (padded(N),) or gc.shape != (C,):
+            raise ValueError("g_t must have P entries and g_c C entries")
+        dx, dwi, dwo = np.empty_like(x64), np.empty_like(wi), np.empty_like(wo)
+        dgt, dgc = np.empty_like(gt), np.empty_like(gc)
+        rc = self.lib.oracle_whtmix_module_grad_separable(
+            _dptr(x64), _dptr(wi), _dptr(gt), _dptr(gc), _dptr(wo), _dptr(dy64), _dptr(dx),
+            _dptr(dwi), _dptr(dwo), _dptr(dgt), _dptr(dgc), B, N, C)
+        if rc != 0:
+            raise ValueError(f"oracle_whtmix_module_grad_separable rejected {(B, N, C)}")
+        return (dx[0] if squeeze else dx), dwi, dwo, dgt, dgc
 
     def fwht(self, v) -> np.ndarray:
         """Unnormalised Sylvester butterfly of a 1-D vector (H_n v, +/-1 H)."""

@@ -325,6 +325,107 @@ int oracle_whtmix_grad_separable(const double *x, const double *dy,
     return 0;
 }
 
+/* Backward through a projection: Z[n][i] = sum over j of X[n][j] W[i][j],
+ * i.e. Z = X W^T with W [C][C] row-major (each sum over j ascending). */
+static void project_t(const double *x, const double *w, double *z, long N, long C)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; ++n)
+        for (long i = 0; i < C; ++i) {
+            double s = 0.0;
+            for (long j = 0; j < C; ++j)
+                s += x[n * C + j] * w[i * C + j];
+            z[n * C + i] = s;
+        }
+}
+
+/* Weight gradient of a projection: acc[i][j] += sum over n of a[n][i] b[n][j]
+ * (acc = A^T B; each row i of acc belongs to one thread, n ascending). */
+static void accumulate_at_b(const double *a, const double *b, double *acc, long N, long C)
+{
+#pragma omp parallel for schedule(static)
+    for (long i = 0; i < C; ++i)
+        for (long n = 0; n < N; ++n) {
+            const double ai = a[n * C + i];
+            for (long j = 0; j < C; ++j)
+                acc[i * C + j] += ai * b[n * C + j];
+        }
+}
+
+/* Gradients of the whole block, eqs. (1)-(4), for an upstream gradient dY:
+ *   Z = X W_in, Z' = mixer(Z), Y = Z' W_out  (forward, recomputed here);
+ *   dZ' = dY W_out^T;      dW_out = sum over b of Z'^T dY;
+ *   dZ and the gain gradient from the mixer's own gradient at (Z, dZ');
+ *   dX = dZ W_in^T;        dW_in = sum over b of X^T dZ.
+ * Joint gain g [P][C] (dg), or separable log gains when g is NULL (dgt, dgc). */
+static int module_grad_impl(const double *x, const double *w_in, const double *g,
+                            const double *g_t, const double *g_c, const double *w_out,
+                            const double *dy, double *dx, double *dw_in, double *dw_out,
+                            double *dg, double *dgt, double *dgc, long B, long N, long C)
+{
+    if (!x || !w_in || !w_out || !dy || !dx || !dw_in || !dw_out || B < 0 || N < 1 ||
+        !is_pow2(C))
+        return -1;
+    const size_t n = (size_t)(B * N * C);
+    double *z = malloc((n ? n : 1) * sizeof(double));
+    double *zp = malloc((n ? n : 1) * sizeof(double));
+    double *dzp = malloc((n ? n : 1) * sizeof(double));
+    double *dz = malloc((n ? n : 1) * sizeof(double));
+    int rc = (z && zp && dzp && dz) ? 0 : -1;
+    const long S = N * C;
+    for (long b = 0; b < B && rc == 0; ++b)
+        project(x + b * S, w_in, z + b * S, N, C);                          /* eq. (1) */
+    if (rc == 0)
+        rc = g ? oracle_whtmix(z, g, zp, B, N, C)                          /* eqs. (2)-(3) */
+               : oracle_whtmix_separable(z, g_t, g_c, zp, B, N, C);
+    for (long b = 0; b < B && rc == 0; ++b)
+        project_t(dy + b * S, w_out, dzp + b * S, N, C);                   /* through eq. (4) */
+    if (rc == 0) {
+        for (long i = 0; i < C * C; ++i)
+            dw_out[i] = 0.0;
+        for (long b = 0; b < B; ++b)
+            accumulate_at_b(zp + b * S, dy + b * S, dw_out, N, C);
+        rc = g ? oracle_whtmix_grad(z, dzp, g, dz, dg, B, N, C)
+               : oracle_whtmix_grad_separable(z, dzp, g_t, g_c, dz, dgt, dgc, B, N, C);
+    }
+    for (long b = 0; b < B && rc == 0; ++b)
+        project_t(dz + b * S, w_in, dx + b * S, N, C);                     /* through eq. (1) */
+    if (rc == 0) {
+        for (long i = 0; i < C * C; ++i)
+            dw_in[i] = 0.0;
+        for (long b = 0; b < B; ++b)
+            accumulate_at_b(x + b * S, dz + b * S, dw_in, N, C);
+    }
+    free(z);
+    free(zp);
+    free(dzp);
+    free(dz);
+    return rc;
+}
+
+int oracle_whtmix_module_grad(const double *x, const double *w_in, const double *g,
+                              const double *w_out, const double *dy, double *dx,
+                              double *dw_in, double *dw_out, double *dg, long B, long N,
+                              long C)
+{
+    if (!g || !dg)
+        return -1;
+    return module_grad_impl(x, w_in, g, NULL, NULL, w_out, dy, dx, dw_in, dw_out, dg, NULL,
+                            NULL, B, N, C);
+}
+
+int oracle_whtmix_module_grad_separable(const double *x, const double *w_in,
+                                        const double *g_t, const double *g_c,
+                                        const double *w_out, const double *dy, double *dx,
+                                        double *dw_in, double *dw_out, double *dgt,
+                                        double *dgc, long B, long N, long C)
+{
+    if (!g_t || !g_c || !dgt || !dgc)
+        return -1;
+    return module_grad_impl(x, w_in, NULL, g_t, g_c, w_out, dy, dx, dw_in, dw_out, NULL, dgt,
+                            dgc, B, N, C);
+}
+
 /* Bare unnormalised butterfly over a contiguous vector, exported so that the
  * tests can pin the transform itself against a dense Sylvester matrix. */
 int oracle_fwht(double *v, long n)

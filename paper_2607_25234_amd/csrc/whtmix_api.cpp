@@ -11,6 +11,7 @@
 
 #include "whtmix.h"
 #include "whtmix_launch.h"
+#include "whtmix_module.h"
 #include "whtmix_plan.h"
 
 namespace {

@@ -35,6 +35,7 @@
 #include <stdint.h>
 
 #include "whtmix_launch.h"
+#include "whtmix_module.h"
 #include "whtmix_plan.h"
 #include "whtmix_tile.h"
 

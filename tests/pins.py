@@ -20,7 +20,8 @@ that does not depend on the oracle's code:
 * the backward pass (dX, dG and the separable log-gain gradients) against
   dense products and against finite differences of the forward mixer;
 * the full block of eqs. (1)-(4) (projections W_in, W_out around the mixer)
-  against dense products.
+  against dense products, and its gradients against an explicit dense
+  operator and finite differences.
 
 The same functions run against the real oracle (``test_oracle_pins.py``) and
 against deliberately broken copies of it (``test_oracle_mutants.py``), which
@@ -359,6 +360,78 @@ def pin_module_dense(o) -> None:
         assert _rel(o.whtmix_module(x, eye, g, eye), o.whtmix(x, g)) < 1e-13
 
 
+def pin_module_grad(o) -> None:
+    """Gradients of the block, eqs. (1)-(4), for L = sum_b <dY_b, Y_b>.
+    dense: the mixer is written out as an explicit (N C) x (N C) matrix M built
+    from dense Hadamard products, and the chain rule is applied with M^T (no use
+    of self-adjointness): dZ' = dY W_out^T, dW_out = sum Z'^T dY, dZ = M^T dZ',
+    dX = dZ W_in^T, dW_in = sum X^T dZ.  finite differences: L is linear in
+    each of X, W_in, W_out and G, so unit central differences are exact up to
+    rounding; in the log gains it is smooth (small step)."""
+    rng = np.random.default_rng(114)
+    B, N, C = 2, 5, 4
+    P = 8
+    Hp, Hc = _hadamard_orth(P), _hadamard_orth(C)
+    x = rng.standard_normal((B, N, C))
+    dy = rng.standard_normal((B, N, C))
+    wi = rng.standard_normal((C, C)) / np.sqrt(C)
+    wo = rng.standard_normal((C, C)) / np.sqrt(C)
+    g = rng.uniform(0.5, 1.5, (P, C))
+
+    def mix(z, G):
+        return (Hp @ (G * (Hp @ _pad_rows(z, P) @ Hc)) @ Hc)[:N]
+
+    M = np.stack([mix(e.reshape(N, C), g).reshape(-1) for e in np.eye(N * C)], axis=1)
+    dx, dwi, dwo, dg = o.whtmix_module_grad(x, wi, g, wo, dy)
+    ref_dwi = np.zeros((C, C))
+    ref_dwo = np.zeros((C, C))
+    for b in range(B):
+        z = x[b] @ wi
+        zp = (M @ z.reshape(-1)).reshape(N, C)
+        dzp = dy[b] @ wo.T
+        ref_dwo += zp.T @ dy[b]
+        dz = (M.T @ dzp.reshape(-1)).reshape(N, C)
+        assert _rel(dx[b], dz @ wi.T) < 1e-12, b
+        ref_dwi += x[b].T @ dz
+    assert _rel(dwi, ref_dwi) < 1e-12 and _rel(dwo, ref_dwo) < 1e-12
+
+    loss = lambda xx, a, gg, bb: float(np.sum(o.whtmix_module(xx, a, gg, bb) * dy))
+    for (i, j) in [(0, 0), (3, 2), (7, 3)]:
+        e = np.zeros((P, C))
+        e[i, j] = 1.0
+        fd = (loss(x, wi, g + 0.5 * e, wo) - loss(x, wi, g - 0.5 * e, wo))
+        assert abs(fd - dg[i, j]) < 1e-11 * max(1.0, abs(fd)), (i, j)
+    for (i, j) in [(0, 1), (2, 3), (3, 0)]:
+        e = np.zeros((C, C))
+        e[i, j] = 1.0
+        fd = loss(x, wi + 0.5 * e, g, wo) - loss(x, wi - 0.5 * e, g, wo)
+        assert abs(fd - dwi[i, j]) < 1e-11 * max(1.0, abs(fd)), ("w_in", i, j)
+        fd = loss(x, wi, g, wo + 0.5 * e) - loss(x, wi, g, wo - 0.5 * e)
+        assert abs(fd - dwo[i, j]) < 1e-11 * max(1.0, abs(fd)), ("w_out", i, j)
+    for (b, n, c) in [(0, 0, 0), (1, 4, 3)]:
+        e = np.zeros((B, N, C))
+        e[b, n, c] = 1.0
+        fd = loss(x + 0.5 * e, wi, g, wo) - loss(x - 0.5 * e, wi, g, wo)
+        assert abs(fd - dx[b, n, c]) < 1e-11 * max(1.0, abs(fd)), (b, n, c)
+
+    gt, gc = rng.normal(0, 0.3, P), rng.normal(0, 0.3, C)
+    sdx, sdwi, sdwo, dgt, dgc = o.whtmix_module_grad_separable(x, wi, gt, gc, wo, dy)
+    G = np.outer(np.exp(gt), np.exp(gc))
+    jdx, jdwi, jdwo, _ = o.whtmix_module_grad(x, wi, G, wo, dy)
+    assert _rel(sdx, jdx) < 1e-12 and _rel(sdwi, jdwi) < 1e-12 and _rel(sdwo, jdwo) < 1e-12
+    sloss = lambda a, b_: float(np.sum(o.whtmix_module_separable(x, wi, a, b_, wo) * dy))
+    h = 1e-5
+    for n in [0, 5]:
+        e = np.zeros(P)
+        e[n] = h
+        fd = (sloss(gt + e, gc) - sloss(gt - e, gc)) / (2 * h)
+        assert abs(fd - dgt[n]) < 1e-7 * max(1.0, abs(fd)), n
+    e = np.zeros(C)
+    e[1] = h
+    fd = (sloss(gt, gc + e) - sloss(gt, gc - e)) / (2 * h)
+    assert abs(fd - dgc[1]) < 1e-7 * max(1.0, abs(fd))
+
+
 def pin_rejects_bad_shapes(o) -> None:
     """The channel transform needs a power-of-two C (section III-B pads only
     the token axis); a token count must be at least 1."""
@@ -387,5 +460,6 @@ ALL_PINS = [
     pin_grad_dense,
     pin_grad_finite_differences,
     pin_module_dense,
+    pin_module_grad,
     pin_rejects_bad_shapes,
 ]

@@ -61,6 +61,12 @@ MUTANTS = {
     # W_out applied to the mixer's input instead of its output
     "projection_order": ("project(m, w_out, y + b * N * C, N, C);",
                          "project(z, w_out, y + b * N * C, N, C);"),
+    # backward through a projection with the weight not transposed
+    "grad_projection_not_transposed": ("s += x[n * C + j] * w[i * C + j];",
+                                       "s += x[n * C + j] * w[j * C + i];"),
+    # dW_out with its operands swapped (its transpose)
+    "grad_weight_operands": ("accumulate_at_b(zp + b * S, dy + b * S, dw_out, N, C);",
+                             "accumulate_at_b(dy + b * S, zp + b * S, dw_out, N, C);"),
     # separable form: log gains used without exponentiation
     "separable_no_exp": ("z[n * C + c] *= exp(g_c[c]);", "z[n * C + c] *= g_c[c];"),
     # separable form: token gain indexed by channel
