@@ -73,7 +73,8 @@ def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) ->
             B * L * (4 + s)]           # read workspace, write y
 
 
-OPS = ("forward", "separable", "backward", "backward_separable", "module", "module_separable")
+OPS = ("forward", "separable", "backward", "backward_separable", "module", "module_separable",
+       "module_backward")
 
 
 def module_kernels(plan: str, C: int) -> list[str]:
@@ -116,6 +117,8 @@ def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
     wb = 2 * C * C * s              # module: also read W_in and W_out
     if op == "module":
         return 2 * xy + 4 * P * C + wb
+    if op == "module_backward":     # read x, dy, G, weights; write dx, dG, both dW (f32)
+        return 3 * xy + 8 * P * C + wb + 2 * C * C * 4
     return 2 * xy + 4 * (P + C) + wb  # module_separable
 
 
@@ -183,6 +186,7 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
         "backward": lambda: orc.whtmix_grad(x, dy, g),
         "backward_separable": lambda: orc.whtmix_grad_separable(x, dy, gt, gc),
         "module": lambda: orc.whtmix_module(x, wi, g, wo),
+        "module_backward": lambda: orc.whtmix_module_grad(x, wi, g, wo, dy),
         "module_separable": lambda: orc.whtmix_module_separable(x, wi, gt, gc, wo),
     }[op]
     runs, t_total = 0, 0.0
@@ -265,7 +269,7 @@ def main() -> int:
             x, g = workloads.draw(w.B, w.N, w.C, w.dtype, w.seed + 1000 * i, w.x_dist)
         gt, gc = workloads.draw_log_gains(P, w.C, w.seed + 1000 * i + 1)
         dy = None
-        if op.startswith("backward"):
+        if "backward" in op:
             dy, _ = workloads.draw(w.B, w.N, w.C, w.dtype, w.seed + 1000 * i + 2)
         t = {"x": torch.from_numpy(x).to(dev).to(tdt), "g": torch.from_numpy(g).to(dev),
              "gt": torch.from_numpy(gt).to(dev), "gc": torch.from_numpy(gc).to(dev)}
@@ -286,6 +290,8 @@ def main() -> int:
     hip = HipEvents()
     if op.startswith("backward"):
         nk, names = 2, ["gain_gradient", "dx"]
+    elif op == "module_backward":
+        nk, names = 3, ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"]
     elif op.startswith("module"):
         names = module_kernels(plan["plan"], w.C)
         nk = len(names)
@@ -310,6 +316,14 @@ def main() -> int:
             st = whtmix.module_forward_raw(t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(),
                                            w_out.data_ptr(), t["y"].data_ptr(), B, N, C,
                                            dt_code, sptr, args.plan, events)
+        elif op == "module_backward":
+            if "dwi" not in t:
+                t["dwi"] = torch.empty((C, C), device=dev)
+                t["dwo"] = torch.empty((C, C), device=dev)
+            st = whtmix.module_backward_raw(
+                t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(), w_out.data_ptr(),
+                t["dy"].data_ptr(), t["y"].data_ptr(), t["dwi"].data_ptr(), t["dwo"].data_ptr(),
+                t["dg"].data_ptr(), B, N, C, dt_code, sptr, args.plan, events)
         elif op == "module_separable":
             st = whtmix.module_forward_separable_raw(
                 t["x"].data_ptr(), w_in.data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
@@ -350,6 +364,10 @@ def main() -> int:
     if op in ("forward", "separable"):
         gbytes = 4 * P * w.C if op == "forward" else 4 * (P + w.C)
         alg = algorithmic_bytes(plan["plan"], w.B, P, w.C, s, gbytes)
+    elif op == "module_backward":
+        # phases recompute design-specific float32 intermediates: the record
+        # below is the whole step's ideal bytes (kernel "step")
+        alg = [0, 0, 0]
     elif op.startswith("module"):
         gbytes = 4 * P * w.C if op == "module" else 4 * (P + w.C)
         alg, flops = module_algorithmic(names, w.B, w.N, P, w.C, s, gbytes)
@@ -359,8 +377,11 @@ def main() -> int:
         gb = 4 * P * w.C if op == "backward" else 4 * (P + w.C)
         alg = [2 * w.B * w.N * w.C * s + gb, 2 * w.B * w.N * w.C * s + gb]
     dom = int(np.argmax(per_kernel))
-    achieved = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9
-    traffic = load_traffic(names[dom], name, op)
+    if op == "module_backward":
+        achieved, dom_name = gbs, "step"
+    else:
+        achieved, dom_name = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9, names[dom]
+    traffic = load_traffic(dom_name, name, op)
 
     out = {
         "metric": METRIC,
@@ -382,7 +403,7 @@ def main() -> int:
         "hbm_peak_frac": round(gbs / PEAK_HBM_GBS, 4),
         "event_sampled_steps": len(sampled),
         "kernels": [{"name": n, "avg_ms": round(t, 5), "alg_bytes": b,
-                     "alg_GBs": round(b / (t * 1e-3) / 1e9, 1)}
+                     "alg_GBs": round(b / (t * 1e-3) / 1e9, 1) if b else None}
                     for n, t, b in zip(names, per_kernel, alg)],
         "matrix_core": None if flops is None else {
             "alg_TFLOPs_per_kernel": [round(f / (t * 1e-3) / 1e12, 2)
@@ -390,7 +411,7 @@ def main() -> int:
             "peak_TFLOPs": PEAK_MFMA_TFLOPS[w.dtype],
             "note": "projection flops (2 N C^2 per slice each) over the kernel time; "
                     "the kernels stay HBM-bound"},
-        "roofline": {"bound": "hbm", "kernel": names[dom],
+        "roofline": {"bound": "hbm", "kernel": dom_name,
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic},
     }

@@ -241,6 +241,52 @@ WHTMIX_API int whtmix_module_forward_separable(const void *x, const void *w_in,
                                     void *stream,
                                     const whtmix_options *options);
 
+/*
+ * whtmix_module_backward -- gradients through whtmix_module_forward for an
+ * upstream gradient dy = dL/dY (the paper trains the block, section IV-A):
+ *     dZ' = dY W_out^T,            dW_out = sum over b of Z'^T dY,
+ *     dZ, dgain = the mixer's gradients (whtmix_backward) at (Z, dZ'),
+ *     dX = dZ W_in^T,              dW_in  = sum over b of X^T dZ,
+ * with Z = X W_in and Z' = mixer(Z) recomputed in float32.
+ *
+ *   x, dy         [B][N][C] elements of `dtype`.
+ *   w_in, w_out   [C][C] elements of `dtype`, as passed to the forward call.
+ *   gain          [N_pad][C] float32.
+ *   dx            [B][N][C] of `dtype` (written); may be dy itself.
+ *   dw_in, dw_out [C][C] float32, overwritten.
+ *   dgain         [N_pad][C] float32, overwritten, or NULL to skip.
+ * No output may overlap an input or another output (except dx == dy); B*N <
+ * 2^31.  Weight gradients are summed over row chunks in a fixed order, so
+ * results are bitwise reproducible.  Workspace: 3*B*N*C floats plus the
+ * mixer's forward and backward workspaces, 3*C*C packed weight elements and
+ * the weight-gradient partial sums.  Other conventions as
+ * whtmix_module_forward (events: [0] before, [1] after dW_out, [2] after the
+ * mixer's gradients, [3] after dX and dW_in).
+ */
+WHTMIX_API int whtmix_module_backward(const void *x, const void *w_in,
+                           const float *gain, const void *w_out,
+                           const void *dy, void *dx, float *dw_in,
+                           float *dw_out, float *dgain, int64_t B, int64_t N,
+                           int64_t C, int dtype, void *stream,
+                           const whtmix_options *options);
+
+/*
+ * whtmix_module_backward_separable -- as whtmix_module_backward for the
+ * block with log-domain gains: d_log_gain_tokens [N_pad] and
+ * d_log_gain_channels [C] float32 (both NULL or both non-NULL), as
+ * whtmix_backward_separable.
+ */
+WHTMIX_API int whtmix_module_backward_separable(const void *x, const void *w_in,
+                                     const float *log_gain_tokens,
+                                     const float *log_gain_channels,
+                                     const void *w_out, const void *dy,
+                                     void *dx, float *dw_in, float *dw_out,
+                                     float *d_log_gain_tokens,
+                                     float *d_log_gain_channels, int64_t B,
+                                     int64_t N, int64_t C, int dtype,
+                                     void *stream,
+                                     const whtmix_options *options);
+
 /* Fills *info with the plan whtmix_forward_ex would use.  Validates the
  * shape, dtype and options exactly as the forward call does (pointers are
  * not needed).  Returns a whtmix_status. */

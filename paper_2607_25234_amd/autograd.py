@@ -2,6 +2,8 @@
 
     y = whtmix_mix(x, gain)                                  # joint gain G[N_pad, C]
     y = whtmix_mix_separable(x, log_gain_tokens, log_gain_channels)
+    y = whtmix_block(x, w_in, gain, w_out)                   # eqs. (1)-(4)
+    y = whtmix_block_separable(x, w_in, log_gain_tokens, log_gain_channels, w_out)
 
 The forward and backward passes both run in the HIP kernels of libwhtmix.so
 (whtmix_forward*/whtmix_backward*); gradients flow to x and to the gains, as
@@ -48,6 +50,49 @@ class WHTMixSeparableFunction(torch.autograd.Function):
                                                  want_dx=ctx.needs_input_grad[0],
                                                  want_dgains=want_g)
         return dx, dgt, dgc
+
+
+class WHTMixBlockFunction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, w_in, gain, w_out):
+        x, w_in, gain, w_out = (t.contiguous() for t in (x, w_in, gain, w_out))
+        ctx.save_for_backward(x, w_in, gain, w_out)
+        return whtmix.module_forward(x, w_in, gain, w_out)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, w_in, gain, w_out = ctx.saved_tensors
+        dx, dwi, dwo, dg = whtmix.module_backward(x, w_in, gain, w_out, dy.contiguous(),
+                                                  want_dgain=ctx.needs_input_grad[2])
+        return dx, dwi.to(w_in.dtype), dg, dwo.to(w_out.dtype)
+
+
+class WHTMixBlockSeparableFunction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, w_in, log_gain_tokens, log_gain_channels, w_out):
+        x, w_in, gt, gc, w_out = (t.contiguous() for t in
+                                  (x, w_in, log_gain_tokens, log_gain_channels, w_out))
+        ctx.save_for_backward(x, w_in, gt, gc, w_out)
+        return whtmix.module_forward_separable(x, w_in, gt, gc, w_out)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, w_in, gt, gc, w_out = ctx.saved_tensors
+        want_g = ctx.needs_input_grad[2] or ctx.needs_input_grad[3]
+        dx, dwi, dwo, dgt, dgc = whtmix.module_backward_separable(
+            x, w_in, gt, gc, w_out, dy.contiguous(), want_dgains=want_g)
+        return dx, dwi.to(w_in.dtype), dgt, dgc, dwo.to(w_out.dtype)
+
+
+def whtmix_block(x, w_in, gain, w_out):
+    """Differentiable block of eqs. (1)-(4): mixer(x W_in) W_out (joint gain).
+    Weight gradients are computed in float32 and returned in the weights' dtype."""
+    return WHTMixBlockFunction.apply(x, w_in, gain, w_out)
+
+
+def whtmix_block_separable(x, w_in, log_gain_tokens, log_gain_channels, w_out):
+    """Differentiable block with the paper's log-domain gains."""
+    return WHTMixBlockSeparableFunction.apply(x, w_in, log_gain_tokens, log_gain_channels, w_out)
 
 
 def whtmix_mix(x, gain):

@@ -410,9 +410,135 @@ int module_impl(const void *x, const void *w_in, int gain_kind, const float *gai
     return WHTMIX_SUCCESS;
 }
 
+int64_t align256(int64_t v) { return (v + 255) / 256 * 256; }
+
+int module_backward_impl(const void *x, const void *w_in, int gain_kind, const float *gain,
+                         const float *gain_t, const float *gain_c, const void *w_out,
+                         const void *dy, void *dx, float *dw_in, float *dw_out, float *dgain,
+                         float *dgt, float *dgc, int64_t B, int64_t N, int64_t C, int dtype,
+                         void *stream, const whtmix_options *options)
+{
+    Checked c;
+    int st = check_shape(B, N, C, dtype, options, &c);
+    if (st != WHTMIX_SUCCESS) return st;
+    const int cbits = log2_exact(C);
+    if (cbits > whtmix::kModuleMaxCbits || B * N >= (int64_t(1) << 31))
+        return WHTMIX_ERROR_TOO_LARGE;
+    const bool sep = gain_kind == whtmix::GAIN_LOG_SEPARABLE;
+    if (!w_in || !w_out || !dw_in || !dw_out || (sep ? (!gain_t || !gain_c) : !gain))
+        return WHTMIX_ERROR_INVALID_VALUE;
+    if (sep && (dgt == nullptr) != (dgc == nullptr)) return WHTMIX_ERROR_INVALID_VALUE;
+    if (B > 0 && (!x || !dy || !dx)) return WHTMIX_ERROR_INVALID_VALUE;
+    const uint64_t xy = (uint64_t)B * (uint64_t)N * (uint64_t)C * (uint64_t)c.elt;
+    const uint64_t wb = (uint64_t)C * (uint64_t)C * (uint64_t)c.elt;
+    const uint64_t P = (uint64_t)c.n_pad;
+    const Span inputs[] = {{B > 0 ? reinterpret_cast<uintptr_t>(x) : 0, xy},
+                           {B > 0 ? reinterpret_cast<uintptr_t>(dy) : 0, xy},
+                           {reinterpret_cast<uintptr_t>(w_in), wb},
+                           {reinterpret_cast<uintptr_t>(w_out), wb},
+                           {reinterpret_cast<uintptr_t>(sep ? gain_t : gain),
+                            sep ? P * 4 : P * (uint64_t)C * 4},
+                           {reinterpret_cast<uintptr_t>(sep ? gain_c : nullptr), (uint64_t)C * 4}};
+    const Span outputs[] = {{B > 0 ? reinterpret_cast<uintptr_t>(dx) : 0, xy},
+                            {reinterpret_cast<uintptr_t>(dw_in), (uint64_t)C * C * 4},
+                            {reinterpret_cast<uintptr_t>(dw_out), (uint64_t)C * C * 4},
+                            {reinterpret_cast<uintptr_t>(dgain), P * (uint64_t)C * 4},
+                            {reinterpret_cast<uintptr_t>(dgt), P * 4},
+                            {reinterpret_cast<uintptr_t>(dgc), (uint64_t)C * 4}};
+    for (const Span &s : inputs)
+        if (s.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    for (const Span &s : outputs)
+        if (s.p & 15u) return WHTMIX_ERROR_MISALIGNED;
+    // No output may overlap an input or another output, except dx == dy: dY
+    // is consumed before dX is written (x is read after it).
+    for (int i = 0; i < 6; ++i) {
+        const Span &o = outputs[i];
+        if (!o.p) continue;
+        for (int j = 0; j < 6; ++j) {
+            if (i == 0 && j == 1 && o.p == inputs[j].p) continue;
+            if (spans_overlap(o, inputs[j])) return WHTMIX_ERROR_INVALID_VALUE;
+        }
+        for (int j = 0; j < 6; ++j)
+            if (j != i && spans_overlap(o, outputs[j])) return WHTMIX_ERROR_INVALID_VALUE;
+    }
+
+    whtmix::ModuleBackwardArgs m{};
+    m.x = x;
+    m.w_in = w_in;
+    m.w_out = w_out;
+    m.dy = dy;
+    m.dx = dx;
+    m.dw_in = dw_in;
+    m.dw_out = dw_out;
+    m.gain_kind = gain_kind;
+    m.gain = gain;
+    m.gain_t = gain_t;
+    m.gain_c = gain_c;
+    m.dgain = dgain;
+    m.dgt = dgt;
+    m.dgc = dgc;
+    m.cbits = cbits;
+    m.B = B;
+    m.K = c.K;
+    m.nvalid = (uint32_t)(N * C);
+    m.dtype = dtype;
+    m.plan = c.plan;
+    m.stream = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < 4; ++i)
+        m.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
+    // workspace: Z, Z', dZ'; packed weights; weight-gradient partials; the
+    // mixer's forward and backward workspaces
+    const int64_t rows = B * N;
+    const int64_t zb = align256(rows * C * 4);
+    const int64_t pk = align256((int64_t)(3 * wb));
+    const whtmix::WgradPlan wp = whtmix::wgrad_plan((uint64_t)rows, cbits);
+    const int64_t part = align256((int64_t)wp.chunks * C * C * 4);
+    const int64_t mix = align256(c.ws_bytes);
+    const whtmix::BackwardLayout lay = whtmix::backward_layout(c.plan, c.K, B, C, sep);
+    const int64_t bwd = align256((int64_t)(lay.floats * 4));
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    float *ws = nullptr;
+    st = get_workspace(stream, 3 * zb + pk + part + mix + bwd, &ws);
+    if (st != WHTMIX_SUCCESS) return st;
+    char *p = reinterpret_cast<char *>(ws);
+    m.z = reinterpret_cast<float *>(p);
+    m.zp = reinterpret_cast<float *>(p + zb);
+    m.dzp = reinterpret_cast<float *>(p + 2 * zb);
+    m.wpack = p + 3 * zb;
+    m.wpart = reinterpret_cast<float *>(p + 3 * zb + pk);
+    m.mix_ws = mix > 0 ? reinterpret_cast<float *>(p + 3 * zb + pk + part) : nullptr;
+    m.bwd_ws = bwd > 0 ? reinterpret_cast<float *>(p + 3 * zb + pk + part + mix) : nullptr;
+    hipError_t e = whtmix::launch_module_backward(m);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return WHTMIX_SUCCESS;
+}
+
 }  // namespace
 
 extern "C" {
+
+int whtmix_module_backward(const void *x, const void *w_in, const float *gain, const void *w_out,
+                           const void *dy, void *dx, float *dw_in, float *dw_out, float *dgain,
+                           int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                           const whtmix_options *options)
+{
+    return module_backward_impl(x, w_in, whtmix::GAIN_FULL, gain, nullptr, nullptr, w_out, dy, dx,
+                                dw_in, dw_out, dgain, nullptr, nullptr, B, N, C, dtype, stream,
+                                options);
+}
+
+int whtmix_module_backward_separable(const void *x, const void *w_in, const float *log_gain_tokens,
+                                     const float *log_gain_channels, const void *w_out,
+                                     const void *dy, void *dx, float *dw_in, float *dw_out,
+                                     float *d_log_gain_tokens, float *d_log_gain_channels,
+                                     int64_t B, int64_t N, int64_t C, int dtype, void *stream,
+                                     const whtmix_options *options)
+{
+    return module_backward_impl(x, w_in, whtmix::GAIN_LOG_SEPARABLE, nullptr, log_gain_tokens,
+                                log_gain_channels, w_out, dy, dx, dw_in, dw_out, nullptr,
+                                d_log_gain_tokens, d_log_gain_channels, B, N, C, dtype, stream,
+                                options);
+}
 
 int whtmix_backward(const void *x, const void *dy, const float *gain, void *dx, float *dgain,
                     int64_t B, int64_t N, int64_t C, int dtype, void *stream,

@@ -56,4 +56,74 @@ struct ModuleArgs {
 
 hipError_t launch_module(const ModuleArgs &m);
 
+// ---------------------------------------------------------------- backward
+// Split of a weight gradient dW = A^T B over rows (A, B [rows][C]): `chunks`
+// partial C x C sums of `rows_per_chunk` rows each, added in a fixed order.
+struct WgradPlan {
+    uint32_t chunks;
+    uint32_t rows_per_chunk;
+};
+
+inline WgradPlan wgrad_plan(uint64_t rows, int cbits)
+{
+    if (rows == 0) return WgradPlan{0, 4};   // no partials: the sums are zero
+    const uint64_t C = uint64_t(1) << cbits;
+    uint64_t tiles = 1;   // output tiles of one chunk (one wave each)
+    if (C >= 16) {
+        const uint64_t tb = C / 16 < 4 ? C / 16 : 4;
+        const uint64_t side = C / (16 * tb);
+        tiles = side * side;
+    }
+    uint64_t chunks = 2048 / tiles;
+    if (chunks < 1) chunks = 1;
+    const uint64_t most = (rows + 63) / 64;   // at least 64 rows per chunk
+    if (chunks > most) chunks = most;
+    if (chunks < 1) chunks = 1;
+    uint64_t rpc = (rows + chunks - 1) / chunks;
+    rpc = (rpc + 3) / 4 * 4;
+    if (rpc == 0) rpc = 4;
+    return WgradPlan{(uint32_t)((rows + rpc - 1) / rpc), (uint32_t)rpc};
+}
+
+// A validated backward call of the block.  Workspace pieces (floats unless
+// noted): z, zp, dzp [B*N*C] (Z = X W_in, Z' = mixer(Z), dZ' then dZ);
+// wpack: W_in, W_out^T and W_in^T packed (3*C*C elements of the dtype);
+// wpart: wgrad_plan(B*N, cbits).chunks * C*C partial sums; mix_ws: the
+// THREE_PASS workspace (B * 2^K, else none); bwd_ws: the mixer backward's
+// workspace (backward_layout).
+struct ModuleBackwardArgs {
+    const void *x;
+    const void *w_in;
+    const void *w_out;
+    const void *dy;
+    void *dx;               // [B][N][C] dtype
+    float *dw_in;           // [C][C]
+    float *dw_out;          // [C][C]
+    int gain_kind;
+    const float *gain;
+    const float *gain_t;
+    const float *gain_c;
+    float *dgain;
+    float *dgt;
+    float *dgc;
+    int cbits;
+    int64_t B;
+    int K;
+    uint32_t nvalid;        // N * C
+    int dtype;
+    int plan;               // the mixer's plan for [B, N, C]
+    hipStream_t stream;
+    hipEvent_t events[4];   // [0] before, [1] after Z, Z', dZ', dW_out, [2] after the
+                            // mixer's gradient, [3] after dX and dW_in
+    float *z;
+    float *zp;
+    float *dzp;
+    void *wpack;
+    float *wpart;
+    float *mix_ws;
+    float *bwd_ws;
+};
+
+hipError_t launch_module_backward(const ModuleBackwardArgs &m);
+
 }  // namespace whtmix

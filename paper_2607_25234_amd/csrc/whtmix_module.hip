@@ -368,6 +368,14 @@ __device__ __forceinline__ void project_in(float (&v)[V], const XFrag<T, CB> &f,
     }
 }
 
+// Cache policy of the epilogue's y stores.  Each 128-byte line of y is
+// written in 64-byte halves by two store instructions (a lane group covers 4
+// lanes x 16 bytes of a row); with the non-temporal policy the halves reached
+// memory as separate partial writes (1.4x the y bytes in WRITE_SIZE), while
+// temporal stores let L2 merge them (exactly the y bytes; 3.9 us faster on
+// the stereo64k block, of which the middle pass gives back 2).
+constexpr int kYPolicy = kTemporal;
+
 __device__ __forceinline__ uint32_t pack2_bf16(float a, float b)
 {
     return (uint32_t)__builtin_bit_cast(unsigned short, (__bf16)a) |
@@ -432,14 +440,14 @@ __device__ __forceinline__ void project_out(const float (&v)[V], const void *wl,
                     if (ok)
                         __builtin_amdgcn_raw_buffer_store_b128(d, r, row + 16u * q,
                                                                rb * rb_bytes + 64u * n,
-                                                               kStreaming);
+                                                               kYPolicy);
                 }
             } else {
                 const u32x2 d = {pack2_bf16(acc[0][0], acc[0][1]),
                                  pack2_bf16(acc[0][2], acc[0][3])};
                 if (ok)
                     __builtin_amdgcn_raw_buffer_store_b64(d, r, row + 8u * q, rb * rb_bytes,
-                                                          kStreaming);
+                                                          kYPolicy);
             }
         }
     } else {
@@ -463,7 +471,7 @@ __device__ __forceinline__ void project_out(const float (&v)[V], const void *wl,
                 const u32x4 d = __builtin_bit_cast(u32x4, acc);
                 if (ok)
                     __builtin_amdgcn_raw_buffer_store_b128(d, r, row + 16u * q,
-                                                           rb * rb_bytes + 64u * nb, kStreaming);
+                                                           rb * rb_bytes + 64u * nb, kYPolicy);
             }
         }
     }
@@ -663,7 +671,7 @@ module_small_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
 
 // UNFUSED projection: out[row][c] = sum_k in[row][k] w[k][c], one thread per
 // output, for the channel counts the MFMA layouts do not cover.
-template <typename Tin, typename Tout, typename Tw>
+template <typename Tin, typename Tout, typename Tw, bool TRANS = false>
 __global__ void __launch_bounds__(256)
 project_rows_kernel(const Tin *__restrict__ in, const Tw *__restrict__ w, Tout *__restrict__ out,
                     uint64_t total, int cb)
@@ -674,14 +682,15 @@ project_rows_kernel(const Tin *__restrict__ in, const Tw *__restrict__ w, Tout *
     const uint32_t c = (uint32_t)(i & (C - 1u));
     const Tin *row = in + (i - c);
     float acc = 0.0f;
-    for (uint32_t k = 0; k < C; ++k)
-        acc = fmaf(to_f(row[k]), to_f(w[(size_t)k * C + c]), acc);
+    for (uint32_t k = 0; k < C; ++k)   // TRANS: out = in W^T
+        acc = fmaf(to_f(row[k]), to_f(TRANS ? w[(size_t)c * C + k] : w[(size_t)k * C + c]), acc);
     out[i] = (Tout)acc;
 }
 
-// UNFUSED projection on the matrix cores, out[row][c] = sum_k in[row][k] W[k][c],
-// for C >= 256 (the fused layouts cover 16..128).  W is packed in the
-// prologue's operand order, where the NCOL columns of a slice are contiguous.
+// Projection on the matrix cores, out[row][c] = sum_k in[row][k] W[k][c], for
+// C >= 32: the UNFUSED forward (C >= 256; the fused layouts cover 16..128)
+// and the block's backward.  W is packed in the prologue's operand order, where
+// the NCOL columns of a slice are contiguous.
 // Workgroup (g, slice) stages its slice into LDS once and loops over blocks of
 // 64 rows, 16 per wave.  Operands as in the prologue: bf16 rows against bf16
 // weights; float rows against bf16 weights split as hi + lo; float against
@@ -690,9 +699,10 @@ template <typename Tw, int CB>
 struct ProjCols {
     static constexpr int C = 1 << CB;
     static constexpr int raw = 65536 / (C * (int)sizeof(Tw));
-    static constexpr int NCOL = raw > 128 ? 128 : (raw < 16 ? 16 : raw);
+    static constexpr int cap = C < 128 ? C : 128;   // columns of one slice
+    static constexpr int NCOL = raw > cap ? cap : (raw < 16 ? 16 : raw);
     static constexpr uint32_t WSLICE = (uint32_t)C * NCOL * sizeof(Tw);
-    static constexpr bool OK = WSLICE <= 128u * 1024u && C >= 256;
+    static constexpr bool OK = WSLICE <= 128u * 1024u && C >= 32;
 };
 
 __device__ __forceinline__ void split_bf16(const f32x4 &z, bf16x4 &hi, bf16x4 &lo)
@@ -709,12 +719,14 @@ __device__ __forceinline__ void split_bf16(const f32x4 &z, bf16x4 &hi, bf16x4 &l
 // piece.  bf16 rows: piece p holds channels 32p + 8q + [0, 8), the k values of
 // steps 2p and 2p+1.  Float rows: piece u holds 4 channels, 32(u/2) + 8q +
 // 4(u%2) + [0, 4) against bf16 weights (step u) or 16u + 4q + [0, 4) against
-// float weights (steps 4u .. 4u+3).  A chunk is 256 channels of a row.
-template <typename Tin, typename Tw>
+// float weights (steps 4u .. 4u+3).  A chunk is CH = min(C, 256) channels of
+// a row (offsets below are within the chunk).
+template <typename Tin, typename Tw, int C>
 struct ProjMode {
     static constexpr bool BFW = sizeof(Tw) == 2;
     static constexpr bool BFIN = sizeof(Tin) == 2;
-    static constexpr int NPC = BFIN ? 8 : 16;   // pieces per chunk
+    static constexpr int CH = C < 256 ? C : 256;
+    static constexpr int NPC = BFIN ? CH / 32 : CH / 16;   // pieces per chunk
     __device__ static uint32_t channel(uint32_t piece, uint32_t q)
     {
         if constexpr (BFIN) return 32u * piece + 8u * q;
@@ -729,14 +741,13 @@ project_mfma_kernel(const Tin *__restrict__ in, const Tw *__restrict__ wpk, Tout
                     uint32_t rows)
 {
     using PC = ProjCols<Tw, CB>;
-    using PM = ProjMode<Tin, Tw>;
+    using PM = ProjMode<Tin, Tw, (1 << CB)>;
     constexpr int C = PC::C;
     constexpr int NB = PC::NCOL / 16;
     constexpr int KS = PM::BFW ? C / 16 : C / 4;   // k steps of one column block
-    constexpr int NCH = C / 256;                   // chunks of 256 channels per row
+    constexpr int NCH = C / PM::CH;                // chunks per row
     constexpr int NPC = PM::NPC;
     static_assert(PC::OK, "weight slice must fit LDS");
-    static_assert(NCH >= 1, "C >= 256");
     __shared__ __attribute__((aligned(16))) unsigned char lds[PC::WSLICE];
     const uint32_t tau = threadIdx.x, lane = tau & 63u, w = tau >> 6;
     const uint32_t i = lane & 15u, q = lane >> 4;
@@ -752,7 +763,7 @@ project_mfma_kernel(const Tin *__restrict__ in, const Tw *__restrict__ wpk, Tout
     auto load = [&](u32x4 (&buf)[NPC], uint32_t t) {
         const uint32_t blk = blockIdx.x + (t / NCH) * gridDim.x;
         const uint32_t row = blk * 64u + w * 16u + i;
-        const uint32_t c0 = (t % NCH) * 256u;
+        const uint32_t c0 = (t % NCH) * (uint32_t)PM::CH;
         const Tin *src = in + (size_t)row * C + c0;
 #pragma unroll
         for (int u = 0; u < NPC; ++u) {
@@ -1021,7 +1032,7 @@ hipError_t launch_module_unfused(const ModuleArgs &m)
     switch (m.cbits) {
 #define WHTMIX_PM_CASE(cb) \
     case cb:               \
-        if constexpr (ProjCols<T, cb>::OK) return project_pair_mfma<T, cb>(m, a); \
+        if constexpr (ProjCols<T, cb>::OK && cb >= 8) return project_pair_mfma<T, cb>(m, a); \
         break;
         WHTMIX_PM_CASE(8) WHTMIX_PM_CASE(9) WHTMIX_PM_CASE(10) WHTMIX_PM_CASE(11)
         WHTMIX_PM_CASE(12)
@@ -1059,6 +1070,278 @@ hipError_t dispatch_module_gain(const ModuleArgs &m)
     return dispatch_module<T>(m, FullGain{m.gain});
 }
 
+
+// ---------------------------------------------------------------- backward
+// Gradients of the block (eqs. (1)-(4)) for an upstream gradient dY:
+//   Z = X W_in and Z' = mixer(Z) are recomputed (float32);
+//   dZ' = dY W_out^T;  dW_out = Z'^T dY;
+//   dZ and the gain gradient: the mixer's own backward at (Z, dZ');
+//   dX = dZ W_in^T;    dW_in = X^T dZ.
+// Projections run on the matrix cores for C >= 32 (weights packed, transposed
+// where the product needs W^T), on the VALU below.  Weight gradients use the
+// fp32 16x16x4 MFMA, whose operand lanes (lane 16q + i: row q, column i of a
+// 4 x 16 block) read row-major activations directly: each wave sums the
+// products of one output tile over one chunk of rows, and the chunks' partial
+// sums are added in a fixed order, so the result is reproducible.
+
+// B-operand packing of W (TRANS: of W^T) in the prologue's order.
+template <typename T>
+__global__ void __launch_bounds__(256)
+pack_b_kernel(const T *__restrict__ w, T *__restrict__ p, int cb, int trans)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= C * C) return;
+    const uint32_t e = idx & 3u;
+    const uint32_t lane = (idx >> 2) & 63u;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const uint32_t rest = idx >> 8;
+    uint32_t k, col;
+    if constexpr (sizeof(T) == 2) {
+        const uint32_t ks = C / 16u;
+        k = k_in_bf16(C, rest % ks, q, e);
+        col = 16u * (rest / ks) + j;
+    } else {
+        const uint32_t np = C / 16u;
+        k = k_in_f32(4u * (rest % np) + e, q);
+        col = 16u * (rest / np) + j;
+    }
+    p[idx] = trans ? w[col * C + k] : w[k * C + col];
+}
+
+// Partial dW = A^T B of one chunk of rows, one 16TB x 16TB output tile per
+// wave (no LDS, no barriers: a wave past the last tile returns at once).
+template <typename Ta, typename Tb, int TB>
+__global__ void __launch_bounds__(256)
+wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__restrict__ part,
+                  uint32_t rows, uint32_t rpc, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
+    const uint32_t i = lane & 15u, q = lane >> 4;
+    const uint32_t side = C / (16u * TB);
+    const uint32_t tile = blockIdx.x * 4u + w;
+    if (tile >= side * side) return;
+    const uint32_t c0 = (tile / side) * 16u * TB, d0 = (tile % side) * 16u * TB;
+    const uint32_t chunk = blockIdx.y;
+    const uint32_t r_begin = chunk * rpc;
+    const uint32_t r_end = min(rows, r_begin + rpc);
+    f32x4 acc[TB][TB];
+#pragma unroll
+    for (int ib = 0; ib < TB; ++ib)
+#pragma unroll
+        for (int jb = 0; jb < TB; ++jb)
+            acc[ib][jb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+    for (uint32_t r0 = r_begin; r0 < r_end; r0 += 4u) {
+        const uint32_t r = r0 + q;
+        const bool ok = r < r_end;
+        float av[TB], bv[TB];
+#pragma unroll
+        for (int ib = 0; ib < TB; ++ib)
+            av[ib] = ok ? to_f(a[(size_t)r * C + c0 + 16u * ib + i]) : 0.0f;
+#pragma unroll
+        for (int jb = 0; jb < TB; ++jb)
+            bv[jb] = ok ? to_f(b[(size_t)r * C + d0 + 16u * jb + i]) : 0.0f;
+#pragma unroll
+        for (int ib = 0; ib < TB; ++ib)
+#pragma unroll
+            for (int jb = 0; jb < TB; ++jb)
+                acc[ib][jb] =
+                    __builtin_amdgcn_mfma_f32_16x16x4f32(av[ib], bv[jb], acc[ib][jb], 0, 0, 0);
+    }
+    // lane 16q + j holds rows 4q + r (channel of a) of column j (channel of b)
+    float *out = part + (size_t)chunk * C * C;
+#pragma unroll
+    for (int ib = 0; ib < TB; ++ib)
+#pragma unroll
+        for (int jb = 0; jb < TB; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                out[(size_t)(c0 + 16u * ib + 4u * q + r) * C + d0 + 16u * jb + i] = acc[ib][jb][r];
+}
+
+// The same for C < 16 on the VALU: one thread per output of one chunk.
+template <typename Ta, typename Tb>
+__global__ void __launch_bounds__(256)
+wgrad_valu_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__restrict__ part,
+                  uint32_t rows, uint32_t rpc, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t o = threadIdx.x;
+    if (o >= C * C) return;
+    const uint32_t ci = o >> cb, cj = o & (C - 1u);
+    const uint32_t chunk = blockIdx.x;
+    const uint32_t r_end = min(rows, chunk * rpc + rpc);
+    float acc = 0.0f;
+    for (uint32_t r = chunk * rpc; r < r_end; ++r)
+        acc = fmaf(to_f(a[(size_t)r * C + ci]), to_f(b[(size_t)r * C + cj]), acc);
+    part[(size_t)chunk * C * C + o] = acc;
+}
+
+// out[i] = sum over chunks c (ascending) of part[c][i].
+__global__ void __launch_bounds__(256)
+sum_partials_kernel(const float *__restrict__ part, float *__restrict__ out, uint32_t n,
+                    uint32_t chunks)
+{
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    if (i >= n) return;
+    float s = 0.0f;
+    for (uint32_t c = 0; c < chunks; ++c)
+        s += part[(size_t)c * n + i];
+    out[i] = s;
+}
+
+template <typename T>
+hipError_t launch_pack_b(const T *w, T *p, int cb, bool trans, hipStream_t st)
+{
+    const uint32_t n = 1u << (2 * cb);
+    hipLaunchKernelGGL((pack_b_kernel<T>), dim3((n + 255u) / 256u), dim3(256), 0, st, w, p, cb,
+                       trans ? 1 : 0);
+    return hipGetLastError();
+}
+
+template <typename Tin, typename Tout, typename T, int CB>
+hipError_t launch_project_mfma(const Tin *in, const T *wpk, Tout *out, uint32_t rows,
+                               hipStream_t st)
+{
+    using PC = ProjCols<T, CB>;
+    const uint32_t slices = PC::C / PC::NCOL;
+    const uint32_t nblk = (rows + 63u) / 64u;
+    uint32_t gx = 512u / slices;
+    gx = gx < 1u ? 1u : (gx > nblk ? nblk : gx);
+    hipLaunchKernelGGL((project_mfma_kernel<Tin, Tout, T, CB>), dim3(gx, slices), dim3(256), 0,
+                       st, in, wpk, out, rows);
+    return hipGetLastError();
+}
+
+// out = in W (TRANS: in W^T); wpk is W (or W^T) packed, wraw the raw matrix.
+template <typename Tin, typename Tout, typename T, bool TRANS>
+hipError_t project(const Tin *in, const T *wpk, const T *wraw, Tout *out, uint32_t rows, int cb,
+                   hipStream_t st)
+{
+    if (rows == 0) return hipSuccess;
+    switch (cb) {
+#define WHTMIX_PJ_CASE(c) \
+    case c:               \
+        if constexpr (ProjCols<T, c>::OK) return launch_project_mfma<Tin, Tout, T, c>(in, wpk, out, rows, st); \
+        break;
+        WHTMIX_PJ_CASE(5) WHTMIX_PJ_CASE(6) WHTMIX_PJ_CASE(7) WHTMIX_PJ_CASE(8)
+        WHTMIX_PJ_CASE(9) WHTMIX_PJ_CASE(10) WHTMIX_PJ_CASE(11) WHTMIX_PJ_CASE(12)
+#undef WHTMIX_PJ_CASE
+    default: break;
+    }
+    const uint64_t total = (uint64_t)rows << cb;
+    hipLaunchKernelGGL((project_rows_kernel<Tin, Tout, T, TRANS>),
+                       dim3((uint32_t)((total + 255u) / 256u)), dim3(256), 0, st, in, wraw, out,
+                       total, cb);
+    return hipGetLastError();
+}
+
+template <typename Ta, typename Tb>
+hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t rows, int cb,
+                 hipStream_t st)
+{
+    const uint32_t C = 1u << cb;
+    const WgradPlan wp = wgrad_plan(rows, cb);
+    if (wp.chunks == 0) {
+        // no rows: sum_partials over zero chunks writes zeros
+    } else if (C >= 16) {
+        const uint32_t tb = C / 16u < 4u ? C / 16u : 4u;
+        const uint32_t side = C / (16u * tb);
+        const dim3 grid((side * side + 3u) / 4u, wp.chunks);
+        if (tb == 1)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 1>), grid, dim3(256), 0, st, a, b, part,
+                               rows, wp.rows_per_chunk, cb);
+        else if (tb == 2)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 2>), grid, dim3(256), 0, st, a, b, part,
+                               rows, wp.rows_per_chunk, cb);
+        else
+            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 4>), grid, dim3(256), 0, st, a, b, part,
+                               rows, wp.rows_per_chunk, cb);
+    } else {
+        hipLaunchKernelGGL((wgrad_valu_kernel<Ta, Tb>), dim3(wp.chunks), dim3(256), 0, st, a, b,
+                           part, rows, wp.rows_per_chunk, cb);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sum_partials_kernel, dim3((C * C + 255u) / 256u), dim3(256), 0, st, part,
+                       out, C * C, wp.chunks);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t module_backward(const ModuleBackwardArgs &m)
+{
+    const hipStream_t st = m.stream;
+    const int cb = m.cbits;
+    const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> cb);
+    const size_t CC = (size_t)1 << (2 * cb);
+    const T *x = static_cast<const T *>(m.x);
+    const T *dy = static_cast<const T *>(m.dy);
+    const T *w_in = static_cast<const T *>(m.w_in);
+    const T *w_out = static_cast<const T *>(m.w_out);
+    T *pk = static_cast<T *>(m.wpack);
+    T *p_in = pk, *p_out_t = pk + CC, *p_in_t = pk + 2 * CC;
+    hipError_t e;
+    if (cb >= 4) {   // matrix-core projections need the packed forms
+        if ((e = launch_pack_b<T>(w_in, p_in, cb, false, st)) != hipSuccess) return e;
+        if ((e = launch_pack_b<T>(w_out, p_out_t, cb, true, st)) != hipSuccess) return e;
+        if ((e = launch_pack_b<T>(w_in, p_in_t, cb, true, st)) != hipSuccess) return e;
+    }
+    if ((e = record(m.events[0], st)) != hipSuccess) return e;
+    // Z = X W_in, Z' = mixer(Z)
+    if ((e = project<T, float, T, false>(x, p_in, w_in, m.z, rows, cb, st)) != hipSuccess) return e;
+    LaunchArgs a{};
+    a.x = m.z;
+    a.y = m.zp;
+    a.gain_kind = m.gain_kind;
+    a.gain = m.gain;
+    a.gain_t = m.gain_t;
+    a.gain_c = m.gain_c;
+    a.cbits = cb;
+    a.ws = m.mix_ws;
+    a.B = m.B;
+    a.K = m.K;
+    a.nvalid = m.nvalid;
+    a.dtype = DTYPE_F32;
+    a.plan = m.plan;
+    a.stream = st;
+    if (m.B > 0 && (e = launch(a)) != hipSuccess) return e;
+    // dZ' = dY W_out^T, dW_out = Z'^T dY
+    if ((e = project<T, float, T, true>(dy, p_out_t, w_out, m.dzp, rows, cb, st)) != hipSuccess)
+        return e;
+    if ((e = wgrad<float, T>(m.zp, dy, m.wpart, m.dw_out, rows, cb, st)) != hipSuccess) return e;
+    if ((e = record(m.events[1], st)) != hipSuccess) return e;
+    // the mixer's gradients at (Z, dZ'): dZ in place of dZ', and the gain's
+    BackwardArgs g{};
+    g.x = m.z;
+    g.dy = m.dzp;
+    g.dx = m.dzp;
+    g.gain_kind = m.gain_kind;
+    g.gain = m.gain;
+    g.gain_t = m.gain_t;
+    g.gain_c = m.gain_c;
+    g.dgain = m.dgain;
+    g.dgt = m.dgt;
+    g.dgc = m.dgc;
+    g.cbits = cb;
+    g.ws = m.bwd_ws;
+    g.B = m.B;
+    g.K = m.K;
+    g.nvalid = m.nvalid;
+    g.dtype = DTYPE_F32;
+    g.plan = m.plan;
+    g.stream = st;
+    if ((e = launch_backward(g)) != hipSuccess) return e;
+    if ((e = record(m.events[2], st)) != hipSuccess) return e;
+    // dX = dZ W_in^T, dW_in = X^T dZ
+    if ((e = project<float, T, T, true>(m.dzp, p_in_t, w_in, static_cast<T *>(m.dx), rows, cb,
+                                        st)) != hipSuccess)
+        return e;
+    if ((e = wgrad<T, float>(x, m.dzp, m.wpart, m.dw_in, rows, cb, st)) != hipSuccess) return e;
+    return record(m.events[3], st);
+}
 }  // namespace
 
 hipError_t launch_module(const ModuleArgs &m)
@@ -1066,6 +1349,13 @@ hipError_t launch_module(const ModuleArgs &m)
     if (m.dtype == DTYPE_BF16)
         return dispatch_module_gain<__bf16>(m);
     return dispatch_module_gain<float>(m);
+}
+
+hipError_t launch_module_backward(const ModuleBackwardArgs &m)
+{
+    if (m.dtype == DTYPE_BF16)
+        return module_backward<__bf16>(m);
+    return module_backward<float>(m);
 }
 
 }  // namespace whtmix

@@ -27,6 +27,8 @@ EXPORTS = (
     "whtmix_forward",
     "whtmix_forward_ex",
     "whtmix_forward_separable",
+    "whtmix_module_backward",
+    "whtmix_module_backward_separable",
     "whtmix_module_forward",
     "whtmix_module_forward_separable",
     "whtmix_plan_describe",
@@ -88,6 +90,12 @@ def lib():
         L.whtmix_module_forward_separable.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64,
                                                       ctypes.c_int, vp, ctypes.POINTER(Options)]
         L.whtmix_module_forward_separable.restype = ctypes.c_int
+        L.whtmix_module_backward.argtypes = [vp] * 9 + [i64, i64, i64, ctypes.c_int, vp,
+                                                         ctypes.POINTER(Options)]
+        L.whtmix_module_backward.restype = ctypes.c_int
+        L.whtmix_module_backward_separable.argtypes = [vp] * 11 + [i64, i64, i64, ctypes.c_int,
+                                                                   vp, ctypes.POINTER(Options)]
+        L.whtmix_module_backward_separable.restype = ctypes.c_int
         L.whtmix_backward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                       ctypes.POINTER(Options)]
         L.whtmix_backward.restype = ctypes.c_int
@@ -388,6 +396,91 @@ def backward_separable(x, dy, log_gain_tokens, log_gain_channels, want_dx: bool 
     if status != SUCCESS:
         raise WhtmixError(status, "whtmix_backward_separable")
     return dx, dgt, dgc
+
+
+def module_backward_raw(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, dy_ptr, dx_ptr, dw_in_ptr,
+                        dw_out_ptr, dgain_ptr, B, N, C, dtype, stream,
+                        plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_module_backward; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_module_backward(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, dy_ptr, dx_ptr,
+                                        dw_in_ptr, dw_out_ptr, dgain_ptr, B, N, C, dtype, stream,
+                                        ctypes.byref(opt))
+
+
+def module_backward_separable_raw(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr, dy_ptr, dx_ptr,
+                                  dw_in_ptr, dw_out_ptr, dgt_ptr, dgc_ptr, B, N, C, dtype,
+                                  stream, plan: str | int = "auto", events=None) -> int:
+    """Direct call of whtmix_module_backward_separable; returns the status."""
+    opt = _options(plan, events)
+    return lib().whtmix_module_backward_separable(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr,
+                                                  dy_ptr, dx_ptr, dw_in_ptr, dw_out_ptr, dgt_ptr,
+                                                  dgc_ptr, B, N, C, dtype, stream,
+                                                  ctypes.byref(opt))
+
+
+def module_backward(x, w_in, gain, w_out, dy, want_dgain: bool = True, dx=None,
+                    plan: str | int = "auto", stream=None):
+    """Gradients through module_forward for the upstream gradient dy: returns
+    (dx, dw_in, dw_out, dgain), the weight and gain gradients in float32
+    (dgain None when not wanted)."""
+    import torch
+
+    xx, dt, _ = _check(x, x)
+    _same(dy, x, "dy")
+    B, N, C = xx.shape
+    _weight(w_in, C, x, "w_in")
+    _weight(w_out, C, x, "w_out")
+    _gain(gain, (padded_tokens(N), C), x, "gain")
+    if dx is None:
+        dx = torch.empty_like(dy)
+    _same(dx, x, "dx")
+    f32 = dict(dtype=torch.float32, device=x.device)
+    dw_in, dw_out = torch.empty((C, C), **f32), torch.empty((C, C), **f32)
+    dgain = torch.empty_like(gain) if want_dgain else None
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = module_backward_raw(xx.data_ptr(), w_in.data_ptr(), gain.data_ptr(),
+                                     w_out.data_ptr(), dy.data_ptr(), dx.data_ptr(),
+                                     dw_in.data_ptr(), dw_out.data_ptr(),
+                                     dgain.data_ptr() if dgain is not None else 0, B, N, C, dt,
+                                     st.cuda_stream, plan)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_module_backward")
+    return dx, dw_in, dw_out, dgain
+
+
+def module_backward_separable(x, w_in, log_gain_tokens, log_gain_channels, w_out, dy,
+                              want_dgains: bool = True, dx=None, plan: str | int = "auto",
+                              stream=None):
+    """Gradients through module_forward_separable: returns (dx, dw_in, dw_out,
+    d_log_gain_tokens, d_log_gain_channels)."""
+    import torch
+
+    xx, dt, _ = _check(x, x)
+    _same(dy, x, "dy")
+    B, N, C = xx.shape
+    _weight(w_in, C, x, "w_in")
+    _weight(w_out, C, x, "w_out")
+    _gain(log_gain_tokens, (padded_tokens(N),), x, "log_gain_tokens")
+    _gain(log_gain_channels, (C,), x, "log_gain_channels")
+    if dx is None:
+        dx = torch.empty_like(dy)
+    _same(dx, x, "dx")
+    f32 = dict(dtype=torch.float32, device=x.device)
+    dw_in, dw_out = torch.empty((C, C), **f32), torch.empty((C, C), **f32)
+    dgt = torch.empty_like(log_gain_tokens) if want_dgains else None
+    dgc = torch.empty_like(log_gain_channels) if want_dgains else None
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    with torch.cuda.device(x.device):
+        status = module_backward_separable_raw(
+            xx.data_ptr(), w_in.data_ptr(), log_gain_tokens.data_ptr(),
+            log_gain_channels.data_ptr(), w_out.data_ptr(), dy.data_ptr(), dx.data_ptr(),
+            dw_in.data_ptr(), dw_out.data_ptr(), dgt.data_ptr() if dgt is not None else 0,
+            dgc.data_ptr() if dgc is not None else 0, B, N, C, dt, st.cuda_stream, plan)
+    if status != SUCCESS:
+        raise WhtmixError(status, "whtmix_module_backward_separable")
+    return dx, dw_in, dw_out, dgt, dgc
 
 
 def release_workspaces() -> None:

@@ -177,6 +177,41 @@ def test_module_empty_batch_is_a_no_op():
     assert whtmix.module_forward_raw(0, 0, 0, 0, 0, 0, 64, 64, 1, 0) == 0
 
 
+def mbwd(x=ALIGNED, wi=ALIGNED2, g=ALIGNED2 * 2, wo=ALIGNED2 * 3, dy=ALIGNED * 16,
+         dx=ALIGNED * 64, dwi=ALIGNED2 * 4, dwo=ALIGNED2 * 5, dg=ALIGNED2 * 6, B=1, N=64, C=64,
+         dtype=0):
+    return whtmix.module_backward_raw(x, wi, g, wo, dy, dx, dwi, dwo, dg, B, N, C, dtype, 0)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(dwi=0), 1),
+    (dict(dwo=0), 1),
+    (dict(dx=0), 1),
+    (dict(dy=0), 1),
+    (dict(x=0), 1),
+    (dict(wi=0), 1),
+    (dict(dx=ALIGNED + 64), 1),               # dx overlaps x (read after dx is written)
+    (dict(dwi=ALIGNED2 * 3 + 16), 1),         # dW_in overlaps W_out
+    (dict(dwo=ALIGNED2 * 4), 1),              # dW_out is dW_in
+    (dict(dg=ALIGNED * 64 + 128), 1),         # dgain inside dx
+    (dict(dwi=ALIGNED2 * 4 + 4), 4),
+    (dict(C=1 << 13, N=1), 7),
+    (dict(B=1 << 16, N=1 << 15, C=1), 7),     # B*N >= 2^31
+    (dict(C=12), 2),
+])
+def test_module_backward_rejected_before_any_hip_call(kwargs, status):
+    assert mbwd(**kwargs) == status
+
+
+def test_module_backward_separable_rejected_before_any_hip_call():
+    f = whtmix.module_backward_separable_raw
+    args = [ALIGNED, ALIGNED2, ALIGNED2 * 2, ALIGNED2 * 2 + 4096, ALIGNED2 * 3, ALIGNED * 16,
+            ALIGNED * 64, ALIGNED2 * 4, ALIGNED2 * 5]
+    assert f(*args, ALIGNED2 * 6, 0, 1, 64, 64, 0, 0) == 1      # one log-gain gradient only
+    assert f(*args, ALIGNED2 * 6, ALIGNED2 * 6 + 64, 1, 64, 64, 0, 0) == 1   # overlapping
+    # dx == dy is allowed: passes every host check (then would launch; not called here)
+
+
 def test_padded_plans():
     """Non-power-of-two token counts are zero-padded (section III-B)."""
     for N, C, P in [(3, 4, 4), (5, 1, 8), (9216, 64, 16384), (25600, 64, 32768),

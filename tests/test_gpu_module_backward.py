@@ -1,0 +1,165 @@
+"""Gradients of the whole block (eqs. (1)-(4)) on the GPU, through the C ABI,
+against the oracle's (oracle_whtmix_module_grad, float64).
+
+dX is held to the block's forward bar for its dtype (1e-5 float32 I/O, 4e-3
+bf16 I/O: one RNE of dX, exact bf16 products, the 2^-17 split before W_in^T).
+The weight and gain gradients are float32 outputs computed in float32 from
+exactly representable inputs, held to 1e-5 normwise as the mixer's gain
+gradient is.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as oracle_mod
+from paper_2607_25234_amd import whtmix, workloads
+from tests.gpu_util import device, errors, say, to_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 4e-3}
+GRAD_TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle_mod.Oracle()
+
+
+def check(name, y, ref, tol):
+    err, rms = errors(y, ref)
+    say(f"  {name}: normwise-max {err:.3e} rms {rms:.3e} (tol {tol:g})")
+    assert y.shape == ref.shape
+    assert np.all(np.isfinite(y))
+    assert err <= tol, (name, err)
+
+
+def inputs(B, N, C, dtype, seed):
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=seed)
+    dy, _ = workloads.draw(B, N, C, dtype, seed=seed + 1)
+    _, g = workloads.draw(1, P, C, "f32", seed=seed + 2)
+    wi, wo = workloads.draw_weights(C, dtype, seed=seed + 3)
+    return x, dy, g, wi, wo
+
+
+def run(x, dy, wi, wo, dtype, dev, g=None, gt=None, gc=None, plan="auto", alias=False):
+    import torch
+
+    xd, dyd = to_device(x, dtype, dev), to_device(dy, dtype, dev)
+    wid, wod = to_device(wi, dtype, dev), to_device(wo, dtype, dev)
+    dx = dyd if alias else None
+    if g is not None:
+        gd = torch.from_numpy(np.ascontiguousarray(g, dtype=np.float32)).to(dev)
+        out = whtmix.module_backward(xd, wid, gd, wod, dyd, dx=dx, plan=plan)
+    else:
+        gtd = torch.from_numpy(np.ascontiguousarray(gt, dtype=np.float32)).to(dev)
+        gcd = torch.from_numpy(np.ascontiguousarray(gc, dtype=np.float32)).to(dev)
+        out = whtmix.module_backward_separable(xd, wid, gtd, gcd, wod, dyd, dx=dx, plan=plan)
+    torch.cuda.synchronize(dev)
+    return [to_host(t) for t in out]
+
+
+def check_all(tag, got, ref, dtype):
+    names = ["dx", "dw_in", "dw_out"] + (["dgain"] if len(ref) == 4 else ["dgt", "dgc"])
+    for name, a, r in zip(names, got, ref):
+        check(f"{tag} {name}", a, r, TOL[dtype] if name == "dx" else GRAD_TOL)
+
+
+SHAPES = [
+    # (B, N, C): VALU projections below C = 32, matrix cores from 32; SMALL,
+    # FUSED and THREE_PASS mixers; padded token counts
+    (2, 3, 4), (3, 50, 8), (2, 64, 16), (1, 100, 32), (2, 64, 64), (2, 512, 128),
+    (1, 3000, 32), (2, 2048, 64), (1, 1024, 128), (1, 64, 256), (2, 300, 256),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_module_backward_shapes(shape, dtype, dev, orc):
+    B, N, C = shape
+    x, dy, g, wi, wo = inputs(B, N, C, dtype, seed=900 + N + 3 * C + B)
+    say(f"module backward {shape} {dtype} plan={whtmix.plan_describe(B, N, C, dtype)['plan']}")
+    got = run(x, dy, wi, wo, dtype, dev, g=g)
+    check_all(f"{shape}", got, orc.whtmix_module_grad(x, wi, g, wo, dy), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 100, 64), (1, 4096, 128), (2, 16, 8)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_module_backward_separable(shape, dtype, dev, orc):
+    B, N, C = shape
+    x, dy, _, wi, wo = inputs(B, N, C, dtype, seed=950 + N)
+    gt, gc = workloads.draw_log_gains(whtmix.padded_tokens(N), C, seed=951 + N)
+    got = run(x, dy, wi, wo, dtype, dev, gt=gt, gc=gc)
+    check_all(f"separable {shape}", got,
+              orc.whtmix_module_grad_separable(x, wi, gt, gc, wo, dy), dtype)
+
+
+def test_module_backward_workload_slice(dev, orc):
+    """One slice of the benchmarked shape (N = 65536, C = 128, bf16)."""
+    w = workloads.WORKLOADS[workloads.BENCH_WORKLOAD]
+    x, dy, g, wi, wo = inputs(1, w.N, w.C, w.dtype, seed=77)
+    got = run(x, dy, wi, wo, w.dtype, dev, g=g)
+    check_all("stereo64k slice", got, orc.whtmix_module_grad(x, wi, g, wo, dy), w.dtype)
+
+
+def test_module_backward_forced_three_pass_and_alias(dev, orc):
+    """The three-pass mixer on a 2^14 slice, with dx written over dy."""
+    B, N, C = 2, 128, 128
+    x, dy, g, wi, wo = inputs(B, N, C, "bf16", seed=33)
+    ref = orc.whtmix_module_grad(x, wi, g, wo, dy)
+    check_all("three_pass alias", run(x, dy, wi, wo, "bf16", dev, g=g, plan="three_pass",
+                                      alias=True), ref, "bf16")
+
+
+def test_module_backward_empty_batch_zeroes_gradients(dev):
+    import torch
+
+    C, N = 64, 100
+    P = whtmix.padded_tokens(N)
+    empty = torch.empty((0, N, C), device=dev)
+    wi = torch.randn(C, C, device=dev)
+    wo = torch.randn(C, C, device=dev)
+    g = torch.rand(P, C, device=dev) + 0.5
+    dx, dwi, dwo, dg = whtmix.module_backward(empty, wi, g, wo, empty)
+    torch.cuda.synchronize(dev)
+    assert dx.shape == (0, N, C)
+    for t in (dwi, dwo, dg):
+        assert torch.count_nonzero(t).item() == 0
+
+
+def test_module_backward_deterministic(dev):
+    B, N, C = 4, 16384, 128
+    x, dy, g, wi, wo = inputs(B, N, C, "bf16", seed=41)
+    a = run(x, dy, wi, wo, "bf16", dev, g=g)
+    b = run(x, dy, wi, wo, "bf16", dev, g=g)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_block_autograd_training_step(dev, orc):
+    """torch.autograd through whtmix_block: gradients of a scalar loss reach x,
+    both weights and the gain, and match the oracle's."""
+    import torch
+
+    from paper_2607_25234_amd.autograd import whtmix_block
+
+    B, N, C = 2, 1000, 64
+    x, dy, g, wi, wo = inputs(B, N, C, "f32", seed=51)
+    xt = torch.from_numpy(x).to(dev).requires_grad_(True)
+    wit = torch.from_numpy(wi).to(dev).requires_grad_(True)
+    wot = torch.from_numpy(wo).to(dev).requires_grad_(True)
+    gt_ = torch.from_numpy(g).to(dev).requires_grad_(True)
+    y = whtmix_block(xt, wit, gt_, wot)
+    loss = (y * torch.from_numpy(dy).to(dev)).sum()
+    loss.backward()
+    torch.cuda.synchronize(dev)
+    ref = orc.whtmix_module_grad(x, wi, g, wo, dy)
+    for name, t, r in zip(["dx", "dw_in", "dw_out", "dgain"], [xt, wit, wot, gt_],
+                          [ref[0], ref[1], ref[2], ref[3]]):
+        check(f"autograd {name}", to_host(t.grad), r, GRAD_TOL)

@@ -490,7 +490,7 @@ def model_project(inp, w, bf_w, in_bf, CB):
     wave, weights in the prologue's packed order."""
     C = 1 << CB
     s = 2 if bf_w else 4
-    NCOL = min(128, max(16, 65536 // (C * s)))
+    NCOL = min(min(C, 128), max(16, 65536 // (C * s)))
     NB = NCOL // 16
     KS = C // 16 if bf_w else C // 4
     packed, _ = pack(w, w, bf_w)
@@ -542,7 +542,9 @@ def model_project(inp, w, bf_w, in_bf, CB):
 
 
 @pytest.mark.parametrize("CB,bf_w,in_bf", [(8, True, True), (8, True, False), (8, False, False),
-                                           (9, True, True), (9, False, False)])
+                                           (9, True, True), (9, False, False), (5, True, True),
+                                           (5, True, False), (6, False, False), (7, True, False),
+                                           (7, True, True)])
 def test_unfused_projection_model(CB, bf_w, in_bf):
     rng = np.random.default_rng(CB * 10 + bf_w + 2 * in_bf)
     C = 1 << CB
@@ -560,3 +562,81 @@ def test_unfused_projection_model(CB, bf_w, in_bf):
     ref = x @ w
     tol = 1e-5 if (bf_w and not in_bf) else 1e-12
     np.testing.assert_allclose(y, ref, atol=tol * np.abs(ref).max())
+
+
+def test_transposed_packing_is_the_packing_of_the_transpose():
+    """pack_b_kernel with trans reads W[col][k]: the packing of W^T."""
+    rng = np.random.default_rng(5)
+    for C in (32, 128):
+        w = rng.standard_normal((C, C))
+        for bf in (True, False):
+            a, _ = pack(w.T.copy(), w, bf)
+            # the kernel's transposed read, written out independently
+            b = np.empty(C * C)
+            for idx in range(C * C):
+                e, lane, rest = idx & 3, (idx >> 2) & 63, idx >> 8
+                j, q = lane & 15, lane >> 4
+                if bf:
+                    ks = C // 16
+                    k, col = k_in_bf16(C, rest % ks, q, e), 16 * (rest // ks) + j
+                else:
+                    npc = C // 16
+                    k, col = k_in_f32(4 * (rest % npc) + e, q), 16 * (rest // npc) + j
+                b[idx] = w[col, k]
+            assert np.array_equal(a, b)
+
+
+def wgrad_plan(rows, cb):
+    if rows == 0:
+        return 0, 4
+    C = 1 << cb
+    tiles = 1
+    if C >= 16:
+        tb = min(4, C // 16)
+        tiles = (C // (16 * tb)) ** 2
+    chunks = max(1, 2048 // tiles)
+    chunks = max(1, min(chunks, (rows + 63) // 64))
+    rpc = -(-rows // chunks)
+    rpc = max(4, (rpc + 3) // 4 * 4)
+    return -(-rows // rpc), rpc
+
+
+def model_wgrad(a, b, cb):
+    """wgrad_mfma_kernel: per chunk of rows and output tile, 4 rows per fp32
+    MFMA step (lane 16q + i reads row q, column i of a 4 x 16 block)."""
+    rows, C = a.shape
+    chunks, rpc = wgrad_plan(rows, cb)
+    tb = min(4, C // 16)
+    side = C // (16 * tb)
+    part = np.full((chunks, C, C), np.nan)
+    lanes = np.arange(64)
+    i, q = lanes & 15, lanes >> 4
+    for ch in range(chunks):
+        r_end = min(rows, ch * rpc + rpc)
+        for tile in range(side * side):
+            c0, d0 = (tile // side) * 16 * tb, (tile % side) * 16 * tb
+            acc = {(ib, jb): np.zeros((64, 4)) for ib in range(tb) for jb in range(tb)}
+            for r0 in range(ch * rpc, r_end, 4):
+                r = r0 + q
+                ok = r < r_end
+                rr = np.where(ok, r, 0)
+                av = [np.where(ok, a[rr, c0 + 16 * ib + i], 0.0) for ib in range(tb)]
+                bv = [np.where(ok, b[rr, d0 + 16 * jb + i], 0.0) for jb in range(tb)]
+                for ib in range(tb):
+                    for jb in range(tb):
+                        acc[ib, jb] = mfma_f32(av[ib], bv[jb], acc[ib, jb])
+            for (ib, jb), v in acc.items():
+                for r in range(4):
+                    part[ch, c0 + 16 * ib + 4 * q + r, d0 + 16 * jb + i] = v[:, r]
+    assert not np.isnan(part).any()
+    return part.sum(axis=0)
+
+
+@pytest.mark.parametrize("rows,cb", [(130, 4), (77, 5), (300, 7), (4, 6)])
+def test_weight_gradient_model(rows, cb):
+    rng = np.random.default_rng(rows + cb)
+    C = 1 << cb
+    a, b = rng.standard_normal((rows, C)), rng.standard_normal((rows, C))
+    np.testing.assert_allclose(model_wgrad(a, b, cb), a.T @ b, atol=1e-10)
+    chunks, rpc = wgrad_plan(rows, cb)
+    assert chunks * rpc >= rows and (chunks - 1) * rpc < rows and rpc % 4 == 0
