@@ -289,7 +289,8 @@ def main() -> int:
     sptr = stream.cuda_stream
     hip = HipEvents()
     if op.startswith("backward"):
-        nk, names = 2, ["gain_gradient", "dx"]
+        nk, names = 2, (["fwd_transforms_gain_gradient", "dx_outer_inv"]
+                        if plan["plan"] == "three_pass" else ["gain_gradient", "dx"])
     elif op == "module_backward":
         nk, names = 3, ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"]
     elif op.startswith("module"):
@@ -371,6 +372,15 @@ def main() -> int:
     elif op.startswith("module"):
         gbytes = 4 * P * w.C if op == "module" else 4 * (P + w.C)
         alg, flops = module_algorithmic(names, w.B, w.N, P, w.C, s, gbytes)
+    elif plan["plan"] == "three_pass":
+        # fused three-pass gradients: phase 1 = OUTER_FWD of x and dy (read
+        # both, write two float32 workspaces) + the middle pass (read both
+        # workspaces and the gain, write dY's back and the gain gradient);
+        # phase 2 = OUTER_INV of dY's workspace into dx
+        gb = 4 * P * w.C if op == "backward" else 4 * (P + w.C)
+        L = P * w.C
+        xb = w.B * w.N * w.C * s
+        alg = [2 * xb + 8 * w.B * L + 12 * w.B * L + gb + 4 * L, 4 * w.B * L + xb]
     else:
         # gain-gradient phase: read x and dy, write the gain gradient;
         # dx phase: the forward mixer applied to dy

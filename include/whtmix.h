@@ -176,7 +176,9 @@ WHTMIX_API int whtmix_forward_separable(const void *x, const float *log_gain_tok
  * so results are bitwise reproducible.  The call uses a float32 workspace of
  * up to 2*B*N_pad*C (+ partial sums) floats; other conventions and options as
  * whtmix_forward_ex (events: [0] before, [1] after the gain gradient, [2]
- * after dx).
+ * after dx).  With the three-pass plan and both outputs requested, the two
+ * gradients share dy's transform: the gain gradient is complete at [1] and
+ * only dx's last pass runs between [1] and [2].
  */
 WHTMIX_API int whtmix_backward(const void *x, const void *dy, const float *gain,
                     void *dx, float *dgain, int64_t B, int64_t N, int64_t C,

@@ -68,6 +68,92 @@ grad_middle_kernel(const float *__restrict__ wsx, const float *__restrict__ wsd,
         o[Gain::at((uint32_t)k << G::SL)] = acc[k] * scale;
 }
 
+// Three-pass dG and dX together.  After OUTER_FWD of x and dy (one launch),
+// one workgroup owns one workspace run for a chunk of slices.  For each slice
+// it transforms both tiles over the HB high bits, so both are now transformed
+// over every bit, and accumulates their product; it then finishes dY's mixer
+// on the same tile (gain, inverse over the HB bits) and stores it back in
+// place for OUTER_INV, which writes dX.  dY's transform is computed once for
+// both gradients.
+//
+// With several slices per chunk the product sum keeps this kernel at one
+// workgroup per CU (it holds the sum, the gain and both tiles: about 200
+// registers), so the loads of the next slice are issued early instead of
+// relying on other workgroups to cover their latency: x's as soon as x's tile
+// has been used, dy's right after the store of the current one.  With one
+// slice per chunk (SINGLE) the product is stored as soon as it is formed and
+// the gain is read after it, when x's tile is dead; 2^15-element tiles (1024
+// threads, at most 128 registers) always take this form.
+template <int A, int HB, int R, class Gain, bool SINGLE>
+__global__ void __launch_bounds__(1 << (HB + R - VB))
+grad_mix_middle_kernel(const float *__restrict__ wsx, float *__restrict__ wsd, Gain gain,
+                       float *__restrict__ out, uint32_t nslices, uint32_t per_chunk)
+{
+    constexpr int M = HB + R;
+    using G = Groups<M, R>;
+    using GM = GainMap<A, R>;
+    constexpr float scale = 1.0f / (float)(1u << (A + HB));
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t run = blockIdx.x & ((1u << (A - R)) - 1u);
+    const uint32_t chunk = blockIdx.x >> (A - R);
+    const uint32_t b0 = chunk * per_chunk;
+    const uint32_t b1 = min(b0 + per_chunk, nslices);
+    const auto tile = [&](const float *ws, uint32_t b) {
+        return buffer(ws + ((size_t)b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
+    };
+    float *o = out + ((size_t)chunk << (A + HB)) + ((size_t)run << R) +
+               GM::at(layout_base<G::SL>(tau));
+    float vx[V], vd[V];
+    load_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b0), tau);
+    load_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b0), tau);
+    if constexpr (SINGLE) {
+        butterflies<G::JT, VB>(vx);
+        butterflies<G::JT, VB>(vd);
+        forward_groups<M, R, 0, G::TOP, true>(lds, vx, tau);
+        forward_groups<M, R, 0, G::TOP, true>(lds, vd, tau);
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            o[GM::at((uint32_t)k << G::SL)] = vx[k] * vd[k] * scale;
+        __builtin_amdgcn_sched_barrier(0);   // keep the gain loads after the product
+        float gv[V];
+        gain.template load<G::SL, GM>(gv, run << R, tau);
+        apply_gain<A + HB>(vd, gv);
+        if constexpr (G::NBOT > 0)
+            inverse_groups<M, R, G::NBOT - 1>(lds, vd, tau);
+        butterflies<G::JT, VB>(vd);
+        store_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b0), tau);
+    } else {
+        float acc[V], gv[V];
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            acc[k] = 0.0f;
+        gain.template load<G::SL, GM>(gv, run << R, tau);   // the same for every slice
+        for (uint32_t b = b0; b < b1; ++b) {   // uniform over the workgroup
+            const bool more = b + 1 < b1;
+            butterflies<G::JT, VB>(vx);
+            butterflies<G::JT, VB>(vd);
+            forward_groups<M, R, 0, G::TOP, true>(lds, vx, tau);
+            forward_groups<M, R, 0, G::TOP, true>(lds, vd, tau);
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                acc[k] = fmaf(vx[k], vd[k], acc[k]);
+            if (more)
+                load_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b + 1), tau);
+            apply_gain<A + HB>(vd, gv);
+            if constexpr (G::NBOT > 0)
+                inverse_groups<M, R, G::NBOT - 1>(lds, vd, tau);
+            butterflies<G::JT, VB>(vd);
+            store_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b), tau);
+            if (more)
+                load_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b + 1), tau);
+        }
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            o[GM::at((uint32_t)k << G::SL)] = acc[k] * scale;
+    }
+}
+
 // Fused dG (2^11 <= L <= 2^15): one workgroup per chunk of slices, each
 // slice transformed whole.
 template <int K, typename T>
@@ -153,17 +239,37 @@ grad_small_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__re
         out[((size_t)chunk << K) + i] = acc[i] * scale;
 }
 
-// out[f] = sum over chunks of part[chunk][f], in chunk order.
+// out[f] = sum over chunks of part[chunk][f], in chunk order.  Four floats
+// per thread when L is a multiple of 4 (both buffers are 16-byte aligned),
+// else (L = 1 or 2) one.
 __global__ void __launch_bounds__(256)
 sum_chunks_kernel(const float *__restrict__ part, float *__restrict__ out, uint64_t L,
                   uint32_t nchunks)
 {
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint64_t f = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; f < L; f += stride) {
-        float s = 0.0f;
-        for (uint32_t c = 0; c < nchunks; ++c)
-            s += part[c * L + f];
-        out[f] = s;
+    const uint64_t i0 = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x;
+    if (L % 4 != 0) {
+        for (uint64_t f = i0; f < L; f += stride) {
+            float s = part[f];
+            for (uint32_t c = 1; c < nchunks; ++c)
+                s += part[c * L + f];
+            out[f] = s;
+        }
+        return;
+    }
+    const uint64_t n4 = L / 4;
+    const float4 *p4 = reinterpret_cast<const float4 *>(part);
+    float4 *o4 = reinterpret_cast<float4 *>(out);
+    for (uint64_t i = i0; i < n4; i += stride) {
+        float4 s = p4[i];
+        for (uint32_t c = 1; c < nchunks; ++c) {
+            const float4 v = p4[c * n4 + i];
+            s.x += v.x;
+            s.y += v.y;
+            s.z += v.z;
+            s.w += v.w;
+        }
+        o4[i] = s;
     }
 }
 
@@ -365,8 +471,10 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
     uint64_t want;
     if (plan == PLAN_THREE_PASS) {
         const Split sp = three_pass_split(K);
+        // about two workgroups per CU over the chunks and runs (the fused
+        // kernel holds one CU each); one slice per chunk for 2^15 tiles
         const uint64_t runs = uint64_t(1) << (sp.A - sp.R);
-        want = (1024 + runs - 1) / runs;
+        want = sp.HB + sp.R == kMaxTile ? (uint64_t)B : (512 + runs - 1) / runs;
     } else {
         want = plan == PLAN_FUSED ? 1024 : 2048;
     }
@@ -396,6 +504,102 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
     return lay;
 }
 
+namespace {
+
+// Separable log-gain gradients from the joint dG in dst:
+// dg_t = row sums and dg_c = column sums of dG o G.
+hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay, const float *dst)
+{
+    const hipStream_t st = a.stream;
+    const uint64_t L = uint64_t(1) << a.K;
+    const uint32_t P = (uint32_t)(L >> a.cbits);
+    hipError_t e;
+    hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
+                       a.gain_c, a.dgt, P, (uint32_t)a.cbits);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const uint32_t C = 1u << a.cbits;
+    hipLaunchKernelGGL(sep_cols_partial_kernel, dim3(lay.col_blocks, C > 256u ? C / 256u : 1u),
+                       dim3(256), 0, st, dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P,
+                       (uint32_t)a.cbits, lay.rows_per_block);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(sep_cols_final_kernel, dim3(C), dim3(256), 0, st, a.ws + lay.colpart,
+                       a.dgc, lay.col_blocks, C);
+    return hipGetLastError();
+}
+
+// Both gradients with the three-pass plan, sharing dY's transform:
+//   OUTER_FWD of x and dy (one launch) -> fused middle (dG, and dY's mixer up
+//   to its last pass) -> [chunk sums] -> [separable sums] -> OUTER_INV (dX).
+template <int K, typename T, class Gain>
+hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
+                            Gain gain)
+{
+    constexpr Split sp = three_pass_split(K);
+    constexpr int A = sp.A, HB = sp.HB, R = sp.R;
+    const hipStream_t st = a.stream;
+    const T *x = static_cast<const T *>(a.x);
+    const T *dy = static_cast<const T *>(a.dy);
+    float *wsx = a.ws + lay.wsx;
+    float *wsd = a.ws + lay.wsd;
+    hipError_t e;
+    hipLaunchKernelGGL((outer_fwd2_kernel<A, HB, R, T>), dim3((uint32_t)(2 * (a.B << HB))),
+                       dim3(1u << (A - VB)), 0, st, x, dy, wsx, wsd, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
+    if (lay.per_chunk == 1) {
+        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, true>),
+                           dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,
+                           wsd, gain, o, (uint32_t)a.B, 1u);
+    } else if constexpr (HB + R < kMaxTile) {
+        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false>),
+                           dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,
+                           wsd, gain, o, (uint32_t)a.B, lay.per_chunk);
+    } else {
+        return hipErrorInvalidValue;   // backward_layout gives 2^15 tiles one slice per chunk
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (lay.nchunks > 1) {
+        const uint64_t L = uint64_t(1) << K;
+        hipLaunchKernelGGL(sum_chunks_kernel, dim3(grid_for(L)), dim3(256), 0, st,
+                           a.ws + lay.part, dst, L, lay.nchunks);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (a.gain_kind == GAIN_LOG_SEPARABLE &&
+        (e = separable_reductions(a, lay, dst)) != hipSuccess)
+        return e;
+    if ((e = record(a.events[1], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
+                       dim3(1u << (A - VB)), 0, st, wsd, static_cast<T *>(a.dx), a.nvalid);
+    return hipGetLastError();
+}
+
+template <typename T, class Gain>
+hipError_t fused_dispatch(const BackwardArgs &a, const BackwardLayout &lay, float *dst, Gain gain)
+{
+    switch (a.K) {
+#define WHTMIX_FB_CASE(k) \
+    case k: return fused_three_pass<k, T, Gain>(a, lay, dst, gain);
+        WHTMIX_FB_CASE(12) WHTMIX_FB_CASE(13) WHTMIX_FB_CASE(14) WHTMIX_FB_CASE(15)
+        WHTMIX_FB_CASE(16) WHTMIX_FB_CASE(17) WHTMIX_FB_CASE(18) WHTMIX_FB_CASE(19)
+        WHTMIX_FB_CASE(20) WHTMIX_FB_CASE(21) WHTMIX_FB_CASE(22) WHTMIX_FB_CASE(23)
+        WHTMIX_FB_CASE(24) WHTMIX_FB_CASE(25) WHTMIX_FB_CASE(26) WHTMIX_FB_CASE(27)
+        WHTMIX_FB_CASE(28) WHTMIX_FB_CASE(29) WHTMIX_FB_CASE(30)
+#undef WHTMIX_FB_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <typename T>
+hipError_t fused_gain(const BackwardArgs &a, const BackwardLayout &lay, float *dst)
+{
+    if (a.gain_kind == GAIN_LOG_SEPARABLE)
+        return fused_dispatch<T>(a, lay, dst,
+                                 LogSeparableGain{a.gain_t, a.gain_c, (uint32_t)a.cbits});
+    return fused_dispatch<T>(a, lay, dst, FullGain{a.gain});
+}
+
+}  // namespace
+
 hipError_t launch_backward(const BackwardArgs &a)
 {
     const hipStream_t st = a.stream;
@@ -405,6 +609,15 @@ hipError_t launch_backward(const BackwardArgs &a)
     hipError_t e = record(a.events[0], st);
     if (e != hipSuccess) return e;
     const bool want_dg = separable ? (a.dgt != nullptr) : (a.dgain != nullptr);
+    // Both gradients with the three-pass plan: the fused path, whose first
+    // launch covers 2*B*L/32 work-items (a 32-bit grid).
+    if (want_dg && a.dx && a.B > 0 && a.plan == PLAN_THREE_PASS &&
+        (uint64_t)a.B * L / 16u <= 0xffffffffull) {
+        float *dst = separable ? a.ws + lay.dg : a.dgain;
+        e = a.dtype == DTYPE_BF16 ? fused_gain<__bf16>(a, lay, dst) : fused_gain<float>(a, lay, dst);
+        if (e != hipSuccess) return e;
+        return record(a.events[2], st);
+    }
     if (want_dg) {
         float *dst = separable ? a.ws + lay.dg : a.dgain;
         if (a.B == 0) {
@@ -415,21 +628,8 @@ hipError_t launch_backward(const BackwardArgs &a)
                                       : grad_dispatch<float>(a, lay, dst);
         }
         if (e != hipSuccess) return e;
-        if (separable) {
-            const uint32_t P = (uint32_t)(L >> a.cbits);
-            hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
-                               a.gain_c, a.dgt, P, (uint32_t)a.cbits);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            const uint32_t C = 1u << a.cbits;
-            hipLaunchKernelGGL(sep_cols_partial_kernel,
-                               dim3(lay.col_blocks, C > 256u ? C / 256u : 1u), dim3(256), 0, st,
-                               dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P, (uint32_t)a.cbits,
-                               lay.rows_per_block);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            hipLaunchKernelGGL(sep_cols_final_kernel, dim3(C), dim3(256), 0, st,
-                               a.ws + lay.colpart, a.dgc, lay.col_blocks, C);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-        }
+        if (separable && (e = separable_reductions(a, lay, dst)) != hipSuccess)
+            return e;
     }
     if ((e = record(a.events[1], st)) != hipSuccess) return e;
     if (a.dx && a.B > 0) {

@@ -8,7 +8,8 @@
 // by matrix throughput, so there is no MFMA here.
 //
 // The tile machinery (layouts, butterflies, LDS exchanges, memory access,
-// gains) is in whtmix_tile.h.
+// gains) and the OUTER_FWD / OUTER_INV kernels, which the backward pass
+// shares, are in whtmix_tile.h.
 //
 // Kernels:
 //   FUSED     whole slice in one tile: forward over all bits, gain, inverse.
@@ -83,29 +84,6 @@ middle_kernel(float *__restrict__ ws, Gain gain, uint32_t nslices)
         inverse_groups<M, R, G::NBOT - 1>(lds, v, tau);
     butterflies<G::JT, VB>(v);
     store_layout<G::TOP, ContigMap, float>(v, tile, tau);
-}
-
-// OUTER_INV: mirror of OUTER_FWD.
-template <int A, int HB, int R, typename T>
-__global__ void __launch_bounds__(1 << (A - VB))
-outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
-{
-    using G = Groups<A, 0>;
-    using Run = RunMap<HB, R>;
-    __shared__ float lds[pad(1u << A)];
-    const uint32_t tau = threadIdx.x;
-    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
-    const size_t b = blk >> HB;
-    const uint32_t hi = blk & ((1u << HB) - 1u);
-    const uint32_t valid = tile_valid<A>(nvalid, hi);
-    if (valid == 0)
-        return;   // wholly padding: nothing to store (uniform per workgroup)
-    float v[V];
-    load_layout<G::SL, Run, float>(
-        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
-    inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
-    butterflies<0, VB>(v);
-    store_tile<G::TOP, A, T>(v, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
 __device__ __forceinline__ float to_float(float v) { return v; }

@@ -294,13 +294,19 @@ __device__ __forceinline__ void store_tile(const float (&v)[V], T *base, uint32_
 // Joint per-frequency gain G[N_pad][C] (linear).
 struct FullGain {
     const float *g;
+    // Each register's base (uniform) is a scalar pointer and the thread's
+    // part a 32-bit byte offset, so every load is one global_load with a
+    // scalar base: no 64-bit vector address per register.
     template <int S, class Map>
     __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
     {
-        const float *p = g + f0 + Map::at(layout_base<S>(tau));
+        const uint32_t voff = Map::at(layout_base<S>(tau)) * 4u;
 #pragma unroll
-        for (int k = 0; k < V; ++k)
-            gv[k] = p[Map::at((uint32_t)k << S)];
+        for (int k = 0; k < V; ++k) {
+            const char *row = reinterpret_cast<const char *>(g + f0 + Map::at((uint32_t)k << S));
+            asm("" : "+s"(row));   // opaque scalar base: not re-associated into a vector one
+            gv[k] = *reinterpret_cast<const float *>(row + voff);
+        }
     }
     __device__ __forceinline__ float at(uint32_t f) const { return g[f]; }
 };
@@ -375,19 +381,18 @@ __device__ __forceinline__ uint32_t tile_valid(uint32_t nvalid, uint32_t hi)
     return nvalid <= start ? 0u : min(nvalid - start, 1u << A);
 }
 
-// OUTER_FWD kernel (forward pass and backward pass): block = b * 2^HB + hi;
+// OUTER_FWD tile (forward pass and backward pass): block = b * 2^HB + hi;
 // the chunk x[b][hi * 2^A ...] (nvalid real elements per slice, the rest
 // zero padding) is transformed over its A bits and stored to the workspace
 // in runs of 2^R, so that each middle tile is contiguous.
 template <int A, int HB, int R, typename T>
-__global__ void __launch_bounds__(1 << (A - VB))
-outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
+__device__ __forceinline__ void outer_fwd_tile(float *lds, const T *__restrict__ x,
+                                               float *__restrict__ ws, uint32_t nvalid,
+                                               uint32_t blk)
 {
     using G = Groups<A, 0>;
     using Run = RunMap<HB, R>;
-    __shared__ float lds[pad(1u << A)];
     const uint32_t tau = threadIdx.x;
-    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     float v[V];
@@ -397,6 +402,55 @@ outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvali
     forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
     store_layout<G::SL, Run, float>(
         v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+}
+
+template <int A, int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (A - VB))
+outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
+{
+    __shared__ float lds[pad(1u << A)];
+    outer_fwd_tile<A, HB, R, T>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
+}
+
+// OUTER_FWD of two operands in one launch (the backward pass's x and dy):
+// the first half of the grid takes x into wsx, the second dy into wsd.  Each
+// half is numbered as a grid of its own; the halves start on the same XCD
+// whenever the renumbering of outer_block applies (it needs a half that is a
+// multiple of 8 blocks).
+template <int A, int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (A - VB))
+outer_fwd2_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ wsx,
+                  float *__restrict__ wsd, uint32_t nvalid)
+{
+    __shared__ float lds[pad(1u << A)];
+    const uint32_t half = gridDim.x >> 1;
+    const bool second = blockIdx.x >= half;
+    const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
+    outer_fwd_tile<A, HB, R, T>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
+}
+
+// OUTER_INV kernel: the mirror of OUTER_FWD (inverse over the A low bits of
+// each workspace chunk, then the store of y).
+template <int A, int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (A - VB))
+outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
+{
+    using G = Groups<A, 0>;
+    using Run = RunMap<HB, R>;
+    __shared__ float lds[pad(1u << A)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    if (valid == 0)
+        return;   // wholly padding: nothing to store (uniform per workgroup)
+    float v[V];
+    load_layout<G::SL, Run, float>(
+        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+    inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
+    butterflies<0, VB>(v);
+    store_tile<G::TOP, A, T>(v, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
 }  // namespace tile

@@ -43,8 +43,11 @@ def inputs(B, N, C, dtype, seed):
     return x, dy, g
 
 
-SHAPES = [(1, 1, 1), (3, 32, 32), (3000, 16, 16), (2, 64, 64), (40, 128, 128), (5, 1000, 16),
-          (2, 4096, 64), (2, 9216, 64), (6, 8192, 32)]
+# Three-pass shapes cover one slice per chunk with chunk sums (2x4096x64,
+# 2x9216x64), several slices per chunk (6x8192x32) and a short last chunk
+# (7x8192x32: chunks of 2, 2, 2, 1); 5x1x2 sums chunks of a 2-element slice.
+SHAPES = [(1, 1, 1), (5, 1, 2), (3, 32, 32), (3000, 16, 16), (2, 64, 64), (40, 128, 128), (5, 1000, 16),
+          (2, 4096, 64), (2, 9216, 64), (6, 8192, 32), (7, 8192, 32)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -74,6 +77,23 @@ def test_backward_workload(dev, orc):
     torch.cuda.synchronize()
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
     check("dx", to_host(dx), dx_ref, TOL[w.dtype])
+    check("dgain", to_host(dg), dg_ref, GRAD_TOL)
+
+
+def test_backward_largest_middle_tile(dev, orc):
+    """A slice of 2^25 (N = 200000 padded to 2^18, C = 128): the middle pass
+    takes 2^15-element tiles, whose gradient kernel stores each slice's
+    product as soon as it is formed."""
+    import torch
+    B, N, C, dtype = 1, 200000, 128, "bf16"
+    x, dy, g = inputs(B, N, C, dtype, seed=950)
+    info = whtmix.plan_describe(B, N, C, dtype)
+    assert info["log2_slice"] - info["outer_bits"] + info["run_bits"] == 15
+    dx, dg = whtmix.backward(to_device(x, dtype, dev), to_device(dy, dtype, dev),
+                             torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize()
+    dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
+    check("dx", to_host(dx), dx_ref, TOL[dtype])
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
 
 

@@ -355,22 +355,36 @@ def chunking(B, want):
     return -(-B // per), per
 
 
-def simulate_grad_three_pass(x, dy, K, split):
-    """Model of the backward dG schedule: outer_fwd of x and dy, then
-    grad_middle_kernel over (chunk, run) blocks, then the chunk sum."""
+def grad_chunking(B, K, split):
+    """Chunks of the three-pass gradient kernels: about 512 workgroups over
+    the chunks and runs, one slice per chunk for 2^15-element middle tiles."""
+    A, HB, R = split
+    runs = 1 << (A - R)
+    return chunking(B, B if HB + R == 15 else -(-512 // runs))
+
+
+def simulate_grad_three_pass(x, dy, g, K, split):
+    """Model of the fused three-pass gradients: outer_fwd2 of x and dy, then
+    grad_mix_middle_kernel over (chunk, run) blocks (product sum, then dY's
+    gain and inverse in place), the chunk sum, and outer_inv of dY's
+    workspace.  Returns (dG, dX)."""
     B = x.shape[0]
     L = 1 << K
+    nvalid = x.shape[1] * x.shape[2]
     A, HB, R = split
     M = HB + R
     wsx, wsd = model_outer_fwd(x, K, split), model_outer_fwd(dy, K, split)
+    gf = g.reshape(L)
     runs = 1 << (A - R)
-    nch, per = chunking(B, -(-1024 // runs))
+    nch, per = grad_chunking(B, K, split)
     out = Access(nch * L)
+    ws_w = Access(B * L)
     part = np.full(nch * L, np.nan)
     for blk in range(nch << (A - R)):
         run, chunk = blk & (runs - 1), blk >> (A - R)
         T = Tile(M, R)
         acc = np.zeros((T.P, V))
+        goff = (run << R) + gain_map(T.idx(T.g.SL), A, R)
         for b in range(chunk * per, min(chunk * per + per, B)):
             off = (b << (A + HB)) + (run << M)
             vx = wsx[off + T.idx(T.g.TOP)].copy()
@@ -380,10 +394,31 @@ def simulate_grad_three_pass(x, dy, K, split):
             vx = T.forward_groups(vx, T.g.TOP)
             vd = T.forward_groups(vd, T.g.TOP)
             acc += vx * vd
+            vd = vd * (gf[goff] * (1.0 / L))
+            if T.g.NBOT > 0:
+                vd = T.inverse_groups(vd)
+            butterflies(vd, T.g.JT, VB)
+            wsd[ws_w.at(off + T.idx(T.g.TOP))] = vd
         o = out.at((chunk << (A + HB)) + (run << R) + gain_map(T.idx(T.g.SL), A, R))
         part[o] = acc / L
     assert np.all(out.count == 1)
-    return part.reshape(nch, L).sum(axis=0)
+    assert np.all(ws_w.count == 1), "dY's workspace rewritten exactly once"
+    dx = np.full(B * nvalid, np.nan)
+    acc_y = Access(B * nvalid)
+    for blk in range(B << HB):
+        b, hi = blk >> HB, blk & ((1 << HB) - 1)
+        valid = tile_valid(nvalid, hi, A)
+        if valid == 0:
+            continue
+        T = Tile(A, 0)
+        v = wsd[b * L + (hi << R) + run_map(T.idx(T.g.SL), HB, R)].copy()
+        v = T.inverse_groups(v)
+        butterflies(v, 0, VB)
+        t = T.idx(T.g.TOP)
+        m = t < valid
+        dx[acc_y.at(b * nvalid + (hi << A) + t[m])] = v[m]
+    assert np.all(acc_y.count == 1)
+    return part.reshape(nch, L).sum(axis=0), dx.reshape(x.shape)
 
 
 def simulate_grad_fused(x, dy, K):
@@ -414,22 +449,41 @@ def simulate_grad_fused(x, dy, K):
 
 
 @pytest.mark.parametrize("B,N,C", [(3, 64, 64), (5, 1000, 16), (2, 4096, 8), (40, 128, 128),
-                                   (2, 300, 64)])
+                                   (2, 300, 64), (7, 2048, 32), (3, 512, 2)])
 def test_grad_schedules(B, N, C, orc):
-    """The backward dG schedules reproduce the oracle's gain gradient."""
+    """The backward schedules reproduce the oracle's gain gradient, and the
+    fused three-pass schedule also its dX."""
     rng = np.random.default_rng(B * N + C)
     P = 1 << (N - 1).bit_length()
     K = (P * C).bit_length() - 1
     x = rng.standard_normal((B, N, C))
     dy = rng.standard_normal((B, N, C))
-    _, ref = orc.whtmix_grad(x, dy, np.ones((P, C)))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    dx_ref, ref = orc.whtmix_grad(x, dy, g)
     ref = ref.reshape(-1)
     if K <= 15:
         got = simulate_grad_fused(x, dy, K)
-        assert np.max(np.abs(got - ref)) < 1e-11 * np.max(np.abs(ref))
+        _, ref1 = orc.whtmix_grad(x, dy, np.ones((P, C)))
+        ref1 = ref1.reshape(-1)
+        assert np.max(np.abs(got - ref1)) < 1e-11 * np.max(np.abs(ref1))
     if K >= 12:
-        got = simulate_grad_three_pass(x, dy, K, three_pass_split(K))
+        got, dx = simulate_grad_three_pass(x, dy, g, K, three_pass_split(K))
         assert np.max(np.abs(got - ref)) < 1e-11 * np.max(np.abs(ref))
+        assert np.max(np.abs(dx - dx_ref)) < 1e-11 * np.max(np.abs(dx_ref))
+
+
+@pytest.mark.parametrize("K", list(range(12, 31)))
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 7, 32, 1000])
+def test_grad_chunking(K, B):
+    """Chunks cover the batch exactly once; 2^15-element middle tiles get one
+    slice per chunk (the only form their 1024-thread kernel has)."""
+    split = three_pass_split(K) if K >= 16 else (11, K - 11, 22 - K)
+    nch, per = grad_chunking(B, K, split)
+    covered = [b for c in range(nch) for b in range(c * per, min(c * per + per, B))]
+    assert covered == list(range(B))
+    assert all(c * per < B for c in range(nch)), "no empty chunk"
+    if split[1] + split[2] == 15:
+        assert per == 1
 
 
 def test_middle_renumbering_is_a_permutation():
