@@ -32,9 +32,10 @@
  * Threading and streams: every entry point is safe to call from several host
  * threads.  Work is enqueued on the caller's stream and the call returns
  * without waiting for it.  The library keeps one float32 workspace of
- * B*N*C*4 bytes per (device, stream) for shapes that need more than one pass;
- * it is allocated (or grown) on the first call that needs it, which therefore
- * synchronises that stream and is not safe inside HIP graph capture.
+ * B*N_pad*C*4 bytes per (device, stream) for shapes that need more than one
+ * pass; it is allocated (or grown) on the first call that needs it, which
+ * therefore synchronises that stream and is not safe inside HIP graph
+ * capture.
  */
 #ifndef WHTMIX_H
 #define WHTMIX_H

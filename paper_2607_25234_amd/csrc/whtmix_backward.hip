@@ -392,12 +392,8 @@ hipError_t grad_three_pass(const T *x, const T *dy, float *dst, const BackwardAr
     float *wsx = a.ws + lay.wsx;
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
-    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
-                       dim3(1u << (A - VB)), 0, st, x, wsx, a.nvalid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
-                       dim3(1u << (A - VB)), 0, st, dy, wsd, a.nvalid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_outer_fwd<K, T>(x, wsx, a.B, a.nvalid, st)) != hipSuccess) return e;
+    if ((e = launch_outer_fwd<K, T>(dy, wsd, a.B, a.nvalid, st)) != hipSuccess) return e;
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     hipLaunchKernelGGL((grad_middle_kernel<A, HB, R>), dim3(lay.nchunks << (A - R)),
                        dim3(1u << (HB + R - VB)), 0, st, wsx, wsd, o, (uint32_t)a.B,
@@ -542,9 +538,7 @@ hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, fl
     float *wsx = a.ws + lay.wsx;
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
-    hipLaunchKernelGGL((outer_fwd2_kernel<A, HB, R, T>), dim3((uint32_t)(2 * (a.B << HB))),
-                       dim3(1u << (A - VB)), 0, st, x, dy, wsx, wsd, a.nvalid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_outer_fwd2<K, T>(x, dy, wsx, wsd, a.B, a.nvalid, st)) != hipSuccess) return e;
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     if (lay.per_chunk == 1) {
         hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, true>),
@@ -568,9 +562,7 @@ hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, fl
         (e = separable_reductions(a, lay, dst)) != hipSuccess)
         return e;
     if ((e = record(a.events[1], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
-                       dim3(1u << (A - VB)), 0, st, wsd, static_cast<T *>(a.dx), a.nvalid);
-    return hipGetLastError();
+    return launch_outer_inv<K, T>(wsd, static_cast<T *>(a.dx), a.B, a.nvalid, st);
 }
 
 template <typename T, class Gain>

@@ -144,23 +144,19 @@ hipError_t launch_three_pass(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
     constexpr Split sp = three_pass_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
-    static_assert(A >= kMinTile && A <= kMaxTile, "outer tile size");
+    static_assert(A >= kMinTile && A <= kMaxOuter, "outer tile size");
     static_assert(HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
     static_assert(HB >= 1 && R >= 0 && R <= A, "split");
     const hipStream_t st = a.stream;
     hipError_t e = record(a.events[0], st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_fwd_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
-                       dim3(1u << (A - VB)), 0, st, x, a.ws, a.nvalid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_outer_fwd<K, T>(x, a.ws, a.B, a.nvalid, st)) != hipSuccess) return e;
     if ((e = record(a.events[1], st)) != hipSuccess) return e;
     hipLaunchKernelGGL((middle_kernel<A, HB, R, Gain>), dim3((uint32_t)(a.B << (A - R))),
                        dim3(1u << (HB + R - VB)), 0, st, a.ws, gain, (uint32_t)a.B);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = record(a.events[2], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((outer_inv_kernel<A, HB, R, T>), dim3((uint32_t)(a.B << HB)),
-                       dim3(1u << (A - VB)), 0, st, a.ws, y, a.nvalid);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_outer_inv<K, T>(a.ws, y, a.B, a.nvalid, st)) != hipSuccess) return e;
     return record(a.events[3], st);
 }
 
@@ -208,7 +204,7 @@ hipError_t dispatch(const LaunchArgs &a, Gain gain)
 template <int K, class Gain>
 hipError_t launch_middle_k(const LaunchArgs &a, Gain gain)
 {
-    constexpr Split sp = three_pass_split(K);
+    constexpr Split sp = module_split(K);
     hipLaunchKernelGGL((middle_kernel<sp.A, sp.HB, sp.R, Gain>),
                        dim3((uint32_t)(a.B << (sp.A - sp.R))), dim3(1u << (sp.HB + sp.R - VB)), 0,
                        a.stream, a.ws, gain, (uint32_t)a.B);

@@ -75,8 +75,9 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
 
 hipError_t launch_backward(const BackwardArgs &a);
 
-// Enqueues only the middle pass of THREE_PASS (a.ws holds the first outer
-// pass's output); a.x, a.y, a.nvalid and a.dtype are not used.
+// Enqueues only the middle pass of the block's three-pass plan (module_split;
+// a.ws holds the first outer pass's output); a.x, a.y, a.nvalid and a.dtype
+// are not used.
 hipError_t launch_middle(const LaunchArgs &a);
 
 

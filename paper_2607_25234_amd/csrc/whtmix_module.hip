@@ -894,7 +894,7 @@ hipError_t launch_module_fused(const ModuleArgs &m, Gain gain)
 template <int K, typename T, class Gain, int CB>
 hipError_t launch_module_three_pass(const ModuleArgs &m, Gain gain)
 {
-    constexpr Split sp = three_pass_split(K);
+    constexpr Split sp = module_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
     const uint32_t n = 1u << (2 * CB);
     const T *pin = static_cast<const T *>(m.wpack);

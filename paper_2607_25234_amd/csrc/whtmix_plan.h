@@ -45,9 +45,24 @@ constexpr Split forced_split(int K)
     return Split{kMinTile, K - kMinTile, 2 * kMinTile - K};
 }
 
-constexpr Split three_pass_split(int K)
+// Split of the block's three-pass kernels (projections fused into the outer
+// passes, whose tiles stay within 2^15 elements).
+constexpr Split module_split(int K)
 {
     return K >= 16 ? auto_split(K) : forced_split(K);
+}
+
+// Split of the mixer's three-pass kernels.  Slices of 2^26 elements and more
+// take outer tiles of 2^16 (two 2^15 register sets per workgroup), which
+// leaves the middle pass one more carried bit: runs of 32 floats (128-byte
+// lines) at 2^26 instead of 16.
+constexpr int kMaxOuter = 16;
+constexpr Split three_pass_split(int K)
+{
+    if (K < 26)
+        return module_split(K);
+    const int HB = K - kMaxOuter;
+    return Split{kMaxOuter, HB, clampi(5, kMinTile - HB, kMaxTile - HB)};
 }
 
 }  // namespace whtmix

@@ -203,23 +203,28 @@ struct GainMap {
     }
 };
 
+// soff0: a uniform byte offset added to every register's (a second
+// register set of a 2^16 tile).
 template <int S, class Map, typename T, int CP = kTemporal>
-__device__ __forceinline__ void load_layout(float (&v)[V], __amdgpu_buffer_rsrc_t r, uint32_t tau)
+__device__ __forceinline__ void load_layout(float (&v)[V], __amdgpu_buffer_rsrc_t r, uint32_t tau,
+                                            uint32_t soff0 = 0)
 {
     const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
 #pragma unroll
     for (int k = 0; k < V; ++k)
-        v[k] = Elt<T>::template load<CP>(r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
+        v[k] = Elt<T>::template load<CP>(r, voff,
+                                         soff0 + Map::at((uint32_t)k << S) * Elt<T>::bytes);
 }
 
 template <int S, class Map, typename T, int CP = kTemporal>
 __device__ __forceinline__ void store_layout(const float (&v)[V], __amdgpu_buffer_rsrc_t r,
-                                             uint32_t tau)
+                                             uint32_t tau, uint32_t soff0 = 0)
 {
     const uint32_t voff = Map::at(layout_base<S>(tau)) * Elt<T>::bytes;
 #pragma unroll
     for (int k = 0; k < V; ++k)
-        Elt<T>::template store<CP>(v[k], r, voff, Map::at((uint32_t)k << S) * Elt<T>::bytes);
+        Elt<T>::template store<CP>(v[k], r, voff,
+                                   soff0 + Map::at((uint32_t)k << S) * Elt<T>::bytes);
 }
 
 // Masked forms for the one tile of a zero-padded slice that straddles the
@@ -451,6 +456,149 @@ outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvali
     inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
     butterflies<0, VB>(v);
     store_tile<G::TOP, A, T>(v, y + b * nvalid + ((size_t)hi << A), valid, tau);
+}
+
+// ---------------------------------------------------------------- 2^16 outer tiles
+// Slices of 2^26 elements and more use outer tiles of 2^16 (three_pass_split):
+// a workgroup of 1024 threads holds two 2^15 sub-tiles (tile bit 15 = 0 and
+// 1) in two register sets.  Bit 15 is a butterfly between the sets; bits
+// 0..14 are the 2^15 schedule above, run on each set in turn through the
+// same LDS.  The RunMap offsets are additive, so the second set's workspace
+// offsets are the first's plus RunMap(2^15).
+
+// (a, b) -> (a + b, a - b) between the two register sets.
+__device__ __forceinline__ void cross_butterflies(float (&v0)[V], float (&v1)[V])
+{
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        const float a = v0[k], b = v1[k];
+        v0[k] = a + b;
+        v1[k] = a - b;
+    }
+}
+
+template <int HB, int R, typename T>
+__device__ __forceinline__ void outer_fwd_tile2(float *lds, const T *__restrict__ x,
+                                                float *__restrict__ ws, uint32_t nvalid,
+                                                uint32_t blk)
+{
+    constexpr int A = 16, M = 15;
+    using G = Groups<M, 0>;
+    using Run = RunMap<HB, R>;
+    const uint32_t tau = threadIdx.x;
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    const T *base = x + b * nvalid + ((size_t)hi << A);
+    float v0[V], v1[V];
+    load_tile<G::TOP, M, T>(v0, base, min(valid, 1u << M), tau);
+    load_tile<G::TOP, M, T>(v1, base + (1u << M), valid > (1u << M) ? valid - (1u << M) : 0u,
+                            tau);
+    cross_butterflies(v0, v1);
+    butterflies<0, VB>(v0);
+    butterflies<0, VB>(v1);
+    forward_groups<M, 0, 0, G::TOP>(lds, v0, tau);
+    forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
+    store_layout<G::SL, Run, float>(v0, r, tau);
+    store_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+}
+
+template <int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (15 - VB))
+outer_fwd_kernel2(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
+{
+    __shared__ float lds[pad(1u << 15)];
+    outer_fwd_tile2<HB, R, T>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
+}
+
+// Two operands in one launch (as outer_fwd2_kernel).
+template <int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (15 - VB))
+outer_fwd2_kernel2(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ wsx,
+                   float *__restrict__ wsd, uint32_t nvalid)
+{
+    __shared__ float lds[pad(1u << 15)];
+    const uint32_t half = gridDim.x >> 1;
+    const bool second = blockIdx.x >= half;
+    const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
+    outer_fwd_tile2<HB, R, T>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
+}
+
+template <int HB, int R, typename T>
+__global__ void __launch_bounds__(1 << (15 - VB))
+outer_inv_kernel2(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
+{
+    constexpr int A = 16, M = 15;
+    using G = Groups<M, 0>;
+    using Run = RunMap<HB, R>;
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    if (valid == 0)
+        return;   // wholly padding: nothing to store (uniform per workgroup)
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
+    float v0[V], v1[V];
+    load_layout<G::SL, Run, float>(v0, r, tau);
+    load_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+    inverse_groups<M, 0, G::NBOT - 1>(lds, v0, tau);
+    inverse_groups<M, 0, G::NBOT - 1>(lds, v1, tau);
+    butterflies<0, VB>(v0);
+    butterflies<0, VB>(v1);
+    cross_butterflies(v0, v1);
+    T *base = y + b * nvalid + ((size_t)hi << A);
+    store_tile<G::TOP, M, T>(v0, base, min(valid, 1u << M), tau);
+    if (valid > (1u << M))
+        store_tile<G::TOP, M, T>(v1, base + (1u << M), valid - (1u << M), tau);
+}
+
+// Launch helpers for the mixer's outer passes (2^11..2^16 tiles).
+template <int K, typename T>
+hipError_t launch_outer_fwd(const T *x, float *ws, int64_t B, uint32_t nvalid, hipStream_t st)
+{
+    constexpr Split sp = three_pass_split(K);
+    const dim3 grid((uint32_t)(B << sp.HB));
+    if constexpr (sp.A == 16)
+        hipLaunchKernelGGL((outer_fwd_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
+                           st, x, ws, nvalid);
+    else
+        hipLaunchKernelGGL((outer_fwd_kernel<sp.A, sp.HB, sp.R, T>), grid,
+                           dim3(1u << (sp.A - VB)), 0, st, x, ws, nvalid);
+    return hipGetLastError();
+}
+
+template <int K, typename T>
+hipError_t launch_outer_fwd2(const T *x, const T *dy, float *wsx, float *wsd, int64_t B,
+                             uint32_t nvalid, hipStream_t st)
+{
+    constexpr Split sp = three_pass_split(K);
+    const dim3 grid((uint32_t)(2 * (B << sp.HB)));
+    if constexpr (sp.A == 16)
+        hipLaunchKernelGGL((outer_fwd2_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
+                           st, x, dy, wsx, wsd, nvalid);
+    else
+        hipLaunchKernelGGL((outer_fwd2_kernel<sp.A, sp.HB, sp.R, T>), grid,
+                           dim3(1u << (sp.A - VB)), 0, st, x, dy, wsx, wsd, nvalid);
+    return hipGetLastError();
+}
+
+template <int K, typename T>
+hipError_t launch_outer_inv(const float *ws, T *y, int64_t B, uint32_t nvalid, hipStream_t st)
+{
+    constexpr Split sp = three_pass_split(K);
+    const dim3 grid((uint32_t)(B << sp.HB));
+    if constexpr (sp.A == 16)
+        hipLaunchKernelGGL((outer_inv_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
+                           st, ws, y, nvalid);
+    else
+        hipLaunchKernelGGL((outer_inv_kernel<sp.A, sp.HB, sp.R, T>), grid,
+                           dim3(1u << (sp.A - VB)), 0, st, ws, y, nvalid);
+    return hipGetLastError();
 }
 
 }  // namespace tile

@@ -238,6 +238,10 @@ def test_plan_table():
     assert d["workspace_bytes"] == 3 * 512 * 128 * 4
     d = whtmix.plan_describe(2, 64, 64, plan="three_pass")
     assert d["plan"] == "three_pass" and d["outer_bits"] == 11
+    d = whtmix.plan_describe(4, 65536, 128, "bf16")
+    assert (d["outer_bits"], d["run_bits"], d["workspace_bytes"]) == (14, 5, 4 << 25)
+    d = whtmix.plan_describe(1, 262144, 256, "bf16")   # 2^16 outer tiles
+    assert (d["outer_bits"], d["run_bits"], d["workspace_bytes"]) == (16, 5, 1 << 28)
     for w in workloads.WORKLOADS.values():
         d = whtmix.plan_describe(w.B, w.N, w.C, w.dtype)
         K = d["log2_slice"]
@@ -245,7 +249,8 @@ def test_plan_table():
         if K >= 16:
             A, R = d["outer_bits"], d["run_bits"]
             assert d["plan"] == "three_pass"
-            assert 11 <= A <= 15 and 11 <= K - A + R <= 15 and R <= A
+            assert 11 <= A <= 16 and 11 <= K - A + R <= 15 and R <= A
+            assert (A == 16) == (K >= 26)
 
 
 def test_every_three_pass_split_fits_the_tiles():
@@ -254,7 +259,7 @@ def test_every_three_pass_split_fits_the_tiles():
         C = 1 << (K - K // 2)
         d = whtmix.plan_describe(1, N, C, plan="three_pass")
         A, R = d["outer_bits"], d["run_bits"]
-        assert 11 <= A <= 15, K
+        assert 11 <= A <= 15 or (A == 16 and K >= 26), K   # 2^16 outer tiles from 2^26
         assert 1 <= K - A and 11 <= K - A + R <= 15 and 0 <= R <= A, K
 
 

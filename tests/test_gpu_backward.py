@@ -80,14 +80,16 @@ def test_backward_workload(dev, orc):
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
 
 
-def test_backward_largest_middle_tile(dev, orc):
-    """A slice of 2^25 (N = 200000 padded to 2^18, C = 128): the middle pass
-    takes 2^15-element tiles, whose gradient kernel stores each slice's
+def test_backward_largest_tiles(dev, orc):
+    """A slice of 2^26 (N = 140000 padded to 2^18, C = 256): 2^16-element
+    outer tiles (the straddling one with its second register set partly valid) and
+    2^15-element middle tiles, whose gradient kernel stores each slice's
     product as soon as it is formed."""
     import torch
-    B, N, C, dtype = 1, 200000, 128, "bf16"
+    B, N, C, dtype = 1, 140000, 256, "bf16"
     x, dy, g = inputs(B, N, C, dtype, seed=950)
     info = whtmix.plan_describe(B, N, C, dtype)
+    assert info["outer_bits"] == 16
     assert info["log2_slice"] - info["outer_bits"] + info["run_bits"] == 15
     dx, dg = whtmix.backward(to_device(x, dtype, dev), to_device(dy, dtype, dev),
                              torch.from_numpy(g).to(dev))

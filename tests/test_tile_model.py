@@ -54,13 +54,22 @@ def clampi(v, lo, hi):
     return max(lo, min(hi, v))
 
 
-def three_pass_split(K):
+def module_split(K):
+    """The block's split (csrc/whtmix_plan.h module_split): tiles <= 2^15."""
     if K >= 16:
         A = clampi((K + 6) // 2, 11, 15)
         HB = K - A
         R = clampi(5, 11 - HB, 15 - HB)
         return A, HB, R
     return 11, K - 11, 22 - K
+
+
+def three_pass_split(K):
+    """The mixer's split: 2^16 outer tiles (two register sets) from K = 26."""
+    if K < 26:
+        return module_split(K)
+    HB = K - 16
+    return 16, HB, clampi(5, 11 - HB, 15 - HB)
 
 
 def butterflies(v, j0, j1):
@@ -145,6 +154,66 @@ def tile_valid(nvalid, hi, A):
     return 0 if nvalid <= start else min(nvalid - start, 1 << A)
 
 
+def outer_sets(A):
+    """Register sets of an outer tile: (tile, offset of the set's t) -- one
+    2^A tile, or for A = 16 two 2^15 sub-tiles at t and t + 2^15."""
+    if A <= 15:
+        return [(Tile(A, 0), 0)]
+    return [(Tile(15, 0), 0), (Tile(15, 0), 1 << 15)]
+
+
+def cross(v0, v1):
+    return v0 + v1, v0 - v1
+
+
+def model_outer_fwd_block(src, nvalid, b, hi, split, acc=None):
+    """One outer_fwd block (outer_fwd_tile / outer_fwd_tile2): returns the
+    workspace offsets (relative to the slice) and values of its tile."""
+    A, HB, R = split
+    valid = tile_valid(nvalid, hi, A)
+    sets = outer_sets(A)
+    vals = []
+    for T, t0 in sets:
+        t = T.idx(T.g.TOP) + t0
+        v = np.zeros(t.shape)
+        m = t < valid
+        o = b * nvalid + (hi << A) + t[m]
+        v[m] = src[acc.at(o) if acc is not None else o]
+        vals.append(v)
+    if len(sets) == 2:
+        vals = list(cross(*vals))
+    offs, out = [], []
+    for (T, t0), v in zip(sets, vals):
+        butterflies(v, 0, VB)
+        v = T.forward_groups(v, T.g.TOP)
+        offs.append((hi << R) + run_map(T.idx(T.g.SL) + t0, HB, R))
+        out.append(v)
+    return offs, out
+
+
+def model_outer_inv_block(ws_slice, nvalid, b, hi, split, acc=None, base=0):
+    """One outer_inv block: returns (y offsets, values) of its valid elements."""
+    A, HB, R = split
+    valid = tile_valid(nvalid, hi, A)
+    sets = outer_sets(A)
+    vals = []
+    for T, t0 in sets:
+        o = base + (hi << R) + run_map(T.idx(T.g.SL) + t0, HB, R)
+        v = ws_slice[acc.at(o) if acc is not None else o].copy()
+        v = T.inverse_groups(v)
+        butterflies(v, 0, VB)
+        vals.append(v)
+    if len(sets) == 2:
+        vals = list(cross(*vals))
+    offs, out = [], []
+    for (T, t0), v in zip(sets, vals):
+        t = T.idx(T.g.TOP) + t0
+        m = t < valid
+        offs.append(b * nvalid + (hi << A) + t[m])
+        out.append(v[m])
+    return offs, out
+
+
 def simulate_three_pass(x, g, K, split):
     """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel.  x holds
     N <= 2^K / C real tokens per slice (zero padding of the token axis)."""
@@ -162,16 +231,9 @@ def simulate_three_pass(x, g, K, split):
     # outer forward: block = b * 2^HB + hi
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        T = Tile(A, 0)
-        valid = tile_valid(nvalid, hi, A)
-        t = T.idx(T.g.TOP)
-        v = np.zeros(t.shape)
-        m = t < valid
-        v[m] = xs[acc_x.at(b * nvalid + (hi << A) + t[m])]
-        butterflies(v, 0, VB)
-        v = T.forward_groups(v, T.g.TOP)
-        wbase = b * L + (hi << R)
-        ws[acc["ws_w1"].at(wbase + run_map(T.idx(T.g.SL), HB, R))] = v
+        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split, acc_x)
+        for o, v in zip(offs, vals):
+            ws[acc["ws_w1"].at(b * L + o)] = v
     # middle: logical tile = run * B + b, XCD renumbering of blocks
     M = HB + R
     nblk = B << (A - R)
@@ -192,17 +254,11 @@ def simulate_three_pass(x, g, K, split):
     # outer inverse
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        valid = tile_valid(nvalid, hi, A)
-        if valid == 0:
+        if tile_valid(nvalid, hi, A) == 0:
             continue
-        T = Tile(A, 0)
-        wbase = b * L + (hi << R)
-        v = ws[acc_r3.at(wbase + run_map(T.idx(T.g.SL), HB, R))].copy()
-        v = T.inverse_groups(v)
-        butterflies(v, 0, VB)
-        t = T.idx(T.g.TOP)
-        m = t < valid
-        y[acc_y.at(b * nvalid + (hi << A) + t[m])] = v[m]
+        offs, vals = model_outer_inv_block(ws, nvalid, b, hi, split, acc_r3, base=b * L)
+        for o, v in zip(offs, vals):
+            y[acc_y.at(o)] = v
     for k, a in acc.items():
         assert np.all(a.count == 1), f"{k}: elements not touched exactly once"
     assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
@@ -274,8 +330,10 @@ def test_three_pass_maps_in_bounds(K):
     L = 1 << K
     B = 3
     Mm = HB + R
-    assert 11 <= A <= 15 and 11 <= Mm <= 15 and 0 <= R <= A and HB >= 1
-    To = Tile(A, 0)
+    assert 11 <= A <= 16 and 11 <= Mm <= 15 and 0 <= R <= A and HB >= 1
+    if K >= 26:   # 2^16 outer tiles: one more carried bit than the block's split
+        assert A == 16 and R == module_split(K)[2] + 1
+    To = Tile(min(A, 15), 0)
     Tm = Tile(Mm, R)
     # groups transform every tile bit in [WT, M) exactly once
     for T in (To, Tm):
@@ -289,13 +347,18 @@ def test_three_pass_maps_in_bounds(K):
     # the outer passes' last layout keeps 32 consecutive lanes on consecutive
     # elements (coalesced workspace runs)
     assert To.g.SL == 5
+    sets = [0] if A <= 15 else [0, 1 << 15]
     for blk in (0, (B << HB) // 2, (B << HB) - 1):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        o = b * L + (hi << A) + To.idx(To.g.TOP)
+        o = np.concatenate([b * L + (hi << A) + To.idx(To.g.TOP) + t0 for t0 in sets])
         assert o.min() >= 0 and o.max() < B * L
-        w = b * L + (hi << R) + run_map(To.idx(To.g.SL), HB, R)
+        assert len(np.unique(o)) == o.size == 1 << A
+        w = np.concatenate([b * L + (hi << R) + run_map(To.idx(To.g.SL) + t0, HB, R)
+                            for t0 in sets])
         assert w.min() >= 0 and w.max() < B * L
         assert len(np.unique(w)) == w.size
+        # the buffer extent of the block's workspace resource covers every offset
+        assert (w - b * L - (hi << R)).max() < run_map((1 << A) - 1, HB, R) + 1
     nblk = B << (A - R)
     for blk in (0, nblk // 2, nblk - 1):
         logical = (blk & 7) * (nblk >> 3) + (blk >> 3) if nblk % 8 == 0 else blk
@@ -306,6 +369,29 @@ def test_three_pass_maps_in_bounds(K):
         goff = (run << R) + gain_map(Tm.idx(Tm.g.SL), A, R)
         assert goff.min() >= 0 and goff.max() < L
     assert pad((1 << 15) - 1) < 160 * 1024 // 4   # LDS fits in 160 KiB
+
+
+@pytest.mark.parametrize("K,split", [(18, (16, 2, 9)), (20, (16, 4, 7)), (17, (16, 1, 10))])
+@pytest.mark.parametrize("N_frac", [1.0, 0.93, 0.8, 0.55])
+def test_pair_outer_tiles(K, split, N_frac, orc):
+    """2^16 outer tiles (two 2^15 register sets and a butterfly between them),
+    executed on small slices by forcing A = 16.  With padding (N > P/2, so the
+    padded size stays P) the straddling tile's second set is partly valid or
+    wholly padding, and later tiles are all padding."""
+    rng = np.random.default_rng(K + int(10 * N_frac))
+    C = 64
+    P = 1 << (K - 6)
+    N = max(1, int(P * N_frac))
+    x = rng.standard_normal((2, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    y = simulate_three_pass(x, g, K, split)
+    ref = orc.whtmix(x, g)
+    assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
+    dy = rng.standard_normal((2, N, C))
+    dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
+    dg, dx = simulate_grad_three_pass(x, dy, g, K, split)
+    assert np.max(np.abs(dg - dg_ref.reshape(-1))) < 1e-11 * np.max(np.abs(dg_ref))
+    assert np.max(np.abs(dx - dx_ref)) < 1e-11 * np.max(np.abs(dx_ref))
 
 
 @pytest.mark.parametrize("N,C", [(1000, 2), (33, 64), (100, 64), (130, 128), (257, 64)])
@@ -336,15 +422,9 @@ def model_outer_fwd(x, K, split):
     ws = np.full(B * L, np.nan)
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        T = Tile(A, 0)
-        valid = tile_valid(nvalid, hi, A)
-        t = T.idx(T.g.TOP)
-        v = np.zeros(t.shape)
-        m = t < valid
-        v[m] = xs[b * nvalid + (hi << A) + t[m]]
-        butterflies(v, 0, VB)
-        v = T.forward_groups(v, T.g.TOP)
-        ws[b * L + (hi << R) + run_map(T.idx(T.g.SL), HB, R)] = v
+        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split)
+        for o, v in zip(offs, vals):
+            ws[b * L + o] = v
     assert not np.isnan(ws).any()
     return ws
 
@@ -407,16 +487,11 @@ def simulate_grad_three_pass(x, dy, g, K, split):
     acc_y = Access(B * nvalid)
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        valid = tile_valid(nvalid, hi, A)
-        if valid == 0:
+        if tile_valid(nvalid, hi, A) == 0:
             continue
-        T = Tile(A, 0)
-        v = wsd[b * L + (hi << R) + run_map(T.idx(T.g.SL), HB, R)].copy()
-        v = T.inverse_groups(v)
-        butterflies(v, 0, VB)
-        t = T.idx(T.g.TOP)
-        m = t < valid
-        dx[acc_y.at(b * nvalid + (hi << A) + t[m])] = v[m]
+        offs, vals = model_outer_inv_block(wsd, nvalid, b, hi, split, base=b * L)
+        for o, v in zip(offs, vals):
+            dx[acc_y.at(o)] = v
     assert np.all(acc_y.count == 1)
     return part.reshape(nch, L).sum(axis=0), dx.reshape(x.shape)
 
