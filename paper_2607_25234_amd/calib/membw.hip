@@ -10,6 +10,13 @@
 //       pattern the WHTMix three-pass traffic (bf16 x -> f32 workspace ->
 //               f32 workspace -> bf16 y, B=4 slices of 2^23) done by plain
 //               copies: the floor for any three-pass schedule of that shape
+//   membw fabric              traffic that leaves the XCDs (L2 misses), with
+//                             eight 16-byte loads in flight per lane:
+//       read    re-read of S bytes, the block -> data map rotated by one
+//               block per launch so no XCD finds its data in its own L2:
+//               Infinity Cache (S <= 256 MiB) vs HBM rate
+//       wr+rd   write S bytes, then read them back (rotated)
+//       rmw     in-place read-modify-write of a resident buffer
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -79,6 +86,60 @@ __global__ void narrow(const float4 *__restrict__ in, uint2 *__restrict__ out, s
         const float4 v = in[i];
         out[i] = make_uint2((__float_as_uint(v.x) >> 16) | (__float_as_uint(v.y) & 0xffff0000u),
                             (__float_as_uint(v.z) >> 16) | (__float_as_uint(v.w) & 0xffff0000u));
+    }
+}
+
+// Chunks of BS*U float4 per block and iteration; chunk c is handled by block
+// (c + rot) mod grid, so a rotation moves every chunk to another XCD.
+constexpr int kU = 8, kBS = 256;
+
+__device__ __forceinline__ size_t first_chunk(int rot)
+{
+    return (blockIdx.x + gridDim.x - (unsigned)rot % gridDim.x) % gridDim.x;
+}
+
+__global__ void __launch_bounds__(kBS)
+fab_read(const float4 *__restrict__ in, float *__restrict__ sink, size_t n4, int rot)
+{
+    const size_t chunk = (size_t)kBS * kU, nch = n4 / chunk;
+    float acc = 0.f;
+    for (size_t c = first_chunk(rot); c < nch; c += gridDim.x) {
+        float4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            v[u] = in[c * chunk + u * kBS + threadIdx.x];
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            acc += v[u].x + v[u].y + v[u].z + v[u].w;
+    }
+    if (acc == 1234.5f)   // never true for the zero-filled buffers: keeps the loads
+        sink[threadIdx.x] = acc;
+}
+
+__global__ void __launch_bounds__(kBS)
+fab_write(float4 *__restrict__ out, size_t n4, int rot, float val)
+{
+    const size_t chunk = (size_t)kBS * kU, nch = n4 / chunk;
+    for (size_t c = first_chunk(rot); c < nch; c += gridDim.x)
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            out[c * chunk + u * kBS + threadIdx.x] = make_float4(val, val, val, val);
+}
+
+__global__ void __launch_bounds__(kBS)
+fab_rmw(float4 *__restrict__ s, size_t n4, int rot)
+{
+    const size_t chunk = (size_t)kBS * kU, nch = n4 / chunk;
+    for (size_t c = first_chunk(rot); c < nch; c += gridDim.x) {
+        float4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            v[u] = s[c * chunk + u * kBS + threadIdx.x];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            v[u].x += 1.f;
+            s[c * chunk + u * kBS + threadIdx.x] = v[u];
+        }
     }
 }
 
@@ -206,6 +267,83 @@ int do_sweep()
     return 0;
 }
 
+int do_fabric()
+{
+    const size_t MiB = 1 << 20, total = 3072 * MiB;
+    hipEvent_t e0, e1, e2;
+    CK(hipEventCreate(&e0));
+    CK(hipEventCreate(&e1));
+    CK(hipEventCreate(&e2));
+    float *sink;
+    char *buf;
+    CK(hipMalloc(&sink, sizeof(float) * kBS));
+    CK(hipMalloc(&buf, total));
+    CK(hipMemset(buf, 0, total));
+    auto grid = [](size_t n4) {
+        const size_t nch = n4 / ((size_t)kBS * kU);
+        return (unsigned)(nch < (size_t)kGrid ? nch : (size_t)kGrid);
+    };
+    for (size_t s : {32, 64, 128, 192, 256, 512, 1024}) {
+        const size_t n4 = s * MiB / 16;
+        const int reps = 20;
+        for (int r = 0; r < 3; ++r)
+            hipLaunchKernelGGL(fab_read, dim3(grid(n4)), dim3(kBS), 0, 0, (const float4 *)buf, sink,
+                               n4, r);
+        CK(hipDeviceSynchronize());
+        CK(hipEventRecord(e0, 0));
+        for (int r = 0; r < reps; ++r)
+            hipLaunchKernelGGL(fab_read, dim3(grid(n4)), dim3(kBS), 0, 0, (const float4 *)buf, sink,
+                               n4, r + 3);
+        CK(hipEventRecord(e1, 0));
+        CK(hipEventSynchronize(e1));
+        std::printf("read %zuMiB %.0f GB/s\n", s,
+                    (double)s * MiB * reps / (elapsed(e0, e1) * 1e-3) / 1e9);
+    }
+    for (size_t s : {64, 128, 256, 512}) {
+        const size_t n4 = s * MiB / 16;
+        const int reps = 10;
+        double tw = 0, tr = 0;
+        for (int r = 0; r < reps + 2; ++r) {
+            // evict: read 2 GiB elsewhere
+            hipLaunchKernelGGL(fab_read, dim3(kGrid), dim3(kBS), 0, 0,
+                               (const float4 *)(buf + 1024 * MiB), sink, 2048 * MiB / 16, 0);
+            CK(hipEventRecord(e0, 0));
+            hipLaunchKernelGGL(fab_write, dim3(grid(n4)), dim3(kBS), 0, 0, (float4 *)buf, n4, r,
+                               0.0f);
+            CK(hipEventRecord(e1, 0));
+            hipLaunchKernelGGL(fab_read, dim3(grid(n4)), dim3(kBS), 0, 0, (const float4 *)buf, sink,
+                               n4, r + 1);
+            CK(hipEventRecord(e2, 0));
+            CK(hipEventSynchronize(e2));
+            if (r >= 2) {
+                tw += elapsed(e0, e1);
+                tr += elapsed(e1, e2);
+            }
+        }
+        std::printf("wr+rd %zuMiB write %.0f GB/s read %.0f GB/s\n", s,
+                    (double)s * MiB * reps / (tw * 1e-3) / 1e9,
+                    (double)s * MiB * reps / (tr * 1e-3) / 1e9);
+    }
+    for (size_t s : {64, 128}) {
+        const size_t n4 = s * MiB / 16;
+        const int reps = 20;
+        for (int r = 0; r < 3; ++r)
+            hipLaunchKernelGGL(fab_rmw, dim3(grid(n4)), dim3(kBS), 0, 0, (float4 *)buf, n4, r);
+        CK(hipDeviceSynchronize());
+        CK(hipEventRecord(e0, 0));
+        for (int r = 0; r < reps; ++r)
+            hipLaunchKernelGGL(fab_rmw, dim3(grid(n4)), dim3(kBS), 0, 0, (float4 *)buf, n4, r + 3);
+        CK(hipEventRecord(e1, 0));
+        CK(hipEventSynchronize(e1));
+        std::printf("rmw %zuMiB %.0f GB/s (read + written bytes)\n", s,
+                    2.0 * s * MiB * reps / (elapsed(e0, e1) * 1e-3) / 1e9);
+    }
+    CK(hipGetLastError());
+    CK(hipFree(buf));
+    CK(hipFree(sink));
+    return 0;
+}
+
 }  // namespace
 
 int main(int argc, char **argv)
@@ -221,6 +359,8 @@ int main(int argc, char **argv)
     }
     if (argc >= 2 && std::strcmp(argv[1], "sweep") == 0)
         return do_sweep();
-    std::fprintf(stderr, "usage: membw copy <MiB> <reps> | membw sweep\n");
+    if (argc >= 2 && std::strcmp(argv[1], "fabric") == 0)
+        return do_fabric();
+    std::fprintf(stderr, "usage: membw copy <MiB> <reps> | membw sweep | membw fabric\n");
     return 2;
 }

@@ -492,7 +492,7 @@ int module_backward_impl(const void *x, const void *w_in, int gain_kind, const f
     const int64_t zb = align256(rows * C * 4);
     const int64_t pk = align256((int64_t)(3 * wb));
     const whtmix::WgradPlan wp = whtmix::wgrad_plan((uint64_t)rows, cbits);
-    const int64_t part = align256((int64_t)wp.chunks * C * C * 4);
+    const int64_t part = align256((int64_t)wp.partial_floats(cbits) * 4);
     const int64_t mix = align256(c.ws_bytes);
     const whtmix::BackwardLayout lay = whtmix::backward_layout(c.plan, c.K, B, C, sep);
     const int64_t bwd = align256((int64_t)(lay.floats * 4));

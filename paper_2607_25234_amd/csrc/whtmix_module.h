@@ -58,27 +58,33 @@ hipError_t launch_module(const ModuleArgs &m);
 
 // ---------------------------------------------------------------- backward
 // Split of a weight gradient dW = A^T B over rows (A, B [rows][C]): `chunks`
-// partial C x C sums of `rows_per_chunk` rows each, added in a fixed order.
+// partial C x C sums of `rows_per_chunk` rows each, added in a fixed order:
+// first in groups of kWgradGroup consecutive chunks, then the group sums.
+constexpr uint32_t kWgradGroup = 16;
 struct WgradPlan {
     uint32_t chunks;
     uint32_t rows_per_chunk;
+    uint32_t groups() const { return (chunks + kWgradGroup - 1) / kWgradGroup; }
+    // floats of partial sums: the chunks' and the groups'
+    uint64_t partial_floats(int cbits) const
+    {
+        return (uint64_t)(chunks + groups()) << (2 * cbits);
+    }
 };
 
+// About 512 workgroups (two per CU) over the chunks and the (C/T)^2 output
+// blocks of the matrix-core kernel (T = min(C, 128)), at least 64 rows per
+// chunk; C < 16 (the VALU kernel, one block per chunk) the same.
 inline WgradPlan wgrad_plan(uint64_t rows, int cbits)
 {
     if (rows == 0) return WgradPlan{0, 4};   // no partials: the sums are zero
     const uint64_t C = uint64_t(1) << cbits;
-    uint64_t tiles = 1;   // output tiles of one chunk (one wave each)
-    if (C >= 16) {
-        const uint64_t tb = C / 16 < 4 ? C / 16 : 4;
-        const uint64_t side = C / (16 * tb);
-        tiles = side * side;
-    }
-    uint64_t chunks = 2048 / tiles;
+    const uint64_t T = C < 128 ? C : 128;
+    const uint64_t blocks = C >= 16 ? (C / T) * (C / T) : 1;
+    uint64_t chunks = 512 / blocks;
     if (chunks < 1) chunks = 1;
     const uint64_t most = (rows + 63) / 64;   // at least 64 rows per chunk
     if (chunks > most) chunks = most;
-    if (chunks < 1) chunks = 1;
     uint64_t rpc = (rows + chunks - 1) / chunks;
     rpc = (rpc + 3) / 4 * 4;
     if (rpc == 0) rpc = 4;

@@ -34,6 +34,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "whtmix_launch.h"
 #include "whtmix_module.h"
 #include "whtmix_plan.h"
@@ -1109,56 +1111,214 @@ pack_b_kernel(const T *__restrict__ w, T *__restrict__ p, int cb, int trans)
     p[idx] = trans ? w[col * C + k] : w[k * C + col];
 }
 
-// Partial dW = A^T B of one chunk of rows, one 16TB x 16TB output tile per
-// wave (no LDS, no barriers: a wave past the last tile returns at once).
-template <typename Ta, typename Tb, int TB>
+// Partial dW = A^T B (A, B [rows][C]) of one chunk of rows on the matrix
+// cores: one workgroup per (chunk, T x T block of dW), T = min(C, 128).
+//
+// Rows go through LDS in blocks of 64: 16-byte global loads, widened to
+// float32 rows padded to LDW floats, the next block's loads issued before the
+// current block's products.  Each wave owns a TQ x TQ quadrant of 16 x 16
+// tiles (T = 16: wave 0 alone).  In one MFMA the lanes (i, q) hold, for
+// k-slot e, the rows kb + q + 4e of column i: any assignment of rows to
+// k-slots is a valid contraction order, and this one makes the four lane
+// groups q read rows one apart, which LDW = T + 16 (48 for T = 16) puts on
+// disjoint banks.
+//
+// Products (float32 accumulation):
+//   float32 x float32: v_mfma_f32_16x16x4_f32, four rows per step;
+//   bf16 x bf16:       v_mfma_f32_16x16x16_bf16, exact;
+//   bf16 x float32:    the float is split into three bf16 terms (residual
+//                      below 2^-27 |v|, finer than float32 itself) and each
+//                      term goes through the bf16 instruction.
+template <typename Ta, typename Tb, int T>
+struct WgradShape {
+    static constexpr int RB = 64;                          // rows per LDS block
+    static constexpr int LDW = T == 16 ? 48 : T + 16;      // padded LDS row (floats)
+    static constexpr int TQ = T >= 32 ? T / 32 : 1;        // tiles per wave side
+    static constexpr int VA = 16 / (int)sizeof(Ta);        // elements per 16-byte load
+    static constexpr int VBL = 16 / (int)sizeof(Tb);
+    static constexpr int NA = (RB * T / VA + 255) / 256;   // loads per thread per block
+    static constexpr int NB = (RB * T / VBL + 255) / 256;
+};
+
+template <typename Te, int VE, int N, int T>
+__device__ __forceinline__ void wgrad_fetch(u32x4 (&r)[N], const Te *__restrict__ src, uint32_t C,
+                                            uint32_t col0, uint32_t row0, uint32_t row_end)
+{
+    constexpr uint32_t PER_ROW = T / VE;
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+        const uint32_t v = threadIdx.x + 256u * (uint32_t)n;
+        const uint32_t row = row0 + v / PER_ROW;
+        r[n] = (u32x4){0u, 0u, 0u, 0u};
+        if (v < 64u * PER_ROW && row < row_end)
+            r[n] = *reinterpret_cast<const u32x4 *>(src + (size_t)row * C + col0 +
+                                                    (v % PER_ROW) * VE);
+    }
+}
+
+template <typename Te, int VE, int N, int T, int LDW>
+__device__ __forceinline__ void wgrad_stage(float *lds, const u32x4 (&r)[N])
+{
+    constexpr uint32_t PER_ROW = T / VE;
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+        const uint32_t v = threadIdx.x + 256u * (uint32_t)n;
+        if (v >= 64u * PER_ROW) continue;
+        float *dst = lds + (v / PER_ROW) * LDW + (v % PER_ROW) * VE;
+        if constexpr (VE == 4) {
+            *reinterpret_cast<f32x4 *>(dst) = __builtin_bit_cast(f32x4, r[n]);
+        } else {   // eight bf16: widening is exact (the bits are the float's high half)
+            const u32x4 u = r[n];
+            *reinterpret_cast<f32x4 *>(dst) =
+                (f32x4){__builtin_bit_cast(float, u.x << 16), __builtin_bit_cast(float, u.x & 0xffff0000u),
+                        __builtin_bit_cast(float, u.y << 16), __builtin_bit_cast(float, u.y & 0xffff0000u)};
+            *reinterpret_cast<f32x4 *>(dst + 4) =
+                (f32x4){__builtin_bit_cast(float, u.z << 16), __builtin_bit_cast(float, u.z & 0xffff0000u),
+                        __builtin_bit_cast(float, u.w << 16), __builtin_bit_cast(float, u.w & 0xffff0000u)};
+        }
+    }
+}
+
+// Three-term bf16 split of four floats: v = hi + mid + lo + d with each term
+// the nearest bf16 of what the previous ones leave (the differences are exact
+// in float32) and |d| <= 2^-27 |v|.
+__device__ __forceinline__ void split3_bf16(const f32x4 &z, bf16x4 &hi, bf16x4 &mid, bf16x4 &lo)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const __bf16 h = (__bf16)z[e];
+        const float r1 = z[e] - (float)h;
+        const __bf16 m = (__bf16)r1;
+        hi[e] = __builtin_bit_cast(short, h);
+        mid[e] = __builtin_bit_cast(short, m);
+        lo[e] = __builtin_bit_cast(short, (__bf16)(r1 - (float)m));
+    }
+}
+
+// Four k-slot values of one lane as bf16, for bf16-origin values: their high
+// halves, exactly.  (The whole vector is bit-cast: a bit_cast of one
+// ext-vector element reads element 0 in this toolchain.)
+__device__ __forceinline__ bf16x4 bf16_exact(const f32x4 &z)
+{
+    const u32x4 u = __builtin_bit_cast(u32x4, z);
+    bf16x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        o[e] = (short)(u[e] >> 16);
+    return o;
+}
+
+// TOUT: store the transposed block (the caller passed B and A to get dW^T's
+// blocks, i.e. dW's).
+template <typename Ta, typename Tb, int T, bool TOUT>
 __global__ void __launch_bounds__(256)
 wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__restrict__ part,
                   uint32_t rows, uint32_t rpc, int cb)
 {
+    using S = WgradShape<Ta, Tb, T>;
+    constexpr int LDW = S::LDW, TQ = S::TQ;
+    constexpr bool F32 = sizeof(Ta) == 4 && sizeof(Tb) == 4;
+    constexpr bool SPLIT_A = sizeof(Ta) == 4 && !F32;   // a is the float operand
+    constexpr bool SPLIT_B = sizeof(Tb) == 4 && !F32;
+    __shared__ float sa[S::RB * LDW], sb[S::RB * LDW];
     const uint32_t C = 1u << cb;
-    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
-    const uint32_t i = lane & 15u, q = lane >> 4;
-    const uint32_t side = C / (16u * TB);
-    const uint32_t tile = blockIdx.x * 4u + w;
-    if (tile >= side * side) return;
-    const uint32_t c0 = (tile / side) * 16u * TB, d0 = (tile % side) * 16u * TB;
+    const uint32_t nside = C / (uint32_t)T;
+    const uint32_t c0 = (blockIdx.x / nside) * T, d0 = (blockIdx.x % nside) * T;
     const uint32_t chunk = blockIdx.y;
     const uint32_t r_begin = chunk * rpc;
     const uint32_t r_end = min(rows, r_begin + rpc);
-    f32x4 acc[TB][TB];
+    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
+    const uint32_t i = lane & 15u, q = lane >> 4;
+    const bool active = T >= 32 || w == 0;
+    const uint32_t tr0 = T >= 32 ? (w >> 1) * TQ : 0u, tc0 = T >= 32 ? (w & 1u) * TQ : 0u;
+    f32x4 acc[TQ][TQ];
 #pragma unroll
-    for (int ib = 0; ib < TB; ++ib)
+    for (int x = 0; x < TQ; ++x)
 #pragma unroll
-        for (int jb = 0; jb < TB; ++jb)
-            acc[ib][jb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-    for (uint32_t r0 = r_begin; r0 < r_end; r0 += 4u) {
-        const uint32_t r = r0 + q;
-        const bool ok = r < r_end;
-        float av[TB], bv[TB];
+        for (int y = 0; y < TQ; ++y)
+            acc[x][y] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+    u32x4 ra[S::NA], rb[S::NB];
+    wgrad_fetch<Ta, S::VA, S::NA, T>(ra, a, C, c0, r_begin, r_end);
+    wgrad_fetch<Tb, S::VBL, S::NB, T>(rb, b, C, d0, r_begin, r_end);
+    for (uint32_t r0 = r_begin; r0 < r_end; r0 += S::RB) {   // uniform over the workgroup
+        __syncthreads();   // the previous block's readers are done
+        wgrad_stage<Ta, S::VA, S::NA, T, LDW>(sa, ra);
+        wgrad_stage<Tb, S::VBL, S::NB, T, LDW>(sb, rb);
+        __syncthreads();
+        if (r0 + S::RB < r_end) {
+            wgrad_fetch<Ta, S::VA, S::NA, T>(ra, a, C, c0, r0 + S::RB, r_end);
+            wgrad_fetch<Tb, S::VBL, S::NB, T>(rb, b, C, d0, r0 + S::RB, r_end);
+        }
+        if (!active)
+            continue;
+        if constexpr (F32) {
+#pragma unroll 2
+            for (int kb = 0; kb < S::RB; kb += 4) {
+                const float *ra_ = sa + (kb + q) * LDW + i;
+                const float *rb_ = sb + (kb + q) * LDW + i;
+                float av[TQ], bv[TQ];
 #pragma unroll
-        for (int ib = 0; ib < TB; ++ib)
-            av[ib] = ok ? to_f(a[(size_t)r * C + c0 + 16u * ib + i]) : 0.0f;
+                for (int x = 0; x < TQ; ++x)
+                    av[x] = ra_[16 * (tr0 + x)];
 #pragma unroll
-        for (int jb = 0; jb < TB; ++jb)
-            bv[jb] = ok ? to_f(b[(size_t)r * C + d0 + 16u * jb + i]) : 0.0f;
+                for (int y = 0; y < TQ; ++y)
+                    bv[y] = rb_[16 * (tc0 + y)];
 #pragma unroll
-        for (int ib = 0; ib < TB; ++ib)
+                for (int x = 0; x < TQ; ++x)
 #pragma unroll
-            for (int jb = 0; jb < TB; ++jb)
-                acc[ib][jb] =
-                    __builtin_amdgcn_mfma_f32_16x16x4f32(av[ib], bv[jb], acc[ib][jb], 0, 0, 0);
+                    for (int y = 0; y < TQ; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x], bv[y], acc[x][y],
+                                                                        0, 0, 0);
+            }
+        } else {
+#pragma unroll 1
+            for (int kb = 0; kb < S::RB; kb += 16) {
+                // the float operand's three terms, the bf16 operand's one
+                constexpr int NSA = SPLIT_A ? 3 : 1, NSB = SPLIT_B ? 3 : 1;
+                bf16x4 av[NSA][TQ], bv[NSB][TQ];
+#pragma unroll
+                for (int x = 0; x < TQ; ++x) {
+                    const float *src = sa + (kb + q) * LDW + 16 * (tr0 + x) + i;
+                    const f32x4 z = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    if constexpr (SPLIT_A)
+                        split3_bf16(z, av[0][x], av[1][x], av[2][x]);
+                    else
+                        av[0][x] = bf16_exact(z);
+                }
+#pragma unroll
+                for (int y = 0; y < TQ; ++y) {
+                    const float *src = sb + (kb + q) * LDW + 16 * (tc0 + y) + i;
+                    const f32x4 z = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    if constexpr (SPLIT_B)
+                        split3_bf16(z, bv[0][y], bv[1][y], bv[2][y]);
+                    else
+                        bv[0][y] = bf16_exact(z);
+                }
+#pragma unroll
+                for (int x = 0; x < TQ; ++x)
+#pragma unroll
+                    for (int y = 0; y < TQ; ++y)
+#pragma unroll
+                        for (int t = 0; t < NSA * NSB; ++t)
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                                av[t % NSA][x], bv[t / NSA][y], acc[x][y], 0, 0, 0);
+            }
+        }
     }
-    // lane 16q + j holds rows 4q + r (channel of a) of column j (channel of b)
+    if (!active)
+        return;
+    // lane 16q + j of a tile holds its rows 4q + r (channels of a) of column j
     float *out = part + (size_t)chunk * C * C;
 #pragma unroll
-    for (int ib = 0; ib < TB; ++ib)
+    for (int x = 0; x < TQ; ++x)
 #pragma unroll
-        for (int jb = 0; jb < TB; ++jb)
+        for (int y = 0; y < TQ; ++y)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                out[(size_t)(c0 + 16u * ib + 4u * q + r) * C + d0 + 16u * jb + i] = acc[ib][jb][r];
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t row = c0 + 16u * (tr0 + x) + 4u * q + r;
+                const uint32_t col = d0 + 16u * (tc0 + y) + i;
+                out[TOUT ? (size_t)col * C + row : (size_t)row * C + col] = acc[x][y][r];
+            }
 }
 
 // The same for C < 16 on the VALU: one thread per output of one chunk.
@@ -1179,17 +1339,20 @@ wgrad_valu_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
     part[(size_t)chunk * C * C + o] = acc;
 }
 
-// out[i] = sum over chunks c (ascending) of part[c][i].
+// out[g][i] = sum over the chunks c of group g = blockIdx.y (ascending, at
+// most `group` of them) of part[c][i]; with one group this is the total.
 __global__ void __launch_bounds__(256)
 sum_partials_kernel(const float *__restrict__ part, float *__restrict__ out, uint32_t n,
-                    uint32_t chunks)
+                    uint32_t chunks, uint32_t group)
 {
     const uint32_t i = blockIdx.x * 256u + threadIdx.x;
     if (i >= n) return;
+    const uint32_t c0 = blockIdx.y * group;
+    const uint32_t c1 = min(chunks, c0 + group);
     float s = 0.0f;
-    for (uint32_t c = 0; c < chunks; ++c)
+    for (uint32_t c = c0; c < c1; ++c)
         s += part[(size_t)c * n + i];
-    out[i] = s;
+    out[(size_t)blockIdx.y * n + i] = s;
 }
 
 template <typename T>
@@ -1247,26 +1410,47 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
     if (wp.chunks == 0) {
         // no rows: sum_partials over zero chunks writes zeros
     } else if (C >= 16) {
-        const uint32_t tb = C / 16u < 4u ? C / 16u : 4u;
-        const uint32_t side = C / (16u * tb);
-        const dim3 grid((side * side + 3u) / 4u, wp.chunks);
-        if (tb == 1)
-            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 1>), grid, dim3(256), 0, st, a, b, part,
-                               rows, wp.rows_per_chunk, cb);
-        else if (tb == 2)
-            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 2>), grid, dim3(256), 0, st, a, b, part,
-                               rows, wp.rows_per_chunk, cb);
+        // A float a against a bf16 b runs as (b, a) with the blocks stored
+        // transposed: the kernel with the bf16 operand first keeps fewer
+        // registers (two workgroups per CU at T = 128 instead of one).
+        constexpr bool SWAP = sizeof(Ta) == 4 && sizeof(Tb) == 2;
+        using T1 = std::conditional_t<SWAP, Tb, Ta>;
+        using T2 = std::conditional_t<SWAP, Ta, Tb>;
+        const T1 *p1 = reinterpret_cast<const T1 *>(SWAP ? (const void *)b : (const void *)a);
+        const T2 *p2 = reinterpret_cast<const T2 *>(SWAP ? (const void *)a : (const void *)b);
+        const uint32_t T = C < 128u ? C : 128u;
+        const dim3 grid((C / T) * (C / T), wp.chunks);
+        if (T == 16)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 16, SWAP>), grid, dim3(256), 0, st, p1,
+                               p2, part, rows, wp.rows_per_chunk, cb);
+        else if (T == 32)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 32, SWAP>), grid, dim3(256), 0, st, p1,
+                               p2, part, rows, wp.rows_per_chunk, cb);
+        else if (T == 64)
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 64, SWAP>), grid, dim3(256), 0, st, p1,
+                               p2, part, rows, wp.rows_per_chunk, cb);
         else
-            hipLaunchKernelGGL((wgrad_mfma_kernel<Ta, Tb, 4>), grid, dim3(256), 0, st, a, b, part,
-                               rows, wp.rows_per_chunk, cb);
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 128, SWAP>), grid, dim3(256), 0, st, p1,
+                               p2, part, rows, wp.rows_per_chunk, cb);
     } else {
         hipLaunchKernelGGL((wgrad_valu_kernel<Ta, Tb>), dim3(wp.chunks), dim3(256), 0, st, a, b,
                            part, rows, wp.rows_per_chunk, cb);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sum_partials_kernel, dim3((C * C + 255u) / 256u), dim3(256), 0, st, part,
-                       out, C * C, wp.chunks);
+    // fixed-order sum: groups of consecutive chunks, then the groups
+    const uint32_t n = C * C, nb = (n + 255u) / 256u;
+    if (wp.chunks <= kWgradGroup) {
+        hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(256), 0, st, part, out, n,
+                           wp.chunks, kWgradGroup);
+        return hipGetLastError();
+    }
+    float *gsum = part + (size_t)wp.chunks * n;
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb, wp.groups()), dim3(256), 0, st, part, gsum, n,
+                       wp.chunks, kWgradGroup);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(256), 0, st, gsum, out, n, wp.groups(),
+                       wp.groups());
     return hipGetLastError();
 }
 

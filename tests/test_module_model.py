@@ -587,56 +587,121 @@ def test_transposed_packing_is_the_packing_of_the_transpose():
 
 
 def wgrad_plan(rows, cb):
+    """csrc/whtmix_module.h wgrad_plan."""
     if rows == 0:
         return 0, 4
     C = 1 << cb
-    tiles = 1
-    if C >= 16:
-        tb = min(4, C // 16)
-        tiles = (C // (16 * tb)) ** 2
-    chunks = max(1, 2048 // tiles)
-    chunks = max(1, min(chunks, (rows + 63) // 64))
+    T = min(C, 128)
+    blocks = (C // T) ** 2 if C >= 16 else 1
+    chunks = max(1, 512 // blocks)
+    chunks = min(chunks, (rows + 63) // 64)
     rpc = -(-rows // chunks)
     rpc = max(4, (rpc + 3) // 4 * 4)
     return -(-rows // rpc), rpc
 
 
-def model_wgrad(a, b, cb):
-    """wgrad_mfma_kernel: per chunk of rows and output tile, 4 rows per fp32
-    MFMA step (lane 16q + i reads row q, column i of a 4 x 16 block)."""
+def bf16_rne(v):
+    """Round float32 values to bf16 (round to nearest even), as float32."""
+    u = np.asarray(v, np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32)
+
+
+def model_wgrad(a, b, cb, kinds=("f32", "f32")):
+    """wgrad_mfma_kernel: per (chunk, T x T block), 64-row LDS blocks, waves
+    owning TQ x TQ quadrants of 16 x 16 tiles; in a step the lanes (i, q)
+    take, for k-slot e, row kb + q + 4e (bf16 instruction, 16 rows) or row
+    kb + q (float32 instruction, 4 rows) of column i.  kinds: the dtypes of
+    a and b; a float against a bf16 operand is split into three bf16 terms."""
+    if kinds == ("f32", "bf16"):   # run as (b, a), blocks stored transposed
+        return model_wgrad(b, a, cb, ("bf16", "f32")).T
     rows, C = a.shape
     chunks, rpc = wgrad_plan(rows, cb)
-    tb = min(4, C // 16)
-    side = C // (16 * tb)
+    T = min(C, 128)
+    TQ = T // 32 if T >= 32 else 1
+    f32 = kinds == ("f32", "f32")
     part = np.full((chunks, C, C), np.nan)
     lanes = np.arange(64)
     i, q = lanes & 15, lanes >> 4
+
+    def parts(v, kind):
+        if f32 or kind == "bf16":
+            return [v]
+        v32 = v.astype(np.float32)
+        hi = bf16_rne(v32)
+        r1 = v32 - hi
+        mid = bf16_rne(r1)
+        return [t.astype(np.float64) for t in (hi, mid, bf16_rne(r1 - mid))]
+
+    nside = C // T
     for ch in range(chunks):
         r_end = min(rows, ch * rpc + rpc)
-        for tile in range(side * side):
-            c0, d0 = (tile // side) * 16 * tb, (tile % side) * 16 * tb
-            acc = {(ib, jb): np.zeros((64, 4)) for ib in range(tb) for jb in range(tb)}
-            for r0 in range(ch * rpc, r_end, 4):
-                r = r0 + q
-                ok = r < r_end
-                rr = np.where(ok, r, 0)
-                av = [np.where(ok, a[rr, c0 + 16 * ib + i], 0.0) for ib in range(tb)]
-                bv = [np.where(ok, b[rr, d0 + 16 * jb + i], 0.0) for jb in range(tb)]
-                for ib in range(tb):
-                    for jb in range(tb):
-                        acc[ib, jb] = mfma_f32(av[ib], bv[jb], acc[ib, jb])
-            for (ib, jb), v in acc.items():
-                for r in range(4):
-                    part[ch, c0 + 16 * ib + 4 * q + r, d0 + 16 * jb + i] = v[:, r]
+        for blk in range(nside * nside):
+            c0, d0 = (blk // nside) * T, (blk % nside) * T
+            for w in range(4 if T >= 32 else 1):
+                tr0, tc0 = ((w >> 1) * TQ, (w & 1) * TQ) if T >= 32 else (0, 0)
+                acc = {(x, y): np.zeros((64, 4)) for x in range(TQ) for y in range(TQ)}
+                for r0 in range(ch * rpc, r_end, 64):
+                    step = 4 if f32 else 16
+                    for kb in range(0, 64, step):
+                        slots = [kb + q] if f32 else [kb + q + 4 * e for e in range(4)]
+                        for x in range(TQ):
+                            for y in range(TQ):
+                                sa, sb = [], []
+                                for rr in slots:
+                                    row = r0 + rr
+                                    ok = row < r_end
+                                    rw = np.where(ok, row, 0)
+                                    sa.append(np.where(ok, a[rw, c0 + 16 * (tr0 + x) + i], 0.0))
+                                    sb.append(np.where(ok, b[rw, d0 + 16 * (tc0 + y) + i], 0.0))
+                                av, bv = np.stack(sa, 1), np.stack(sb, 1)   # [64 lanes, k]
+                                for pa in parts(av, kinds[0]):
+                                    for pb in parts(bv, kinds[1]):
+                                        acc[x, y] = mfma_k(pa, pb, acc[x, y])
+                for (x, y), v in acc.items():
+                    for r in range(4):
+                        part[ch, c0 + 16 * (tr0 + x) + 4 * q + r, d0 + 16 * (tc0 + y) + i] = v[:, r]
     assert not np.isnan(part).any()
-    return part.sum(axis=0)
+    # fixed-order sum: groups of 16 consecutive chunks, then the groups
+    groups = [part[g:g + 16].sum(axis=0) for g in range(0, chunks, 16)]
+    return np.sum(groups, axis=0)
 
 
-@pytest.mark.parametrize("rows,cb", [(130, 4), (77, 5), (300, 7), (4, 6)])
-def test_weight_gradient_model(rows, cb):
+def mfma_k(av, bv, acc):
+    """One 16x16xK MFMA: lane 16q + i holds k-slots of row i (a) / column i
+    (b); the result lane 16q + j holds rows 4q + r of column j."""
+    K = av.shape[1]
+    A = np.zeros((16, 4 * K))
+    Bm = np.zeros((4 * K, 16))
+    for lane in range(64):
+        ii, qq = lane & 15, lane >> 4
+        A[ii, qq * K:(qq + 1) * K] = av[lane]
+        Bm[qq * K:(qq + 1) * K, ii] = bv[lane]
+    D = A @ Bm
+    out = acc.copy()
+    for lane in range(64):
+        j, qq = lane & 15, lane >> 4
+        out[lane] += D[4 * qq:4 * qq + 4, j]
+    return out
+
+
+@pytest.mark.parametrize("rows,cb", [(130, 4), (77, 5), (300, 7), (4, 6), (1100, 4), (70, 8)])
+@pytest.mark.parametrize("kinds", [("f32", "f32"), ("f32", "bf16"), ("bf16", "f32"),
+                                   ("bf16", "bf16")])
+def test_weight_gradient_model(rows, cb, kinds):
+    """The modelled kernel's index maps reproduce A^T B: exactly for float32 x
+    float32 and bf16 x bf16, within the hi/lo split's residual otherwise."""
     rng = np.random.default_rng(rows + cb)
     C = 1 << cb
-    a, b = rng.standard_normal((rows, C)), rng.standard_normal((rows, C))
-    np.testing.assert_allclose(model_wgrad(a, b, cb), a.T @ b, atol=1e-10)
+    a = rng.standard_normal((rows, C)).astype(np.float32).astype(np.float64)
+    b = rng.standard_normal((rows, C)).astype(np.float32).astype(np.float64)
+    if kinds[0] == "bf16":
+        a = bf16_rne(a).astype(np.float64)
+    if kinds[1] == "bf16":
+        b = bf16_rne(b).astype(np.float64)
+    ref = a.T @ b
+    got = model_wgrad(a, b, cb, kinds)
+    tol = 1e-10 if kinds[0] == kinds[1] else 2.0 ** -26
+    assert np.max(np.abs(got - ref)) <= tol * np.max(np.abs(a).sum(0)[:, None] * np.abs(b).max(0))
     chunks, rpc = wgrad_plan(rows, cb)
     assert chunks * rpc >= rows and (chunks - 1) * rpc < rows and rpc % 4 == 0
