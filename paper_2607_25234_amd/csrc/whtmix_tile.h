@@ -178,6 +178,113 @@ __device__ __forceinline__ void inverse_groups(float *lds, float (&v)[V], uint32
     }
 }
 
+// ---------------------------------------------------------------- vector-first layout
+// Outer passes move x and y with 16-byte accesses: 2^VW elements (VW = 3 for
+// bf16, 2 for float32) of consecutive t per access.  Their first layout puts
+// t bits [0, VW) and [M - 5 + VW, M) in the registers:
+//     t = (k mod 2^VW) | (tau << VW) | ((k >> VW) << (M - 5 + VW)),
+// so register group j of 2^VW is one access.  The windows then cover
+// [VW, M - 5 + VW) from the bottom, as Groups does from bit 0.  Writes from
+// this layout to LDS hit 32 distinct banks per half-wave (the pad of one word
+// per 32 spreads the 2^VW-strided lanes), like the window layouts.
+template <int M, int VWID>
+struct VGroups {
+    static constexpr int TOPHI = M - VB + VWID;               // first top bit
+    static constexpr int NBOT = (M - VB + VB - 1) / VB;
+    static constexpr int S(int i) { return VWID + VB * i; }
+    static constexpr int NB(int i) { return (TOPHI - S(i)) < VB ? (TOPHI - S(i)) : VB; }
+    static constexpr int SL = VWID + VB * (NBOT - 1);
+    static_assert(VWID > 0 && SL + VB <= M, "vector-first layout needs a larger tile");
+    __device__ static __forceinline__ uint32_t base(uint32_t tau) { return tau << VWID; }
+    __host__ __device__ static constexpr uint32_t reg(uint32_t k)
+    {
+        return (k & ((1u << VWID) - 1u)) | ((k >> VWID) << TOPHI);
+    }
+};
+
+// Vector width (log2 elements per 16-byte access) the outer passes use for a
+// 2^M tile of elements of `bytes` bytes, or 0 for per-element accesses.
+// bf16 only: its per-element accesses move 2 bytes per lane, and 16-byte ones
+// measured 4-6% faster per step (stereo64k, stereo256k); float32 per-element
+// accesses already move 4 bytes per lane and the vector-first layout measured
+// no better (within +-4% per kernel on stereo16k and text4k).  The layout
+// itself works for float32 (VW = 2, tiles from 2^12).
+constexpr int vec_width(int M, int bytes)
+{
+    const int vw = bytes == 2 ? 3 : 0;
+    return vw > 0 && vw + VB * ((M - VB + VB - 1) / VB) <= M ? vw : 0;
+}
+
+// From the vector-first layout to window SB (the tile's first use of LDS).
+template <int M, int VWID, int SB>
+__device__ __forceinline__ void exchange_from_vec(float *lds, float (&v)[V], uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    const uint32_t pa = pad(VG::base(tau));
+    const uint32_t pb = pad(layout_base<SB>(tau));
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pa + pad(VG::reg((uint32_t)k))] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] = lds[pb + pad((uint32_t)k << SB)];
+}
+
+// From window SA to the vector-first layout.
+template <int M, int VWID, int SA>
+__device__ __forceinline__ void exchange_to_vec(float *lds, float (&v)[V], uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    const uint32_t pa = pad(layout_base<SA>(tau));
+    const uint32_t pb = pad(VG::base(tau));
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pa + pad((uint32_t)k << SA)] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        v[k] = lds[pb + pad(VG::reg((uint32_t)k))];
+}
+
+// Forward windows I, I+1, ... after the vector-first group (LEAD0: wait for
+// earlier readers of the LDS before the first write).
+template <int M, int VWID, int I, bool LEAD0 = false>
+__device__ __forceinline__ void vforward_groups(float *lds, float (&v)[V], uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    if constexpr (I < VG::NBOT) {
+        constexpr int S = VG::S(I);
+        if constexpr (I == 0) {
+            if (LEAD0)
+                __syncthreads();
+            exchange_from_vec<M, VWID, S>(lds, v, tau);
+        } else {
+            exchange<VG::S(I - 1), S>(lds, v, tau);
+        }
+        butterflies<0, VG::NB(I)>(v);
+        vforward_groups<M, VWID, I + 1>(lds, v, tau);
+    }
+}
+
+// Inverse windows I, I-1, ..., 0 (data in window I's layout), ending in the
+// vector-first layout.
+template <int M, int VWID, int I>
+__device__ __forceinline__ void vinverse_groups(float *lds, float (&v)[V], uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    if constexpr (I >= 0) {
+        constexpr int S = VG::S(I);
+        butterflies<0, VG::NB(I)>(v);
+        if constexpr (I == 0)
+            exchange_to_vec<M, VWID, S>(lds, v, tau);
+        else
+            exchange<S, VG::S(I - 1)>(lds, v, tau);
+        vinverse_groups<M, VWID, I - 1>(lds, v, tau);
+    }
+}
+
 // ---------------------------------------------------------------- address maps
 // Each map sends tile-local t to an element offset from the tile's base by
 // moving bit fields, so map(a | b) = map(a) + map(b) for disjoint a, b: the
@@ -290,6 +397,104 @@ __device__ __forceinline__ void store_tile(const float (&v)[V], T *base, uint32_
         store_layout_masked<S, ContigMap, T>(v, buffer(base, valid * Elt<T>::bytes), tau, valid);
 }
 
+typedef unsigned int vu32x4 __attribute__((ext_vector_type(4)));
+typedef float vf32x4 __attribute__((ext_vector_type(4)));
+
+// A tile of 2^M elements in the vector-first layout, 16-byte accesses
+// (streaming cache policy).  Partial tiles (the straddling tile of a padded
+// slice) take per-element masked accesses in the same layout.  Whole vectors
+// are bit-cast and then indexed: a bit_cast of one ext-vector element reads
+// element 0 in this toolchain.
+template <int M, int VWID, typename T>
+__device__ __forceinline__ void load_tile_vec(float (&v)[V], const T *base, uint32_t valid,
+                                              uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    constexpr int PER = 1 << VWID;   // elements per access
+    static_assert(PER * (int)sizeof(T) == 16, "16-byte accesses");
+    if (valid >= (1u << M)) {
+        const __amdgpu_buffer_rsrc_t r = buffer(base, (1u << M) * Elt<T>::bytes);
+        const uint32_t voff = VG::base(tau) * Elt<T>::bytes;
+#pragma unroll
+        for (int j = 0; j < V / PER; ++j) {
+            const vu32x4 q = __builtin_bit_cast(
+                vu32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                            r, voff, VG::reg((uint32_t)(j * PER)) * Elt<T>::bytes, kStreaming));
+            if constexpr (sizeof(T) == 4) {
+                const vf32x4 f = __builtin_bit_cast(vf32x4, q);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[j * PER + e] = f[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t w = q[e];
+                    v[j * PER + 2 * e] = __builtin_bit_cast(float, w << 16);
+                    v[j * PER + 2 * e + 1] = __builtin_bit_cast(float, w & 0xffff0000u);
+                }
+            }
+        }
+    } else if (valid == 0) {
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            v[k] = 0.0f;
+    } else {
+        const __amdgpu_buffer_rsrc_t r = buffer(base, valid * Elt<T>::bytes);
+        const uint32_t tb = VG::base(tau);
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            const uint32_t t = tb | VG::reg((uint32_t)k);
+            v[k] = t < valid ? Elt<T>::template load<kStreaming>(r, tb * Elt<T>::bytes,
+                                                                 VG::reg((uint32_t)k) *
+                                                                     Elt<T>::bytes)
+                             : 0.0f;
+        }
+    }
+}
+
+template <int M, int VWID, typename T>
+__device__ __forceinline__ void store_tile_vec(const float (&v)[V], T *base, uint32_t valid,
+                                               uint32_t tau)
+{
+    using VG = VGroups<M, VWID>;
+    constexpr int PER = 1 << VWID;
+    static_assert(PER * (int)sizeof(T) == 16, "16-byte accesses");
+    if (valid >= (1u << M)) {
+        const __amdgpu_buffer_rsrc_t r = buffer(base, (1u << M) * Elt<T>::bytes);
+        const uint32_t voff = VG::base(tau) * Elt<T>::bytes;
+#pragma unroll
+        for (int j = 0; j < V / PER; ++j) {
+            vu32x4 q;
+            if constexpr (sizeof(T) == 4) {
+                const vf32x4 f = {v[j * PER], v[j * PER + 1], v[j * PER + 2], v[j * PER + 3]};
+                q = __builtin_bit_cast(vu32x4, f);
+            } else {   // round to nearest even, two bf16 per word
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t lo =
+                        __builtin_bit_cast(unsigned short, (__bf16)v[j * PER + 2 * e]);
+                    const uint32_t hi =
+                        __builtin_bit_cast(unsigned short, (__bf16)v[j * PER + 2 * e + 1]);
+                    q[e] = lo | (hi << 16);
+                }
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(q, r, voff,
+                                                   VG::reg((uint32_t)(j * PER)) * Elt<T>::bytes,
+                                                   kStreaming);
+        }
+    } else if (valid > 0) {
+        const __amdgpu_buffer_rsrc_t r = buffer(base, valid * Elt<T>::bytes);
+        const uint32_t tb = VG::base(tau);
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            const uint32_t t = tb | VG::reg((uint32_t)k);
+            if (t < valid)
+                Elt<T>::template store<kStreaming>(v[k], r, tb * Elt<T>::bytes,
+                                                   VG::reg((uint32_t)k) * Elt<T>::bytes);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- gains
 // f is the flat index n*C + c of the (padded) slice.  The gain is read with
 // plain global loads: for its 128-byte-run pattern they measured markedly
@@ -390,31 +595,42 @@ __device__ __forceinline__ uint32_t tile_valid(uint32_t nvalid, uint32_t hi)
 // the chunk x[b][hi * 2^A ...] (nvalid real elements per slice, the rest
 // zero padding) is transformed over its A bits and stored to the workspace
 // in runs of 2^R, so that each middle tile is contiguous.
-template <int A, int HB, int R, typename T>
+// VWID > 0: x is read with 16-byte accesses in the vector-first layout (the
+// launcher checks that every slice starts 16-byte aligned).
+template <int A, int HB, int R, typename T, int VWID>
 __device__ __forceinline__ void outer_fwd_tile(float *lds, const T *__restrict__ x,
                                                float *__restrict__ ws, uint32_t nvalid,
                                                uint32_t blk)
 {
-    using G = Groups<A, 0>;
     using Run = RunMap<HB, R>;
     const uint32_t tau = threadIdx.x;
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
+    const T *src = x + b * nvalid + ((size_t)hi << A);
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
     float v[V];
-    load_tile<G::TOP, A, T>(v, x + b * nvalid + ((size_t)hi << A), tile_valid<A>(nvalid, hi),
-                            tau);
-    butterflies<0, VB>(v);
-    forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
-    store_layout<G::SL, Run, float>(
-        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+    if constexpr (VWID > 0) {
+        using VG = VGroups<A, VWID>;
+        load_tile_vec<A, VWID, T>(v, src, tile_valid<A>(nvalid, hi), tau);
+        butterflies<0, VB>(v);
+        vforward_groups<A, VWID, 0>(lds, v, tau);
+        store_layout<VG::SL, Run, float>(v, r, tau);
+    } else {
+        using G = Groups<A, 0>;
+        load_tile<G::TOP, A, T>(v, src, tile_valid<A>(nvalid, hi), tau);
+        butterflies<0, VB>(v);
+        forward_groups<A, 0, 0, G::TOP>(lds, v, tau);
+        store_layout<G::SL, Run, float>(v, r, tau);
+    }
 }
 
-template <int A, int HB, int R, typename T>
+template <int A, int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (A - VB))
 outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
 {
     __shared__ float lds[pad(1u << A)];
-    outer_fwd_tile<A, HB, R, T>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
+    outer_fwd_tile<A, HB, R, T, VWID>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
 }
 
 // OUTER_FWD of two operands in one launch (the backward pass's x and dy):
@@ -422,7 +638,7 @@ outer_fwd_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvali
 // half is numbered as a grid of its own; the halves start on the same XCD
 // whenever the renumbering of outer_block applies (it needs a half that is a
 // multiple of 8 blocks).
-template <int A, int HB, int R, typename T>
+template <int A, int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (A - VB))
 outer_fwd2_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ wsx,
                   float *__restrict__ wsd, uint32_t nvalid)
@@ -431,16 +647,15 @@ outer_fwd2_kernel(const T *__restrict__ x, const T *__restrict__ dy, float *__re
     const uint32_t half = gridDim.x >> 1;
     const bool second = blockIdx.x >= half;
     const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
-    outer_fwd_tile<A, HB, R, T>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
+    outer_fwd_tile<A, HB, R, T, VWID>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
 }
 
 // OUTER_INV kernel: the mirror of OUTER_FWD (inverse over the A low bits of
 // each workspace chunk, then the store of y).
-template <int A, int HB, int R, typename T>
+template <int A, int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (A - VB))
 outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
 {
-    using G = Groups<A, 0>;
     using Run = RunMap<HB, R>;
     __shared__ float lds[pad(1u << A)];
     const uint32_t tau = threadIdx.x;
@@ -450,12 +665,23 @@ outer_inv_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvali
     const uint32_t valid = tile_valid<A>(nvalid, hi);
     if (valid == 0)
         return;   // wholly padding: nothing to store (uniform per workgroup)
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
+    T *dst = y + b * nvalid + ((size_t)hi << A);
     float v[V];
-    load_layout<G::SL, Run, float>(
-        v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
-    inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
-    butterflies<0, VB>(v);
-    store_tile<G::TOP, A, T>(v, y + b * nvalid + ((size_t)hi << A), valid, tau);
+    if constexpr (VWID > 0) {
+        using VG = VGroups<A, VWID>;
+        load_layout<VG::SL, Run, float>(v, r, tau);
+        vinverse_groups<A, VWID, VG::NBOT - 1>(lds, v, tau);
+        butterflies<0, VB>(v);
+        store_tile_vec<A, VWID, T>(v, dst, valid, tau);
+    } else {
+        using G = Groups<A, 0>;
+        load_layout<G::SL, Run, float>(v, r, tau);
+        inverse_groups<A, 0, G::NBOT - 1>(lds, v, tau);
+        butterflies<0, VB>(v);
+        store_tile<G::TOP, A, T>(v, dst, valid, tau);
+    }
 }
 
 // ---------------------------------------------------------------- 2^16 outer tiles
@@ -477,44 +703,58 @@ __device__ __forceinline__ void cross_butterflies(float (&v0)[V], float (&v1)[V]
     }
 }
 
-template <int HB, int R, typename T>
+template <int HB, int R, typename T, int VWID>
 __device__ __forceinline__ void outer_fwd_tile2(float *lds, const T *__restrict__ x,
                                                 float *__restrict__ ws, uint32_t nvalid,
                                                 uint32_t blk)
 {
     constexpr int A = 16, M = 15;
-    using G = Groups<M, 0>;
     using Run = RunMap<HB, R>;
     const uint32_t tau = threadIdx.x;
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const uint32_t valid = tile_valid<A>(nvalid, hi);
+    const uint32_t valid0 = min(valid, 1u << M);
+    const uint32_t valid1 = valid > (1u << M) ? valid - (1u << M) : 0u;
     const T *base = x + b * nvalid + ((size_t)hi << A);
-    float v0[V], v1[V];
-    load_tile<G::TOP, M, T>(v0, base, min(valid, 1u << M), tau);
-    load_tile<G::TOP, M, T>(v1, base + (1u << M), valid > (1u << M) ? valid - (1u << M) : 0u,
-                            tau);
-    cross_butterflies(v0, v1);
-    butterflies<0, VB>(v0);
-    butterflies<0, VB>(v1);
-    forward_groups<M, 0, 0, G::TOP>(lds, v0, tau);
-    forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
     const __amdgpu_buffer_rsrc_t r =
         buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
-    store_layout<G::SL, Run, float>(v0, r, tau);
-    store_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+    float v0[V], v1[V];
+    if constexpr (VWID > 0) {
+        using VG = VGroups<M, VWID>;
+        load_tile_vec<M, VWID, T>(v0, base, valid0, tau);
+        load_tile_vec<M, VWID, T>(v1, base + (1u << M), valid1, tau);
+        cross_butterflies(v0, v1);
+        butterflies<0, VB>(v0);
+        butterflies<0, VB>(v1);
+        vforward_groups<M, VWID, 0>(lds, v0, tau);
+        vforward_groups<M, VWID, 0, true>(lds, v1, tau);
+        store_layout<VG::SL, Run, float>(v0, r, tau);
+        store_layout<VG::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+    } else {
+        using G = Groups<M, 0>;
+        load_tile<G::TOP, M, T>(v0, base, valid0, tau);
+        load_tile<G::TOP, M, T>(v1, base + (1u << M), valid1, tau);
+        cross_butterflies(v0, v1);
+        butterflies<0, VB>(v0);
+        butterflies<0, VB>(v1);
+        forward_groups<M, 0, 0, G::TOP>(lds, v0, tau);
+        forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
+        store_layout<G::SL, Run, float>(v0, r, tau);
+        store_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+    }
 }
 
-template <int HB, int R, typename T>
+template <int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (15 - VB))
 outer_fwd_kernel2(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
 {
     __shared__ float lds[pad(1u << 15)];
-    outer_fwd_tile2<HB, R, T>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
+    outer_fwd_tile2<HB, R, T, VWID>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
 }
 
 // Two operands in one launch (as outer_fwd2_kernel).
-template <int HB, int R, typename T>
+template <int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (15 - VB))
 outer_fwd2_kernel2(const T *__restrict__ x, const T *__restrict__ dy, float *__restrict__ wsx,
                    float *__restrict__ wsd, uint32_t nvalid)
@@ -523,15 +763,14 @@ outer_fwd2_kernel2(const T *__restrict__ x, const T *__restrict__ dy, float *__r
     const uint32_t half = gridDim.x >> 1;
     const bool second = blockIdx.x >= half;
     const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
-    outer_fwd_tile2<HB, R, T>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
+    outer_fwd_tile2<HB, R, T, VWID>(lds, second ? dy : x, second ? wsd : wsx, nvalid, blk);
 }
 
-template <int HB, int R, typename T>
+template <int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (15 - VB))
 outer_inv_kernel2(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
 {
     constexpr int A = 16, M = 15;
-    using G = Groups<M, 0>;
     using Run = RunMap<HB, R>;
     __shared__ float lds[pad(1u << M)];
     const uint32_t tau = threadIdx.x;
@@ -543,32 +782,74 @@ outer_inv_kernel2(const float *__restrict__ ws, T *__restrict__ y, uint32_t nval
         return;   // wholly padding: nothing to store (uniform per workgroup)
     const __amdgpu_buffer_rsrc_t r =
         buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
-    float v0[V], v1[V];
-    load_layout<G::SL, Run, float>(v0, r, tau);
-    load_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
-    inverse_groups<M, 0, G::NBOT - 1>(lds, v0, tau);
-    inverse_groups<M, 0, G::NBOT - 1>(lds, v1, tau);
-    butterflies<0, VB>(v0);
-    butterflies<0, VB>(v1);
-    cross_butterflies(v0, v1);
     T *base = y + b * nvalid + ((size_t)hi << A);
-    store_tile<G::TOP, M, T>(v0, base, min(valid, 1u << M), tau);
-    if (valid > (1u << M))
-        store_tile<G::TOP, M, T>(v1, base + (1u << M), valid - (1u << M), tau);
+    float v0[V], v1[V];
+    if constexpr (VWID > 0) {
+        using VG = VGroups<M, VWID>;
+        load_layout<VG::SL, Run, float>(v0, r, tau);
+        load_layout<VG::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+        vinverse_groups<M, VWID, VG::NBOT - 1>(lds, v0, tau);
+        vinverse_groups<M, VWID, VG::NBOT - 1>(lds, v1, tau);
+        butterflies<0, VB>(v0);
+        butterflies<0, VB>(v1);
+        cross_butterflies(v0, v1);
+        store_tile_vec<M, VWID, T>(v0, base, min(valid, 1u << M), tau);
+        if (valid > (1u << M))
+            store_tile_vec<M, VWID, T>(v1, base + (1u << M), valid - (1u << M), tau);
+    } else {
+        using G = Groups<M, 0>;
+        load_layout<G::SL, Run, float>(v0, r, tau);
+        load_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+        inverse_groups<M, 0, G::NBOT - 1>(lds, v0, tau);
+        inverse_groups<M, 0, G::NBOT - 1>(lds, v1, tau);
+        butterflies<0, VB>(v0);
+        butterflies<0, VB>(v1);
+        cross_butterflies(v0, v1);
+        store_tile<G::TOP, M, T>(v0, base, min(valid, 1u << M), tau);
+        if (valid > (1u << M))
+            store_tile<G::TOP, M, T>(v1, base + (1u << M), valid - (1u << M), tau);
+    }
 }
 
-// Launch helpers for the mixer's outer passes (2^11..2^16 tiles).
+// Launch helpers for the mixer's outer passes (2^11..2^16 tiles).  x and y
+// move with 16-byte accesses when the tile allows (vec_width) and every
+// slice starts 16-byte aligned (x and y themselves are 16-byte aligned).
+template <int A, typename T>
+constexpr int outer_vec_width()
+{
+    return vec_width(A < 15 ? A : 15, (int)sizeof(T));
+}
+
+template <int A, typename T>
+inline bool use_vec(uint32_t nvalid)
+{
+    return outer_vec_width<A, T>() > 0 && ((uint64_t)nvalid * sizeof(T)) % 16u == 0;
+}
+
 template <int K, typename T>
 hipError_t launch_outer_fwd(const T *x, float *ws, int64_t B, uint32_t nvalid, hipStream_t st)
 {
     constexpr Split sp = three_pass_split(K);
+    constexpr int VW = outer_vec_width<sp.A, T>();
     const dim3 grid((uint32_t)(B << sp.HB));
-    if constexpr (sp.A == 16)
-        hipLaunchKernelGGL((outer_fwd_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
-                           st, x, ws, nvalid);
-    else
-        hipLaunchKernelGGL((outer_fwd_kernel<sp.A, sp.HB, sp.R, T>), grid,
-                           dim3(1u << (sp.A - VB)), 0, st, x, ws, nvalid);
+    const bool vec = use_vec<sp.A, T>(nvalid);
+    if constexpr (sp.A == 16) {
+        const dim3 block(1u << (15 - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_fwd_kernel2<sp.HB, sp.R, T, VW>), grid, block, 0, st, x, ws,
+                               nvalid);
+        else
+            hipLaunchKernelGGL((outer_fwd_kernel2<sp.HB, sp.R, T, 0>), grid, block, 0, st, x, ws,
+                               nvalid);
+    } else {
+        const dim3 block(1u << (sp.A - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_fwd_kernel<sp.A, sp.HB, sp.R, T, VW>), grid, block, 0, st, x,
+                               ws, nvalid);
+        else
+            hipLaunchKernelGGL((outer_fwd_kernel<sp.A, sp.HB, sp.R, T, 0>), grid, block, 0, st, x,
+                               ws, nvalid);
+    }
     return hipGetLastError();
 }
 
@@ -577,13 +858,26 @@ hipError_t launch_outer_fwd2(const T *x, const T *dy, float *wsx, float *wsd, in
                              uint32_t nvalid, hipStream_t st)
 {
     constexpr Split sp = three_pass_split(K);
+    constexpr int VW = outer_vec_width<sp.A, T>();
     const dim3 grid((uint32_t)(2 * (B << sp.HB)));
-    if constexpr (sp.A == 16)
-        hipLaunchKernelGGL((outer_fwd2_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
-                           st, x, dy, wsx, wsd, nvalid);
-    else
-        hipLaunchKernelGGL((outer_fwd2_kernel<sp.A, sp.HB, sp.R, T>), grid,
-                           dim3(1u << (sp.A - VB)), 0, st, x, dy, wsx, wsd, nvalid);
+    const bool vec = use_vec<sp.A, T>(nvalid);
+    if constexpr (sp.A == 16) {
+        const dim3 block(1u << (15 - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_fwd2_kernel2<sp.HB, sp.R, T, VW>), grid, block, 0, st, x, dy,
+                               wsx, wsd, nvalid);
+        else
+            hipLaunchKernelGGL((outer_fwd2_kernel2<sp.HB, sp.R, T, 0>), grid, block, 0, st, x, dy,
+                               wsx, wsd, nvalid);
+    } else {
+        const dim3 block(1u << (sp.A - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_fwd2_kernel<sp.A, sp.HB, sp.R, T, VW>), grid, block, 0, st,
+                               x, dy, wsx, wsd, nvalid);
+        else
+            hipLaunchKernelGGL((outer_fwd2_kernel<sp.A, sp.HB, sp.R, T, 0>), grid, block, 0, st, x,
+                               dy, wsx, wsd, nvalid);
+    }
     return hipGetLastError();
 }
 
@@ -591,13 +885,26 @@ template <int K, typename T>
 hipError_t launch_outer_inv(const float *ws, T *y, int64_t B, uint32_t nvalid, hipStream_t st)
 {
     constexpr Split sp = three_pass_split(K);
+    constexpr int VW = outer_vec_width<sp.A, T>();
     const dim3 grid((uint32_t)(B << sp.HB));
-    if constexpr (sp.A == 16)
-        hipLaunchKernelGGL((outer_inv_kernel2<sp.HB, sp.R, T>), grid, dim3(1u << (15 - VB)), 0,
-                           st, ws, y, nvalid);
-    else
-        hipLaunchKernelGGL((outer_inv_kernel<sp.A, sp.HB, sp.R, T>), grid,
-                           dim3(1u << (sp.A - VB)), 0, st, ws, y, nvalid);
+    const bool vec = use_vec<sp.A, T>(nvalid);
+    if constexpr (sp.A == 16) {
+        const dim3 block(1u << (15 - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_inv_kernel2<sp.HB, sp.R, T, VW>), grid, block, 0, st, ws, y,
+                               nvalid);
+        else
+            hipLaunchKernelGGL((outer_inv_kernel2<sp.HB, sp.R, T, 0>), grid, block, 0, st, ws, y,
+                               nvalid);
+    } else {
+        const dim3 block(1u << (sp.A - VB));
+        if (vec)
+            hipLaunchKernelGGL((outer_inv_kernel<sp.A, sp.HB, sp.R, T, VW>), grid, block, 0, st, ws,
+                               y, nvalid);
+        else
+            hipLaunchKernelGGL((outer_inv_kernel<sp.A, sp.HB, sp.R, T, 0>), grid, block, 0, st, ws,
+                               y, nvalid);
+    }
     return hipGetLastError();
 }
 

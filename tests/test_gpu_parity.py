@@ -76,9 +76,12 @@ def test_shapes(shape, dtype, dev, orc):
 # including the paper's stereo joint token counts 9216, 25600 and 50176
 # (384x768, 640x1280 and 896x1792 images).
 # 139872 x 256 pads to a 2^26 slice: 2^16-element outer tiles, the
-# straddling one with its second 2^15 register set wholly padding.
+# straddling one with its second 2^15 register set wholly padding.  bf16
+# slices whose byte size is a multiple of 16 move with 16-byte accesses (the
+# straddling tile element by element); 262143 x 4 in bf16 (2 097 144 bytes)
+# is not, and takes per-element accesses throughout.
 PADDED = [(1, 3, 4), (2, 5, 8), (1, 100, 8), (3, 1000, 16), (2, 130, 128), (2, 9216, 64),
-          (1, 25600, 64), (1, 50176, 64), (2, 36864, 64), (1, 139872, 256)]
+          (1, 25600, 64), (1, 50176, 64), (2, 36864, 64), (1, 139872, 256), (2, 262143, 4)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -30,8 +30,13 @@ def layout_base(S, tau):
 
 
 def layout_index(S, tau):
-    """[P, 32] tile indices of every thread's registers in layout S."""
+    """[P, 32] tile indices of every thread's registers in layout S (a window
+    start), or in the vector-first layout ("v", VW, M): register k holds
+    t = (k mod 2^VW) | (tau << VW) | ((k >> VW) << (M - 5 + VW))."""
     k = np.arange(V)[None, :]
+    if isinstance(S, tuple):
+        _, vw, M = S
+        return (k & ((1 << vw) - 1)) | (tau[:, None] << vw) | ((k >> vw) << (M - VB + vw))
     return layout_base(S, tau)[:, None] | (k << S)
 
 
@@ -48,6 +53,28 @@ class Groups:
 
     def NB(self, i):
         return min(VB, self.TOP - self.S(i))
+
+
+class VGroups:
+    """Bit groups of an outer tile whose first layout is vector-first
+    (csrc/whtmix_tile.h VGroups): the first group is t bits [0, VW) and
+    [M - 5 + VW, M) straight from 16-byte loads; the windows then cover
+    [VW, M - 5 + VW) from the bottom."""
+
+    def __init__(self, M, vw):
+        self.M, self.WT, self.vw = M, vw, vw
+        self.TOP = ("v", vw, M)
+        self.JT = 0
+        self.top_hi = M - VB + vw
+        self.NBOT = (M - VB + VB - 1) // VB
+        self.SL = vw + VB * (self.NBOT - 1)
+        assert self.SL + VB <= M, "last window past the tile"
+
+    def S(self, i):
+        return self.vw + VB * i
+
+    def NB(self, i):
+        return min(VB, self.top_hi - self.S(i))
 
 
 def clampi(v, lo, hi):
@@ -84,8 +111,8 @@ def butterflies(v, j0, j1):
 class Tile:
     """One workgroup: P threads x 32 registers, plus an LDS array."""
 
-    def __init__(self, M, WT):
-        self.g = Groups(M, WT)
+    def __init__(self, M, WT, vw=0):
+        self.g = VGroups(M, vw) if vw else Groups(M, WT)
         self.P = 1 << (M - VB)
         self.tau = np.arange(self.P)
         self.lds = np.full(pad(1 << M), np.nan)
@@ -154,24 +181,37 @@ def tile_valid(nvalid, hi, A):
     return 0 if nvalid <= start else min(nvalid - start, 1 << A)
 
 
-def outer_sets(A):
+def outer_sets(A, vw=0):
     """Register sets of an outer tile: (tile, offset of the set's t) -- one
-    2^A tile, or for A = 16 two 2^15 sub-tiles at t and t + 2^15."""
+    2^A tile, or for A = 16 two 2^15 sub-tiles at t and t + 2^15.  vw: the
+    vector-first layout for 2^vw-element global accesses (0: the top window)."""
     if A <= 15:
-        return [(Tile(A, 0), 0)]
-    return [(Tile(15, 0), 0), (Tile(15, 0), 1 << 15)]
+        return [(Tile(A, 0, vw), 0)]
+    return [(Tile(15, 0, vw), 0), (Tile(15, 0, vw), 1 << 15)]
+
+
+def outer_vw(A, elt_bytes, nvalid, widths={2: 3, 4: 0}):
+    """csrc/whtmix_tile.h vec_width / use_vec: the vector width of an outer
+    pass (log2 of the elements per 16-byte access), or 0 for per-element
+    accesses.  The kernels use it for bf16 only; `widths` lets the model
+    exercise the layout's float32 form (VW = 2) too."""
+    vw = widths[elt_bytes]
+    M = min(A, 15)
+    if vw == 0 or (nvalid * elt_bytes) % 16 != 0 or vw + VB * ((M - VB + VB - 1) // VB) > M:
+        return 0
+    return vw
 
 
 def cross(v0, v1):
     return v0 + v1, v0 - v1
 
 
-def model_outer_fwd_block(src, nvalid, b, hi, split, acc=None):
+def model_outer_fwd_block(src, nvalid, b, hi, split, acc=None, vw=0):
     """One outer_fwd block (outer_fwd_tile / outer_fwd_tile2): returns the
     workspace offsets (relative to the slice) and values of its tile."""
     A, HB, R = split
     valid = tile_valid(nvalid, hi, A)
-    sets = outer_sets(A)
+    sets = outer_sets(A, vw)
     vals = []
     for T, t0 in sets:
         t = T.idx(T.g.TOP) + t0
@@ -191,11 +231,11 @@ def model_outer_fwd_block(src, nvalid, b, hi, split, acc=None):
     return offs, out
 
 
-def model_outer_inv_block(ws_slice, nvalid, b, hi, split, acc=None, base=0):
+def model_outer_inv_block(ws_slice, nvalid, b, hi, split, acc=None, base=0, vw=0):
     """One outer_inv block: returns (y offsets, values) of its valid elements."""
     A, HB, R = split
     valid = tile_valid(nvalid, hi, A)
-    sets = outer_sets(A)
+    sets = outer_sets(A, vw)
     vals = []
     for T, t0 in sets:
         o = base + (hi << R) + run_map(T.idx(T.g.SL) + t0, HB, R)
@@ -214,9 +254,10 @@ def model_outer_inv_block(ws_slice, nvalid, b, hi, split, acc=None, base=0):
     return offs, out
 
 
-def simulate_three_pass(x, g, K, split):
+def simulate_three_pass(x, g, K, split, vw=0):
     """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel.  x holds
-    N <= 2^K / C real tokens per slice (zero padding of the token axis)."""
+    N <= 2^K / C real tokens per slice (zero padding of the token axis).
+    vw: the outer passes' vector-first layout (0: per-element accesses)."""
     B = x.shape[0]
     L = 1 << K
     nvalid = x.shape[1] * x.shape[2]
@@ -231,7 +272,7 @@ def simulate_three_pass(x, g, K, split):
     # outer forward: block = b * 2^HB + hi
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split, acc_x)
+        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split, acc_x, vw)
         for o, v in zip(offs, vals):
             ws[acc["ws_w1"].at(b * L + o)] = v
     # middle: logical tile = run * B + b, XCD renumbering of blocks
@@ -256,7 +297,7 @@ def simulate_three_pass(x, g, K, split):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
         if tile_valid(nvalid, hi, A) == 0:
             continue
-        offs, vals = model_outer_inv_block(ws, nvalid, b, hi, split, acc_r3, base=b * L)
+        offs, vals = model_outer_inv_block(ws, nvalid, b, hi, split, acc_r3, base=b * L, vw=vw)
         for o, v in zip(offs, vals):
             y[acc_y.at(o)] = v
     for k, a in acc.items():
@@ -371,9 +412,10 @@ def test_three_pass_maps_in_bounds(K):
     assert pad((1 << 15) - 1) < 160 * 1024 // 4   # LDS fits in 160 KiB
 
 
+@pytest.mark.parametrize("vw", [0, 2, 3])
 @pytest.mark.parametrize("K,split", [(18, (16, 2, 9)), (20, (16, 4, 7)), (17, (16, 1, 10))])
 @pytest.mark.parametrize("N_frac", [1.0, 0.93, 0.8, 0.55])
-def test_pair_outer_tiles(K, split, N_frac, orc):
+def test_pair_outer_tiles(K, split, N_frac, vw, orc):
     """2^16 outer tiles (two 2^15 register sets and a butterfly between them),
     executed on small slices by forcing A = 16.  With padding (N > P/2, so the
     padded size stays P) the straddling tile's second set is partly valid or
@@ -384,14 +426,90 @@ def test_pair_outer_tiles(K, split, N_frac, orc):
     N = max(1, int(P * N_frac))
     x = rng.standard_normal((2, N, C))
     g = rng.uniform(0.5, 1.5, (P, C))
-    y = simulate_three_pass(x, g, K, split)
+    y = simulate_three_pass(x, g, K, split, vw)
     ref = orc.whtmix(x, g)
     assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
     dy = rng.standard_normal((2, N, C))
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
-    dg, dx = simulate_grad_three_pass(x, dy, g, K, split)
+    dg, dx = simulate_grad_three_pass(x, dy, g, K, split, vw)
     assert np.max(np.abs(dg - dg_ref.reshape(-1))) < 1e-11 * np.max(np.abs(dg_ref))
     assert np.max(np.abs(dx - dx_ref)) < 1e-11 * np.max(np.abs(dx_ref))
+
+
+def bank_conflicts(addr, banks):
+    """Worst number of lanes of one wave (64 lanes; with 32 banks served in
+    two halves of 32) that hit the same bank in one LDS access."""
+    worst = 1
+    for w0 in range(0, addr.shape[0], 64):
+        for k in range(addr.shape[1]):
+            a = addr[w0:w0 + 64, k]
+            halves = [a[:32], a[32:]] if banks == 32 else [a]
+            for h in halves:
+                _, cnt = np.unique(h % banks, return_counts=True)
+                worst = max(worst, int(cnt.max()))
+    return worst
+
+
+@pytest.mark.parametrize("M,vw", [(12, 2), (13, 2), (14, 2), (15, 2), (13, 3), (14, 3), (15, 3)])
+def test_vector_first_layouts(M, vw):
+    """The vector-first layout: each thread's 2^vw registers of one access
+    are consecutive elements (one 16-byte load or store); the layouts of the
+    outer pass cover the tile once each; every LDS write and read of their
+    exchanges is free of bank conflicts (32 banks, a wave served by halves:
+    the model the existing window layouts are built for)."""
+    T = Tile(M, 0, vw)
+    g = T.g
+    first = T.idx(g.TOP)
+    assert sorted(first.reshape(-1)) == list(range(1 << M))
+    step = 1 << vw
+    for j in range(V // step):
+        blk = first[:, j * step:(j + 1) * step]
+        assert np.all(blk == blk[:, :1] + np.arange(step)), "a 16-byte access is contiguous"
+        assert np.all(blk[:, 0] % step == 0)
+    layouts = [g.TOP] + [g.S(i) for i in range(g.NBOT)]
+    for L in layouts:
+        idx = T.idx(L)
+        assert sorted(idx.reshape(-1)) == list(range(1 << M))
+        assert bank_conflicts(pad(idx), 32) == 1, L
+    bits = list(range(vw)) + list(range(g.top_hi, M))
+    for i in range(g.NBOT):
+        bits += list(range(g.S(i), g.S(i) + g.NB(i)))
+    assert sorted(bits) == list(range(M)), "every tile bit transformed once"
+    assert g.SL == layouts[-1] and g.SL >= 6   # 64 lanes on 64 consecutive elements
+
+
+@pytest.mark.parametrize("K,vw", [(18, 2), (19, 2), (20, 3), (21, 3)])
+def test_vector_first_schedules(K, vw, orc):
+    """Executed forward and backward schedules with vector-first outer
+    passes reproduce the oracle (power-of-two and padded token counts)."""
+    split = three_pass_split(K)
+    rng = np.random.default_rng(K * 10 + vw)
+    C = 64
+    P = 1 << (K - 6)
+    if outer_vw(split[0], 2 if vw == 3 else 4, P * C, {2: 3, 4: 2}) != vw:
+        pytest.skip("outer tile too small for this width")
+    for N in (P, P - P // 8 + 3):
+        x = rng.standard_normal((2, N, C))
+        g = rng.uniform(0.5, 1.5, (P, C))
+        ref = orc.whtmix(x, g)
+        y = simulate_three_pass(x, g, K, split, vw)
+        assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
+        dy = rng.standard_normal((2, N, C))
+        dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
+        dg, dx = simulate_grad_three_pass(x, dy, g, K, split, vw)
+        assert np.max(np.abs(dg - dg_ref.reshape(-1))) < 1e-11 * np.max(np.abs(dg_ref))
+        assert np.max(np.abs(dx - dx_ref)) < 1e-11 * np.max(np.abs(dx_ref))
+
+
+def test_vector_width_rule():
+    """Vector accesses need 16-byte aligned slices and a tile whose last
+    window fits (bf16 from 2^13 elements; the float32 form from 2^12)."""
+    assert outer_vw(12, 2, 4096) == 0 and outer_vw(13, 2, 8192) == 3
+    assert outer_vw(14, 2, 1000 * 16) == 3 and outer_vw(14, 2, 1001 * 4) == 0
+    assert outer_vw(16, 2, 1 << 26) == 3 and outer_vw(14, 4, 1 << 14) == 0
+    f32 = {2: 3, 4: 2}
+    assert outer_vw(11, 4, 4096, f32) == 0 and outer_vw(12, 4, 4096, f32) == 2
+    assert outer_vw(14, 4, 4 * 1001, f32) == 2 and outer_vw(14, 4, 1001, f32) == 0
 
 
 @pytest.mark.parametrize("N,C", [(1000, 2), (33, 64), (100, 64), (130, 128), (257, 64)])
@@ -412,7 +530,7 @@ def test_padded_schedules(N, C, orc):
         assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
 
 
-def model_outer_fwd(x, K, split):
+def model_outer_fwd(x, K, split, vw=0):
     """outer_fwd_kernel over a batch: the low-bit transforms in the run layout."""
     B = x.shape[0]
     L = 1 << K
@@ -422,7 +540,7 @@ def model_outer_fwd(x, K, split):
     ws = np.full(B * L, np.nan)
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
-        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split)
+        offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split, vw=vw)
         for o, v in zip(offs, vals):
             ws[b * L + o] = v
     assert not np.isnan(ws).any()
@@ -443,7 +561,7 @@ def grad_chunking(B, K, split):
     return chunking(B, B if HB + R == 15 else -(-512 // runs))
 
 
-def simulate_grad_three_pass(x, dy, g, K, split):
+def simulate_grad_three_pass(x, dy, g, K, split, vw=0):
     """Model of the fused three-pass gradients: outer_fwd2 of x and dy, then
     grad_mix_middle_kernel over (chunk, run) blocks (product sum, then dY's
     gain and inverse in place), the chunk sum, and outer_inv of dY's
@@ -453,7 +571,7 @@ def simulate_grad_three_pass(x, dy, g, K, split):
     nvalid = x.shape[1] * x.shape[2]
     A, HB, R = split
     M = HB + R
-    wsx, wsd = model_outer_fwd(x, K, split), model_outer_fwd(dy, K, split)
+    wsx, wsd = model_outer_fwd(x, K, split, vw), model_outer_fwd(dy, K, split, vw)
     gf = g.reshape(L)
     runs = 1 << (A - R)
     nch, per = grad_chunking(B, K, split)
@@ -489,7 +607,7 @@ def simulate_grad_three_pass(x, dy, g, K, split):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
         if tile_valid(nvalid, hi, A) == 0:
             continue
-        offs, vals = model_outer_inv_block(wsd, nvalid, b, hi, split, base=b * L)
+        offs, vals = model_outer_inv_block(wsd, nvalid, b, hi, split, base=b * L, vw=vw)
         for o, v in zip(offs, vals):
             dx[acc_y.at(o)] = v
     assert np.all(acc_y.count == 1)
