@@ -411,6 +411,12 @@ def main() -> int:
                    "input_sets": nsets},
         "tokens_per_s": round(tokens, 1),
         "hbm_peak_frac": round(gbs / PEAK_HBM_GBS, 4),
+        # the whole step on the bytes its kernels must move by their design
+        # (x, y, the gain and both float32 workspace round trips): the other
+        # reading of the fraction of HBM peak
+        "path": None if not all(alg) else {
+            "bytes": int(sum(alg)), "GB_s": round(sum(alg) / (ms_per_step * 1e-3) / 1e9, 1),
+            "frac": round(sum(alg) / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
         "event_sampled_steps": len(sampled),
         "kernels": [{"name": n, "avg_ms": round(t, 5), "alg_bytes": b,
                      "alg_GBs": round(b / (t * 1e-3) / 1e9, 1) if b else None}
