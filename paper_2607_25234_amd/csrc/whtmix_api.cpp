@@ -3,6 +3,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -119,6 +120,13 @@ int hip_fail(hipError_t e, const char *what)
 // Caller holds g_ws_mutex.
 int get_workspace(void *stream, int64_t bytes, float **out)
 {
+    // Test hook: with WHTMIX_TEST_FAIL_WORKSPACE set in the environment every
+    // workspace request fails as an allocation failure would, before any HIP
+    // call, so the status path can be tested without exhausting the device.
+    if (std::getenv("WHTMIX_TEST_FAIL_WORKSPACE")) {
+        g_last_error = "workspace allocation refused (WHTMIX_TEST_FAIL_WORKSPACE)";
+        return WHTMIX_ERROR_OUT_OF_MEMORY;
+    }
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");

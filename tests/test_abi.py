@@ -263,6 +263,26 @@ def test_every_three_pass_split_fits_the_tiles():
         assert 1 <= K - A and 11 <= K - A + R <= 15 and 0 <= R <= A, K
 
 
+def test_workspace_failure_is_reported_before_any_launch(monkeypatch):
+    """A workspace that cannot be allocated returns OUT_OF_MEMORY with its text
+    and enqueues nothing (the library's test hook refuses every workspace
+    request before any HIP call, so this runs without a GPU)."""
+    torch = pytest.importorskip("torch")
+    if torch.cuda.device_count() > 0:
+        pytest.skip("fake device addresses are for hosts without a GPU")
+    monkeypatch.setenv("WHTMIX_TEST_FAIL_WORKSPACE", "1")
+    lib = whtmix.lib()
+    # three-pass shapes need a workspace: forward, backward, the block
+    assert whtmix.forward_raw(ALIGNED, ALIGNED2, ALIGNED, 2, 4096, 64, 0, 0) == 5
+    assert "WHTMIX_TEST_FAIL_WORKSPACE" in whtmix.last_error()
+    assert whtmix.backward_raw(ALIGNED, ALIGNED + (1 << 22), ALIGNED2, ALIGNED + (2 << 22),
+                               ALIGNED2 + (1 << 22), 2, 4096, 64, 0, 0) == 5
+    assert lib.whtmix_status_string(5).decode()
+    # a shape with no workspace (the fused plan) never reaches the allocator,
+    # so it would launch: it is not called here without a GPU
+    assert whtmix.plan_describe(2, 256, 64)["workspace_bytes"] == 0
+
+
 def test_python_forward_rejects_host_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(1, 64, 64)
