@@ -77,12 +77,13 @@ OPS = ("forward", "separable", "backward", "backward_separable", "module", "modu
        "module_backward")
 
 
-def module_kernels(plan: str, C: int) -> list[str]:
+def module_kernels(plan: str, path: str) -> list[str]:
     """Kernels between the events of a whtmix_module_forward call (the weight
-    repacking kernel runs before the first event)."""
-    if plan == "small":
+    repacking kernel runs before the first event); path: the library's
+    module_path for the shape ("small", "mfma" or "unfused")."""
+    if plan == "small" or path == "small":
         return ["module_small"]
-    if not 16 <= C <= 128:
+    if path != "mfma":
         return ["unfused"]
     return ["module_outer_fwd", "middle", "module_outer_inv"] if plan == "three_pass" \
         else ["module_fused"]
@@ -294,7 +295,7 @@ def main() -> int:
     elif op == "module_backward":
         nk, names = 3, ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"]
     elif op.startswith("module"):
-        names = module_kernels(plan["plan"], w.C)
+        names = module_kernels(plan["plan"], plan["module_path"])
         nk = len(names)
     else:
         nk, names = plan["kernels"], kernel_names(plan["plan"])

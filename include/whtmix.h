@@ -109,6 +109,12 @@ typedef struct whtmix_plan_info {
                              by the middle pass */
     int64_t workspace_bytes; /* float32 workspace this call needs */
     int64_t padded_tokens;   /* N_pad */
+    /* How whtmix_module_forward runs this shape: 0 SMALL (projections on the
+     * vector ALUs), 1 projections fused into the mixer's kernels on the
+     * matrix cores, 2 projection kernels around the float32 mixer; -1 when C
+     * exceeds the block's limit. */
+    int module_path;
+    int module_outer_bits;   /* THREE_PASS: the block's outer-pass bits */
 } whtmix_plan_info;
 
 /*

@@ -175,6 +175,14 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->run_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.R : 0;
     info->workspace_bytes = c.ws_bytes;
     info->padded_tokens = c.n_pad;
+    const int cbits = log2_exact(C);
+    info->module_path = cbits <= whtmix::kModuleMaxCbits
+                            ? whtmix::module_path(c.plan, cbits, dtype, c.K)
+                            : -1;
+    info->module_outer_bits =
+        info->module_path >= 0 && c.plan == whtmix::PLAN_THREE_PASS
+            ? whtmix::module_outer_bits(info->module_path, cbits, c.K)
+            : 0;
     return WHTMIX_SUCCESS;
 }
 
@@ -393,7 +401,7 @@ int module_impl(const void *x, const void *w_in, int gain_kind, const float *gai
     m.stream = static_cast<hipStream_t>(stream);
     for (int i = 0; i < 4; ++i)
         m.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
-    const int path = whtmix::module_path(c.plan, cbits);
+    const int path = whtmix::module_path(c.plan, cbits, dtype, c.K);
     // workspace: mixer (THREE_PASS), then packed weights or Z, 256-byte aligned
     const int64_t mix = path == whtmix::MODULE_SMALL ? 0 : c.ws_bytes;
     // FUSED_MFMA: the packed weights; UNFUSED: Z, then the packed weights

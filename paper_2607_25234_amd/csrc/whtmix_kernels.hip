@@ -201,14 +201,27 @@ hipError_t dispatch(const LaunchArgs &a, Gain gain)
     }
 }
 
+template <int A, int HB, int R, class Gain>
+hipError_t launch_middle_split(const LaunchArgs &a, Gain gain)
+{
+    static_assert(HB >= 1 && HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
+    hipLaunchKernelGGL((middle_kernel<A, HB, R, Gain>), dim3((uint32_t)(a.B << (A - R))),
+                       dim3(1u << (HB + R - VB)), 0, a.stream, a.ws, gain, (uint32_t)a.B);
+    return hipGetLastError();
+}
+
 template <int K, class Gain>
 hipError_t launch_middle_k(const LaunchArgs &a, Gain gain)
 {
+    if constexpr (K >= kPairModuleMinK) {
+        constexpr Split sp = pair_split(K);
+        if (a.pair_outer)
+            return launch_middle_split<sp.A, sp.HB, sp.R, Gain>(a, gain);
+    }
+    if (a.pair_outer)
+        return hipErrorInvalidValue;
     constexpr Split sp = module_split(K);
-    hipLaunchKernelGGL((middle_kernel<sp.A, sp.HB, sp.R, Gain>),
-                       dim3((uint32_t)(a.B << (sp.A - sp.R))), dim3(1u << (sp.HB + sp.R - VB)), 0,
-                       a.stream, a.ws, gain, (uint32_t)a.B);
-    return hipGetLastError();
+    return launch_middle_split<sp.A, sp.HB, sp.R, Gain>(a, gain);
 }
 
 template <class Gain>

@@ -30,6 +30,7 @@ struct LaunchArgs {
     int plan;       // PlanKind, resolved (never AUTO)
     hipStream_t stream;
     hipEvent_t events[4];   // optional, may be null
+    bool pair_outer;        // launch_middle only: the outer passes used 2^16 tiles
 };
 
 // Enqueues the plan's kernels on a.stream.  Returns the first HIP error.
@@ -75,9 +76,9 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
 
 hipError_t launch_backward(const BackwardArgs &a);
 
-// Enqueues only the middle pass of the block's three-pass plan (module_split;
-// a.ws holds the first outer pass's output); a.x, a.y, a.nvalid and a.dtype
-// are not used.
+// Enqueues only the middle pass of the block's three-pass plan (module_split,
+// or pair_split when a.pair_outer; a.ws holds the first outer pass's output);
+// a.x, a.y, a.nvalid and a.dtype are not used.
 hipError_t launch_middle(const LaunchArgs &a);
 
 

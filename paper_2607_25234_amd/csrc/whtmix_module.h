@@ -13,19 +13,32 @@ namespace whtmix {
 // ---------------------------------------------------------------- the block
 // How the block with its projections runs (whtmix_module.hip):
 //   SMALL       the mixer's SMALL plan, projections on the VALU in LDS;
-//   FUSED_MFMA  16 <= C <= 128 with the FUSED or THREE_PASS plan: MFMA
-//               prologue and epilogue inside the mixer's kernels;
+//   FUSED_MFMA  16 <= C <= 128 with the FUSED or THREE_PASS plan, and bf16
+//               C = 256 with the THREE_PASS plan from 2^17 elements per slice
+//               (2^16 outer tiles): MFMA prologue and epilogue inside the
+//               mixer's kernels;
 //   UNFUSED     any other C: projection kernels around the fp32 mixer.
 enum ModulePath { MODULE_SMALL = 0, MODULE_FUSED_MFMA = 1, MODULE_UNFUSED = 2 };
 constexpr int kModuleMfmaMinCbits = 4;
 constexpr int kModuleMfmaMaxCbits = 7;
 constexpr int kModuleMaxCbits = 12;   // weights of C*C elements, C <= 4096
 
-inline int module_path(int plan, int cbits)
+inline int module_path(int plan, int cbits, int dtype, int K)
 {
     if (plan == PLAN_SMALL) return MODULE_SMALL;
     if (cbits >= kModuleMfmaMinCbits && cbits <= kModuleMfmaMaxCbits) return MODULE_FUSED_MFMA;
+    if (cbits == kPairModuleCbits && dtype == DTYPE_BF16 && plan == PLAN_THREE_PASS &&
+        K >= kPairModuleMinK)
+        return MODULE_FUSED_MFMA;
     return MODULE_UNFUSED;
+}
+
+// Flat-index bits of the outer passes of the block's THREE_PASS plan.
+inline int module_outer_bits(int path, int cbits, int K)
+{
+    if (path == MODULE_FUSED_MFMA)
+        return cbits == kPairModuleCbits ? pair_split(K).A : module_split(K).A;
+    return three_pass_split(K).A;   // UNFUSED: the mixer's own plan
 }
 
 // A validated call of the block.  Workspace: the THREE_PASS workspace `ws`

@@ -76,6 +76,14 @@ struct Epi {
     }
 };
 
+// 2^15 tiles: registers hold t bits 0-3 and 9; threads hold bits 4-8
+// (lanes 0-4) and 10-14.  From layout 4, where bits 4-8 are done, one
+// exchange reaches every bit below 10.
+struct Low4Hi9 {
+    static constexpr int reg(int j) { return j < 4 ? j : 9; }
+    __device__ static uint32_t base(uint32_t tau) { return ((tau & 31u) << 4) | ((tau >> 5) << 10); }
+};
+
 template <class L>
 constexpr uint32_t reg_offset(uint32_t k)
 {
@@ -128,15 +136,16 @@ template <int M>
 __device__ __forceinline__ void forward_from_prologue(float *lds, float (&v)[V], uint32_t tau)
 {
     butterflies_on<31>(v);
-    relayout<Std<4>, Std<0>, true>(lds, v, tau);   // LEAD: the weights were read from LDS
-    butterflies_on<15>(v);                          // bits 0-3
+    // LEAD: the weights (or the previous register set) were read from LDS
     if constexpr (M <= 14) {
+        relayout<Std<4>, Std<0>, true>(lds, v, tau);
+        butterflies_on<15>(v);                      // bits 0-3
         relayout<Std<0>, Std<M - 5>>(lds, v, tau);
         butterflies_on<31u & ~((1u << (14 - M)) - 1u)>(v);   // bits 9 .. M-1
     } else {
-        relayout<Std<0>, Std<5>>(lds, v, tau);
-        butterflies_on<16>(v);                      // bit 9
-        relayout<Std<5>, Std<10>>(lds, v, tau);
+        relayout<Std<4>, Low4Hi9, true>(lds, v, tau);
+        butterflies_on<31>(v);                      // bits 0-3 and 9
+        relayout<Low4Hi9, Std<10>>(lds, v, tau);
         butterflies_on<31>(v);                      // bits 10-14
     }
 }
@@ -619,6 +628,203 @@ module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_ou
     project_out<T, CB, A>(v, wl, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
+// ---------------------------------------------------------------- C = 256 (bf16)
+// Outer tiles of 2^16 elements = 256 tokens x 256 channels (t = token * 256 +
+// channel), 1024 threads of two 2^15 register sets (pair_split).  Wave w owns
+// 16 tokens, one 16-row MFMA block, against all 256 channels: 16 column
+// blocks x 4 results = 64 values per lane, exactly the two sets.
+//
+// Forward: MFMA row m = 4q + r of wave w is token
+//     (r & 1) | q << 1 | w << 3 | (r >> 1) << 7,
+// so set s = t bit 15 (token bit 7) and within a set register nb | (r & 1) << 4
+// holds t bits 4-8 (channel block nb, token bit 0) while lanes 0-3 (column j)
+// hold channel bits 0-3, lanes 4-5 (q) t bits 9-10 and waves t bits 11-14:
+// layout 4 of the set's 2^15 elements, as for C <= 128.  Bit 15 is a register
+// butterfly between the sets.
+//
+// Inverse: set s = t bit 5 (channel bit 5).  Dropping that bit (t') leaves a
+// 2^15 set laid out like a C = 128 tile, so the C = 128 inverse schedule ends
+// in the epilogue layout Epi<15, 7>: lane (j, q) of wave w holds channels
+// 64 q + 32 s + [0, 32) of token j | w << 4, the B operand of
+// Y^T = W_out^T Z'^T for 16 k steps of 16 channels.
+constexpr int kPairCB = kPairModuleCbits;
+constexpr uint32_t kPairC = 1u << kPairCB;
+constexpr uint32_t kPairThreads = 1u << (15 - VB);
+constexpr uint32_t kPairKs = kPairC / 16u;                      // k steps
+constexpr uint32_t kPairWChunks = kPairC * kPairC * 2u / 16u;   // 16-byte pieces of W
+static_assert(kPairC * kPairC * 2u <= pad(1u << 15) * 4u, "W fits the tile's LDS");
+static_assert(kPairWChunks % kPairThreads == 0, "whole prefetch per thread");
+
+// Set-local index t' (t bit 5 dropped) -> workspace offset.
+template <class Map>
+struct DropBit5 {
+    __host__ __device__ static constexpr uint32_t at(uint32_t tp)
+    {
+        return Map::at((tp & 31u) | ((tp >> 5) << 6));
+    }
+};
+
+// X fragments of the wave's 16 tokens: k step kk holds channels
+// 32 (kk / 2) + 8 q + 4 (kk % 2) + [0, 4) (16-byte loads of 8 channels).
+__device__ __forceinline__ void load_x_pair(bf16x4 (&a)[kPairKs], const __bf16 *tile,
+                                            uint32_t valid, uint32_t tau)
+{
+    const uint32_t lane = tau & 63u, w = tau >> 6;
+    const uint32_t i = lane & 15u, q = lane >> 4;
+    const uint32_t tok = (i & 1u) | (((i >> 2) & 3u) << 1) | (w << 3) | (((i >> 1) & 1u) << 7);
+    const bool ok = tok * kPairC < valid;
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 2u);
+    const uint32_t voff = tok * kPairC * 2u + 16u * q;
+#pragma unroll
+    for (uint32_t p = 0; p < kPairKs / 2u; ++p) {
+        u32x4 d = {0u, 0u, 0u, 0u};
+        if (ok)
+            d = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 64u * p, kStreaming);
+        a[2 * p] = __builtin_bit_cast(bf16x4, (u32x2){d.x, d.y});
+        a[2 * p + 1] = __builtin_bit_cast(bf16x4, (u32x2){d.z, d.w});
+    }
+}
+
+// Z = X W_in into the two sets (packed W_in in LDS).
+__device__ __forceinline__ void project_in_pair(float (&v0)[V], float (&v1)[V],
+                                                const bf16x4 (&a)[kPairKs], const void *wl,
+                                                uint32_t tau)
+{
+    const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+    const uint32_t lane = tau & 63u;
+#pragma unroll
+    for (int nb = 0; nb < 16; ++nb) {
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (uint32_t kk = 0; kk < kPairKs; ++kk)
+            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a[kk], wb[(nb * kPairKs + kk) * 64u + lane],
+                                                             acc, 0, 0, 0);
+        v0[nb] = acc[0];
+        v0[nb | 16] = acc[1];
+        v1[nb] = acc[2];
+        v1[nb | 16] = acc[3];
+    }
+}
+
+// Y = Z' W_out for the wave's 16 tokens from the two sets' epilogue-layout
+// registers (packed W_out in LDS); rows past `valid` are not stored.
+__device__ __forceinline__ void project_out_pair(const float (&v0)[V], const float (&v1)[V],
+                                                 const void *wl, __bf16 *tile, uint32_t valid,
+                                                 uint32_t tau)
+{
+    const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+    const uint32_t lane = tau & 63u, w = tau >> 6;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const uint32_t tok = j | (w << 4);
+    const bool ok = tok * kPairC < valid;
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 2u);
+    const uint32_t voff = tok * kPairC * 2u + 16u * q;
+    // the two-term split Z' = hi + lo; step kk element e is channel
+    // 64 q + 4 kk + e: set kk / 8, register 4 (kk % 8) + e
+    bf16x4 hi[kPairKs], lo[kPairKs];
+#pragma unroll
+    for (uint32_t kk = 0; kk < kPairKs; ++kk) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float z = kk < 8 ? v0[4 * kk + e] : v1[4 * (kk - 8) + e];
+            const __bf16 h = (__bf16)z;
+            hi[kk][e] = __builtin_bit_cast(short, h);
+            lo[kk][e] = __builtin_bit_cast(short, (__bf16)(z - (float)h));
+        }
+    }
+    // blocks 2n, 2n+1: channels 32 n + 8 q + [0, 8), one 16-byte store
+#pragma unroll
+    for (uint32_t n = 0; n < 8; ++n) {
+        f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (uint32_t kk = 0; kk < kPairKs; ++kk) {
+            const bf16x4 a0 = wb[((2 * n) * kPairKs + kk) * 64u + lane];
+            const bf16x4 a1 = wb[((2 * n + 1) * kPairKs + kk) * 64u + lane];
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, hi[kk], acc0, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, lo[kk], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, hi[kk], acc1, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, lo[kk], acc1, 0, 0, 0);
+        }
+        const u32x4 d = {pack2_bf16(acc0[0], acc0[1]), pack2_bf16(acc0[2], acc0[3]),
+                         pack2_bf16(acc1[0], acc1[1]), pack2_bf16(acc1[2], acc1[3])};
+        if (ok)
+            __builtin_amdgcn_raw_buffer_store_b128(d, r, voff, 64u * n, kYPolicy);
+    }
+}
+
+// THREE_PASS first pass, C = 256: prologue, forward over the 16 low bits.
+template <int HB, int R>
+__global__ void __launch_bounds__(kPairThreads)
+module_outer_fwd_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restrict__ w_in,
+                             float *__restrict__ ws, uint32_t nvalid)
+{
+    constexpr int A = 16, M = 15;
+    using Run = RunMap<HB, R>;
+    __shared__ __attribute__((aligned(16))) float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    bf16x4 a[kPairKs];
+    load_x_pair(a, x + b * nvalid + ((size_t)hi << A), valid, tau);
+    stage_weights<kPairWChunks, kPairThreads>(lds, w_in, tau);
+    __syncthreads();
+    float v0[V], v1[V];
+    project_in_pair(v0, v1, a, lds, tau);
+    cross_butterflies(v0, v1);   // bit 15
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
+    forward_from_prologue<M>(lds, v0, tau);
+    store_layout<M - 5, Run, float>(v0, r, tau);
+    forward_from_prologue<M>(lds, v1, tau);
+    store_layout<M - 5, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+}
+
+// THREE_PASS last pass, C = 256: inverse over the 16 low bits, epilogue, y.
+template <int HB, int R>
+__global__ void __launch_bounds__(kPairThreads)
+module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restrict__ w_out,
+                             __bf16 *__restrict__ y, uint32_t nvalid)
+{
+    constexpr int A = 16, M = 15;
+    using Run = RunMap<HB, R>;
+    using SetMap = DropBit5<Run>;
+    // W_out: PRE of its PER 16-byte pieces per thread are prefetched into
+    // registers at the start (all of them would spill: the two sets hold 64)
+    constexpr uint32_t PER = kPairWChunks / kPairThreads, PRE = 4;
+    __shared__ __attribute__((aligned(16))) float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
+    const size_t b = blk >> HB;
+    const uint32_t hi = blk & ((1u << HB) - 1u);
+    const uint32_t valid = tile_valid<A>(nvalid, hi);
+    if (valid == 0)
+        return;   // wholly padding: nothing to store (uniform per workgroup)
+    const u32x4 *wsrc = static_cast<const u32x4 *>(static_cast<const void *>(w_out));
+    u32x4 wreg[PER];
+#pragma unroll
+    for (uint32_t i = 0; i < PRE; ++i)
+        wreg[i] = wsrc[tau + i * kPairThreads];
+    const __amdgpu_buffer_rsrc_t r =
+        buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
+    float v0[V], v1[V];
+    load_layout<M - 5, SetMap, float>(v0, r, tau);
+    load_layout<M - 5, SetMap, float>(v1, r, tau, Run::at(1u << 5) * 4u);
+    inverse_to_epilogue<M, 7, false>(lds, v0, tau);
+    inverse_to_epilogue<M, 7, true>(lds, v1, tau);
+#pragma unroll
+    for (uint32_t i = PRE; i < PER; ++i)
+        wreg[i] = wsrc[tau + i * kPairThreads];
+    cross_butterflies(v0, v1);   // t bit 5
+    __syncthreads();             // every thread has read its epilogue-layout values
+#pragma unroll
+    for (uint32_t i = 0; i < PER; ++i)
+        reinterpret_cast<u32x4 *>(lds)[tau + i * kPairThreads] = wreg[i];
+    __syncthreads();
+    project_out_pair(v0, v1, lds, y + b * nvalid + ((size_t)hi << A), valid, tau);
+}
+
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
 
@@ -893,6 +1099,24 @@ hipError_t launch_module_fused(const ModuleArgs &m, Gain gain)
     return record(m.events[1], m.stream);
 }
 
+// Arguments of the mixer's middle pass inside the block's three-pass plan.
+LaunchArgs middle_args(const ModuleArgs &m, bool pair_outer)
+{
+    LaunchArgs a{};
+    a.gain_kind = m.gain_kind;
+    a.gain = m.gain;
+    a.gain_t = m.gain_t;
+    a.gain_c = m.gain_c;
+    a.cbits = m.cbits;
+    a.ws = m.ws;
+    a.B = m.B;
+    a.K = m.K;
+    a.plan = PLAN_THREE_PASS;
+    a.stream = m.stream;
+    a.pair_outer = pair_outer;
+    return a;
+}
+
 template <int K, typename T, class Gain, int CB>
 hipError_t launch_module_three_pass(const ModuleArgs &m, Gain gain)
 {
@@ -908,24 +1132,51 @@ hipError_t launch_module_three_pass(const ModuleArgs &m, Gain gain)
                        m.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = record(m.events[1], st)) != hipSuccess) return e;
-    LaunchArgs a{};
-    a.gain_kind = m.gain_kind;
-    a.gain = m.gain;
-    a.gain_t = m.gain_t;
-    a.gain_c = m.gain_c;
-    a.cbits = m.cbits;
-    a.ws = m.ws;
-    a.B = m.B;
-    a.K = K;
-    a.plan = PLAN_THREE_PASS;
-    a.stream = st;
-    if ((e = launch_middle(a)) != hipSuccess) return e;
+    if ((e = launch_middle(middle_args(m, false))) != hipSuccess) return e;
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
     hipLaunchKernelGGL((module_outer_inv_kernel<A, HB, R, T, CB>), dim3((uint32_t)(m.B << HB)),
                        dim3(1u << (A - VB)), 0, st, m.ws, pin + n, static_cast<T *>(m.y),
                        m.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return record(m.events[3], st);
+}
+
+// C = 256 (bf16): the three passes on 2^16 outer tiles.
+template <int K>
+hipError_t launch_module_pair(const ModuleArgs &m)
+{
+    constexpr Split sp = pair_split(K);
+    constexpr int HB = sp.HB, R = sp.R;
+    static_assert(sp.A == 16 && HB >= 1, "pair split");
+    const __bf16 *pin = static_cast<const __bf16 *>(m.wpack);
+    const hipStream_t st = m.stream;
+    const dim3 grid((uint32_t)(m.B << HB)), block(kPairThreads);
+    hipError_t e = record(m.events[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((module_outer_fwd_pair_kernel<HB, R>), grid, block, 0, st,
+                       static_cast<const __bf16 *>(m.x), pin, m.ws, m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(m.events[1], st)) != hipSuccess) return e;
+    if ((e = launch_middle(middle_args(m, true))) != hipSuccess) return e;
+    if ((e = record(m.events[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((module_outer_inv_pair_kernel<HB, R>), grid, block, 0, st, m.ws,
+                       pin + kPairC * kPairC, static_cast<__bf16 *>(m.y), m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(m.events[3], st);
+}
+
+hipError_t dispatch_pair(const ModuleArgs &m)
+{
+    switch (m.K) {
+#define WHTMIX_MP_CASE(k) \
+    case k: return launch_module_pair<k>(m);
+        WHTMIX_MP_CASE(17) WHTMIX_MP_CASE(18) WHTMIX_MP_CASE(19) WHTMIX_MP_CASE(20)
+        WHTMIX_MP_CASE(21) WHTMIX_MP_CASE(22) WHTMIX_MP_CASE(23) WHTMIX_MP_CASE(24)
+        WHTMIX_MP_CASE(25) WHTMIX_MP_CASE(26) WHTMIX_MP_CASE(27) WHTMIX_MP_CASE(28)
+        WHTMIX_MP_CASE(29) WHTMIX_MP_CASE(30)
+#undef WHTMIX_MP_CASE
+    default: return hipErrorInvalidValue;
+    }
 }
 
 template <typename T, class Gain, int CB>
@@ -964,6 +1215,9 @@ hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
     case 5: return dispatch_k<T, Gain, 5>(m, gain);
     case 6: return dispatch_k<T, Gain, 6>(m, gain);
     case 7: return dispatch_k<T, Gain, 7>(m, gain);
+    case kPairCB:
+        if constexpr (std::is_same<T, __bf16>::value) return dispatch_pair(m);
+        return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
     }
 }
@@ -1057,7 +1311,7 @@ hipError_t launch_module_unfused(const ModuleArgs &m)
 template <typename T, class Gain>
 hipError_t dispatch_module(const ModuleArgs &m, Gain gain)
 {
-    switch (module_path(m.plan, m.cbits)) {
+    switch (module_path(m.plan, m.cbits, m.dtype, m.K)) {
     case MODULE_SMALL: return launch_module_small<T, Gain>(m, gain);
     case MODULE_FUSED_MFMA: return dispatch_fused_module<T, Gain>(m, gain);
     default: return launch_module_unfused<T>(m);

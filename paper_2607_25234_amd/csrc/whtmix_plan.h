@@ -52,17 +52,27 @@ constexpr Split module_split(int K)
     return K >= 16 ? auto_split(K) : forced_split(K);
 }
 
-// Split of the mixer's three-pass kernels.  Slices of 2^26 elements and more
-// take outer tiles of 2^16 (two 2^15 register sets per workgroup), which
-// leaves the middle pass one more carried bit: runs of 32 floats (128-byte
-// lines) at 2^26 instead of 16.
+// Split with outer tiles of 2^16 (two 2^15 register sets per workgroup),
+// K >= 17.
 constexpr int kMaxOuter = 16;
-constexpr Split three_pass_split(int K)
+constexpr Split pair_split(int K)
 {
-    if (K < 26)
-        return module_split(K);
     const int HB = K - kMaxOuter;
     return Split{kMaxOuter, HB, clampi(5, kMinTile - HB, kMaxTile - HB)};
 }
+
+// Split of the mixer's three-pass kernels.  Slices of 2^26 elements and more
+// take outer tiles of 2^16, which leaves the middle pass one more carried
+// bit: runs of 32 floats (128-byte lines) at 2^26 instead of 16.
+constexpr Split three_pass_split(int K)
+{
+    return K < 26 ? module_split(K) : pair_split(K);
+}
+
+// The block with C = 2^8 channels (bf16) takes 2^16 outer tiles at every
+// three-pass size: a tile of 256 tokens gives each wave 16 whole rows, the
+// shape of the 16-row matrix-core operands.
+constexpr int kPairModuleCbits = 8;
+constexpr int kPairModuleMinK = 17;
 
 }  // namespace whtmix

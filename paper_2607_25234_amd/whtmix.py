@@ -50,11 +50,15 @@ class Options(ctypes.Structure):
     _fields_ = [("plan", ctypes.c_int), ("events", ctypes.c_void_p * 4)]
 
 
+MODULE_PATHS = {0: "small", 1: "mfma", 2: "unfused"}
+
+
 class PlanInfo(ctypes.Structure):
     _fields_ = [("plan", ctypes.c_int), ("kernels", ctypes.c_int),
                 ("log2_slice", ctypes.c_int), ("outer_bits", ctypes.c_int),
                 ("run_bits", ctypes.c_int), ("workspace_bytes", ctypes.c_int64),
-                ("padded_tokens", ctypes.c_int64)]
+                ("padded_tokens", ctypes.c_int64), ("module_path", ctypes.c_int),
+                ("module_outer_bits", ctypes.c_int)]
 
 
 _lib = None
@@ -144,7 +148,9 @@ def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = 
     return {"plan": PLAN_NAMES[info.plan], "kernels": info.kernels,
             "log2_slice": info.log2_slice, "outer_bits": info.outer_bits,
             "run_bits": info.run_bits, "workspace_bytes": info.workspace_bytes,
-            "padded_tokens": info.padded_tokens}
+            "padded_tokens": info.padded_tokens,
+            "module_path": MODULE_PATHS.get(info.module_path),
+            "module_outer_bits": info.module_outer_bits}
 
 
 def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,

@@ -253,6 +253,28 @@ def test_plan_table():
             assert (A == 16) == (K >= 26)
 
 
+@pytest.mark.parametrize("shape", [(1, 512, 256), (2, 700, 256), (1, 262144, 256)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_block_c256_takes_pair_tiles(shape):
+    """bf16 C = 256 from 2^17 elements per slice: the projections fused into
+    2^16-element outer tiles; float32 C = 256 stays unfused."""
+    B, N, C = shape
+    d = whtmix.plan_describe(B, N, C, "bf16")
+    assert (d["plan"], d["module_path"], d["module_outer_bits"]) == ("three_pass", "mfma", 16)
+    f = whtmix.plan_describe(B, N, C, "f32")
+    assert f["module_path"] == "unfused" and f["module_outer_bits"] == f["outer_bits"]
+
+
+def test_block_paths():
+    assert whtmix.plan_describe(1, 256, 256, "bf16")["module_path"] == "unfused"   # 2^16
+    assert whtmix.plan_describe(1, 64, 256, "bf16")["module_path"] == "unfused"    # FUSED plan
+    assert whtmix.plan_describe(2, 4, 4, "bf16")["module_path"] == "small"
+    d = whtmix.plan_describe(4, 65536, 128, "bf16")
+    assert (d["module_path"], d["module_outer_bits"]) == ("mfma", 14)
+    assert whtmix.plan_describe(1, 256, 64)["module_outer_bits"] == 0    # FUSED plan
+    assert whtmix.plan_describe(1, 4, 8192)["module_path"] is None      # C above the limit
+
+
 def test_every_three_pass_split_fits_the_tiles():
     for K in range(12, 31):
         N = 1 << (K // 2)

@@ -20,9 +20,10 @@ def test_module_algorithmic_bytes_and_flops():
     L = 65536 * 128
     assert b == [4 * L * 2 + 4 * L * 4 + 128 * 128 * 2, 4 * L * 8 + 4 * L, 4 * L * 4 + 4 * L * 2 + 128 * 128 * 2]
     assert f == [2 * 4 * 65536 * 128 * 128, 0, 2 * 4 * 65536 * 128 * 128]
-    assert bench.module_kernels("three_pass", 128) == names
-    assert bench.module_kernels("three_pass", 256) == ["unfused"]
-    assert bench.module_kernels("fused", 64) == ["module_fused"]
+    assert bench.module_kernels("three_pass", "mfma") == names
+    assert bench.module_kernels("three_pass", "unfused") == ["unfused"]
+    assert bench.module_kernels("fused", "mfma") == ["module_fused"]
+    assert bench.module_kernels("small", "small") == ["module_small"]
 
 
 def test_traffic_lookup_tolerates_every_record(tmp_path, monkeypatch):

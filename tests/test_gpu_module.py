@@ -66,10 +66,10 @@ def inputs(B, N, C, dtype, seed):
 
 
 def path(B, N, C, dtype, plan="auto"):
-    p = whtmix.plan_describe(B, N, C, dtype, plan)["plan"]
-    if p == "small":
+    d = whtmix.plan_describe(B, N, C, dtype, plan)
+    if d["module_path"] == "small":
         return "small"
-    return "mfma-" + p if 16 <= C <= 128 else "unfused-" + p
+    return f"{d['module_path']}-{d['plan']}"
 
 
 @pytest.mark.parametrize("name", list(workloads.WORKLOADS))
@@ -95,11 +95,15 @@ SHAPES = [
     # THREE_PASS with MFMA projections
     (2, 4096, 16), (1, 3000, 32), (2, 2048, 128), (1, 9216, 64), (1, 8192, 128),
     (1, 1 << 15, 32),
+    # C = 256: bf16 THREE_PASS on 2^16 outer tiles (ragged and wholly padded
+    # tiles included); float32 and the FUSED plan UNFUSED
+    (1, 512, 256), (2, 700, 256), (1, 4096, 256), (1, 9216, 256),
     # UNFUSED: C outside [16, 128] (matrix-core projections from C = 256; VALU below 16
     # and for float32 C = 4096, whose weight slice does not fit LDS)
     (2, 512, 8), (1, 64, 256), (3, 1000, 256), (1, 8, 512), (1, 3, 1024), (1, 16, 2048),
     (1, 4, 4096),
 ]
+
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -127,7 +131,8 @@ def test_module_forced_three_pass(shape, dtype, dev, orc):
     check(f"{shape} three_pass", y, orc.whtmix_module(x, wi, g, wo), dtype)
 
 
-SEPARABLE = [(2, 16, 32), (2, 200, 64), (1, 4096, 128), (2, 9216, 64), (1, 100, 256)]
+SEPARABLE = [(2, 16, 32), (2, 200, 64), (1, 4096, 128), (2, 9216, 64), (1, 100, 256),
+             (1, 2000, 256)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -155,7 +160,7 @@ def test_module_separable_workload(dev, orc):
 
 @pytest.mark.parametrize("shape,plan", [((2, 16, 64), "auto"), ((2, 100, 64), "auto"),
                                         ((1, 4096, 128), "auto"), ((2, 128, 32), "three_pass"),
-                                        ((1, 512, 8), "auto")])
+                                        ((1, 512, 8), "auto"), ((1, 1000, 256), "auto")])
 def test_module_in_place(shape, plan, dev, orc):
     """y may be x itself (every path reads all of its x before writing y)."""
     B, N, C = shape

@@ -200,16 +200,26 @@ class Tracker:
         self.layout = LB
 
 
+class Low4Hi9:
+    """2^15 tiles: registers hold t bits 0-3 and 9; threads bits 4-8, 10-14."""
+
+    def reg(self, j):
+        return j if j < 4 else 9
+
+    def base(self, tau):
+        return ((tau & 31) << 4) | ((tau >> 5) << 10)
+
+
 def forward_from_prologue(tr, M):
     tr.butterflies(31)
-    tr.relayout(Std(0))
-    tr.butterflies(15)
     if M <= 14:
+        tr.relayout(Std(0))
+        tr.butterflies(15)
         tr.relayout(Std(M - 5))
         tr.butterflies(31 & ~((1 << (14 - M)) - 1))
     else:
-        tr.relayout(Std(5))
-        tr.butterflies(16)
+        tr.relayout(Low4Hi9())
+        tr.butterflies(31)
         tr.relayout(Std(10))
         tr.butterflies(31)
 
@@ -482,6 +492,173 @@ def test_fused_model_matches_oracle(oracle, N, CB, bf):
     ref = oracle.whtmix_module(x, w_in, g, w_out)
     tol = 1e-5 if bf else 1e-12
     np.testing.assert_allclose(y, ref, atol=tol * np.abs(ref).max())
+
+
+# ------------------------------------------------------------------ C = 256: 2^16 pair tiles
+# A bf16 block with C = 256 runs its outer passes on tiles of 256 tokens x 256
+# channels (t = token * 256 + channel), 1024 threads of two register sets of
+# 32.  Forward: set = t bit 15 (token bit 7), each set in layout 4 of its 2^15
+# elements straight from the MFMA results.  Inverse: set = t bit 5 (channel bit
+# 5); within a set t' drops that bit and the set's elements are laid out like
+# a C = 128 tile, so the epilogue layout is Epi(15, 7).
+PC, PCB, PM = 256, 8, 15
+
+
+def mfma_bf16_fast(a, b, acc):
+    """mfma_bf16 with array reshapes (same lane layout)."""
+    A = a.reshape(4, 16, 4).transpose(1, 0, 2).reshape(16, 16)
+    B = b.reshape(4, 16, 4).transpose(0, 2, 1).reshape(16, 16)
+    D = A @ B
+    return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
+
+
+def pair_token(m, w):
+    """Token of MFMA row m = 4q + r in wave w: r0 -> token bit 0, q -> bits
+    1-2, the wave -> bits 3-6, r1 -> bit 7 (the register set)."""
+    return (m & 1) | (((m >> 2) & 3) << 1) | (w << 3) | (((m >> 1) & 1) << 7)
+
+
+def model_prologue_pair(xtile, valid, p_in):
+    """[2, 1024, 32] registers of Z = X W_in: set s, register nb | r0 << 4."""
+    v = np.zeros((2, 1024, 32))
+    lanes = np.arange(64)
+    i, q = lanes & 15, lanes >> 4
+    ks = PC // 16
+    for w in range(16):
+        tok = pair_token(i, w)
+        rows = np.zeros((64, PC))
+        ok = tok * PC < valid
+        rows[ok] = xtile[tok[ok]]
+        for nb in range(16):
+            acc = np.zeros((64, 4))
+            for kk in range(ks):
+                cols = np.array([[k_in_bf16(PC, kk, q[l], r) for r in range(4)]
+                                 for l in range(64)])
+                a = rows[lanes[:, None], cols]
+                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 4 + np.arange(4)[None, :]
+                acc = mfma_bf16_fast(a, p_in[idx], acc)
+            for r in range(4):
+                v[r >> 1, w * 64:(w + 1) * 64, nb | ((r & 1) << 4)] = acc[:, r]
+    return v
+
+
+def cross(v0, v1):
+    return v0 + v1, v0 - v1
+
+
+def expand5(tp):
+    """Set-local index t' -> tile index with bit 5 clear."""
+    return (tp & 31) | ((tp >> 5) << 6)
+
+
+def model_epilogue_pair(v0, v1, p_out, valid):
+    """Y = Z' W_out from the two sets' Epi(15, 7) registers; lane (j, q) of
+    wave w holds channels 64 q + 32 s + k' of token j | w << 4."""
+    out = np.full(1 << 16, np.nan)
+    written = np.zeros(1 << 16, dtype=int)
+    lanes = np.arange(64)
+    j, q = lanes & 15, lanes >> 4
+    ks = PC // 16
+    for w in range(16):
+        vw = np.concatenate([v0[w * 64:(w + 1) * 64], v1[w * 64:(w + 1) * 64]], axis=1)
+        row = (j | (w << 4)) * PC * 2
+        accs = []
+        for nb in range(16):
+            acc = np.zeros((64, 4))
+            for kk in range(ks):
+                hi, lo = split_bf16(vw[:, 4 * kk:4 * kk + 4])
+                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 4 + np.arange(4)[None, :]
+                a = p_out[idx]
+                acc = mfma_bf16_fast(a, hi, acc)
+                acc = mfma_bf16_fast(a, lo, acc)
+            accs.append(acc)
+        for n in range(8):
+            vals = np.concatenate([accs[2 * n], accs[2 * n + 1]], axis=1)
+            off = row + 16 * q + 64 * n
+            for l in range(64):
+                for u in range(8):
+                    t = (off[l] + 2 * u) // 2
+                    if 2 * t + 2 <= valid * 2:
+                        out[t] = vals[l, u]
+                        written[t] += 1
+    assert written.max() <= 1, "an element stored twice"
+    assert (written[:valid] == 1).all(), "an element of the tile not stored"
+    return out
+
+
+def test_fast_mfma_model_is_the_lane_model():
+    rng = np.random.default_rng(3)
+    a, b, c = rng.standard_normal((64, 4)), rng.standard_normal((64, 4)), rng.standard_normal((64, 4))
+    np.testing.assert_allclose(mfma_bf16_fast(a, b, c), mfma_bf16(a, b, c), atol=1e-12)
+
+
+def test_pair_prologue_fragments_are_layout_4():
+    """C = 256: the MFMA results of each set, read as layout 4 of that set's
+    2^15 elements, are Z = X W_in (ragged tile: the last 37 tokens padding)."""
+    rng = np.random.default_rng(256)
+    w_in, w_out = _weights(rng, PC)
+    w_in = round_to_bf16(w_in.astype(np.float32)).astype(np.float64)
+    p_in, _ = pack(w_in, w_out, True)
+    x = round_to_bf16(rng.standard_normal((256, PC)).astype(np.float32)).astype(np.float64)
+    valid = (256 - 37) * PC
+    v = model_prologue_pair(x, valid, p_in)
+    ref = x.copy()
+    ref[valid // PC:] = 0.0
+    ref = (ref @ w_in).reshape(-1)
+    for s in range(2):
+        z = from_registers(v[s], Std(4), PM)
+        np.testing.assert_allclose(z, ref[s << PM:(s + 1) << PM], atol=1e-12)
+
+
+def test_pair_schedules_cover_every_bit_once():
+    """Forward: cross butterfly (bit 15), then each set from layout 4 to the
+    store layout 10; inverse: each set (t bit 5) from layout 10 to the
+    epilogue layout, then the cross butterfly.  Both give the transform over
+    all 16 bits; every exchange stays in bounds, at most 2-way bank
+    conflicts."""
+    rng = np.random.default_rng(16)
+    flat = rng.standard_normal(1 << 16)
+    full = wht_bits(flat, 16)
+    v = [to_registers(flat[s << PM:(s + 1) << PM], Std(4), PM) for s in range(2)]
+    v0, v1 = cross(v[0], v[1])
+    trs = [Tracker(PM, v0, Std(4)), Tracker(PM, v1, Std(4))]
+    for tr in trs:
+        forward_from_prologue(tr, PM)
+        assert sorted(tr.done) == list(range(PM))
+        assert isinstance(tr.layout, Std) and tr.layout.S == 10
+        assert all(wr <= 2 and rd <= 2 for wr, rd in tr.conflicts)
+    for s in range(2):
+        np.testing.assert_allclose(from_registers(trs[s].v, Std(10), PM),
+                                   full[s << PM:(s + 1) << PM], atol=1e-9)
+    tp = np.arange(1 << PM)
+    sets = [flat[expand5(tp) | (s << 5)] for s in range(2)]
+    trs = [Tracker(PM, to_registers(sets[s], Std(10), PM), Std(10)) for s in range(2)]
+    for tr in trs:
+        inverse_to_epilogue(tr, PM, 7)
+        assert sorted(tr.done) == list(range(PM))
+        assert all(wr <= 2 and rd <= 2 for wr, rd in tr.conflicts)
+    e0, e1 = cross(trs[0].v, trs[1].v)
+    for s, e in enumerate((e0, e1)):
+        np.testing.assert_allclose(from_registers(e, Epi(PM, 7), PM),
+                                   full[expand5(tp) | (s << 5)], atol=1e-9)
+
+
+def test_pair_epilogue_stores_y():
+    """Epilogue registers of Z' (both sets) give Y = Z' W_out; each valid
+    element stored once, nothing past the valid rows."""
+    rng = np.random.default_rng(257)
+    w_in, w_out = _weights(rng, PC)
+    w_out = round_to_bf16(w_out.astype(np.float32)).astype(np.float64)
+    _, p_out = pack(w_in, w_out, True)
+    z = rng.standard_normal((256, PC))
+    valid = (256 - 11) * PC
+    flat = z.reshape(-1)
+    tp = np.arange(1 << PM)
+    v = [to_registers(flat[expand5(tp) | (s << 5)], Epi(PM, 7), PM) for s in range(2)]
+    y = model_epilogue_pair(v[0], v[1], p_out, valid)
+    assert np.isnan(y[valid:]).all()
+    ref = (z @ w_out).reshape(-1)[:valid]
+    np.testing.assert_allclose(y[:valid], ref, atol=1e-5 * np.abs(ref).max())
 
 
 # ------------------------------------------------------------------ UNFUSED MFMA projection
