@@ -520,6 +520,22 @@ __device__ __forceinline__ void stage_weights(void *lds, const void *w, uint32_t
         d[c] = s[c];
 }
 
+// The same copy without a trip through registers (global_load_lds_dwordx4):
+// piece c = tau + i NT lands at byte 16 c, so each wave's 64 pieces of a step
+// are contiguous from a wave-uniform base, the instruction's LDS pattern.
+// The caller waits (vmcnt) and synchronises before reading.
+template <uint32_t CHUNKS, uint32_t NT>
+__device__ __forceinline__ void stage_weights_dma(void *lds, const void *w, uint32_t tau)
+{
+    static_assert(CHUNKS % NT == 0 && NT % 64 == 0, "whole waves");
+    const uint32_t wave = tau >> 6;
+#pragma unroll
+    for (uint32_t i = 0; i < CHUNKS / NT; ++i)
+        __builtin_amdgcn_global_load_lds(
+            static_cast<const char *>(w) + 16u * (tau + i * NT),
+            static_cast<char *>(lds) + 16u * (wave * 64u + i * NT), 16, 0, 0);
+}
+
 // ---------------------------------------------------------------- kernels
 // FUSED: one workgroup per slice (M = K).
 template <int K, typename T, class Gain, int CB>
@@ -646,12 +662,34 @@ module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_ou
 // 2^15 set laid out like a C = 128 tile, so the C = 128 inverse schedule ends
 // in the epilogue layout Epi<15, 7>: lane (j, q) of wave w holds channels
 // 64 q + 32 s + [0, 32) of token j | w << 4, the B operand of
-// Y^T = W_out^T Z'^T for 16 k steps of 16 channels.
+// Y^T = W_out^T Z'^T.
+//
+// Both products use v_mfma_f32_16x16x32_bf16 (lane 16 g + i supplies k = 8 g
+// + [0, 8) of row i of A / column i of B), half the instructions of the
+// 16x16x16 form: step kk of the prologue is channels 32 kk + 8 g + [0, 8) (one
+// 16-byte load of x), of the epilogue channels 64 g + 8 kk + [0, 8).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kPairCB = kPairModuleCbits;
 constexpr uint32_t kPairC = 1u << kPairCB;
 constexpr uint32_t kPairThreads = 1u << (15 - VB);
-constexpr uint32_t kPairKs = kPairC / 16u;                      // k steps
+constexpr uint32_t kPairKs = kPairC / 32u;                      // k steps
 constexpr uint32_t kPairWChunks = kPairC * kPairC * 2u / 16u;   // 16-byte pieces of W
+
+// One thread per packed element: index ((nb * kPairKs + kk) * 64 + 16 g + j)
+// * 8 + e holds W_in[32 kk + 8 g + e][16 nb + j] (B operand of Z = X W_in) and
+// W_out[64 g + 8 kk + e][oc_bf16(nb, j)] (A operand of Y^T = W_out^T Z'^T).
+__global__ void __launch_bounds__(256)
+pack_pair_weights_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_out,
+                         __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out)
+{
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= kPairC * kPairC) return;
+    const uint32_t e = idx & 7u, lane = (idx >> 3) & 63u;
+    const uint32_t j = lane & 15u, g = lane >> 4;
+    const uint32_t kk = (idx >> 9) % kPairKs, nb = (idx >> 9) / kPairKs;
+    p_in[idx] = w_in[(32u * kk + 8u * g + e) * kPairC + 16u * nb + j];
+    p_out[idx] = w_out[(64u * g + 8u * kk + e) * kPairC + oc_bf16(kPairC, nb, j)];
+}
 static_assert(kPairC * kPairC * 2u <= pad(1u << 15) * 4u, "W fits the tile's LDS");
 static_assert(kPairWChunks % kPairThreads == 0, "whole prefetch per thread");
 
@@ -665,8 +703,8 @@ struct DropBit5 {
 };
 
 // X fragments of the wave's 16 tokens: k step kk holds channels
-// 32 (kk / 2) + 8 q + 4 (kk % 2) + [0, 4) (16-byte loads of 8 channels).
-__device__ __forceinline__ void load_x_pair(bf16x4 (&a)[kPairKs], const __bf16 *tile,
+// 32 kk + 8 q + [0, 8).
+__device__ __forceinline__ void load_x_pair(bf16x8 (&a)[kPairKs], const __bf16 *tile,
                                             uint32_t valid, uint32_t tau)
 {
     const uint32_t lane = tau & 63u, w = tau >> 6;
@@ -676,29 +714,28 @@ __device__ __forceinline__ void load_x_pair(bf16x4 (&a)[kPairKs], const __bf16 *
     const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 2u);
     const uint32_t voff = tok * kPairC * 2u + 16u * q;
 #pragma unroll
-    for (uint32_t p = 0; p < kPairKs / 2u; ++p) {
+    for (uint32_t kk = 0; kk < kPairKs; ++kk) {
         u32x4 d = {0u, 0u, 0u, 0u};
         if (ok)
-            d = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 64u * p, kStreaming);
-        a[2 * p] = __builtin_bit_cast(bf16x4, (u32x2){d.x, d.y});
-        a[2 * p + 1] = __builtin_bit_cast(bf16x4, (u32x2){d.z, d.w});
+            d = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 64u * kk, kStreaming);
+        a[kk] = __builtin_bit_cast(bf16x8, d);
     }
 }
 
 // Z = X W_in into the two sets (packed W_in in LDS).
 __device__ __forceinline__ void project_in_pair(float (&v0)[V], float (&v1)[V],
-                                                const bf16x4 (&a)[kPairKs], const void *wl,
+                                                const bf16x8 (&a)[kPairKs], const void *wl,
                                                 uint32_t tau)
 {
-    const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+    const bf16x8 *wb = static_cast<const bf16x8 *>(wl);
     const uint32_t lane = tau & 63u;
 #pragma unroll
     for (int nb = 0; nb < 16; ++nb) {
         f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (uint32_t kk = 0; kk < kPairKs; ++kk)
-            acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a[kk], wb[(nb * kPairKs + kk) * 64u + lane],
-                                                             acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kk], wb[(nb * kPairKs + kk) * 64u + lane],
+                                                          acc, 0, 0, 0);
         v0[nb] = acc[0];
         v0[nb | 16] = acc[1];
         v1[nb] = acc[2];
@@ -706,44 +743,53 @@ __device__ __forceinline__ void project_in_pair(float (&v0)[V], float (&v1)[V],
     }
 }
 
-// Y = Z' W_out for the wave's 16 tokens from the two sets' epilogue-layout
-// registers (packed W_out in LDS); rows past `valid` are not stored.
-__device__ __forceinline__ void project_out_pair(const float (&v0)[V], const float (&v1)[V],
-                                                 const void *wl, __bf16 *tile, uint32_t valid,
-                                                 uint32_t tau)
+// The two-term split Z' = hi + lo of the two sets' epilogue-layout registers,
+// as B operands: step kk element e is channel 64 q + 8 kk + e, i.e. set
+// kk / 4, register 8 (kk % 4) + e.
+__device__ __forceinline__ void split_pair(const float (&v0)[V], const float (&v1)[V],
+                                           bf16x8 (&hi)[kPairKs], bf16x8 (&lo)[kPairKs])
 {
-    const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
+#pragma unroll
+    for (uint32_t kk = 0; kk < kPairKs; ++kk) {
+        u32x4 h2, l2;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float z0 = kk < 4 ? v0[8 * kk + 2 * e] : v1[8 * (kk - 4) + 2 * e];
+            const float z1 = kk < 4 ? v0[8 * kk + 2 * e + 1] : v1[8 * (kk - 4) + 2 * e + 1];
+            const float h0 = (float)(__bf16)z0, h1 = (float)(__bf16)z1;
+            h2[e] = pack2_bf16(z0, z1);
+            l2[e] = pack2_bf16(z0 - h0, z1 - h1);
+        }
+        hi[kk] = __builtin_bit_cast(bf16x8, h2);
+        lo[kk] = __builtin_bit_cast(bf16x8, l2);
+    }
+}
+
+// Y = Z' W_out for the wave's 16 tokens (packed W_out in LDS); rows past
+// `valid` are not stored.
+__device__ __forceinline__ void project_out_pair(const bf16x8 (&hi)[kPairKs],
+                                                 const bf16x8 (&lo)[kPairKs], const void *wl,
+                                                 __bf16 *tile, uint32_t valid, uint32_t tau)
+{
+    const bf16x8 *wb = static_cast<const bf16x8 *>(wl);
     const uint32_t lane = tau & 63u, w = tau >> 6;
     const uint32_t j = lane & 15u, q = lane >> 4;
     const uint32_t tok = j | (w << 4);
     const bool ok = tok * kPairC < valid;
     const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 2u);
     const uint32_t voff = tok * kPairC * 2u + 16u * q;
-    // the two-term split Z' = hi + lo; step kk element e is channel
-    // 64 q + 4 kk + e: set kk / 8, register 4 (kk % 8) + e
-    bf16x4 hi[kPairKs], lo[kPairKs];
-#pragma unroll
-    for (uint32_t kk = 0; kk < kPairKs; ++kk) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float z = kk < 8 ? v0[4 * kk + e] : v1[4 * (kk - 8) + e];
-            const __bf16 h = (__bf16)z;
-            hi[kk][e] = __builtin_bit_cast(short, h);
-            lo[kk][e] = __builtin_bit_cast(short, (__bf16)(z - (float)h));
-        }
-    }
     // blocks 2n, 2n+1: channels 32 n + 8 q + [0, 8), one 16-byte store
 #pragma unroll
     for (uint32_t n = 0; n < 8; ++n) {
         f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (uint32_t kk = 0; kk < kPairKs; ++kk) {
-            const bf16x4 a0 = wb[((2 * n) * kPairKs + kk) * 64u + lane];
-            const bf16x4 a1 = wb[((2 * n + 1) * kPairKs + kk) * 64u + lane];
-            acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, hi[kk], acc0, 0, 0, 0);
-            acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, lo[kk], acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, hi[kk], acc1, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, lo[kk], acc1, 0, 0, 0);
+            const bf16x8 a0 = wb[((2 * n) * kPairKs + kk) * 64u + lane];
+            const bf16x8 a1 = wb[((2 * n + 1) * kPairKs + kk) * 64u + lane];
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, hi[kk], acc0, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, lo[kk], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, hi[kk], acc1, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, lo[kk], acc1, 0, 0, 0);
         }
         const u32x4 d = {pack2_bf16(acc0[0], acc0[1]), pack2_bf16(acc0[2], acc0[3]),
                          pack2_bf16(acc1[0], acc1[1]), pack2_bf16(acc1[2], acc1[3])};
@@ -766,9 +812,10 @@ module_outer_fwd_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restr
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const uint32_t valid = tile_valid<A>(nvalid, hi);
-    bf16x4 a[kPairKs];
+    bf16x8 a[kPairKs];
     load_x_pair(a, x + b * nvalid + ((size_t)hi << A), valid, tau);
-    stage_weights<kPairWChunks, kPairThreads>(lds, w_in, tau);
+    stage_weights_dma<kPairWChunks, kPairThreads>(lds, w_in, tau);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     float v0[V], v1[V];
     project_in_pair(v0, v1, a, lds, tau);
@@ -790,9 +837,6 @@ module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restr
     constexpr int A = 16, M = 15;
     using Run = RunMap<HB, R>;
     using SetMap = DropBit5<Run>;
-    // W_out: PRE of its PER 16-byte pieces per thread are prefetched into
-    // registers at the start (all of them would spill: the two sets hold 64)
-    constexpr uint32_t PER = kPairWChunks / kPairThreads, PRE = 4;
     __shared__ __attribute__((aligned(16))) float lds[pad(1u << M)];
     const uint32_t tau = threadIdx.x;
     const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
@@ -801,28 +845,21 @@ module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restr
     const uint32_t valid = tile_valid<A>(nvalid, hi);
     if (valid == 0)
         return;   // wholly padding: nothing to store (uniform per workgroup)
-    const u32x4 *wsrc = static_cast<const u32x4 *>(static_cast<const void *>(w_out));
-    u32x4 wreg[PER];
-#pragma unroll
-    for (uint32_t i = 0; i < PRE; ++i)
-        wreg[i] = wsrc[tau + i * kPairThreads];
     const __amdgpu_buffer_rsrc_t r =
         buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>());
     float v0[V], v1[V];
     load_layout<M - 5, SetMap, float>(v0, r, tau);
     load_layout<M - 5, SetMap, float>(v1, r, tau, Run::at(1u << 5) * 4u);
+    cross_butterflies(v0, v1);   // t bit 5 (the bit groups commute)
     inverse_to_epilogue<M, 7, false>(lds, v0, tau);
     inverse_to_epilogue<M, 7, true>(lds, v1, tau);
-#pragma unroll
-    for (uint32_t i = PRE; i < PER; ++i)
-        wreg[i] = wsrc[tau + i * kPairThreads];
-    cross_butterflies(v0, v1);   // t bit 5
     __syncthreads();             // every thread has read its epilogue-layout values
-#pragma unroll
-    for (uint32_t i = 0; i < PER; ++i)
-        reinterpret_cast<u32x4 *>(lds)[tau + i * kPairThreads] = wreg[i];
+    stage_weights_dma<kPairWChunks, kPairThreads>(lds, w_out, tau);
+    bf16x8 zh[kPairKs], zl[kPairKs];
+    split_pair(v0, v1, zh, zl);  // while W_out arrives
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    project_out_pair(v0, v1, lds, y + b * nvalid + ((size_t)hi << A), valid, tau);
+    project_out_pair(zh, zl, lds, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
 __device__ __forceinline__ float to_f(float v) { return v; }
@@ -1208,7 +1245,16 @@ hipError_t dispatch_k(const ModuleArgs &m, Gain gain)
 template <typename T, class Gain>
 hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
 {
-    hipError_t e = launch_pack<T>(m, false);
+    hipError_t e;
+    if (m.cbits == kPairCB) {
+        hipLaunchKernelGGL(pack_pair_weights_kernel, dim3(kPairC * kPairC / 256u), dim3(256), 0,
+                           m.stream, static_cast<const __bf16 *>(m.w_in),
+                           static_cast<const __bf16 *>(m.w_out), static_cast<__bf16 *>(m.wpack),
+                           static_cast<__bf16 *>(m.wpack) + kPairC * kPairC);
+        e = hipGetLastError();
+    } else {
+        e = launch_pack<T>(m, false);
+    }
     if (e != hipSuccess) return e;
     switch (m.cbits) {
     case 4: return dispatch_k<T, Gain, 4>(m, gain);

@@ -512,6 +512,30 @@ def mfma_bf16_fast(a, b, acc):
     return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
 
 
+def mfma_bf16_x32(a, b, acc):
+    """16x16x32 (gfx950): a, b [64, 8]; lane 16 g + i supplies row i of A
+    (column i of B) with k = 8 g + e; the result layout is the 16x16x16 one."""
+    A = a.reshape(4, 16, 8).transpose(1, 0, 2).reshape(16, 32)
+    B = b.reshape(4, 16, 8).transpose(0, 2, 1).reshape(32, 16)
+    D = A @ B
+    return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
+
+
+def pack_pair(w_in, w_out):
+    """C = 256 operands of the 16x16x32 instruction: packed index
+    ((nb * 8 + kk) * 64 + 16 g + j) * 8 + e holds W_in[32 kk + 8 g + e][16 nb + j]
+    and W_out[64 g + 8 kk + e][oc_bf16(nb, j)]."""
+    C = w_in.shape[0]
+    idx = np.arange(C * C)
+    e, lane, rest = idx & 7, (idx >> 3) & 63, idx >> 9
+    j, g = lane & 15, lane >> 4
+    kk, nb = rest % (C // 32), rest // (C // 32)
+    si = (32 * kk + 8 * g + e) * C + 16 * nb + j
+    so = (64 * g + 8 * kk + e) * C + np.array([oc_bf16(C, int(n), int(m)) for n, m in zip(nb, j)])
+    assert sorted(si) == list(range(C * C)) and sorted(so) == list(range(C * C))
+    return w_in.reshape(-1)[si], w_out.reshape(-1)[so]
+
+
 def pair_token(m, w):
     """Token of MFMA row m = 4q + r in wave w: r0 -> token bit 0, q -> bits
     1-2, the wave -> bits 3-6, r1 -> bit 7 (the register set)."""
@@ -519,11 +543,12 @@ def pair_token(m, w):
 
 
 def model_prologue_pair(xtile, valid, p_in):
-    """[2, 1024, 32] registers of Z = X W_in: set s, register nb | r0 << 4."""
+    """[2, 1024, 32] registers of Z = X W_in: set s, register nb | r0 << 4.
+    Step kk of lane group q is one 16-byte load: channels 32 kk + 8 q + [0, 8)."""
     v = np.zeros((2, 1024, 32))
     lanes = np.arange(64)
     i, q = lanes & 15, lanes >> 4
-    ks = PC // 16
+    ks = PC // 32
     for w in range(16):
         tok = pair_token(i, w)
         rows = np.zeros((64, PC))
@@ -532,11 +557,10 @@ def model_prologue_pair(xtile, valid, p_in):
         for nb in range(16):
             acc = np.zeros((64, 4))
             for kk in range(ks):
-                cols = np.array([[k_in_bf16(PC, kk, q[l], r) for r in range(4)]
-                                 for l in range(64)])
+                cols = 32 * kk + 8 * q[:, None] + np.arange(8)[None, :]
                 a = rows[lanes[:, None], cols]
-                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 4 + np.arange(4)[None, :]
-                acc = mfma_bf16_fast(a, p_in[idx], acc)
+                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 8 + np.arange(8)[None, :]
+                acc = mfma_bf16_x32(a, p_in[idx], acc)
             for r in range(4):
                 v[r >> 1, w * 64:(w + 1) * 64, nb | ((r & 1) << 4)] = acc[:, r]
     return v
@@ -558,19 +582,19 @@ def model_epilogue_pair(v0, v1, p_out, valid):
     written = np.zeros(1 << 16, dtype=int)
     lanes = np.arange(64)
     j, q = lanes & 15, lanes >> 4
-    ks = PC // 16
+    ks = PC // 32
     for w in range(16):
         vw = np.concatenate([v0[w * 64:(w + 1) * 64], v1[w * 64:(w + 1) * 64]], axis=1)
         row = (j | (w << 4)) * PC * 2
         accs = []
         for nb in range(16):
             acc = np.zeros((64, 4))
-            for kk in range(ks):
-                hi, lo = split_bf16(vw[:, 4 * kk:4 * kk + 4])
-                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 4 + np.arange(4)[None, :]
+            for kk in range(ks):     # channels 64 q + 8 kk + [0, 8)
+                hi, lo = split_bf16(vw[:, 8 * kk:8 * kk + 8])
+                idx = ((nb * ks + kk) * 64 + lanes[:, None]) * 8 + np.arange(8)[None, :]
                 a = p_out[idx]
-                acc = mfma_bf16_fast(a, hi, acc)
-                acc = mfma_bf16_fast(a, lo, acc)
+                acc = mfma_bf16_x32(a, hi, acc)
+                acc = mfma_bf16_x32(a, lo, acc)
             accs.append(acc)
         for n in range(8):
             vals = np.concatenate([accs[2 * n], accs[2 * n + 1]], axis=1)
@@ -590,6 +614,10 @@ def test_fast_mfma_model_is_the_lane_model():
     rng = np.random.default_rng(3)
     a, b, c = rng.standard_normal((64, 4)), rng.standard_normal((64, 4)), rng.standard_normal((64, 4))
     np.testing.assert_allclose(mfma_bf16_fast(a, b, c), mfma_bf16(a, b, c), atol=1e-12)
+    # the 16x16x32 form is two 16x16x16 products over k = 8 g + [0, 4) and 8 g + [4, 8)
+    a8, b8 = rng.standard_normal((64, 8)), rng.standard_normal((64, 8))
+    two = mfma_bf16(a8[:, 4:], b8[:, 4:], mfma_bf16(a8[:, :4], b8[:, :4], c))
+    np.testing.assert_allclose(mfma_bf16_x32(a8, b8, c), two, atol=1e-12)
 
 
 def test_pair_prologue_fragments_are_layout_4():
@@ -598,7 +626,7 @@ def test_pair_prologue_fragments_are_layout_4():
     rng = np.random.default_rng(256)
     w_in, w_out = _weights(rng, PC)
     w_in = round_to_bf16(w_in.astype(np.float32)).astype(np.float64)
-    p_in, _ = pack(w_in, w_out, True)
+    p_in, _ = pack_pair(w_in, w_out)
     x = round_to_bf16(rng.standard_normal((256, PC)).astype(np.float32)).astype(np.float64)
     valid = (256 - 37) * PC
     v = model_prologue_pair(x, valid, p_in)
@@ -649,7 +677,7 @@ def test_pair_epilogue_stores_y():
     rng = np.random.default_rng(257)
     w_in, w_out = _weights(rng, PC)
     w_out = round_to_bf16(w_out.astype(np.float32)).astype(np.float64)
-    _, p_out = pack(w_in, w_out, True)
+    _, p_out = pack_pair(w_in, w_out)
     z = rng.standard_normal((256, PC))
     valid = (256 - 11) * PC
     flat = z.reshape(-1)
