@@ -4,10 +4,11 @@
 // MFMA prologue and epilogue, so Z never makes an extra trip through HBM.
 //
 // Projections (C = 2^CB channels, 16 <= C <= 128):
-//   * bf16: v_mfma_f32_16x16x16_bf16.  X W_in multiplies bf16 by bf16, which
-//     is exact in the fp32 accumulator.  Z' W_out has an fp32 left operand:
-//     it is split as Z' = hi + lo (two bf16, hi = RNE(Z'), lo = RNE(Z' - hi),
-//     which leaves a residual below 2^-17 |Z'|) and multiplied in two MFMAs.
+//   * bf16: v_mfma_f32_16x16x32_bf16 (v_mfma_f32_16x16x16_bf16 for C = 16).
+//     X W_in multiplies bf16 by bf16, which is exact in the fp32 accumulator.
+//     Z' W_out has an fp32 left operand: it is split as Z' = hi + lo (two
+//     bf16, hi = RNE(Z'), lo = RNE(Z' - hi), which leaves a residual below
+//     2^-17 |Z'|) and multiplied in two MFMAs.
 //   * fp32: v_mfma_f32_16x16x4_f32.
 //   The contraction order over k is free, so each lane's k values are chosen
 //   to make its loads of X 16-byte pieces and its register reads contiguous.
@@ -47,6 +48,7 @@ namespace {
 using namespace tile;
 
 typedef short bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -179,15 +181,21 @@ struct Proj {
     static constexpr int NRB = 1 << (7 - CB);    // 16-row MFMA blocks per wave
     static constexpr int NNB = C / 16;           // 16-column blocks
     static constexpr bool BF = sizeof(T) == 2;
-    // k steps per column block: 16 (bf16) or 4 (fp32) k values per MFMA
+    // bf16 from C = 32: the 16x16x32 instruction, KS2 steps of 32 k values
+    static constexpr bool X32 = BF && C >= 32;
+    static constexpr int KS2 = C / 32;
+    // k steps per column block of the 16x16x16 (bf16, C = 16) and 16x16x4
+    // (fp32) instructions: 16 or 4 k values per MFMA
     static constexpr int KS = BF ? C / 16 : C / 4;
     // A-fragment registers per lane and row block (X: C/4 values)
     static constexpr uint32_t WBYTES = (uint32_t)C * C * sizeof(T);
 };
 
-// k value order of the prologue (X W_in).  bf16: lane group q, step kk,
-// element r: channel 32(kk/2) + 8q + 4(kk%2) + r (C >= 32; each lane reads its
-// channels as 16-byte pieces of 8), or 4q + r (C = 16).  fp32: step s:
+// k value order of the 16x16x16 bf16 and 16x16x4 fp32 products (the fused
+// kernels' float32 and C = 16 forms, and the projection kernel; the fused bf16
+// forms from C = 32 use pack_x32_kernel's order).  bf16: lane group q, step
+// kk, element r: channel 32(kk/2) + 8q + 4(kk%2) + r (C >= 32; each lane reads
+// its channels as 16-byte pieces of 8), or 4q + r (C = 16).  fp32: step s:
 // channel 16(s/4) + 4q + s%4 (16-byte pieces of 4).
 __host__ __device__ constexpr uint32_t k_in_bf16(uint32_t C, uint32_t kk, uint32_t q, uint32_t r)
 {
@@ -241,6 +249,28 @@ pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *
     }
 }
 
+// bf16, C >= 32: the operands of v_mfma_f32_16x16x32_bf16, whose lane 16 g + i
+// supplies k = 8 g + [0, 8) of row i of A / column i of B.  One thread per
+// packed element: index ((nb * C/32 + kk) * 64 + 16 g + j) * 8 + e holds
+// W_in[32 kk + 8 g + e][16 nb + j] (B operand of Z = X W_in: step kk of lane
+// group g is channels 32 kk + 8 g + [0, 8) of x, one 16-byte load) and
+// W_out[(C/4) g + 8 kk + e][oc_bf16(C, nb, j)] (A operand of Y^T = W_out^T Z'^T:
+// lane group g holds channels [g C/4, (g+1) C/4) of Z').
+__global__ void __launch_bounds__(256)
+pack_x32_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_out,
+                __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= C * C) return;
+    const uint32_t e = idx & 7u, lane = (idx >> 3) & 63u;
+    const uint32_t j = lane & 15u, g = lane >> 4;
+    const uint32_t ks = C / 32u;
+    const uint32_t kk = (idx >> 9) % ks, nb = (idx >> 9) / ks;
+    p_in[idx] = w_in[(32u * kk + 8u * g + e) * C + 16u * nb + j];
+    p_out[idx] = w_out[((C / 4u) * g + 8u * kk + e) * C + oc_bf16(C, nb, j)];
+}
+
 // X fragments of the prologue: per row block, the lane's C/4 channels of its
 // token, as bf16x4 per k step (bf16) or floats (fp32).
 template <typename T, int CB>
@@ -249,7 +279,8 @@ struct XFrag;
 template <int CB>
 struct XFrag<__bf16, CB> {
     using P = Proj<__bf16, CB>;
-    bf16x4 a[P::NRB][P::KS];
+    using Frag = typename std::conditional<P::X32, bf16x8, bf16x4>::type;
+    Frag a[P::NRB][P::X32 ? P::KS2 : P::KS];
 };
 template <int CB>
 struct XFrag<float, CB> {
@@ -286,14 +317,13 @@ __device__ __forceinline__ void load_x_frags(XFrag<T, CB> &f, const T *tile, uin
         if constexpr (P::BF) {
             if constexpr (P::C >= 32) {
 #pragma unroll
-                for (int p = 0; p < P::C / 32; ++p) {
+                for (int p = 0; p < P::C / 32; ++p) {   // channels 32 p + 8 q + [0, 8)
                     u32x4 d = {0u, 0u, 0u, 0u};
                     if (ok)
                         d = __builtin_amdgcn_raw_buffer_load_b128(r, row + 16u * q,
                                                                   rb * rb_bytes + 64u * p,
                                                                   kStreaming);
-                    f.a[rb][2 * p] = __builtin_bit_cast(bf16x4, (u32x2){d.x, d.y});
-                    f.a[rb][2 * p + 1] = __builtin_bit_cast(bf16x4, (u32x2){d.z, d.w});
+                    f.a[rb][p] = __builtin_bit_cast(bf16x8, d);
                 }
             } else {
                 u32x2 d = {0u, 0u};
@@ -330,7 +360,26 @@ __device__ __forceinline__ void project_in(float (&v)[V], const XFrag<T, CB> &f,
 {
     using P = Proj<T, CB>;
     const uint32_t lane = tau & 63u;
-    if constexpr (P::BF) {
+    if constexpr (P::X32) {
+        const bf16x8 *wb = static_cast<const bf16x8 *>(wl);
+#pragma unroll
+        for (int nb = 0; nb < P::NNB; ++nb) {
+            bf16x8 b[P::KS2];
+#pragma unroll
+            for (int kk = 0; kk < P::KS2; ++kk)
+                b[kk] = wb[(nb * P::KS2 + kk) * 64 + lane];
+#pragma unroll
+            for (int rb = 0; rb < P::NRB; ++rb) {
+                f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int kk = 0; kk < P::KS2; ++kk)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[rb][kk], b[kk], acc, 0, 0, 0);
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    v[nb | (r << (CB - 4)) | (rb << (CB - 2))] = acc[r];
+            }
+        }
+    } else if constexpr (P::BF) {
         const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
 #pragma unroll
         for (int nb = 0; nb < P::NNB; ++nb) {
@@ -410,7 +459,52 @@ __device__ __forceinline__ void project_out(const float (&v)[V], const void *wl,
     const uint32_t row = tok0 * (uint32_t)(P::C * sizeof(T));
     constexpr uint32_t rb_bytes = (1u << (M - 7)) * P::C * sizeof(T);
     constexpr int RB_SHIFT = CB - 2;   // register bits of the row block
-    if constexpr (P::BF) {
+    if constexpr (P::X32) {
+        const bf16x8 *wb = static_cast<const bf16x8 *>(wl);
+#pragma unroll
+        for (int rb = 0; rb < P::NRB; ++rb) {
+            // step kk element e: channel q C/4 + 8 kk + e
+            bf16x8 hi[P::KS2], lo[P::KS2];
+#pragma unroll
+            for (int kk = 0; kk < P::KS2; ++kk) {
+                u32x4 h2, l2;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float z0 = v[(8 * kk + 2 * e) | (rb << RB_SHIFT)];
+                    const float z1 = v[(8 * kk + 2 * e + 1) | (rb << RB_SHIFT)];
+                    const float h0 = (float)(__bf16)z0, h1 = (float)(__bf16)z1;
+                    h2[e] = pack2_bf16(z0, z1);
+                    l2[e] = pack2_bf16(z0 - h0, z1 - h1);
+                }
+                hi[kk] = __builtin_bit_cast(bf16x8, h2);
+                lo[kk] = __builtin_bit_cast(bf16x8, l2);
+            }
+            f32x4 acc[P::NNB];
+#pragma unroll
+            for (int nb = 0; nb < P::NNB; ++nb) {
+                acc[nb] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int kk = 0; kk < P::KS2; ++kk) {
+                    const bf16x8 a = wb[(nb * P::KS2 + kk) * 64 + lane];
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi[kk], acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo[kk], acc[nb], 0, 0, 0);
+                }
+            }
+            // the row block's token; MFMAs above run with every lane active
+            const bool ok = whole || (tok0 + ((uint32_t)rb << (M - 7))) * (uint32_t)P::C < valid;
+            // blocks 2n, 2n+1: channels 32 n + 8 q + [0, 8)
+#pragma unroll
+            for (int n = 0; n < P::NNB / 2; ++n) {
+                const u32x4 d = {pack2_bf16(acc[2 * n][0], acc[2 * n][1]),
+                                 pack2_bf16(acc[2 * n][2], acc[2 * n][3]),
+                                 pack2_bf16(acc[2 * n + 1][0], acc[2 * n + 1][1]),
+                                 pack2_bf16(acc[2 * n + 1][2], acc[2 * n + 1][3])};
+                if (ok)
+                    __builtin_amdgcn_raw_buffer_store_b128(d, r, row + 16u * q,
+                                                           rb * rb_bytes + 64u * n, kYPolicy);
+            }
+        }
+    } else if constexpr (P::BF) {
         const bf16x4 *wb = static_cast<const bf16x4 *>(wl);
 #pragma unroll
         for (int rb = 0; rb < P::NRB; ++rb) {
@@ -668,28 +762,12 @@ module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_ou
 // + [0, 8) of row i of A / column i of B), half the instructions of the
 // 16x16x16 form: step kk of the prologue is channels 32 kk + 8 g + [0, 8) (one
 // 16-byte load of x), of the epilogue channels 64 g + 8 kk + [0, 8).
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kPairCB = kPairModuleCbits;
 constexpr uint32_t kPairC = 1u << kPairCB;
 constexpr uint32_t kPairThreads = 1u << (15 - VB);
 constexpr uint32_t kPairKs = kPairC / 32u;                      // k steps
 constexpr uint32_t kPairWChunks = kPairC * kPairC * 2u / 16u;   // 16-byte pieces of W
 
-// One thread per packed element: index ((nb * kPairKs + kk) * 64 + 16 g + j)
-// * 8 + e holds W_in[32 kk + 8 g + e][16 nb + j] (B operand of Z = X W_in) and
-// W_out[64 g + 8 kk + e][oc_bf16(nb, j)] (A operand of Y^T = W_out^T Z'^T).
-__global__ void __launch_bounds__(256)
-pack_pair_weights_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_out,
-                         __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out)
-{
-    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
-    if (idx >= kPairC * kPairC) return;
-    const uint32_t e = idx & 7u, lane = (idx >> 3) & 63u;
-    const uint32_t j = lane & 15u, g = lane >> 4;
-    const uint32_t kk = (idx >> 9) % kPairKs, nb = (idx >> 9) / kPairKs;
-    p_in[idx] = w_in[(32u * kk + 8u * g + e) * kPairC + 16u * nb + j];
-    p_out[idx] = w_out[(64u * g + 8u * kk + e) * kPairC + oc_bf16(kPairC, nb, j)];
-}
 static_assert(kPairC * kPairC * 2u <= pad(1u << 15) * 4u, "W fits the tile's LDS");
 static_assert(kPairWChunks % kPairThreads == 0, "whole prefetch per thread");
 
@@ -1246,11 +1324,12 @@ template <typename T, class Gain>
 hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
 {
     hipError_t e;
-    if (m.cbits == kPairCB) {
-        hipLaunchKernelGGL(pack_pair_weights_kernel, dim3(kPairC * kPairC / 256u), dim3(256), 0,
-                           m.stream, static_cast<const __bf16 *>(m.w_in),
+    if (std::is_same<T, __bf16>::value && m.cbits >= 5) {
+        const uint32_t n = 1u << (2 * m.cbits);
+        hipLaunchKernelGGL(pack_x32_kernel, dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
+                           static_cast<const __bf16 *>(m.w_in),
                            static_cast<const __bf16 *>(m.w_out), static_cast<__bf16 *>(m.wpack),
-                           static_cast<__bf16 *>(m.wpack) + kPairC * kPairC);
+                           static_cast<__bf16 *>(m.wpack) + n, m.cbits);
         e = hipGetLastError();
     } else {
         e = launch_pack<T>(m, false);

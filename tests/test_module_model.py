@@ -104,6 +104,41 @@ def pack(w_in, w_out, bf):
     return p_in, p_out
 
 
+def mfma_bf16_x32(a, b, acc):
+    """16x16x32 (gfx950): a, b [64, 8]; lane 16 g + i supplies row i of A
+    (column i of B) with k = 8 g + e; the result layout is the 16x16x16 one."""
+    A = a.reshape(4, 16, 8).transpose(1, 0, 2).reshape(16, 32)
+    B = b.reshape(4, 16, 8).transpose(0, 2, 1).reshape(32, 16)
+    D = A @ B
+    return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
+
+
+def pack_x32(w_in, w_out):
+    """bf16, C >= 32: operands of the 16x16x32 instruction.  Packed index
+    ((nb * C/32 + kk) * 64 + 16 g + j) * 8 + e holds W_in[32 kk + 8 g + e][16 nb + j]
+    and W_out[(C/4) g + 8 kk + e][oc_bf16(nb, j)]."""
+    C = w_in.shape[0]
+    idx = np.arange(C * C)
+    e, lane, rest = idx & 7, (idx >> 3) & 63, idx >> 9
+    j, g = lane & 15, lane >> 4
+    kk, nb = rest % (C // 32), rest // (C // 32)
+    si = (32 * kk + 8 * g + e) * C + 16 * nb + j
+    so = ((C // 4) * g + 8 * kk + e) * C + np.array([oc_bf16(C, int(n), int(m))
+                                                      for n, m in zip(nb, j)])
+    assert sorted(si) == list(range(C * C)) and sorted(so) == list(range(C * C))
+    return w_in.reshape(-1)[si], w_out.reshape(-1)[so]
+
+
+def x32(C, bf):
+    """The fused kernels' bf16 products take the 16x16x32 instruction from C = 32."""
+    return bf and C >= 32
+
+
+def pack_fused(w_in, w_out, bf):
+    """Packed weights of the fused kernels."""
+    return pack_x32(w_in, w_out) if x32(w_in.shape[0], bf) else pack(w_in, w_out, bf)
+
+
 # ------------------------------------------------------------------ layouts
 class Std:
     def __init__(self, S):
@@ -288,7 +323,14 @@ def model_prologue(xtile, valid, p_in, CB, M, bf):
         for nb in range(NNB):
             for rb in range(NRB):
                 acc = np.zeros((64, 4))
-                if bf:
+                if x32(C, bf):       # step kk: channels 32 kk + 8 q + [0, 8)
+                    for kk in range(C // 32):
+                        cols = 32 * kk + 8 * q[:, None] + np.arange(8)[None, :]
+                        a = rows[rb][lanes[:, None], cols]
+                        idx = ((nb * (C // 32) + kk) * 64 + lanes[:, None]) * 8 + \
+                            np.arange(8)[None, :]
+                        acc = mfma_bf16_x32(a, p_in[idx], acc)
+                elif bf:
                     for kk in range(C // 16):
                         a = np.array([[rows[rb][l, k_in_bf16(C, kk, q[l], r)] for r in range(4)]
                                       for l in range(64)])
@@ -335,7 +377,17 @@ def model_epilogue(v, p_out, CB, M, valid, bf):
             accs = []
             for nb in range(NNB):
                 acc = np.zeros((64, 4))
-                if bf:
+                if x32(C, bf):       # step kk: channels q C/4 + 8 kk + [0, 8)
+                    for kk in range(C // 32):
+                        z = np.stack([vw[:, (8 * kk + e) | (rb << (CB - 2))] for e in range(8)],
+                                     axis=1)
+                        hi, lo = split_bf16(z)
+                        idx = ((nb * (C // 32) + kk) * 64 + lanes[:, None]) * 8 + \
+                            np.arange(8)[None, :]
+                        a = p_out[idx]
+                        acc = mfma_bf16_x32(a, hi, acc)
+                        acc = mfma_bf16_x32(a, lo, acc)
+                elif bf:
                     for kk in range(C // 16):
                         z = np.stack([vw[:, (4 * kk + e) | (rb << (CB - 2))] for e in range(4)],
                                      axis=1)
@@ -390,6 +442,7 @@ def test_packing_is_a_permutation(CB, bf):
     rng = np.random.default_rng(CB)
     w_in, w_out = _weights(rng, 1 << CB)
     pack(w_in, w_out, bf)
+    pack_fused(w_in, w_out, bf)
 
 
 @pytest.mark.parametrize("CB,M,bf", [c for c in CASES if c[1] in (11, 14)])
@@ -398,7 +451,7 @@ def test_prologue_fragments_are_layout_4(CB, M, bf):
     rng = np.random.default_rng(100 * CB + M)
     C = 1 << CB
     w_in, w_out = _weights(rng, C)
-    p_in, _ = pack(w_in, w_out, bf)
+    p_in, _ = pack_fused(w_in, w_out, bf)
     rows = (1 << M) // C
     x = rng.standard_normal((rows, C))
     valid = (rows - 3) * C          # a ragged tile: the last 3 rows are padding
@@ -439,7 +492,7 @@ def test_epilogue_stores_y(CB, M, bf):
     rng = np.random.default_rng(31 * CB + M)
     C = 1 << CB
     w_in, w_out = _weights(rng, C)
-    _, p_out = pack(w_in, w_out, bf)
+    _, p_out = pack_fused(w_in, w_out, bf)
     rows = (1 << M) // C
     z = rng.standard_normal((rows, C))
     valid = (rows - 5) * C
@@ -457,7 +510,7 @@ def _block_tile_model(x, w_in, g, w_out, CB, bf):
     N = x.shape[0]
     P = 1 << (N - 1).bit_length()
     M = (P * C).bit_length() - 1
-    p_in, p_out = pack(w_in, w_out, bf)
+    p_in, p_out = pack_fused(w_in, w_out, bf)
     xt = np.zeros((P, C))
     xt[:N] = x
     v = model_prologue(xt, N * C, p_in, CB, M, bf)
@@ -510,30 +563,6 @@ def mfma_bf16_fast(a, b, acc):
     B = b.reshape(4, 16, 4).transpose(0, 2, 1).reshape(16, 16)
     D = A @ B
     return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
-
-
-def mfma_bf16_x32(a, b, acc):
-    """16x16x32 (gfx950): a, b [64, 8]; lane 16 g + i supplies row i of A
-    (column i of B) with k = 8 g + e; the result layout is the 16x16x16 one."""
-    A = a.reshape(4, 16, 8).transpose(1, 0, 2).reshape(16, 32)
-    B = b.reshape(4, 16, 8).transpose(0, 2, 1).reshape(32, 16)
-    D = A @ B
-    return acc + D.reshape(4, 4, 16).transpose(0, 2, 1).reshape(64, 4)
-
-
-def pack_pair(w_in, w_out):
-    """C = 256 operands of the 16x16x32 instruction: packed index
-    ((nb * 8 + kk) * 64 + 16 g + j) * 8 + e holds W_in[32 kk + 8 g + e][16 nb + j]
-    and W_out[64 g + 8 kk + e][oc_bf16(nb, j)]."""
-    C = w_in.shape[0]
-    idx = np.arange(C * C)
-    e, lane, rest = idx & 7, (idx >> 3) & 63, idx >> 9
-    j, g = lane & 15, lane >> 4
-    kk, nb = rest % (C // 32), rest // (C // 32)
-    si = (32 * kk + 8 * g + e) * C + 16 * nb + j
-    so = (64 * g + 8 * kk + e) * C + np.array([oc_bf16(C, int(n), int(m)) for n, m in zip(nb, j)])
-    assert sorted(si) == list(range(C * C)) and sorted(so) == list(range(C * C))
-    return w_in.reshape(-1)[si], w_out.reshape(-1)[so]
 
 
 def pair_token(m, w):
@@ -626,7 +655,7 @@ def test_pair_prologue_fragments_are_layout_4():
     rng = np.random.default_rng(256)
     w_in, w_out = _weights(rng, PC)
     w_in = round_to_bf16(w_in.astype(np.float32)).astype(np.float64)
-    p_in, _ = pack_pair(w_in, w_out)
+    p_in, _ = pack_x32(w_in, w_out)
     x = round_to_bf16(rng.standard_normal((256, PC)).astype(np.float32)).astype(np.float64)
     valid = (256 - 37) * PC
     v = model_prologue_pair(x, valid, p_in)
@@ -677,7 +706,7 @@ def test_pair_epilogue_stores_y():
     rng = np.random.default_rng(257)
     w_in, w_out = _weights(rng, PC)
     w_out = round_to_bf16(w_out.astype(np.float32)).astype(np.float64)
-    _, p_out = pack_pair(w_in, w_out)
+    _, p_out = pack_x32(w_in, w_out)
     z = rng.standard_normal((256, PC))
     valid = (256 - 11) * PC
     flat = z.reshape(-1)
