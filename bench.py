@@ -293,7 +293,9 @@ def main() -> int:
         nk, names = 2, (["fwd_transforms_gain_gradient", "dx_outer_inv"]
                         if plan["plan"] == "three_pass" else ["gain_gradient", "dx"])
     elif op == "module_backward":
-        nk, names = 3, ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"]
+        nk, names = 3, (["transforms_and_gain_gradient", "z_prime_and_dw_out", "dx_and_dw_in"]
+                        if plan["module_backward_fused"] else
+                        ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"])
     elif op.startswith("module"):
         names = module_kernels(plan["plan"], plan["module_path"])
         nk = len(names)

@@ -115,6 +115,12 @@ typedef struct whtmix_plan_info {
      * exceeds the block's limit. */
     int module_path;
     int module_outer_bits;   /* THREE_PASS: the block's outer-pass bits */
+    /* 1 when whtmix_module_backward runs its projections inside the mixer
+     * backward's passes (given B > 0 and a requested gain gradient); its
+     * events then bracket [transforms of Z and dZ', gain gradient], [Z',
+     * dW_out], [dX, dW_in] instead of [Z, Z', dZ', dW_out], [the mixer's
+     * gradients], [dX, dW_in]. */
+    int module_backward_fused;
 } whtmix_plan_info;
 
 /*

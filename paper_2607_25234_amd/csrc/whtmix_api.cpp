@@ -183,6 +183,7 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
         info->module_path >= 0 && c.plan == whtmix::PLAN_THREE_PASS
             ? whtmix::module_outer_bits(info->module_path, cbits, c.K)
             : 0;
+    info->module_backward_fused = whtmix::module_backward_fused(c.plan, cbits, dtype, c.K) ? 1 : 0;
     return WHTMIX_SUCCESS;
 }
 

@@ -523,22 +523,18 @@ hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay
     return hipGetLastError();
 }
 
-// Both gradients with the three-pass plan, sharing dY's transform:
-//   OUTER_FWD of x and dy (one launch) -> fused middle (dG, and dY's mixer up
-//   to its last pass) -> [chunk sums] -> [separable sums] -> OUTER_INV (dX).
-template <int K, typename T, class Gain>
-hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
-                            Gain gain)
+// The fused middle on the outer transforms in wsx and wsd (dG, and dY's mixer
+// up to its last pass, in place in wsd) -> [chunk sums] -> [separable sums].
+template <int K, class Gain>
+hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
+                             Gain gain)
 {
     constexpr Split sp = three_pass_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
     const hipStream_t st = a.stream;
-    const T *x = static_cast<const T *>(a.x);
-    const T *dy = static_cast<const T *>(a.dy);
-    float *wsx = a.ws + lay.wsx;
+    const float *wsx = a.ws + lay.wsx;
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
-    if ((e = launch_outer_fwd2<K, T>(x, dy, wsx, wsd, a.B, a.nvalid, st)) != hipSuccess) return e;
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     if (lay.per_chunk == 1) {
         hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, true>),
@@ -561,8 +557,42 @@ hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, fl
     if (a.gain_kind == GAIN_LOG_SEPARABLE &&
         (e = separable_reductions(a, lay, dst)) != hipSuccess)
         return e;
+    return hipSuccess;
+}
+
+// Both gradients with the three-pass plan, sharing dY's transform:
+//   OUTER_FWD of x and dy (one launch) -> the fused middle phase -> OUTER_INV (dX).
+template <int K, typename T, class Gain>
+hipError_t fused_three_pass(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
+                            Gain gain)
+{
+    const hipStream_t st = a.stream;
+    float *wsx = a.ws + lay.wsx;
+    float *wsd = a.ws + lay.wsd;
+    hipError_t e = launch_outer_fwd2<K, T>(static_cast<const T *>(a.x),
+                                           static_cast<const T *>(a.dy), wsx, wsd, a.B,
+                                           a.nvalid, st);
+    if (e != hipSuccess) return e;
+    if ((e = grad_middle_phase<K, Gain>(a, lay, dst, gain)) != hipSuccess) return e;
     if ((e = record(a.events[1], st)) != hipSuccess) return e;
     return launch_outer_inv<K, T>(wsd, static_cast<T *>(a.dx), a.B, a.nvalid, st);
+}
+
+template <class Gain>
+hipError_t middle_phase_dispatch(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
+                                 Gain gain)
+{
+    switch (a.K) {
+#define WHTMIX_GM_CASE(k) \
+    case k: return grad_middle_phase<k, Gain>(a, lay, dst, gain);
+        WHTMIX_GM_CASE(12) WHTMIX_GM_CASE(13) WHTMIX_GM_CASE(14) WHTMIX_GM_CASE(15)
+        WHTMIX_GM_CASE(16) WHTMIX_GM_CASE(17) WHTMIX_GM_CASE(18) WHTMIX_GM_CASE(19)
+        WHTMIX_GM_CASE(20) WHTMIX_GM_CASE(21) WHTMIX_GM_CASE(22) WHTMIX_GM_CASE(23)
+        WHTMIX_GM_CASE(24) WHTMIX_GM_CASE(25) WHTMIX_GM_CASE(26) WHTMIX_GM_CASE(27)
+        WHTMIX_GM_CASE(28) WHTMIX_GM_CASE(29) WHTMIX_GM_CASE(30)
+#undef WHTMIX_GM_CASE
+    default: return hipErrorInvalidValue;
+    }
 }
 
 template <typename T, class Gain>
@@ -591,6 +621,20 @@ hipError_t fused_gain(const BackwardArgs &a, const BackwardLayout &lay, float *d
 }
 
 }  // namespace
+
+hipError_t launch_backward_middle(const BackwardArgs &a)
+{
+    const bool separable = a.gain_kind == GAIN_LOG_SEPARABLE;
+    const bool want_dg = separable ? (a.dgt != nullptr && a.dgc != nullptr) : (a.dgain != nullptr);
+    if (!want_dg || a.B < 1 || a.plan != PLAN_THREE_PASS)
+        return hipErrorInvalidValue;
+    const BackwardLayout lay = backward_layout(a.plan, a.K, a.B, int64_t(1) << a.cbits, separable);
+    float *dst = separable ? a.ws + lay.dg : a.dgain;
+    if (separable)
+        return middle_phase_dispatch(a, lay, dst,
+                                     LogSeparableGain{a.gain_t, a.gain_c, (uint32_t)a.cbits});
+    return middle_phase_dispatch(a, lay, dst, FullGain{a.gain});
+}
 
 hipError_t launch_backward(const BackwardArgs &a)
 {

@@ -76,6 +76,12 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
 
 hipError_t launch_backward(const BackwardArgs &a);
 
+// Only the middle phase of the three-pass backward (three_pass_split): a.ws
+// holds backward_layout's wsx and wsd, the outer forward transforms of x and
+// dy made by the caller.  Writes the gain gradient (which must be requested)
+// and leaves dY's mixer up to its last pass in wsd; wsx is read only.
+hipError_t launch_backward_middle(const BackwardArgs &a);
+
 // Enqueues only the middle pass of the block's three-pass plan (module_split,
 // or pair_split when a.pair_outer; a.ws holds the first outer pass's output);
 // a.x, a.y, a.nvalid and a.dtype are not used.

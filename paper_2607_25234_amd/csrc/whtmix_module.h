@@ -104,6 +104,16 @@ inline WgradPlan wgrad_plan(uint64_t rows, int cbits)
     return WgradPlan{(uint32_t)((rows + rpc - 1) / rpc), (uint32_t)rpc};
 }
 
+// The block's backward runs its projections inside the mixer backward's
+// passes (bf16, 32 <= C <= 128, THREE_PASS slices up to 2^25 elements, when a
+// gain gradient is requested); otherwise as projection kernels around the
+// mixer's forward and backward on float32 Z, Z' and dZ'.
+inline bool module_backward_fused(int plan, int cbits, int dtype, int K)
+{
+    return plan == PLAN_THREE_PASS && dtype == DTYPE_BF16 && cbits >= 5 &&
+           cbits <= kModuleMfmaMaxCbits && K >= 12 && K <= 25;
+}
+
 // A validated backward call of the block.  Workspace pieces (floats unless
 // noted): z, zp, dzp [B*N*C] (Z = X W_in, Z' = mixer(Z), dZ' then dZ);
 // wpack: W_in, W_out^T and W_in^T packed (3*C*C elements of the dtype);
@@ -132,8 +142,10 @@ struct ModuleBackwardArgs {
     int dtype;
     int plan;               // the mixer's plan for [B, N, C]
     hipStream_t stream;
-    hipEvent_t events[4];   // [0] before, [1] after Z, Z', dZ', dW_out, [2] after the
-                            // mixer's gradient, [3] after dX and dW_in
+    hipEvent_t events[4];   // [0] before; then after each phase: unfused, [1] Z, Z',
+                            // dZ', dW_out, [2] the mixer's gradient, [3] dX and dW_in;
+                            // fused, [1] the transforms of Z and dZ' and dG, [2] Z'
+                            // and dW_out, [3] dX and dW_in
     float *z;
     float *zp;
     float *dzp;

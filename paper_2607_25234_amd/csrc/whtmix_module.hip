@@ -255,10 +255,11 @@ pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *
 // W_in[32 kk + 8 g + e][16 nb + j] (B operand of Z = X W_in: step kk of lane
 // group g is channels 32 kk + 8 g + [0, 8) of x, one 16-byte load) and
 // W_out[(C/4) g + 8 kk + e][oc_bf16(C, nb, j)] (A operand of Y^T = W_out^T Z'^T:
-// lane group g holds channels [g C/4, (g+1) C/4) of Z').
+// lane group g holds channels [g C/4, (g+1) C/4) of Z').  out_t_as_in: p_out is
+// instead W_out^T in p_in's order (the prologue operand of dZ' = dY W_out^T).
 __global__ void __launch_bounds__(256)
 pack_x32_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_out,
-                __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out, int cb)
+                __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out, int cb, int out_t_as_in)
 {
     const uint32_t C = 1u << cb;
     const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
@@ -268,7 +269,8 @@ pack_x32_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_ou
     const uint32_t ks = C / 32u;
     const uint32_t kk = (idx >> 9) % ks, nb = (idx >> 9) / ks;
     p_in[idx] = w_in[(32u * kk + 8u * g + e) * C + 16u * nb + j];
-    p_out[idx] = w_out[((C / 4u) * g + 8u * kk + e) * C + oc_bf16(C, nb, j)];
+    p_out[idx] = out_t_as_in ? w_out[(16u * nb + j) * C + 32u * kk + 8u * g + e]
+                             : w_out[((C / 4u) * g + 8u * kk + e) * C + oc_bf16(C, nb, j)];
 }
 
 // X fragments of the prologue: per row block, the lane's C/4 channels of its
@@ -674,15 +676,14 @@ module_fused_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
 
 // THREE_PASS first pass: prologue, forward over the A low bits, workspace.
 template <int A, int HB, int R, typename T, int CB>
-__global__ void __launch_bounds__(1 << (A - VB))
-module_outer_fwd_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
-                        float *__restrict__ ws, uint32_t nvalid)
+__device__ __forceinline__ void module_outer_fwd_tile(float *lds, const T *__restrict__ x,
+                                                      const T *__restrict__ w_in,
+                                                      float *__restrict__ ws, uint32_t nvalid,
+                                                      uint32_t blk)
 {
     using L = Lds<A, T, CB>;
     using Run = RunMap<HB, R>;
-    __shared__ __attribute__((aligned(16))) float lds[L::fwd_bytes() / 4];
     const uint32_t tau = threadIdx.x;
-    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const uint32_t valid = tile_valid<A>(nvalid, hi);
@@ -695,6 +696,33 @@ module_outer_fwd_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
     forward_from_prologue<A>(lds, v, tau);
     store_layout<A - 5, Run, float>(
         v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
+}
+
+template <int A, int HB, int R, typename T, int CB>
+__global__ void __launch_bounds__(1 << (A - VB))
+module_outer_fwd_kernel(const T *__restrict__ x, const T *__restrict__ w_in,
+                        float *__restrict__ ws, uint32_t nvalid)
+{
+    __shared__ __attribute__((aligned(16))) float lds[Lds<A, T, CB>::fwd_bytes() / 4];
+    module_outer_fwd_tile<A, HB, R, T, CB>(lds, x, w_in, ws, nvalid,
+                                           outer_block<R>(blockIdx.x, gridDim.x));
+}
+
+// Two operands in one launch (the block's backward: Z = X W_in and
+// dZ' = dY W_out^T): the first half of the grid takes (x, wa) into wsx, the
+// second (dy, wb) into wsd, each half numbered as a grid of its own.
+template <int A, int HB, int R, typename T, int CB>
+__global__ void __launch_bounds__(1 << (A - VB))
+module_outer_fwd2_kernel(const T *__restrict__ x, const T *__restrict__ wa,
+                         const T *__restrict__ dy, const T *__restrict__ wb,
+                         float *__restrict__ wsx, float *__restrict__ wsd, uint32_t nvalid)
+{
+    __shared__ __attribute__((aligned(16))) float lds[Lds<A, T, CB>::fwd_bytes() / 4];
+    const uint32_t half = gridDim.x >> 1;
+    const bool second = blockIdx.x >= half;
+    const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
+    module_outer_fwd_tile<A, HB, R, T, CB>(lds, second ? dy : x, second ? wb : wa,
+                                           second ? wsd : wsx, nvalid, blk);
 }
 
 // THREE_PASS last pass: inverse over the A low bits, epilogue, y.
@@ -1329,7 +1357,7 @@ hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
         hipLaunchKernelGGL(pack_x32_kernel, dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
                            static_cast<const __bf16 *>(m.w_in),
                            static_cast<const __bf16 *>(m.w_out), static_cast<__bf16 *>(m.wpack),
-                           static_cast<__bf16 *>(m.wpack) + n, m.cbits);
+                           static_cast<__bf16 *>(m.wpack) + n, m.cbits, 0);
         e = hipGetLastError();
     } else {
         e = launch_pack<T>(m, false);
@@ -1833,9 +1861,115 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
     return hipGetLastError();
 }
 
+// The block's backward with its projections fused into the mixer backward's
+// passes (module_backward_fused decides when):
+//   OUTER_FWD of Z = X W_in and dZ' = dY W_out^T, matrix-core prologues, one
+//   launch -> the backward's middle phase: dG, and dZ' through the gain up to
+//   its last pass in wsd (wsx, the transform of Z, is only read)      [1]
+//   -> the forward middle on wsx, OUTER_INV -> Z' (float32); dW_out = Z'^T dY [2]
+//   -> OUTER_INV of wsd -> dZ (float32); dX = dZ W_in^T; dW_in = X^T dZ    [3]
+// Z and dZ' never reach memory: they exist only as the outer transforms.
+template <int K, int CB>
+hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
+{
+    constexpr Split sp = module_split(K);
+    constexpr int A = sp.A, HB = sp.HB, R = sp.R;
+    static_assert(A == three_pass_split(K).A && R == three_pass_split(K).R,
+                  "the backward's middle phase runs the mixer's split");
+    using T = __bf16;
+    const hipStream_t st = m.stream;
+    const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> CB);
+    const uint32_t CC = 1u << (2 * CB);
+    const T *x = static_cast<const T *>(m.x);
+    const T *dy = static_cast<const T *>(m.dy);
+    const T *w_in = static_cast<const T *>(m.w_in);
+    T *pk = static_cast<T *>(m.wpack);
+    T *p_in = pk, *p_out_t = pk + CC, *p_in_t = pk + 2 * CC;
+    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in,
+                       static_cast<const T *>(m.w_out), p_in, p_out_t, CB, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = launch_pack_b<T>(w_in, p_in_t, CB, true, st)) != hipSuccess) return e;
+    if ((e = record(m.events[0], st)) != hipSuccess) return e;
+    const bool separable = m.gain_kind == GAIN_LOG_SEPARABLE;
+    const BackwardLayout lay =
+        backward_layout(PLAN_THREE_PASS, K, m.B, int64_t(1) << CB, separable);
+    float *wsx = m.bwd_ws + lay.wsx;
+    float *wsd = m.bwd_ws + lay.wsd;
+    hipLaunchKernelGGL((module_outer_fwd2_kernel<A, HB, R, T, CB>),
+                       dim3((uint32_t)(2 * (m.B << HB))), dim3(1u << (A - VB)), 0, st, x, p_in,
+                       dy, p_out_t, wsx, wsd, m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    BackwardArgs g{};
+    g.gain_kind = m.gain_kind;
+    g.gain = m.gain;
+    g.gain_t = m.gain_t;
+    g.gain_c = m.gain_c;
+    g.dgain = m.dgain;
+    g.dgt = m.dgt;
+    g.dgc = m.dgc;
+    g.cbits = CB;
+    g.ws = m.bwd_ws;
+    g.B = m.B;
+    g.K = K;
+    g.nvalid = m.nvalid;
+    g.dtype = DTYPE_F32;
+    g.plan = PLAN_THREE_PASS;
+    g.stream = st;
+    if ((e = launch_backward_middle(g)) != hipSuccess) return e;
+    if ((e = record(m.events[1], st)) != hipSuccess) return e;
+    LaunchArgs f{};
+    f.gain_kind = m.gain_kind;
+    f.gain = m.gain;
+    f.gain_t = m.gain_t;
+    f.gain_c = m.gain_c;
+    f.cbits = CB;
+    f.ws = wsx;
+    f.B = m.B;
+    f.K = K;
+    f.plan = PLAN_THREE_PASS;
+    f.stream = st;
+    if ((e = launch_middle(f)) != hipSuccess) return e;
+    if ((e = launch_outer_inv<K, float>(wsx, m.zp, m.B, m.nvalid, st)) != hipSuccess) return e;
+    if ((e = wgrad<float, T>(m.zp, dy, m.wpart, m.dw_out, rows, CB, st)) != hipSuccess) return e;
+    if ((e = record(m.events[2], st)) != hipSuccess) return e;
+    if ((e = launch_outer_inv<K, float>(wsd, m.dzp, m.B, m.nvalid, st)) != hipSuccess) return e;
+    if ((e = project<float, T, T, true>(m.dzp, p_in_t, w_in, static_cast<T *>(m.dx), rows, CB,
+                                        st)) != hipSuccess)
+        return e;
+    if ((e = wgrad<T, float>(x, m.dzp, m.wpart, m.dw_in, rows, CB, st)) != hipSuccess) return e;
+    return record(m.events[3], st);
+}
+
+template <int CB>
+hipError_t module_backward_fused_cb(const ModuleBackwardArgs &m)
+{
+    switch (m.K) {
+#define WHTMIX_MB_CASE(k) \
+    case k: return module_backward_fused_k<k, CB>(m);
+        WHTMIX_MB_CASE(12) WHTMIX_MB_CASE(13) WHTMIX_MB_CASE(14) WHTMIX_MB_CASE(15)
+        WHTMIX_MB_CASE(16) WHTMIX_MB_CASE(17) WHTMIX_MB_CASE(18) WHTMIX_MB_CASE(19)
+        WHTMIX_MB_CASE(20) WHTMIX_MB_CASE(21) WHTMIX_MB_CASE(22) WHTMIX_MB_CASE(23)
+        WHTMIX_MB_CASE(24) WHTMIX_MB_CASE(25)
+#undef WHTMIX_MB_CASE
+    default: return hipErrorInvalidValue;
+    }
+}
+
 template <typename T>
 hipError_t module_backward(const ModuleBackwardArgs &m)
 {
+    const bool want_dg = m.gain_kind == GAIN_LOG_SEPARABLE ? (m.dgt != nullptr)
+                                                           : (m.dgain != nullptr);
+    if (want_dg && m.B > 0 && ((uint64_t)m.B << m.K) / 16u <= 0xffffffffull &&
+        module_backward_fused(m.plan, m.cbits, m.dtype, m.K)) {
+        switch (m.cbits) {
+        case 5: return module_backward_fused_cb<5>(m);
+        case 6: return module_backward_fused_cb<6>(m);
+        case 7: return module_backward_fused_cb<7>(m);
+        default: break;
+        }
+    }
     const hipStream_t st = m.stream;
     const int cb = m.cbits;
     const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> cb);

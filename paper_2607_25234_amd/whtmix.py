@@ -58,7 +58,7 @@ class PlanInfo(ctypes.Structure):
                 ("log2_slice", ctypes.c_int), ("outer_bits", ctypes.c_int),
                 ("run_bits", ctypes.c_int), ("workspace_bytes", ctypes.c_int64),
                 ("padded_tokens", ctypes.c_int64), ("module_path", ctypes.c_int),
-                ("module_outer_bits", ctypes.c_int)]
+                ("module_outer_bits", ctypes.c_int), ("module_backward_fused", ctypes.c_int)]
 
 
 _lib = None
@@ -150,7 +150,8 @@ def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = 
             "run_bits": info.run_bits, "workspace_bytes": info.workspace_bytes,
             "padded_tokens": info.padded_tokens,
             "module_path": MODULE_PATHS.get(info.module_path),
-            "module_outer_bits": info.module_outer_bits}
+            "module_outer_bits": info.module_outer_bits,
+            "module_backward_fused": bool(info.module_backward_fused)}
 
 
 def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,

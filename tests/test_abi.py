@@ -275,6 +275,19 @@ def test_block_paths():
     assert whtmix.plan_describe(1, 4, 8192)["module_path"] is None      # C above the limit
 
 
+def test_block_backward_paths():
+    """The block's backward fuses its projections for bf16 32 <= C <= 128 on
+    three-pass slices up to 2^25 elements."""
+    fused = lambda *a: whtmix.plan_describe(*a)["module_backward_fused"]
+    assert fused(4, 65536, 128, "bf16")
+    assert fused(1, 3000, 32, "bf16") and fused(2, 128, 128, "bf16", "three_pass")
+    assert not fused(4, 65536, 128, "f32")              # float32
+    assert not fused(1, 65536, 16, "bf16")              # C = 16: VALU-sized products
+    assert not fused(1, 262144, 256, "bf16")            # C = 256
+    assert not fused(1, 256, 64, "bf16")                # FUSED plan
+    assert not fused(1, 1 << 19, 128, "bf16")           # 2^26 elements
+
+
 def test_every_three_pass_split_fits_the_tiles():
     for K in range(12, 31):
         N = 1 << (K // 2)

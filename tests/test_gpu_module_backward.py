@@ -75,6 +75,8 @@ SHAPES = [
     # FUSED and THREE_PASS mixers; padded token counts
     (2, 3, 4), (3, 50, 8), (2, 64, 16), (1, 100, 32), (2, 64, 64), (2, 512, 128),
     (1, 3000, 32), (2, 2048, 64), (1, 1024, 128), (1, 64, 256), (2, 300, 256),
+    # bf16 32 <= C <= 128 three-pass: projections inside the backward's passes
+    (3, 5000, 64), (2, 20000, 32),
 ]
 
 
