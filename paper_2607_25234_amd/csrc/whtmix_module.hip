@@ -255,22 +255,35 @@ pack_weights_kernel(const T *__restrict__ w_in, const T *__restrict__ w_out, T *
 // W_in[32 kk + 8 g + e][16 nb + j] (B operand of Z = X W_in: step kk of lane
 // group g is channels 32 kk + 8 g + [0, 8) of x, one 16-byte load) and
 // W_out[(C/4) g + 8 kk + e][oc_bf16(C, nb, j)] (A operand of Y^T = W_out^T Z'^T:
-// lane group g holds channels [g C/4, (g+1) C/4) of Z').  out_t_as_in: p_out is
-// instead W_out^T in p_in's order (the prologue operand of dZ' = dY W_out^T).
-__global__ void __launch_bounds__(256)
-pack_x32_kernel(const __bf16 *__restrict__ w_in, const __bf16 *__restrict__ w_out,
-                __bf16 *__restrict__ p_in, __bf16 *__restrict__ p_out, int cb, int out_t_as_in)
+// lane group g holds channels [g C/4, (g+1) C/4) of Z').  The block's backward
+// packs transposed matrices in the same orders (dZ' = dY W_out^T through the
+// prologue, dX = dZ W_in^T through the epilogue).
+enum PackMode { PACK_PROLOGUE = 0, PACK_EPILOGUE = 1, PACK_PROLOGUE_T = 2, PACK_EPILOGUE_T = 3 };
+
+__device__ __forceinline__ uint32_t pack_x32_source(uint32_t idx, uint32_t C, int mode)
 {
-    const uint32_t C = 1u << cb;
-    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
-    if (idx >= C * C) return;
     const uint32_t e = idx & 7u, lane = (idx >> 3) & 63u;
     const uint32_t j = lane & 15u, g = lane >> 4;
     const uint32_t ks = C / 32u;
     const uint32_t kk = (idx >> 9) % ks, nb = (idx >> 9) / ks;
-    p_in[idx] = w_in[(32u * kk + 8u * g + e) * C + 16u * nb + j];
-    p_out[idx] = out_t_as_in ? w_out[(16u * nb + j) * C + 32u * kk + 8u * g + e]
-                             : w_out[((C / 4u) * g + 8u * kk + e) * C + oc_bf16(C, nb, j)];
+    // (k, column) of the operand, then the element of W (or of W^T)
+    const bool pro = mode == PACK_PROLOGUE || mode == PACK_PROLOGUE_T;
+    const uint32_t k = pro ? 32u * kk + 8u * g + e : (C / 4u) * g + 8u * kk + e;
+    const uint32_t col = pro ? 16u * nb + j : oc_bf16(C, nb, j);
+    return mode >= PACK_PROLOGUE_T ? col * C + k : k * C + col;
+}
+
+// pa = wa packed in mode_a; pb = wb in mode_b unless pb is null.
+__global__ void __launch_bounds__(256)
+pack_x32_kernel(const __bf16 *__restrict__ wa, __bf16 *__restrict__ pa, int mode_a,
+                const __bf16 *__restrict__ wb, __bf16 *__restrict__ pb, int mode_b, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= C * C) return;
+    pa[idx] = wa[pack_x32_source(idx, C, mode_a)];
+    if (pb)
+        pb[idx] = wb[pack_x32_source(idx, C, mode_b)];
 }
 
 // X fragments of the prologue: per row block, the lane's C/4 channels of its
@@ -584,6 +597,35 @@ __device__ __forceinline__ void project_out(const float (&v)[V], const void *wl,
     }
 }
 
+// Stores Z' itself (float32, row-major like y) from the epilogue layout of a
+// 2^M tile: lane (j, q) of wave w holds channels q C/4 + [0, C/4) of tokens
+// j | w << 4 | rb << (M-7); rows past `valid` are not stored.
+template <int CB, int M>
+__device__ __forceinline__ void store_epilogue_f32(const float (&v)[V], float *tile,
+                                                   uint32_t valid, uint32_t tau)
+{
+    constexpr uint32_t C = 1u << CB;
+    constexpr int NRB = 1 << (7 - CB), RB_SHIFT = CB - 2;
+    const uint32_t lane = tau & 63u, w = tau >> 6;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 4u);
+    const bool whole = valid >= (1u << M);
+    const uint32_t tok0 = j | (w << 4);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+        const uint32_t tok = tok0 + ((uint32_t)rb << (M - 7));
+        const bool ok = whole || tok * C < valid;
+#pragma unroll
+        for (uint32_t s4 = 0; s4 < C / 16u; ++s4) {
+            const f32x4 d = {v[(4 * s4) | (rb << RB_SHIFT)], v[(4 * s4 + 1) | (rb << RB_SHIFT)],
+                             v[(4 * s4 + 2) | (rb << RB_SHIFT)], v[(4 * s4 + 3) | (rb << RB_SHIFT)]};
+            if (ok)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, d), r,
+                                                       tok * C * 4u + q * C, 16u * s4, kTemporal);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- LDS plan
 // The tile's exchanges use pad(2^M) floats.  The prologue's weights share
 // that space (they are dead before the first exchange).  The epilogue's
@@ -725,11 +767,12 @@ module_outer_fwd2_kernel(const T *__restrict__ x, const T *__restrict__ wa,
                                            second ? wsd : wsx, nvalid, blk);
 }
 
-// THREE_PASS last pass: inverse over the A low bits, epilogue, y.
-template <int A, int HB, int R, typename T, int CB>
+// THREE_PASS last pass: inverse over the A low bits, epilogue, y.  ZOUT: also
+// store the inverse-transformed tile itself (float32) to z.
+template <int A, int HB, int R, typename T, int CB, bool ZOUT = false>
 __global__ void __launch_bounds__(1 << (A - VB))
 module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_out,
-                        T *__restrict__ y, uint32_t nvalid)
+                        T *__restrict__ y, float *__restrict__ z, uint32_t nvalid)
 {
     using L = Lds<A, T, CB>;
     using Run = RunMap<HB, R>;
@@ -754,6 +797,8 @@ module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_ou
     load_layout<A - 5, Run, float>(
         v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
     inverse_to_epilogue<A, CB, false>(lds, v, tau);
+    if constexpr (ZOUT)
+        store_epilogue_f32<CB, A>(v, z + b * nvalid + ((size_t)hi << A), valid, tau);
     const void *wl = wregion;
     if constexpr (!L::SEPARATE) {
         __syncthreads();
@@ -1279,7 +1324,7 @@ hipError_t launch_module_three_pass(const ModuleArgs &m, Gain gain)
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
     hipLaunchKernelGGL((module_outer_inv_kernel<A, HB, R, T, CB>), dim3((uint32_t)(m.B << HB)),
                        dim3(1u << (A - VB)), 0, st, m.ws, pin + n, static_cast<T *>(m.y),
-                       m.nvalid);
+                       nullptr, m.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return record(m.events[3], st);
 }
@@ -1355,9 +1400,9 @@ hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
     if (std::is_same<T, __bf16>::value && m.cbits >= 5) {
         const uint32_t n = 1u << (2 * m.cbits);
         hipLaunchKernelGGL(pack_x32_kernel, dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
-                           static_cast<const __bf16 *>(m.w_in),
-                           static_cast<const __bf16 *>(m.w_out), static_cast<__bf16 *>(m.wpack),
-                           static_cast<__bf16 *>(m.wpack) + n, m.cbits, 0);
+                           static_cast<const __bf16 *>(m.w_in), static_cast<__bf16 *>(m.wpack),
+                           (int)PACK_PROLOGUE, static_cast<const __bf16 *>(m.w_out),
+                           static_cast<__bf16 *>(m.wpack) + n, (int)PACK_EPILOGUE, m.cbits);
         e = hipGetLastError();
     } else {
         e = launch_pack<T>(m, false);
@@ -1867,7 +1912,8 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
 //   launch -> the backward's middle phase: dG, and dZ' through the gain up to
 //   its last pass in wsd (wsx, the transform of Z, is only read)      [1]
 //   -> the forward middle on wsx, OUTER_INV -> Z' (float32); dW_out = Z'^T dY [2]
-//   -> OUTER_INV of wsd -> dZ (float32); dX = dZ W_in^T; dW_in = X^T dZ    [3]
+//   -> OUTER_INV of wsd with the epilogue: dZ (float32) and dX = dZ W_in^T;
+//      dW_in = X^T dZ                                                     [3]
 // Z and dZ' never reach memory: they exist only as the outer transforms.
 template <int K, int CB>
 hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
@@ -1884,12 +1930,16 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     const T *dy = static_cast<const T *>(m.dy);
     const T *w_in = static_cast<const T *>(m.w_in);
     T *pk = static_cast<T *>(m.wpack);
-    T *p_in = pk, *p_out_t = pk + CC, *p_in_t = pk + 2 * CC;
-    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in,
-                       static_cast<const T *>(m.w_out), p_in, p_out_t, CB, 1);
+    T *p_in = pk, *p_out_t = pk + CC, *p_in_te = pk + 2 * CC;
+    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in, p_in,
+                       (int)PACK_PROLOGUE, static_cast<const T *>(m.w_out), p_out_t,
+                       (int)PACK_PROLOGUE_T, CB);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = launch_pack_b<T>(w_in, p_in_t, CB, true, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in,
+                       p_in_te, (int)PACK_EPILOGUE_T, static_cast<const T *>(nullptr),
+                       static_cast<T *>(nullptr), 0, CB);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = record(m.events[0], st)) != hipSuccess) return e;
     const bool separable = m.gain_kind == GAIN_LOG_SEPARABLE;
     const BackwardLayout lay =
@@ -1933,10 +1983,11 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     if ((e = launch_outer_inv<K, float>(wsx, m.zp, m.B, m.nvalid, st)) != hipSuccess) return e;
     if ((e = wgrad<float, T>(m.zp, dy, m.wpart, m.dw_out, rows, CB, st)) != hipSuccess) return e;
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
-    if ((e = launch_outer_inv<K, float>(wsd, m.dzp, m.B, m.nvalid, st)) != hipSuccess) return e;
-    if ((e = project<float, T, T, true>(m.dzp, p_in_t, w_in, static_cast<T *>(m.dx), rows, CB,
-                                        st)) != hipSuccess)
-        return e;
+    // dZ (float32, for dW_in) and dX = dZ W_in^T from one pass over wsd
+    hipLaunchKernelGGL((module_outer_inv_kernel<A, HB, R, T, CB, true>),
+                       dim3((uint32_t)(m.B << HB)), dim3(1u << (A - VB)), 0, st, wsd, p_in_te,
+                       static_cast<T *>(m.dx), m.dzp, m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = wgrad<T, float>(x, m.dzp, m.wpart, m.dw_in, rows, CB, st)) != hipSuccess) return e;
     return record(m.events[3], st);
 }
