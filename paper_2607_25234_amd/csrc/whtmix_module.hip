@@ -598,32 +598,27 @@ __device__ __forceinline__ void project_out(const float (&v)[V], const void *wl,
 }
 
 // Stores Z' itself (float32, row-major like y) from the epilogue layout of a
-// 2^M tile: lane (j, q) of wave w holds channels q C/4 + [0, C/4) of tokens
-// j | w << 4 | rb << (M-7); rows past `valid` are not stored.
-template <int CB, int M>
-__device__ __forceinline__ void store_epilogue_f32(const float (&v)[V], float *tile,
+// 2^M tile, through LDS into layout M-5, whose registers each cover 2^(M-5)
+// consecutive elements (the epilogue layout's own stores would write 16 bytes
+// to each of 64 lines per instruction).  Waits for earlier readers of the
+// LDS first; the caller synchronises before the LDS is written again.
+template <int M, int CB>
+__device__ __forceinline__ void store_epilogue_f32(float *lds, const float (&v)[V], float *tile,
                                                    uint32_t valid, uint32_t tau)
 {
-    constexpr uint32_t C = 1u << CB;
-    constexpr int NRB = 1 << (7 - CB), RB_SHIFT = CB - 2;
-    const uint32_t lane = tau & 63u, w = tau >> 6;
-    const uint32_t j = lane & 15u, q = lane >> 4;
-    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 4u);
-    const bool whole = valid >= (1u << M);
-    const uint32_t tok0 = j | (w << 4);
+    using E = Epi<M, CB>;
+    const uint32_t pe = pad(E::base(tau));
+    __syncthreads();
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) {
-        const uint32_t tok = tok0 + ((uint32_t)rb << (M - 7));
-        const bool ok = whole || tok * C < valid;
+    for (int k = 0; k < V; ++k)
+        lds[pe + pad(reg_offset<E>((uint32_t)k))] = v[k];
+    __syncthreads();
+    float u[V];
+    const uint32_t ps = pad(layout_base<M - 5>(tau));
 #pragma unroll
-        for (uint32_t s4 = 0; s4 < C / 16u; ++s4) {
-            const f32x4 d = {v[(4 * s4) | (rb << RB_SHIFT)], v[(4 * s4 + 1) | (rb << RB_SHIFT)],
-                             v[(4 * s4 + 2) | (rb << RB_SHIFT)], v[(4 * s4 + 3) | (rb << RB_SHIFT)]};
-            if (ok)
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, d), r,
-                                                       tok * C * 4u + q * C, 16u * s4, kTemporal);
-        }
-    }
+    for (int k = 0; k < V; ++k)
+        u[k] = lds[ps + pad((uint32_t)k << (M - 5))];
+    store_tile<M - 5, M, float>(u, tile, valid, tau);
 }
 
 // ---------------------------------------------------------------- LDS plan
@@ -798,7 +793,7 @@ module_outer_inv_kernel(const float *__restrict__ ws, const T *__restrict__ w_ou
         v, buffer(ws + (b << (A + HB)) + ((size_t)hi << R), extent_bytes<Run, A, float>()), tau);
     inverse_to_epilogue<A, CB, false>(lds, v, tau);
     if constexpr (ZOUT)
-        store_epilogue_f32<CB, A>(v, z + b * nvalid + ((size_t)hi << A), valid, tau);
+        store_epilogue_f32<A, CB>(lds, v, z + b * nvalid + ((size_t)hi << A), valid, tau);
     const void *wl = wregion;
     if constexpr (!L::SEPARATE) {
         __syncthreads();
