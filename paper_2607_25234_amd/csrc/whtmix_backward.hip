@@ -84,9 +84,13 @@ grad_middle_kernel(const float *__restrict__ wsx, const float *__restrict__ wsd,
 // slice per chunk (SINGLE) the product is stored as soon as it is formed and
 // the gain is read after it, when x's tile is dead; 2^15-element tiles (1024
 // threads, at most 128 registers) always take this form.
-template <int A, int HB, int R, class Gain, bool SINGLE>
+//
+// MIX_X: x's tile also goes through the gain and the inverse and is stored
+// back to wsx (the forward mixer's middle pass on x, for the block's backward,
+// which needs Z' as well), after the product and before the next slice's load.
+template <int A, int HB, int R, class Gain, bool SINGLE, bool MIX_X = false>
 __global__ void __launch_bounds__(1 << (HB + R - VB))
-grad_mix_middle_kernel(const float *__restrict__ wsx, float *__restrict__ wsd, Gain gain,
+grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain gain,
                        float *__restrict__ out, uint32_t nslices, uint32_t per_chunk)
 {
     constexpr int M = HB + R;
@@ -118,6 +122,13 @@ grad_mix_middle_kernel(const float *__restrict__ wsx, float *__restrict__ wsd, G
         __builtin_amdgcn_sched_barrier(0);   // keep the gain loads after the product
         float gv[V];
         gain.template load<G::SL, GM>(gv, run << R, tau);
+        if constexpr (MIX_X) {
+            apply_gain<A + HB>(vx, gv);
+            if constexpr (G::NBOT > 0)
+                inverse_groups<M, R, G::NBOT - 1>(lds, vx, tau);
+            butterflies<G::JT, VB>(vx);
+            store_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b0), tau);
+        }
         apply_gain<A + HB>(vd, gv);
         if constexpr (G::NBOT > 0)
             inverse_groups<M, R, G::NBOT - 1>(lds, vd, tau);
@@ -138,6 +149,13 @@ grad_mix_middle_kernel(const float *__restrict__ wsx, float *__restrict__ wsd, G
 #pragma unroll
             for (int k = 0; k < V; ++k)
                 acc[k] = fmaf(vx[k], vd[k], acc[k]);
+            if constexpr (MIX_X) {
+                apply_gain<A + HB>(vx, gv);
+                if constexpr (G::NBOT > 0)
+                    inverse_groups<M, R, G::NBOT - 1>(lds, vx, tau);
+                butterflies<G::JT, VB>(vx);
+                store_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b), tau);
+            }
             if (more)
                 load_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b + 1), tau);
             apply_gain<A + HB>(vd, gv);
@@ -525,23 +543,23 @@ hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay
 
 // The fused middle on the outer transforms in wsx and wsd (dG, and dY's mixer
 // up to its last pass, in place in wsd) -> [chunk sums] -> [separable sums].
-template <int K, class Gain>
+template <int K, class Gain, bool MIX_X = false>
 hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, float *dst,
                              Gain gain)
 {
     constexpr Split sp = three_pass_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
     const hipStream_t st = a.stream;
-    const float *wsx = a.ws + lay.wsx;
+    float *wsx = a.ws + lay.wsx;
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     if (lay.per_chunk == 1) {
-        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, true>),
+        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, true, MIX_X>),
                            dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,
                            wsd, gain, o, (uint32_t)a.B, 1u);
     } else if constexpr (HB + R < kMaxTile) {
-        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false>),
+        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false, MIX_X>),
                            dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,
                            wsd, gain, o, (uint32_t)a.B, lay.per_chunk);
     } else {
@@ -584,12 +602,11 @@ hipError_t middle_phase_dispatch(const BackwardArgs &a, const BackwardLayout &la
 {
     switch (a.K) {
 #define WHTMIX_GM_CASE(k) \
-    case k: return grad_middle_phase<k, Gain>(a, lay, dst, gain);
+    case k: return grad_middle_phase<k, Gain, true>(a, lay, dst, gain);
         WHTMIX_GM_CASE(12) WHTMIX_GM_CASE(13) WHTMIX_GM_CASE(14) WHTMIX_GM_CASE(15)
         WHTMIX_GM_CASE(16) WHTMIX_GM_CASE(17) WHTMIX_GM_CASE(18) WHTMIX_GM_CASE(19)
         WHTMIX_GM_CASE(20) WHTMIX_GM_CASE(21) WHTMIX_GM_CASE(22) WHTMIX_GM_CASE(23)
-        WHTMIX_GM_CASE(24) WHTMIX_GM_CASE(25) WHTMIX_GM_CASE(26) WHTMIX_GM_CASE(27)
-        WHTMIX_GM_CASE(28) WHTMIX_GM_CASE(29) WHTMIX_GM_CASE(30)
+        WHTMIX_GM_CASE(24) WHTMIX_GM_CASE(25)
 #undef WHTMIX_GM_CASE
     default: return hipErrorInvalidValue;
     }

@@ -1904,9 +1904,9 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
 // The block's backward with its projections fused into the mixer backward's
 // passes (module_backward_fused decides when):
 //   OUTER_FWD of Z = X W_in and dZ' = dY W_out^T, matrix-core prologues, one
-//   launch -> the backward's middle phase: dG, and dZ' through the gain up to
-//   its last pass in wsd (wsx, the transform of Z, is only read)      [1]
-//   -> the forward middle on wsx, OUTER_INV -> Z' (float32); dW_out = Z'^T dY [2]
+//   launch -> the backward's middle phase: dG, and both Z and dZ' through the
+//   gain up to their last pass, in place in wsx and wsd                 [1]
+//   -> OUTER_INV of wsx -> Z' (float32); dW_out = Z'^T dY                 [2]
 //   -> OUTER_INV of wsd with the epilogue: dZ (float32) and dX = dZ W_in^T;
 //      dW_in = X^T dZ                                                     [3]
 // Z and dZ' never reach memory: they exist only as the outer transforms.
@@ -1963,18 +1963,6 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     g.stream = st;
     if ((e = launch_backward_middle(g)) != hipSuccess) return e;
     if ((e = record(m.events[1], st)) != hipSuccess) return e;
-    LaunchArgs f{};
-    f.gain_kind = m.gain_kind;
-    f.gain = m.gain;
-    f.gain_t = m.gain_t;
-    f.gain_c = m.gain_c;
-    f.cbits = CB;
-    f.ws = wsx;
-    f.B = m.B;
-    f.K = K;
-    f.plan = PLAN_THREE_PASS;
-    f.stream = st;
-    if ((e = launch_middle(f)) != hipSuccess) return e;
     if ((e = launch_outer_inv<K, float>(wsx, m.zp, m.B, m.nvalid, st)) != hipSuccess) return e;
     if ((e = wgrad<float, T>(m.zp, dy, m.wpart, m.dw_out, rows, CB, st)) != hipSuccess) return e;
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
