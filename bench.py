@@ -297,7 +297,10 @@ def main() -> int:
                         if plan["module_backward_fused"] else
                         ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"])
     elif op.startswith("module"):
-        names = module_kernels(plan["plan"], plan["module_path"])
+        # the block runs 2^16-element slices with the three-pass plan even
+        # where the mixer's forward is FUSED
+        names = module_kernels("three_pass" if plan["module_outer_bits"] else plan["plan"],
+                               plan["module_path"])
         nk = len(names)
     else:
         nk, names = plan["kernels"], kernel_names(plan["plan"])

@@ -78,11 +78,14 @@ typedef enum whtmix_status {
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
  *   L <= 2^10          one small workgroup per slice, all stages in LDS;
  *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass;
- *   L >= 2^16          THREE_PASS: forward over the low bits of the flat
+ *   L = 2^16           FUSED (two register sets) from B = 48 slices, else
+ *                      THREE_PASS (the backward pass and the block run 2^16
+ *                      slices with THREE_PASS whatever the plan);
+ *   L >= 2^17          THREE_PASS: forward over the low bits of the flat
  *                      index, then forward over the high bits + gain +
  *                      inverse over the high bits, then inverse over the low
  *                      bits, exchanging through the workspace.
- * THREE_PASS may also be forced for 2^12 <= L <= 2^15 (tests compare it with
+ * THREE_PASS may also be forced for 2^12 <= L <= 2^16 (tests compare it with
  * FUSED on the same shapes). */
 typedef enum whtmix_plan {
     WHTMIX_PLAN_AUTO = 0,
@@ -99,7 +102,10 @@ typedef struct whtmix_options {
     void *events[4];
 } whtmix_options;
 
-/* Describes how a shape would run (no GPU work, no allocation). */
+/* Describes how a shape would run (no GPU work, no allocation).  plan,
+ * kernels and workspace_bytes are whtmix_forward's; the backward pass and the
+ * block run 2^16-element slices, whose forward is FUSED, with the three-pass
+ * plan (and its workspace). */
 typedef struct whtmix_plan_info {
     int plan;             /* resolved whtmix_plan (never AUTO) */
     int kernels;          /* kernels launched per call (1 or 3) */

@@ -84,13 +84,14 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     case whtmix::PLAN_AUTO:
         plan = K <= whtmix::kMaxSmall ? whtmix::PLAN_SMALL
                : K <= whtmix::kMaxTile ? whtmix::PLAN_FUSED
-                                       : whtmix::PLAN_THREE_PASS;
+               : K == whtmix::kMaxFused && B >= whtmix::kFusedPairMinBatch ? whtmix::PLAN_FUSED
+                                                                          : whtmix::PLAN_THREE_PASS;
         break;
     case whtmix::PLAN_SMALL:
         if (K > whtmix::kMaxSmall) return WHTMIX_ERROR_INVALID_VALUE;
         break;
     case whtmix::PLAN_FUSED:
-        if (K < whtmix::kMinTile || K > whtmix::kMaxTile) return WHTMIX_ERROR_INVALID_VALUE;
+        if (K < whtmix::kMinTile || K > whtmix::kMaxFused) return WHTMIX_ERROR_INVALID_VALUE;
         break;
     case whtmix::PLAN_THREE_PASS:
         if (K < whtmix::kMinTile + 1) return WHTMIX_ERROR_INVALID_VALUE;
@@ -108,6 +109,19 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         out->ws_bytes = B * L * 4;
     }
     return WHTMIX_SUCCESS;
+}
+
+// The single-workgroup FUSED plan reaches 2^16 elements (two register sets)
+// in the mixer's forward only: the backward pass and the block run the
+// three-pass plan for such slices.
+void three_pass_beyond_one_tile(int64_t B, Checked *c)
+{
+    if (c->plan == whtmix::PLAN_FUSED && c->K > whtmix::kMaxTile) {
+        c->plan = whtmix::PLAN_THREE_PASS;
+        c->kernels = 3;
+        c->split = whtmix::three_pass_split(c->K);
+        c->ws_bytes = B * (int64_t(1) << c->K) * 4;
+    }
 }
 
 int hip_fail(hipError_t e, const char *what)
@@ -176,14 +190,17 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->workspace_bytes = c.ws_bytes;
     info->padded_tokens = c.n_pad;
     const int cbits = log2_exact(C);
+    Checked blk = c;   // the block's plan
+    three_pass_beyond_one_tile(B, &blk);
     info->module_path = cbits <= whtmix::kModuleMaxCbits
-                            ? whtmix::module_path(c.plan, cbits, dtype, c.K)
+                            ? whtmix::module_path(blk.plan, cbits, dtype, blk.K)
                             : -1;
     info->module_outer_bits =
-        info->module_path >= 0 && c.plan == whtmix::PLAN_THREE_PASS
-            ? whtmix::module_outer_bits(info->module_path, cbits, c.K)
+        info->module_path >= 0 && blk.plan == whtmix::PLAN_THREE_PASS
+            ? whtmix::module_outer_bits(info->module_path, cbits, blk.K)
             : 0;
-    info->module_backward_fused = whtmix::module_backward_fused(c.plan, cbits, dtype, c.K) ? 1 : 0;
+    info->module_backward_fused =
+        whtmix::module_backward_fused(blk.plan, cbits, dtype, blk.K) ? 1 : 0;
     return WHTMIX_SUCCESS;
 }
 
@@ -284,6 +301,7 @@ int backward_impl(const void *x, const void *dy, int gain_kind, const float *gai
     Checked c;
     int st = check_shape(B, N, C, dtype, options, &c);
     if (st != WHTMIX_SUCCESS) return st;
+    three_pass_beyond_one_tile(B, &c);
     const bool sep = gain_kind == whtmix::GAIN_LOG_SEPARABLE;
     const bool want_dg = sep ? (dgt != nullptr || dgc != nullptr) : dgain != nullptr;
     if (sep && (dgt == nullptr) != (dgc == nullptr)) return WHTMIX_ERROR_INVALID_VALUE;
@@ -358,6 +376,7 @@ int module_impl(const void *x, const void *w_in, int gain_kind, const float *gai
     Checked c;
     int st = check_shape(B, N, C, dtype, options, &c);
     if (st != WHTMIX_SUCCESS) return st;
+    three_pass_beyond_one_tile(B, &c);
     const int cbits = log2_exact(C);
     if (cbits > whtmix::kModuleMaxCbits) return WHTMIX_ERROR_TOO_LARGE;
     if (B == 0) return WHTMIX_SUCCESS;
@@ -438,6 +457,7 @@ int module_backward_impl(const void *x, const void *w_in, int gain_kind, const f
     Checked c;
     int st = check_shape(B, N, C, dtype, options, &c);
     if (st != WHTMIX_SUCCESS) return st;
+    three_pass_beyond_one_tile(B, &c);
     const int cbits = log2_exact(C);
     if (cbits > whtmix::kModuleMaxCbits || B * N >= (int64_t(1) << 31))
         return WHTMIX_ERROR_TOO_LARGE;

@@ -55,6 +55,49 @@ fused_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, uint32_t nva
     store_tile<G::TOP, K, T>(v, y + base, nvalid, tau);
 }
 
+// FUSED for 2^16 elements: one 1024-thread workgroup holds the slice as two
+// 2^15 register sets (set = tile bit 15).  Bit 15 is a register butterfly
+// between the sets, right after the load and right before the store; bits
+// 0..14 run the 2^15 schedule on each set in turn through the same LDS.  The
+// gain of the second set is read when the first set is done with its own.
+template <typename T, class Gain>
+__global__ void __launch_bounds__(1 << (15 - VB))
+fused_pair_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, uint32_t nvalid)
+{
+    constexpr int K = 16, M = 15;
+    using G = Groups<M, 0>;
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const size_t base = (size_t)blockIdx.x * nvalid;
+    const uint32_t valid0 = min(nvalid, 1u << M);
+    const uint32_t valid1 = nvalid > (1u << M) ? nvalid - (1u << M) : 0u;
+    float v0[V], v1[V];
+    load_tile<G::TOP, M, T>(v0, x + base, valid0, tau);
+    load_tile<G::TOP, M, T>(v1, x + base + (1u << M), valid1, tau);
+    cross_butterflies(v0, v1);
+    butterflies<0, VB>(v0);
+    butterflies<0, VB>(v1);
+    forward_groups<M, 0, 0, G::TOP>(lds, v0, tau);
+    forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
+    {
+        float gv[V];
+        gain.template load<G::SL, ContigMap>(gv, 0, tau);
+        apply_gain<K>(v0, gv);
+    }
+    inverse_groups<M, 0, G::NBOT - 1>(lds, v0, tau);
+    butterflies<0, VB>(v0);
+    {
+        float gv[V];
+        gain.template load<G::SL, ContigMap>(gv, 1u << M, tau);
+        apply_gain<K>(v1, gv);
+    }
+    inverse_groups<M, 0, G::NBOT - 1>(lds, v1, tau);
+    butterflies<0, VB>(v1);
+    cross_butterflies(v0, v1);
+    store_tile<G::TOP, M, T>(v0, y + base, valid0, tau);
+    store_tile<G::TOP, M, T>(v1, y + base + (1u << M), valid1, tau);
+}
+
 // MIDDLE: logical tile = run * B + b (the B slices sharing a gain tile are
 // adjacent); workgroups are renumbered so adjacent logical tiles land on the
 // same XCD (blocks are dealt round-robin over the 8 XCDs) and share its L2.
@@ -139,6 +182,17 @@ hipError_t launch_fused(const T *x, T *y, Gain gain, const LaunchArgs &a)
     return record(a.events[1], a.stream);
 }
 
+template <typename T, class Gain>
+hipError_t launch_fused_pair(const T *x, T *y, Gain gain, const LaunchArgs &a)
+{
+    hipError_t e = record(a.events[0], a.stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((fused_pair_kernel<T, Gain>), dim3((uint32_t)a.B), dim3(1u << (15 - VB)), 0,
+                       a.stream, x, y, gain, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(a.events[1], a.stream);
+}
+
 template <int K, typename T, class Gain>
 hipError_t launch_three_pass(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
@@ -185,6 +239,7 @@ hipError_t dispatch(const LaunchArgs &a, Gain gain)
             WHTMIX_FUSED_CASE(11) WHTMIX_FUSED_CASE(12) WHTMIX_FUSED_CASE(13)
             WHTMIX_FUSED_CASE(14) WHTMIX_FUSED_CASE(15)
 #undef WHTMIX_FUSED_CASE
+        case kMaxFused: return launch_fused_pair<T, Gain>(x, y, gain, a);
         default: return hipErrorInvalidValue;
         }
     }

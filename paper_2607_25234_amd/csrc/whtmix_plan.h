@@ -17,6 +17,13 @@ constexpr int kMaxLog2Slice = 30;   // N*C <= 2^30
 constexpr int kMaxSmall = 10;       // SMALL: L <= 2^10
 constexpr int kMinTile = 11;        // tiles hold 2^11 .. 2^15 elements
 constexpr int kMaxTile = 15;
+// FUSED (one workgroup per slice): up to 2^16 elements, as two 2^15 register
+// sets above 2^15 (the mixer's forward; the backward pass and the block run
+// the three-pass plan for 2^16-element slices).  One workgroup moves a 2^16
+// slice in about 23 us whatever the batch, so AUTO takes it from 48 slices,
+// where the three passes (15 us at 16 slices, 24 us at 48) stop being faster.
+constexpr int kMaxFused = 16;
+constexpr int kFusedPairMinBatch = 48;
 
 // THREE_PASS split for slice bits K:
 //   outer passes: contiguous chunks of 2^A elements (all A low bits of f);

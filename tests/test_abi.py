@@ -74,8 +74,8 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(g=ALIGNED + 16, y=ALIGNED), 1),     # gain inside y
     (dict(plan=9), 1),
     (dict(plan=1, N=64, C=64), 1),            # SMALL needs N*C <= 2^10
-    (dict(plan=2, N=8, C=8), 1),              # FUSED needs 2^11..2^15
-    (dict(plan=2, N=1024, C=64), 1),
+    (dict(plan=2, N=8, C=8), 1),              # FUSED needs 2^11..2^16
+    (dict(plan=2, N=2048, C=64), 1),
     (dict(plan=3, N=32, C=64), 1),            # THREE_PASS needs >= 2^12
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
@@ -236,6 +236,15 @@ def test_plan_table():
     d = whtmix.plan_describe(3, 512, 128, "bf16")
     assert d["plan"] == "three_pass" and d["kernels"] == 3
     assert d["workspace_bytes"] == 3 * 512 * 128 * 4
+    # 2^16 from 48 slices: one workgroup of two register sets for the forward;
+    # the block and the backward pass take the three-pass plan
+    assert whtmix.plan_describe(47, 512, 128, "bf16")["plan"] == "three_pass"
+    d = whtmix.plan_describe(48, 512, 128, "bf16")
+    assert (d["plan"], d["kernels"], d["workspace_bytes"]) == ("fused", 1, 0)
+    assert (d["module_path"], d["module_outer_bits"]) == ("mfma", 11)
+    assert d["module_backward_fused"]
+    d = whtmix.plan_describe(3, 512, 128, "bf16", "fused")
+    assert (d["plan"], d["workspace_bytes"]) == ("fused", 0)
     d = whtmix.plan_describe(2, 64, 64, plan="three_pass")
     assert d["plan"] == "three_pass" and d["outer_bits"] == 11
     d = whtmix.plan_describe(4, 65536, 128, "bf16")
@@ -246,7 +255,7 @@ def test_plan_table():
         d = whtmix.plan_describe(w.B, w.N, w.C, w.dtype)
         K = d["log2_slice"]
         assert 1 << K == w.N * w.C
-        if K >= 16:
+        if K >= 16:   # every workload's 2^16 slices come in batches below 48
             A, R = d["outer_bits"], d["run_bits"]
             assert d["plan"] == "three_pass"
             assert 11 <= A <= 16 and 11 <= K - A + R <= 15 and R <= A

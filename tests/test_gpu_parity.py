@@ -81,7 +81,9 @@ def test_shapes(shape, dtype, dev, orc):
 # straddling tile element by element); 262143 x 4 in bf16 (2 097 144 bytes)
 # is not, and takes per-element accesses throughout.
 PADDED = [(1, 3, 4), (2, 5, 8), (1, 100, 8), (3, 1000, 16), (2, 130, 128), (2, 9216, 64),
-          (1, 25600, 64), (1, 50176, 64), (2, 36864, 64), (1, 139872, 256), (2, 262143, 4)]
+          (1, 25600, 64), (1, 50176, 64), (2, 36864, 64), (1, 139872, 256), (2, 262143, 4),
+          # 2^16 in one workgroup: the second register set partly or wholly padding
+          (2, 1000, 64), (1, 300, 128), (3, 513, 64)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -91,16 +93,28 @@ def test_padded_tokens(shape, dtype, dev, orc):
     P = whtmix.padded_tokens(N)
     x, _ = workloads.draw(B, N, C, dtype, seed=300 + N)
     _, g = workloads.draw(1, P, C, "f32", seed=301 + N)
-    plan = whtmix.plan_describe(B, N, C, dtype)["plan"]
+    d = whtmix.plan_describe(B, N, C, dtype)
+    plan, K = d["plan"], d["log2_slice"]
     say(f"padded {shape} -> P={P} {dtype} plan={plan}")
     ref = orc.whtmix(x, g)
     check(f"{shape}", run_gpu(x, g, dtype, dev), ref, dtype)
-    if plan == "fused":
-        check(f"{shape} three_pass", run_gpu(x, g, dtype, dev, plan="three_pass"), ref, dtype)
+    # the other plan of slices one workgroup can hold (2^11..2^16)
+    if 12 <= K <= 16:
+        other = "three_pass" if plan == "fused" else "fused"
+        check(f"{shape} {other}", run_gpu(x, g, dtype, dev, plan=other), ref, dtype)
+
+
+def test_fused_2_16_large_batch(dev, orc):
+    """2^16-element slices in batches of 48 and more take one workgroup each."""
+    B, N, C = 64, 1000, 64
+    assert whtmix.plan_describe(B, N, C)["plan"] == "fused"
+    x, g = workloads.draw(B, N, C, "f32", seed=61)
+    _, g = workloads.draw(1, 1024, C, "f32", seed=62)
+    check("2^16 x 64", run_gpu(x, g, "f32", dev), orc.whtmix(x, g), "f32")
 
 
 SEPARABLE = [(1, 1, 1), (2, 32, 32), (3, 64, 128), (2, 4096, 64), (1, 9216, 64),
-             (2, 16384, 128), (1, 1000, 16)]
+             (2, 16384, 128), (1, 1000, 16), (2, 1000, 64)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -140,7 +154,7 @@ def test_separable_zero_log_gain_and_joint_equivalence(dev):
     assert errors(ys, yj)[0] < 2e-6
 
 
-@pytest.mark.parametrize("K", [12, 13, 14, 15])
+@pytest.mark.parametrize("K", [12, 13, 14, 15, 16])
 def test_three_pass_matches_fused(K, dev, orc):
     """Slices that fit one workgroup, forced through the three-pass plan too."""
     N, C = 1 << (K - 6), 64

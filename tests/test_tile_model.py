@@ -333,9 +333,60 @@ def simulate_fused(x, g, K):
     return y.reshape(x.shape)
 
 
+def simulate_fused_pair(x, g):
+    """fused_pair_kernel: a 2^16 slice in one workgroup of two 2^15 register
+    sets (tile bit 15 = the set), each through the 2^15 schedule; the set
+    butterfly right after the load and right before the store."""
+    K = 16
+    B = x.shape[0]
+    L = 1 << K
+    nvalid = x.shape[1] * x.shape[2]
+    xs = x.reshape(B * nvalid)
+    y = np.full(B * nvalid, np.nan)
+    acc_x, acc_y, acc_g = Access(B * nvalid), Access(B * nvalid), Access(L)
+    for b in range(B):
+        sets = outer_sets(16)
+        vals = []
+        for T, t0 in sets:
+            t = T.idx(T.g.TOP) + t0
+            m = t < nvalid
+            v = np.zeros(t.shape)
+            v[m] = xs[acc_x.at(b * nvalid + t[m])]
+            vals.append(v)
+        vals = list(cross(*vals))
+        for i, (T, t0) in enumerate(sets):
+            butterflies(vals[i], 0, VB)
+            vals[i] = T.forward_groups(vals[i], T.g.TOP)
+        for i, (T, t0) in enumerate(sets):
+            vals[i] = vals[i] * (g.reshape(L)[acc_g.at(T.idx(T.g.SL) + t0)] * (1.0 / L))
+            vals[i] = T.inverse_groups(vals[i])
+            butterflies(vals[i], 0, VB)
+        vals = list(cross(*vals))
+        for (T, t0), v in zip(sets, vals):
+            t = T.idx(T.g.TOP) + t0
+            m = t < nvalid
+            y[acc_y.at(b * nvalid + t[m])] = v[m]
+    assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
+    assert np.all(acc_g.count == B)
+    return y.reshape(x.shape)
+
+
 @pytest.fixture(scope="module")
 def orc():
     return oracle_mod.Oracle()
+
+
+@pytest.mark.parametrize("N,C", [(1024, 64), (1000, 64), (300, 128), (65536, 1)])
+def test_fused_pair_schedule(N, C, orc):
+    """2^16 slices in one workgroup, padded token counts included."""
+    rng = np.random.default_rng(N + C)
+    P = 1 << (N - 1).bit_length()
+    assert P * C == 1 << 16
+    x = rng.standard_normal((2, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    y = simulate_fused_pair(x, g)
+    ref = orc.whtmix(x, g)
+    assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
 
 
 @pytest.mark.parametrize("K", [11, 12, 13, 14, 15])
