@@ -1626,33 +1626,34 @@ __device__ __forceinline__ void wgrad_stage(float *lds, const u32x4 (&r)[N])
     }
 }
 
-// Three-term bf16 split of four floats: v = hi + mid + lo + d with each term
-// the nearest bf16 of what the previous ones leave (the differences are exact
-// in float32) and |d| <= 2^-27 |v|.
-__device__ __forceinline__ void split3_bf16(const f32x4 &z, bf16x4 &hi, bf16x4 &mid, bf16x4 &lo)
+// Eight k-slot values (two groups of four) for the 16x16x32 instruction.
+// Three-term bf16 split of floats: v = hi + mid + lo + d with each term the
+// nearest bf16 of what the previous ones leave (the differences are exact in
+// float32) and |d| <= 2^-27 |v|.
+__device__ __forceinline__ void split3_bf16x8(const f32x4 &z0, const f32x4 &z1, bf16x8 &hi,
+                                              bf16x8 &mid, bf16x8 &lo)
 {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const __bf16 h = (__bf16)z[e];
-        const float r1 = z[e] - (float)h;
+    for (int e = 0; e < 8; ++e) {
+        const float z = e < 4 ? z0[e] : z1[e - 4];
+        const __bf16 h = (__bf16)z;
+        const float r1 = z - (float)h;
         const __bf16 m = (__bf16)r1;
-        hi[e] = __builtin_bit_cast(short, h);
-        mid[e] = __builtin_bit_cast(short, m);
-        lo[e] = __builtin_bit_cast(short, (__bf16)(r1 - (float)m));
+        hi[e] = h;
+        mid[e] = m;
+        lo[e] = (__bf16)(r1 - (float)m);
     }
 }
 
-// Four k-slot values of one lane as bf16, for bf16-origin values: their high
-// halves, exactly.  (The whole vector is bit-cast: a bit_cast of one
-// ext-vector element reads element 0 in this toolchain.)
-__device__ __forceinline__ bf16x4 bf16_exact(const f32x4 &z)
+// bf16-origin values as bf16: their high halves, exactly.  (Whole vectors are
+// bit-cast: a bit_cast of one ext-vector element reads element 0 in this
+// toolchain.)
+__device__ __forceinline__ bf16x8 bf16_exact8(const f32x4 &z0, const f32x4 &z1)
 {
-    const u32x4 u = __builtin_bit_cast(u32x4, z);
-    bf16x4 o;
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-        o[e] = (short)(u[e] >> 16);
-    return o;
+    const u32x4 u0 = __builtin_bit_cast(u32x4, z0), u1 = __builtin_bit_cast(u32x4, z1);
+    const u32x4 o = {(u0[0] >> 16) | (u0[1] & 0xffff0000u), (u0[2] >> 16) | (u0[3] & 0xffff0000u),
+                     (u1[0] >> 16) | (u1[1] & 0xffff0000u), (u1[2] >> 16) | (u1[3] & 0xffff0000u)};
+    return __builtin_bit_cast(bf16x8, o);
 }
 
 // TOUT: store the transposed block (the caller passed B and A to get dW^T's
@@ -1719,27 +1720,30 @@ wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
             }
         } else {
 #pragma unroll 1
-            for (int kb = 0; kb < S::RB; kb += 16) {
-                // the float operand's three terms, the bf16 operand's one
+            for (int kb = 0; kb < S::RB; kb += 32) {
+                // the float operand's three terms, the bf16 operand's one;
+                // k-slot e of lane (i, q) is row kb + q + 4e
                 constexpr int NSA = SPLIT_A ? 3 : 1, NSB = SPLIT_B ? 3 : 1;
-                bf16x4 av[NSA][TQ], bv[NSB][TQ];
+                bf16x8 av[NSA][TQ], bv[NSB][TQ];
 #pragma unroll
                 for (int x = 0; x < TQ; ++x) {
                     const float *src = sa + (kb + q) * LDW + 16 * (tr0 + x) + i;
-                    const f32x4 z = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    const f32x4 z0 = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    const f32x4 z1 = {src[16 * LDW], src[20 * LDW], src[24 * LDW], src[28 * LDW]};
                     if constexpr (SPLIT_A)
-                        split3_bf16(z, av[0][x], av[1][x], av[2][x]);
+                        split3_bf16x8(z0, z1, av[0][x], av[1][x], av[2][x]);
                     else
-                        av[0][x] = bf16_exact(z);
+                        av[0][x] = bf16_exact8(z0, z1);
                 }
 #pragma unroll
                 for (int y = 0; y < TQ; ++y) {
                     const float *src = sb + (kb + q) * LDW + 16 * (tc0 + y) + i;
-                    const f32x4 z = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    const f32x4 z0 = {src[0], src[4 * LDW], src[8 * LDW], src[12 * LDW]};
+                    const f32x4 z1 = {src[16 * LDW], src[20 * LDW], src[24 * LDW], src[28 * LDW]};
                     if constexpr (SPLIT_B)
-                        split3_bf16(z, bv[0][y], bv[1][y], bv[2][y]);
+                        split3_bf16x8(z0, z1, bv[0][y], bv[1][y], bv[2][y]);
                     else
-                        bv[0][y] = bf16_exact(z);
+                        bv[0][y] = bf16_exact8(z0, z1);
                 }
 #pragma unroll
                 for (int x = 0; x < TQ; ++x)
@@ -1747,7 +1751,7 @@ wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
                     for (int y = 0; y < TQ; ++y)
 #pragma unroll
                         for (int t = 0; t < NSA * NSB; ++t)
-                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                                 av[t % NSA][x], bv[t / NSA][y], acc[x][y], 0, 0, 0);
             }
         }

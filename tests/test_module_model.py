@@ -844,8 +844,8 @@ def bf16_rne(v):
 def model_wgrad(a, b, cb, kinds=("f32", "f32")):
     """wgrad_mfma_kernel: per (chunk, T x T block), 64-row LDS blocks, waves
     owning TQ x TQ quadrants of 16 x 16 tiles; in a step the lanes (i, q)
-    take, for k-slot e, row kb + q + 4e (bf16 instruction, 16 rows) or row
-    kb + q (float32 instruction, 4 rows) of column i.  kinds: the dtypes of
+    take, for k-slot e, row kb + q + 4e (16x16x32 bf16 instruction, 32 rows)
+    or row kb + q (float32 instruction, 4 rows) of column i.  kinds: the dtypes of
     a and b; a float against a bf16 operand is split into three bf16 terms."""
     if kinds == ("f32", "bf16"):   # run as (b, a), blocks stored transposed
         return model_wgrad(b, a, cb, ("bf16", "f32")).T
@@ -876,9 +876,9 @@ def model_wgrad(a, b, cb, kinds=("f32", "f32")):
                 tr0, tc0 = ((w >> 1) * TQ, (w & 1) * TQ) if T >= 32 else (0, 0)
                 acc = {(x, y): np.zeros((64, 4)) for x in range(TQ) for y in range(TQ)}
                 for r0 in range(ch * rpc, r_end, 64):
-                    step = 4 if f32 else 16
+                    step = 4 if f32 else 32
                     for kb in range(0, 64, step):
-                        slots = [kb + q] if f32 else [kb + q + 4 * e for e in range(4)]
+                        slots = [kb + q] if f32 else [kb + q + 4 * e for e in range(8)]
                         for x in range(TQ):
                             for y in range(TQ):
                                 sa, sb = [], []
