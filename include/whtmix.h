@@ -236,11 +236,12 @@ WHTMIX_API int whtmix_backward_separable(const void *x, const void *dy,
  * not overlap y except x == y.  Arithmetic is float32: for bf16 the products
  * X W_in are exact, Z' W_out uses a two-term bf16 split of Z' (relative
  * residual below 2^-17), and y is rounded to nearest even once.  For
- * 16 <= C <= 128 the projections run on the matrix cores inside the mixer's
- * first and last kernels (three kernels plus a small weight-repacking kernel
- * for N_pad*C > 2^15); other C run separate projection kernels around the
- * float32 mixer.  Workspace: the mixer's, plus 2*C*C elements of packed
- * weights or B*N*C floats of Z.  Other conventions, plans and options as
+ * 16 <= C <= 128, and for bf16 C = 256 from N_pad*C = 2^17, the projections
+ * run on the matrix cores inside the mixer's first and last kernels (three
+ * kernels plus a small weight-repacking kernel for N_pad*C > 2^15;
+ * whtmix_plan_describe's module_path says which); other shapes run separate
+ * projection kernels around the float32 mixer.  Workspace: the mixer's, plus
+ * 2*C*C elements of packed weights or B*N*C floats of Z.  Other conventions, plans and options as
  * whtmix_forward_ex (events: for the three-pass plan around each of its
  * three passes, otherwise [0] before and [1] after the call's kernels).
  */
@@ -268,7 +269,10 @@ WHTMIX_API int whtmix_module_forward_separable(const void *x, const void *w_in,
  *     dZ' = dY W_out^T,            dW_out = sum over b of Z'^T dY,
  *     dZ, dgain = the mixer's gradients (whtmix_backward) at (Z, dZ'),
  *     dX = dZ W_in^T,              dW_in  = sum over b of X^T dZ,
- * with Z = X W_in and Z' = mixer(Z) recomputed in float32.
+ * with Z = X W_in and Z' = mixer(Z) recomputed in float32.  For bf16 with
+ * 32 <= C <= 128 on three-pass slices up to 2^25 elements (and a requested
+ * gain gradient) the projections run inside the mixer backward's passes and
+ * Z and dZ' are never stored (whtmix_plan_describe's module_backward_fused).
  *
  *   x, dy         [B][N][C] elements of `dtype`.
  *   w_in, w_out   [C][C] elements of `dtype`, as passed to the forward call.
@@ -281,8 +285,10 @@ WHTMIX_API int whtmix_module_forward_separable(const void *x, const void *w_in,
  * results are bitwise reproducible.  Workspace: 3*B*N*C floats plus the
  * mixer's forward and backward workspaces, 3*C*C packed weight elements and
  * the weight-gradient partial sums.  Other conventions as
- * whtmix_module_forward (events: [0] before, [1] after dW_out, [2] after the
- * mixer's gradients, [3] after dX and dW_in).
+ * whtmix_module_forward (events: [0] before, then after each phase: [1]
+ * dW_out, [2] the mixer's gradients, [3] dX and dW_in; with the projections
+ * inside the mixer's passes [1] the gain gradient, [2] dW_out, [3] dX and
+ * dW_in).
  */
 WHTMIX_API int whtmix_module_backward(const void *x, const void *w_in,
                            const float *gain, const void *w_out,
