@@ -28,10 +28,13 @@
 // Plans (the mixer's, whtmix_plan.h):
 //   FUSED       K <= 15: one workgroup per slice, prologue + mixer + epilogue.
 //   THREE_PASS  prologue in the first outer pass, the unchanged middle pass,
-//               epilogue in the second outer pass.
+//               epilogue in the second outer pass; bf16 C = 256 on 2^16
+//               outer tiles of two register sets (the pair kernels below).
 //   SMALL       K <= 10: one LDS-resident workgroup per slice, VALU products.
-//   UNFUSED     any other C: projection kernels around the fp32 mixer (on the
-//               matrix cores for C >= 256 where a weight slice fits LDS).
+//   UNFUSED     any other shape: projection kernels around the fp32 mixer (on
+//               the matrix cores from C = 256 where a weight slice fits LDS).
+// The block's backward fuses its projections into the mixer backward's
+// passes for bf16 32 <= C <= 128 (module_backward_fused_k).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -837,7 +840,7 @@ constexpr uint32_t kPairKs = kPairC / 32u;                      // k steps
 constexpr uint32_t kPairWChunks = kPairC * kPairC * 2u / 16u;   // 16-byte pieces of W
 
 static_assert(kPairC * kPairC * 2u <= pad(1u << 15) * 4u, "W fits the tile's LDS");
-static_assert(kPairWChunks % kPairThreads == 0, "whole prefetch per thread");
+static_assert(kPairWChunks % kPairThreads == 0, "whole pieces of W per thread");
 
 // Set-local index t' (t bit 5 dropped) -> workspace offset.
 template <class Map>
