@@ -183,6 +183,33 @@ def test_module_identity_weights_reduce_to_the_mixer(dev):
     assert errors(y, ym)[0] < 1e-6
 
 
+@pytest.mark.parametrize("shape", [(1, 1 << 19, 256), (1, 139872, 256)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_module_c256_large_identity_weights(shape, dev):
+    """bf16 C = 256 at 2^27 elements (runs of 16 floats, renumbered outer
+    blocks) and at 2^26 with padding: W_in = W_out = I gives the mixer alone.
+    Each output is the nearest bf16 of a float32 value, and the two float32
+    values differ by rounding only, so an element may differ by one bf16 ulp
+    (2^-7 of its magnitude at most): the bar is 2^-7 normwise."""
+    import torch
+
+    B, N, C = shape
+    d = whtmix.plan_describe(B, N, C, "bf16")
+    assert (d["module_path"], d["module_outer_bits"]) == ("mfma", 16)
+    gen = torch.Generator(device="cpu").manual_seed(N)
+    x = torch.randn(B, N, C, generator=gen).to(dev).to(torch.bfloat16)
+    P = whtmix.padded_tokens(N)
+    g = (torch.rand(P, C, generator=gen) + 0.5).to(dev)
+    eye = torch.eye(C, device=dev, dtype=torch.bfloat16)
+    say(f"module identity {shape} bf16")
+    y = whtmix.module_forward(x, eye, g, eye)
+    ym = whtmix.forward(x, g)
+    torch.cuda.synchronize(dev)
+    err, rms = errors(to_host(y), to_host(ym))
+    say(f"  normwise-max {err:.3e} rms {rms:.3e}")
+    assert err <= 2.0 ** -7 and rms < 1e-3, (err, rms)
+
+
 def test_module_deterministic(dev):
     B, N, C = 4, 16384, 128
     x, g, wi, wo = inputs(B, N, C, "bf16", seed=31)
