@@ -276,17 +276,24 @@ __device__ __forceinline__ uint32_t pack_x32_source(uint32_t idx, uint32_t C, in
     return mode >= PACK_PROLOGUE_T ? col * C + k : k * C + col;
 }
 
-// pa = wa packed in mode_a; pb = wb in mode_b unless pb is null.
+// Up to three packings in one launch: p[i] = w[i] packed in mode[i] for the
+// entries whose p[i] is not null.
+struct PackX32Jobs {
+    const __bf16 *w[3];
+    __bf16 *p[3];
+    int mode[3];
+};
+
 __global__ void __launch_bounds__(256)
-pack_x32_kernel(const __bf16 *__restrict__ wa, __bf16 *__restrict__ pa, int mode_a,
-                const __bf16 *__restrict__ wb, __bf16 *__restrict__ pb, int mode_b, int cb)
+pack_x32_kernel(PackX32Jobs jobs, int cb)
 {
     const uint32_t C = 1u << cb;
     const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
     if (idx >= C * C) return;
-    pa[idx] = wa[pack_x32_source(idx, C, mode_a)];
-    if (pb)
-        pb[idx] = wb[pack_x32_source(idx, C, mode_b)];
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+        if (jobs.p[i])
+            jobs.p[i][idx] = jobs.w[i][pack_x32_source(idx, C, jobs.mode[i])];
 }
 
 // X fragments of the prologue: per row block, the lane's C/4 channels of its
@@ -1397,10 +1404,13 @@ hipError_t dispatch_fused_module(const ModuleArgs &m, Gain gain)
     hipError_t e;
     if (std::is_same<T, __bf16>::value && m.cbits >= 5) {
         const uint32_t n = 1u << (2 * m.cbits);
-        hipLaunchKernelGGL(pack_x32_kernel, dim3((n + 255u) / 256u), dim3(256), 0, m.stream,
-                           static_cast<const __bf16 *>(m.w_in), static_cast<__bf16 *>(m.wpack),
-                           (int)PACK_PROLOGUE, static_cast<const __bf16 *>(m.w_out),
-                           static_cast<__bf16 *>(m.wpack) + n, (int)PACK_EPILOGUE, m.cbits);
+        const PackX32Jobs jobs{{static_cast<const __bf16 *>(m.w_in),
+                                static_cast<const __bf16 *>(m.w_out), nullptr},
+                               {static_cast<__bf16 *>(m.wpack),
+                                static_cast<__bf16 *>(m.wpack) + n, nullptr},
+                               {PACK_PROLOGUE, PACK_EPILOGUE, 0}};
+        hipLaunchKernelGGL(pack_x32_kernel, dim3((n + 255u) / 256u), dim3(256), 0, m.stream, jobs,
+                           m.cbits);
         e = hipGetLastError();
     } else {
         e = launch_pack<T>(m, false);
@@ -1933,15 +1943,12 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     const T *w_in = static_cast<const T *>(m.w_in);
     T *pk = static_cast<T *>(m.wpack);
     T *p_in = pk, *p_out_t = pk + CC, *p_in_te = pk + 2 * CC;
-    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in, p_in,
-                       (int)PACK_PROLOGUE, static_cast<const T *>(m.w_out), p_out_t,
-                       (int)PACK_PROLOGUE_T, CB);
+    const PackX32Jobs jobs{{w_in, static_cast<const T *>(m.w_out), w_in},
+                           {p_in, p_out_t, p_in_te},
+                           {PACK_PROLOGUE, PACK_PROLOGUE_T, PACK_EPILOGUE_T}};
+    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, jobs, CB);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, w_in,
-                       p_in_te, (int)PACK_EPILOGUE_T, static_cast<const T *>(nullptr),
-                       static_cast<T *>(nullptr), 0, CB);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = record(m.events[0], st)) != hipSuccess) return e;
     const bool separable = m.gain_kind == GAIN_LOG_SEPARABLE;
     const BackwardLayout lay =
