@@ -606,7 +606,8 @@ hipError_t middle_phase_dispatch(const BackwardArgs &a, const BackwardLayout &la
         WHTMIX_GM_CASE(12) WHTMIX_GM_CASE(13) WHTMIX_GM_CASE(14) WHTMIX_GM_CASE(15)
         WHTMIX_GM_CASE(16) WHTMIX_GM_CASE(17) WHTMIX_GM_CASE(18) WHTMIX_GM_CASE(19)
         WHTMIX_GM_CASE(20) WHTMIX_GM_CASE(21) WHTMIX_GM_CASE(22) WHTMIX_GM_CASE(23)
-        WHTMIX_GM_CASE(24) WHTMIX_GM_CASE(25)
+        WHTMIX_GM_CASE(24) WHTMIX_GM_CASE(25) WHTMIX_GM_CASE(26) WHTMIX_GM_CASE(27)
+        WHTMIX_GM_CASE(28)
 #undef WHTMIX_GM_CASE
     default: return hipErrorInvalidValue;
     }

@@ -80,7 +80,7 @@ hipError_t launch_backward(const BackwardArgs &a);
 // holds backward_layout's wsx and wsd, the outer forward transforms of x and
 // dy made by the caller.  Writes the gain gradient (which must be requested)
 // and leaves the mixer of both x and dY up to its last pass in wsx and wsd
-// (the middle pass of each, in place).  Slices of 2^12..2^25 elements.
+// (the middle pass of each, in place).  Slices of 2^12..2^28 elements.
 hipError_t launch_backward_middle(const BackwardArgs &a);
 
 // Enqueues only the middle pass of the block's three-pass plan (module_split,

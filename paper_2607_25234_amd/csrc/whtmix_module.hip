@@ -956,15 +956,14 @@ __device__ __forceinline__ void project_out_pair(const bf16x8 (&hi)[kPairKs],
 
 // THREE_PASS first pass, C = 256: prologue, forward over the 16 low bits.
 template <int HB, int R>
-__global__ void __launch_bounds__(kPairThreads)
-module_outer_fwd_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restrict__ w_in,
-                             float *__restrict__ ws, uint32_t nvalid)
+__device__ __forceinline__ void module_outer_fwd_pair_tile(float *lds, const __bf16 *__restrict__ x,
+                                                           const __bf16 *__restrict__ w_in,
+                                                           float *__restrict__ ws,
+                                                           uint32_t nvalid, uint32_t blk)
 {
     constexpr int A = 16, M = 15;
     using Run = RunMap<HB, R>;
-    __shared__ __attribute__((aligned(16))) float lds[pad(1u << M)];
     const uint32_t tau = threadIdx.x;
-    const uint32_t blk = outer_block<R>(blockIdx.x, gridDim.x);
     const size_t b = blk >> HB;
     const uint32_t hi = blk & ((1u << HB) - 1u);
     const uint32_t valid = tile_valid<A>(nvalid, hi);
@@ -984,11 +983,65 @@ module_outer_fwd_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restr
     store_layout<M - 5, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
 }
 
-// THREE_PASS last pass, C = 256: inverse over the 16 low bits, epilogue, y.
 template <int HB, int R>
 __global__ void __launch_bounds__(kPairThreads)
+module_outer_fwd_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restrict__ w_in,
+                             float *__restrict__ ws, uint32_t nvalid)
+{
+    __shared__ __attribute__((aligned(16))) float lds[pad(1u << 15)];
+    module_outer_fwd_pair_tile<HB, R>(lds, x, w_in, ws, nvalid,
+                                      outer_block<R>(blockIdx.x, gridDim.x));
+}
+
+// Two operands in one launch (the block's backward), as module_outer_fwd2_kernel.
+template <int HB, int R>
+__global__ void __launch_bounds__(kPairThreads)
+module_outer_fwd2_pair_kernel(const __bf16 *__restrict__ x, const __bf16 *__restrict__ wa,
+                              const __bf16 *__restrict__ dy, const __bf16 *__restrict__ wb,
+                              float *__restrict__ wsx, float *__restrict__ wsd, uint32_t nvalid)
+{
+    __shared__ __attribute__((aligned(16))) float lds[pad(1u << 15)];
+    const uint32_t half = gridDim.x >> 1;
+    const bool second = blockIdx.x >= half;
+    const uint32_t blk = outer_block<R>(blockIdx.x - (second ? half : 0u), half);
+    module_outer_fwd_pair_tile<HB, R>(lds, second ? dy : x, second ? wb : wa, second ? wsd : wsx,
+                                      nvalid, blk);
+}
+
+// Stores one set's inverse-transformed elements (float32, row-major like y)
+// from the epilogue layout, through LDS into layout 10 of the set (t bit 5 =
+// s dropped): each register then covers 2^10 set elements in runs of 32
+// consecutive floats.  Waits for earlier readers of the LDS first.
+__device__ __forceinline__ void store_pair_set_f32(float *lds, const float (&v)[V], float *tile,
+                                                   uint32_t valid, uint32_t s, uint32_t tau)
+{
+    using E = Epi<15, 7>;
+    using Map = DropBit5<ContigMap>;
+    const uint32_t pe = pad(E::base(tau));
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pe + pad(reg_offset<E>((uint32_t)k))] = v[k];
+    __syncthreads();
+    const uint32_t tb = layout_base<10>(tau);
+    const uint32_t ps = pad(tb);
+    // set element t' < valid / 2 holds token t' / 128 < valid / 256: a real row
+    const __amdgpu_buffer_rsrc_t r = buffer(tile, valid * 4u);
+    const uint32_t voff = (Map::at(tb) + (s << 5)) * 4u;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        const float u = lds[ps + pad((uint32_t)k << 10)];
+        if ((tb | ((uint32_t)k << 10)) < valid / 2u)
+            Elt<float>::store<kStreaming>(u, r, voff, Map::at((uint32_t)k << 10) * 4u);
+    }
+}
+
+// THREE_PASS last pass, C = 256: inverse over the 16 low bits, epilogue, y.
+// ZOUT: also store the inverse-transformed tile itself (float32) to z.
+template <int HB, int R, bool ZOUT = false>
+__global__ void __launch_bounds__(kPairThreads)
 module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restrict__ w_out,
-                             __bf16 *__restrict__ y, uint32_t nvalid)
+                             __bf16 *__restrict__ y, float *__restrict__ z, uint32_t nvalid)
 {
     constexpr int A = 16, M = 15;
     using Run = RunMap<HB, R>;
@@ -1009,6 +1062,11 @@ module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restr
     cross_butterflies(v0, v1);   // t bit 5 (the bit groups commute)
     inverse_to_epilogue<M, 7, false>(lds, v0, tau);
     inverse_to_epilogue<M, 7, true>(lds, v1, tau);
+    if constexpr (ZOUT) {
+        float *zt = z + b * nvalid + ((size_t)hi << A);
+        store_pair_set_f32(lds, v0, zt, valid, 0u, tau);
+        store_pair_set_f32(lds, v1, zt, valid, 1u, tau);
+    }
     __syncthreads();             // every thread has read its epilogue-layout values
     stage_weights_dma<kPairWChunks, kPairThreads>(lds, w_out, tau);
     bf16x8 zh[kPairKs], zl[kPairKs];
@@ -1353,7 +1411,7 @@ hipError_t launch_module_pair(const ModuleArgs &m)
     if ((e = launch_middle(middle_args(m, true))) != hipSuccess) return e;
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
     hipLaunchKernelGGL((module_outer_inv_pair_kernel<HB, R>), grid, block, 0, st, m.ws,
-                       pin + kPairC * kPairC, static_cast<__bf16 *>(m.y), m.nvalid);
+                       pin + kPairC * kPairC, static_cast<__bf16 *>(m.y), nullptr, m.nvalid);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return record(m.events[3], st);
 }
@@ -1989,6 +2047,68 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     return record(m.events[3], st);
 }
 
+// The same for bf16 C = 256 on the 2^16 outer tiles (pair_split, which is the
+// mixer's split, and so the backward middle phase's, from 2^26 elements).
+template <int K>
+hipError_t module_backward_fused_pair(const ModuleBackwardArgs &m)
+{
+    constexpr Split sp = pair_split(K);
+    constexpr int HB = sp.HB, R = sp.R;
+    static_assert(K >= 26 && sp.A == three_pass_split(K).A && R == three_pass_split(K).R,
+                  "the backward's middle phase runs the mixer's split");
+    using T = __bf16;
+    constexpr int CB = kPairCB;
+    const hipStream_t st = m.stream;
+    const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> CB);
+    const uint32_t CC = 1u << (2 * CB);
+    const T *x = static_cast<const T *>(m.x);
+    const T *dy = static_cast<const T *>(m.dy);
+    const T *w_in = static_cast<const T *>(m.w_in);
+    T *pk = static_cast<T *>(m.wpack);
+    T *p_in = pk, *p_out_t = pk + CC, *p_in_te = pk + 2 * CC;
+    const PackX32Jobs jobs{{w_in, static_cast<const T *>(m.w_out), w_in},
+                           {p_in, p_out_t, p_in_te},
+                           {PACK_PROLOGUE, PACK_PROLOGUE_T, PACK_EPILOGUE_T}};
+    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, jobs, CB);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = record(m.events[0], st)) != hipSuccess) return e;
+    const bool separable = m.gain_kind == GAIN_LOG_SEPARABLE;
+    const BackwardLayout lay = backward_layout(PLAN_THREE_PASS, K, m.B, kPairC, separable);
+    float *wsx = m.bwd_ws + lay.wsx;
+    float *wsd = m.bwd_ws + lay.wsd;
+    hipLaunchKernelGGL((module_outer_fwd2_pair_kernel<HB, R>), dim3((uint32_t)(2 * (m.B << HB))),
+                       dim3(kPairThreads), 0, st, x, p_in, dy, p_out_t, wsx, wsd, m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    BackwardArgs g{};
+    g.gain_kind = m.gain_kind;
+    g.gain = m.gain;
+    g.gain_t = m.gain_t;
+    g.gain_c = m.gain_c;
+    g.dgain = m.dgain;
+    g.dgt = m.dgt;
+    g.dgc = m.dgc;
+    g.cbits = CB;
+    g.ws = m.bwd_ws;
+    g.B = m.B;
+    g.K = K;
+    g.nvalid = m.nvalid;
+    g.dtype = DTYPE_F32;
+    g.plan = PLAN_THREE_PASS;
+    g.stream = st;
+    if ((e = launch_backward_middle(g)) != hipSuccess) return e;
+    if ((e = record(m.events[1], st)) != hipSuccess) return e;
+    if ((e = launch_outer_inv<K, float>(wsx, m.zp, m.B, m.nvalid, st)) != hipSuccess) return e;
+    if ((e = wgrad<float, T>(m.zp, dy, m.wpart, m.dw_out, rows, CB, st)) != hipSuccess) return e;
+    if ((e = record(m.events[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((module_outer_inv_pair_kernel<HB, R, true>), dim3((uint32_t)(m.B << HB)),
+                       dim3(kPairThreads), 0, st, wsd, p_in_te, static_cast<T *>(m.dx), m.dzp,
+                       m.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = wgrad<T, float>(x, m.dzp, m.wpart, m.dw_in, rows, CB, st)) != hipSuccess) return e;
+    return record(m.events[3], st);
+}
+
 template <int CB>
 hipError_t module_backward_fused_cb(const ModuleBackwardArgs &m)
 {
@@ -2015,6 +2135,14 @@ hipError_t module_backward(const ModuleBackwardArgs &m)
         case 5: return module_backward_fused_cb<5>(m);
         case 6: return module_backward_fused_cb<6>(m);
         case 7: return module_backward_fused_cb<7>(m);
+        case kPairCB:
+            switch (m.K) {
+            case 26: return module_backward_fused_pair<26>(m);
+            case 27: return module_backward_fused_pair<27>(m);
+            case 28: return module_backward_fused_pair<28>(m);
+            default: break;
+            }
+            break;
         default: break;
         }
     }

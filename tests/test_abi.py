@@ -292,7 +292,9 @@ def test_block_backward_paths():
     assert fused(1, 3000, 32, "bf16") and fused(2, 128, 128, "bf16", "three_pass")
     assert not fused(4, 65536, 128, "f32")              # float32
     assert not fused(1, 65536, 16, "bf16")              # C = 16: VALU-sized products
-    assert not fused(1, 262144, 256, "bf16")            # C = 256
+    assert fused(1, 262144, 256, "bf16") and fused(1, 1 << 20, 256, "bf16")   # C = 256, 2^26..2^28
+    assert not fused(1, 65536, 256, "bf16")             # C = 256 below 2^26 (module split)
+    assert not fused(1, 1 << 21, 256, "bf16")           # 2^29
     assert not fused(1, 256, 64, "bf16")                # FUSED plan
     assert not fused(1, 1 << 19, 128, "bf16")           # 2^26 elements
 

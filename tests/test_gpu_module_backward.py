@@ -119,6 +119,47 @@ def test_module_backward_forced_three_pass_and_alias(dev, orc):
                                       alias=True), ref, "bf16")
 
 
+@pytest.mark.parametrize("shape", [(1, 140000, 256), (2, 262144, 256), (4, 65536, 128)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_module_backward_by_composition(shape, dev):
+    """Shapes whose oracle takes minutes (2^26-element slices), through the
+    projections-inside-the-passes backward, against the chain rule composed
+    from the validated mixer (forward, and backward for dgain) and float32
+    matrix products on the same device:
+        Z = X W_in, Z' = mixer(Z), dZ' = dY W_out^T, dZ = mixer(dZ') (the
+        mixer is self-adjoint), dX = dZ W_in^T, dW_in = X^T dZ, dW_out = Z'^T dY.
+    Both sides are float32 up to rounding order (the weight gradients' three-
+    term split leaves 2^-27), so the float32 bar holds for the float32
+    outputs; dX is bf16, rounded once."""
+    import torch
+
+    B, N, C = shape
+    d = whtmix.plan_describe(B, N, C, "bf16")
+    assert d["module_backward_fused"], d
+    gen = torch.Generator(device="cpu").manual_seed(N + C)
+    P = whtmix.padded_tokens(N)
+    x = torch.randn(B, N, C, generator=gen).to(dev).to(torch.bfloat16)
+    dy = torch.randn(B, N, C, generator=gen).to(dev).to(torch.bfloat16)
+    wi = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(torch.bfloat16)
+    wo = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(torch.bfloat16)
+    g = (torch.rand(P, C, generator=gen) + 0.5).to(dev)
+    say(f"module backward by composition {shape} bf16")
+    dx, dwi, dwo, dg = whtmix.module_backward(x, wi, g, wo, dy)
+    xf, dyf, wif, wof = x.float(), dy.float(), wi.float(), wo.float()
+    z = torch.matmul(xf, wif)
+    zp = whtmix.forward(z, g)
+    dzp = torch.matmul(dyf, wof.t().contiguous())
+    dz = whtmix.forward(dzp, g)
+    _, dg_ref = whtmix.backward(z, dzp, g, want_dx=False)
+    dx_ref = torch.matmul(dz, wif.t().contiguous())
+    dwi_ref = torch.matmul(xf.reshape(-1, C).t().contiguous(), dz.reshape(-1, C))
+    dwo_ref = torch.matmul(zp.reshape(-1, C).t().contiguous(), dyf.reshape(-1, C))
+    torch.cuda.synchronize(dev)
+    check("dx", to_host(dx), to_host(dx_ref), TOL["bf16"])
+    for name, a, r in [("dw_in", dwi, dwi_ref), ("dw_out", dwo, dwo_ref), ("dgain", dg, dg_ref)]:
+        check(name, to_host(a), to_host(r), GRAD_TOL)
+
+
 def test_module_backward_empty_batch_zeroes_gradients(dev):
     import torch
 
