@@ -105,15 +105,15 @@ inline WgradPlan wgrad_plan(uint64_t rows, int cbits)
 }
 
 // The block's backward runs its projections inside the mixer backward's
-// passes (bf16, THREE_PASS, when a gain gradient is requested: 32 <= C <= 128
-// on slices up to 2^25 elements, and C = 256 on 2^26..2^28, where the block's
-// and the mixer's splits agree); otherwise as projection kernels around the
-// mixer's forward and backward on float32 Z, Z' and dZ'.
+// passes (THREE_PASS, when a gain gradient is requested: 16 <= C <= 128 on
+// slices up to 2^25 elements, and bf16 C = 256 on 2^26..2^28, where the
+// block's and the mixer's splits agree); otherwise as projection kernels
+// around the mixer's forward and backward on float32 Z, Z' and dZ'.
 inline bool module_backward_fused(int plan, int cbits, int dtype, int K)
 {
-    if (plan != PLAN_THREE_PASS || dtype != DTYPE_BF16) return false;
-    if (cbits >= 5 && cbits <= kModuleMfmaMaxCbits) return K >= 12 && K <= 25;
-    return cbits == kPairModuleCbits && K >= 26 && K <= 28;
+    if (plan != PLAN_THREE_PASS) return false;
+    if (cbits >= kModuleMfmaMinCbits && cbits <= kModuleMfmaMaxCbits) return K >= 12 && K <= 25;
+    return dtype == DTYPE_BF16 && cbits == kPairModuleCbits && K >= 26 && K <= 28;
 }
 
 // A validated backward call of the block.  Workspace pieces (floats unless

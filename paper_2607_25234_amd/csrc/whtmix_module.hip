@@ -278,11 +278,13 @@ __device__ __forceinline__ uint32_t pack_x32_source(uint32_t idx, uint32_t C, in
 
 // Up to three packings in one launch: p[i] = w[i] packed in mode[i] for the
 // entries whose p[i] is not null.
-struct PackX32Jobs {
-    const __bf16 *w[3];
-    __bf16 *p[3];
+template <typename T>
+struct PackJobs {
+    const T *w[3];
+    T *p[3];
     int mode[3];
 };
+using PackX32Jobs = PackJobs<__bf16>;
 
 __global__ void __launch_bounds__(256)
 pack_x32_kernel(PackX32Jobs jobs, int cb)
@@ -294,6 +296,41 @@ pack_x32_kernel(PackX32Jobs jobs, int cb)
     for (int i = 0; i < 3; ++i)
         if (jobs.p[i])
             jobs.p[i][idx] = jobs.w[i][pack_x32_source(idx, C, jobs.mode[i])];
+}
+
+// The orders of pack_weights_kernel (the 16x16x16 bf16 products at C = 16 and
+// the 16x16x4 float32 ones) in the four modes of pack_x32_kernel.
+template <typename T>
+__device__ __forceinline__ uint32_t pack_std_source(uint32_t idx, uint32_t C, int mode)
+{
+    const uint32_t e = idx & 3u, lane = (idx >> 2) & 63u;
+    const uint32_t j = lane & 15u, q = lane >> 4;
+    const uint32_t rest = idx >> 8;
+    const bool pro = mode == PACK_PROLOGUE || mode == PACK_PROLOGUE_T;
+    uint32_t k, col;
+    if constexpr (sizeof(T) == 2) {
+        const uint32_t ks = C / 16u, kk = rest % ks, nb = rest / ks;
+        k = pro ? k_in_bf16(C, kk, q, e) : q * (C / 4u) + 4u * kk + e;
+        col = pro ? 16u * nb + j : oc_bf16(C, nb, j);
+    } else {
+        const uint32_t np = C / 16u, p = rest % np, nb = rest / np, s = 4u * p + e;
+        k = pro ? k_in_f32(s, q) : q * (C / 4u) + s;
+        col = 16u * nb + j;
+    }
+    return mode >= PACK_PROLOGUE_T ? col * C + k : k * C + col;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+pack_std_kernel(PackJobs<T> jobs, int cb)
+{
+    const uint32_t C = 1u << cb;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    if (idx >= C * C) return;
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+        if (jobs.p[i])
+            jobs.p[i][idx] = jobs.w[i][pack_std_source<T>(idx, C, jobs.mode[i])];
 }
 
 // X fragments of the prologue: per row block, the lane's C/4 channels of its
@@ -1985,14 +2022,13 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
 //   -> OUTER_INV of wsd with the epilogue: dZ (float32) and dX = dZ W_in^T;
 //      dW_in = X^T dZ                                                     [3]
 // Z and dZ' never reach memory: they exist only as the outer transforms.
-template <int K, int CB>
+template <typename T, int K, int CB>
 hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
 {
     constexpr Split sp = module_split(K);
     constexpr int A = sp.A, HB = sp.HB, R = sp.R;
     static_assert(A == three_pass_split(K).A && R == three_pass_split(K).R,
                   "the backward's middle phase runs the mixer's split");
-    using T = __bf16;
     const hipStream_t st = m.stream;
     const uint32_t rows = (uint32_t)(((uint64_t)m.B * m.nvalid) >> CB);
     const uint32_t CC = 1u << (2 * CB);
@@ -2001,10 +2037,14 @@ hipError_t module_backward_fused_k(const ModuleBackwardArgs &m)
     const T *w_in = static_cast<const T *>(m.w_in);
     T *pk = static_cast<T *>(m.wpack);
     T *p_in = pk, *p_out_t = pk + CC, *p_in_te = pk + 2 * CC;
-    const PackX32Jobs jobs{{w_in, static_cast<const T *>(m.w_out), w_in},
+    const PackJobs<T> jobs{{w_in, static_cast<const T *>(m.w_out), w_in},
                            {p_in, p_out_t, p_in_te},
                            {PACK_PROLOGUE, PACK_PROLOGUE_T, PACK_EPILOGUE_T}};
-    hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, jobs, CB);
+    if constexpr (Proj<T, CB>::X32)
+        hipLaunchKernelGGL(pack_x32_kernel, dim3((CC + 255u) / 256u), dim3(256), 0, st, jobs, CB);
+    else
+        hipLaunchKernelGGL((pack_std_kernel<T>), dim3((CC + 255u) / 256u), dim3(256), 0, st, jobs,
+                           CB);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = record(m.events[0], st)) != hipSuccess) return e;
@@ -2109,12 +2149,12 @@ hipError_t module_backward_fused_pair(const ModuleBackwardArgs &m)
     return record(m.events[3], st);
 }
 
-template <int CB>
+template <typename T, int CB>
 hipError_t module_backward_fused_cb(const ModuleBackwardArgs &m)
 {
     switch (m.K) {
 #define WHTMIX_MB_CASE(k) \
-    case k: return module_backward_fused_k<k, CB>(m);
+    case k: return module_backward_fused_k<T, k, CB>(m);
         WHTMIX_MB_CASE(12) WHTMIX_MB_CASE(13) WHTMIX_MB_CASE(14) WHTMIX_MB_CASE(15)
         WHTMIX_MB_CASE(16) WHTMIX_MB_CASE(17) WHTMIX_MB_CASE(18) WHTMIX_MB_CASE(19)
         WHTMIX_MB_CASE(20) WHTMIX_MB_CASE(21) WHTMIX_MB_CASE(22) WHTMIX_MB_CASE(23)
@@ -2132,10 +2172,12 @@ hipError_t module_backward(const ModuleBackwardArgs &m)
     if (want_dg && m.B > 0 && ((uint64_t)m.B << m.K) / 16u <= 0xffffffffull &&
         module_backward_fused(m.plan, m.cbits, m.dtype, m.K)) {
         switch (m.cbits) {
-        case 5: return module_backward_fused_cb<5>(m);
-        case 6: return module_backward_fused_cb<6>(m);
-        case 7: return module_backward_fused_cb<7>(m);
+        case 4: return module_backward_fused_cb<T, 4>(m);
+        case 5: return module_backward_fused_cb<T, 5>(m);
+        case 6: return module_backward_fused_cb<T, 6>(m);
+        case 7: return module_backward_fused_cb<T, 7>(m);
         case kPairCB:
+            if constexpr (!std::is_same<T, __bf16>::value) break;
             switch (m.K) {
             case 26: return module_backward_fused_pair<26>(m);
             case 27: return module_backward_fused_pair<27>(m);

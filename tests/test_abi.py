@@ -285,13 +285,14 @@ def test_block_paths():
 
 
 def test_block_backward_paths():
-    """The block's backward fuses its projections for bf16 32 <= C <= 128 on
-    three-pass slices up to 2^25 elements."""
+    """The block's backward fuses its projections for 16 <= C <= 128 on
+    three-pass slices up to 2^25 elements, and bf16 C = 256 on 2^26..2^28."""
     fused = lambda *a: whtmix.plan_describe(*a)["module_backward_fused"]
     assert fused(4, 65536, 128, "bf16")
     assert fused(1, 3000, 32, "bf16") and fused(2, 128, 128, "bf16", "three_pass")
-    assert not fused(4, 65536, 128, "f32")              # float32
-    assert not fused(1, 65536, 16, "bf16")              # C = 16: VALU-sized products
+    assert fused(4, 65536, 128, "f32") and fused(1, 65536, 16, "bf16")
+    assert not fused(1, 65536, 8, "bf16")               # C = 8: VALU projections
+    assert not fused(1, 262144, 256, "f32")             # float32 C = 256
     assert fused(1, 262144, 256, "bf16") and fused(1, 1 << 20, 256, "bf16")   # C = 256, 2^26..2^28
     assert not fused(1, 65536, 256, "bf16")             # C = 256 below 2^26 (module split)
     assert not fused(1, 1 << 21, 256, "bf16")           # 2^29

@@ -119,9 +119,11 @@ def test_module_backward_forced_three_pass_and_alias(dev, orc):
                                       alias=True), ref, "bf16")
 
 
-@pytest.mark.parametrize("shape", [(1, 140000, 256), (2, 262144, 256), (4, 65536, 128)],
-                         ids=lambda s: "x".join(map(str, s)))
-def test_module_backward_by_composition(shape, dev):
+@pytest.mark.parametrize("shape,dtype", [((1, 140000, 256), "bf16"), ((2, 262144, 256), "bf16"),
+                                         ((4, 65536, 128), "bf16"), ((2, 16384, 128), "f32"),
+                                         ((32, 4096, 64), "f32"), ((1, 65536, 16), "bf16")],
+                         ids=lambda s: "x".join(map(str, s)) if isinstance(s, tuple) else s)
+def test_module_backward_by_composition(shape, dtype, dev):
     """Shapes whose oracle takes minutes (2^26-element slices), through the
     projections-inside-the-passes backward, against the chain rule composed
     from the validated mixer (forward, and backward for dgain) and float32
@@ -130,20 +132,22 @@ def test_module_backward_by_composition(shape, dev):
         mixer is self-adjoint), dX = dZ W_in^T, dW_in = X^T dZ, dW_out = Z'^T dY.
     Both sides are float32 up to rounding order (the weight gradients' three-
     term split leaves 2^-27), so the float32 bar holds for the float32
-    outputs; dX is bf16, rounded once."""
+    outputs; dX in bf16 is rounded once."""
     import torch
 
     B, N, C = shape
-    d = whtmix.plan_describe(B, N, C, "bf16")
+    d = whtmix.plan_describe(B, N, C, dtype)
     assert d["module_backward_fused"], d
     gen = torch.Generator(device="cpu").manual_seed(N + C)
     P = whtmix.padded_tokens(N)
-    x = torch.randn(B, N, C, generator=gen).to(dev).to(torch.bfloat16)
-    dy = torch.randn(B, N, C, generator=gen).to(dev).to(torch.bfloat16)
-    wi = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(torch.bfloat16)
-    wo = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(torch.bfloat16)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = torch.randn(B, N, C, generator=gen).to(dev).to(tdt)
+    dy = torch.randn(B, N, C, generator=gen).to(dev).to(tdt)
+    wi = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(tdt)
+    wo = (torch.randn(C, C, generator=gen) / C ** 0.5).to(dev).to(tdt)
     g = (torch.rand(P, C, generator=gen) + 0.5).to(dev)
-    say(f"module backward by composition {shape} bf16")
+    say(f"module backward by composition {shape} {dtype}")
+    torch.backends.cuda.matmul.allow_tf32 = False   # float32 products in float32
     dx, dwi, dwo, dg = whtmix.module_backward(x, wi, g, wo, dy)
     xf, dyf, wif, wof = x.float(), dy.float(), wi.float(), wo.float()
     z = torch.matmul(xf, wif)
@@ -155,7 +159,7 @@ def test_module_backward_by_composition(shape, dev):
     dwi_ref = torch.matmul(xf.reshape(-1, C).t().contiguous(), dz.reshape(-1, C))
     dwo_ref = torch.matmul(zp.reshape(-1, C).t().contiguous(), dyf.reshape(-1, C))
     torch.cuda.synchronize(dev)
-    check("dx", to_host(dx), to_host(dx_ref), TOL["bf16"])
+    check("dx", to_host(dx), to_host(dx_ref), TOL[dtype])
     for name, a, r in [("dw_in", dwi, dwi_ref), ("dw_out", dwo, dwo_ref), ("dgain", dg, dg_ref)]:
         check(name, to_host(a), to_host(r), GRAD_TOL)
 
