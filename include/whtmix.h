@@ -269,8 +269,8 @@ WHTMIX_API int whtmix_module_forward_separable(const void *x, const void *w_in,
  *     dZ' = dY W_out^T,            dW_out = sum over b of Z'^T dY,
  *     dZ, dgain = the mixer's gradients (whtmix_backward) at (Z, dZ'),
  *     dX = dZ W_in^T,              dW_in  = sum over b of X^T dZ,
- * with Z = X W_in and Z' = mixer(Z) recomputed in float32.  For bf16 with
- * 32 <= C <= 128 on three-pass slices up to 2^25 elements, and C = 256 on
+ * with Z = X W_in and Z' = mixer(Z) recomputed in float32.  For 16 <= C <=
+ * 128 on three-pass slices up to 2^25 elements, and bf16 C = 256 on
  * 2^26..2^28 (with a requested gain gradient), the projections run inside
  * the mixer backward's passes and Z and dZ' are never stored
  * (whtmix_plan_describe's module_backward_fused).
