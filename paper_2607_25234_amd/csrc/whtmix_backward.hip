@@ -121,7 +121,7 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
             o[GM::at((uint32_t)k << G::SL)] = vx[k] * vd[k] * scale;
         __builtin_amdgcn_sched_barrier(0);   // keep the gain loads after the product
         float gv[V];
-        gain.template load<G::SL, GM>(gv, run << R, tau);
+        gain.template load<G::SL, GM, true>(gv, run << R, tau);
         if constexpr (MIX_X) {
             apply_gain<A + HB>(vx, gv);
             if constexpr (G::NBOT > 0)
@@ -139,7 +139,7 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
 #pragma unroll
         for (int k = 0; k < V; ++k)
             acc[k] = 0.0f;
-        gain.template load<G::SL, GM>(gv, run << R, tau);   // the same for every slice
+        gain.template load<G::SL, GM, true>(gv, run << R, tau);   // the same for every slice
         for (uint32_t b = b0; b < b1; ++b) {   // uniform over the workgroup
             const bool more = b + 1 < b1;
             butterflies<G::JT, VB>(vx);

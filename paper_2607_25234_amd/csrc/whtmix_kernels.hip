@@ -119,7 +119,7 @@ middle_kernel(float *__restrict__ ws, Gain gain, uint32_t nslices)
         buffer(ws + (b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
     float v[V], gv[V];
     load_layout<G::TOP, ContigMap, float>(v, tile, tau);
-    gain.template load<G::SL, GainMap<A, R>>(gv, run << R, tau);
+    gain.template load<G::SL, GainMap<A, R>, true>(gv, run << R, tau);
     butterflies<G::JT, VB>(v);
     forward_groups<M, R, 0, G::TOP>(lds, v, tau);
     apply_gain<A + HB>(v, gv);
