@@ -193,6 +193,17 @@ hipError_t launch_fused_pair(const T *x, T *y, Gain gain, const LaunchArgs &a)
     return record(a.events[1], a.stream);
 }
 
+template <int A, int HB, int R, class Gain>
+hipError_t launch_middle_split(const LaunchArgs &a, Gain gain)
+{
+    static_assert(HB >= 1 && HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
+    return with_middle_gain(gain, a.B, [&](auto g) {
+        hipLaunchKernelGGL((middle_kernel<A, HB, R, decltype(g)>), dim3((uint32_t)(a.B << (A - R))),
+                           dim3(1u << (HB + R - VB)), 0, a.stream, a.ws, g, (uint32_t)a.B);
+        return hipGetLastError();
+    });
+}
+
 template <int K, typename T, class Gain>
 hipError_t launch_three_pass(const T *x, T *y, Gain gain, const LaunchArgs &a)
 {
@@ -206,9 +217,7 @@ hipError_t launch_three_pass(const T *x, T *y, Gain gain, const LaunchArgs &a)
     if (e != hipSuccess) return e;
     if ((e = launch_outer_fwd<K, T>(x, a.ws, a.B, a.nvalid, st)) != hipSuccess) return e;
     if ((e = record(a.events[1], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((middle_kernel<A, HB, R, Gain>), dim3((uint32_t)(a.B << (A - R))),
-                       dim3(1u << (HB + R - VB)), 0, st, a.ws, gain, (uint32_t)a.B);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_middle_split<A, HB, R>(a, gain)) != hipSuccess) return e;
     if ((e = record(a.events[2], st)) != hipSuccess) return e;
     if ((e = launch_outer_inv<K, T>(a.ws, y, a.B, a.nvalid, st)) != hipSuccess) return e;
     return record(a.events[3], st);
@@ -256,14 +265,6 @@ hipError_t dispatch(const LaunchArgs &a, Gain gain)
     }
 }
 
-template <int A, int HB, int R, class Gain>
-hipError_t launch_middle_split(const LaunchArgs &a, Gain gain)
-{
-    static_assert(HB >= 1 && HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
-    hipLaunchKernelGGL((middle_kernel<A, HB, R, Gain>), dim3((uint32_t)(a.B << (A - R))),
-                       dim3(1u << (HB + R - VB)), 0, a.stream, a.ws, gain, (uint32_t)a.B);
-    return hipGetLastError();
-}
 
 template <int K, class Gain>
 hipError_t launch_middle_k(const LaunchArgs &a, Gain gain)

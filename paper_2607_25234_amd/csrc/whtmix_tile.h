@@ -501,25 +501,32 @@ __device__ __forceinline__ void store_tile_vec(const float (&v)[V], T *base, uin
 // faster than buffer loads on gfx950.  It is requested right after the data
 // tile so its latency overlaps the forward butterflies.
 
-// Joint per-frequency gain G[N_pad][C] (linear).
-struct FullGain {
+// Joint per-frequency gain G[N_pad][C] (linear).  NT: the middle pass's
+// loads (MIDDLE) are non-temporal.  The host picks it for a batch of one
+// slice, whose middle pass reads each gain element exactly once, so the gain
+// does not displace the workspace in the Infinity Cache (stereo256k 334 ->
+// 309 us per step); with more slices each gain tile is read once per slice
+// on one XCD and temporal loads let those reads hit (non-temporal ones cost
+// text4k, 32 slices, 38 -> 42 us).  A type, not a run-time flag: the
+// compiler merges the loads of the two branches of a flag and drops the hint.
+template <bool NT>
+struct FullGainT {
     const float *g;
-    // Each register's base (uniform) is a scalar pointer and the thread's
-    // part a 32-bit byte offset, so every load is one global_load with a
-    // scalar base: no 64-bit vector address per register.  STREAM: the middle
-    // pass reads each gain element once per call (its B slices on adjacent
-    // tiles of one XCD): non-temporal loads keep the gain from displacing the
-    // workspace in the Infinity Cache (stereo256k 334 -> 309 us per step).
-    template <int S, class Map, bool STREAM = false>
+    // Each register's base (uniform) is a scalar pointer into global memory
+    // and the thread's part a 32-bit byte offset, so every load is one
+    // global_load with a scalar base: no 64-bit vector address per register,
+    // and (unlike a flat load) no share of the LDS wait counter.
+    template <int S, class Map, bool MIDDLE = false>
     __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
     {
+        typedef const __attribute__((address_space(1))) float gfloat;
         const uint32_t voff = Map::at(layout_base<S>(tau)) * 4u;
 #pragma unroll
         for (int k = 0; k < V; ++k) {
             const char *row = reinterpret_cast<const char *>(g + f0 + Map::at((uint32_t)k << S));
             asm("" : "+s"(row));   // opaque scalar base: not re-associated into a vector one
-            const float *p = reinterpret_cast<const float *>(row + voff);
-            if constexpr (STREAM)
+            gfloat *p = (gfloat *)(row + voff);
+            if constexpr (NT && MIDDLE)
                 gv[k] = __builtin_nontemporal_load(p);
             else
                 gv[k] = *p;
@@ -527,6 +534,21 @@ struct FullGain {
     }
     __device__ __forceinline__ float at(uint32_t f) const { return g[f]; }
 };
+using FullGain = FullGainT<false>;
+using StreamedGain = FullGainT<true>;
+
+// Calls f with the gain a middle pass over `slices` slices reads: the
+// streamed form of a joint gain for one slice, else the gain itself.
+template <class Gain, class F>
+inline hipError_t with_middle_gain(Gain gain, int64_t, F &&f)
+{
+    return f(gain);
+}
+template <class F>
+inline hipError_t with_middle_gain(FullGain gain, int64_t slices, F &&f)
+{
+    return slices == 1 ? f(StreamedGain{gain.g}) : f(gain);
+}
 
 // The paper's parametrisation (eqs. (2)-(3)): log-domain gains g_t[N_pad]
 // over token frequencies and g_c[C] over channel frequencies; the gain of
@@ -542,7 +564,7 @@ struct LogSeparableGain {
     {
         return __expf(gt[f >> cbits] + gc[f & ((1u << cbits) - 1u)]);
     }
-    template <int S, class Map, bool STREAM = false>
+    template <int S, class Map, bool MIDDLE = false>
     __device__ __forceinline__ void load(float (&gv)[V], uint32_t f0, uint32_t tau) const
     {
         const uint32_t fb = f0 + Map::at(layout_base<S>(tau));
