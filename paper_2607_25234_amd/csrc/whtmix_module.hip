@@ -1900,16 +1900,29 @@ wgrad_valu_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
 
 // out[g][i] = sum over the chunks c of group g = blockIdx.y (ascending, at
 // most `group` of them) of part[c][i]; with one group this is the total.
-__global__ void __launch_bounds__(256)
+// Eight loads are issued before their adds (in the same ascending order), so
+// a thread waits for one memory round trip per eight chunks, not per chunk.
+constexpr uint32_t kSumThreads = 64;
+__global__ void __launch_bounds__(kSumThreads)
 sum_partials_kernel(const float *__restrict__ part, float *__restrict__ out, uint32_t n,
                     uint32_t chunks, uint32_t group)
 {
-    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t i = blockIdx.x * kSumThreads + threadIdx.x;
     if (i >= n) return;
     const uint32_t c0 = blockIdx.y * group;
     const uint32_t c1 = min(chunks, c0 + group);
     float s = 0.0f;
-    for (uint32_t c = c0; c < c1; ++c)
+    uint32_t c = c0;
+    for (; c + 8u <= c1; c += 8u) {
+        float v[8];
+#pragma unroll
+        for (uint32_t j = 0; j < 8u; ++j)
+            v[j] = part[(size_t)(c + j) * n + i];
+#pragma unroll
+        for (uint32_t j = 0; j < 8u; ++j)
+            s += v[j];
+    }
+    for (; c < c1; ++c)
         s += part[(size_t)c * n + i];
     out[(size_t)blockIdx.y * n + i] = s;
 }
@@ -1998,18 +2011,18 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // fixed-order sum: groups of consecutive chunks, then the groups
-    const uint32_t n = C * C, nb = (n + 255u) / 256u;
+    const uint32_t n = C * C, nb = (n + kSumThreads - 1u) / kSumThreads;
     if (wp.chunks <= kWgradGroup) {
-        hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(256), 0, st, part, out, n,
+        hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(kSumThreads), 0, st, part, out, n,
                            wp.chunks, kWgradGroup);
         return hipGetLastError();
     }
     float *gsum = part + (size_t)wp.chunks * n;
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb, wp.groups()), dim3(256), 0, st, part, gsum, n,
-                       wp.chunks, kWgradGroup);
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb, wp.groups()), dim3(kSumThreads), 0, st, part,
+                       gsum, n, wp.chunks, kWgradGroup);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(256), 0, st, gsum, out, n, wp.groups(),
-                       wp.groups());
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(kSumThreads), 0, st, gsum, out, n,
+                       wp.groups(), wp.groups());
     return hipGetLastError();
 }
 
