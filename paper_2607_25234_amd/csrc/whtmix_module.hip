@@ -1764,9 +1764,9 @@ __device__ __forceinline__ bf16x8 bf16_exact8(const f32x4 &z0, const f32x4 &z1)
     return __builtin_bit_cast(bf16x8, o);
 }
 
-// TOUT: store the transposed block (the caller passed B and A to get dW^T's
-// blocks, i.e. dW's).
-template <typename Ta, typename Tb, int T, bool TOUT>
+// Partial blocks are stored as computed, rows of a by columns of b (a caller
+// that passed B and A gets dW^T and transposes in the final sum).
+template <typename Ta, typename Tb, int T>
 __global__ void __launch_bounds__(256)
 wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__restrict__ part,
                   uint32_t rows, uint32_t rpc, int cb)
@@ -1876,7 +1876,7 @@ wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
             for (int r = 0; r < 4; ++r) {
                 const uint32_t row = c0 + 16u * (tr0 + x) + 4u * q + r;
                 const uint32_t col = d0 + 16u * (tc0 + y) + i;
-                out[TOUT ? (size_t)col * C + row : (size_t)row * C + col] = acc[x][y][r];
+                out[(size_t)row * C + col] = acc[x][y][r];
             }
 }
 
@@ -1900,12 +1900,14 @@ wgrad_valu_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
 
 // out[g][i] = sum over the chunks c of group g = blockIdx.y (ascending, at
 // most `group` of them) of part[c][i]; with one group this is the total.
-// Eight loads are issued before their adds (in the same ascending order), so
-// a thread waits for one memory round trip per eight chunks, not per chunk.
+// tcb > 0: part holds C x C matrices (C = 2^tcb) and out gets the transposed
+// sum.  Eight loads are issued before their adds (in the same ascending
+// order), so a thread waits for one memory round trip per eight chunks, not
+// per chunk.
 constexpr uint32_t kSumThreads = 64;
 __global__ void __launch_bounds__(kSumThreads)
 sum_partials_kernel(const float *__restrict__ part, float *__restrict__ out, uint32_t n,
-                    uint32_t chunks, uint32_t group)
+                    uint32_t chunks, uint32_t group, uint32_t tcb)
 {
     const uint32_t i = blockIdx.x * kSumThreads + threadIdx.x;
     if (i >= n) return;
@@ -1924,7 +1926,8 @@ sum_partials_kernel(const float *__restrict__ part, float *__restrict__ out, uin
     }
     for (; c < c1; ++c)
         s += part[(size_t)c * n + i];
-    out[(size_t)blockIdx.y * n + i] = s;
+    const uint32_t o = tcb ? ((i & ((1u << tcb) - 1u)) << tcb) | (i >> tcb) : i;
+    out[(size_t)blockIdx.y * n + o] = s;
 }
 
 template <typename T>
@@ -1979,13 +1982,14 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
 {
     const uint32_t C = 1u << cb;
     const WgradPlan wp = wgrad_plan(rows, cb);
+    // A float a against a bf16 b runs on the matrix cores as (b, a), whose sum
+    // is transposed at the end: the kernel with the bf16 operand first keeps
+    // fewer registers (two workgroups per CU at T = 128 instead of one).
+    constexpr bool SWAP = sizeof(Ta) == 4 && sizeof(Tb) == 2;
+    const bool swapped = SWAP && C >= 16;
     if (wp.chunks == 0) {
         // no rows: sum_partials over zero chunks writes zeros
     } else if (C >= 16) {
-        // A float a against a bf16 b runs as (b, a) with the blocks stored
-        // transposed: the kernel with the bf16 operand first keeps fewer
-        // registers (two workgroups per CU at T = 128 instead of one).
-        constexpr bool SWAP = sizeof(Ta) == 4 && sizeof(Tb) == 2;
         using T1 = std::conditional_t<SWAP, Tb, Ta>;
         using T2 = std::conditional_t<SWAP, Ta, Tb>;
         const T1 *p1 = reinterpret_cast<const T1 *>(SWAP ? (const void *)b : (const void *)a);
@@ -1993,16 +1997,16 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
         const uint32_t T = C < 128u ? C : 128u;
         const dim3 grid((C / T) * (C / T), wp.chunks);
         if (T == 16)
-            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 16, SWAP>), grid, dim3(256), 0, st, p1,
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 16>), grid, dim3(256), 0, st, p1,
                                p2, part, rows, wp.rows_per_chunk, cb);
         else if (T == 32)
-            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 32, SWAP>), grid, dim3(256), 0, st, p1,
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 32>), grid, dim3(256), 0, st, p1,
                                p2, part, rows, wp.rows_per_chunk, cb);
         else if (T == 64)
-            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 64, SWAP>), grid, dim3(256), 0, st, p1,
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 64>), grid, dim3(256), 0, st, p1,
                                p2, part, rows, wp.rows_per_chunk, cb);
         else
-            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 128, SWAP>), grid, dim3(256), 0, st, p1,
+            hipLaunchKernelGGL((wgrad_mfma_kernel<T1, T2, 128>), grid, dim3(256), 0, st, p1,
                                p2, part, rows, wp.rows_per_chunk, cb);
     } else {
         hipLaunchKernelGGL((wgrad_valu_kernel<Ta, Tb>), dim3(wp.chunks), dim3(256), 0, st, a, b,
@@ -2012,17 +2016,18 @@ hipError_t wgrad(const Ta *a, const Tb *b, float *part, float *out, uint32_t row
     if (e != hipSuccess) return e;
     // fixed-order sum: groups of consecutive chunks, then the groups
     const uint32_t n = C * C, nb = (n + kSumThreads - 1u) / kSumThreads;
+    const uint32_t tcb = swapped ? (uint32_t)cb : 0u;
     if (wp.chunks <= kWgradGroup) {
         hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(kSumThreads), 0, st, part, out, n,
-                           wp.chunks, kWgradGroup);
+                           wp.chunks, kWgradGroup, tcb);
         return hipGetLastError();
     }
     float *gsum = part + (size_t)wp.chunks * n;
     hipLaunchKernelGGL(sum_partials_kernel, dim3(nb, wp.groups()), dim3(kSumThreads), 0, st, part,
-                       gsum, n, wp.chunks, kWgradGroup);
+                       gsum, n, wp.chunks, kWgradGroup, 0u);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(sum_partials_kernel, dim3(nb), dim3(kSumThreads), 0, st, gsum, out, n,
-                       wp.groups(), wp.groups());
+                       wp.groups(), wp.groups(), tcb);
     return hipGetLastError();
 }
 

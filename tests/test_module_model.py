@@ -847,7 +847,7 @@ def model_wgrad(a, b, cb, kinds=("f32", "f32")):
     take, for k-slot e, row kb + q + 4e (16x16x32 bf16 instruction, 32 rows)
     or row kb + q (float32 instruction, 4 rows) of column i.  kinds: the dtypes of
     a and b; a float against a bf16 operand is split into three bf16 terms."""
-    if kinds == ("f32", "bf16"):   # run as (b, a), blocks stored transposed
+    if kinds == ("f32", "bf16"):   # run as (b, a), the sum transposed at the end
         return model_wgrad(b, a, cb, ("bf16", "f32")).T
     rows, C = a.shape
     chunks, rpc = wgrad_plan(rows, cb)
