@@ -1686,7 +1686,9 @@ pack_b_kernel(const T *__restrict__ w, T *__restrict__ p, int cb, int trans)
 //                      term goes through the bf16 instruction.
 template <typename Ta, typename Tb, int T>
 struct WgradShape {
-    static constexpr int RB = 64;                          // rows per LDS block
+    // rows per LDS block: 32 for float32 x float32 at T = 128, whose 64-row
+    // prefetch would leave one workgroup per CU; 64 otherwise
+    static constexpr int RB = sizeof(Ta) == 4 && sizeof(Tb) == 4 && T == 128 ? 32 : 64;
     static constexpr int LDW = T == 16 ? 48 : T + 16;      // padded LDS row (floats)
     static constexpr int TQ = T >= 32 ? T / 32 : 1;        // tiles per wave side
     static constexpr int VA = 16 / (int)sizeof(Ta);        // elements per 16-byte load
@@ -1695,7 +1697,7 @@ struct WgradShape {
     static constexpr int NB = (RB * T / VBL + 255) / 256;
 };
 
-template <typename Te, int VE, int N, int T>
+template <typename Te, int VE, int N, int T, int RB>
 __device__ __forceinline__ void wgrad_fetch(u32x4 (&r)[N], const Te *__restrict__ src, uint32_t C,
                                             uint32_t col0, uint32_t row0, uint32_t row_end)
 {
@@ -1705,20 +1707,20 @@ __device__ __forceinline__ void wgrad_fetch(u32x4 (&r)[N], const Te *__restrict_
         const uint32_t v = threadIdx.x + 256u * (uint32_t)n;
         const uint32_t row = row0 + v / PER_ROW;
         r[n] = (u32x4){0u, 0u, 0u, 0u};
-        if (v < 64u * PER_ROW && row < row_end)
+        if (v < (uint32_t)RB * PER_ROW && row < row_end)
             r[n] = *reinterpret_cast<const u32x4 *>(src + (size_t)row * C + col0 +
                                                     (v % PER_ROW) * VE);
     }
 }
 
-template <typename Te, int VE, int N, int T, int LDW>
+template <typename Te, int VE, int N, int T, int LDW, int RB>
 __device__ __forceinline__ void wgrad_stage(float *lds, const u32x4 (&r)[N])
 {
     constexpr uint32_t PER_ROW = T / VE;
 #pragma unroll
     for (int n = 0; n < N; ++n) {
         const uint32_t v = threadIdx.x + 256u * (uint32_t)n;
-        if (v >= 64u * PER_ROW) continue;
+        if (v >= (uint32_t)RB * PER_ROW) continue;
         float *dst = lds + (v / PER_ROW) * LDW + (v % PER_ROW) * VE;
         if constexpr (VE == 4) {
             *reinterpret_cast<f32x4 *>(dst) = __builtin_bit_cast(f32x4, r[n]);
@@ -1794,16 +1796,16 @@ wgrad_mfma_kernel(const Ta *__restrict__ a, const Tb *__restrict__ b, float *__r
         for (int y = 0; y < TQ; ++y)
             acc[x][y] = (f32x4){0.0f, 0.0f, 0.0f, 0.0f};
     u32x4 ra[S::NA], rb[S::NB];
-    wgrad_fetch<Ta, S::VA, S::NA, T>(ra, a, C, c0, r_begin, r_end);
-    wgrad_fetch<Tb, S::VBL, S::NB, T>(rb, b, C, d0, r_begin, r_end);
+    wgrad_fetch<Ta, S::VA, S::NA, T, S::RB>(ra, a, C, c0, r_begin, r_end);
+    wgrad_fetch<Tb, S::VBL, S::NB, T, S::RB>(rb, b, C, d0, r_begin, r_end);
     for (uint32_t r0 = r_begin; r0 < r_end; r0 += S::RB) {   // uniform over the workgroup
         __syncthreads();   // the previous block's readers are done
-        wgrad_stage<Ta, S::VA, S::NA, T, LDW>(sa, ra);
-        wgrad_stage<Tb, S::VBL, S::NB, T, LDW>(sb, rb);
+        wgrad_stage<Ta, S::VA, S::NA, T, LDW, S::RB>(sa, ra);
+        wgrad_stage<Tb, S::VBL, S::NB, T, LDW, S::RB>(sb, rb);
         __syncthreads();
         if (r0 + S::RB < r_end) {
-            wgrad_fetch<Ta, S::VA, S::NA, T>(ra, a, C, c0, r0 + S::RB, r_end);
-            wgrad_fetch<Tb, S::VBL, S::NB, T>(rb, b, C, d0, r0 + S::RB, r_end);
+            wgrad_fetch<Ta, S::VA, S::NA, T, S::RB>(ra, a, C, c0, r0 + S::RB, r_end);
+            wgrad_fetch<Tb, S::VBL, S::NB, T, S::RB>(rb, b, C, d0, r0 + S::RB, r_end);
         }
         if (!active)
             continue;

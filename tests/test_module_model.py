@@ -842,7 +842,8 @@ def bf16_rne(v):
 
 
 def model_wgrad(a, b, cb, kinds=("f32", "f32")):
-    """wgrad_mfma_kernel: per (chunk, T x T block), 64-row LDS blocks, waves
+    """wgrad_mfma_kernel: per (chunk, T x T block), LDS blocks of RB rows (32
+    for float32 x float32 at T = 128, else 64), waves
     owning TQ x TQ quadrants of 16 x 16 tiles; in a step the lanes (i, q)
     take, for k-slot e, row kb + q + 4e (16x16x32 bf16 instruction, 32 rows)
     or row kb + q (float32 instruction, 4 rows) of column i.  kinds: the dtypes of
@@ -854,6 +855,7 @@ def model_wgrad(a, b, cb, kinds=("f32", "f32")):
     T = min(C, 128)
     TQ = T // 32 if T >= 32 else 1
     f32 = kinds == ("f32", "f32")
+    RB = 32 if f32 and T == 128 else 64
     part = np.full((chunks, C, C), np.nan)
     lanes = np.arange(64)
     i, q = lanes & 15, lanes >> 4
@@ -875,9 +877,9 @@ def model_wgrad(a, b, cb, kinds=("f32", "f32")):
             for w in range(4 if T >= 32 else 1):
                 tr0, tc0 = ((w >> 1) * TQ, (w & 1) * TQ) if T >= 32 else (0, 0)
                 acc = {(x, y): np.zeros((64, 4)) for x in range(TQ) for y in range(TQ)}
-                for r0 in range(ch * rpc, r_end, 64):
+                for r0 in range(ch * rpc, r_end, RB):
                     step = 4 if f32 else 32
-                    for kb in range(0, 64, step):
+                    for kb in range(0, RB, step):
                         slots = [kb + q] if f32 else [kb + q + 4 * e for e in range(8)]
                         for x in range(TQ):
                             for y in range(TQ):
@@ -919,7 +921,8 @@ def mfma_k(av, bv, acc):
     return out
 
 
-@pytest.mark.parametrize("rows,cb", [(130, 4), (77, 5), (300, 7), (4, 6), (1100, 4), (70, 8)])
+@pytest.mark.parametrize("rows,cb", [(130, 4), (77, 5), (300, 7), (1000, 7), (4, 6), (1100, 4),
+                                     (70, 8)])
 @pytest.mark.parametrize("kinds", [("f32", "f32"), ("f32", "bf16"), ("bf16", "f32"),
                                    ("bf16", "bf16")])
 def test_weight_gradient_model(rows, cb, kinds):
