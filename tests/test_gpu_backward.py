@@ -47,7 +47,7 @@ def inputs(B, N, C, dtype, seed):
 # 2x9216x64), several slices per chunk (6x8192x32) and a short last chunk
 # (7x8192x32: chunks of 2, 2, 2, 1); 5x1x2 sums chunks of a 2-element slice.
 SHAPES = [(1, 1, 1), (5, 1, 2), (3, 32, 32), (3000, 16, 16), (2, 64, 64), (40, 128, 128), (5, 1000, 16),
-          (2, 4096, 64), (2, 9216, 64), (6, 8192, 32), (7, 8192, 32)]
+          (2, 4096, 64), (2, 9216, 64), (6, 8192, 32), (7, 8192, 32), (1, 4096, 64), (1, 9000, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
