@@ -191,7 +191,7 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
         "module_separable": lambda: orc.whtmix_module_separable(x, wi, gt, gc, wo),
     }[op]
     runs, t_total = 0, 0.0
-    while runs == 0 or (t_total < seconds and runs < 50):
+    while runs == 0 or (t_total < seconds and runs < 1000):
         t0 = time.perf_counter()
         call()
         t_total += time.perf_counter() - t0
