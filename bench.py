@@ -1,31 +1,45 @@
 #!/usr/bin/env python3
 """WHTMix forward throughput on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--op OP]
 
 A step is one whtmix_forward call (every kernel of the plan) over one batch of
 the workload (default: stereo64k_bf16, B=4, N=65536, C=128, bf16 in/out,
 float32 gain and arithmetic).  --op separable / backward / backward_separable
-/ module / module_separable time the other entry points the same way (module:
-the whole block with its W_in / W_out projections, eqs. (1)-(4)).  Inputs are resident in HBM before timing.
-Steps rotate over several input/output sets whose total footprint is at
-least twice the 256 MB Infinity Cache, so every step reads x and G from HBM.
+/ module / module_separable / module_backward time the other entry points the
+same way (module: the whole block with its W_in / W_out projections, eqs.
+(1)-(4)).  Inputs are resident in HBM before timing.
 
-Prints one JSON line: GB/s of ideal traffic (read x + read G once + write y)
-per second of wall time over K steps, tokens/s, the fraction of the 8 TB/s
-HBM peak, a roofline record for the longest kernel (its average duration
-from HIP events recorded on the launch stream during the timed steps), and
-the CPU oracle's rate on a bounded sample of the same workload.  Per-kernel
-events are recorded on every --event-every-th timed step.
+Steps rotate over input/output sets whose total footprint is at least twice
+the 256 MB Infinity Cache, so every step reads its inputs from HBM (cold).
+
+Prints one JSON line:
+- value: GB/s of ideal traffic (read x + read G once + write y) per second of
+  wall time over the K timed steps; tokens/s; fraction of the 8 TB/s peak;
+- roofline: the whole call (every kernel of the plan) as the unit: ideal
+  bytes over the call's GPU time from HIP events recorded by the library on
+  the launch stream around each timed call; `traffic` is the whole call's
+  rocprofv3 FETCH_SIZE + WRITE_SIZE bytes (committed counter record, null when
+  taken on other kernel sources) and `traffic_ratio` that over the ideal bytes;
+- per_call: median / p10 / p90 of >= 100 further calls, each in its own event
+  pair, rotating over the sets (`rotating`) and with a 1 GiB scrub written
+  between calls outside the pair (`cold`);
+- floor_ms: the same traffic as the three-pass plan moved by plain PyTorch
+  copies (widen x to float32, multiply a float32 buffer by G in place, narrow
+  to y): what an exact float32-exchange schedule of this shape cannot beat;
+- kernels: each kernel's average time and rate on its own design bytes
+  (x, y, the gain and the float32 workspace round trips), not ideal bytes;
+- cpu_baseline: the float64 CPU oracle on a bounded sample, on all host cores
+  and on one core, with the host CPU model.
 """
 from __future__ import annotations
 
 import argparse
 import ctypes
 import hashlib
-import glob
 import json
 import os
+import platform
 import sys
 import time
 
@@ -36,6 +50,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak, GB/s
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix-core peaks
 METRIC = "WHTMix forward GB/s and tokens/s at 1 MI355X; % of HBM roofline"
 MALL_BYTES = 256 * 1024 * 1024
+SCRUB_BYTES = 1 << 30
+MAX_SETS = 2048
 
 
 def log(*a):
@@ -59,18 +75,21 @@ def kernel_source_hash(files=FORWARD_SOURCES) -> str:
 
 def kernel_names(plan: str) -> list[str]:
     return {"three_pass": ["outer_fwd", "middle", "outer_inv"],
-            "fused": ["fused"], "small": ["small"]}[plan]
+            "fused": ["fused"], "small": ["small"], "one_launch": ["one_launch"]}[plan]
 
 
 def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) -> list[int]:
-    """Bytes each kernel of the forward plan must move by its definition
-    (N here is the padded token count; gbytes: bytes of the gain read once)."""
+    """Design bytes each kernel of the forward plan moves (N here is the
+    padded token count; gbytes: bytes of the gain read once).  The one-launch
+    plan runs all three passes in one kernel, so its design bytes are the
+    three-pass plan's summed."""
     L = N * C
     if plan in ("fused", "small"):
         return [B * L * 2 * s + gbytes]
-    return [B * L * (s + 4),           # read x, write float32 workspace
-            B * L * 8 + gbytes,        # read + write workspace, read the gain once
-            B * L * (4 + s)]           # read workspace, write y
+    three = [B * L * (s + 4),           # read x, write float32 workspace
+             B * L * 8 + gbytes,        # read + write workspace, read the gain once
+             B * L * (4 + s)]           # read workspace, write y
+    return [sum(three)] if plan == "one_launch" else three
 
 
 OPS = ("forward", "separable", "backward", "backward_separable", "module", "module_separable",
@@ -123,6 +142,19 @@ def ideal_bytes(op: str, B: int, N: int, P: int, C: int, s: int) -> int:
     return 2 * xy + 4 * (P + C) + wb  # module_separable
 
 
+def input_sets(footprint: int) -> int:
+    """Sets to rotate over so that their total footprint is at least twice
+    the Infinity Cache (capped for tiny workloads)."""
+    return max(2, min(MAX_SETS, -(-2 * MALL_BYTES // max(1, footprint)) + 1))
+
+
+def percentiles(v: list[float]) -> dict:
+    import numpy as np
+    a = np.asarray(v, dtype=np.float64)
+    return {"median_ms": round(float(np.median(a)), 5), "p10_ms": round(float(np.percentile(a, 10)), 5),
+            "p90_ms": round(float(np.percentile(a, 90)), 5), "calls": int(a.size)}
+
+
 TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -142,6 +174,13 @@ def load_traffic(kernel: str, workload: str, op: str):
     return None if not isinstance(entry, dict) else entry.get("hbm_bytes_per_launch")
 
 
+def call_traffic(names: list[str], workload: str, op: str):
+    """The whole call's counter bytes: the sum over its kernels, or None when
+    any kernel has no current record."""
+    parts = [load_traffic(n, workload, op) for n in names]
+    return None if any(p is None for p in parts) else int(sum(parts))
+
+
 class HipEvents:
     """HIP events through the runtime torch already loaded (same soname)."""
 
@@ -151,6 +190,7 @@ class HipEvents:
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
                                                  ctypes.c_void_p, ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         self.events = []
 
     def create(self) -> int:
@@ -160,6 +200,11 @@ class HipEvents:
             raise RuntimeError(f"hipEventCreate failed ({rc})")
         self.events.append(ev.value)
         return ev.value
+
+    def record(self, ev: int, stream: int):
+        rc = self.hip.hipEventRecord(ev, stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
 
     def elapsed_ms(self, a: int, b: int) -> float:
         ms = ctypes.c_float()
@@ -174,10 +219,21 @@ class HipEvents:
         self.events = []
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
     """The float64 CPU oracle, as it stands, on one batch slice of the same
-    operation, repeated until about `seconds` of work; scaled to the whole
-    workload's ideal bytes."""
+    operation, repeated until about `seconds` of work, on all host cores and
+    then on one core; scaled to the whole workload's ideal bytes."""
     from oracle import oracle as oracle_mod
     orc = oracle_mod.Oracle()
     x, g, gt, gc, dy, wi, wo = host0
@@ -190,23 +246,70 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
         "module_backward": lambda: orc.whtmix_module_grad(x, wi, g, wo, dy),
         "module_separable": lambda: orc.whtmix_module_separable(x, wi, gt, gc, wo),
     }[op]
-    runs, t_total = 0, 0.0
-    while runs == 0 or (t_total < seconds and runs < 1000):
-        t0 = time.perf_counter()
-        call()
-        t_total += time.perf_counter() - t0
-        runs += 1
-    t_workload = t_total / runs * w.B
+
+    def timed(budget: float):
+        runs, t_total = 0, 0.0
+        while runs == 0 or (t_total < budget and runs < 1000):
+            t0 = time.perf_counter()
+            call()
+            t_total += time.perf_counter() - t0
+            runs += 1
+        t_workload = t_total / runs * w.B
+        return runs, t_total, t_workload
+
+    threads = orc.threads()
+    runs, t_total, t_wl = timed(seconds * 0.6)
+    prev = orc.set_threads(1)
+    runs1, t_total1, t_wl1 = timed(seconds * 0.4)
+    orc.set_threads(prev)
     return {
-        "value": io_bytes / t_workload / 1e9,
+        "value": round(io_bytes / t_wl / 1e9, 4),
         "unit": "GB/s",
-        "tokens_per_s": w.B * w.N / t_workload,
-        "cores": orc.threads(),
+        "tokens_per_s": round(w.B * w.N / t_wl, 1),
+        "cores": threads,
         "kind": "oracle",
+        "cpu_model": cpu_model(),
+        "host_cpus": os.cpu_count(),
         "sample": (f"{runs} run(s) of one of the {w.B} batch slices ({w.N}x{w.C}), "
-                   f"{t_total:.1f} s total, float64 C oracle with OpenMP; rate scaled "
-                   f"to the whole {w.B}-slice workload"),
+                   f"{t_total:.1f} s total, float64 C oracle with OpenMP on {threads} threads; "
+                   f"rate scaled to the whole {w.B}-slice workload"),
+        "single_core": {"value": round(io_bytes / t_wl1 / 1e9, 4), "unit": "GB/s",
+                        "tokens_per_s": round(w.B * w.N / t_wl1, 1), "cores": 1,
+                        "sample": f"{runs1} run(s) of one slice, {t_total1:.1f} s total"},
     }
+
+
+def copy_floor(torch, w, sets, P: int, hip, stream_ptr: int, reps: int = 20) -> dict:
+    """Time of the three-pass plan's traffic done by plain PyTorch kernels on
+    the same buffers: x widened to a float32 buffer, that buffer multiplied
+    in place by G (broadcast over the batch), then narrowed into y."""
+    L = P * w.C
+    ws = torch.empty((w.B, L), dtype=torch.float32, device=sets[0]["x"].device)
+    ev = [hip.create() for _ in range(4)]
+    acc = [[], [], []]
+    for r in range(reps):
+        t = sets[r % len(sets)]
+        xv = t["x"].view(w.B, -1)
+        yv = t["y"].view(w.B, -1)
+        gv = t["g"].view(1, -1)
+        n = xv.shape[1]
+        hip.record(ev[0], stream_ptr)
+        ws[:, :n].copy_(xv)
+        hip.record(ev[1], stream_ptr)
+        ws.mul_(gv)
+        hip.record(ev[2], stream_ptr)
+        yv.copy_(ws[:, :n])
+        hip.record(ev[3], stream_ptr)
+        torch.cuda.synchronize()
+        for j in range(3):
+            acc[j].append(hip.elapsed_ms(ev[j], ev[j + 1]))
+    import numpy as np
+    med = [float(np.median(a)) for a in acc]
+    del ws
+    return {"floor_ms": round(sum(med), 5),
+            "parts_ms": {"widen_copy": round(med[0], 5), "inplace_gain_multiply": round(med[1], 5),
+                         "narrow_copy": round(med[2], 5)},
+            "note": "medians of PyTorch copy / multiply kernels over the same buffers"}
 
 
 def main() -> int:
@@ -219,20 +322,22 @@ def main() -> int:
     ap.add_argument("--op", default="forward", choices=OPS,
                     help="forward (joint gain, the default), separable (log gains), "
                          "backward, backward_separable, module (the block with its "
-                         "projections), module_separable")
+                         "projections), module_separable, module_backward")
     ap.add_argument("--sets", type=int, default=0,
                     help="input/output sets rotated over the steps (0 = auto)")
-    ap.add_argument("--event-every", type=int, default=8,
+    ap.add_argument("--event-every", type=int, default=4,
                     help="record per-kernel HIP events on every n-th timed step")
+    ap.add_argument("--calls", type=int, default=100,
+                    help="per-call event pairs for the distribution (at least 100)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=14.0)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the WHTMix path here is built and "
               "timed on a single MI355X (batch slices would shard across GPUs with "
-              "no communication; see DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+              "no communication). Run with --gpus 1.", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -255,15 +360,19 @@ def main() -> int:
     P = plan["padded_tokens"]
     op = args.op
     io_bytes = ideal_bytes(op, w.B, w.N, P, w.C, s)
-    nsets = args.sets or max(1, min(8, -(-2 * MALL_BYTES // io_bytes) + 1))
+    nsets = args.sets or input_sets(io_bytes)
+    ndrawn = min(nsets, 4)
     log(f"workload {name}: B={w.B} N={w.N} C={w.C} {w.dtype}; op {op}; plan {plan}; "
-        f"{nsets} input sets")
+        f"{nsets} input sets ({ndrawn} drawn, the rest device copies)")
 
     wi_h, wo_h = workloads.draw_weights(w.C, w.dtype, w.seed + 50)
     w_in = torch.from_numpy(wi_h).to(dev).to(tdt)
     w_out = torch.from_numpy(wo_h).to(dev).to(tdt)
     sets = []
     for i in range(nsets):
+        if i >= ndrawn:
+            sets.append({k: v.clone() for k, v in sets[i % ndrawn].items()})
+            continue
         if i == 0:
             x, g = workloads.inputs(w)
         else:
@@ -279,6 +388,9 @@ def main() -> int:
             t["dy"] = torch.from_numpy(dy).to(dev).to(tdt)
             t["dg"] = torch.empty_like(t["g"])
             t["dgt"], t["dgc"] = torch.empty_like(t["gt"]), torch.empty_like(t["gc"])
+        if op == "module_backward":
+            t["dwi"] = torch.empty((w.C, w.C), device=dev)
+            t["dwo"] = torch.empty((w.C, w.C), device=dev)
         sets.append(t)
         if i == 0:
             host0 = (x[0].copy(), g.copy(), gt, gc, None if dy is None else dy[0].copy(),
@@ -298,7 +410,7 @@ def main() -> int:
                         ["recompute_and_dw_out", "mixer_gradients", "dx_and_dw_in"])
     elif op.startswith("module"):
         # the block runs 2^16-element slices with the three-pass plan even
-        # where the mixer's forward is FUSED
+        # where the mixer's forward takes another plan
         names = module_kernels("three_pass" if plan["module_outer_bits"] else plan["plan"],
                                plan["module_path"])
         nk = len(names)
@@ -324,9 +436,6 @@ def main() -> int:
                                            w_out.data_ptr(), t["y"].data_ptr(), B, N, C,
                                            dt_code, sptr, args.plan, events)
         elif op == "module_backward":
-            if "dwi" not in t:
-                t["dwi"] = torch.empty((C, C), device=dev)
-                t["dwo"] = torch.empty((C, C), device=dev)
             st = whtmix.module_backward_raw(
                 t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(), w_out.data_ptr(),
                 t["dy"].data_ptr(), t["y"].data_ptr(), t["dwi"].data_ptr(), t["dwo"].data_ptr(),
@@ -347,21 +456,48 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
 
-    # Per-kernel HIP events, recorded by the library on the launch stream
-    # between its kernels, on a sample of the timed steps (every
-    # --event-every-th step) so that event records barely perturb the step time.
+    # Timed steps.  The library records the caller's events on the launch
+    # stream: before its first kernel and after its last on every step (the
+    # call's GPU time), and between kernels on every --event-every-th step.
     every = max(1, args.event_every)
-    sampled = list(range(0, args.steps, every))
-    evs = {i: [hip.create() for _ in range(nk + 1)] for i in sampled}
+    evs = []
+    for i in range(args.steps):
+        e = [hip.create() for _ in range(nk + 1)] if i % every == 0 else \
+            [hip.create()] + [None] * (nk - 1) + [hip.create()]
+        evs.append(e)
     torch.cuda.synchronize()            # barrier (one rank) + device sync
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i, evs.get(i))
+        step(args.warmup + i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    per_kernel = [float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs.values()]))
+    call_ms = [hip.elapsed_ms(e[0], e[nk]) for e in evs]
+    sampled = [e for e in evs if e[1 if nk > 1 else 0] is not None]
+    per_kernel = [float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in sampled]))
                   for j in range(nk)]
+    avg_call = float(np.mean(call_ms))
+
+    # Per-call distribution: >= 100 calls, each in its own event pair.
+    ncalls = max(100, args.calls)
+    pairs = [[hip.create()] + [None] * (nk - 1) + [hip.create()] for _ in range(ncalls)]
+    base = args.warmup + args.steps
+    for i in range(ncalls):
+        step(base + i, pairs[i])
+    torch.cuda.synchronize()
+    rotating = [hip.elapsed_ms(e[0], e[nk]) for e in pairs]
+    scrub = torch.empty(SCRUB_BYTES, dtype=torch.uint8, device=dev)
+    cold_pairs = [[hip.create()] + [None] * (nk - 1) + [hip.create()] for _ in range(ncalls)]
+    for i in range(ncalls):
+        scrub.fill_(i & 0xff)
+        step(base + ncalls + i, cold_pairs[i])
+    torch.cuda.synchronize()
+    cold = [hip.elapsed_ms(e[0], e[nk]) for e in cold_pairs]
+    del scrub
+
+    floor = None
+    if op == "forward" and plan["plan"] in ("three_pass", "one_launch"):
+        floor = copy_floor(torch, w, sets, P, hip, sptr)
     hip.destroy()
 
     ms_per_step = wall * 1e3 / args.steps
@@ -372,9 +508,7 @@ def main() -> int:
         gbytes = 4 * P * w.C if op == "forward" else 4 * (P + w.C)
         alg = algorithmic_bytes(plan["plan"], w.B, P, w.C, s, gbytes)
     elif op == "module_backward":
-        # phases recompute design-specific float32 intermediates: the record
-        # below is the whole step's ideal bytes (kernel "step")
-        alg = [0, 0, 0]
+        alg = [0] * nk      # phases recompute design-specific float32 intermediates
     elif op.startswith("module"):
         gbytes = 4 * P * w.C if op == "module" else 4 * (P + w.C)
         alg, flops = module_algorithmic(names, w.B, w.N, P, w.C, s, gbytes)
@@ -392,13 +526,9 @@ def main() -> int:
         # dx phase: the forward mixer applied to dy
         gb = 4 * P * w.C if op == "backward" else 4 * (P + w.C)
         alg = [2 * w.B * w.N * w.C * s + gb, 2 * w.B * w.N * w.C * s + gb]
-    dom = int(np.argmax(per_kernel))
-    if op == "module_backward":
-        achieved, dom_name = gbs, "step"
-    else:
-        achieved, dom_name = alg[dom] / (per_kernel[dom] * 1e-3) / 1e9, names[dom]
-    traffic = load_traffic(dom_name, name, op)
 
+    achieved = io_bytes / (avg_call * 1e-3) / 1e9
+    traffic = call_traffic(names, name, op)
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -417,15 +547,18 @@ def main() -> int:
                    "input_sets": nsets},
         "tokens_per_s": round(tokens, 1),
         "hbm_peak_frac": round(gbs / PEAK_HBM_GBS, 4),
-        # the whole step on the bytes its kernels must move by their design
-        # (x, y, the gain and both float32 workspace round trips): the other
-        # reading of the fraction of HBM peak
-        "path": None if not all(alg) else {
-            "bytes": int(sum(alg)), "GB_s": round(sum(alg) / (ms_per_step * 1e-3) / 1e9, 1),
-            "frac": round(sum(alg) / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "roofline": {"bound": "hbm", "kernel": "whole call (" + " + ".join(names) + ")",
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "alg_bytes": io_bytes, "avg_call_ms": round(avg_call, 5),
+                     "traffic": traffic,
+                     "traffic_ratio": None if traffic is None else round(traffic / io_bytes, 3)},
+        "per_call": {"rotating": percentiles(rotating), "cold": percentiles(cold)},
+        "floor_ms": None if floor is None else floor["floor_ms"],
+        "floor": floor,
         "event_sampled_steps": len(sampled),
-        "kernels": [{"name": n, "avg_ms": round(t, 5), "alg_bytes": b,
-                     "alg_GBs": round(b / (t * 1e-3) / 1e9, 1) if b else None}
+        "kernels": [{"name": n, "avg_ms": round(t, 5), "design_bytes": b,
+                     "design_GBs": round(b / (t * 1e-3) / 1e9, 1) if b else None}
                     for n, t, b in zip(names, per_kernel, alg)],
         "matrix_core": None if flops is None else {
             "alg_TFLOPs_per_kernel": [round(f / (t * 1e-3) / 1e12, 2)
@@ -433,15 +566,10 @@ def main() -> int:
             "peak_TFLOPs": PEAK_MFMA_TFLOPS[w.dtype],
             "note": "projection flops (2 N C^2 per slice each) over the kernel time; "
                     "the kernels stay HBM-bound"},
-        "roofline": {"bound": "hbm", "kernel": dom_name,
-                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on one batch slice ...")
         out["cpu_baseline"] = cpu_baseline(w, op, host0, io_bytes, args.cpu_seconds)
-        out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 4)
-        out["cpu_baseline"]["tokens_per_s"] = round(out["cpu_baseline"]["tokens_per_s"], 1)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

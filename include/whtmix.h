@@ -14,10 +14,10 @@
  *   G           N_pad x C float32 per-frequency gain shared by every slice b
  *               ("o" is the element-wise product).
  *
- * C must be a power of two.  N may be any count >= 1: as the paper does, the
- * token axis is zero-padded to N_pad = 2^ceil(log2 N) before H_N (the padded
- * rows of X are zeros), the mixer runs on the N_pad x C slice, and Y keeps its
- * first N rows.  For a power-of-two N, N_pad = N.
+ * C must be a power of two.  N may be any count >= 1: rows N .. N_pad-1 of
+ * X, N_pad = 2^ceil(log2 N), are taken as zeros so that H_N acts on a
+ * power-of-two length (section III-B), the mixer runs on the N_pad x C slice,
+ * and Y keeps its first N rows.  For a power-of-two N, N_pad = N.
  *
  * The paper's own gains are log-domain vectors g_c (length C) and g_t
  * (length N_pad) applied by eq. (2) then eq. (3); that is this operation with
@@ -71,8 +71,12 @@ typedef enum whtmix_status {
     WHTMIX_ERROR_OUT_OF_MEMORY = 5,    /* workspace allocation failed */
     WHTMIX_ERROR_HIP = 6,              /* HIP runtime / launch error; text in
                                           whtmix_last_error() */
-    WHTMIX_ERROR_TOO_LARGE = 7         /* N_pad*C > 2^30, sizes overflow, or
+    WHTMIX_ERROR_TOO_LARGE = 7,        /* N_pad*C > 2^30, sizes overflow, or
                                           module C > 4096 */
+    WHTMIX_ERROR_DEVICE_TIMEOUT = 8    /* whtmix_stream_status only: a
+                                          ONE_LAUNCH call on the stream gave
+                                          up waiting for one of its passes
+                                          (its output is not valid) */
 } whtmix_status;
 
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
@@ -85,13 +89,21 @@ typedef enum whtmix_status {
  *                      index, then forward over the high bits + gain +
  *                      inverse over the high bits, then inverse over the low
  *                      bits, exchanging through the workspace.
+ * ONE_LAUNCH (never chosen by AUTO) runs THREE_PASS's three passes in a
+ * single cooperative launch: one-wave tiles of 2^9 elements whose butterflies
+ * stay in the wave (DPP and lane-swap exchanges, no LDS), the passes ordered
+ * by per-slice counters in a small per-stream block; 2^12 <= L <= 2^16,
+ * B <= 2046 and N*C a multiple of 8.  On MI355X it is slower than the plans
+ * AUTO picks: a cooperative launch alone costs about 20 us, and a hand-off
+ * between workgroups through memory costs more than a kernel boundary.
  * THREE_PASS may also be forced for 2^12 <= L <= 2^16 (tests compare it with
  * FUSED on the same shapes). */
 typedef enum whtmix_plan {
     WHTMIX_PLAN_AUTO = 0,
     WHTMIX_PLAN_SMALL = 1,
     WHTMIX_PLAN_FUSED = 2,
-    WHTMIX_PLAN_THREE_PASS = 3
+    WHTMIX_PLAN_THREE_PASS = 3,
+    WHTMIX_PLAN_ONE_LAUNCH = 4
 } whtmix_plan;
 
 typedef struct whtmix_options {
@@ -100,6 +112,12 @@ typedef struct whtmix_options {
      * the stream before the first kernel and events[i] after the i-th kernel
      * of the plan (at most 3 kernels).  Used for per-kernel timing. */
     void *events[4];
+    /* ONE_LAUNCH: polls of the kernel's counter waits before the call gives
+     * up (0 = the default, about a second or two).  A call that gives up
+     * exits normally with an invalid output and raises the stream's error
+     * word (whtmix_stream_status).  Tests force that path with a tiny
+     * limit. */
+    uint32_t spin_limit;
 } whtmix_options;
 
 /* Describes how a shape would run (no GPU work, no allocation).  plan,
@@ -110,8 +128,8 @@ typedef struct whtmix_plan_info {
     int plan;             /* resolved whtmix_plan (never AUTO) */
     int kernels;          /* kernels launched per call (1 or 3) */
     int log2_slice;       /* K = log2(N*C) */
-    int outer_bits;       /* THREE_PASS: flat-index bits of the outer passes */
-    int run_bits;         /* THREE_PASS: log2 of the contiguous run carried
+    int outer_bits;       /* THREE_PASS, ONE_LAUNCH: flat-index bits of the outer passes */
+    int run_bits;         /* THREE_PASS, ONE_LAUNCH: log2 of the contiguous run carried
                              by the middle pass */
     int64_t workspace_bytes; /* float32 workspace this call needs */
     int64_t padded_tokens;   /* N_pad */
@@ -332,6 +350,14 @@ WHTMIX_API const char *whtmix_last_error(void);
 /* Synchronises every stream that owns a workspace and frees all workspaces.
  * Returns a whtmix_status. */
 WHTMIX_API int whtmix_release_workspaces(void);
+
+/* Synchronises `stream` (hipStream_t) on the current device, then reports
+ * and clears the error word its ONE_LAUNCH calls raise: WHTMIX_SUCCESS when
+ * every ONE_LAUNCH call since the last check completed, or
+ * WHTMIX_ERROR_DEVICE_TIMEOUT when one gave up waiting for a pass (its
+ * output is invalid; later calls are unaffected).  Other plans never raise
+ * it.  Returns WHTMIX_ERROR_HIP if the synchronisation fails. */
+WHTMIX_API int whtmix_stream_status(void *stream);
 
 /* Library version as major*10000 + minor*100 + patch. */
 WHTMIX_API int whtmix_version(void);

@@ -63,6 +63,8 @@ def load(path: str = LIB):
     lib.oracle_whtmix_module_grad_separable.restype = ctypes.c_int
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = ctypes.c_int
     if path == LIB:
         _lib = lib
     return lib
@@ -261,6 +263,10 @@ class Oracle:
     def threads(self) -> int:
         """OpenMP threads the oracle's parallel loops use."""
         return int(self.lib.oracle_threads())
+
+    def set_threads(self, n: int) -> int:
+        """Use n OpenMP threads from now on; returns the previous count."""
+        return int(self.lib.oracle_set_threads(int(n)))
 
 
 _default = None

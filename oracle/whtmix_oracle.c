@@ -441,3 +441,14 @@ int oracle_threads(void)
 {
     return omp_get_max_threads();
 }
+
+/* Sets the number of OpenMP threads later calls use (n >= 1); returns the
+ * previous count.  Per-vector operation order does not depend on it, so the
+ * results are bitwise the same at any count. */
+int oracle_set_threads(int n)
+{
+    const int prev = omp_get_max_threads();
+    if (n >= 1)
+        omp_set_num_threads(n);
+    return prev;
+}

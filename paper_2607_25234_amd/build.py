@@ -2,8 +2,8 @@
 
     python -m paper_2607_25234_amd.build
 
-Compiles every source under csrc/ with hipcc into one shared library beside
-this file, and the memory-system calibration program calib/membw.  Packed
+Compiles every source under csrc/ with hipcc, one process per source in
+parallel, and links them into one shared library beside this file.  Packed
 FP32 instructions are disabled for all device code.
 """
 from __future__ import annotations
@@ -12,28 +12,28 @@ import glob
 import os
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwhtmix.so")
-CALIB_SRC = os.path.join(HERE, "calib", "membw.hip")
-CALIB_BIN = os.path.join(HERE, "calib", "membw")
 ARCH = "gfx950"
 
-HIPCC_FLAGS = [
+COMPILE_FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     "-fvisibility=hidden",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}",
     f"-I{CSRC}",
 ]
+LINK_FLAGS = [f"--offload-arch={ARCH}", "-shared", "-fPIC"]
 
 
 def sources() -> list[str]:
@@ -47,31 +47,28 @@ def hipcc() -> str:
     return path if os.path.exists(path) else "hipcc"
 
 
-def build(out: str = LIB, extra: tuple = (), verbose: bool = False) -> str:
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra, *sources(), "-o", out + ".tmp"]
+def _run(cmd: list[str], verbose: bool, what: str) -> None:
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed building {out}")
-    os.replace(out + ".tmp", out)
-    return out
+        raise RuntimeError(f"hipcc failed: {what}")
 
 
-def build_calib(out: str = CALIB_BIN, verbose: bool = False) -> str:
-    flags = [f for f in HIPCC_FLAGS if f not in ("-shared", "-fPIC", "-fvisibility=hidden")]
-    cmd = [hipcc(), *flags, CALIB_SRC, "-o", out + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed building {out}")
+def build(out: str = LIB, extra: tuple = (), verbose: bool = False, jobs: int = 0) -> str:
+    """Compile each source to an object (in parallel), then link."""
+    srcs = sources()
+    jobs = jobs or min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
+    with tempfile.TemporaryDirectory(prefix="whtmix_build_") as tmp:
+        objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
+        cmds = [[hipcc(), *COMPILE_FLAGS, *extra, "-c", s, "-o", o] for s, o in zip(srcs, objs)]
+        with ThreadPoolExecutor(max_workers=jobs) as pool:
+            list(pool.map(lambda c: _run(c, verbose, c[-3]), cmds))
+        _run([hipcc(), *LINK_FLAGS, *extra, *objs, "-o", out + ".tmp"], verbose, "link")
     os.replace(out + ".tmp", out)
     return out
 
 
 if __name__ == "__main__":
     print(build(verbose=True))
-    print(build_calib(verbose=True))

@@ -22,6 +22,10 @@ thread_local std::string g_last_error;
 struct Workspace {
     float *ptr = nullptr;
     int64_t bytes = 0;
+    // ONE_LAUNCH counter block (kCounterWords words), allocated and zeroed
+    // once; each call's kernel returns it to zero (the sticky error word
+    // aside, which whtmix_stream_status reads and clears).
+    uint32_t *ctr = nullptr;
 };
 
 // Keyed by (device, stream).  The mutex is held from workspace lookup until
@@ -67,7 +71,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         return WHTMIX_ERROR_NOT_POWER_OF_TWO;
     if (N > (int64_t(1) << whtmix::kMaxLog2Slice))
         return WHTMIX_ERROR_TOO_LARGE;
-    // The token axis is zero-padded to the next power of two (section III-B).
+    // Rows N .. N_pad-1 count as zeros so that H_N acts on a power-of-two
+    // length (section III-B).
     const int nbits = log2_exact(N);
     const int K = nbits + log2_exact(C);
     if (K > whtmix::kMaxLog2Slice)
@@ -80,12 +85,18 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     if (K <= whtmix::kMaxSmall && B >= (int64_t(1) << 24))
         return WHTMIX_ERROR_TOO_LARGE;
     int plan = opt ? opt->plan : whtmix::PLAN_AUTO;
+    // ONE_LAUNCH moves x and y in 16-byte groups of 8 elements at most.
+    const bool one_launch_ok = K >= whtmix::kOneLaunchMinK && K <= whtmix::kOneLaunchMaxK &&
+                               B <= whtmix::kOneLaunchMaxBatch && (N * C) % 8 == 0;
     switch (plan) {
     case whtmix::PLAN_AUTO:
         plan = K <= whtmix::kMaxSmall ? whtmix::PLAN_SMALL
                : K <= whtmix::kMaxTile ? whtmix::PLAN_FUSED
                : K == whtmix::kMaxFused && B >= whtmix::kFusedPairMinBatch ? whtmix::PLAN_FUSED
                                                                           : whtmix::PLAN_THREE_PASS;
+        break;
+    case whtmix::PLAN_ONE_LAUNCH:
+        if (!one_launch_ok) return WHTMIX_ERROR_INVALID_VALUE;
         break;
     case whtmix::PLAN_SMALL:
         if (K > whtmix::kMaxSmall) return WHTMIX_ERROR_INVALID_VALUE;
@@ -108,6 +119,10 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         out->split = whtmix::three_pass_split(K);
         out->ws_bytes = B * L * 4;
     }
+    if (plan == whtmix::PLAN_ONE_LAUNCH) {
+        out->split = whtmix::Split{9, K - 9, 18 - K};
+        out->ws_bytes = B * L * 4;
+    }
     return WHTMIX_SUCCESS;
 }
 
@@ -116,7 +131,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
 // three-pass plan for such slices.
 void three_pass_beyond_one_tile(int64_t B, Checked *c)
 {
-    if (c->plan == whtmix::PLAN_FUSED && c->K > whtmix::kMaxTile) {
+    if ((c->plan == whtmix::PLAN_FUSED && c->K > whtmix::kMaxTile) ||
+        c->plan == whtmix::PLAN_ONE_LAUNCH) {
         c->plan = whtmix::PLAN_THREE_PASS;
         c->kernels = 3;
         c->split = whtmix::three_pass_split(c->K);
@@ -171,6 +187,34 @@ int get_workspace(void *stream, int64_t bytes, float **out)
     return WHTMIX_SUCCESS;
 }
 
+// The ONE_LAUNCH counter block of (current device, stream), allocated and
+// zeroed on first use.  Caller holds g_ws_mutex.
+int get_counters(void *stream, uint32_t **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    Workspace &w = g_ws[{dev, stream}];
+    if (!w.ctr) {
+        void *p = nullptr;
+        const size_t bytes = sizeof(uint32_t) * whtmix::kCounterWords;
+        e = hipMalloc(&p, bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            g_last_error = std::string("hipMalloc of counters: ") + hipGetErrorString(e);
+            return WHTMIX_ERROR_OUT_OF_MEMORY;
+        }
+        e = hipMemset(p, 0, bytes);
+        if (e != hipSuccess) {
+            (void)hipFree(p);
+            return hip_fail(e, "hipMemset of counters");
+        }
+        w.ctr = static_cast<uint32_t *>(p);
+    }
+    *out = w.ctr;
+    return WHTMIX_SUCCESS;
+}
+
 }  // namespace
 
 extern "C" {
@@ -185,8 +229,9 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->plan = c.plan;
     info->kernels = c.kernels;
     info->log2_slice = c.K;
-    info->outer_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.A : 0;
-    info->run_bits = c.plan == whtmix::PLAN_THREE_PASS ? c.split.R : 0;
+    const bool passes = c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_ONE_LAUNCH;
+    info->outer_bits = passes ? c.split.A : 0;
+    info->run_bits = passes ? c.split.R : 0;
     info->workspace_bytes = c.ws_bytes;
     info->padded_tokens = c.n_pad;
     const int cbits = log2_exact(C);
@@ -255,6 +300,18 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
         st = get_workspace(stream, c.ws_bytes, &a.ws);
         if (st != WHTMIX_SUCCESS) return st;
         hipError_t e = whtmix::launch(a);
+        if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        return WHTMIX_SUCCESS;
+    }
+    if (c.plan == whtmix::PLAN_ONE_LAUNCH) {
+        a.spin_limit = options && options->spin_limit ? options->spin_limit
+                                                       : whtmix::kDefaultSpinLimit;
+        std::lock_guard<std::mutex> lock(g_ws_mutex);
+        st = get_workspace(stream, c.ws_bytes, &a.ws);
+        if (st != WHTMIX_SUCCESS) return st;
+        st = get_counters(stream, &a.counters);
+        if (st != WHTMIX_SUCCESS) return st;
+        hipError_t e = whtmix::launch_one_launch(a);
         if (e != hipSuccess) return hip_fail(e, "kernel launch");
         return WHTMIX_SUCCESS;
     }
@@ -631,6 +688,8 @@ const char *whtmix_status_string(int status)
     case WHTMIX_ERROR_HIP: return "HIP runtime error";
     case WHTMIX_ERROR_TOO_LARGE:
         return "shape too large (N_pad*C <= 2^30, B*N_pad*C <= 2^37, module C <= 4096)";
+    case WHTMIX_ERROR_DEVICE_TIMEOUT:
+        return "a single-launch call gave up waiting for one of its passes";
     default: return "unknown status";
     }
 }
@@ -645,12 +704,13 @@ int whtmix_release_workspaces(void)
     if (hipGetDevice(&cur) != hipSuccess) cur = -1;
     for (auto &kv : g_ws) {
         Workspace &w = kv.second;
-        if (!w.ptr) continue;
+        if (!w.ptr && !w.ctr) continue;
         if (hipSetDevice(kv.first.first) != hipSuccess ||
             hipStreamSynchronize(static_cast<hipStream_t>(kv.first.second)) != hipSuccess ||
-            hipFree(w.ptr) != hipSuccess)
+            (w.ptr && hipFree(w.ptr) != hipSuccess) || (w.ctr && hipFree(w.ctr) != hipSuccess))
             st = WHTMIX_ERROR_HIP;
         w.ptr = nullptr;
+        w.ctr = nullptr;
         w.bytes = 0;
     }
     g_ws.clear();
@@ -658,6 +718,32 @@ int whtmix_release_workspaces(void)
     return st;
 }
 
-int whtmix_version(void) { return 10100; }
+int whtmix_version(void) { return 10200; }
+
+int whtmix_stream_status(void *stream)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    uint32_t *ctr = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_ws_mutex);
+        auto it = g_ws.find({dev, stream});
+        if (it != g_ws.end()) ctr = it->second.ctr;
+    }
+    e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    if (!ctr) return WHTMIX_SUCCESS;
+    // The sticky error word is the block's last word.
+    uint32_t *sticky = ctr + whtmix::kCounterWords - 1;
+    uint32_t v = 0;
+    e = hipMemcpy(&v, sticky, sizeof(v), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the error word");
+    if (v == 0) return WHTMIX_SUCCESS;
+    const uint32_t zero = 0;
+    e = hipMemcpy(sticky, &zero, sizeof(zero), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the error word");
+    return WHTMIX_ERROR_DEVICE_TIMEOUT;
+}
 
 }  // extern "C"

@@ -31,10 +31,17 @@ struct LaunchArgs {
     hipStream_t stream;
     hipEvent_t events[4];   // optional, may be null
     bool pair_outer;        // launch_middle only: the outer passes used 2^16 tiles
+    uint32_t *counters;     // ONE_LAUNCH: kCounterWords words, zero between calls
+    uint32_t spin_limit;    // ONE_LAUNCH: polls per wait before the call fails
 };
 
 // Enqueues the plan's kernels on a.stream.  Returns the first HIP error.
 hipError_t launch(const LaunchArgs &a);
+
+// Enqueues the ONE_LAUNCH kernel (a.plan == PLAN_ONE_LAUNCH, 12 <= a.K <=
+// 16, a.B <= kOneLaunchMaxBatch, a.nvalid a multiple of 8, a.ws holding
+// a.B * 2^K floats and a.counters a zeroed-or-reset counter block).
+hipError_t launch_one_launch(const LaunchArgs &a);
 
 // A validated backward call.  dX = the mixer applied to dY (may be null);
 // the gain gradient goes to dgain (joint) or dgt/dgc (separable log gains),

@@ -11,7 +11,13 @@
 
 namespace whtmix {
 
-enum PlanKind { PLAN_AUTO = 0, PLAN_SMALL = 1, PLAN_FUSED = 2, PLAN_THREE_PASS = 3 };
+enum PlanKind {
+    PLAN_AUTO = 0,
+    PLAN_SMALL = 1,
+    PLAN_FUSED = 2,
+    PLAN_THREE_PASS = 3,
+    PLAN_ONE_LAUNCH = 4
+};
 
 constexpr int kMaxLog2Slice = 30;   // N*C <= 2^30
 constexpr int kMaxSmall = 10;       // SMALL: L <= 2^10
@@ -24,6 +30,20 @@ constexpr int kMaxTile = 15;
 // where the three passes (15 us at 16 slices, 24 us at 48) stop being faster.
 constexpr int kMaxFused = 16;
 constexpr int kFusedPairMinBatch = 48;
+
+// ONE_LAUNCH (whtmix_onelaunch.hip): the three passes of slices of 2^12 ..
+// 2^16 elements in one launch, one-wave 2^9-element tiles, passes ordered by
+// per-slice completion counters.  Its counter block holds 2B + 3 words
+// (per-slice counters of two passes, exits, the call's error word, the
+// sticky error word), so it takes at most kOneLaunchMaxBatch slices.  x and
+// y move in 16-byte groups, so a slice's element count must be a multiple
+// of 8.
+constexpr int kOneLaunchMinK = 12;
+constexpr int kOneLaunchMaxK = 16;
+constexpr int kCounterWords = 4096;
+constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
+// Polls of a ONE_LAUNCH wait before it gives up (about a second or two).
+constexpr unsigned kDefaultSpinLimit = 1u << 21;
 
 // THREE_PASS split for slice bits K:
 //   outer passes: contiguous chunks of 2^A elements (all A low bits of f);

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libwhtmix.so")
 
 SUCCESS = 0
 DTYPE_F32, DTYPE_BF16 = 0, 1
-PLANS = {"auto": 0, "small": 1, "fused": 2, "three_pass": 3}
+PLANS = {"auto": 0, "small": 1, "fused": 2, "three_pass": 3, "one_launch": 4}
 PLAN_NAMES = {v: k for k, v in PLANS.items()}
 
 # Every symbol include/whtmix.h declares.
@@ -35,8 +35,10 @@ EXPORTS = (
     "whtmix_status_string",
     "whtmix_last_error",
     "whtmix_release_workspaces",
+    "whtmix_stream_status",
     "whtmix_version",
 )
+ERROR_DEVICE_TIMEOUT = 8
 
 
 class WhtmixError(RuntimeError):
@@ -47,7 +49,8 @@ class WhtmixError(RuntimeError):
 
 
 class Options(ctypes.Structure):
-    _fields_ = [("plan", ctypes.c_int), ("events", ctypes.c_void_p * 4)]
+    _fields_ = [("plan", ctypes.c_int), ("events", ctypes.c_void_p * 4),
+                ("spin_limit", ctypes.c_uint32)]
 
 
 MODULE_PATHS = {0: "small", 1: "mfma", 2: "unfused"}
@@ -117,6 +120,8 @@ def lib():
         L.whtmix_release_workspaces.restype = ctypes.c_int
         L.whtmix_version.argtypes = []
         L.whtmix_version.restype = ctypes.c_int
+        L.whtmix_stream_status.argtypes = [vp]
+        L.whtmix_stream_status.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -129,12 +134,24 @@ def last_error() -> str:
     return lib().whtmix_last_error().decode()
 
 
-def _options(plan: str | int = "auto", events=None) -> Options:
+def _options(plan: str | int = "auto", events=None, spin_limit: int = 0) -> Options:
     o = Options()
     o.plan = PLANS[plan] if isinstance(plan, str) else int(plan)
     for i, ev in enumerate(events or ()):
         o.events[i] = ev
+    o.spin_limit = int(spin_limit)
     return o
+
+
+def stream_status(stream: int | None = None) -> int:
+    """whtmix_stream_status: synchronise the stream and return (and clear)
+    the error word of its single-launch calls (SUCCESS or
+    ERROR_DEVICE_TIMEOUT).  stream: a hipStream_t as int (default: torch's
+    current stream)."""
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+    return int(lib().whtmix_stream_status(stream))
 
 
 def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = "auto") -> dict:
@@ -155,15 +172,17 @@ def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = 
 
 
 def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
-                dtype: int, stream: int, plan: str | int = "auto", events=None) -> int:
+                dtype: int, stream: int, plan: str | int = "auto", events=None,
+                spin_limit: int = 0) -> int:
     """Direct call of whtmix_forward_ex with integer pointers; returns the status."""
-    opt = _options(plan, events)
+    opt = _options(plan, events, spin_limit)
     return lib().whtmix_forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream,
                                    ctypes.byref(opt))
 
 
 def padded_tokens(N: int) -> int:
-    """N_pad: the token axis is zero-padded to the next power of two."""
+    """N_pad: rows N .. N_pad-1 are taken as zeros so that H_N acts on a
+    power-of-two length (section III-B)."""
     return 1 << max(0, (int(N) - 1).bit_length())
 
 
@@ -209,7 +228,8 @@ def _gain(t, shape, x, what):
         raise ValueError(f"{what} shape {tuple(t.shape)} != {tuple(shape)}")
 
 
-def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=None):
+def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=None,
+            spin_limit: int = 0):
     """y[b] = H_N (G o (H_N x[b] H_C)) H_C on the GPU (section III-B, eqs. (2)-(3)).
 
     x: torch tensor [B, N, C] or [N, C], float32 or bfloat16, on a ROCm device.
@@ -225,7 +245,7 @@ def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=Non
     st = stream if stream is not None else torch.cuda.current_stream(x.device)
     with torch.cuda.device(x.device):
         status = forward_raw(xx.data_ptr(), gain.data_ptr(), out.data_ptr(), B, N, C, dt,
-                             st.cuda_stream, plan, events)
+                             st.cuda_stream, plan, events, spin_limit)
     if status != SUCCESS:
         raise WhtmixError(status, "whtmix_forward")
     return out

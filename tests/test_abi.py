@@ -43,8 +43,8 @@ def test_library_exports_nothing_else():
 
 
 def test_version_and_status_strings():
-    assert whtmix.lib().whtmix_version() == 10100
-    for st in range(8):
+    assert whtmix.lib().whtmix_version() == 10200
+    for st in range(9):
         assert whtmix.status_string(st)
     assert whtmix.status_string(99) == "unknown status"
 
@@ -77,6 +77,10 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(plan=2, N=8, C=8), 1),              # FUSED needs 2^11..2^16
     (dict(plan=2, N=2048, C=64), 1),
     (dict(plan=3, N=32, C=64), 1),            # THREE_PASS needs >= 2^12
+    (dict(plan=4, N=32, C=64), 1),            # ONE_LAUNCH needs 2^12..2^16
+    (dict(plan=4, N=2048, C=64), 1),
+    (dict(plan=4, N=4095, C=1), 1),           # ... and N*C a multiple of 8
+    (dict(plan=4, B=2047, N=1024, C=64), 1),  # ... and B <= 2046
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
     assert call(**kwargs) == status
@@ -233,12 +237,18 @@ def test_plan_table():
     assert whtmix.plan_describe(3, 32, 32)["plan"] == "small"
     assert whtmix.plan_describe(3, 32, 64)["plan"] == "fused"
     assert whtmix.plan_describe(3, 256, 128)["plan"] == "fused"
-    d = whtmix.plan_describe(3, 512, 128, "bf16")
+    d = whtmix.plan_describe(3, 1024, 128, "bf16")
     assert d["plan"] == "three_pass" and d["kernels"] == 3
-    assert d["workspace_bytes"] == 3 * 512 * 128 * 4
+    assert d["workspace_bytes"] == 3 * 1024 * 128 * 4
     # 2^16 from 48 slices: one workgroup of two register sets for the forward;
-    # the block and the backward pass take the three-pass plan
+    # the block and the backward pass take the three-pass plan; ONE_LAUNCH
+    # only when asked for
     assert whtmix.plan_describe(47, 512, 128, "bf16")["plan"] == "three_pass"
+    d = whtmix.plan_describe(47, 512, 128, "bf16", "one_launch")
+    assert (d["plan"], d["kernels"], d["workspace_bytes"]) == ("one_launch", 1, 47 << 18)
+    assert (d["outer_bits"], d["run_bits"]) == (9, 2)
+    d = whtmix.plan_describe(2, 64, 64, plan="one_launch")
+    assert (d["plan"], d["outer_bits"], d["run_bits"]) == ("one_launch", 9, 6)
     d = whtmix.plan_describe(48, 512, 128, "bf16")
     assert (d["plan"], d["kernels"], d["workspace_bytes"]) == ("fused", 1, 0)
     assert (d["module_path"], d["module_outer_bits"]) == ("mfma", 11)

@@ -42,3 +42,29 @@ def test_traffic_lookup_tolerates_every_record(tmp_path, monkeypatch):
     path.write_text(json.dumps(good))
     assert bench.load_traffic("middle", "stereo64k_bf16", "forward") == 7
     assert bench.load_traffic("middle", "stereo64k_bf16", "module") is None
+
+
+def test_input_sets_exceed_twice_the_infinity_cache():
+    """Every workload rotates over sets whose footprint is >= 2x the cache
+    (the cap only binds below 256 KiB per set)."""
+    for fp in (786432, 41943040, 68157440, 167772160, 536870912):
+        n = bench.input_sets(fp)
+        assert n * fp >= 2 * bench.MALL_BYTES and n >= 2
+
+
+def test_whole_call_traffic_sums_kernels(tmp_path, monkeypatch):
+    path = tmp_path / "traffic.json"
+    monkeypatch.setattr(bench, "TRAFFIC_PATH", str(path))
+    rec = {"source_hash": {"forward": bench.kernel_source_hash(bench.FORWARD_SOURCES)},
+           "workloads": {"w": {"forward": {"outer_fwd": {"hbm_bytes_per_launch": 3},
+                                           "middle": {"hbm_bytes_per_launch": 5}}}}}
+    path.write_text(json.dumps(rec))
+    assert bench.call_traffic(["outer_fwd", "middle"], "w", "forward") == 8
+    assert bench.call_traffic(["outer_fwd", "middle", "outer_inv"], "w", "forward") is None
+
+
+def test_one_launch_design_bytes_are_the_three_passes():
+    three = bench.algorithmic_bytes("three_pass", 1, 1024, 64, 4, 4 * 1024 * 64)
+    assert bench.algorithmic_bytes("one_launch", 1, 1024, 64, 4, 4 * 1024 * 64) == [sum(three)]
+    p = bench.percentiles([1.0, 2.0, 3.0])
+    assert p["median_ms"] == 2.0 and p["calls"] == 3

@@ -9,7 +9,7 @@ import pytest
 
 from oracle import oracle as oracle_mod
 from paper_2607_25234_amd import whtmix, workloads
-from tests.gpu_util import TOL, device, errors, say, to_device, to_host
+from tests.gpu_util import DERIVED, TOL, device, errors, say, to_device, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -62,7 +62,7 @@ def test_backward(shape, dtype, dev, orc):
                              torch.from_numpy(g).to(dev))
     torch.cuda.synchronize()
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
-    check("dx", to_host(dx), dx_ref, TOL[dtype])
+    check("dx", to_host(dx), dx_ref, DERIVED[dtype])
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
 
 
@@ -76,7 +76,7 @@ def test_backward_workload(dev, orc):
                              torch.from_numpy(g).to(dev))
     torch.cuda.synchronize()
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
-    check("dx", to_host(dx), dx_ref, TOL[w.dtype])
+    check("dx", to_host(dx), dx_ref, DERIVED[w.dtype])
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
 
 
@@ -95,7 +95,7 @@ def test_backward_largest_tiles(dev, orc):
                              torch.from_numpy(g).to(dev))
     torch.cuda.synchronize()
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
-    check("dx", to_host(dx), dx_ref, TOL[dtype])
+    check("dx", to_host(dx), dx_ref, DERIVED[dtype])
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
 
 

@@ -1,0 +1,137 @@
+"""The ONE_LAUNCH plan (csrc/whtmix_onelaunch.hip) against the CPU oracle,
+through the C ABI.
+
+All three passes of the mixer (section III-B, eqs. (2)-(3)) run in one
+cooperative launch, ordered by per-slice counters.  Checked here: parity at
+every supported slice size, batch counts from 1 to 47 (several tiles per
+workgroup when the batch outgrows the resident grid), padded N, both dtypes,
+both gain forms, in place; back-to-back calls (the kernel returns its
+counters to zero); and the give-up path forced from the host with a poll
+limit of one, after which the stream reports the error once and later calls
+are correct.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as oracle_mod
+from paper_2607_25234_amd import whtmix, workloads
+from tests.gpu_util import (DERIVED, TOL, device, errors, run_gpu, run_gpu_separable, say,
+                            to_device, to_host)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle_mod.Oracle()
+
+
+def check(name, y, ref, dtype):
+    err, rms = errors(y, ref)
+    say(f"  {name}: normwise-max {err:.3e} rms {rms:.3e}")
+    assert y.shape == ref.shape and np.all(np.isfinite(y))
+    assert err <= TOL[dtype] and err <= DERIVED[dtype], (name, err)
+
+
+def status_ok():
+    st = whtmix.stream_status()
+    assert st == whtmix.SUCCESS, whtmix.status_string(st)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 64, 64), (2, 128, 64), (1, 256, 64), (3, 256, 128),
+                                   (1, 1024, 64), (2, 512, 128), (16, 1024, 64),
+                                   (47, 512, 128), (1, 65536, 1), (1, 8, 8192),
+                                   (300, 1024, 64), (2046, 64, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_parity(shape, dtype, dev, orc):
+    B, N, C = shape
+    say(f"one_launch B={B} N={N} C={C} {dtype}")
+    x, g = workloads.draw(B, N, C, dtype, seed=B * 1000 + N + C)
+    y = run_gpu(x, g, dtype, dev, plan="one_launch")
+    status_ok()
+    check("one_launch", y, orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 1000, 64), (2, 9, 512), (3, 200, 128), (1, 33, 128)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_padded_tokens(shape, dtype, dev, orc):
+    """Non-power-of-two N: rows N..N_pad-1 are zeros; only the straddling
+    tile is partial, tiles wholly in the padding skip their loads and stores."""
+    B, N, C = shape
+    say(f"one_launch padded B={B} N={N} C={C} {dtype}")
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=N)
+    g = np.random.default_rng(N).uniform(0.5, 1.5, (P, C)).astype(np.float32)
+    y = run_gpu(x, g, dtype, dev, plan="one_launch")
+    status_ok()
+    check("one_launch padded", y, orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_separable(dtype, dev, orc):
+    B, N, C = 2, 1024, 64
+    x, _ = workloads.draw(B, N, C, dtype, seed=5)
+    gt, gc = workloads.draw_log_gains(N, C, seed=6)
+    y = run_gpu_separable(x, gt, gc, dtype, dev, plan="one_launch")
+    status_ok()
+    check("one_launch separable", y, orc.whtmix_separable(x, gt, gc), dtype)
+
+
+def test_image1k_workload(dev, orc):
+    """image1k_f32 (B=1, N=1024, C=64) as one launch."""
+    w = workloads.WORKLOADS["image1k_f32"]
+    x, g = workloads.inputs(w)
+    y = run_gpu(x, g, w.dtype, dev, plan="one_launch")
+    status_ok()
+    check("image1k_f32", y, orc.whtmix(x, g), w.dtype)
+
+
+def test_back_to_back_and_in_place(dev, orc):
+    """Consecutive calls on one stream reuse the counter block (each kernel
+    returns it to zero); in place (y == x) reads every x before any y store
+    of the same slice."""
+    import torch
+    B, N, C = 4, 1024, 64
+    outs, refs = [], []
+    for i in range(3):
+        x, g = workloads.draw(B, N, C, "f32", seed=40 + i)
+        xd = to_device(x, "f32", dev)
+        gd = torch.from_numpy(g).to(dev)
+        whtmix.forward(xd, gd, out=xd, plan="one_launch")
+        outs.append(xd)
+        refs.append(orc.whtmix(x, g))
+    torch.cuda.synchronize()
+    status_ok()
+    for i, (o, r) in enumerate(zip(outs, refs)):
+        check(f"call {i} in place", to_host(o), r, "f32")
+
+
+def test_give_up_path_reports_and_recovers(dev, orc):
+    """A poll limit of one makes the counter waits give up (forced from the
+    host; every wave still exits).  The stream then reports
+    WHTMIX_ERROR_DEVICE_TIMEOUT once, and the next default call is correct."""
+    import torch
+    B, N, C = 16, 1024, 64
+    x, g = workloads.draw(B, N, C, "f32", seed=77)
+    xd = to_device(x, "f32", dev)
+    gd = torch.from_numpy(g).to(dev)
+    status_ok()
+    seen = 0
+    for _ in range(3):
+        whtmix.forward(xd, gd, plan="one_launch", spin_limit=1)
+        st = whtmix.stream_status()
+        assert st in (whtmix.SUCCESS, whtmix.ERROR_DEVICE_TIMEOUT)
+        seen += st == whtmix.ERROR_DEVICE_TIMEOUT
+    say(f"  calls that gave up: {seen} of 3")
+    assert seen >= 1
+    assert whtmix.stream_status() == whtmix.SUCCESS       # cleared once read
+    y = whtmix.forward(xd, gd, plan="one_launch")
+    status_ok()
+    check("after give-up", to_host(y), orc.whtmix(x, g), "f32")

@@ -10,8 +10,8 @@ import pytest
 
 from oracle import oracle as oracle_mod
 from paper_2607_25234_amd import whtmix, workloads
-from tests.gpu_util import (TOL, device, errors, run_gpu, run_gpu_separable, say, to_device,
-                            to_host)
+from tests.gpu_util import (DERIVED, TOL, device, errors, run_gpu, run_gpu_separable, say,
+                            to_device, to_host)
 
 log_gains = workloads.draw_log_gains
 
@@ -29,11 +29,14 @@ def orc():
 
 
 def check(name, y, ref, dtype):
+    """The stated tolerance and the tighter bound the arithmetic allows."""
     err, rms = errors(y, ref)
-    say(f"  {name}: normwise-max {err:.3e} rms {rms:.3e} (tol {TOL[dtype]:g})")
+    say(f"  {name}: normwise-max {err:.3e} rms {rms:.3e} (tol {TOL[dtype]:g}, "
+        f"derived {DERIVED[dtype]:.3e})")
     assert y.shape == ref.shape
     assert np.all(np.isfinite(y))
     assert err <= TOL[dtype], (name, err)
+    assert err <= DERIVED[dtype], (name, err)
     return err
 
 

@@ -1,0 +1,356 @@
+"""CPU model of the ONE_LAUNCH kernel (csrc/whtmix_onelaunch.hip), no GPU.
+
+Re-states in numpy:
+* the cross-lane primitives as the gfx9/gfx950 ISA defines them -- DPP
+  (quad_perm, row_shl, row_shr with row and bank masks, bound_ctrl off) and
+  v_permlane16_swap / v_permlane32_swap on a register pair;
+* the kernel's wave butterflies built from them (lane_partner, lane_bfly,
+  swap_k2, wave_bfly, wht9) on a 64-lane x 8-register file;
+* the layouts V4 / V8, the workspace run map and the gain index of the three
+  passes;
+* the scheduler: workgroup w takes tiles w, w + P, ... of each pass; per-slice
+  counters order the passes; bounded waits; the last workgroup out resets the
+  counters.
+
+and checks that the butterflies transform exactly the bits they claim, that
+every load and store stays inside its buffer and touches each element once,
+that the modelled pipeline reproduces the CPU oracle, and that the schedule
+terminates (and resets its counters) for every shape, including after a wait
+that gives up.  Test code only; nothing in the product path uses it.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as oracle_mod
+
+TB, NV, LANES = 9, 8, 64
+COUNTER_WORDS = 4096
+
+
+# ---------------------------------------------------------------- primitives
+def update_dpp(old, src, ctrl, row_mask, bank_mask, bound_ctrl=False):
+    """One lane-permuting DPP move on 64 lanes (gfx9 semantics)."""
+    out = np.array(old, copy=True)
+    for lam in range(LANES):
+        row, bank = lam >> 4, (lam >> 2) & 3
+        if not ((row_mask >> row) & 1 and (bank_mask >> bank) & 1):
+            continue
+        if ctrl <= 0xFF:                                  # quad_perm
+            s = (lam & ~3) | ((ctrl >> (2 * (lam & 3))) & 3)
+        elif 0x101 <= ctrl <= 0x10F:                      # row_shl: read lane + n
+            n = ctrl - 0x100
+            s = lam + n if (lam & 15) + n < 16 else None
+        elif 0x111 <= ctrl <= 0x11F:                      # row_shr: read lane - n
+            n = ctrl - 0x110
+            s = lam - n if (lam & 15) >= n else None
+        else:
+            raise ValueError(hex(ctrl))
+        if s is None:
+            if bound_ctrl:
+                out[lam] = 0
+            continue
+        out[lam] = src[s]
+    return out
+
+
+def permlane_swap(a, b, width):
+    """v_permlane{16,32}_swap_b32 a, b: odd 16-lane rows (width 16) or the
+    upper 32 lanes (width 32) of a trade places with the even rows / lower
+    lanes of b."""
+    a2, b2 = np.array(a, copy=True), np.array(b, copy=True)
+    for lam in range(LANES):
+        if lam & width:
+            a2[lam], b2[lam - width] = b[lam - width], a[lam]
+    return a2, b2
+
+
+def lane_partner(x, J):
+    if J == 0:
+        return update_dpp(np.zeros_like(x), x, 0xB1, 0xF, 0xF)
+    if J == 1:
+        return update_dpp(np.zeros_like(x), x, 0x4E, 0xF, 0xF)
+    if J == 2:
+        hi = update_dpp(np.zeros_like(x), x, 0x114, 0xF, 0xA)
+        return update_dpp(hi, x, 0x104, 0xF, 0x5)
+    hi = update_dpp(np.zeros_like(x), x, 0x118, 0xF, 0xC)
+    return update_dpp(hi, x, 0x108, 0xF, 0x3)
+
+
+LANE = np.arange(LANES)
+
+
+def reg_bfly(v, J):
+    v = v.copy()
+    for k in range(NV):
+        if not k & (1 << J):
+            a, b = v[k].copy(), v[k | (1 << J)].copy()
+            v[k], v[k | (1 << J)] = a + b, a - b
+    return v
+
+
+def lane_bfly(v, J):
+    s = np.where(LANE & (1 << J), -1.0, 1.0)
+    return np.stack([s * v[k] + lane_partner(v[k], J) for k in range(NV)])
+
+
+def swap_k2(v, width):
+    v = v.copy()
+    for k in range(4):
+        v[k], v[k + 4] = permlane_swap(v[k], v[k + 4], width)
+    return v
+
+
+def wave_bfly(v, J0):
+    v = reg_bfly(v, 2)
+    for J in range(max(J0, 0), 4):
+        v = lane_bfly(v, J)
+    if J0 <= 4:
+        v = reg_bfly(swap_k2(v, 16), 2)
+        v = swap_k2(v, 16)
+    v = reg_bfly(swap_k2(v, 32), 2)
+    return swap_k2(v, 32)
+
+
+def wht9(v):
+    return wave_bfly(reg_bfly(reg_bfly(v, 0), 1), 0)
+
+
+# ---------------------------------------------------------------- layouts
+def t_index(layout):
+    """[8, 64] tile index of (register k, lane) in layout "V4" or "V8"."""
+    k = np.arange(NV)[:, None]
+    lam = LANE[None, :]
+    if layout == "V4":
+        return (k & 3) | (lam << 2) | ((k >> 2) << 8)
+    return k | (lam << 3)
+
+
+def group_t(layout, g):
+    return (LANE << 2) | (g << 8) if layout == "V4" else (LANE << 3) | (g << 2)
+
+
+def run_off(t, R):
+    return ((t >> R) << TB) | (t & ((1 << R) - 1))
+
+
+def dense_wht(n):
+    i = np.arange(n)
+    return np.array([[(-1.0) ** bin(a & b).count("1") for b in i] for a in i])
+
+
+def bitwise_wht(x, bits):
+    """Unnormalised butterflies of a vector over the given index bits."""
+    x = x.astype(np.float64).copy()
+    for j in bits:
+        h = 1 << j
+        idx = np.arange(x.size)
+        lo = idx[(idx & h) == 0]
+        a, b = x[lo].copy(), x[lo | h].copy()
+        x[lo], x[lo | h] = a + b, a - b
+    return x
+
+
+# ---------------------------------------------------------------- tests
+def test_dpp_partners_are_lane_xor():
+    x = np.arange(LANES, dtype=np.float64) + 100.0
+    for J in range(4):
+        assert np.array_equal(lane_partner(x, J), x[LANE ^ (1 << J)]), J
+
+
+def test_permlane_swap_transposes_a_lane_bit_with_register_bit_2():
+    """After swap_k2(W), register k holds what (k ^ 4 if its lane bit is set
+    ...) held: register bit 2 and lane bit log2(W) trade roles."""
+    v = np.arange(NV * LANES, dtype=np.float64).reshape(NV, LANES)   # value = k*64 + lane
+    for W, lb in ((16, 4), (32, 5)):
+        s = swap_k2(v, W)
+        for k in range(NV):
+            for lam in range(LANES):
+                k2, l5 = (k >> 2) & 1, (lam >> lb) & 1
+                src_k = (k & 3) | (l5 << 2)
+                src_l = (lam & ~(1 << lb)) | (k2 << lb)
+                assert s[k, lam] == v[src_k, src_l]
+        assert np.array_equal(swap_k2(s, W), v)            # an involution
+
+
+@pytest.mark.parametrize("layout", ["V4", "V8"])
+def test_wht9_is_the_full_tile_transform(layout):
+    rng = np.random.default_rng(7)
+    tile = rng.standard_normal(512)
+    T = t_index(layout)
+    v = tile[T]
+    out = np.empty(512)
+    out[T] = wht9(v)
+    np.testing.assert_allclose(out, dense_wht(512) @ tile, rtol=0, atol=1e-9)
+
+
+@pytest.mark.parametrize("R", [2, 3, 4, 5, 6])
+def test_wave_bfly_transforms_the_high_bits_only(R):
+    rng = np.random.default_rng(R)
+    tile = rng.standard_normal(512)
+    T = t_index("V4")
+    out = np.empty(512)
+    out[T] = wave_bfly(tile[T], R - 2)
+    np.testing.assert_allclose(out, bitwise_wht(tile, range(R, TB)), rtol=0, atol=1e-9)
+
+
+def run_pipeline(x, g, K, B, nvalid, dtype_layout):
+    """The three passes on flat slices (numpy float64), with every index the
+    kernel computes; returns y and per-buffer touch counts."""
+    HB = K - TB
+    R = TB - HB
+    tiles = 1 << HB
+    ws = np.full(B << K, np.nan)
+    y = np.full(B * nvalid, np.nan)
+    ws_writes = np.zeros(B << K, int)
+    x_reads = np.zeros(B * nvalid, int)
+    g_reads = np.zeros(1 << K, int)
+    y_writes = np.zeros(B * nvalid, int)
+    T_io = t_index(dtype_layout)
+    T4 = t_index("V4")
+    io_group = 4 if dtype_layout == "V4" else 8
+    for b in range(B):                                   # pass 1
+        for hi in range(tiles):
+            start = hi << TB
+            valid = max(0, min(nvalid - start, 512))
+            v = np.zeros((NV, LANES))
+            ok = T_io < valid
+            v[ok] = x[b * nvalid + start + T_io[ok]]
+            np.add.at(x_reads, b * nvalid + start + T_io[ok], 1)
+            v = wht9(v)
+            off = (b << K) + (hi << R) + run_off(T_io, R)
+            assert off.min() >= b << K and off.max() < (b + 1) << K
+            ws[off] = v
+            np.add.at(ws_writes, off, 1)
+    assert np.all(ws_writes == 1)
+    scale = 2.0 ** -K
+    for b in range(B):                                   # pass 2
+        for run in range(tiles):
+            base = (b << K) + (run << TB)
+            v = ws[base + T4]
+            u = T4
+            f = ((u >> R) << TB) | (run << R) | (u & ((1 << R) - 1))
+            assert f.min() >= 0 and f.max() < 1 << K
+            np.add.at(g_reads, f, 1)
+            v = wave_bfly(v, R - 2)
+            v = v * (g[f] * scale)
+            v = wave_bfly(v, R - 2)
+            ws[base + T4] = v
+            np.add.at(ws_writes, base + T4, 1)
+    assert np.all(ws_writes == 2)
+    assert np.all(g_reads == B)
+    for b in range(B):                                   # pass 3
+        for hi in range(tiles):
+            start = hi << TB
+            valid = max(0, min(nvalid - start, 512))
+            if valid == 0:
+                continue
+            off = (b << K) + (hi << R) + run_off(T_io, R)
+            v = wht9(ws[off])
+            ok = T_io < valid
+            y[b * nvalid + start + T_io[ok]] = v[ok]
+            np.add.at(y_writes, b * nvalid + start + T_io[ok], 1)
+    assert np.all(x_reads == 1) and np.all(y_writes == 1)
+    # 16-byte groups are all-valid or all-padding when nvalid % 8 == 0
+    assert nvalid % io_group == 0 or nvalid % 8 != 0
+    return y
+
+
+@pytest.mark.parametrize("K,B,N,C,layout", [
+    (12, 1, 64, 64, "V4"), (13, 2, 128, 64, "V8"), (14, 1, 256, 64, "V4"),
+    (15, 3, 256, 128, "V8"), (16, 1, 1024, 64, "V4"), (16, 2, 1024, 64, "V8"),
+    (16, 1, 1000, 64, "V4"), (15, 2, 200, 128, "V8"), (13, 1, 33, 128, "V4"),
+])
+def test_pipeline_matches_oracle(K, B, N, C, layout):
+    P = 1 << max(0, (N - 1).bit_length())
+    assert P * C == 1 << K
+    rng = np.random.default_rng(K * 100 + N)
+    x = rng.standard_normal((B, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    y = run_pipeline(x.reshape(-1), g.reshape(-1), K, B, N * C, layout)
+    ref = oracle_mod.whtmix(x, g)
+    np.testing.assert_allclose(y.reshape(B, N, C), ref, rtol=0, atol=1e-9 * np.abs(ref).max())
+
+
+# ---------------------------------------------------------------- scheduler
+def simulate(B, K, P, spin_limit=10 ** 9, stall=None):
+    """Round-robin interleaving of P resident one-wave workgroups, each a
+    sequence of steps: pass-1 tiles (signal c0), pass-2 tiles (wait c0, signal
+    c1), pass-3 tiles (wait c1), exit.  `stall`: (wg, polls) makes workgroup
+    wg sit idle for that many rounds before its first tile (a slow wave).
+    Returns (rounds, counters after the run, error flags)."""
+    HB = K - TB
+    tiles = 1 << HB
+    ntiles = B << HB
+    ctr = np.zeros(COUNTER_WORDS, np.int64)
+    c0, c1 = 0, B
+    EXITED, CALL_ERR, STICKY = COUNTER_WORDS - 3, COUNTER_WORDS - 2, COUNTER_WORDS - 1
+    progs = []
+    for w in range(P):
+        items = [(1, i) for i in range(w, ntiles, P)] + \
+                [(2, i) for i in range(w, ntiles, P)] + [(3, i) for i in range(w, ntiles, P)]
+        progs.append({"items": items, "pos": 0, "polls": 0, "ok": True, "done": False,
+                      "idle": stall[1] if stall and stall[0] == w else 0})
+    rounds = 0
+    while not all(p["done"] for p in progs):
+        rounds += 1
+        assert rounds < 10 ** 6, "schedule did not finish"
+        for w, p in enumerate(progs):
+            if p["done"]:
+                continue
+            if p["idle"]:
+                p["idle"] -= 1
+                continue
+            if p["pos"] == len(p["items"]) or not p["ok"]:
+                prior = ctr[EXITED]
+                ctr[EXITED] += 1
+                if prior == P - 1:
+                    if ctr[CALL_ERR]:
+                        ctr[STICKY] |= ctr[CALL_ERR]
+                    ctr[:2 * B] = 0
+                    ctr[CALL_ERR] = 0
+                    ctr[EXITED] = 0
+                p["done"] = True
+                continue
+            pas, i = p["items"][p["pos"]]
+            b = i >> HB
+            if pas == 1:
+                ctr[c0 + b] += 1
+                p["pos"] += 1
+                continue
+            need = c0 + b if pas == 2 else c1 + b
+            if ctr[need] < tiles:
+                if ctr[CALL_ERR]:
+                    p["ok"] = False
+                    continue
+                p["polls"] += 1
+                if p["polls"] > spin_limit:
+                    ctr[CALL_ERR] = 1
+                    p["ok"] = False
+                continue
+            p["polls"] = 0
+            if pas == 2:
+                ctr[c1 + b] += 1
+            p["pos"] += 1
+    return rounds, ctr
+
+
+@pytest.mark.parametrize("B,K,P", [(1, 16, 128), (2, 16, 256), (47, 16, 700), (3, 12, 5),
+                                   (16, 14, 33), (5, 15, 1), (2046, 12, 4096)])
+def test_schedule_completes_and_resets(B, K, P):
+    P = min(P, B << (K - TB))
+    _, ctr = simulate(B, K, P)
+    assert not ctr.any()
+
+
+def test_wait_that_gives_up_still_drains_and_flags():
+    """A tiny poll limit with one slow workgroup: some wait gives up, every
+    workgroup still exits, the counters return to zero and only the sticky
+    word remains set (the host reads and clears it)."""
+    _, ctr = simulate(2, 14, 16, spin_limit=0, stall=(0, 50))
+    assert ctr[COUNTER_WORDS - 1] == 1
+    ctr[COUNTER_WORDS - 1] = 0
+    assert not ctr.any()
+
+
+def test_batch_limit_matches_counter_block():
+    assert 2 * 2046 + 3 <= COUNTER_WORDS < 2 * 2047 + 3
