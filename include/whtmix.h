@@ -170,6 +170,23 @@ typedef struct whtmix_plan_info {
 WHTMIX_API int whtmix_forward(const void *x, const float *gain, void *y,
                    int64_t B, int64_t N, int64_t C, int dtype, void *stream);
 
+/*
+ * whtmix_forward_noalloc -- whtmix_forward for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, result, plan (AUTO) and checks as
+ * whtmix_forward, but the three-pass workspace is a fixed 32 MiB device array
+ * inside the library (one per device, held until the process ends) instead
+ * of the per-stream workspace, and the call allocates nothing: no hipMalloc,
+ * no hipFree, no stream synchronisation.  Limit: shapes whose plan needs a
+ * workspace must have B * N_pad * C <= 2^23; larger ones return
+ * WHTMIX_ERROR_TOO_LARGE (text in whtmix_last_error()) with nothing
+ * enqueued.  Every call on a device shares that device's array, so calls
+ * that overlap on one device (on different streams or host threads) race;
+ * serialise them.
+ */
+WHTMIX_API int whtmix_forward_noalloc(const void *x, const float *gain, void *y,
+                           int64_t B, int64_t N, int64_t C, int dtype, void *stream);
+
 /* As whtmix_forward, with options (NULL = defaults). */
 WHTMIX_API int whtmix_forward_ex(const void *x, const float *gain, void *y,
                       int64_t B, int64_t N, int64_t C, int dtype, void *stream,

@@ -253,9 +253,11 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
 
 namespace {
 
+// noalloc: the three-pass workspace is the fixed device scratch instead of
+// the per-stream workspace, and nothing is allocated.
 int forward_impl(const void *x, int gain_kind, const float *gain, const float *gain_t,
                  const float *gain_c, void *y, int64_t B, int64_t N, int64_t C, int dtype,
-                 void *stream, const whtmix_options *options)
+                 void *stream, const whtmix_options *options, bool noalloc = false)
 {
     Checked c;
     int st = check_shape(B, N, C, dtype, options, &c);
@@ -295,6 +297,20 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
     for (int i = 0; i < 4; ++i)
         a.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
 
+    if (c.plan == whtmix::PLAN_THREE_PASS && noalloc) {
+        if (c.ws_bytes > whtmix::kNoAllocScratchFloats * 4) {
+            g_last_error = "whtmix_forward_noalloc: the call needs " + std::to_string(c.ws_bytes) +
+                           " bytes of workspace, more than the fixed " +
+                           std::to_string(whtmix::kNoAllocScratchFloats * 4) +
+                           "-byte scratch (B * N_pad * C <= 2^23)";
+            return WHTMIX_ERROR_TOO_LARGE;
+        }
+        hipError_t e = whtmix::noalloc_scratch(&a.ws);
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the scratch");
+        e = whtmix::launch(a);
+        if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        return WHTMIX_SUCCESS;
+    }
     if (c.plan == whtmix::PLAN_THREE_PASS) {
         std::lock_guard<std::mutex> lock(g_ws_mutex);
         st = get_workspace(stream, c.ws_bytes, &a.ws);
@@ -674,6 +690,13 @@ int whtmix_forward(const void *x, const float *gain, void *y, int64_t B, int64_t
                    int dtype, void *stream)
 {
     return whtmix_forward_ex(x, gain, y, B, N, C, dtype, stream, nullptr);
+}
+
+int whtmix_forward_noalloc(const void *x, const float *gain, void *y, int64_t B, int64_t N,
+                           int64_t C, int dtype, void *stream)
+{
+    return forward_impl(x, whtmix::GAIN_FULL, gain, nullptr, nullptr, y, B, N, C, dtype, stream,
+                        nullptr, true);
 }
 
 const char *whtmix_status_string(int status)

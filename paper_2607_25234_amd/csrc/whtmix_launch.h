@@ -43,6 +43,11 @@ hipError_t launch(const LaunchArgs &a);
 // a.B * 2^K floats and a.counters a zeroed-or-reset counter block).
 hipError_t launch_one_launch(const LaunchArgs &a);
 
+// Device address of the fixed scratch array on the current device
+// (kNoAllocScratchFloats floats; whtmix_noalloc.hip).  Looks the address up
+// once per device; allocates nothing.
+hipError_t noalloc_scratch(float **out);
+
 // A validated backward call.  dX = the mixer applied to dY (may be null);
 // the gain gradient goes to dgain (joint) or dgt/dgc (separable log gains),
 // any of which may be null to skip it.

@@ -45,6 +45,10 @@ constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
 // Polls of a ONE_LAUNCH wait before it gives up (about a second or two).
 constexpr unsigned kDefaultSpinLimit = 1u << 21;
 
+// whtmix_forward_noalloc: the fixed device scratch (32 MiB of floats) that
+// holds its three-pass workspace, B * N_pad * C floats at most.
+constexpr long long kNoAllocScratchFloats = 1ll << 23;
+
 // THREE_PASS split for slice bits K:
 //   outer passes: contiguous chunks of 2^A elements (all A low bits of f);
 //   middle pass : the HB = K - A high bits, for a run of 2^R contiguous low

@@ -26,6 +26,7 @@ EXPORTS = (
     "whtmix_backward_separable",
     "whtmix_forward",
     "whtmix_forward_ex",
+    "whtmix_forward_noalloc",
     "whtmix_forward_separable",
     "whtmix_module_backward",
     "whtmix_module_backward_separable",
@@ -88,6 +89,8 @@ def lib():
         L.whtmix_forward_ex.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                         ctypes.POINTER(Options)]
         L.whtmix_forward_ex.restype = ctypes.c_int
+        L.whtmix_forward_noalloc.argtypes = [vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
+        L.whtmix_forward_noalloc.restype = ctypes.c_int
         L.whtmix_forward_separable.argtypes = [vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp,
                                                ctypes.POINTER(Options)]
         L.whtmix_forward_separable.restype = ctypes.c_int
@@ -178,6 +181,13 @@ def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
     opt = _options(plan, events, spin_limit)
     return lib().whtmix_forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream,
                                    ctypes.byref(opt))
+
+
+def forward_noalloc_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
+                        dtype: int, stream: int) -> int:
+    """Direct call of whtmix_forward_noalloc (the fixed-scratch variant that
+    allocates nothing); returns the status."""
+    return lib().whtmix_forward_noalloc(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream)
 
 
 def padded_tokens(N: int) -> int:

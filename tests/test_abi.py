@@ -346,3 +346,15 @@ def test_python_forward_rejects_host_tensors():
     g = torch.ones(64, 64)
     with pytest.raises(ValueError):
         whtmix.forward(x, g)
+
+
+def test_noalloc_rejects_beyond_its_scratch_before_any_hip_call():
+    """whtmix_forward_noalloc: B * N_pad * C above 2^23 with a workspace plan
+    is TOO_LARGE; the usual argument checks come first."""
+    big = (1 << 40, 1 << 41, 1 << 42)
+    assert whtmix.forward_noalloc_raw(*big, 5, 16384, 128, 0, 0) == 7
+    assert "scratch" in whtmix.last_error()
+    assert whtmix.forward_noalloc_raw(*big, 1, 65536, 256, 1, 0) == 7
+    assert whtmix.forward_noalloc_raw(0, 1 << 41, 1 << 42, 1, 64, 64, 0, 0) == 1
+    assert whtmix.forward_noalloc_raw(*big, 1, 64, 63, 0, 0) == 2
+    assert whtmix.forward_noalloc_raw(*big, 0, 64, 64, 0, 0) == 0
