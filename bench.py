@@ -15,20 +15,22 @@ the 256 MB Infinity Cache, so every step reads its inputs from HBM (cold).
 
 Prints one JSON line:
 - value: GB/s of ideal traffic (read x + read G once + write y) per second of
-  wall time over the K timed steps; tokens/s; fraction of the 8 TB/s peak;
+  wall time over the K timed steps (which carry no HIP events: each event
+  record costs the stream about 3 us); tokens/s; fraction of the 8 TB/s peak;
+- per_call: median / p10 / p90 of >= 100 further calls, each between two
+  HIP events the library records on the launch stream before its first and
+  after its last kernel, rotating over the sets (`rotating`), and again with
+  a 1 GiB scrub written before each call outside its events (`cold`);
 - roofline: the whole call (every kernel of the plan) as the unit: ideal
-  bytes over the call's GPU time from HIP events recorded by the library on
-  the launch stream around each timed call; `traffic` is the whole call's
+  bytes over the mean rotating call time; `traffic` is the whole call's
   rocprofv3 FETCH_SIZE + WRITE_SIZE bytes (committed counter record, null when
   taken on other kernel sources) and `traffic_ratio` that over the ideal bytes;
-- per_call: median / p10 / p90 of >= 100 further calls, each in its own event
-  pair, rotating over the sets (`rotating`) and with a 1 GiB scrub written
-  between calls outside the pair (`cold`);
-- floor_ms: the same traffic as the three-pass plan moved by plain PyTorch
-  copies (widen x to float32, multiply a float32 buffer by G in place, narrow
-  to y): what an exact float32-exchange schedule of this shape cannot beat;
-- kernels: each kernel's average time and rate on its own design bytes
-  (x, y, the gain and the float32 workspace round trips), not ideal bytes;
+- floor_ms: the three-pass plan's x, float32-workspace and y traffic moved by
+  plain PyTorch kernels of the same shapes (widen x, scale the workspace in
+  place, narrow into y), without the gain read;
+- kernels: each kernel's average time (events between kernels, which add
+  about 3 us each) and rate on its own design bytes (x, y, the gain and the
+  float32 workspace round trips), not ideal bytes;
 - cpu_baseline: the float64 CPU oracle on a bounded sample, on all host cores
   and on one core, with the host CPU model.
 """
@@ -280,25 +282,22 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
 
 
 def copy_floor(torch, w, sets, P: int, hip, stream_ptr: int, reps: int = 20) -> dict:
-    """Time of the three-pass plan's traffic done by plain PyTorch kernels on
-    the same buffers: x widened to a float32 buffer, that buffer multiplied
-    in place by G (broadcast over the batch), then narrowed into y."""
-    L = P * w.C
-    ws = torch.empty((w.B, L), dtype=torch.float32, device=sets[0]["x"].device)
+    """The three-pass plan's x, workspace and y traffic done by plain PyTorch
+    kernels on buffers of the same shapes: x widened into a float32 buffer,
+    that buffer scaled in place, then narrowed into y (medians).  The gain's
+    read (4 N_pad C bytes once) is not in it."""
+    ws = torch.empty((w.B, P, w.C), dtype=torch.float32, device=sets[0]["x"].device)
+    n = w.N
     ev = [hip.create() for _ in range(4)]
     acc = [[], [], []]
     for r in range(reps):
         t = sets[r % len(sets)]
-        xv = t["x"].view(w.B, -1)
-        yv = t["y"].view(w.B, -1)
-        gv = t["g"].view(1, -1)
-        n = xv.shape[1]
         hip.record(ev[0], stream_ptr)
-        ws[:, :n].copy_(xv)
+        ws[:, :n].copy_(t["x"])
         hip.record(ev[1], stream_ptr)
-        ws.mul_(gv)
+        ws.mul_(1.5)
         hip.record(ev[2], stream_ptr)
-        yv.copy_(ws[:, :n])
+        t["y"].copy_(ws[:, :n])
         hip.record(ev[3], stream_ptr)
         torch.cuda.synchronize()
         for j in range(3):
@@ -307,9 +306,10 @@ def copy_floor(torch, w, sets, P: int, hip, stream_ptr: int, reps: int = 20) -> 
     med = [float(np.median(a)) for a in acc]
     del ws
     return {"floor_ms": round(sum(med), 5),
-            "parts_ms": {"widen_copy": round(med[0], 5), "inplace_gain_multiply": round(med[1], 5),
+            "parts_ms": {"widen_copy": round(med[0], 5), "inplace_scale": round(med[1], 5),
                          "narrow_copy": round(med[2], 5)},
-            "note": "medians of PyTorch copy / multiply kernels over the same buffers"}
+            "note": "PyTorch copy_ / mul_ kernels moving x, the float32 workspace and y as the "
+                    "three passes do, without the gain read"}
 
 
 def main() -> int:
@@ -456,32 +456,22 @@ def main() -> int:
         step(i)
     torch.cuda.synchronize()
 
-    # Timed steps.  The library records the caller's events on the launch
-    # stream: before its first kernel and after its last on every step (the
-    # call's GPU time), and between kernels on every --event-every-th step.
-    every = max(1, args.event_every)
-    evs = []
-    for i in range(args.steps):
-        e = [hip.create() for _ in range(nk + 1)] if i % every == 0 else \
-            [hip.create()] + [None] * (nk - 1) + [hip.create()]
-        evs.append(e)
+    # Timed steps: no HIP events inside them (each event record costs the
+    # stream about 3 us, measured), only the host clock around the K steps.
     torch.cuda.synchronize()            # barrier (one rank) + device sync
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(args.warmup + i)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    call_ms = [hip.elapsed_ms(e[0], e[nk]) for e in evs]
-    sampled = [e for e in evs if e[1 if nk > 1 else 0] is not None]
-    per_kernel = [float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in sampled]))
-                  for j in range(nk)]
-    avg_call = float(np.mean(call_ms))
-
-    # Per-call distribution: >= 100 calls, each in its own event pair.
+    # Per-call distribution: >= 100 further calls on the same stream and sets,
+    # each between two HIP events the library records before its first and
+    # after its last kernel; then the same with a 1 GiB scrub written before
+    # each call, outside its events (cold caches).
     ncalls = max(100, args.calls)
-    pairs = [[hip.create()] + [None] * (nk - 1) + [hip.create()] for _ in range(ncalls)]
     base = args.warmup + args.steps
+    pairs = [[hip.create()] + [None] * (nk - 1) + [hip.create()] for _ in range(ncalls)]
     for i in range(ncalls):
         step(base + i, pairs[i])
     torch.cuda.synchronize()
@@ -494,6 +484,20 @@ def main() -> int:
     torch.cuda.synchronize()
     cold = [hip.elapsed_ms(e[0], e[nk]) for e in cold_pairs]
     del scrub
+    avg_call = float(np.mean(rotating))
+
+    # Per-kernel split: events between the kernels on a sample of calls
+    # (--event-every of them out of 4x as many); each inner event adds about
+    # 3 us to the kernel after it, so these sum above the call time.
+    every = max(1, args.event_every)
+    kev = [[hip.create() for _ in range(nk + 1)] if i % every == 0 else None
+           for i in range(4 * every * 8)]
+    for i, e in enumerate(kev):
+        step(base + 2 * ncalls + i, e)
+    torch.cuda.synchronize()
+    sampled = [e for e in kev if e is not None]
+    per_kernel = [float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in sampled]))
+                  for j in range(nk)]
 
     floor = None
     if op == "forward" and plan["plan"] in ("three_pass", "one_launch"):
@@ -554,6 +558,9 @@ def main() -> int:
                      "traffic": traffic,
                      "traffic_ratio": None if traffic is None else round(traffic / io_bytes, 3)},
         "per_call": {"rotating": percentiles(rotating), "cold": percentiles(cold)},
+        "timing": "timed steps carry no events; the call time is the mean of the rotating "
+                  "per-call event pairs; kernel times come from separate calls with events "
+                  "between their kernels (about 3 us each)",
         "floor_ms": None if floor is None else floor["floor_ms"],
         "floor": floor,
         "event_sampled_steps": len(sampled),

@@ -197,7 +197,7 @@ template <int A, int HB, int R, class Gain>
 hipError_t launch_middle_split(const LaunchArgs &a, Gain gain)
 {
     static_assert(HB >= 1 && HB + R >= kMinTile && HB + R <= kMaxTile, "middle tile size");
-    return with_middle_gain(gain, a.B, [&](auto g) {
+    return with_forward_middle_gain(gain, a.B, A + HB, [&](auto g) {
         hipLaunchKernelGGL((middle_kernel<A, HB, R, decltype(g)>), dim3((uint32_t)(a.B << (A - R))),
                            dim3(1u << (HB + R - VB)), 0, a.stream, a.ws, g, (uint32_t)a.B);
         return hipGetLastError();

@@ -505,8 +505,9 @@ __device__ __forceinline__ void store_tile_vec(const float (&v)[V], T *base, uin
 // loads (MIDDLE) are non-temporal.  The host picks it for a batch of one
 // slice, whose middle pass reads each gain element exactly once, so the gain
 // does not displace the workspace in the Infinity Cache (stereo256k 334 ->
-// 309 us per step); with more slices each gain tile is read once per slice
-// on one XCD and temporal loads let those reads hit (non-temporal ones cost
+// 309 us per step), and for gains of 16 MiB and more (with_forward_middle_gain).
+// With more slices each gain tile is read once per slice on one XCD, and for
+// small gains temporal loads let those reads hit (non-temporal ones cost
 // text4k, 32 slices, 38 -> 42 us).  A type, not a run-time flag: the
 // compiler merges the loads of the two branches of a flag and drops the hint.
 template <bool NT>
@@ -548,6 +549,23 @@ template <class F>
 inline hipError_t with_middle_gain(FullGain gain, int64_t slices, F &&f)
 {
     return slices == 1 ? f(StreamedGain{gain.g}) : f(gain);
+}
+
+// The forward middle pass also streams a joint gain of 2^22 elements (16 MiB)
+// or more whatever the batch: keeping the workspace in the Infinity Cache
+// then outweighs the L2 hits of the slices that share a gain tile
+// (stereo64k, four slices of 2^23: 120.6 -> 118.5 us per step).  Smaller
+// gains keep temporal loads (stereo16k and text4k measured slower streamed).
+constexpr int kStreamGainMinK = 22;
+template <class Gain, class F>
+inline hipError_t with_forward_middle_gain(Gain gain, int64_t slices, int, F &&f)
+{
+    return with_middle_gain(gain, slices, f);
+}
+template <class F>
+inline hipError_t with_forward_middle_gain(FullGain gain, int64_t slices, int K, F &&f)
+{
+    return slices == 1 || K >= kStreamGainMinK ? f(StreamedGain{gain.g}) : f(gain);
 }
 
 // The paper's parametrisation (eqs. (2)-(3)): log-domain gains g_t[N_pad]
