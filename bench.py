@@ -261,9 +261,20 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
 
     threads = orc.threads()
     runs, t_total, t_wl = timed(seconds * 0.6)
-    prev = orc.set_threads(1)
-    runs1, t_total1, t_wl1 = timed(seconds * 0.4)
-    orc.set_threads(prev)
+    # one core: skipped when a single run would take far beyond its share
+    # of the budget (perfect scaling would make it threads x slower)
+    est1 = t_total / runs * threads
+    single = None
+    if est1 <= 4 * seconds * 0.4:
+        prev = orc.set_threads(1)
+        runs1, t_total1, t_wl1 = timed(seconds * 0.4)
+        orc.set_threads(prev)
+        single = {"value": round(io_bytes / t_wl1 / 1e9, 4), "unit": "GB/s",
+                  "tokens_per_s": round(w.B * w.N / t_wl1, 1), "cores": 1,
+                  "sample": f"{runs1} run(s) of one slice, {t_total1:.1f} s total"}
+    else:
+        single = {"value": None, "cores": 1,
+                  "sample": f"skipped: one run of one slice would take about {est1:.0f} s on one core"}
     return {
         "value": round(io_bytes / t_wl / 1e9, 4),
         "unit": "GB/s",
@@ -275,9 +286,7 @@ def cpu_baseline(w, op: str, host0, io_bytes: int, seconds: float) -> dict:
         "sample": (f"{runs} run(s) of one of the {w.B} batch slices ({w.N}x{w.C}), "
                    f"{t_total:.1f} s total, float64 C oracle with OpenMP on {threads} threads; "
                    f"rate scaled to the whole {w.B}-slice workload"),
-        "single_core": {"value": round(io_bytes / t_wl1 / 1e9, 4), "unit": "GB/s",
-                        "tokens_per_s": round(w.B * w.N / t_wl1, 1), "cores": 1,
-                        "sample": f"{runs1} run(s) of one slice, {t_total1:.1f} s total"},
+        "single_core": single,
     }
 
 

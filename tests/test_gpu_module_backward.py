@@ -110,6 +110,22 @@ def test_module_backward_workload_slice(dev, orc):
     check_all("stereo64k slice", got, orc.whtmix_module_grad(x, wi, g, wo, dy), w.dtype)
 
 
+def test_module_backward_c256_pair_tiles_against_oracle(dev, orc):
+    """One 2^26-element slice (N = 262144, C = 256, bf16): the fused pair-tile
+    block backward (2^16-element outer tiles with the projections inside the
+    passes) against oracle_whtmix_module_grad in float64 (about a minute of
+    host time on every core)."""
+    B, N, C = 1, 262144, 256
+    d = whtmix.plan_describe(B, N, C, "bf16")
+    assert d["module_backward_fused"] and d["module_outer_bits"] == 16, d
+    x, dy, g, wi, wo = inputs(B, N, C, "bf16", seed=260)
+    say(f"module backward {(B, N, C)} bf16 pair tiles: GPU, then the oracle "
+        f"on {orc.threads()} threads")
+    got = run(x, dy, wi, wo, "bf16", dev, g=g)
+    ref = orc.whtmix_module_grad(x, wi, g, wo, dy)
+    check_all("2^26 pair tiles", got, ref, "bf16")
+
+
 def test_module_backward_forced_three_pass_and_alias(dev, orc):
     """The three-pass mixer on a 2^14 slice, with dx written over dy."""
     B, N, C = 2, 128, 128
