@@ -135,3 +135,30 @@ def test_give_up_path_reports_and_recovers(dev, orc):
     y = whtmix.forward(xd, gd, plan="one_launch")
     status_ok()
     check("after give-up", to_host(y), orc.whtmix(x, g), "f32")
+
+
+def test_two_streams_run_independently(dev, orc):
+    """Calls on two streams at once: each stream has its own workspace and
+    counter block, so the two kernels may overlap on the GPU."""
+    import torch
+    B, N, C = 8, 1024, 64
+    streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+    outs, refs = [], []
+    for i, s in enumerate(streams):
+        x, g = workloads.draw(B, N, C, "f32", seed=500 + i)
+        xd, gd = to_device(x, "f32", dev), torch.from_numpy(g).to(dev)
+        torch.cuda.synchronize(dev)
+        with torch.cuda.stream(s):
+            outs.append([whtmix.forward(xd, gd, plan="one_launch", stream=s) for _ in range(3)])
+        refs.append(orc.whtmix(x, g))
+    for s in streams:
+        assert whtmix.stream_status(s.cuda_stream) == whtmix.SUCCESS
+    for i, (o, r) in enumerate(zip(outs, refs)):
+        for j, y in enumerate(o):
+            check(f"stream {i} call {j}", to_host(y), r, "f32")
+
+
+def test_status_of_a_stream_without_single_launch_calls(dev):
+    import torch
+    s = torch.cuda.Stream(dev)
+    assert whtmix.stream_status(s.cuda_stream) == whtmix.SUCCESS
