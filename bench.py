@@ -62,7 +62,8 @@ def log(*a):
 
 # Sources the kernels of each path are compiled from: a counter record taken
 # on other sources is not reported.
-FORWARD_SOURCES = ("whtmix_kernels.hip", "whtmix_tile.h", "whtmix_plan.h", "whtmix_launch.h")
+FORWARD_SOURCES = ("whtmix_kernels.hip", "whtmix_tile.h", "whtmix_plan.h", "whtmix_launch.h",
+                   "whtmix_wave.hip")
 MODULE_SOURCES = FORWARD_SOURCES + ("whtmix_module.hip", "whtmix_module.h")
 
 
@@ -77,6 +78,7 @@ def kernel_source_hash(files=FORWARD_SOURCES) -> str:
 
 def kernel_names(plan: str) -> list[str]:
     return {"three_pass": ["outer_fwd", "middle", "outer_inv"],
+            "wave_tiles": ["wave_pass1", "wave_middle", "wave_pass3"],
             "fused": ["fused"], "small": ["small"], "one_launch": ["one_launch"]}[plan]
 
 
@@ -91,7 +93,19 @@ def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) ->
     three = [B * L * (s + 4),           # read x, write float32 workspace
              B * L * 8 + gbytes,        # read + write workspace, read the gain once
              B * L * (4 + s)]           # read workspace, write y
-    return [sum(three)] if plan == "one_launch" else three
+    return [sum(three)] if plan == "one_launch" else three   # three_pass and wave_tiles
+
+
+def backward_plan(plan: dict) -> str:
+    """The plan the backward pass and the block run for a forward plan: slices
+    of 2^16 and more take the three-pass plan, smaller wave-tile shapes the
+    one-workgroup plan (the library's rule)."""
+    p = plan["plan"]
+    if p in ("wave_tiles", "one_launch"):
+        return "three_pass" if plan["log2_slice"] >= 16 or p == "one_launch" else "fused"
+    if p == "fused" and plan["log2_slice"] >= 16:
+        return "three_pass"
+    return p
 
 
 OPS = ("forward", "separable", "backward", "backward_separable", "module", "module_separable",
@@ -412,7 +426,7 @@ def main() -> int:
     hip = HipEvents()
     if op.startswith("backward"):
         nk, names = 2, (["fwd_transforms_gain_gradient", "dx_outer_inv"]
-                        if plan["plan"] == "three_pass" else ["gain_gradient", "dx"])
+                        if backward_plan(plan) == "three_pass" else ["gain_gradient", "dx"])
     elif op == "module_backward":
         nk, names = 3, (["transforms_and_gain_gradient", "z_prime_and_dw_out", "dx_and_dw_in"]
                         if plan["module_backward_fused"] else
@@ -420,7 +434,7 @@ def main() -> int:
     elif op.startswith("module"):
         # the block runs 2^16-element slices with the three-pass plan even
         # where the mixer's forward takes another plan
-        names = module_kernels("three_pass" if plan["module_outer_bits"] else plan["plan"],
+        names = module_kernels("three_pass" if plan["module_outer_bits"] else backward_plan(plan),
                                plan["module_path"])
         nk = len(names)
     else:
@@ -509,7 +523,7 @@ def main() -> int:
                   for j in range(nk)]
 
     floor = None
-    if op == "forward" and plan["plan"] in ("three_pass", "one_launch"):
+    if op == "forward" and plan["plan"] in ("three_pass", "one_launch", "wave_tiles"):
         floor = copy_floor(torch, w, sets, P, hip, sptr)
     hip.destroy()
 
@@ -525,7 +539,7 @@ def main() -> int:
     elif op.startswith("module"):
         gbytes = 4 * P * w.C if op == "module" else 4 * (P + w.C)
         alg, flops = module_algorithmic(names, w.B, w.N, P, w.C, s, gbytes)
-    elif plan["plan"] == "three_pass":
+    elif backward_plan(plan) == "three_pass":
         # fused three-pass gradients: phase 1 = OUTER_FWD of x and dy (read
         # both, write two float32 workspaces) + the middle pass (read both
         # workspaces and the gain, write dY's back and the gain gradient);

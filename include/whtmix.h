@@ -81,29 +81,33 @@ typedef enum whtmix_status {
 
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
  *   L <= 2^10          one small workgroup per slice, all stages in LDS;
- *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass;
- *   L = 2^16           FUSED (two register sets) from B = 48 slices, else
- *                      THREE_PASS (the backward pass and the block run 2^16
- *                      slices with THREE_PASS whatever the plan);
+ *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass; for
+ *                      L = 2^15 up to 16 slices WAVE_TILES instead;
+ *   L = 2^16           WAVE_TILES up to 3 slices, FUSED (two register sets)
+ *                      from 48 slices, THREE_PASS between;
  *   L >= 2^17          THREE_PASS: forward over the low bits of the flat
  *                      index, then forward over the high bits + gain +
  *                      inverse over the high bits, then inverse over the low
  *                      bits, exchanging through the workspace.
- * ONE_LAUNCH (never chosen by AUTO) runs THREE_PASS's three passes in a
- * single cooperative launch: one-wave tiles of 2^9 elements whose butterflies
- * stay in the wave (DPP and lane-swap exchanges, no LDS), the passes ordered
- * by per-slice counters in a small per-stream block; 2^12 <= L <= 2^16,
- * B <= 2046 and N*C a multiple of 8.  On MI355X it is slower than the plans
+ * WAVE_TILES runs the same three passes on one-wave tiles of 2^9 elements
+ * whose butterflies stay inside the wave (DPP and lane-swap exchanges, no
+ * LDS): three launches of 2^(K-9) workgroups per slice; 2^12 <= L <= 2^16
+ * and N*C a multiple of 8 (AUTO falls back to the plans above otherwise).
+ * ONE_LAUNCH (never chosen by AUTO) runs WAVE_TILES's three passes in a
+ * single cooperative launch, ordered by per-slice counters in a small
+ * per-stream block; B <= 2046 besides.  On MI355X it is slower than the plans
  * AUTO picks: a cooperative launch alone costs about 20 us, and a hand-off
  * between workgroups through memory costs more than a kernel boundary.
  * THREE_PASS may also be forced for 2^12 <= L <= 2^16 (tests compare it with
- * FUSED on the same shapes). */
+ * FUSED on the same shapes).  The backward pass and the block take FUSED
+ * for slices up to 2^15 and THREE_PASS from 2^16 whatever the forward plan. */
 typedef enum whtmix_plan {
     WHTMIX_PLAN_AUTO = 0,
     WHTMIX_PLAN_SMALL = 1,
     WHTMIX_PLAN_FUSED = 2,
     WHTMIX_PLAN_THREE_PASS = 3,
-    WHTMIX_PLAN_ONE_LAUNCH = 4
+    WHTMIX_PLAN_ONE_LAUNCH = 4,
+    WHTMIX_PLAN_WAVE_TILES = 5
 } whtmix_plan;
 
 typedef struct whtmix_options {
@@ -128,8 +132,9 @@ typedef struct whtmix_plan_info {
     int plan;             /* resolved whtmix_plan (never AUTO) */
     int kernels;          /* kernels launched per call (1 or 3) */
     int log2_slice;       /* K = log2(N*C) */
-    int outer_bits;       /* THREE_PASS, ONE_LAUNCH: flat-index bits of the outer passes */
-    int run_bits;         /* THREE_PASS, ONE_LAUNCH: log2 of the contiguous run carried
+    int outer_bits;       /* THREE_PASS, WAVE_TILES, ONE_LAUNCH: flat-index bits of the
+                             outer passes */
+    int run_bits;         /* THREE_PASS, WAVE_TILES, ONE_LAUNCH: log2 of the contiguous run carried
                              by the middle pass */
     int64_t workspace_bytes; /* float32 workspace this call needs */
     int64_t padded_tokens;   /* N_pad */
@@ -174,7 +179,7 @@ WHTMIX_API int whtmix_forward(const void *x, const float *gain, void *y,
  * whtmix_forward_noalloc -- whtmix_forward for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc).  Same arguments, result, plan (AUTO) and checks as
- * whtmix_forward, but the three-pass workspace is a fixed 32 MiB device array
+ * whtmix_forward, but the workspace of the three-pass and wave-tile plans is a fixed 32 MiB device array
  * inside the library (one per device, held until the process ends) instead
  * of the per-stream workspace, and the call allocates nothing: no hipMalloc,
  * no hipFree, no stream synchronisation.  Limit: shapes whose plan needs a

@@ -85,18 +85,24 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     if (K <= whtmix::kMaxSmall && B >= (int64_t(1) << 24))
         return WHTMIX_ERROR_TOO_LARGE;
     int plan = opt ? opt->plan : whtmix::PLAN_AUTO;
-    // ONE_LAUNCH moves x and y in 16-byte groups of 8 elements at most.
-    const bool one_launch_ok = K >= whtmix::kOneLaunchMinK && K <= whtmix::kOneLaunchMaxK &&
-                               B <= whtmix::kOneLaunchMaxBatch && (N * C) % 8 == 0;
+    // The wave-tile plans move x and y in 16-byte groups of up to 8 elements.
+    const bool wave_ok = K >= whtmix::kWaveMinK && K <= whtmix::kWaveMaxK && (N * C) % 8 == 0;
     switch (plan) {
     case whtmix::PLAN_AUTO:
         plan = K <= whtmix::kMaxSmall ? whtmix::PLAN_SMALL
+               : K == whtmix::kMaxTile && wave_ok && B <= whtmix::kWave15MaxBatch
+                   ? whtmix::PLAN_WAVE_TILES
                : K <= whtmix::kMaxTile ? whtmix::PLAN_FUSED
                : K == whtmix::kMaxFused && B >= whtmix::kFusedPairMinBatch ? whtmix::PLAN_FUSED
-                                                                          : whtmix::PLAN_THREE_PASS;
+               : K == whtmix::kMaxFused && wave_ok && B <= whtmix::kWave16MaxBatch
+                   ? whtmix::PLAN_WAVE_TILES
+                   : whtmix::PLAN_THREE_PASS;
+        break;
+    case whtmix::PLAN_WAVE_TILES:
+        if (!wave_ok) return WHTMIX_ERROR_INVALID_VALUE;
         break;
     case whtmix::PLAN_ONE_LAUNCH:
-        if (!one_launch_ok) return WHTMIX_ERROR_INVALID_VALUE;
+        if (!wave_ok || B > whtmix::kOneLaunchMaxBatch) return WHTMIX_ERROR_INVALID_VALUE;
         break;
     case whtmix::PLAN_SMALL:
         if (K > whtmix::kMaxSmall) return WHTMIX_ERROR_INVALID_VALUE;
@@ -114,25 +120,36 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     out->n_pad = int64_t(1) << nbits;
     out->plan = plan;
     out->elt = dtype == WHTMIX_DTYPE_BF16 ? 2 : 4;
-    out->kernels = plan == whtmix::PLAN_THREE_PASS ? 3 : 1;
+    out->kernels =
+        plan == whtmix::PLAN_THREE_PASS || plan == whtmix::PLAN_WAVE_TILES ? 3 : 1;
     if (plan == whtmix::PLAN_THREE_PASS) {
         out->split = whtmix::three_pass_split(K);
         out->ws_bytes = B * L * 4;
     }
-    if (plan == whtmix::PLAN_ONE_LAUNCH) {
+    if (plan == whtmix::PLAN_WAVE_TILES || plan == whtmix::PLAN_ONE_LAUNCH) {
         out->split = whtmix::Split{9, K - 9, 18 - K};
         out->ws_bytes = B * L * 4;
     }
     return WHTMIX_SUCCESS;
 }
 
-// The single-workgroup FUSED plan reaches 2^16 elements (two register sets)
-// in the mixer's forward only: the backward pass and the block run the
-// three-pass plan for such slices.
+// The plan the backward pass and the block take for a forward plan.  The
+// single-workgroup FUSED plan reaches 2^16 elements (two register sets) and
+// the wave-tile plans exist in the mixer's forward only: the backward pass
+// and the block run slices of 2^16 with the three-pass plan, and the
+// wave-tile plans' smaller slices with FUSED (THREE_PASS when forced to
+// ONE_LAUNCH).
 void three_pass_beyond_one_tile(int64_t B, Checked *c)
 {
+    if (c->plan == whtmix::PLAN_WAVE_TILES && c->K <= whtmix::kMaxTile) {
+        c->plan = whtmix::PLAN_FUSED;
+        c->kernels = 1;
+        c->split = whtmix::Split{0, 0, 0};
+        c->ws_bytes = 0;
+        return;
+    }
     if ((c->plan == whtmix::PLAN_FUSED && c->K > whtmix::kMaxTile) ||
-        c->plan == whtmix::PLAN_ONE_LAUNCH) {
+        c->plan == whtmix::PLAN_ONE_LAUNCH || c->plan == whtmix::PLAN_WAVE_TILES) {
         c->plan = whtmix::PLAN_THREE_PASS;
         c->kernels = 3;
         c->split = whtmix::three_pass_split(c->K);
@@ -229,7 +246,8 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->plan = c.plan;
     info->kernels = c.kernels;
     info->log2_slice = c.K;
-    const bool passes = c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_ONE_LAUNCH;
+    const bool passes = c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_ONE_LAUNCH ||
+                        c.plan == whtmix::PLAN_WAVE_TILES;
     info->outer_bits = passes ? c.split.A : 0;
     info->run_bits = passes ? c.split.R : 0;
     info->workspace_bytes = c.ws_bytes;
@@ -253,7 +271,7 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
 
 namespace {
 
-// noalloc: the three-pass workspace is the fixed device scratch instead of
+// noalloc: the three-pass or wave-tile workspace is the fixed device scratch instead of
 // the per-stream workspace, and nothing is allocated.
 int forward_impl(const void *x, int gain_kind, const float *gain, const float *gain_t,
                  const float *gain_c, void *y, int64_t B, int64_t N, int64_t C, int dtype,
@@ -297,7 +315,8 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
     for (int i = 0; i < 4; ++i)
         a.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
 
-    if (c.plan == whtmix::PLAN_THREE_PASS && noalloc) {
+    const bool wave = c.plan == whtmix::PLAN_WAVE_TILES || c.plan == whtmix::PLAN_ONE_LAUNCH;
+    if (noalloc && (c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_WAVE_TILES)) {
         if (c.ws_bytes > whtmix::kNoAllocScratchFloats * 4) {
             g_last_error = "whtmix_forward_noalloc: the call needs " + std::to_string(c.ws_bytes) +
                            " bytes of workspace, more than the fixed " +
@@ -307,15 +326,15 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
         }
         hipError_t e = whtmix::noalloc_scratch(&a.ws);
         if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the scratch");
-        e = whtmix::launch(a);
+        e = wave ? whtmix::launch_wave(a) : whtmix::launch(a);
         if (e != hipSuccess) return hip_fail(e, "kernel launch");
         return WHTMIX_SUCCESS;
     }
-    if (c.plan == whtmix::PLAN_THREE_PASS) {
+    if (c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_WAVE_TILES) {
         std::lock_guard<std::mutex> lock(g_ws_mutex);
         st = get_workspace(stream, c.ws_bytes, &a.ws);
         if (st != WHTMIX_SUCCESS) return st;
-        hipError_t e = whtmix::launch(a);
+        hipError_t e = wave ? whtmix::launch_wave(a) : whtmix::launch(a);
         if (e != hipSuccess) return hip_fail(e, "kernel launch");
         return WHTMIX_SUCCESS;
     }
@@ -327,7 +346,7 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
         if (st != WHTMIX_SUCCESS) return st;
         st = get_counters(stream, &a.counters);
         if (st != WHTMIX_SUCCESS) return st;
-        hipError_t e = whtmix::launch_one_launch(a);
+        hipError_t e = whtmix::launch_wave(a);
         if (e != hipSuccess) return hip_fail(e, "kernel launch");
         return WHTMIX_SUCCESS;
     }

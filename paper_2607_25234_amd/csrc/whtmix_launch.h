@@ -38,10 +38,11 @@ struct LaunchArgs {
 // Enqueues the plan's kernels on a.stream.  Returns the first HIP error.
 hipError_t launch(const LaunchArgs &a);
 
-// Enqueues the ONE_LAUNCH kernel (a.plan == PLAN_ONE_LAUNCH, 12 <= a.K <=
-// 16, a.B <= kOneLaunchMaxBatch, a.nvalid a multiple of 8, a.ws holding
-// a.B * 2^K floats and a.counters a zeroed-or-reset counter block).
-hipError_t launch_one_launch(const LaunchArgs &a);
+// Enqueues the wave-tile kernels (whtmix_wave.hip): a.plan is WAVE_TILES
+// (three launches) or ONE_LAUNCH (one cooperative launch; a.B <=
+// kOneLaunchMaxBatch and a.counters a zeroed-or-reset counter block);
+// 12 <= a.K <= 16, a.nvalid a multiple of 8, a.ws holding a.B * 2^K floats.
+hipError_t launch_wave(const LaunchArgs &a);
 
 // Device address of the fixed scratch array on the current device
 // (kNoAllocScratchFloats floats; whtmix_noalloc.hip).  Looks the address up

@@ -16,7 +16,8 @@ enum PlanKind {
     PLAN_SMALL = 1,
     PLAN_FUSED = 2,
     PLAN_THREE_PASS = 3,
-    PLAN_ONE_LAUNCH = 4
+    PLAN_ONE_LAUNCH = 4,
+    PLAN_WAVE_TILES = 5
 };
 
 constexpr int kMaxLog2Slice = 30;   // N*C <= 2^30
@@ -31,15 +32,19 @@ constexpr int kMaxTile = 15;
 constexpr int kMaxFused = 16;
 constexpr int kFusedPairMinBatch = 48;
 
-// ONE_LAUNCH (whtmix_onelaunch.hip): the three passes of slices of 2^12 ..
-// 2^16 elements in one launch, one-wave 2^9-element tiles, passes ordered by
-// per-slice completion counters.  Its counter block holds 2B + 3 words
-// (per-slice counters of two passes, exits, the call's error word, the
-// sticky error word), so it takes at most kOneLaunchMaxBatch slices.  x and
+// Wave tiles (whtmix_wave.hip): the three passes of slices of 2^12 .. 2^16
+// elements on one-wave 2^9-element tiles, as three launches (WAVE_TILES) or
+// one (ONE_LAUNCH, passes ordered by per-slice completion counters).  x and
 // y move in 16-byte groups, so a slice's element count must be a multiple
-// of 8.
-constexpr int kOneLaunchMinK = 12;
-constexpr int kOneLaunchMaxK = 16;
+// of 8.  ONE_LAUNCH's counter block holds 2B + 3 words (per-slice counters
+// of two passes, exits, the call's error word, the sticky error word), so it
+// takes at most kOneLaunchMaxBatch slices.
+constexpr int kWaveMinK = 12;
+constexpr int kWaveMaxK = 16;
+// AUTO takes WAVE_TILES for slices of 2^16 elements up to 3 slices and of
+// 2^15 up to 16 (measured crossovers against THREE_PASS and FUSED).
+constexpr int kWave16MaxBatch = 3;
+constexpr int kWave15MaxBatch = 16;
 constexpr int kCounterWords = 4096;
 constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
 // Polls of a ONE_LAUNCH wait before it gives up (about a second or two).

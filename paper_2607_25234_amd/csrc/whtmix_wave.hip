@@ -1,15 +1,19 @@
-// ONE_LAUNCH plan: the whole mixer of slices of 2^12 .. 2^16 elements in a
-// single kernel launch (gfx950).
+// Wave tiles: the three passes of slices of 2^12 .. 2^16 elements on
+// one-wave tiles of 2^9 elements whose butterflies stay inside the wave
+// (gfx950).  Two plans run them:
+//   WAVE_TILES  three launches, one tile per workgroup; AUTO takes it for small
+//               batches of 2^15- and 2^16-element slices (image1k: 9.2 -> 7.3 us
+//               per call against THREE_PASS; 2^15 slices 12.8 -> 7.1 us
+//               against one workgroup per slice);
+//   ONE_LAUNCH  all three passes in a single cooperative launch, ordered by
+//               per-slice completion counters (forced only: slower).
 //
 // The mixer of one slice is y = (1/L) H_L (g o H_L x) on the flat index
 // f = n*C + c, L = N_pad*C = 2^K (the channel and token transforms of section
 // III-B, eqs. (2)-(3), are one Walsh-Hadamard transform over the K bits of f;
-// whtmix_plan.h).  It runs as the same three passes as THREE_PASS -- forward
-// over the 9 low bits of f, forward over the HB = K-9 high bits + gain +
-// inverse over them, inverse over the low bits -- but inside one launch, each
-// pass waiting for the previous one through per-slice completion counters
-// instead of a kernel boundary.  At these sizes every kernel of the
-// three-kernel plan is mostly launch and drain latency.
+// whtmix_plan.h), run as three passes: forward over the 9 low bits of f,
+// forward over the HB = K-9 high bits + gain + inverse over them, inverse over
+// the low bits.
 //
 // Tiles.  A workgroup is one wave; a tile is 2^9 elements, 8 per lane.  Every
 // butterfly stays inside the wave, with no LDS:
@@ -39,20 +43,21 @@
 //   3. tile (b, hi): gathered from the runs, inverse over its 9 bits, stored to
 //      y with round to nearest even for bf16.
 //
-// Scheduling.  The grid is launched cooperatively (every workgroup resident).
-// Workgroup w takes tiles w, w + P, w + 2P, ... of each pass in turn.  Counter
-// c0[b] (c1[b]) counts finished pass-1 (pass-2) tiles of slice b; a pass-2
-// (pass-3) tile of slice b starts once it reaches 2^HB.  The smallest
-// unfinished tile never waits on anything unfinished, and its workgroup is
-// resident and working on it, so the schedule always completes.  Each wait is
-// bounded: after `spin_limit` polls it raises the call's error word and every
-// later wait gives up at once, so every wave exits.  The last workgroup to
-// exit (it counts exits) folds the call's error word into a sticky word that
-// the host reads, and returns all counters to zero for the next call.
-//
-// Memory ordering: a finished tile's stores are released to agent scope by
-// the counter increment (all lanes' stores complete first); a wait ends with
-// an agent-scope acquire fence before the tile's loads.
+// ONE_LAUNCH scheduling.  The grid is launched cooperatively (every workgroup
+// resident).  Workgroup w takes tiles w, w + P, w + 2P, ... of each pass in
+// turn.  Counter c0[b] (c1[b]) counts finished pass-1 (pass-2) tiles of slice
+// b; a pass-2 (pass-3) tile of slice b starts once it reaches 2^HB.  The
+// smallest unfinished tile never waits on anything unfinished, and its
+// workgroup is resident and working on it, so the schedule always completes.
+// Each wait is bounded: after `spin_limit` polls it raises the call's error
+// word and every later wait gives up at once, so every wave exits.  The last
+// workgroup to exit (it counts exits) folds the call's error word into a
+// sticky word that the host reads, and returns all counters to zero for the
+// next call.  Memory ordering: a finished tile's stores are released to agent
+// scope by the counter increment (all lanes' stores complete first); a wait
+// ends with an agent-scope acquire fence before the tile's loads.  A
+// cooperative launch alone costs about 20 us, and such a hand-off costs more
+// than a kernel boundary, which is why AUTO never picks it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -63,7 +68,7 @@
 #include "whtmix_tile.h"
 
 namespace whtmix {
-namespace onelaunch {
+namespace wave {
 
 constexpr int TB = 9;    // tile bits
 constexpr int NV = 8;    // values per lane
@@ -350,17 +355,122 @@ __device__ __forceinline__ bool wait_for(const uint32_t *c, uint32_t target, uin
     return ok;
 }
 
-// ---------------------------------------------------------------- the kernel
+// ---------------------------------------------------------------- pass tiles
+// The three passes on one tile each (shared by both plans).  Slice bits K,
+// HB = K - 9 high bits, R = 9 - HB carried run bits.
+template <int K>
+struct Shape {
+    static constexpr int HB = K - TB;
+    static constexpr int R = TB - HB;
+    static_assert(HB >= 3 && R >= 2, "wave tiles cover 2^12 .. 2^16 elements per slice");
+    static constexpr uint32_t TILES = 1u << HB;   // tiles per slice and pass
+};
+
+__device__ __forceinline__ uint32_t tile_valid9(uint32_t nvalid, uint32_t hi)
+{
+    const uint32_t start = hi << TB;
+    return nvalid <= start ? 0u : min(nvalid - start, 1u << TB);
+}
+
+// Pass 1: tile (b, hi) of x, forward over its 9 bits, stored as runs.
+template <int K, typename T>
+__device__ __forceinline__ void pass1_tile(const T *__restrict__ x, float *__restrict__ ws,
+                                           uint32_t b, uint32_t hi, uint32_t nvalid,
+                                           uint32_t lane)
+{
+    using S = Shape<K>;
+    float v[NV];
+    load_x<T>(v, x + (size_t)b * nvalid + (hi << TB), tile_valid9(nvalid, hi), lane);
+    wht9(v, lane);
+    float *dst = ws + ((size_t)b << K) + (hi << S::R);
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+        st4(v, g, dst + run_off<S::R>(group_t<sizeof(T)>(lane, g)));
+}
+
+// Pass 2: tile (b, run) of the workspace, forward over the HB high bits,
+// times the gain (gv, already gathered) and 2^-K, inverse; in place.
+template <int K>
+__device__ __forceinline__ void pass2_tile(float *__restrict__ ws, const float (&gv)[NV],
+                                           uint32_t b, uint32_t run, uint32_t lane)
+{
+    using S = Shape<K>;
+    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
+    float *tile = ws + ((size_t)b << K) + (run << TB);
+    float v[NV];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+        ld4(v, g, tile + group_t<4>(lane, g));
+    wave_bfly<S::R - 2>(v, lane);
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        v[k] *= gv[k] * scale;
+    wave_bfly<S::R - 2>(v, lane);
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+        st4(v, g, tile + group_t<4>(lane, g));
+}
+
+// Pass 3: tile (b, hi) gathered from the runs, inverse over its 9 bits,
+// stored to y (nothing for a tile wholly in the padding).
+template <int K, typename T>
+__device__ __forceinline__ void pass3_tile(const float *__restrict__ ws, T *__restrict__ y,
+                                           uint32_t b, uint32_t hi, uint32_t nvalid,
+                                           uint32_t lane)
+{
+    using S = Shape<K>;
+    const uint32_t valid = tile_valid9(nvalid, hi);
+    if (valid == 0)
+        return;   // uniform per workgroup
+    const float *src = ws + ((size_t)b << K) + (hi << S::R);
+    float v[NV];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+        ld4(v, g, src + run_off<S::R>(group_t<sizeof(T)>(lane, g)));
+    wht9(v, lane);
+    store_y<T>(v, y + (size_t)b * nvalid + (hi << TB), valid, lane);
+}
+
+// ---------------------------------------------------------------- WAVE_TILES
+// Three launches, one tile per workgroup: tile i = b * 2^HB + (hi or run).
+template <int K, typename T>
+__global__ void __launch_bounds__(64)
+wave_pass1_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
+{
+    using S = Shape<K>;
+    pass1_tile<K, T>(x, ws, blockIdx.x >> S::HB, blockIdx.x & (S::TILES - 1u), nvalid,
+                     threadIdx.x);
+}
+
+template <int K, class Gain>
+__global__ void __launch_bounds__(64)
+wave_pass2_kernel(float *__restrict__ ws, Gain gain)
+{
+    using S = Shape<K>;
+    const uint32_t run = blockIdx.x & (S::TILES - 1u);
+    float gv[NV];
+    load_gain<S::R>(gain, gv, run, threadIdx.x);
+    pass2_tile<K>(ws, gv, blockIdx.x >> S::HB, run, threadIdx.x);
+}
+
+template <int K, typename T>
+__global__ void __launch_bounds__(64)
+wave_pass3_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
+{
+    using S = Shape<K>;
+    pass3_tile<K, T>(ws, y, blockIdx.x >> S::HB, blockIdx.x & (S::TILES - 1u), nvalid,
+                     threadIdx.x);
+}
+
+// ---------------------------------------------------------------- ONE_LAUNCH
 template <int K, typename T, class Gain>
 __global__ void __launch_bounds__(64)
 one_launch_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, float *__restrict__ ws,
                   uint32_t *ctr, uint32_t B, uint32_t nvalid, uint32_t spin_limit)
 {
-    constexpr int HB = K - TB;
-    constexpr int R = TB - HB;
-    static_assert(HB >= 3 && R >= 2, "ONE_LAUNCH covers 2^12 .. 2^16 elements per slice");
-    constexpr uint32_t TILES = 1u << HB;                  // tiles per slice and pass
-    constexpr float scale = 1.0f / (float)(1u << K);      // exact power of two
+    using S = Shape<K>;
+    constexpr int HB = S::HB;
+    constexpr uint32_t TILES = S::TILES;
     const uint32_t lane = threadIdx.x;
     const uint32_t P = gridDim.x;
     const uint32_t ntiles = B << HB;
@@ -369,20 +479,12 @@ one_launch_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, float *
     // Gain of this workgroup's first middle tile, read before any waiting.
     float gv[NV];
     if (blockIdx.x < ntiles)
-        load_gain<R>(gain, gv, blockIdx.x & (TILES - 1u), lane);
+        load_gain<S::R>(gain, gv, blockIdx.x & (TILES - 1u), lane);
 
     // Pass 1: forward over the 9 low bits of f, stored as runs.
     for (uint32_t i = blockIdx.x; i < ntiles; i += P) {
-        const uint32_t b = i >> HB, hi = i & (TILES - 1u);
-        const uint32_t start = hi << TB;
-        const uint32_t valid = nvalid <= start ? 0u : min(nvalid - start, 1u << TB);
-        float v[NV];
-        load_x<T>(v, x + (size_t)b * nvalid + start, valid, lane);
-        wht9(v, lane);
-        float *dst = ws + ((size_t)b << K) + (hi << R);
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-            st4(v, g, dst + run_off<R>(group_t<sizeof(T)>(lane, g)));
+        const uint32_t b = i >> HB;
+        pass1_tile<K, T>(x, ws, b, i & (TILES - 1u), nvalid, lane);
         signal_done(cn.c0 + b);
     }
 
@@ -391,41 +493,19 @@ one_launch_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, float *
     for (uint32_t i = blockIdx.x; ok && i < ntiles; i += P) {
         const uint32_t b = i >> HB, run = i & (TILES - 1u);
         if (i != blockIdx.x)
-            load_gain<R>(gain, gv, run, lane);
+            load_gain<S::R>(gain, gv, run, lane);
         ok = wait_for(cn.c0 + b, TILES, cn.call_err, spin_limit);
         if (!ok) break;
-        float *tile = ws + ((size_t)b << K) + (run << TB);
-        float v[NV];
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-            ld4(v, g, tile + group_t<4>(lane, g));
-        wave_bfly<R - 2>(v, lane);
-#pragma unroll
-        for (int k = 0; k < NV; ++k)
-            v[k] *= gv[k] * scale;
-        wave_bfly<R - 2>(v, lane);
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-            st4(v, g, tile + group_t<4>(lane, g));
+        pass2_tile<K>(ws, gv, b, run, lane);
         signal_done(cn.c1 + b);
     }
 
     // Pass 3: inverse over the 9 low bits, stored to y.
     for (uint32_t i = blockIdx.x; ok && i < ntiles; i += P) {
-        const uint32_t b = i >> HB, hi = i & (TILES - 1u);
-        const uint32_t start = hi << TB;
-        const uint32_t valid = nvalid <= start ? 0u : min(nvalid - start, 1u << TB);
+        const uint32_t b = i >> HB;
         ok = wait_for(cn.c1 + b, TILES, cn.call_err, spin_limit);
         if (!ok) break;
-        if (valid == 0)
-            continue;   // wholly padding: nothing to store (uniform per workgroup)
-        const float *src = ws + ((size_t)b << K) + (hi << R);
-        float v[NV];
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-            ld4(v, g, src + run_off<R>(group_t<sizeof(T)>(lane, g)));
-        wht9(v, lane);
-        store_y<T>(v, y + (size_t)b * nvalid + start, valid, lane);
+        pass3_tile<K, T>(ws, y, b, i & (TILES - 1u), nvalid, lane);
     }
 
     // Exit: the last workgroup out resets the counters for the next call.
@@ -453,11 +533,10 @@ inline hipError_t record(hipEvent_t ev, hipStream_t st)
 }
 
 template <int K, typename T, class Gain>
-hipError_t launch_k(const LaunchArgs &a, Gain gain)
+hipError_t launch_one_launch_k(const LaunchArgs &a, Gain gain)
 {
     auto kern = one_launch_kernel<K, T, Gain>;
-    constexpr int HB = K - TB;
-    const uint32_t ntiles = (uint32_t)a.B << HB;
+    const uint32_t ntiles = (uint32_t)a.B << Shape<K>::HB;
     // Every workgroup must be resident: at most the device's resident count.
     static thread_local int cached_dev = -1, cached_max = 0;
     int dev = 0;
@@ -487,6 +566,33 @@ hipError_t launch_k(const LaunchArgs &a, Gain gain)
     return record(a.events[1], a.stream);
 }
 
+template <int K, typename T, class Gain>
+hipError_t launch_wave_tiles_k(const LaunchArgs &a, Gain gain)
+{
+    const dim3 grid((uint32_t)a.B << Shape<K>::HB), block(64);
+    const T *x = static_cast<const T *>(a.x);
+    T *y = static_cast<T *>(a.y);
+    const hipStream_t st = a.stream;
+    hipError_t e = record(a.events[0], st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((wave_pass1_kernel<K, T>), grid, block, 0, st, x, a.ws, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(a.events[1], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((wave_pass2_kernel<K, Gain>), grid, block, 0, st, a.ws, gain);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = record(a.events[2], st)) != hipSuccess) return e;
+    hipLaunchKernelGGL((wave_pass3_kernel<K, T>), grid, block, 0, st, a.ws, y, a.nvalid);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return record(a.events[3], st);
+}
+
+template <int K, typename T, class Gain>
+hipError_t launch_k(const LaunchArgs &a, Gain gain)
+{
+    return a.plan == PLAN_ONE_LAUNCH ? launch_one_launch_k<K, T, Gain>(a, gain)
+                                     : launch_wave_tiles_k<K, T, Gain>(a, gain);
+}
+
 template <typename T, class Gain>
 hipError_t dispatch_k(const LaunchArgs &a, Gain gain)
 {
@@ -510,13 +616,15 @@ hipError_t dispatch_gain(const LaunchArgs &a)
     return dispatch_k<T>(a, tile::FullGain{a.gain});
 }
 
-}  // namespace onelaunch
+}  // namespace wave
 
-hipError_t launch_one_launch(const LaunchArgs &a)
+hipError_t launch_wave(const LaunchArgs &a)
 {
+    if (a.plan != PLAN_ONE_LAUNCH && a.plan != PLAN_WAVE_TILES)
+        return hipErrorInvalidValue;
     if (a.dtype == DTYPE_BF16)
-        return onelaunch::dispatch_gain<__bf16>(a);
-    return onelaunch::dispatch_gain<float>(a);
+        return wave::dispatch_gain<__bf16>(a);
+    return wave::dispatch_gain<float>(a);
 }
 
 }  // namespace whtmix

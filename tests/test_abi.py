@@ -81,6 +81,9 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(plan=4, N=2048, C=64), 1),
     (dict(plan=4, N=4095, C=1), 1),           # ... and N*C a multiple of 8
     (dict(plan=4, B=2047, N=1024, C=64), 1),  # ... and B <= 2046
+    (dict(plan=5, N=32, C=64), 1),            # WAVE_TILES needs 2^12..2^16
+    (dict(plan=5, N=4096, C=32), 1),
+    (dict(plan=5, N=4095, C=1), 1),           # ... and N*C a multiple of 8
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
     assert call(**kwargs) == status
@@ -236,7 +239,8 @@ def test_plan_table():
     assert d["plan"] == "small" and d["kernels"] == 1 and d["workspace_bytes"] == 0
     assert whtmix.plan_describe(3, 32, 32)["plan"] == "small"
     assert whtmix.plan_describe(3, 32, 64)["plan"] == "fused"
-    assert whtmix.plan_describe(3, 256, 128)["plan"] == "fused"
+    assert whtmix.plan_describe(3, 256, 64)["plan"] == "fused"
+    assert whtmix.plan_describe(3, 256, 128)["plan"] == "wave_tiles"   # 2^15, few slices
     d = whtmix.plan_describe(3, 1024, 128, "bf16")
     assert d["plan"] == "three_pass" and d["kernels"] == 3
     assert d["workspace_bytes"] == 3 * 1024 * 128 * 4
@@ -249,6 +253,16 @@ def test_plan_table():
     assert (d["outer_bits"], d["run_bits"]) == (9, 2)
     d = whtmix.plan_describe(2, 64, 64, plan="one_launch")
     assert (d["plan"], d["outer_bits"], d["run_bits"]) == ("one_launch", 9, 6)
+    # small batches of 2^15 and 2^16 slices: three launches of one-wave tiles
+    for B, N, C, plan in [(1, 1024, 64, "wave_tiles"), (3, 1024, 64, "wave_tiles"),
+                          (4, 1024, 64, "three_pass"), (16, 512, 64, "wave_tiles"),
+                          (17, 512, 64, "fused"), (1, 32767, 1, "fused"),
+                          (1, 65535, 1, "three_pass"), (2, 256, 64, "fused")]:
+        assert whtmix.plan_describe(B, N, C)["plan"] == plan, (B, N, C)
+    d = whtmix.plan_describe(1, 1024, 64)
+    assert (d["kernels"], d["workspace_bytes"], d["module_path"], d["module_outer_bits"]) == \
+        (3, 1 << 18, "mfma", 11)
+    assert whtmix.plan_describe(2, 512, 64)["module_outer_bits"] == 0   # the block: FUSED
     d = whtmix.plan_describe(48, 512, 128, "bf16")
     assert (d["plan"], d["kernels"], d["workspace_bytes"]) == ("fused", 1, 0)
     assert (d["module_path"], d["module_outer_bits"]) == ("mfma", 11)
@@ -265,7 +279,9 @@ def test_plan_table():
         d = whtmix.plan_describe(w.B, w.N, w.C, w.dtype)
         K = d["log2_slice"]
         assert 1 << K == w.N * w.C
-        if K >= 16:   # every workload's 2^16 slices come in batches below 48
+        if K == 16:   # image1k: one 2^16 slice
+            assert (d["plan"], d["kernels"], d["outer_bits"], d["run_bits"]) == ("wave_tiles", 3, 9, 2)
+        if K > 16:
             A, R = d["outer_bits"], d["run_bits"]
             assert d["plan"] == "three_pass"
             assert 11 <= A <= 16 and 11 <= K - A + R <= 15 and R <= A

@@ -68,3 +68,15 @@ def test_one_launch_design_bytes_are_the_three_passes():
     assert bench.algorithmic_bytes("one_launch", 1, 1024, 64, 4, 4 * 1024 * 64) == [sum(three)]
     p = bench.percentiles([1.0, 2.0, 3.0])
     assert p["median_ms"] == 2.0 and p["calls"] == 3
+
+
+def test_backward_plan_follows_the_library_rule():
+    def p(plan, K):
+        return {"plan": plan, "log2_slice": K}
+    assert bench.backward_plan(p("wave_tiles", 16)) == "three_pass"
+    assert bench.backward_plan(p("wave_tiles", 15)) == "fused"
+    assert bench.backward_plan(p("one_launch", 13)) == "three_pass"
+    assert bench.backward_plan(p("fused", 16)) == "three_pass"
+    assert bench.backward_plan(p("fused", 14)) == "fused"
+    assert bench.backward_plan(p("three_pass", 23)) == "three_pass"
+    assert bench.kernel_names("wave_tiles") == ["wave_pass1", "wave_middle", "wave_pass3"]

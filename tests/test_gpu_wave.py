@@ -1,14 +1,15 @@
-"""The ONE_LAUNCH plan (csrc/whtmix_onelaunch.hip) against the CPU oracle,
-through the C ABI.
+"""The wave-tile plans (csrc/whtmix_wave.hip) against the CPU oracle, through
+the C ABI.
 
-All three passes of the mixer (section III-B, eqs. (2)-(3)) run in one
-cooperative launch, ordered by per-slice counters.  Checked here: parity at
-every supported slice size, batch counts from 1 to 47 (several tiles per
-workgroup when the batch outgrows the resident grid), padded N, both dtypes,
-both gain forms, in place; back-to-back calls (the kernel returns its
-counters to zero); and the give-up path forced from the host with a poll
-limit of one, after which the stream reports the error once and later calls
-are correct.
+Both run the mixer (section III-B, eqs. (2)-(3)) as three passes on one-wave
+2^9-element tiles whose butterflies stay in the wave: WAVE_TILES as three
+launches, ONE_LAUNCH in one cooperative launch ordered by per-slice counters.
+Checked here: parity at every supported slice size, batch counts from 1 to
+2046 (several tiles per workgroup when a single launch outgrows the resident
+grid), padded N, both dtypes, both gain forms, in place; back-to-back calls
+(the single launch returns its counters to zero); and the give-up path forced
+from the host with a poll limit of one, after which the stream reports the
+error once and later calls are correct.
 """
 import numpy as np
 import pytest
@@ -43,57 +44,66 @@ def status_ok():
     assert st == whtmix.SUCCESS, whtmix.status_string(st)
 
 
+PLANS = ["one_launch", "wave_tiles"]
+
+
+@pytest.mark.parametrize("plan", PLANS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", [(1, 64, 64), (2, 128, 64), (1, 256, 64), (3, 256, 128),
                                    (1, 1024, 64), (2, 512, 128), (16, 1024, 64),
                                    (47, 512, 128), (1, 65536, 1), (1, 8, 8192),
                                    (300, 1024, 64), (2046, 64, 64)],
                          ids=lambda s: "x".join(map(str, s)))
-def test_parity(shape, dtype, dev, orc):
+def test_parity(shape, dtype, plan, dev, orc):
     B, N, C = shape
-    say(f"one_launch B={B} N={N} C={C} {dtype}")
+    say(f"{plan} B={B} N={N} C={C} {dtype}")
     x, g = workloads.draw(B, N, C, dtype, seed=B * 1000 + N + C)
-    y = run_gpu(x, g, dtype, dev, plan="one_launch")
+    y = run_gpu(x, g, dtype, dev, plan=plan)
     status_ok()
-    check("one_launch", y, orc.whtmix(x, g), dtype)
+    check(plan, y, orc.whtmix(x, g), dtype)
 
 
+@pytest.mark.parametrize("plan", PLANS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", [(1, 1000, 64), (2, 9, 512), (3, 200, 128), (1, 33, 128)],
                          ids=lambda s: "x".join(map(str, s)))
-def test_padded_tokens(shape, dtype, dev, orc):
+def test_padded_tokens(shape, dtype, plan, dev, orc):
     """Non-power-of-two N: rows N..N_pad-1 are zeros; only the straddling
     tile is partial, tiles wholly in the padding skip their loads and stores."""
     B, N, C = shape
-    say(f"one_launch padded B={B} N={N} C={C} {dtype}")
+    say(f"{plan} padded B={B} N={N} C={C} {dtype}")
     P = whtmix.padded_tokens(N)
     x, _ = workloads.draw(B, N, C, dtype, seed=N)
     g = np.random.default_rng(N).uniform(0.5, 1.5, (P, C)).astype(np.float32)
-    y = run_gpu(x, g, dtype, dev, plan="one_launch")
+    y = run_gpu(x, g, dtype, dev, plan=plan)
     status_ok()
-    check("one_launch padded", y, orc.whtmix(x, g), dtype)
+    check(f"{plan} padded", y, orc.whtmix(x, g), dtype)
 
 
+@pytest.mark.parametrize("plan", PLANS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_separable(dtype, dev, orc):
+def test_separable(dtype, plan, dev, orc):
     B, N, C = 2, 1024, 64
     x, _ = workloads.draw(B, N, C, dtype, seed=5)
     gt, gc = workloads.draw_log_gains(N, C, seed=6)
-    y = run_gpu_separable(x, gt, gc, dtype, dev, plan="one_launch")
+    y = run_gpu_separable(x, gt, gc, dtype, dev, plan=plan)
     status_ok()
-    check("one_launch separable", y, orc.whtmix_separable(x, gt, gc), dtype)
+    check(f"{plan} separable", y, orc.whtmix_separable(x, gt, gc), dtype)
 
 
-def test_image1k_workload(dev, orc):
-    """image1k_f32 (B=1, N=1024, C=64) as one launch."""
+@pytest.mark.parametrize("plan", PLANS + ["auto"])
+def test_image1k_workload(plan, dev, orc):
+    """image1k_f32 (B=1, N=1024, C=64); AUTO takes WAVE_TILES for it."""
     w = workloads.WORKLOADS["image1k_f32"]
+    assert whtmix.plan_describe(w.B, w.N, w.C, w.dtype)["plan"] == "wave_tiles"
     x, g = workloads.inputs(w)
-    y = run_gpu(x, g, w.dtype, dev, plan="one_launch")
+    y = run_gpu(x, g, w.dtype, dev, plan=plan)
     status_ok()
-    check("image1k_f32", y, orc.whtmix(x, g), w.dtype)
+    check(f"image1k_f32 {plan}", y, orc.whtmix(x, g), w.dtype)
 
 
-def test_back_to_back_and_in_place(dev, orc):
+@pytest.mark.parametrize("plan", PLANS)
+def test_back_to_back_and_in_place(plan, dev, orc):
     """Consecutive calls on one stream reuse the counter block (each kernel
     returns it to zero); in place (y == x) reads every x before any y store
     of the same slice."""
@@ -104,7 +114,7 @@ def test_back_to_back_and_in_place(dev, orc):
         x, g = workloads.draw(B, N, C, "f32", seed=40 + i)
         xd = to_device(x, "f32", dev)
         gd = torch.from_numpy(g).to(dev)
-        whtmix.forward(xd, gd, out=xd, plan="one_launch")
+        whtmix.forward(xd, gd, out=xd, plan=plan)
         outs.append(xd)
         refs.append(orc.whtmix(x, g))
     torch.cuda.synchronize()

@@ -1,4 +1,4 @@
-"""CPU model of the ONE_LAUNCH kernel (csrc/whtmix_onelaunch.hip), no GPU.
+"""CPU model of the wave-tile kernels (csrc/whtmix_wave.hip), no GPU.
 
 Re-states in numpy:
 * the cross-lane primitives as the gfx9/gfx950 ISA defines them -- DPP
@@ -8,9 +8,10 @@ Re-states in numpy:
   swap_k2, wave_bfly, wht9) on a 64-lane x 8-register file;
 * the layouts V4 / V8, the workspace run map and the gain index of the three
   passes;
-* the scheduler: workgroup w takes tiles w, w + P, ... of each pass; per-slice
-  counters order the passes; bounded waits; the last workgroup out resets the
-  counters.
+* the single-launch scheduler: workgroup w takes tiles w, w + P, ... of each
+  pass; per-slice counters order the passes; bounded waits; the last
+  workgroup out resets the counters (the three-launch form runs the same
+  tiles, one per workgroup, with kernel boundaries between the passes).
 
 and checks that the butterflies transform exactly the bits they claim, that
 every load and store stays inside its buffer and touches each element once,

@@ -35,11 +35,12 @@ def _run(entry, x, g, dtype, dev):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_noalloc_matches_forward_twice(dtype):
-    """The first call fills most of the scratch (2^23 floats), the second,
-    smaller one reuses it; a FUSED-plan call needs no scratch at all."""
+    """The first call fills the scratch (2^23 floats), the second, smaller one
+    reuses it, the third runs the wave-tile plan in it; a FUSED-plan call
+    needs no scratch at all."""
     dev = device()
     orc = oracle_mod.Oracle()
-    for i, (B, N, C) in enumerate([(4, 16384, 128), (3, 4096, 64), (2, 256, 64)]):
+    for i, (B, N, C) in enumerate([(4, 16384, 128), (3, 4096, 64), (1, 1024, 64), (2, 256, 64)]):
         say(f"noalloc call {i}: B={B} N={N} C={C} {dtype} "
             f"plan={whtmix.plan_describe(B, N, C, dtype)['plan']}")
         x, g = workloads.draw(B, N, C, dtype, seed=900 + i)
