@@ -433,13 +433,23 @@ __device__ __forceinline__ void pass3_tile(const float *__restrict__ ws, T *__re
 
 // ---------------------------------------------------------------- WAVE_TILES
 // Three launches, one tile per workgroup: tile i = b * 2^HB + (hi or run).
+// The runs are 2^R floats (16 bytes at R = 2), so the 2^(5-R) neighbouring
+// tiles whose runs share a 128-byte line of the workspace (passes 1 and 3) or
+// of the gain (pass 2) are numbered onto one XCD (tile::outer_block): each
+// line is then written back or fetched once, by one L2, not once per XCD.
+template <int K>
+__device__ __forceinline__ uint32_t wave_tile()
+{
+    return tile::outer_block<Shape<K>::R>(blockIdx.x, gridDim.x);
+}
+
 template <int K, typename T>
 __global__ void __launch_bounds__(64)
 wave_pass1_kernel(const T *__restrict__ x, float *__restrict__ ws, uint32_t nvalid)
 {
     using S = Shape<K>;
-    pass1_tile<K, T>(x, ws, blockIdx.x >> S::HB, blockIdx.x & (S::TILES - 1u), nvalid,
-                     threadIdx.x);
+    const uint32_t i = wave_tile<K>();
+    pass1_tile<K, T>(x, ws, i >> S::HB, i & (S::TILES - 1u), nvalid, threadIdx.x);
 }
 
 template <int K, class Gain>
@@ -447,10 +457,11 @@ __global__ void __launch_bounds__(64)
 wave_pass2_kernel(float *__restrict__ ws, Gain gain)
 {
     using S = Shape<K>;
-    const uint32_t run = blockIdx.x & (S::TILES - 1u);
+    const uint32_t i = wave_tile<K>();
+    const uint32_t run = i & (S::TILES - 1u);
     float gv[NV];
     load_gain<S::R>(gain, gv, run, threadIdx.x);
-    pass2_tile<K>(ws, gv, blockIdx.x >> S::HB, run, threadIdx.x);
+    pass2_tile<K>(ws, gv, i >> S::HB, run, threadIdx.x);
 }
 
 template <int K, typename T>
@@ -458,8 +469,8 @@ __global__ void __launch_bounds__(64)
 wave_pass3_kernel(const float *__restrict__ ws, T *__restrict__ y, uint32_t nvalid)
 {
     using S = Shape<K>;
-    pass3_tile<K, T>(ws, y, blockIdx.x >> S::HB, blockIdx.x & (S::TILES - 1u), nvalid,
-                     threadIdx.x);
+    const uint32_t i = wave_tile<K>();
+    pass3_tile<K, T>(ws, y, i >> S::HB, i & (S::TILES - 1u), nvalid, threadIdx.x);
 }
 
 // ---------------------------------------------------------------- ONE_LAUNCH

@@ -256,6 +256,44 @@ def run_pipeline(x, g, K, B, nvalid, dtype_layout):
     return y
 
 
+def wave_tile(blk, nblk, R):
+    """The wave-tile kernels' block renumbering (tile::outer_block)."""
+    if R >= 5:
+        return blk
+    g = 1 << (5 - R)
+    if nblk % (8 * g):
+        return blk
+    return (blk & ~(8 * g - 1)) | ((blk & 7) * g) | ((blk >> 3) & (g - 1))
+
+
+@pytest.mark.parametrize("K", [12, 13, 14, 15, 16])
+@pytest.mark.parametrize("B", [1, 2, 3, 16])
+@pytest.mark.parametrize("layout", ["V4", "V8"])
+def test_shared_lines_stay_on_one_xcd(K, B, layout):
+    """Blocks are dealt round-robin over the 8 XCDs (block i on XCD i mod 8).
+    After the renumbering every 128-byte line of the workspace that passes 1
+    and 3 write or read, and every line of the gain that pass 2 reads, is
+    touched by blocks of one XCD only; the renumbering is a permutation."""
+    HB = K - TB
+    R = TB - HB
+    nblk = B << HB
+    wave_tile_map = [wave_tile(i, nblk, R) for i in range(nblk)]
+    assert sorted(wave_tile_map) == list(range(nblk))
+    T_io = t_index(layout)
+    T4 = t_index("V4")
+    ws_line_xcd, g_line_xcd = {}, {}
+    for blk, i in enumerate(wave_tile_map):
+        b, t = i >> HB, i & ((1 << HB) - 1)
+        xcd = blk % 8
+        off = (b << K) + (t << R) + run_off(T_io, R)           # passes 1 and 3 (t = hi)
+        for line in np.unique(off >> 5):
+            assert ws_line_xcd.setdefault(int(line), xcd) == xcd
+        f = ((T4 >> R) << TB) | (t << R) | (T4 & ((1 << R) - 1))   # pass 2 (t = run)
+        for line in np.unique(f >> 5):
+            assert g_line_xcd.setdefault((b, int(line)), xcd) == xcd
+    assert len(ws_line_xcd) == (B << K) >> 5
+
+
 @pytest.mark.parametrize("K,B,N,C,layout", [
     (12, 1, 64, 64, "V4"), (13, 2, 128, 64, "V8"), (14, 1, 256, 64, "V4"),
     (15, 3, 256, 128, "V8"), (16, 1, 1024, 64, "V4"), (16, 2, 1024, 64, "V8"),
