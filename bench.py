@@ -440,37 +440,41 @@ def main() -> int:
     else:
         nk, names = plan["kernels"], kernel_names(plan["plan"])
 
+    # device addresses resolved once per set, as a serving loop holds them
+    ptrs = [{k: v.data_ptr() for k, v in t.items()} for t in sets]
+    p_in, p_out = w_in.data_ptr(), w_out.data_ptr()
+
     def step(i, events=None):
-        t = sets[i % nsets]
+        t = ptrs[i % nsets]
         B, N, C = w.B, w.N, w.C
         if op == "forward":
-            st = whtmix.forward_raw(t["x"].data_ptr(), t["g"].data_ptr(), t["y"].data_ptr(),
+            st = whtmix.forward_raw(t["x"], t["g"], t["y"],
                                     B, N, C, dt_code, sptr, args.plan, events)
         elif op == "separable":
-            st = whtmix.forward_separable_raw(t["x"].data_ptr(), t["gt"].data_ptr(),
-                                              t["gc"].data_ptr(), t["y"].data_ptr(), B, N, C,
+            st = whtmix.forward_separable_raw(t["x"], t["gt"],
+                                              t["gc"], t["y"], B, N, C,
                                               dt_code, sptr, args.plan, events)
         elif op == "backward":
-            st = whtmix.backward_raw(t["x"].data_ptr(), t["dy"].data_ptr(), t["g"].data_ptr(),
-                                     t["y"].data_ptr(), t["dg"].data_ptr(), B, N, C, dt_code,
+            st = whtmix.backward_raw(t["x"], t["dy"], t["g"],
+                                     t["y"], t["dg"], B, N, C, dt_code,
                                      sptr, args.plan, events)
         elif op == "module":
-            st = whtmix.module_forward_raw(t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(),
-                                           w_out.data_ptr(), t["y"].data_ptr(), B, N, C,
+            st = whtmix.module_forward_raw(t["x"], p_in, t["g"],
+                                           p_out, t["y"], B, N, C,
                                            dt_code, sptr, args.plan, events)
         elif op == "module_backward":
             st = whtmix.module_backward_raw(
-                t["x"].data_ptr(), w_in.data_ptr(), t["g"].data_ptr(), w_out.data_ptr(),
-                t["dy"].data_ptr(), t["y"].data_ptr(), t["dwi"].data_ptr(), t["dwo"].data_ptr(),
-                t["dg"].data_ptr(), B, N, C, dt_code, sptr, args.plan, events)
+                t["x"], p_in, t["g"], p_out,
+                t["dy"], t["y"], t["dwi"], t["dwo"],
+                t["dg"], B, N, C, dt_code, sptr, args.plan, events)
         elif op == "module_separable":
             st = whtmix.module_forward_separable_raw(
-                t["x"].data_ptr(), w_in.data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
-                w_out.data_ptr(), t["y"].data_ptr(), B, N, C, dt_code, sptr, args.plan, events)
+                t["x"], p_in, t["gt"], t["gc"],
+                p_out, t["y"], B, N, C, dt_code, sptr, args.plan, events)
         else:
             st = whtmix.backward_separable_raw(
-                t["x"].data_ptr(), t["dy"].data_ptr(), t["gt"].data_ptr(), t["gc"].data_ptr(),
-                t["y"].data_ptr(), t["dgt"].data_ptr(), t["dgc"].data_ptr(), B, N, C, dt_code,
+                t["x"], t["dy"], t["gt"], t["gc"],
+                t["y"], t["dgt"], t["dgc"], B, N, C, dt_code,
                 sptr, args.plan, events)
         if st != whtmix.SUCCESS:
             raise whtmix.WhtmixError(st, f"whtmix {op}")

@@ -147,6 +147,15 @@ def _options(plan: str | int = "auto", events=None, spin_limit: int = 0) -> Opti
     return o
 
 
+def _opt_arg(plan: str | int = "auto", events=None, spin_limit: int = 0):
+    """The options argument of an entry point: NULL when every option is
+    its default (the library then takes AUTO, no events, the default spin
+    limit), which saves building the structure on each call."""
+    if events is None and not spin_limit and (plan == "auto" or plan == 0):
+        return None
+    return ctypes.byref(_options(plan, events, spin_limit))
+
+
 def stream_status(stream: int | None = None) -> int:
     """whtmix_stream_status: synchronise the stream and return (and clear)
     the error word of its single-launch calls (SUCCESS or
@@ -179,9 +188,8 @@ def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
                 dtype: int, stream: int, plan: str | int = "auto", events=None,
                 spin_limit: int = 0) -> int:
     """Direct call of whtmix_forward_ex with integer pointers; returns the status."""
-    opt = _options(plan, events, spin_limit)
     return lib().whtmix_forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream,
-                                   ctypes.byref(opt))
+                                   _opt_arg(plan, events, spin_limit))
 
 
 def forward_noalloc_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
@@ -201,9 +209,8 @@ def forward_separable_raw(x_ptr: int, gt_ptr: int, gc_ptr: int, y_ptr: int, B: i
                           C: int, dtype: int, stream: int, plan: str | int = "auto",
                           events=None) -> int:
     """Direct call of whtmix_forward_separable; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_forward_separable(x_ptr, gt_ptr, gc_ptr, y_ptr, B, N, C, dtype, stream,
-                                          ctypes.byref(opt))
+                                          _opt_arg(plan, events))
 
 
 def _check(x, out):
@@ -286,9 +293,8 @@ def module_forward_raw(x_ptr: int, w_in_ptr: int, gain_ptr: int, w_out_ptr: int,
                        B: int, N: int, C: int, dtype: int, stream: int,
                        plan: str | int = "auto", events=None) -> int:
     """Direct call of whtmix_module_forward; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_module_forward(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, y_ptr, B, N, C,
-                                       dtype, stream, ctypes.byref(opt))
+                                       dtype, stream, _opt_arg(plan, events))
 
 
 def module_forward_separable_raw(x_ptr: int, w_in_ptr: int, gt_ptr: int, gc_ptr: int,
@@ -296,10 +302,9 @@ def module_forward_separable_raw(x_ptr: int, w_in_ptr: int, gt_ptr: int, gc_ptr:
                                  dtype: int, stream: int, plan: str | int = "auto",
                                  events=None) -> int:
     """Direct call of whtmix_module_forward_separable; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_module_forward_separable(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr,
                                                  y_ptr, B, N, C, dtype, stream,
-                                                 ctypes.byref(opt))
+                                                 _opt_arg(plan, events))
 
 
 def _weight(w, C, x, what):
@@ -357,17 +362,15 @@ def module_forward_separable(x, w_in, log_gain_tokens, log_gain_channels, w_out,
 def backward_raw(x_ptr, dy_ptr, gain_ptr, dx_ptr, dgain_ptr, B, N, C, dtype, stream,
                  plan: str | int = "auto", events=None) -> int:
     """Direct call of whtmix_backward (0 for a skipped output); returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_backward(x_ptr, dy_ptr, gain_ptr, dx_ptr, dgain_ptr, B, N, C, dtype,
-                                 stream, ctypes.byref(opt))
+                                 stream, _opt_arg(plan, events))
 
 
 def backward_separable_raw(x_ptr, dy_ptr, gt_ptr, gc_ptr, dx_ptr, dgt_ptr, dgc_ptr, B, N, C,
                            dtype, stream, plan: str | int = "auto", events=None) -> int:
     """Direct call of whtmix_backward_separable; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_backward_separable(x_ptr, dy_ptr, gt_ptr, gc_ptr, dx_ptr, dgt_ptr,
-                                           dgc_ptr, B, N, C, dtype, stream, ctypes.byref(opt))
+                                           dgc_ptr, B, N, C, dtype, stream, _opt_arg(plan, events))
 
 
 def _same(a, x, what):
@@ -440,21 +443,19 @@ def module_backward_raw(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, dy_ptr, dx_ptr, dw
                         dw_out_ptr, dgain_ptr, B, N, C, dtype, stream,
                         plan: str | int = "auto", events=None) -> int:
     """Direct call of whtmix_module_backward; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_module_backward(x_ptr, w_in_ptr, gain_ptr, w_out_ptr, dy_ptr, dx_ptr,
                                         dw_in_ptr, dw_out_ptr, dgain_ptr, B, N, C, dtype, stream,
-                                        ctypes.byref(opt))
+                                        _opt_arg(plan, events))
 
 
 def module_backward_separable_raw(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr, dy_ptr, dx_ptr,
                                   dw_in_ptr, dw_out_ptr, dgt_ptr, dgc_ptr, B, N, C, dtype,
                                   stream, plan: str | int = "auto", events=None) -> int:
     """Direct call of whtmix_module_backward_separable; returns the status."""
-    opt = _options(plan, events)
     return lib().whtmix_module_backward_separable(x_ptr, w_in_ptr, gt_ptr, gc_ptr, w_out_ptr,
                                                   dy_ptr, dx_ptr, dw_in_ptr, dw_out_ptr, dgt_ptr,
                                                   dgc_ptr, B, N, C, dtype, stream,
-                                                  ctypes.byref(opt))
+                                                  _opt_arg(plan, events))
 
 
 def module_backward(x, w_in, gain, w_out, dy, want_dgain: bool = True, dx=None,

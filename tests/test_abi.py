@@ -234,6 +234,20 @@ def test_empty_batch_is_a_no_op():
     assert whtmix.forward_raw(0, 0, 0, 0, 1 << 20, 1 << 7, 1, 0) == 0
 
 
+def test_default_options_pass_null():
+    """With every option at its default the binding passes NULL options
+    (documented as the defaults); any other option builds the structure."""
+    assert whtmix._opt_arg() is None
+    assert whtmix._opt_arg("auto", None, 0) is None and whtmix._opt_arg(0) is None
+    assert whtmix._opt_arg("three_pass") is not None
+    assert whtmix._opt_arg("auto", spin_limit=5) is not None
+    assert whtmix._opt_arg("auto", events=[None] * 4) is not None
+    # the NULL path is checked like the structure path, before any HIP call
+    assert whtmix.forward_raw(0, 0, 0, 1, 64, 64, 0, 0) == 1
+    assert whtmix.forward_raw(0, 0, 0, 1, 64, 64, 0, 0, "fused") == 1
+    assert call(C=12) == 2 and call(C=12, plan=3) == 2
+
+
 def test_plan_table():
     d = whtmix.plan_describe(1, 1, 1)
     assert d["plan"] == "small" and d["kernels"] == 1 and d["workspace_bytes"] == 0
