@@ -50,6 +50,22 @@ constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
 // Polls of a ONE_LAUNCH wait before it gives up (about a second or two).
 constexpr unsigned kDefaultSpinLimit = 1u << 21;
 
+// Forward middle pass: slices per workgroup.  A workgroup takes one run in nb
+// slices in turn and reads the run's gain once.  nb doubles while it divides
+// B and the grid keeps at least kMiddleMinWaves waves (16 per CU, a full
+// round of the 2^14-element tiles); stereo64k (4 slices of 2^23) gets 4:
+// its middle pass 51.2 -> 48.9 us.  run_bits = A - R, thread_bits = the
+// log2 of the workgroup size.
+constexpr long long kMiddleMinWaves = 4096;
+constexpr long long middle_slices_per_group(long long B, int run_bits, int thread_bits)
+{
+    const long long waves = thread_bits > 6 ? 1ll << (thread_bits - 6) : 1ll;
+    long long nb = 1;
+    while (B % (2 * nb) == 0 && (B / (2 * nb)) * (1ll << run_bits) * waves >= kMiddleMinWaves)
+        nb *= 2;
+    return nb;
+}
+
 // whtmix_forward_noalloc: the fixed device scratch (32 MiB of floats) that
 // holds its three-pass workspace, B * N_pad * C floats at most.
 constexpr long long kNoAllocScratchFloats = 1ll << 23;

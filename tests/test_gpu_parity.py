@@ -218,6 +218,34 @@ def test_deterministic_and_batch_independent(dev):
         assert np.array_equal(yb[0], y1[b])
 
 
+@pytest.mark.parametrize("shape,dtype,nb", [
+    ((2, 65536, 128), "bf16", 2), ((8, 65536, 128), "bf16", 8), ((32, 16384, 64), "f32", 4),
+], ids=["2x2^23", "8x2^23", "32x2^20"])
+def test_middle_slice_groups(shape, dtype, nb, dev, orc):
+    """Batches whose middle pass runs nb slices per workgroup (the run's gain
+    read once for the group): every sampled slice is bit-identical to a
+    one-slice call (which takes nb = 1) and matches the oracle."""
+    import torch
+    from tests.test_tile_model import VB, middle_slices_per_group, three_pass_split
+    B, N, C = shape
+    K = (N * C).bit_length() - 1
+    A, HB, R = three_pass_split(K)
+    assert middle_slices_per_group(B, A - R, HB + R - VB) == nb
+    assert whtmix.plan_describe(B, N, C, dtype)["plan"] == "three_pass"
+    say(f"slice groups: B={B} N={N} C={C} {dtype} nb={nb}")
+    x, g = workloads.draw(B, N, C, dtype, seed=41)
+    xd = to_device(x, dtype, dev)
+    gd = torch.from_numpy(g).to(dev)
+    y = whtmix.forward(xd, gd)
+    torch.cuda.synchronize(dev)
+    for b in (0, nb - 1, B - 1):
+        yb = whtmix.forward(xd[b:b + 1].contiguous(), gd)
+        assert torch.equal(yb[0], y[b]), b
+    yh = to_host(y)
+    sample = [0, B - 1]
+    check(f"slice groups {shape}", yh[sample], orc.whtmix(x[sample], g), dtype)
+
+
 def test_bf16_round_to_nearest_even(dev):
     """N = C = 1 reduces the mixer to y = g x: products placed exactly on bf16
     halfway points must round to the even neighbour."""

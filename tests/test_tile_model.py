@@ -254,10 +254,23 @@ def model_outer_inv_block(ws_slice, nvalid, b, hi, split, acc=None, base=0, vw=0
     return offs, out
 
 
-def simulate_three_pass(x, g, K, split, vw=0):
+KMIDDLE_MIN_WAVES = 4096
+
+
+def middle_slices_per_group(B, run_bits, thread_bits):
+    """Slices per forward middle workgroup (the library's rule)."""
+    waves = 1 << (thread_bits - 6) if thread_bits > 6 else 1
+    nb = 1
+    while B % (2 * nb) == 0 and (B // (2 * nb)) * (1 << run_bits) * waves >= KMIDDLE_MIN_WAVES:
+        nb *= 2
+    return nb
+
+
+def simulate_three_pass(x, g, K, split, vw=0, nb=None):
     """Model of outer_fwd_kernel, middle_kernel, outer_inv_kernel.  x holds
     N <= 2^K / C real tokens per slice (zero padding of the token axis).
-    vw: the outer passes' vector-first layout (0: per-element accesses)."""
+    vw: the outer passes' vector-first layout (0: per-element accesses).
+    nb: slices per middle workgroup (default: the library's rule)."""
     B = x.shape[0]
     L = 1 << K
     nvalid = x.shape[1] * x.shape[2]
@@ -275,23 +288,32 @@ def simulate_three_pass(x, g, K, split, vw=0):
         offs, vals = model_outer_fwd_block(xs, nvalid, b, hi, split, acc_x, vw)
         for o, v in zip(offs, vals):
             ws[acc["ws_w1"].at(b * L + o)] = v
-    # middle: logical tile = run * B + b, XCD renumbering of blocks
+    # middle: the run's gain read once, then the group's nb slices in turn;
+    # nb = 1: logical tile = run * B + b with the XCD renumbering of blocks,
+    # nb > 1: block = group * 2^(A-R) + run
     M = HB + R
-    nblk = B << (A - R)
+    if nb is None:
+        nb = middle_slices_per_group(B, A - R, M - VB)
+    assert B % nb == 0
+    nblk = (B // nb) << (A - R)
     for blk in range(nblk):
-        logical = (blk & 7) * (nblk >> 3) + (blk >> 3) if nblk % 8 == 0 else blk
-        run, b = logical // B, logical % B
+        if nb == 1:
+            logical = (blk & 7) * (nblk >> 3) + (blk >> 3) if nblk % 8 == 0 else blk
+            run, b0 = logical // B, logical % B
+        else:
+            run, b0 = blk & ((1 << (A - R)) - 1), (blk >> (A - R)) * nb
         T = Tile(M, R)
-        base = b * (1 << (A + HB)) + (run << M)
-        v = ws[acc["ws_r2"].at(base + T.idx(T.g.TOP))].copy()
-        butterflies(v, T.g.JT, VB)
-        v = T.forward_groups(v, T.g.TOP)
-        goff = acc_g.at((run << R) + gain_map(T.idx(T.g.SL), A, R))
-        v = v * (gf[goff] * (1.0 / L))
-        if T.g.NBOT > 0:
-            v = T.inverse_groups(v)
-        butterflies(v, T.g.JT, VB)
-        ws[acc["ws_w2"].at(base + T.idx(T.g.TOP))] = v
+        gv = gf[acc_g.at((run << R) + gain_map(T.idx(T.g.SL), A, R))]
+        for b in range(b0, b0 + nb):
+            base = b * (1 << (A + HB)) + (run << M)
+            v = ws[acc["ws_r2"].at(base + T.idx(T.g.TOP))].copy()
+            butterflies(v, T.g.JT, VB)
+            v = T.forward_groups(v, T.g.TOP)
+            v = v * (gv * (1.0 / L))
+            if T.g.NBOT > 0:
+                v = T.inverse_groups(v)
+            butterflies(v, T.g.JT, VB)
+            ws[acc["ws_w2"].at(base + T.idx(T.g.TOP))] = v
     # outer inverse
     for blk in range(B << HB):
         b, hi = blk >> HB, blk & ((1 << HB) - 1)
@@ -304,7 +326,7 @@ def simulate_three_pass(x, g, K, split, vw=0):
         assert np.all(a.count == 1), f"{k}: elements not touched exactly once"
     assert np.all(acc_x.count == 1) and np.all(acc_y.count == 1)
     assert np.all(acc_r3.count <= 1)
-    assert np.all(acc_g.count == B), "each gain element read once per slice"
+    assert np.all(acc_g.count == B // nb), "each gain element read once per slice group"
     return y.reshape(x.shape)
 
 
@@ -412,6 +434,38 @@ def test_three_pass_schedule(K, orc):
         y = simulate_three_pass(x, g, K, three_pass_split(K))
         ref = orc.whtmix(x, g)
         assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref)), (K, B)
+
+
+@pytest.mark.parametrize("nb", [2, 4, 8])
+def test_middle_slice_groups(nb, orc):
+    """The middle pass over groups of nb slices gives the one-slice result,
+    with each gain element read once per group."""
+    rng = np.random.default_rng(7 + nb)
+    K, B = 17, 8
+    N, C = 1 << 11, 64
+    x = rng.standard_normal((B, N, C))
+    g = rng.uniform(0.5, 1.5, (N, C))
+    y = simulate_three_pass(x, g, K, three_pass_split(K), nb=nb)
+    y1 = simulate_three_pass(x, g, K, three_pass_split(K), nb=1)
+    assert np.array_equal(y, y1)
+    ref = orc.whtmix(x, g)
+    assert np.max(np.abs(y - ref)) < 1e-11 * np.max(np.abs(ref))
+
+
+def test_middle_slices_per_group_rule():
+    """Groups only where the grid keeps >= 4096 waves: the 2^23-element
+    slices of the four-slice stereo workload get 4; the other workloads 1."""
+    def nb(B, K):
+        A, HB, R = three_pass_split(K)
+        return middle_slices_per_group(B, A - R, HB + R - VB)
+    assert nb(4, 23) == 4 and nb(2, 23) == 2 and nb(8, 23) == 8 and nb(16, 23) == 16
+    assert nb(1, 23) == 1 and nb(3, 23) == 1 and nb(6, 23) == 2
+    assert nb(2, 21) == 1 and nb(32, 18) == 1 and nb(1, 26) == 1
+    assert nb(32, 20) == 4 and nb(4, 26) == 4
+    for B in range(1, 70):
+        for K in range(12, 31):
+            n = nb(B, K)
+            assert B % n == 0 and n & (n - 1) == 0
 
 
 @pytest.mark.parametrize("K", list(range(12, 31)))
@@ -734,6 +788,24 @@ def test_middle_renumbering_is_a_permutation():
     for nblk in (8, 16, 24, 4096, 3 * 8):
         seen = sorted((blk & 7) * (nblk >> 3) + (blk >> 3) for blk in range(nblk))
         assert seen == list(range(nblk))
+
+
+def test_middle_groups_share_a_gain_on_one_xcd():
+    """Blocks are dealt round-robin over the 8 XCDs.  With slice groups the
+    middle blocks of one run (one per group) are 2^(A-R) apart, a multiple
+    of 8 for every automatic split, so they read the run's gain through one
+    L2; with one slice per block the renumbering puts a run's B blocks on
+    one XCD when B divides the per-XCD share."""
+    for K in range(16, 31):
+        A, HB, R = three_pass_split(K)
+        assert (1 << (A - R)) % 8 == 0, K
+        for B in (1, 2, 4, 32):
+            nblk = B << (A - R)
+            xcd = {}
+            for blk in range(nblk):
+                logical = (blk & 7) * (nblk >> 3) + (blk >> 3)
+                xcd.setdefault(logical // B, set()).add(blk % 8)
+            assert all(len(v) == 1 for v in xcd.values()), (K, B)
 
 
 def outer_block(blk, nblk, R):
