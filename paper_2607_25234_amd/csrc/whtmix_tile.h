@@ -775,8 +775,8 @@ __device__ __forceinline__ void outer_fwd_tile2(float *lds, const T *__restrict_
         butterflies<0, VB>(v0);
         butterflies<0, VB>(v1);
         vforward_groups<M, VWID, 0>(lds, v0, tau);
+        store_layout<VG::SL, Run, float>(v0, r, tau);   // in flight through set 1's exchanges
         vforward_groups<M, VWID, 0, true>(lds, v1, tau);
-        store_layout<VG::SL, Run, float>(v0, r, tau);
         store_layout<VG::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
     } else {
         using G = Groups<M, 0>;
@@ -786,8 +786,8 @@ __device__ __forceinline__ void outer_fwd_tile2(float *lds, const T *__restrict_
         butterflies<0, VB>(v0);
         butterflies<0, VB>(v1);
         forward_groups<M, 0, 0, G::TOP>(lds, v0, tau);
-        forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
         store_layout<G::SL, Run, float>(v0, r, tau);
+        forward_groups<M, 0, 0, G::TOP, true>(lds, v1, tau);
         store_layout<G::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
     }
 }
