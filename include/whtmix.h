@@ -92,7 +92,8 @@ typedef enum whtmix_status {
  * WAVE_TILES runs the same three passes on one-wave tiles of 2^9 elements
  * whose butterflies stay inside the wave (DPP and lane-swap exchanges, no
  * LDS): three launches of 2^(K-9) workgroups per slice; 2^12 <= L <= 2^16
- * and N*C a multiple of 8 (AUTO falls back to the plans above otherwise).
+ * and N*C a multiple of 8 (AUTO falls back to the plans above otherwise);
+ * forced, B*L <= 2^35 besides (WHTMIX_ERROR_TOO_LARGE beyond).
  * ONE_LAUNCH (never chosen by AUTO) runs WAVE_TILES's three passes in a
  * single cooperative launch, ordered by per-slice counters in a small
  * per-stream block; B <= 2046 besides.  On MI355X it is slower than the plans

@@ -100,6 +100,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         break;
     case whtmix::PLAN_WAVE_TILES:
         if (!wave_ok) return WHTMIX_ERROR_INVALID_VALUE;
+        // one 64-thread workgroup per 2^9 elements: B*L/8 work-items
+        if (B > (int64_t(1) << 35) / L) return WHTMIX_ERROR_TOO_LARGE;
         break;
     case whtmix::PLAN_ONE_LAUNCH:
         if (!wave_ok || B > whtmix::kOneLaunchMaxBatch) return WHTMIX_ERROR_INVALID_VALUE;

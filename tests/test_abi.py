@@ -84,6 +84,7 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(plan=5, N=32, C=64), 1),            # WAVE_TILES needs 2^12..2^16
     (dict(plan=5, N=4096, C=32), 1),
     (dict(plan=5, N=4095, C=1), 1),           # ... and N*C a multiple of 8
+    (dict(plan=5, B=(1 << 19) + 1, N=1024, C=64), 7),   # ... and B*N*C/8 work-items in 32 bits
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
     assert call(**kwargs) == status
