@@ -8,7 +8,8 @@ the workload (default: stereo64k_bf16, B=4, N=65536, C=128, bf16 in/out,
 float32 gain and arithmetic).  --op separable / backward / backward_separable
 / module / module_separable / module_backward time the other entry points the
 same way (module: the whole block with its W_in / W_out projections, eqs.
-(1)-(4)).  Inputs are resident in HBM before timing.
+(1)-(4)).  Inputs are resident in HBM before timing; the calls run on a
+stream of their own (default priority).
 
 Steps rotate over input/output sets whose total footprint is at least twice
 the 256 MB Infinity Cache, so every step reads its inputs from HBM (cold).
@@ -421,7 +422,10 @@ def main() -> int:
         del x, g
     torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream(dev)
+    # A stream of its own (default priority): every call, event, scrub and
+    # floor kernel below is ordered on it.
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.set_stream(stream)
     sptr = stream.cuda_stream
     hip = HipEvents()
     if op.startswith("backward"):
