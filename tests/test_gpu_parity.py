@@ -107,6 +107,50 @@ def test_padded_tokens(shape, dtype, dev, orc):
         check(f"{shape} {other}", run_gpu(x, g, dtype, dev, plan=other), ref, dtype)
 
 
+def _random_cases(n=40, seed=2607):
+    """Seeded shapes over every plan's range: N*C from 1 to 2^20 elements,
+    token counts that are powers of two or not, 1-6 slices, both dtypes."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        K = int(rng.integers(0, 21))
+        c = int(rng.integers(0, min(K, 9) + 1))
+        hi = 1 << (K - c)
+        N = hi if rng.random() < 0.5 or hi == 1 else int(rng.integers(hi // 2 + 1, hi + 1))
+        B = int(rng.integers(1, 7))
+        while B > 1 and B * hi * (1 << c) > (1 << 21):
+            B -= 1
+        cases.append((B, N, 1 << c, "bf16" if i % 2 else "f32"))
+    return cases
+
+
+RANDOM_CASES = _random_cases()
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES,
+                         ids=[f"r{i:02d}-{b}x{n}x{c}-{d}" for i, (b, n, c, d) in
+                              enumerate(RANDOM_CASES)])
+def test_random_shapes_every_plan(case, dev, orc):
+    """Each seeded shape through AUTO and every plan it allows, against the
+    oracle: the plans must agree with the definition wherever they apply."""
+    B, N, C, dtype = case
+    x, _ = workloads.draw(B, N, C, dtype, seed=5000 + 7 * N + C + B)
+    P = whtmix.padded_tokens(N)
+    _, g = workloads.draw(1, P, C, "f32", seed=5001 + N)
+    g = g.reshape(P, C)
+    ref = orc.whtmix(x, g)
+    plans = ["auto"]
+    for p in ("small", "fused", "three_pass", "wave_tiles", "one_launch"):
+        try:
+            whtmix.plan_describe(B, N, C, dtype, p)
+        except whtmix.WhtmixError:
+            continue
+        plans.append(p)
+    for p in plans:
+        say(f"random {case} plan={p}")
+        check(f"{case} {p}", run_gpu(x, g, dtype, dev, plan=p), ref, dtype)
+
+
 def test_fused_2_16_large_batch(dev, orc):
     """2^16-element slices in batches of 48 and more take one workgroup each."""
     B, N, C = 64, 1000, 64
