@@ -70,3 +70,25 @@ def run_gpu_separable(x: np.ndarray, gt: np.ndarray, gc: np.ndarray, dtype: str,
     torch.cuda.synchronize(dev)
     return to_host(y)
 
+
+
+def random_cases(n: int, seed: int, max_elems: int = 1 << 21) -> list[tuple]:
+    """Seeded (B, N, C, dtype) cases over every plan's range: N*C from 1 to
+    2^20 elements, token counts that are powers of two or not, 1-6 slices
+    (B * N_pad * C <= max_elems), float32 and bf16 alternately."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        K = int(rng.integers(0, 21))
+        c = int(rng.integers(0, min(K, 9) + 1))
+        hi = 1 << (K - c)
+        N = hi if rng.random() < 0.5 or hi == 1 else int(rng.integers(hi // 2 + 1, hi + 1))
+        B = int(rng.integers(1, 7))
+        while B > 1 and B * hi * (1 << c) > max_elems:
+            B -= 1
+        cases.append((B, N, 1 << c, "bf16" if i % 2 else "f32"))
+    return cases
+
+
+def case_ids(cases) -> list[str]:
+    return [f"r{i:02d}-{b}x{n}x{c}-{d}" for i, (b, n, c, d) in enumerate(cases)]

@@ -9,7 +9,8 @@ import pytest
 
 from oracle import oracle as oracle_mod
 from paper_2607_25234_amd import whtmix, workloads
-from tests.gpu_util import DERIVED, TOL, device, errors, say, to_device, to_host
+from tests.gpu_util import (DERIVED, TOL, case_ids, device, errors, random_cases, say,
+                            to_device, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -97,6 +98,34 @@ def test_backward_largest_tiles(dev, orc):
     dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
     check("dx", to_host(dx), dx_ref, DERIVED[dtype])
     check("dgain", to_host(dg), dg_ref, GRAD_TOL)
+
+
+BACKWARD_CASES = random_cases(24, 2609)
+
+
+@pytest.mark.parametrize("case", BACKWARD_CASES, ids=case_ids(BACKWARD_CASES))
+def test_random_shapes_backward(case, dev, orc):
+    """dX and dG on seeded shapes (every plan's range, padded token counts),
+    and the separable log-gain gradients on the same inputs."""
+    import torch
+    B, N, C, dtype = case
+    P = whtmix.padded_tokens(N)
+    x, dy, g = inputs(B, N, C, dtype, seed=7000 + 7 * N + C + B)
+    say(f"random backward {case} plan={whtmix.plan_describe(B, N, C, dtype)['plan']}")
+    xd, dyd = to_device(x, dtype, dev), to_device(dy, dtype, dev)
+    dx, dg = whtmix.backward(xd, dyd, torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize()
+    dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
+    check("dx", to_host(dx), dx_ref, DERIVED[dtype])
+    check("dgain", to_host(dg), dg_ref, GRAD_TOL)
+    gt, gc = workloads.draw_log_gains(P, C, seed=7001 + N)
+    dx, dgt, dgc = whtmix.backward_separable(xd, dyd, torch.from_numpy(gt).to(dev),
+                                             torch.from_numpy(gc).to(dev))
+    torch.cuda.synchronize()
+    dx_ref, dgt_ref, dgc_ref = orc.whtmix_grad_separable(x, dy, gt, gc)
+    check("dx (separable)", to_host(dx), dx_ref, DERIVED[dtype])
+    check("d log_gain_tokens", to_host(dgt), dgt_ref, GRAD_TOL)
+    check("d log_gain_channels", to_host(dgc), dgc_ref, GRAD_TOL)
 
 
 @pytest.mark.parametrize("shape", [(2, 32, 32), (3, 1000, 16), (2, 4096, 64), (4, 9216, 64)],

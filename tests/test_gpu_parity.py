@@ -10,8 +10,8 @@ import pytest
 
 from oracle import oracle as oracle_mod
 from paper_2607_25234_amd import whtmix, workloads
-from tests.gpu_util import (DERIVED, TOL, device, errors, run_gpu, run_gpu_separable, say,
-                            to_device, to_host)
+from tests.gpu_util import (DERIVED, TOL, case_ids, device, errors, random_cases, run_gpu,
+                            run_gpu_separable, say, to_device, to_host)
 
 log_gains = workloads.draw_log_gains
 
@@ -107,29 +107,10 @@ def test_padded_tokens(shape, dtype, dev, orc):
         check(f"{shape} {other}", run_gpu(x, g, dtype, dev, plan=other), ref, dtype)
 
 
-def _random_cases(n=40, seed=2607):
-    """Seeded shapes over every plan's range: N*C from 1 to 2^20 elements,
-    token counts that are powers of two or not, 1-6 slices, both dtypes."""
-    rng = np.random.default_rng(seed)
-    cases = []
-    for i in range(n):
-        K = int(rng.integers(0, 21))
-        c = int(rng.integers(0, min(K, 9) + 1))
-        hi = 1 << (K - c)
-        N = hi if rng.random() < 0.5 or hi == 1 else int(rng.integers(hi // 2 + 1, hi + 1))
-        B = int(rng.integers(1, 7))
-        while B > 1 and B * hi * (1 << c) > (1 << 21):
-            B -= 1
-        cases.append((B, N, 1 << c, "bf16" if i % 2 else "f32"))
-    return cases
+RANDOM_CASES = random_cases(40, 2607)
 
 
-RANDOM_CASES = _random_cases()
-
-
-@pytest.mark.parametrize("case", RANDOM_CASES,
-                         ids=[f"r{i:02d}-{b}x{n}x{c}-{d}" for i, (b, n, c, d) in
-                              enumerate(RANDOM_CASES)])
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=case_ids(RANDOM_CASES))
 def test_random_shapes_every_plan(case, dev, orc):
     """Each seeded shape through AUTO and every plan it allows, against the
     oracle: the plans must agree with the definition wherever they apply."""
@@ -149,6 +130,22 @@ def test_random_shapes_every_plan(case, dev, orc):
     for p in plans:
         say(f"random {case} plan={p}")
         check(f"{case} {p}", run_gpu(x, g, dtype, dev, plan=p), ref, dtype)
+
+
+SEPARABLE_CASES = random_cases(24, 2608)
+
+
+@pytest.mark.parametrize("case", SEPARABLE_CASES, ids=case_ids(SEPARABLE_CASES))
+def test_random_shapes_separable(case, dev, orc):
+    """The separable form (eqs. (2)-(3), log-domain gains) on seeded shapes,
+    through AUTO, against the oracle's two-stage form."""
+    B, N, C, dtype = case
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=6000 + 7 * N + C + B)
+    gt, gc = log_gains(P, C, seed=6001 + N)
+    say(f"random separable {case}")
+    check(f"{case} separable", run_gpu_separable(x, gt, gc, dtype, dev),
+          orc.whtmix_separable(x, gt, gc), dtype)
 
 
 def test_fused_2_16_large_batch(dev, orc):
