@@ -555,12 +555,13 @@ hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, f
     hipError_t e;
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     if (lay.per_chunk == 1) {
-        with_middle_gain(gain, a.B, [&](auto g) {
+        e = with_middle_gain(gain, a.B, [&](auto g) {
             hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, decltype(g), true, MIX_X>),
                                dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
                                wsx, wsd, g, o, (uint32_t)a.B, 1u);
-            return hipSuccess;
+            return hipGetLastError();
         });
+        if (e != hipSuccess) return e;
     } else if constexpr (HB + R < kMaxTile) {
         hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false, MIX_X>),
                            dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,

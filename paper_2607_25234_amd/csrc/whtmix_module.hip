@@ -695,9 +695,16 @@ __device__ __forceinline__ void stage_weights(void *lds, const void *w, uint32_t
 {
     u32x4 *d = static_cast<u32x4 *>(lds);
     const u32x4 *s = static_cast<const u32x4 *>(w);
+    // Chunks tau, tau + NT, ... below CHUNKS, over a compile-time trip count so
+    // the copy unrolls (a tau-dependent count left it a loop; the float32
+    // block on 32 slices of 2^18 took 64 us per call then, 58 now, and on 2
+    // slices of 2^21 58 then, 51 now).
 #pragma unroll
-    for (uint32_t c = tau; c < CHUNKS; c += NT)
-        d[c] = s[c];
+    for (uint32_t i = 0; i < (CHUNKS + NT - 1) / NT; ++i) {
+        const uint32_t c = tau + i * NT;
+        if (CHUNKS % NT == 0 || c < CHUNKS)
+            d[c] = s[c];
+    }
 }
 
 // The same copy without a trip through registers (global_load_lds_dwordx4):
