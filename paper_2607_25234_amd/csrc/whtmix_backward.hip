@@ -541,6 +541,18 @@ hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay
     return hipGetLastError();
 }
 
+// Calls f with the streamed form of a joint gain (other gains unchanged).
+template <class Gain, class F>
+inline hipError_t with_streamed_gain(Gain gain, F &&f)
+{
+    return f(gain);
+}
+template <class F>
+inline hipError_t with_streamed_gain(FullGain gain, F &&f)
+{
+    return f(StreamedGain{gain.g});
+}
+
 // The fused middle on the outer transforms in wsx and wsd (dG, and dY's mixer
 // up to its last pass, in place in wsd) -> [chunk sums] -> [separable sums].
 template <int K, class Gain, bool MIX_X = false>
@@ -563,9 +575,16 @@ hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, f
         });
         if (e != hipSuccess) return e;
     } else if constexpr (HB + R < kMaxTile) {
-        hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false, MIX_X>),
-                           dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st, wsx,
-                           wsd, gain, o, (uint32_t)a.B, lay.per_chunk);
+        // each workgroup reads its run's gain once and holds it for the chunk's
+        // slices: a joint gain streams (non-temporal), so it does not displace
+        // the two workspaces
+        e = with_streamed_gain(gain, [&](auto g) {
+            hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, decltype(g), false, MIX_X>),
+                               dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
+                               wsx, wsd, g, o, (uint32_t)a.B, lay.per_chunk);
+            return hipGetLastError();
+        });
+        if (e != hipSuccess) return e;
     } else {
         return hipErrorInvalidValue;   // backward_layout gives 2^15 tiles one slice per chunk
     }
