@@ -371,6 +371,68 @@ sep_cols_partial_kernel(const float *__restrict__ dG, const float *__restrict__ 
         part[(size_t)blockIdx.x * C + c] = red[tid];
 }
 
+// Row sums (dg_t) and column partial sums of dG*G in one pass over dG, for
+// C = 2^CB <= 256.  Block blockIdx.x covers rows [r0, r0 + rows_per_block);
+// each step a wave takes RPW = 64 / SEG rows, a row's C columns spread over
+// SEG = min(C, 64) lanes (KPL = C / SEG columns each), so a row sum is a
+// segmented wave reduction and needs no LDS.  Each exp is taken once.  The
+// column sums of a wave's RPW rows are added across the wave, then over the
+// four waves in LDS: part[blockIdx.x][c], fixed order throughout.
+template <int CB>
+__global__ void __launch_bounds__(256)
+sep_rows_cols_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
+                     const float *__restrict__ gc, float *__restrict__ dgt,
+                     float *__restrict__ part, uint32_t P, uint32_t rows_per_block)
+{
+    constexpr uint32_t C = 1u << CB;
+    constexpr uint32_t SEG = C < 64u ? C : 64u;
+    constexpr uint32_t RPW = 64u / SEG;
+    constexpr uint32_t KPL = C / SEG;
+    __shared__ float red[4][C];
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    const uint32_t c0 = lane & (SEG - 1u);
+    const uint32_t rw = lane / SEG;
+    const uint32_t r0 = blockIdx.x * rows_per_block;
+    const uint32_t r1 = min(r0 + rows_per_block, P);
+    float gcv[KPL], cs[KPL];
+#pragma unroll
+    for (uint32_t k = 0; k < KPL; ++k) {
+        gcv[k] = gc[c0 + SEG * k];
+        cs[k] = 0.0f;
+    }
+    for (uint32_t rb = r0; rb < r1; rb += 4u * RPW) {   // uniform over the block
+        const uint32_t r = rb + wave * RPW + rw;
+        float rs = 0.0f;
+        if (r < r1) {
+            const float g = gt[r];
+            const float *d = dG + (size_t)r * C;
+#pragma unroll
+            for (uint32_t k = 0; k < KPL; ++k) {
+                const float p = d[c0 + SEG * k] * __expf(g + gcv[k]);
+                cs[k] += p;
+                rs += p;
+            }
+        }
+#pragma unroll
+        for (uint32_t off = SEG >> 1; off > 0; off >>= 1)
+            rs += __shfl_xor(rs, off, 64);
+        if (c0 == 0 && r < r1)
+            dgt[r] = rs;
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < KPL; ++k) {
+        float t = cs[k];
+#pragma unroll
+        for (uint32_t off = SEG; off < 64u; off <<= 1)
+            t += __shfl_xor(t, off, 64);
+        if (rw == 0)
+            red[wave][c0 + SEG * k] = t;
+    }
+    __syncthreads();
+    for (uint32_t c = threadIdx.x; c < C; c += 256u)
+        part[(size_t)blockIdx.x * C + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+}
+
 // dgc[c] = sum over row blocks of part[b][c]: one block per column, 256-way
 // strided sums then a fixed-order tree.
 __global__ void __launch_bounds__(256)
@@ -505,8 +567,11 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
         const uint64_t P = L / (uint64_t)C;
         lay.dg = cursor;
         cursor += L;
-        uint64_t rpb = (P + 4095) / 4096;
-        if (rpb < 64) rpb = 64;
+        // about 2048 row blocks (the single-pass kernel's workgroups), at least
+        // one step of its rows: 256 / min(C, 64)
+        uint64_t rpb = (P + 2047) / 2048;
+        const uint64_t step = 256 / (C < 64 ? (uint64_t)C : 64);
+        if (rpb < step) rpb = step;
         lay.rows_per_block = (uint32_t)rpb;
         lay.col_blocks = (uint32_t)((P + rpb - 1) / rpb);
         lay.colpart = cursor;
@@ -520,6 +585,10 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
 
 namespace {
 
+// The single-pass row / column reduction covers C <= 2^8; wider C keeps the
+// separate row and column kernels.
+constexpr int kSepFusedMaxCbits = 8;
+
 // Separable log-gain gradients from the joint dG in dst:
 // dg_t = row sums and dg_c = column sums of dG o G.
 hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay, const float *dst)
@@ -527,15 +596,34 @@ hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay
     const hipStream_t st = a.stream;
     const uint64_t L = uint64_t(1) << a.K;
     const uint32_t P = (uint32_t)(L >> a.cbits);
-    hipError_t e;
-    hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
-                       a.gain_c, a.dgt, P, (uint32_t)a.cbits);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     const uint32_t C = 1u << a.cbits;
-    hipLaunchKernelGGL(sep_cols_partial_kernel, dim3(lay.col_blocks, C > 256u ? C / 256u : 1u),
-                       dim3(256), 0, st, dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P,
-                       (uint32_t)a.cbits, lay.rows_per_block);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipError_t e;
+    if (a.cbits <= kSepFusedMaxCbits) {
+        // one pass: row sums and column partials together
+        const dim3 grid(lay.col_blocks), block(256);
+        float *colpart = a.ws + lay.colpart;
+        switch (a.cbits) {
+#define WHTMIX_SEP_CASE(cb)                                                                    \
+    case cb:                                                                                  \
+        hipLaunchKernelGGL(sep_rows_cols_kernel<cb>, grid, block, 0, st, dst, a.gain_t,       \
+                           a.gain_c, a.dgt, colpart, P, lay.rows_per_block);                  \
+        break;
+            WHTMIX_SEP_CASE(0) WHTMIX_SEP_CASE(1) WHTMIX_SEP_CASE(2) WHTMIX_SEP_CASE(3)
+            WHTMIX_SEP_CASE(4) WHTMIX_SEP_CASE(5) WHTMIX_SEP_CASE(6) WHTMIX_SEP_CASE(7)
+            WHTMIX_SEP_CASE(8)
+#undef WHTMIX_SEP_CASE
+        default: return hipErrorInvalidValue;
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+        hipLaunchKernelGGL(sep_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, st, dst, a.gain_t,
+                           a.gain_c, a.dgt, P, (uint32_t)a.cbits);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(sep_cols_partial_kernel, dim3(lay.col_blocks, C / 256u), dim3(256), 0,
+                           st, dst, a.gain_t, a.gain_c, a.ws + lay.colpart, P, (uint32_t)a.cbits,
+                           lay.rows_per_block);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(sep_cols_final_kernel, dim3(C), dim3(256), 0, st, a.ws + lay.colpart,
                        a.dgc, lay.col_blocks, C);
     return hipGetLastError();
