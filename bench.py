@@ -80,6 +80,7 @@ def kernel_source_hash(files=FORWARD_SOURCES) -> str:
 def kernel_names(plan: str) -> list[str]:
     return {"three_pass": ["outer_fwd", "middle", "outer_inv"],
             "wave_tiles": ["wave_pass1", "wave_middle", "wave_pass3"],
+            "two_pass": ["fold_pass", "wave_pass3"],
             "fused": ["fused"], "small": ["small"], "one_launch": ["one_launch"]}[plan]
 
 
@@ -94,6 +95,10 @@ def algorithmic_bytes(plan: str, B: int, N: int, C: int, s: int, gbytes: int) ->
     three = [B * L * (s + 4),           # read x, write float32 workspace
              B * L * 8 + gbytes,        # read + write workspace, read the gain once
              B * L * (4 + s)]           # read workspace, write y
+    if plan == "two_pass":
+        # the fold pass reads the slice once from memory (its workgroups'
+        # re-reads hit L2), reads the gain, writes the workspace
+        return [B * L * (s + 4) + gbytes, three[2]]
     return [sum(three)] if plan == "one_launch" else three   # three_pass and wave_tiles
 
 
@@ -102,7 +107,7 @@ def backward_plan(plan: dict) -> str:
     of 2^16 and more take the three-pass plan, smaller wave-tile shapes the
     one-workgroup plan (the library's rule)."""
     p = plan["plan"]
-    if p in ("wave_tiles", "one_launch"):
+    if p in ("wave_tiles", "one_launch", "two_pass"):
         return "three_pass" if plan["log2_slice"] >= 16 or p == "one_launch" else "fused"
     if p == "fused" and plan["log2_slice"] >= 16:
         return "three_pass"
@@ -531,7 +536,7 @@ def main() -> int:
                   for j in range(nk)]
 
     floor = None
-    if op == "forward" and plan["plan"] in ("three_pass", "one_launch", "wave_tiles"):
+    if op == "forward" and plan["plan"] in ("three_pass", "one_launch", "wave_tiles", "two_pass"):
         floor = copy_floor(torch, w, sets, P, hip, sptr)
     hip.destroy()
 

@@ -82,7 +82,7 @@ typedef enum whtmix_status {
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
  *   L <= 2^10          one small workgroup per slice, all stages in LDS;
  *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass; for
- *                      L = 2^15 up to 16 slices WAVE_TILES instead;
+ *                      L = 2^15 up to 40 slices TWO_PASS instead;
  *   L = 2^16           WAVE_TILES up to 3 slices, FUSED (two register sets)
  *                      from 48 slices, THREE_PASS between;
  *   L >= 2^17          THREE_PASS: forward over the low bits of the flat
@@ -93,7 +93,13 @@ typedef enum whtmix_status {
  * whose butterflies stay inside the wave (DPP and lane-swap exchanges, no
  * LDS): three launches of 2^(K-9) workgroups per slice; 2^12 <= L <= 2^16
  * and N*C a multiple of 8 (AUTO falls back to the plans above otherwise);
- * forced, B*L <= 2^35 besides (WHTMIX_ERROR_TOO_LARGE beyond).
+ * forced, B*L < 2^35 besides (WHTMIX_ERROR_TOO_LARGE beyond).
+ * TWO_PASS (L = 2^15 or 2^16, N*C a multiple of 8) replaces WAVE_TILES's
+ * first two launches by one: each of a slice's 2^(K-12) workgroups reads the
+ * whole slice and forms its share of the low-bit transform as a signed sum
+ * of the slice's blocks, then runs the high bits, the gain and their
+ * inverse; WAVE_TILES's last launch follows.  B rounded up to a multiple of
+ * 8, times L, must stay below 2^35.
  * ONE_LAUNCH (never chosen by AUTO) runs WAVE_TILES's three passes in a
  * single cooperative launch, ordered by per-slice counters in a small
  * per-stream block; B <= 2046 besides.  On MI355X it is slower than the plans
@@ -108,7 +114,8 @@ typedef enum whtmix_plan {
     WHTMIX_PLAN_FUSED = 2,
     WHTMIX_PLAN_THREE_PASS = 3,
     WHTMIX_PLAN_ONE_LAUNCH = 4,
-    WHTMIX_PLAN_WAVE_TILES = 5
+    WHTMIX_PLAN_WAVE_TILES = 5,
+    WHTMIX_PLAN_TWO_PASS = 6
 } whtmix_plan;
 
 typedef struct whtmix_options {

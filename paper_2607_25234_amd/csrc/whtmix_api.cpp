@@ -79,8 +79,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
         return WHTMIX_ERROR_TOO_LARGE;
     const int64_t L = int64_t(1) << K;
     // Work-items per launch are B*L/32 (tiled plans) or B*256 (small plan);
-    // both must fit the 32-bit grid size.
-    if (B > (int64_t(1) << 37) / L)
+    // both must stay below 2^32 (the grid size is a 32-bit count).
+    if (B > ((int64_t(1) << 37) - 1) / L)
         return WHTMIX_ERROR_TOO_LARGE;
     if (K <= whtmix::kMaxSmall && B >= (int64_t(1) << 24))
         return WHTMIX_ERROR_TOO_LARGE;
@@ -90,8 +90,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     switch (plan) {
     case whtmix::PLAN_AUTO:
         plan = K <= whtmix::kMaxSmall ? whtmix::PLAN_SMALL
-               : K == whtmix::kMaxTile && wave_ok && B <= whtmix::kWave15MaxBatch
-                   ? whtmix::PLAN_WAVE_TILES
+               : K == whtmix::kMaxTile && wave_ok && B <= whtmix::kTwoPass15MaxBatch
+                   ? whtmix::PLAN_TWO_PASS
                : K <= whtmix::kMaxTile ? whtmix::PLAN_FUSED
                : K == whtmix::kMaxFused && B >= whtmix::kFusedPairMinBatch ? whtmix::PLAN_FUSED
                : K == whtmix::kMaxFused && wave_ok && B <= whtmix::kWave16MaxBatch
@@ -101,7 +101,12 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     case whtmix::PLAN_WAVE_TILES:
         if (!wave_ok) return WHTMIX_ERROR_INVALID_VALUE;
         // one 64-thread workgroup per 2^9 elements: B*L/8 work-items
-        if (B > (int64_t(1) << 35) / L) return WHTMIX_ERROR_TOO_LARGE;
+        if (B > ((int64_t(1) << 35) - 1) / L) return WHTMIX_ERROR_TOO_LARGE;
+        break;
+    case whtmix::PLAN_TWO_PASS:
+        if (!wave_ok || K < whtmix::kTwoPassMinK) return WHTMIX_ERROR_INVALID_VALUE;
+        // the fold pass runs B*L/8 work-items with B rounded up to a multiple of 8
+        if ((B + 7) / 8 * 8 > ((int64_t(1) << 35) - 1) / L) return WHTMIX_ERROR_TOO_LARGE;
         break;
     case whtmix::PLAN_ONE_LAUNCH:
         if (!wave_ok || B > whtmix::kOneLaunchMaxBatch) return WHTMIX_ERROR_INVALID_VALUE;
@@ -122,13 +127,15 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
     out->n_pad = int64_t(1) << nbits;
     out->plan = plan;
     out->elt = dtype == WHTMIX_DTYPE_BF16 ? 2 : 4;
-    out->kernels =
-        plan == whtmix::PLAN_THREE_PASS || plan == whtmix::PLAN_WAVE_TILES ? 3 : 1;
+    out->kernels = plan == whtmix::PLAN_THREE_PASS || plan == whtmix::PLAN_WAVE_TILES ? 3
+                   : plan == whtmix::PLAN_TWO_PASS                                  ? 2
+                                                                                    : 1;
     if (plan == whtmix::PLAN_THREE_PASS) {
         out->split = whtmix::three_pass_split(K);
         out->ws_bytes = B * L * 4;
     }
-    if (plan == whtmix::PLAN_WAVE_TILES || plan == whtmix::PLAN_ONE_LAUNCH) {
+    if (plan == whtmix::PLAN_WAVE_TILES || plan == whtmix::PLAN_ONE_LAUNCH ||
+        plan == whtmix::PLAN_TWO_PASS) {
         out->split = whtmix::Split{9, K - 9, 18 - K};
         out->ws_bytes = B * L * 4;
     }
@@ -143,7 +150,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
 // ONE_LAUNCH).
 void three_pass_beyond_one_tile(int64_t B, Checked *c)
 {
-    if (c->plan == whtmix::PLAN_WAVE_TILES && c->K <= whtmix::kMaxTile) {
+    if ((c->plan == whtmix::PLAN_WAVE_TILES || c->plan == whtmix::PLAN_TWO_PASS) &&
+        c->K <= whtmix::kMaxTile) {
         c->plan = whtmix::PLAN_FUSED;
         c->kernels = 1;
         c->split = whtmix::Split{0, 0, 0};
@@ -151,7 +159,8 @@ void three_pass_beyond_one_tile(int64_t B, Checked *c)
         return;
     }
     if ((c->plan == whtmix::PLAN_FUSED && c->K > whtmix::kMaxTile) ||
-        c->plan == whtmix::PLAN_ONE_LAUNCH || c->plan == whtmix::PLAN_WAVE_TILES) {
+        c->plan == whtmix::PLAN_ONE_LAUNCH || c->plan == whtmix::PLAN_WAVE_TILES ||
+        c->plan == whtmix::PLAN_TWO_PASS) {
         c->plan = whtmix::PLAN_THREE_PASS;
         c->kernels = 3;
         c->split = whtmix::three_pass_split(c->K);
@@ -249,7 +258,7 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
     info->kernels = c.kernels;
     info->log2_slice = c.K;
     const bool passes = c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_ONE_LAUNCH ||
-                        c.plan == whtmix::PLAN_WAVE_TILES;
+                        c.plan == whtmix::PLAN_WAVE_TILES || c.plan == whtmix::PLAN_TWO_PASS;
     info->outer_bits = passes ? c.split.A : 0;
     info->run_bits = passes ? c.split.R : 0;
     info->workspace_bytes = c.ws_bytes;
@@ -273,8 +282,8 @@ int whtmix_plan_describe(int64_t B, int64_t N, int64_t C, int dtype,
 
 namespace {
 
-// noalloc: the three-pass or wave-tile workspace is the fixed device scratch instead of
-// the per-stream workspace, and nothing is allocated.
+// noalloc: the three-pass, two-pass or wave-tile workspace is the fixed device scratch
+// instead of the per-stream workspace, and nothing is allocated.
 int forward_impl(const void *x, int gain_kind, const float *gain, const float *gain_t,
                  const float *gain_c, void *y, int64_t B, int64_t N, int64_t C, int dtype,
                  void *stream, const whtmix_options *options, bool noalloc = false)
@@ -317,8 +326,11 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
     for (int i = 0; i < 4; ++i)
         a.events[i] = options ? static_cast<hipEvent_t>(options->events[i]) : nullptr;
 
-    const bool wave = c.plan == whtmix::PLAN_WAVE_TILES || c.plan == whtmix::PLAN_ONE_LAUNCH;
-    if (noalloc && (c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_WAVE_TILES)) {
+    const bool wave = c.plan == whtmix::PLAN_WAVE_TILES || c.plan == whtmix::PLAN_ONE_LAUNCH ||
+                      c.plan == whtmix::PLAN_TWO_PASS;
+    const bool uses_ws = c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_WAVE_TILES ||
+                         c.plan == whtmix::PLAN_TWO_PASS;
+    if (noalloc && uses_ws) {
         if (c.ws_bytes > whtmix::kNoAllocScratchFloats * 4) {
             g_last_error = "whtmix_forward_noalloc: the call needs " + std::to_string(c.ws_bytes) +
                            " bytes of workspace, more than the fixed " +
@@ -332,7 +344,7 @@ int forward_impl(const void *x, int gain_kind, const float *gain, const float *g
         if (e != hipSuccess) return hip_fail(e, "kernel launch");
         return WHTMIX_SUCCESS;
     }
-    if (c.plan == whtmix::PLAN_THREE_PASS || c.plan == whtmix::PLAN_WAVE_TILES) {
+    if (uses_ws) {
         std::lock_guard<std::mutex> lock(g_ws_mutex);
         st = get_workspace(stream, c.ws_bytes, &a.ws);
         if (st != WHTMIX_SUCCESS) return st;

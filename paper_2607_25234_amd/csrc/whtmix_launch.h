@@ -39,9 +39,10 @@ struct LaunchArgs {
 hipError_t launch(const LaunchArgs &a);
 
 // Enqueues the wave-tile kernels (whtmix_wave.hip): a.plan is WAVE_TILES
-// (three launches) or ONE_LAUNCH (one cooperative launch; a.B <=
-// kOneLaunchMaxBatch and a.counters a zeroed-or-reset counter block);
-// 12 <= a.K <= 16, a.nvalid a multiple of 8, a.ws holding a.B * 2^K floats.
+// (three launches), TWO_PASS (two launches; a.K is 15 or 16) or ONE_LAUNCH
+// (one cooperative launch; a.B <= kOneLaunchMaxBatch and a.counters a
+// zeroed-or-reset counter block); 12 <= a.K <= 16, a.nvalid a multiple of 8,
+// a.ws holding a.B * 2^K floats.
 hipError_t launch_wave(const LaunchArgs &a);
 
 // Device address of the fixed scratch array on the current device

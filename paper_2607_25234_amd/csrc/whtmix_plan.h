@@ -17,7 +17,8 @@ enum PlanKind {
     PLAN_FUSED = 2,
     PLAN_THREE_PASS = 3,
     PLAN_ONE_LAUNCH = 4,
-    PLAN_WAVE_TILES = 5
+    PLAN_WAVE_TILES = 5,
+    PLAN_TWO_PASS = 6
 };
 
 constexpr int kMaxLog2Slice = 30;   // N*C <= 2^30
@@ -41,10 +42,17 @@ constexpr int kFusedPairMinBatch = 48;
 // takes at most kOneLaunchMaxBatch slices.
 constexpr int kWaveMinK = 12;
 constexpr int kWaveMaxK = 16;
-// AUTO takes WAVE_TILES for slices of 2^16 elements up to 3 slices and of
-// 2^15 up to 16 (measured crossovers against THREE_PASS and FUSED).
+// AUTO takes WAVE_TILES for slices of 2^16 elements up to 3 slices (measured
+// crossover against THREE_PASS).
 constexpr int kWave16MaxBatch = 3;
-constexpr int kWave15MaxBatch = 16;
+// TWO_PASS (whtmix_wave.hip): a fold pass in place of passes 1 and 2, then
+// pass 3; slices of 2^15 and 2^16 elements.  AUTO takes it for 2^15-element
+// slices up to 40 (one launch fewer than WAVE_TILES, and from 17 slices
+// faster than one workgroup per slice until about 48).  For 2^16 slices each
+// fold workgroup reads 256 KiB (float32) and, with x arriving from memory,
+// the pass loses the launch it saves, so AUTO keeps WAVE_TILES there.
+constexpr int kTwoPassMinK = 15;
+constexpr int kTwoPass15MaxBatch = 40;
 constexpr int kCounterWords = 4096;
 constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
 // Polls of a ONE_LAUNCH wait before it gives up (about a second or two).

@@ -537,6 +537,173 @@ one_launch_kernel(const T *__restrict__ x, T *__restrict__ y, Gain gain, float *
     }
 }
 
+// ---------------------------------------------------------------- TWO_PASS
+// Two launches for slices of 2^15 and 2^16 elements: a fold pass that
+// replaces passes 1 and 2, then pass 3 as above.
+//
+// Write t9 = mu*2^Q + j for the 9 low bits of f (Q = 21 - K low bits j, the
+// A = 9 - Q bits mu above them) and hi for the HB high bits.  H_2^9 is
+// H_2^A (on mu) times H_2^Q (on j), so the forward transform over the low
+// bits, read at one value m of mu, is
+//   u[hi][m*2^Q + j] = H_2^Q( sum_a (-1)^popcount(m & a) x[hi][a*2^Q + .] )[j]:
+// a signed sum of the 2^A blocks of 2^Q elements of row hi, then a
+// transform of length 2^Q.  Workgroup (b, m) evaluates it for all 2^HB rows
+// from the whole slice (read 2^(9-Q) times over, once per workgroup, from
+// L2), so it holds the 2^12 elements (hi, j) with mu = m fully transformed
+// over the low bits.  It then runs the forward over hi, the gain, the
+// inverse over hi, and stores its elements to the workspace in the run
+// layout that pass 3 gathers (8 whole middle tiles, 16 contiguous KiB).
+// One launch boundary fewer than WAVE_TILES, at the price of each workgroup
+// reading the whole slice.
+//
+// 512 threads, 8 values each, in two register layouts:
+//   M1: j = (t mod 2^LJ) << 2 | k mod 4, hi = t >> LJ | (k >> 2) << (HB - 1);
+//   M2: j = t mod 2^Q, hi = (h mod 2^W0) | k << W0 | (h >> W0) << (HB - 1),
+//       h = t >> Q;
+// with LJ = Q - 2 lane bits of j and W0 = 6 - LJ lane bits of hi in M1.  M1
+// holds j's low bits in registers and lanes (the fold's 16-byte groups,
+// H_2^Q by registers and DPP) and hi's bits except the three wave bits
+// [W0, W0 + 3) in lanes (DPP, permlane swaps) and register bit 2; M2 holds
+// those three wave bits in registers.  The layouts meet in a 16 KiB LDS
+// array in natural [hi][j] order (M1 writes 16-byte rows of a wave's 1 KiB,
+// M2 reads 64 consecutive floats per register: no bank conflicts).
+template <int K>
+struct Fold {
+    static constexpr int HB = K - TB;     // high bits of f
+    static constexpr int R = TB - HB;     // workspace run bits (pass 3's layout)
+    static constexpr int Q = 21 - K;      // low bits a workgroup keeps
+    static constexpr int A = TB - Q;      // folded bits: 2^A workgroups per slice
+    static constexpr int LJ = Q - 2;      // lane bits of j in M1
+    static constexpr int W0 = 6 - LJ;     // lane bits of hi in M1
+    static_assert((K == 15 || K == 16) && HB == W0 + 4 && R >= 2 && Q - R == 3,
+                  "the fold pass covers 2^15- and 2^16-element slices");
+};
+
+__device__ __forceinline__ float fold_sign(uint32_t m, uint32_t a)
+{
+    return (__builtin_popcount(m & a) & 1) ? -1.0f : 1.0f;
+}
+
+// Four consecutive x elements at byte offset voff + soff of the slice's
+// buffer resource, as float32.  The resource spans the slice's valid
+// elements, so groups past them (padded N; whole groups, as nvalid is a
+// multiple of 8) read as zeros, with no branch: every load of the fold is
+// issued before the first is waited for.  Temporal: the slice is read by
+// every workgroup of its fold and stays in L2.
+template <typename T>
+__device__ __forceinline__ f32x4 load_x4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    if constexpr (sizeof(T) == 4) {
+        return __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, tile::kTemporal));
+    } else {
+        typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 q = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, tile::kTemporal));
+        return f32x4{__builtin_bit_cast(float, q[0] << 16),
+                     __builtin_bit_cast(float, q[0] & 0xffff0000u),
+                     __builtin_bit_cast(float, q[1] << 16),
+                     __builtin_bit_cast(float, q[1] & 0xffff0000u)};
+    }
+}
+
+// Workgroups are dealt to the 8 XCDs round-robin (block i on XCD i mod 8), so
+// block i takes slice b = (i >> (A + 3)) * 8 + i mod 8, part m = (i >> 3) mod
+// 2^A: the 2^A workgroups of a slice share one XCD, whose L2 fetches the
+// slice once for all of them (a slice read by every XCD at once costs
+// 2.5 us more per call when it comes from memory).  The grid covers B
+// rounded up to a multiple of 8; blocks past the last slice exit at once.
+template <int K, typename T, class Gain>
+__global__ void __launch_bounds__(512)
+fold_pass_kernel(const T *__restrict__ x, float *__restrict__ ws, Gain gain, uint32_t nvalid,
+                 uint32_t nslices)
+{
+    using F = Fold<K>;
+    constexpr int HB = F::HB, Q = F::Q, LJ = F::LJ, W0 = F::W0;
+    constexpr float scale = 1.0f / (float)(1u << K);   // exact power of two
+    __shared__ __attribute__((aligned(16))) float lds[1u << (HB + Q)];
+
+    const uint32_t t = threadIdx.x, lane = t & 63u;
+    const uint32_t b = ((blockIdx.x >> (F::A + 3)) << 3) | (blockIdx.x & 7u);
+    const uint32_t m = (blockIdx.x >> 3) & ((1u << F::A) - 1u);
+    if (b >= nslices)
+        return;   // uniform per workgroup, before any barrier
+
+    // M2 coordinates and this workgroup's gains (read first, used last).
+    const uint32_t j2 = t & ((1u << Q) - 1u), h2 = t >> Q;
+    auto hi2 = [&](int k) {
+        return (h2 & ((1u << W0) - 1u)) | ((uint32_t)k << W0) | ((h2 >> W0) << (HB - 1));
+    };
+    float gv[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        gv[k] = gain.at((hi2(k) << TB) | (m << Q) | j2) * scale;
+
+    // M1 coordinates.
+    const uint32_t j1 = (t & ((1u << LJ) - 1u)) << 2;
+    const uint32_t h1 = t >> LJ;   // hi without its top bit (register bit 2)
+
+    // Fold: the signed sum over a of the blocks of row hi, then H over j.
+    constexpr uint32_t EB = sizeof(T);
+    const __amdgpu_buffer_rsrc_t xr = tile::buffer(x + (size_t)b * nvalid, nvalid * EB);
+    const uint32_t voff = ((h1 << TB) | j1) * EB;
+    float v[NV];
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+        const uint32_t row = ((uint32_t)rr << (HB - 1 + TB)) * EB;
+        f32x4 acc = load_x4<T>(xr, voff, row);
+#pragma unroll
+        for (uint32_t a = 1; a < (1u << F::A); ++a)
+            acc += fold_sign(m, a) * load_x4<T>(xr, voff, row + (a << Q) * EB);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[4 * rr + e] = acc[e];
+    }
+    reg_bfly<0>(v);
+    reg_bfly<1>(v);
+    lane_bfly<0>(v, lane);
+    lane_bfly<1>(v, lane);
+    lane_bfly<2>(v, lane);
+    if constexpr (LJ == 4)
+        lane_bfly<3>(v, lane);
+
+    // Forward over hi: its lane bits and top bit here, its wave bits in M2.
+    wave_bfly<LJ>(v, lane);
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr)
+        st4(v, rr, lds + (((h1 | ((uint32_t)rr << (HB - 1))) << Q) | j1));
+    __syncthreads();
+    float u[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        u[k] = lds[(hi2(k) << Q) | j2];
+    reg_bfly<0>(u);
+    reg_bfly<1>(u);
+    reg_bfly<2>(u);
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        u[k] *= gv[k];
+    reg_bfly<0>(u);
+    reg_bfly<1>(u);
+    reg_bfly<2>(u);
+    // Each thread writes back the words it read: no barrier between.
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        lds[(hi2(k) << Q) | j2] = u[k];
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr)
+        ld4(v, rr, lds + (((h1 | ((uint32_t)rr << (HB - 1))) << Q) | j1));
+    wave_bfly<LJ>(v, lane);
+
+    // Store in pass 3's run layout: t9 -> (t9 >> R) << 9 | hi << R | t9 mod 2^R.
+    const uint32_t t9 = (m << Q) | j1;
+    float *dst = ws + ((size_t)b << K) + ((t9 >> F::R) << TB) + (t9 & ((1u << F::R) - 1u));
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr)
+        st4(v, rr, dst + ((h1 | ((uint32_t)rr << (HB - 1))) << F::R));
+}
+
 // ---------------------------------------------------------------- launch
 inline hipError_t record(hipEvent_t ev, hipStream_t st)
 {
@@ -598,8 +765,32 @@ hipError_t launch_wave_tiles_k(const LaunchArgs &a, Gain gain)
 }
 
 template <int K, typename T, class Gain>
+hipError_t launch_two_pass_k(const LaunchArgs &a, Gain gain)
+{
+    if constexpr (K == 15 || K == 16) {
+        const T *x = static_cast<const T *>(a.x);
+        T *y = static_cast<T *>(a.y);
+        const hipStream_t st = a.stream;
+        hipError_t e = record(a.events[0], st);
+        if (e != hipSuccess) return e;
+        const uint32_t groups = (uint32_t)((a.B + 7) / 8);   // of 8 slices, one per XCD
+        hipLaunchKernelGGL((fold_pass_kernel<K, T, Gain>), dim3(groups << (Fold<K>::A + 3)),
+                           dim3(512), 0, st, x, a.ws, gain, a.nvalid, (uint32_t)a.B);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = record(a.events[1], st)) != hipSuccess) return e;
+        hipLaunchKernelGGL((wave_pass3_kernel<K, T>), dim3((uint32_t)a.B << Shape<K>::HB),
+                           dim3(64), 0, st, a.ws, y, a.nvalid);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return record(a.events[2], st);
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+template <int K, typename T, class Gain>
 hipError_t launch_k(const LaunchArgs &a, Gain gain)
 {
+    if (a.plan == PLAN_TWO_PASS) return launch_two_pass_k<K, T, Gain>(a, gain);
     return a.plan == PLAN_ONE_LAUNCH ? launch_one_launch_k<K, T, Gain>(a, gain)
                                      : launch_wave_tiles_k<K, T, Gain>(a, gain);
 }
@@ -631,7 +822,7 @@ hipError_t dispatch_gain(const LaunchArgs &a)
 
 hipError_t launch_wave(const LaunchArgs &a)
 {
-    if (a.plan != PLAN_ONE_LAUNCH && a.plan != PLAN_WAVE_TILES)
+    if (a.plan != PLAN_ONE_LAUNCH && a.plan != PLAN_WAVE_TILES && a.plan != PLAN_TWO_PASS)
         return hipErrorInvalidValue;
     if (a.dtype == DTYPE_BF16)
         return wave::dispatch_gain<__bf16>(a);

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libwhtmix.so")
 SUCCESS = 0
 DTYPE_F32, DTYPE_BF16 = 0, 1
 PLANS = {"auto": 0, "small": 1, "fused": 2, "three_pass": 3, "one_launch": 4,
-         "wave_tiles": 5}
+         "wave_tiles": 5, "two_pass": 6}
 PLAN_NAMES = {v: k for k, v in PLANS.items()}
 
 # Every symbol include/whtmix.h declares.

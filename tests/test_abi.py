@@ -84,7 +84,11 @@ def call(x=ALIGNED, g=ALIGNED2, y=ALIGNED, B=1, N=64, C=64, dtype=0, plan=0):
     (dict(plan=5, N=32, C=64), 1),            # WAVE_TILES needs 2^12..2^16
     (dict(plan=5, N=4096, C=32), 1),
     (dict(plan=5, N=4095, C=1), 1),           # ... and N*C a multiple of 8
-    (dict(plan=5, B=(1 << 19) + 1, N=1024, C=64), 7),   # ... and B*N*C/8 work-items in 32 bits
+    (dict(plan=5, B=1 << 19, N=1024, C=64), 7),   # ... and B*N*C/8 < 2^32 work-items
+    (dict(B=1 << 21, N=1024, C=64), 7),           # tiled plans: B*N*C/32 < 2^32
+    (dict(plan=6, N=32, C=64), 1),                # TWO_PASS needs 2^15..2^16
+    (dict(plan=6, N=32767, C=1), 1),              # ... and N*C a multiple of 8
+    (dict(plan=6, B=(1 << 19) - 7, N=1024, C=64), 7),   # ... and B rounded up to 8
 ])
 def test_rejected_before_any_hip_call(kwargs, status):
     assert call(**kwargs) == status
@@ -255,7 +259,7 @@ def test_plan_table():
     assert whtmix.plan_describe(3, 32, 32)["plan"] == "small"
     assert whtmix.plan_describe(3, 32, 64)["plan"] == "fused"
     assert whtmix.plan_describe(3, 256, 64)["plan"] == "fused"
-    assert whtmix.plan_describe(3, 256, 128)["plan"] == "wave_tiles"   # 2^15, few slices
+    assert whtmix.plan_describe(3, 256, 128)["plan"] == "two_pass"   # 2^15, up to 40 slices
     d = whtmix.plan_describe(3, 1024, 128, "bf16")
     assert d["plan"] == "three_pass" and d["kernels"] == 3
     assert d["workspace_bytes"] == 3 * 1024 * 128 * 4
@@ -268,10 +272,22 @@ def test_plan_table():
     assert (d["outer_bits"], d["run_bits"]) == (9, 2)
     d = whtmix.plan_describe(2, 64, 64, plan="one_launch")
     assert (d["plan"], d["outer_bits"], d["run_bits"]) == ("one_launch", 9, 6)
+    # TWO_PASS: slices of 2^15 and 2^16 only, two launches, the wave tiles'
+    # workspace; the block and the backward pass run as for WAVE_TILES
+    d = whtmix.plan_describe(3, 1024, 64, "bf16", "two_pass")
+    assert (d["plan"], d["kernels"], d["workspace_bytes"]) == ("two_pass", 2, 3 << 18)
+    assert (d["outer_bits"], d["run_bits"], d["module_outer_bits"]) == (9, 2, 11)
+    d = whtmix.plan_describe(5, 256, 128, plan="two_pass")
+    assert (d["plan"], d["outer_bits"], d["run_bits"], d["module_outer_bits"]) == \
+        ("two_pass", 9, 3, 0)
+    for B, N, C in [(1, 256, 64), (1, 128, 64), (1, 1024, 128), (1, 32767, 1)]:
+        with pytest.raises(whtmix.WhtmixError):
+            whtmix.plan_describe(B, N, C, plan="two_pass")   # K < 15, K > 16, N*C % 8
     # small batches of 2^15 and 2^16 slices: three launches of one-wave tiles
     for B, N, C, plan in [(1, 1024, 64, "wave_tiles"), (3, 1024, 64, "wave_tiles"),
-                          (4, 1024, 64, "three_pass"), (16, 512, 64, "wave_tiles"),
-                          (17, 512, 64, "fused"), (1, 32767, 1, "fused"),
+                          (4, 1024, 64, "three_pass"), (16, 512, 64, "two_pass"),
+                          (40, 512, 64, "two_pass"), (41, 512, 64, "fused"),
+                          (1, 32767, 1, "fused"),
                           (1, 65535, 1, "three_pass"), (2, 256, 64, "fused")]:
         assert whtmix.plan_describe(B, N, C)["plan"] == plan, (B, N, C)
     d = whtmix.plan_describe(1, 1024, 64)

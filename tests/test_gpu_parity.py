@@ -121,7 +121,7 @@ def test_random_shapes_every_plan(case, dev, orc):
     g = g.reshape(P, C)
     ref = orc.whtmix(x, g)
     plans = ["auto"]
-    for p in ("small", "fused", "three_pass", "wave_tiles", "one_launch"):
+    for p in ("small", "fused", "three_pass", "wave_tiles", "one_launch", "two_pass"):
         try:
             whtmix.plan_describe(B, N, C, dtype, p)
         except whtmix.WhtmixError:

@@ -4,6 +4,8 @@ the C ABI.
 Both run the mixer (section III-B, eqs. (2)-(3)) as three passes on one-wave
 2^9-element tiles whose butterflies stay in the wave: WAVE_TILES as three
 launches, ONE_LAUNCH in one cooperative launch ordered by per-slice counters.
+TWO_PASS (2^15- and 2^16-element slices) replaces the first two passes by a
+fold pass whose workgroups each read the whole slice.
 Checked here: parity at every supported slice size, batch counts from 1 to
 2046 (several tiles per workgroup when a single launch outgrows the resident
 grid), padded N, both dtypes, both gain forms, in place; back-to-back calls
@@ -80,7 +82,38 @@ def test_padded_tokens(shape, dtype, plan, dev, orc):
     check(f"{plan} padded", y, orc.whtmix(x, g), dtype)
 
 
-@pytest.mark.parametrize("plan", PLANS)
+TWO_PASS_SHAPES = [(3, 256, 128), (1, 512, 64), (1, 1024, 64), (2, 512, 128), (16, 1024, 64),
+                   (47, 512, 128), (1, 65536, 1), (1, 8, 8192), (300, 1024, 64),
+                   (1, 32768, 1), (5, 128, 256), (600, 256, 128)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", TWO_PASS_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_two_pass_parity(shape, dtype, dev, orc):
+    B, N, C = shape
+    say(f"two_pass B={B} N={N} C={C} {dtype}")
+    x, g = workloads.draw(B, N, C, dtype, seed=B * 1000 + N + C + 1)
+    y = run_gpu(x, g, dtype, dev, plan="two_pass")
+    check("two_pass", y, orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(1, 1000, 64), (3, 200, 128), (2, 300, 128), (1, 129, 256),
+                                   (2, 17, 2048), (1, 24584, 1)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_two_pass_padded_tokens(shape, dtype, dev, orc):
+    """The fold reads zeros for rows past N (whole 16-byte groups: N*C is a
+    multiple of 8); pass 3 stores only the valid rows."""
+    B, N, C = shape
+    say(f"two_pass padded B={B} N={N} C={C} {dtype}")
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=N + 1)
+    g = np.random.default_rng(N + 1).uniform(0.5, 1.5, (P, C)).astype(np.float32)
+    y = run_gpu(x, g, dtype, dev, plan="two_pass")
+    check("two_pass padded", y, orc.whtmix(x, g), dtype)
+
+
+@pytest.mark.parametrize("plan", PLANS + ["two_pass"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_separable(dtype, plan, dev, orc):
     B, N, C = 2, 1024, 64
@@ -91,7 +124,7 @@ def test_separable(dtype, plan, dev, orc):
     check(f"{plan} separable", y, orc.whtmix_separable(x, gt, gc), dtype)
 
 
-@pytest.mark.parametrize("plan", PLANS + ["auto"])
+@pytest.mark.parametrize("plan", PLANS + ["two_pass", "auto"])
 def test_image1k_workload(plan, dev, orc):
     """image1k_f32 (B=1, N=1024, C=64); AUTO takes WAVE_TILES for it."""
     w = workloads.WORKLOADS["image1k_f32"]
@@ -102,7 +135,7 @@ def test_image1k_workload(plan, dev, orc):
     check(f"image1k_f32 {plan}", y, orc.whtmix(x, g), w.dtype)
 
 
-@pytest.mark.parametrize("plan", PLANS)
+@pytest.mark.parametrize("plan", PLANS + ["two_pass"])
 def test_back_to_back_and_in_place(plan, dev, orc):
     """Consecutive calls on one stream reuse the counter block (each kernel
     returns it to zero); in place (y == x) reads every x before any y store

@@ -393,3 +393,165 @@ def test_wait_that_gives_up_still_drains_and_flags():
 
 def test_batch_limit_matches_counter_block():
     assert 2 * 2046 + 3 <= COUNTER_WORDS < 2 * 2047 + 3
+
+
+# ---------------------------------------------------------------- TWO_PASS
+def fold_pass(x, g, K, B, nvalid, ws, counts):
+    """The fold pass (fold_pass_kernel): workgroup (b, m) of 512 threads,
+    8 waves of 64 lanes x 8 registers, with the kernel's M1 / M2 layouts,
+    LDS addresses and workspace offsets.  Writes ws, counts every access."""
+    HB = K - TB
+    R, Q = TB - HB, 21 - K
+    A, LJ = TB - Q, Q - 2
+    W0 = 6 - LJ
+    t = np.arange(512)
+    j1, h1 = (t & ((1 << LJ) - 1)) << 2, t >> LJ
+    j2, h2 = t & ((1 << Q) - 1), t >> Q
+
+    def hi2(k):
+        return (h2 & ((1 << W0) - 1)) | (k << W0) | ((h2 >> W0) << (HB - 1))
+
+    def per_wave(v, fn):
+        w = v.reshape(NV, 8, LANES)
+        return np.stack([fn(w[:, i, :]) for i in range(8)], axis=1).reshape(NV, 512)
+
+    def lane_stage(v):
+        v = reg_bfly(reg_bfly(v, 0), 1)
+        for J in range(LJ):
+            v = lane_bfly(v, J)
+        return v
+
+    for b in range(B):
+        for m in range(1 << A):
+            gv = np.stack([g[(hi2(k) << TB) | (m << Q) | j2] for k in range(NV)]) * 2.0 ** -K
+            np.add.at(counts["g"], np.stack([(hi2(k) << TB) | (m << Q) | j2
+                                             for k in range(NV)]).ravel(), 1)
+            v = np.zeros((NV, 512))
+            for rr in range(2):
+                row = (h1 | (rr << (HB - 1))) << TB
+                for a in range(1 << A):
+                    s = -1.0 if bin(m & a).count("1") & 1 else 1.0
+                    i0 = row + (a << Q) + j1
+                    ok = i0 < nvalid                       # whole 4-groups (nvalid % 8 == 0)
+                    for e in range(4):
+                        idx = b * nvalid + i0 + e
+                        v[4 * rr + e, ok] += s * x[idx[ok]]
+                        np.add.at(counts["x"], idx[ok], 1)
+            v = per_wave(v, lane_stage)
+            v = per_wave(v, lambda w: wave_bfly(w, LJ))
+            lds = np.full(1 << (HB + Q), np.nan)
+            lds_w = np.zeros(lds.size, int)
+            for rr in range(2):
+                a0 = ((h1 | (rr << (HB - 1))) << Q) | j1
+                for wv in range(8):                        # a wave writes 1 KiB contiguous
+                    seg = a0[wv * 64:(wv + 1) * 64]
+                    assert np.array_equal(np.sort(seg), seg.min() + 4 * np.arange(64))
+                for e in range(4):
+                    lds[a0 + e] = v[4 * rr + e]
+                    np.add.at(lds_w, a0 + e, 1)
+            assert np.all(lds_w == 1)
+            addr2 = np.stack([(hi2(k) << Q) | j2 for k in range(NV)])
+            for k in range(NV):                            # 64 consecutive floats per wave
+                for wv in range(8):
+                    seg = addr2[k, wv * 64:(wv + 1) * 64]
+                    assert np.array_equal(np.sort(seg), seg.min() + np.arange(64))
+            assert np.array_equal(np.sort(addr2.ravel()), np.arange(lds.size))
+            u = lds[addr2]
+            u = reg_bfly(reg_bfly(reg_bfly(u, 0), 1), 2) * gv
+            u = reg_bfly(reg_bfly(reg_bfly(u, 0), 1), 2)
+            lds[addr2] = u
+            for rr in range(2):
+                a0 = ((h1 | (rr << (HB - 1))) << Q) | j1
+                for e in range(4):
+                    v[4 * rr + e] = lds[a0 + e]
+            v = per_wave(v, lambda w: wave_bfly(w, LJ))
+            t9 = (m << Q) | j1
+            dst = (b << K) + ((t9 >> R) << TB) + (t9 & ((1 << R) - 1))
+            for rr in range(2):
+                for e in range(4):
+                    off = dst + ((h1 | (rr << (HB - 1))) << R) + e
+                    assert off.min() >= b << K and off.max() < (b + 1) << K
+                    ws[off] = v[4 * rr + e]
+                    np.add.at(counts["ws"], off, 1)
+
+
+def run_two_pass(x, g, K, B, nvalid, layout):
+    HB = K - TB
+    R = TB - HB
+    ws = np.full(B << K, np.nan)
+    counts = {"x": np.zeros(B * nvalid, int), "g": np.zeros(1 << K, int),
+              "ws": np.zeros(B << K, int)}
+    fold_pass(x, g, K, B, nvalid, ws, counts)
+    assert np.all(counts["ws"] == 1)
+    assert np.all(counts["g"] == B)
+    # each workgroup reads its whole slice once
+    assert np.all(counts["x"] == 1 << (TB - (21 - K)))
+    y = np.full(B * nvalid, np.nan)
+    T_io = t_index(layout)
+    for b in range(B):                                   # pass 3, as in run_pipeline
+        for hi in range(1 << HB):
+            start = hi << TB
+            valid = max(0, min(nvalid - start, 512))
+            if valid == 0:
+                continue
+            v = wht9(ws[(b << K) + (hi << R) + run_off(T_io, R)])
+            ok = T_io < valid
+            y[b * nvalid + start + T_io[ok]] = v[ok]
+    return y
+
+
+@pytest.mark.parametrize("K,B,N,C,layout", [
+    (16, 1, 1024, 64, "V4"), (15, 2, 256, 128, "V8"), (16, 1, 1000, 64, "V4"),
+    (15, 1, 200, 128, "V4"), (16, 2, 512, 128, "V8"),
+])
+def test_two_pass_matches_oracle(K, B, N, C, layout):
+    """The fold pass then pass 3 reproduce the oracle (padded N included):
+    the fold's signs, H over j, the hi butterflies split between M1 and M2
+    and the run layout pass 3 gathers are all exercised."""
+    P = 1 << max(0, (N - 1).bit_length())
+    assert P * C == 1 << K
+    rng = np.random.default_rng(K * 10 + B + N)
+    x = rng.standard_normal((B, N, C))
+    g = rng.uniform(0.5, 1.5, (P, C))
+    y = run_two_pass(x.reshape(-1), g.reshape(-1), K, B, N * C, layout)
+    ref = oracle_mod.whtmix(x, g)
+    np.testing.assert_allclose(y.reshape(B, N, C), ref, rtol=0, atol=1e-9 * np.abs(ref).max())
+
+
+@pytest.mark.parametrize("K", [15, 16])
+def test_fold_workgroup_owns_whole_middle_tiles(K):
+    """Workgroup m writes t9 in [m*2^Q, (m+1)*2^Q): 2^(Q-R) = 8 whole runs
+    of pass 3's layout, i.e. 2^12 contiguous floats."""
+    HB, Q = K - TB, 21 - K
+    R = TB - HB
+    assert Q - R == 3 and HB + Q == 12
+    for m in range(1 << (TB - Q)):
+        t9 = (m << Q) + np.arange(1 << Q)
+        offs = np.concatenate([((t >> R) << TB) + (np.arange(1 << HB) << R) + (t & ((1 << R) - 1))
+                               for t in t9])
+        assert np.array_equal(np.sort(offs), (m << 12) + np.arange(1 << 12))
+
+
+@pytest.mark.parametrize("K", [15, 16])
+@pytest.mark.parametrize("B", [1, 3, 8, 13, 16, 47])
+def test_fold_blocks_cover_each_slice_on_one_xcd(K, B):
+    """fold_pass_kernel's block numbering: block i (on XCD i mod 8) takes
+    slice ((i >> (A+3)) << 3) | (i & 7) and part (i >> 3) mod 2^A; the grid is
+    B rounded up to 8 slices.  Every (slice, part) is taken once, the parts
+    of a slice share one XCD, and only blocks past the last slice idle."""
+    A = TB - (21 - K)
+    grid = ((B + 7) // 8) << (A + 3)
+    seen, xcd_of = {}, {}
+    idle = 0
+    for i in range(grid):
+        b = ((i >> (A + 3)) << 3) | (i & 7)
+        m = (i >> 3) & ((1 << A) - 1)
+        if b >= B:
+            idle += 1
+            continue
+        assert (b, m) not in seen
+        seen[(b, m)] = i
+        assert xcd_of.setdefault(b, i % 8) == i % 8
+    assert len(seen) == B << A
+    assert idle == grid - (B << A)
+    assert grid * 512 < 1 << 32
