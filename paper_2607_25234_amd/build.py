@@ -2,9 +2,11 @@
 
     python -m paper_2607_25234_amd.build
 
-Compiles every source under csrc/ with hipcc, one process per source in
-parallel, and links them into one shared library beside this file.  Packed
-FP32 instructions are disabled for all device code.
+Compiles every HIP / C++ source under csrc/ with hipcc, one process per
+source in parallel, and links them into one shared library beside this file.
+Packed FP32 instructions are disabled for all device code.  Then builds the
+binding's CPython call module (csrc/whtmix_pycall.c, host code only) with the
+host C compiler.
 """
 from __future__ import annotations
 
@@ -12,6 +14,7 @@ import glob
 import os
 import subprocess
 import sys
+import sysconfig
 import tempfile
 from concurrent.futures import ThreadPoolExecutor
 
@@ -20,6 +23,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwhtmix.so")
+PYCALL = os.path.join(HERE, "_whtmix_call" + sysconfig.get_config_var("EXT_SUFFIX"))
 ARCH = "gfx950"
 
 COMPILE_FLAGS = [
@@ -53,7 +57,17 @@ def _run(cmd: list[str], verbose: bool, what: str) -> None:
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed: {what}")
+        raise RuntimeError(f"{cmd[0]} failed: {what}")
+
+
+def build_pycall(out: str = PYCALL, verbose: bool = False) -> str:
+    """The CPython call module of the forward entry points (no HIP code)."""
+    cc = os.environ.get("CC", "gcc")
+    src = os.path.join(CSRC, "whtmix_pycall.c")
+    _run([cc, "-O2", "-shared", "-fPIC", "-Wall", "-Wextra", "-Werror",
+          f"-I{sysconfig.get_paths()['include']}", src, "-o", out + ".tmp"], verbose, src)
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def build(out: str = LIB, extra: tuple = (), verbose: bool = False, jobs: int = 0) -> str:
@@ -67,6 +81,8 @@ def build(out: str = LIB, extra: tuple = (), verbose: bool = False, jobs: int = 
             list(pool.map(lambda c: _run(c, verbose, c[-3]), cmds))
         _run([hipcc(), *LINK_FLAGS, *extra, *objs, "-o", out + ".tmp"], verbose, "link")
     os.replace(out + ".tmp", out)
+    if out == LIB:
+        build_pycall(verbose=verbose)
     return out
 
 

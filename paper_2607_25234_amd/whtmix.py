@@ -184,12 +184,44 @@ def plan_describe(B: int, N: int, C: int, dtype: str = "f32", plan: str | int = 
             "module_backward_fused": bool(info.module_backward_fused)}
 
 
+_call_mod = None
+
+
+def _call():
+    """The CPython call module of the forward entry points
+    (csrc/whtmix_pycall.c), bound to the functions of the loaded library.
+    It is built with the library; there is no fallback."""
+    global _call_mod
+    if _call_mod is None:
+        L = lib()
+        try:
+            from paper_2607_25234_amd import _whtmix_call as m
+        except ImportError as e:
+            raise ImportError("the binding's call module (_whtmix_call) is missing: build it "
+                              "with `python -m paper_2607_25234_amd.build`") from e
+        m.bind(ctypes.cast(L.whtmix_forward_ex, ctypes.c_void_p).value,
+               ctypes.cast(L.whtmix_forward_separable, ctypes.c_void_p).value)
+        _call_mod = m
+    return _call_mod
+
+
+def _opt_address(plan, events, spin_limit):
+    """(structure, address) of the options argument; (None, 0) for NULL.  The
+    caller keeps the structure alive across the call."""
+    if events is None and not spin_limit and (plan == "auto" or plan == 0):
+        return None, 0
+    o = _options(plan, events, spin_limit)
+    return o, ctypes.addressof(o)
+
+
 def forward_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
                 dtype: int, stream: int, plan: str | int = "auto", events=None,
                 spin_limit: int = 0) -> int:
     """Direct call of whtmix_forward_ex with integer pointers; returns the status."""
-    return lib().whtmix_forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream,
-                                   _opt_arg(plan, events, spin_limit))
+    o, addr = _opt_address(plan, events, spin_limit)
+    st = _call().forward_ex(x_ptr, gain_ptr, y_ptr, B, N, C, dtype, stream, addr)
+    del o
+    return st
 
 
 def forward_noalloc_raw(x_ptr: int, gain_ptr: int, y_ptr: int, B: int, N: int, C: int,
@@ -209,8 +241,10 @@ def forward_separable_raw(x_ptr: int, gt_ptr: int, gc_ptr: int, y_ptr: int, B: i
                           C: int, dtype: int, stream: int, plan: str | int = "auto",
                           events=None) -> int:
     """Direct call of whtmix_forward_separable; returns the status."""
-    return lib().whtmix_forward_separable(x_ptr, gt_ptr, gc_ptr, y_ptr, B, N, C, dtype, stream,
-                                          _opt_arg(plan, events))
+    o, addr = _opt_address(plan, events, 0)
+    st = _call().forward_separable(x_ptr, gt_ptr, gc_ptr, y_ptr, B, N, C, dtype, stream, addr)
+    del o
+    return st
 
 
 def _check(x, out):
@@ -251,8 +285,8 @@ def forward(x, gain, out=None, plan: str | int = "auto", stream=None, events=Non
     """y[b] = H_N (G o (H_N x[b] H_C)) H_C on the GPU (section III-B, eqs. (2)-(3)).
 
     x: torch tensor [B, N, C] or [N, C], float32 or bfloat16, on a ROCm device.
-    gain: float32 [N_pad, C] (N_pad = N rounded up to a power of two; the token
-    axis is zero-padded) on the same device.  out: optional tensor like x (may
+    gain: float32 [N_pad, C] (N_pad = N rounded up to a power of two; rows past
+    N count as zeros) on the same device.  out: optional tensor like x (may
     be x itself for in-place).  stream: a torch.cuda.Stream (default: the
     current stream)."""
     import torch

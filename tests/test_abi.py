@@ -253,6 +253,35 @@ def test_default_options_pass_null():
     assert call(C=12) == 2 and call(C=12, plan=3) == 2
 
 
+def test_call_module_marshals_only():
+    """The forward entry points go through the binding's CPython call module,
+    bound to the same library functions ctypes sees; its argument checks
+    mirror ctypes' (ints or None for pointers) and every status comes from
+    the library."""
+    m = whtmix._call()
+    L = whtmix.lib()
+    assert whtmix._opt_address("auto", None, 0) == (None, 0)
+    o, addr = whtmix._opt_address("three_pass", None, 0)
+    assert addr == ctypes.addressof(o) and o.plan == whtmix.PLANS["three_pass"]
+    # identical statuses through both routes, for defaults and forced plans
+    for args in [(0, 0, 0, 1, 64, 64, 0, 0), (ALIGNED, ALIGNED2, ALIGNED, 1, 64, 12, 0, 0),
+                 (ALIGNED, ALIGNED2, ALIGNED, 1, 64, 64, 9, 0),
+                 (ALIGNED + 4, ALIGNED2, ALIGNED2 * 2, 1, 64, 64, 0, 0)]:
+        assert m.forward_ex(*args, 0) == L.whtmix_forward_ex(*args, None)
+        assert m.forward_ex(*args, None) == L.whtmix_forward_ex(*args, None)
+    o, addr = whtmix._opt_address(9, None, 0)     # an invalid plan, in the structure
+    assert m.forward_ex(ALIGNED, ALIGNED2, ALIGNED, 1, 64, 64, 0, 0, addr) == 1
+    assert m.forward_separable(0, 0, 0, 0, 1, 64, 64, 0, 0, 0) == 1
+    with pytest.raises(TypeError):
+        m.forward_ex(1.5, 0, 0, 1, 64, 64, 0, 0, 0)
+    with pytest.raises(TypeError):
+        m.forward_ex(0, 0, 0, 1, 64, 64, 0, 0)          # 8 arguments
+    with pytest.raises(OverflowError):
+        m.forward_ex(0, 0, 0, 1 << 64, 64, 64, 0, 0, 0)
+    with pytest.raises(OverflowError):
+        m.forward_ex(0, 0, 0, 1, 64, 64, 1 << 40, 0, 0)
+
+
 def test_plan_table():
     d = whtmix.plan_describe(1, 1, 1)
     assert d["plan"] == "small" and d["kernels"] == 1 and d["workspace_bytes"] == 0
