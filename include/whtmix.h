@@ -187,8 +187,8 @@ WHTMIX_API int whtmix_forward(const void *x, const float *gain, void *y,
  * whtmix_forward_noalloc -- whtmix_forward for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid hipMalloc).  Same arguments, result, plan (AUTO) and checks as
- * whtmix_forward, but the workspace of the three-pass and wave-tile plans is a fixed 32 MiB device array
- * inside the library (one per device, held until the process ends) instead
+ * whtmix_forward, but the workspace of the three-pass, two-pass and wave-tile
+ * plans is a fixed 32 MiB device array inside the library (one per device, held until the process ends) instead
  * of the per-stream workspace, and the call allocates nothing: no hipMalloc,
  * no hipFree, no stream synchronisation.  Limit: shapes whose plan needs a
  * workspace must have B * N_pad * C <= 2^23; larger ones return

@@ -1,5 +1,5 @@
 // Fixed device scratch for whtmix_forward_noalloc: the float32 workspace of
-// the three-pass and wave-tile plans in a file-scope device array, so that the call makes
+// the three-pass, two-pass and wave-tile plans in a file-scope device array, so that the call makes
 // no allocation (for callers that cannot allocate: code under HIP graph
 // capture, tight serving loops).
 //
@@ -7,8 +7,8 @@
 // array's device address comes from hipGetSymbolAddress, once per device
 // (each device holds its own copy at its own address), and only that
 // address is ever passed to kernels.  Every call on a device shares its
-// array: calls that overlap on one device race.  Both plans write
-// every workspace element before reading it, so nothing needs clearing.
+// array: calls that overlap on one device race.  Each plan writes every
+// workspace element before reading it, so nothing needs clearing.
 #include <hip/hip_runtime.h>
 
 #include <map>

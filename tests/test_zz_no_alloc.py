@@ -1,5 +1,5 @@
 """whtmix_forward_noalloc (the entry point that allocates nothing, its
-three-pass workspace in a fixed device array) against whtmix_forward,
+three-pass, two-pass or wave-tile workspace in a fixed device array) against whtmix_forward,
 through the C ABI: two calls in a row, the second with a smaller input.
 Both run the same kernels, so the outputs agree bit for bit; each is also
 held to the oracle's bar.
@@ -36,11 +36,12 @@ def _run(entry, x, g, dtype, dev):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_noalloc_matches_forward_twice(dtype):
     """The first call fills the scratch (2^23 floats), the second, smaller one
-    reuses it, the third runs the wave-tile plan in it; a FUSED-plan call
-    needs no scratch at all."""
+    reuses it, the third runs the wave-tile plan in it and the fourth the
+    two-pass plan; a FUSED-plan call needs no scratch at all."""
     dev = device()
     orc = oracle_mod.Oracle()
-    for i, (B, N, C) in enumerate([(4, 16384, 128), (3, 4096, 64), (1, 1024, 64), (2, 256, 64)]):
+    for i, (B, N, C) in enumerate([(4, 16384, 128), (3, 4096, 64), (1, 1024, 64), (5, 512, 64),
+                                   (2, 256, 64)]):
         say(f"noalloc call {i}: B={B} N={N} C={C} {dtype} "
             f"plan={whtmix.plan_describe(B, N, C, dtype)['plan']}")
         x, g = workloads.draw(B, N, C, dtype, seed=900 + i)
