@@ -781,24 +781,28 @@ int whtmix_stream_status(void *stream)
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    uint32_t *ctr = nullptr;
-    {
-        std::lock_guard<std::mutex> lock(g_ws_mutex);
-        auto it = g_ws.find({dev, stream});
-        if (it != g_ws.end()) ctr = it->second.ctr;
-    }
     e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    // Held while the error word is read and cleared, so that a concurrent
+    // whtmix_release_workspaces cannot free the counter block meanwhile.
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    auto it = g_ws.find({dev, stream});
+    uint32_t *ctr = it != g_ws.end() ? it->second.ctr : nullptr;
     if (!ctr) return WHTMIX_SUCCESS;
     // The sticky error word is the block's last word.
     uint32_t *sticky = ctr + whtmix::kCounterWords - 1;
+    // Copies on the (idle) stream itself: the lock is not held across a
+    // device-wide synchronisation.
+    const hipStream_t st = static_cast<hipStream_t>(stream);
     uint32_t v = 0;
-    e = hipMemcpy(&v, sticky, sizeof(v), hipMemcpyDeviceToHost);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the error word");
+    e = hipMemcpyAsync(&v, sticky, sizeof(v), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "copy of the error word");
     if (v == 0) return WHTMIX_SUCCESS;
     const uint32_t zero = 0;
-    e = hipMemcpy(sticky, &zero, sizeof(zero), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the error word");
+    e = hipMemcpyAsync(sticky, &zero, sizeof(zero), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "copy of the error word");
     return WHTMIX_ERROR_DEVICE_TIMEOUT;
 }
 
