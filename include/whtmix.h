@@ -82,9 +82,10 @@ typedef enum whtmix_status {
 /* Execution plans.  AUTO picks by the padded slice size L = N_pad*C:
  *   L <= 2^10          one small workgroup per slice, all stages in LDS;
  *   2^11 <= L <= 2^15  FUSED: one workgroup per slice, a single pass; for
- *                      L = 2^15 up to 40 slices TWO_PASS instead;
- *   L = 2^16           WAVE_TILES up to 3 slices, FUSED (two register sets)
- *                      from 48 slices, THREE_PASS between;
+ *                      L = 2^15 up to 48 slices TWO_PASS instead;
+ *   L = 2^16           WAVE_TILES up to 3 slices, TWO_PASS from 4 to 16,
+ *                      FUSED (two register sets) from 48 slices, THREE_PASS
+ *                      between;
  *   L >= 2^17          THREE_PASS: forward over the low bits of the flat
  *                      index, then forward over the high bits + gain +
  *                      inverse over the high bits, then inverse over the low

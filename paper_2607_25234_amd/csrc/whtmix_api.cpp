@@ -96,6 +96,8 @@ int check_shape(int64_t B, int64_t N, int64_t C, int dtype, const whtmix_options
                : K == whtmix::kMaxFused && B >= whtmix::kFusedPairMinBatch ? whtmix::PLAN_FUSED
                : K == whtmix::kMaxFused && wave_ok && B <= whtmix::kWave16MaxBatch
                    ? whtmix::PLAN_WAVE_TILES
+               : K == whtmix::kMaxFused && wave_ok && B <= whtmix::kTwoPass16MaxBatch
+                   ? whtmix::PLAN_TWO_PASS
                    : whtmix::PLAN_THREE_PASS;
         break;
     case whtmix::PLAN_WAVE_TILES:

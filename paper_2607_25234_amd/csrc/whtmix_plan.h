@@ -47,12 +47,15 @@ constexpr int kWaveMaxK = 16;
 constexpr int kWave16MaxBatch = 3;
 // TWO_PASS (whtmix_wave.hip): a fold pass in place of passes 1 and 2, then
 // pass 3; slices of 2^15 and 2^16 elements.  AUTO takes it for 2^15-element
-// slices up to 40 (one launch fewer than WAVE_TILES, and from 17 slices
-// faster than one workgroup per slice until about 48).  For 2^16 slices each
-// fold workgroup reads 256 KiB (float32) and, with x arriving from memory,
-// the pass loses the launch it saves, so AUTO keeps WAVE_TILES there.
+// slices up to 48 (one launch fewer than WAVE_TILES, and from 17 slices
+// faster than one workgroup per slice until about 48) and for 2^16-element
+// slices from 4 (after WAVE_TILES) up to 16 (then THREE_PASS): measured
+// faster there with x in cache and with x from memory.  Up to 3 slices of
+// 2^16 a fold workgroup's 256 KiB read (float32) from memory costs about the
+// launch it saves.
 constexpr int kTwoPassMinK = 15;
-constexpr int kTwoPass15MaxBatch = 40;
+constexpr int kTwoPass15MaxBatch = 48;
+constexpr int kTwoPass16MaxBatch = 16;
 constexpr int kCounterWords = 4096;
 constexpr int kOneLaunchMaxBatch = (kCounterWords - 3) / 2;
 // Polls of a ONE_LAUNCH wait before it gives up (about a second or two).

@@ -288,7 +288,7 @@ def test_plan_table():
     assert whtmix.plan_describe(3, 32, 32)["plan"] == "small"
     assert whtmix.plan_describe(3, 32, 64)["plan"] == "fused"
     assert whtmix.plan_describe(3, 256, 64)["plan"] == "fused"
-    assert whtmix.plan_describe(3, 256, 128)["plan"] == "two_pass"   # 2^15, up to 40 slices
+    assert whtmix.plan_describe(3, 256, 128)["plan"] == "two_pass"   # 2^15, up to 48 slices
     d = whtmix.plan_describe(3, 1024, 128, "bf16")
     assert d["plan"] == "three_pass" and d["kernels"] == 3
     assert d["workspace_bytes"] == 3 * 1024 * 128 * 4
@@ -314,8 +314,9 @@ def test_plan_table():
             whtmix.plan_describe(B, N, C, plan="two_pass")   # K < 15, K > 16, N*C % 8
     # small batches of 2^15 and 2^16 slices: three launches of one-wave tiles
     for B, N, C, plan in [(1, 1024, 64, "wave_tiles"), (3, 1024, 64, "wave_tiles"),
-                          (4, 1024, 64, "three_pass"), (16, 512, 64, "two_pass"),
-                          (40, 512, 64, "two_pass"), (41, 512, 64, "fused"),
+                          (4, 1024, 64, "two_pass"), (16, 1024, 64, "two_pass"),
+                          (17, 1024, 64, "three_pass"), (16, 512, 64, "two_pass"),
+                          (48, 512, 64, "two_pass"), (49, 512, 64, "fused"),
                           (1, 32767, 1, "fused"),
                           (1, 65535, 1, "three_pass"), (2, 256, 64, "fused")]:
         assert whtmix.plan_describe(B, N, C)["plan"] == plan, (B, N, C)
