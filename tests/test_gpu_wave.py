@@ -113,6 +113,20 @@ def test_two_pass_padded_tokens(shape, dtype, dev, orc):
     check("two_pass padded", y, orc.whtmix(x, g), dtype)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(3, 200, 128), (9, 1000, 64)], ids=lambda s: "x".join(map(str, s)))
+def test_two_pass_separable_padded(shape, dtype, dev, orc):
+    """The fold forms exp(g_t[n] + g_c[c]) for all N_pad token frequencies,
+    padded rows included; with 9 slices the last group of eight slices has
+    seven slices' blocks idle."""
+    B, N, C = shape
+    say(f"two_pass separable padded B={B} N={N} C={C} {dtype}")
+    x, _ = workloads.draw(B, N, C, dtype, seed=N + 3)
+    gt, gc = workloads.draw_log_gains(whtmix.padded_tokens(N), C, seed=N + 4)
+    y = run_gpu_separable(x, gt, gc, dtype, dev, plan="two_pass")
+    check("two_pass separable padded", y, orc.whtmix_separable(x, gt, gc), dtype)
+
+
 @pytest.mark.parametrize("plan", PLANS + ["two_pass"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_separable(dtype, plan, dev, orc):
