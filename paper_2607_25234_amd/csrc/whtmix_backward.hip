@@ -336,7 +336,8 @@ __device__ __forceinline__ void block_sum_256(float *red)
 // covers rows [rblk*RB, ...) and columns [strip*256, ...).  With C <= 256 the
 // 256 threads hold 256/C rows of the C columns per step and their sums per
 // column are added in LDS; with C > 256 each thread owns one column of the
-// strip.  part[rblk][c] receives the block's sums.
+// strip.  part[c][rblk] receives the block's sums (column-major, so that
+// the final sum over row blocks reads each column contiguously).
 __global__ void __launch_bounds__(256)
 sep_cols_partial_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
                         const float *__restrict__ gc, float *__restrict__ part, uint32_t P,
@@ -368,16 +369,20 @@ sep_cols_partial_kernel(const float *__restrict__ dG, const float *__restrict__ 
         }
     }
     if (tid < cw)
-        part[(size_t)blockIdx.x * C + c] = red[tid];
+        part[(size_t)c * gridDim.x + blockIdx.x] = red[tid];
 }
 
 // Row sums (dg_t) and column partial sums of dG*G in one pass over dG, for
 // C = 2^CB <= 256.  Block blockIdx.x covers rows [r0, r0 + rows_per_block);
-// each step a wave takes RPW = 64 / SEG rows, a row's C columns spread over
-// SEG = min(C, 64) lanes (KPL = C / SEG columns each), so a row sum is a
-// segmented wave reduction and needs no LDS.  Each exp is taken once.  The
-// column sums of a wave's RPW rows are added across the wave, then over the
-// four waves in LDS: part[blockIdx.x][c], fixed order throughout.
+// a row's C columns spread over SEG = min(C, 64) lanes, KPL = C / SEG
+// consecutive columns each (one 4-, 8- or 16-byte load), so a wave takes
+// RPW = 64 / SEG rows at a time and a row sum is a segmented wave reduction
+// with no LDS.  Each iteration issues the loads of U such row steps (the
+// block's four waves interleaved) before using any: rows past the block
+// load its last row again and add nothing, so no load sits in a branch that
+// would make the wave wait for it.  Each exp is taken once.  The column sums
+// of a wave's rows are added across the wave, then over the four waves in
+// LDS: part[c][blockIdx.x] (column-major), fixed order throughout.
 template <int CB>
 __global__ void __launch_bounds__(256)
 sep_rows_cols_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
@@ -388,36 +393,52 @@ sep_rows_cols_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
     constexpr uint32_t SEG = C < 64u ? C : 64u;
     constexpr uint32_t RPW = 64u / SEG;
     constexpr uint32_t KPL = C / SEG;
+    constexpr uint32_t U = 4;
+    typedef float fvec __attribute__((ext_vector_type(KPL)));
     __shared__ float red[4][C];
     const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
-    const uint32_t c0 = lane & (SEG - 1u);
+    const uint32_t c0 = (lane & (SEG - 1u)) * KPL;   // first of the lane's KPL columns
     const uint32_t rw = lane / SEG;
     const uint32_t r0 = blockIdx.x * rows_per_block;
-    const uint32_t r1 = min(r0 + rows_per_block, P);
+    const uint32_t r1 = min(r0 + rows_per_block, P);   // > r0: the grid covers P rows
     float gcv[KPL], cs[KPL];
 #pragma unroll
     for (uint32_t k = 0; k < KPL; ++k) {
-        gcv[k] = gc[c0 + SEG * k];
+        gcv[k] = gc[c0 + k];
         cs[k] = 0.0f;
     }
-    for (uint32_t rb = r0; rb < r1; rb += 4u * RPW) {   // uniform over the block
-        const uint32_t r = rb + wave * RPW + rw;
-        float rs = 0.0f;
-        if (r < r1) {
-            const float g = gt[r];
-            const float *d = dG + (size_t)r * C;
+    for (uint32_t rb = r0; rb < r1; rb += U * 4u * RPW) {   // uniform over the block
+        float v[U][KPL], g[U];
 #pragma unroll
-            for (uint32_t k = 0; k < KPL; ++k) {
-                const float p = d[c0 + SEG * k] * __expf(g + gcv[k]);
-                cs[k] += p;
-                rs += p;
+        for (uint32_t u = 0; u < U; ++u) {
+            const uint32_t r = min(rb + (u * 4u + wave) * RPW + rw, r1 - 1u);
+            g[u] = gt[r];
+            if constexpr (KPL == 1) {
+                v[u][0] = dG[(size_t)r * C + c0];
+            } else {
+                const fvec q = *reinterpret_cast<const fvec *>(dG + (size_t)r * C + c0);
+#pragma unroll
+                for (uint32_t k = 0; k < KPL; ++k)
+                    v[u][k] = q[k];
             }
         }
 #pragma unroll
-        for (uint32_t off = SEG >> 1; off > 0; off >>= 1)
-            rs += __shfl_xor(rs, off, 64);
-        if (c0 == 0 && r < r1)
-            dgt[r] = rs;
+        for (uint32_t u = 0; u < U; ++u) {
+            const uint32_t r = rb + (u * 4u + wave) * RPW + rw;
+            const bool live = r < r1;
+            float rs = 0.0f;
+#pragma unroll
+            for (uint32_t k = 0; k < KPL; ++k) {
+                const float p = live ? v[u][k] * __expf(g[u] + gcv[k]) : 0.0f;
+                cs[k] += p;
+                rs += p;
+            }
+#pragma unroll
+            for (uint32_t off = SEG >> 1; off > 0; off >>= 1)
+                rs += __shfl_xor(rs, off, 64);
+            if ((lane & (SEG - 1u)) == 0 && live)
+                dgt[r] = rs;
+        }
     }
 #pragma unroll
     for (uint32_t k = 0; k < KPL; ++k) {
@@ -426,24 +447,25 @@ sep_rows_cols_kernel(const float *__restrict__ dG, const float *__restrict__ gt,
         for (uint32_t off = SEG; off < 64u; off <<= 1)
             t += __shfl_xor(t, off, 64);
         if (rw == 0)
-            red[wave][c0 + SEG * k] = t;
+            red[wave][c0 + k] = t;
     }
     __syncthreads();
     for (uint32_t c = threadIdx.x; c < C; c += 256u)
-        part[(size_t)blockIdx.x * C + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+        part[(size_t)c * gridDim.x + blockIdx.x] =
+            ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
 }
 
-// dgc[c] = sum over row blocks of part[b][c]: one block per column, 256-way
-// strided sums then a fixed-order tree.
+// dgc[c] = sum over row blocks of part[c][b] (column-major: each block
+// reads its column contiguously): one block per column, 256-way strided sums
+// then a fixed-order tree.
 __global__ void __launch_bounds__(256)
-sep_cols_final_kernel(const float *__restrict__ part, float *__restrict__ dgc, uint32_t nblk,
-                      uint32_t C)
+sep_cols_final_kernel(const float *__restrict__ part, float *__restrict__ dgc, uint32_t nblk)
 {
     __shared__ float red[256];
     const uint32_t c = blockIdx.x;
     float s = 0.0f;
     for (uint32_t b = threadIdx.x; b < nblk; b += 256)
-        s += part[(size_t)b * C + c];
+        s += part[(size_t)c * nblk + b];
     red[threadIdx.x] = s;
     block_sum_256(red);
     if (threadIdx.x == 0)
@@ -625,7 +647,7 @@ hipError_t separable_reductions(const BackwardArgs &a, const BackwardLayout &lay
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(sep_cols_final_kernel, dim3(C), dim3(256), 0, st, a.ws + lay.colpart,
-                       a.dgc, lay.col_blocks, C);
+                       a.dgc, lay.col_blocks);
     return hipGetLastError();
 }
 

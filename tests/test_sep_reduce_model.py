@@ -6,7 +6,11 @@ import numpy as np
 import pytest
 
 
-def sep_rows_cols_model(dG, G, rows_per_block):
+def sep_rows_cols_model(dG, G, rows_per_block, U=4):
+    """Lane l of wave w holds columns (l mod SEG)*KPL + [0, KPL) of row
+    rb + (u*4 + w)*RPW + l // SEG in step u of the iteration at rb (U steps
+    per iteration, the block's four waves interleaved); a row past the block
+    is loaded as the block's last row and adds nothing."""
     P, C = dG.shape
     SEG = min(C, 64)
     RPW = 64 // SEG
@@ -14,33 +18,38 @@ def sep_rows_cols_model(dG, G, rows_per_block):
     nblk = -(-P // rows_per_block)
     seen = np.zeros((P, C), int)
     dgt = np.full(P, np.nan)
-    part = np.zeros((nblk, C))
+    part = np.zeros((C, nblk))                            # column-major, as stored
     for blk in range(nblk):
         r0, r1 = blk * rows_per_block, min((blk + 1) * rows_per_block, P)
+        assert r1 > r0
         red = np.zeros((4, C))
         for wave in range(4):
             cs = np.zeros((64, KPL))
-            for rb in range(r0, r1, 4 * RPW):
-                rs = np.zeros(64)
-                for lane in range(64):
-                    r = rb + wave * RPW + lane // SEG
-                    if r >= r1:
-                        continue
-                    for k in range(KPL):
-                        c = lane % SEG + SEG * k
-                        p = dG[r, c] * G[r, c]
-                        seen[r, c] += 1
-                        cs[lane, k] += p
-                        rs[lane] += p
-                for lane in range(0, 64, SEG):          # segmented reduction
-                    r = rb + wave * RPW + lane // SEG
-                    if r < r1:
-                        dgt[r] = rs[lane:lane + SEG].sum()
+            for rb in range(r0, r1, U * 4 * RPW):
+                for u in range(U):
+                    rs = np.zeros(64)
+                    for lane in range(64):
+                        r = rb + (u * 4 + wave) * RPW + lane // SEG
+                        rl = min(r, r1 - 1)               # the load's row, always in range
+                        assert r0 <= rl < r1
+                        for k in range(KPL):
+                            c = (lane % SEG) * KPL + k
+                            assert 0 <= c < C
+                            if r >= r1:
+                                continue
+                            p = dG[r, c] * G[r, c]
+                            seen[r, c] += 1
+                            cs[lane, k] += p
+                            rs[lane] += p
+                    for lane in range(0, 64, SEG):          # segmented reduction
+                        r = rb + (u * 4 + wave) * RPW + lane // SEG
+                        if r < r1:
+                            dgt[r] = rs[lane:lane + SEG].sum()
             for lane in range(SEG):                      # rows of the wave, then waves
                 for k in range(KPL):
-                    red[wave, lane + SEG * k] = cs[lane::SEG, k].sum()
-        part[blk] = red.sum(axis=0)
-    return dgt, part, seen
+                    red[wave, lane * KPL + k] = cs[lane::SEG, k].sum()
+        part[:, blk] = red.sum(axis=0)
+    return dgt, part.T, seen
 
 
 @pytest.mark.parametrize("C", [1, 2, 16, 32, 64, 128, 256])
