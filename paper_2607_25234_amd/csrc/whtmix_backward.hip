@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "whtmix_launch.h"
 #include "whtmix_plan.h"
 #include "whtmix_tile.h"
@@ -68,6 +70,59 @@ grad_middle_kernel(const float *__restrict__ wsx, const float *__restrict__ wsd,
         o[Gain::at((uint32_t)k << G::SL)] = acc[k] * scale;
 }
 
+// The separable log-gain gradients' partial sums over one middle tile
+// (f = hi * 2^A + run * 2^R + e), p = dG * G in layout R = 5 (register k holds
+// hi bits 0-4, lane bits 0-4 hold e, the thread's higher bits hi bits 5 and
+// up).  With R <= log2 C = cbits <= A, e is channel bits 0-4, the run's low
+// qb = cbits - 5 bits are the channel group q, and a row hi of the tile is
+// one token n = f >> cbits.  p goes through the tile's LDS in natural [hi][e]
+// order (the exchanges are over), then
+//   rows: thread tau adds row hi = tau's 32 elements, stored contiguously per
+//         workgroup to rowpart[chunk][q][run >> qb][hi]
+//         (sep_fused_final_kernel puts the rows in token order);
+//   columns: thread tau adds column e = tau mod 32 over 32 rows, the groups
+//         are added in `red`, to colpart[c][chunk][run >> qb].
+// Fixed order throughout; registers stay as few as for storing dG.
+template <int A, int HB, int R>
+__device__ __forceinline__ void sep_tile_sums(const float (&p)[V], float *lds, float *red,
+                                              uint32_t tau, uint32_t run, uint32_t chunk,
+                                              uint32_t nchunks, uint32_t cbits,
+                                              float *__restrict__ rowpart,
+                                              float *__restrict__ colpart)
+{
+    constexpr uint32_t NG = 1u << (HB - 5);   // groups of 32 rows
+    const uint32_t qb = cbits - R;
+    const uint32_t q = run & ((1u << qb) - 1u);
+    const uint32_t base = layout_base<R>(tau);
+    __syncthreads();   // every thread's last reads of the tile exchanges are done
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pad(base + ((uint32_t)k << R))] = p[k];
+    __syncthreads();
+    float rs = 0.0f;
+#pragma unroll
+    for (uint32_t e = 0; e < 32u; ++e)
+        rs += lds[pad((tau << R) + e)];
+    const size_t rblock = ((size_t)((chunk << qb) | q) << (A - cbits)) | (run >> qb);
+    rowpart[(rblock << HB) + tau] = rs;
+    float cs = 0.0f;
+    const uint32_t g = tau >> 5, e = tau & 31u;
+#pragma unroll
+    for (uint32_t i = 0; i < 32u; ++i)
+        cs += lds[pad((((g << 5) + i) << R) + e)];
+    red[g * 32u + e] = cs;
+    __syncthreads();
+    if (tau < 32u) {
+        float t = 0.0f;
+#pragma unroll
+        for (uint32_t w = 0; w < NG; ++w)
+            t += red[w * 32u + tau];
+        const uint32_t c = (q << R) | tau;
+        const uint32_t np = nchunks << (A - cbits);
+        colpart[(size_t)c * np + ((chunk << (A - cbits)) | (run >> qb))] = t;
+    }
+}
+
 // Three-pass dG and dX together.  After OUTER_FWD of x and dy (one launch),
 // one workgroup owns one workspace run for a chunk of slices.  For each slice
 // it transforms both tiles over the HB high bits, so both are now transformed
@@ -88,10 +143,16 @@ grad_middle_kernel(const float *__restrict__ wsx, const float *__restrict__ wsd,
 // MIX_X: x's tile also goes through the gain and the inverse and is stored
 // back to wsx (the forward mixer's middle pass on x, for the block's backward,
 // which needs Z' as well), after the product and before the next slice's load.
-template <int A, int HB, int R, class Gain, bool SINGLE, bool MIX_X = false>
+//
+// SEPSUM (separable gains, several slices per chunk form, R = 5, HB >= 6,
+// R <= log2 C <= A): instead of storing dG the workgroup forms the two
+// log-gain gradients' partial sums of p = dG * G over its tile
+// (sep_tile_sums) and writes them to rowpart / colpart.
+template <int A, int HB, int R, class Gain, bool SINGLE, bool MIX_X = false, bool SEPSUM = false>
 __global__ void __launch_bounds__(1 << (HB + R - VB))
 grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain gain,
-                       float *__restrict__ out, uint32_t nslices, uint32_t per_chunk)
+                       float *__restrict__ out, uint32_t nslices, uint32_t per_chunk,
+                       float *__restrict__ rowpart, float *__restrict__ colpart, uint32_t cbits)
 {
     constexpr int M = HB + R;
     using G = Groups<M, R>;
@@ -106,8 +167,11 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
     const auto tile = [&](const float *ws, uint32_t b) {
         return buffer(ws + ((size_t)b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
     };
-    float *o = out + ((size_t)chunk << (A + HB)) + ((size_t)run << R) +
-               GM::at(layout_base<G::SL>(tau));
+    static_assert(!SEPSUM || (!SINGLE && R == VB && G::SL == R && HB >= 6),
+                  "the fused separable sums take the product in layout R = 5");
+    float *o = SEPSUM ? out
+                      : out + ((size_t)chunk << (A + HB)) + ((size_t)run << R) +
+                            GM::at(layout_base<G::SL>(tau));
     float vx[V], vd[V];
     load_layout<G::TOP, ContigMap, float>(vx, tile(wsx, b0), tau);
     load_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b0), tau);
@@ -166,9 +230,19 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
             if (more)
                 load_layout<G::TOP, ContigMap, float>(vd, tile(wsd, b + 1), tau);
         }
+        if constexpr (SEPSUM) {
+            float p[V];
 #pragma unroll
-        for (int k = 0; k < V; ++k)
-            o[GM::at((uint32_t)k << G::SL)] = acc[k] * scale;
+            for (int k = 0; k < V; ++k)
+                p[k] = acc[k] * scale * gv[k];
+            __shared__ float red[32u << (HB > 5 ? HB - 5 : 0)];
+            sep_tile_sums<A, HB, R>(p, lds, red, tau, run, chunk, gridDim.x >> (A - R), cbits,
+                                    rowpart, colpart);
+        } else {
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                o[GM::at((uint32_t)k << G::SL)] = acc[k] * scale;
+        }
     }
 }
 
@@ -472,6 +546,36 @@ sep_cols_final_kernel(const float *__restrict__ part, float *__restrict__ dgc, u
         dgc[c] = red[0];
 }
 
+// The fused separable sums' last step: blocks [0, nrowblk) give the row
+// sums, i = rl * 2^HB + hi of rowpart[j][rl][hi] (j = chunk * Q + q, nq of
+// them) going to token n = hi * 2^(A - cbits) + rl; the next C blocks
+// dgc[c] = sum over colpart[c][0 .. np).  Fixed order.
+__global__ void __launch_bounds__(256)
+sep_fused_final_kernel(const float *__restrict__ rowpart, const float *__restrict__ colpart,
+                       float *__restrict__ dgt, float *__restrict__ dgc, uint32_t P, uint32_t nq,
+                       uint32_t np, uint32_t nrowblk, uint32_t hb, uint32_t rlbits)
+{
+    __shared__ float red[256];
+    if (blockIdx.x < nrowblk) {   // uniform per block
+        const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+        if (i < P) {
+            float s = 0.0f;
+            for (uint32_t j = 0; j < nq; ++j)
+                s += rowpart[(size_t)j * P + i];
+            dgt[((i & ((1u << hb) - 1u)) << rlbits) | (i >> hb)] = s;
+        }
+        return;
+    }
+    const uint32_t c = blockIdx.x - nrowblk;
+    float s = 0.0f;
+    for (uint32_t b = threadIdx.x; b < np; b += 256u)
+        s += colpart[(size_t)c * np + b];
+    red[threadIdx.x] = s;
+    block_sum_256(red);
+    if (threadIdx.x == 0)
+        dgc[c] = red[0];
+}
+
 inline hipError_t record(hipEvent_t ev, hipStream_t st)
 {
     return ev ? hipEventRecord(ev, st) : hipSuccess;
@@ -599,6 +703,23 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
         lay.colpart = cursor;
         cursor += (uint64_t)lay.col_blocks * (uint64_t)C;
     }
+    int cbits = 0;
+    while ((int64_t(1) << cbits) < C) ++cbits;
+    if (separable && plan == PLAN_THREE_PASS) {
+        // where the middle pass can, it forms the partial sums itself
+        // (grad_mix_middle_kernel SEPSUM; the paths that store dG use the
+        // regions above): rows [chunk][C / 2^R][P], columns
+        // [C][chunk][2^(A - cbits)]
+        const Split sp = three_pass_split(K);
+        if (sp.R == VB && sp.HB >= 6 && sp.HB + sp.R < kMaxTile && cbits >= sp.R &&
+            cbits <= sp.A) {
+            lay.sep_fused = 1;
+            lay.rowpart = cursor;
+            cursor += (uint64_t)lay.nchunks * (L >> sp.R);
+            lay.fcolpart = cursor;
+            cursor += (uint64_t)C * ((uint64_t)lay.nchunks << (sp.A - cbits));
+        }
+    }
     // The dX pass runs after dG and reuses the start of the workspace.
     const uint64_t fwd = plan == PLAN_THREE_PASS ? (uint64_t)B * L : 0;
     lay.floats = cursor > fwd ? cursor : fwd;
@@ -675,12 +796,32 @@ hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, f
     float *wsx = a.ws + lay.wsx;
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
+    if constexpr (std::is_same_v<Gain, LogSeparableGain> && R == VB && HB >= 6 &&
+                  HB + R < kMaxTile) {
+        if (lay.sep_fused) {
+            // the middle pass forms the row and column partial sums of dG * G
+            // (any slices per chunk), then one small kernel adds them up
+            hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false, MIX_X, true>),
+                               dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
+                               wsx, wsd, gain, nullptr, (uint32_t)a.B, lay.per_chunk,
+                               a.ws + lay.rowpart, a.ws + lay.fcolpart, (uint32_t)a.cbits);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            const uint32_t P = (uint32_t)((uint64_t(1) << K) >> a.cbits);
+            const uint32_t nrowblk = (P + 255u) / 256u;
+            hipLaunchKernelGGL(sep_fused_final_kernel, dim3(nrowblk + (1u << a.cbits)),
+                               dim3(256), 0, st, a.ws + lay.rowpart, a.ws + lay.fcolpart, a.dgt,
+                               a.dgc, P, lay.nchunks << (a.cbits - R),
+                               lay.nchunks << (A - a.cbits), nrowblk, (uint32_t)HB,
+                               (uint32_t)(A - a.cbits));
+            return hipGetLastError();
+        }
+    }
     float *o = lay.nchunks > 1 ? a.ws + lay.part : dst;
     if (lay.per_chunk == 1) {
         e = with_middle_gain(gain, a.B, [&](auto g) {
             hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, decltype(g), true, MIX_X>),
                                dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
-                               wsx, wsd, g, o, (uint32_t)a.B, 1u);
+                               wsx, wsd, g, o, (uint32_t)a.B, 1u, nullptr, nullptr, 0u);
             return hipGetLastError();
         });
         if (e != hipSuccess) return e;
@@ -691,7 +832,8 @@ hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, f
         e = with_streamed_gain(gain, [&](auto g) {
             hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, decltype(g), false, MIX_X>),
                                dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
-                               wsx, wsd, g, o, (uint32_t)a.B, lay.per_chunk);
+                               wsx, wsd, g, o, (uint32_t)a.B, lay.per_chunk, nullptr, nullptr,
+                               0u);
             return hipGetLastError();
         });
         if (e != hipSuccess) return e;

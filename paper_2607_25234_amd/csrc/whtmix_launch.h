@@ -81,8 +81,11 @@ struct BackwardLayout {
     uint64_t part;          // per-chunk partial dG sums (when nchunks > 1)
     uint64_t dg;            // dG for the separable reductions
     uint64_t colpart;       // column partial sums (separable)
+    uint64_t rowpart;       // row and column partial sums formed by the middle
+    uint64_t fcolpart;      // pass (separable, sep_fused)
     uint32_t nchunks, per_chunk;
     uint32_t rows_per_block, col_blocks;
+    uint32_t sep_fused;     // separable: the middle pass forms the partial sums itself
     uint64_t floats;        // total workspace
 };
 

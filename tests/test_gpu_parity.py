@@ -375,7 +375,7 @@ def test_large_slices_by_properties(shape, dev):
             xb = x[b, r0:r0 + rows].double()
             coef += float(torch.mv(xb.t().contiguous(), sn[r0:r0 + rows]).dot(sc))
         # error scale: the coefficient <x, B> has standard deviation rms(x)
-        # (B has unit norm), so judge against max(|<x, B>|, rms(x))
+        # (B has unit norm), so compare against max(|<x, B>|, rms(x))
         xrms = float(x[b].double().pow(2).mean().sqrt())
         amp = max(abs(coef) * scale, xrms) * scale
         worst = 0.0

@@ -83,3 +83,98 @@ def test_layout_rule_blocks(C, P):
     assert np.all(seen == 1)
     np.testing.assert_allclose(dgt, (dG * G).sum(axis=1), rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(part.sum(axis=0), (dG * G).sum(axis=0), rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- fused sums
+def sep_tile_sums_model(p, tau_count, run, chunk, nchunks, A, HB, cbits, rowpart, colpart,
+                        writes):
+    """sep_tile_sums on one middle tile: p[k][tau] = dG*G of the element with
+    tile index t = e | k << 5 | (tau >> 5) << 10 (e = tau mod 32), i.e. f =
+    ((t >> 5) << A) | (run << 5) | e.  Models the LDS round trip (with the
+    pad of one word per 32; each word written once, conflict-free banks), the
+    per-thread row and column sums and the group sum."""
+    R = 5
+    qb = cbits - R
+    q = run & ((1 << qb) - 1)
+    M = HB + R
+    pad = lambda t: t + (t >> 5)
+    lds = np.full(pad((1 << M) - 1) + 1, np.nan)
+    lw = np.zeros(lds.size, int)
+    taus = np.arange(tau_count)
+    base = (taus & 31) | ((taus >> 5) << 10)
+    for k in range(32):
+        a = pad(base + (k << R))
+        lds[a] = p[k]
+        np.add.at(lw, a, 1)
+        for w in range(0, tau_count, 64):                 # 32 distinct banks per half-wave
+            for h in (0, 32):
+                seg = a[w + h:w + h + 32]
+                if seg.size:
+                    assert len(set(seg % 32)) == seg.size
+    assert lw.sum() == 1 << M and lw.max() == 1
+    rblock = (((chunk << qb) | q) << (A - cbits)) | (run >> qb)
+    for tau in range(tau_count):                          # row hi = tau
+        rs = sum(lds[pad((tau << R) + e)] for e in range(32))
+        idx = (rblock << HB) + tau
+        assert 0 <= idx < rowpart.size
+        rowpart[idx] = rs
+        writes["row"][idx] += 1
+    ng = tau_count // 32
+    red = np.zeros((ng, 32))
+    for tau in range(tau_count):
+        g, e = tau >> 5, tau & 31
+        red[g, e] = sum(lds[pad((((g << 5) + i) << R) + e)] for i in range(32))
+    np_ = nchunks << (A - cbits)
+    for e in range(32):
+        c = (q << R) | e
+        idx = c * np_ + ((chunk << (A - cbits)) | (run >> qb))
+        assert 0 <= idx < colpart.size
+        colpart[idx] = red[:, e].sum()
+        writes["col"][idx] += 1
+
+
+def sep_fused_final_model(rowpart, colpart, P, C, nq, HB, rlbits):
+    """sep_fused_final_kernel: storage index i = rl * 2^HB + hi -> token
+    hi * 2^rlbits + rl; columns summed over their partials."""
+    dgt = np.full(P, np.nan)
+    hit = np.zeros(P, int)
+    for i in range(P):
+        n = ((i & ((1 << HB) - 1)) << rlbits) | (i >> HB)
+        dgt[n] = sum(rowpart[j * P + i] for j in range(nq))
+        hit[n] += 1
+    assert np.all(hit == 1)
+    return dgt, colpart.reshape(C, -1).sum(axis=1)
+
+
+@pytest.mark.parametrize("A,HB,cbits,B,nchunks", [(14, 9, 7, 4, 1), (12, 6, 6, 8, 4),
+                                                    (13, 8, 7, 2, 2), (11, 7, 11, 3, 3),
+                                                    (12, 7, 5, 1, 1)])
+def test_fused_separable_sums(A, HB, cbits, B, nchunks):
+    """Over every (chunk, run) tile the fused partial sums, then the final
+    kernel's fixed-order sums, give dg_t = row sums and dg_c = column sums of
+    dG * G; every partial is written exactly once, inside its buffer."""
+    R = 5
+    K = A + HB
+    C, P = 1 << cbits, 1 << (K - cbits)
+    rng = np.random.default_rng(K + cbits)
+    dGG = rng.standard_normal((nchunks, 1 << K))          # per-chunk p over the flat index f
+    tau_count = 1 << (HB + R - 5)
+    rowpart = np.full(nchunks * (1 << (K - R)), np.nan)
+    colpart = np.full(C * (nchunks << (A - cbits)), np.nan)
+    writes = {"row": np.zeros(rowpart.size, int), "col": np.zeros(colpart.size, int)}
+    tau = np.arange(tau_count)
+    for chunk in range(nchunks):
+        for run in range(1 << (A - R)):
+            p = np.empty((32, tau_count))
+            for k in range(32):
+                t = (tau & 31) | (k << 5) | ((tau >> 5) << 10)
+                f = ((t >> R) << A) | (run << R) | (t & 31)
+                p[k] = dGG[chunk, f]
+            sep_tile_sums_model(p, tau_count, run, chunk, nchunks, A, HB, cbits, rowpart,
+                                colpart, writes)
+    assert np.all(writes["row"] == 1) and np.all(writes["col"] == 1)
+    nq = nchunks << (cbits - R)
+    dgt, dgc = sep_fused_final_model(rowpart, colpart, P, C, nq, HB, A - cbits)
+    tot = dGG.sum(axis=0).reshape(P, C)
+    np.testing.assert_allclose(dgt, tot.sum(axis=1), rtol=1e-12, atol=1e-10)
+    np.testing.assert_allclose(dgc, tot.sum(axis=0), rtol=1e-12, atol=1e-10)
