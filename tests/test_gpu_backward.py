@@ -146,6 +146,34 @@ def test_backward_separable(shape, dev, orc):
     check("d log_gain_channels", to_host(dgc), dgc_ref, GRAD_TOL)
 
 
+@pytest.mark.parametrize("shape,dtype", [
+    ((1, 8192, 128), "bf16"), ((6, 4096, 64), "f32"), ((2, 16384, 256), "bf16"),
+    ((3, 4096, 32), "f32"), ((2, 6000, 64), "f32"), ((4, 65536, 128), "bf16"),
+], ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else v)
+def test_backward_separable_fused_sums(shape, dtype, dev, orc):
+    """Shapes where the middle pass forms the log-gain gradients' partial sums
+    itself (three-pass split with R = 5 and 6..9 high bits, 32 <= C <= 2^A):
+    one slice (a chunk of one), three chunks of two slices, C = 256 (eight
+    channel groups), C = 32 (one), padded N, and the benchmarked workload."""
+    import torch
+    B, N, C = shape
+    P = whtmix.padded_tokens(N)
+    info = whtmix.plan_describe(B, N, C, dtype)
+    assert info["plan"] == "three_pass" and info["run_bits"] == 5
+    assert 6 <= info["log2_slice"] - info["outer_bits"] <= 9
+    x, dy, _ = inputs(B, N, C, dtype, seed=640 + N + C)
+    gt, gc = workloads.draw_log_gains(P, C, seed=641 + N + C)
+    say(f"separable fused sums {shape} {dtype}")
+    dx, dgt, dgc = whtmix.backward_separable(
+        to_device(x, dtype, dev), to_device(dy, dtype, dev), torch.from_numpy(gt).to(dev),
+        torch.from_numpy(gc).to(dev))
+    torch.cuda.synchronize()
+    dx_ref, dgt_ref, dgc_ref = orc.whtmix_grad_separable(x, dy, gt, gc)
+    check("dx", to_host(dx), dx_ref, DERIVED[dtype])
+    check("d log_gain_tokens", to_host(dgt), dgt_ref, GRAD_TOL)
+    check("d log_gain_channels", to_host(dgc), dgc_ref, GRAD_TOL)
+
+
 def test_backward_in_place_and_deterministic(dev, orc):
     """dx may overwrite dy (the gain gradient is taken first); repeated calls
     are bitwise identical (fixed-order batch sum)."""
