@@ -123,6 +123,58 @@ __device__ __forceinline__ void sep_tile_sums(const float (&p)[V], float *lds, f
     }
 }
 
+// The same sums in the one-slice-per-chunk form (SINGLE, 2^15-element tiles),
+// which does not hold the gain: d = dG in the tile's LDS, and since
+// G[n][c] = exp(g_t[n]) exp(g_c[c]) the row sum is exp(g_t[n]) times the
+// sum of d exp(g_c[c]) and the column sum exp(g_c[c]) times the sum of
+// d exp(g_t[n]); both factors come from small LDS tables (the tile's 32
+// channels, its 2^HB rows).  Products are stored to LDS as they are formed,
+// so this needs no register array beyond the two tiles.
+template <int A, int HB, int R>
+__device__ __forceinline__ void sep_tile_sums_single(
+    const float (&vx)[V], const float (&vd)[V], float scale, float *lds, float *red, float *egc,
+    float *egt, const float *__restrict__ gt, const float *__restrict__ gc, uint32_t tau,
+    uint32_t run, uint32_t chunk, uint32_t nchunks, uint32_t cbits, float *__restrict__ rowpart,
+    float *__restrict__ colpart)
+{
+    constexpr uint32_t NG = 1u << (HB - 5);
+    const uint32_t qb = cbits - R;
+    const uint32_t q = run & ((1u << qb) - 1u);
+    const uint32_t rl = run >> qb;
+    const uint32_t base = layout_base<R>(tau);
+    __syncthreads();   // every thread's last reads of the tile exchanges are done
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+        lds[pad(base + ((uint32_t)k << R))] = vx[k] * vd[k] * scale;
+    if (tau < 32u)
+        egc[tau] = __expf(gc[(q << R) | tau]);
+    egt[tau] = __expf(gt[((size_t)tau << (A - cbits)) | rl]);   // row hi = tau: token n
+    __syncthreads();
+    float rs = 0.0f;
+#pragma unroll
+    for (uint32_t e = 0; e < 32u; ++e)
+        rs += lds[pad((tau << R) + e)] * egc[e];
+    const size_t rblock = ((size_t)((chunk << qb) | q) << (A - cbits)) | rl;
+    rowpart[(rblock << HB) + tau] = rs * egt[tau];
+    float cs = 0.0f;
+    const uint32_t g = tau >> 5, e = tau & 31u;
+#pragma unroll
+    for (uint32_t i = 0; i < 32u; ++i)
+        cs += lds[pad((((g << 5) + i) << R) + e)] * egt[(g << 5) + i];
+    red[g * 32u + e] = cs;
+    __syncthreads();
+    if (tau < 32u) {
+        float t = 0.0f;
+#pragma unroll
+        for (uint32_t w = 0; w < NG; ++w)
+            t += red[w * 32u + tau];
+        const uint32_t c = (q << R) | tau;
+        const uint32_t np = nchunks << (A - cbits);
+        colpart[(size_t)c * np + ((chunk << (A - cbits)) | rl)] = t * egc[tau];
+    }
+    __syncthreads();   // the tile's LDS is free again for the inverse exchanges
+}
+
 // Three-pass dG and dX together.  After OUTER_FWD of x and dy (one launch),
 // one workgroup owns one workspace run for a chunk of slices.  For each slice
 // it transforms both tiles over the HB high bits, so both are now transformed
@@ -144,10 +196,10 @@ __device__ __forceinline__ void sep_tile_sums(const float (&p)[V], float *lds, f
 // back to wsx (the forward mixer's middle pass on x, for the block's backward,
 // which needs Z' as well), after the product and before the next slice's load.
 //
-// SEPSUM (separable gains, several slices per chunk form, R = 5, HB >= 6,
-// R <= log2 C <= A): instead of storing dG the workgroup forms the two
-// log-gain gradients' partial sums of p = dG * G over its tile
-// (sep_tile_sums) and writes them to rowpart / colpart.
+// SEPSUM (separable gains, R = 5, HB >= 6, R <= log2 C <= A): instead of
+// storing dG the workgroup forms the two log-gain gradients' partial sums of
+// dG * G over its tile and writes them to rowpart / colpart (sep_tile_sums
+// with several slices per chunk, sep_tile_sums_single with one).
 template <int A, int HB, int R, class Gain, bool SINGLE, bool MIX_X = false, bool SEPSUM = false>
 __global__ void __launch_bounds__(1 << (HB + R - VB))
 grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain gain,
@@ -167,7 +219,7 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
     const auto tile = [&](const float *ws, uint32_t b) {
         return buffer(ws + ((size_t)b << (A + HB)) + ((size_t)run << M), (1u << M) * 4u);
     };
-    static_assert(!SEPSUM || (!SINGLE && R == VB && G::SL == R && HB >= 6),
+    static_assert(!SEPSUM || (R == VB && G::SL == R && HB >= 6),
                   "the fused separable sums take the product in layout R = 5");
     float *o = SEPSUM ? out
                       : out + ((size_t)chunk << (A + HB)) + ((size_t)run << R) +
@@ -180,9 +232,16 @@ grad_mix_middle_kernel(float *__restrict__ wsx, float *__restrict__ wsd, Gain ga
         butterflies<G::JT, VB>(vd);
         forward_groups<M, R, 0, G::TOP, true>(lds, vx, tau);
         forward_groups<M, R, 0, G::TOP, true>(lds, vd, tau);
+        if constexpr (SEPSUM && std::is_same_v<Gain, LogSeparableGain>) {
+            __shared__ float red[32u << (HB - 5)], egt[1u << HB], egc[32];
+            sep_tile_sums_single<A, HB, R>(vx, vd, scale, lds, red, egc, egt, gain.gt, gain.gc,
+                                           tau, run, chunk, gridDim.x >> (A - R), cbits,
+                                           rowpart, colpart);
+        } else {
 #pragma unroll
-        for (int k = 0; k < V; ++k)
-            o[GM::at((uint32_t)k << G::SL)] = vx[k] * vd[k] * scale;
+            for (int k = 0; k < V; ++k)
+                o[GM::at((uint32_t)k << G::SL)] = vx[k] * vd[k] * scale;
+        }
         __builtin_amdgcn_sched_barrier(0);   // keep the gain loads after the product
         float gv[V];
         gain.template load<G::SL, GM, true>(gv, run << R, tau);
@@ -711,7 +770,7 @@ BackwardLayout backward_layout(int plan, int K, int64_t B, int64_t C, bool separ
         // regions above): rows [chunk][C / 2^R][P], columns
         // [C][chunk][2^(A - cbits)]
         const Split sp = three_pass_split(K);
-        if (sp.R == VB && sp.HB >= 6 && sp.HB + sp.R < kMaxTile && cbits >= sp.R &&
+        if (sp.R == VB && sp.HB >= 6 && sp.HB + sp.R <= kMaxTile && cbits >= sp.R &&
             cbits <= sp.A) {
             lay.sep_fused = 1;
             lay.rowpart = cursor;
@@ -797,11 +856,14 @@ hipError_t grad_middle_phase(const BackwardArgs &a, const BackwardLayout &lay, f
     float *wsd = a.ws + lay.wsd;
     hipError_t e;
     if constexpr (std::is_same_v<Gain, LogSeparableGain> && R == VB && HB >= 6 &&
-                  HB + R < kMaxTile) {
+                  HB + R <= kMaxTile) {
         if (lay.sep_fused) {
             // the middle pass forms the row and column partial sums of dG * G
-            // (any slices per chunk), then one small kernel adds them up
-            hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, false, MIX_X, true>),
+            // (the several-slices form up to 2^14-element tiles, any slices
+            // per chunk; the one-slice form for 2^15), then one small kernel
+            // adds them up
+            constexpr bool single = HB + R == kMaxTile;
+            hipLaunchKernelGGL((grad_mix_middle_kernel<A, HB, R, Gain, single, MIX_X, true>),
                                dim3(lay.nchunks << (A - R)), dim3(1u << (HB + R - VB)), 0, st,
                                wsx, wsd, gain, nullptr, (uint32_t)a.B, lay.per_chunk,
                                a.ws + lay.rowpart, a.ws + lay.fcolpart, (uint32_t)a.cbits);

@@ -149,18 +149,21 @@ def test_backward_separable(shape, dev, orc):
 @pytest.mark.parametrize("shape,dtype", [
     ((1, 8192, 128), "bf16"), ((6, 4096, 64), "f32"), ((2, 16384, 256), "bf16"),
     ((3, 4096, 32), "f32"), ((2, 6000, 64), "f32"), ((4, 65536, 128), "bf16"),
+    ((1, 140000, 256), "bf16"), ((2, 65536, 512), "bf16"),
 ], ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else v)
 def test_backward_separable_fused_sums(shape, dtype, dev, orc):
     """Shapes where the middle pass forms the log-gain gradients' partial sums
-    itself (three-pass split with R = 5 and 6..9 high bits, 32 <= C <= 2^A):
+    itself (three-pass split with R = 5 and 6..10 high bits, 32 <= C <= 2^A):
     one slice (a chunk of one), three chunks of two slices, C = 256 (eight
-    channel groups), C = 32 (one), padded N, and the benchmarked workload."""
+    channel groups), C = 32 (one), padded N, the benchmarked workload, and
+    2^15-element middle tiles (one slice per chunk, the exp factors applied to
+    the row and column sums) at 2^26 padded and at 2^25 x 2 with C = 512."""
     import torch
     B, N, C = shape
     P = whtmix.padded_tokens(N)
     info = whtmix.plan_describe(B, N, C, dtype)
     assert info["plan"] == "three_pass" and info["run_bits"] == 5
-    assert 6 <= info["log2_slice"] - info["outer_bits"] <= 9
+    assert 6 <= info["log2_slice"] - info["outer_bits"] <= 10
     x, dy, _ = inputs(B, N, C, dtype, seed=640 + N + C)
     gt, gc = workloads.draw_log_gains(P, C, seed=641 + N + C)
     say(f"separable fused sums {shape} {dtype}")

@@ -178,3 +178,62 @@ def test_fused_separable_sums(A, HB, cbits, B, nchunks):
     tot = dGG.sum(axis=0).reshape(P, C)
     np.testing.assert_allclose(dgt, tot.sum(axis=1), rtol=1e-12, atol=1e-10)
     np.testing.assert_allclose(dgc, tot.sum(axis=0), rtol=1e-12, atol=1e-10)
+
+
+def sep_tile_sums_single_model(d, gt, gc, tau_count, run, chunk, nchunks, A, HB, cbits,
+                               rowpart, colpart, writes):
+    """sep_tile_sums_single on one 2^(HB+5)-element tile: d[k][tau] = dG (no
+    gain); the exp tables hold exp(g_c) of the tile's 32 channels and exp(g_t)
+    of the token of each row hi = tau."""
+    R = 5
+    qb = cbits - R
+    q, rl = run & ((1 << qb) - 1), run >> qb
+    taus = np.arange(tau_count)
+    egc = np.exp(gc[(q << R) | np.arange(32)])
+    egt = np.exp(gt[(taus << (A - cbits)) | rl])
+    tile = np.empty((tau_count, 32))                      # [hi][e]
+    for k in range(32):
+        hi = k | ((taus >> 5) << 5)
+        tile[hi, taus & 31] = d[k]
+    rblock = (((chunk << qb) | q) << (A - cbits)) | rl
+    idx = (rblock << HB) + taus
+    rowpart[idx] = (tile * egc[None, :]).sum(axis=1) * egt
+    np.add.at(writes["row"], idx, 1)
+    np_ = nchunks << (A - cbits)
+    for e in range(32):
+        c = (q << R) | e
+        idx = c * np_ + ((chunk << (A - cbits)) | rl)
+        colpart[idx] = (tile[:, e] * egt).sum() * egc[e]
+        writes["col"][idx] += 1
+
+
+@pytest.mark.parametrize("A,HB,cbits,nchunks", [(12, 10, 7, 2), (13, 10, 8, 1), (11, 10, 5, 3)])
+def test_fused_separable_sums_single_form(A, HB, cbits, nchunks):
+    """The one-slice form with the separable exp factors applied to the row
+    and column sums gives the same gradients as sums of dG * exp(g_t + g_c)."""
+    R = 5
+    K = A + HB
+    C, P = 1 << cbits, 1 << (K - cbits)
+    rng = np.random.default_rng(K + cbits + nchunks)
+    dG = rng.standard_normal((nchunks, 1 << K))
+    gt = 0.3 * rng.standard_normal(P)
+    gc = 0.3 * rng.standard_normal(C)
+    tau_count = 1 << HB
+    rowpart = np.full(nchunks * (1 << (K - R)), np.nan)
+    colpart = np.full(C * (nchunks << (A - cbits)), np.nan)
+    writes = {"row": np.zeros(rowpart.size, int), "col": np.zeros(colpart.size, int)}
+    tau = np.arange(tau_count)
+    kk = np.arange(32)[:, None]
+    t = (tau[None, :] & 31) | (kk << 5) | ((tau[None, :] >> 5) << 10)
+    for chunk in range(nchunks):
+        for run in range(1 << (A - R)):
+            d = dG[chunk, ((t >> R) << A) | (run << R) | (t & 31)]
+            sep_tile_sums_single_model(d, gt, gc, tau_count, run, chunk, nchunks, A, HB, cbits,
+                                       rowpart, colpart, writes)
+    assert np.all(writes["row"] == 1) and np.all(writes["col"] == 1)
+    dgt, dgc = sep_fused_final_model(rowpart, colpart, P, C, nchunks << (cbits - R), HB,
+                                     A - cbits)
+    G = np.exp(gt[:, None] + gc[None, :])
+    tot = dG.sum(axis=0).reshape(P, C) * G
+    np.testing.assert_allclose(dgt, tot.sum(axis=1), rtol=1e-10, atol=1e-9)
+    np.testing.assert_allclose(dgc, tot.sum(axis=0), rtol=1e-10, atol=1e-9)
