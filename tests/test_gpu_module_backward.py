@@ -126,6 +126,34 @@ def test_module_backward_c256_pair_tiles_against_oracle(dev, orc):
     check_all("2^26 pair tiles", got, ref, "bf16")
 
 
+def test_module_backward_separable_pair_tiles_by_joint_gain(dev):
+    """One 2^26-element slice (N = 140000 padded, C = 256, bf16): the pair-tile
+    block backward with separable gains, whose middle pass forms the log-gain
+    sums itself (one slice per chunk, 2^15-element tiles), against the same
+    call with the joint gain G = exp(g_t + g_c) (its dG checked against the
+    oracle above): dX and both weight gradients agree, and the log-gain
+    gradients equal the row and column sums of dG * G taken on the host."""
+    B, N, C = 1, 140000, 256
+    P = whtmix.padded_tokens(N)
+    d = whtmix.plan_describe(B, N, C, "bf16")
+    assert d["module_backward_fused"] and d["module_outer_bits"] == 16, d
+    x, dy, _, wi, wo = inputs(B, N, C, "bf16", seed=970)
+    gt, gc = workloads.draw_log_gains(P, C, seed=971)
+    G = np.exp(gt.astype(np.float64)[:, None] + gc.astype(np.float64)[None, :])
+    say(f"module backward separable {(B, N, C)} bf16 against the joint gain")
+    dx_s, dwi_s, dwo_s, dgt, dgc = run(x, dy, wi, wo, "bf16", dev, gt=gt, gc=gc)
+    dx_j, dwi_j, dwo_j, dg = run(x, dy, wi, wo, "bf16", dev, g=G.astype(np.float32))
+    # two bf16 roundings of float32 values that agree to about 1e-7 differ by
+    # at most one bf16 ulp, 2^-7 of the element at most (not the 2^-8 of one
+    # rounding against the exact value)
+    check("dx", dx_s, dx_j, 2.0 ** -7 + GRAD_TOL)
+    check("dw_in", dwi_s, dwi_j, GRAD_TOL)
+    check("dw_out", dwo_s, dwo_j, GRAD_TOL)
+    dgg = dg.astype(np.float64).reshape(P, C) * G
+    check("dgt", dgt, dgg.sum(axis=1), GRAD_TOL)
+    check("dgc", dgc, dgg.sum(axis=0), GRAD_TOL)
+
+
 def test_module_backward_forced_three_pass_and_alias(dev, orc):
     """The three-pass mixer on a 2^14 slice, with dx written over dy."""
     B, N, C = 2, 128, 128
