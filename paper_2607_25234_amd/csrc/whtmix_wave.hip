@@ -1,10 +1,12 @@
 // Wave tiles: the three passes of slices of 2^12 .. 2^16 elements on
 // one-wave tiles of 2^9 elements whose butterflies stay inside the wave
-// (gfx950).  Two plans run them:
-//   WAVE_TILES  three launches, one tile per workgroup; AUTO takes it for small
-//               batches of 2^15- and 2^16-element slices (image1k: 9.2 -> 7.3 us
-//               per call against THREE_PASS; 2^15 slices 12.8 -> 7.1 us
-//               against one workgroup per slice);
+// (gfx950).  Three plans run them:
+//   WAVE_TILES  three launches, one tile per workgroup; AUTO takes it for up
+//               to 3 slices of 2^16 elements (image1k: 9.2 -> 7.3 us per call
+//               against THREE_PASS);
+//   TWO_PASS    a fold pass in place of the first two launches (below), then
+//               the third; AUTO takes it for up to 48 slices of 2^15 and 4-16
+//               of 2^16;
 //   ONE_LAUNCH  all three passes in a single cooperative launch, ordered by
 //               per-slice completion counters (forced only: slower).
 //
