@@ -800,6 +800,87 @@ outer_fwd_kernel2(const T *__restrict__ x, float *__restrict__ ws, uint32_t nval
     outer_fwd_tile2<HB, R, T, VWID>(lds, x, ws, nvalid, outer_block<R>(blockIdx.x, gridDim.x));
 }
 
+// OUTER_FWD over 2^16 tiles, bf16 x in 16-byte groups, as a grid of one
+// resident workgroup per CU that takes tiles blockIdx.x, blockIdx.x +
+// gridDim.x, ...: the next tile's x (both register sets, 32 words per
+// thread, when the tile is whole) is loaded while this tile is transformed
+// and stored, since one 1024-thread workgroup per CU leaves no other
+// workgroup to cover the load latency.
+template <int HB, int R>
+__global__ void __launch_bounds__(1 << (15 - VB))
+outer_fwd_kernel2_pf(const __bf16 *__restrict__ x, float *__restrict__ ws, uint32_t nvalid,
+                     uint32_t ntiles)
+{
+    constexpr int A = 16, M = 15, VWID = 3, PER = 8, NQ = V / PER;
+    using VG = VGroups<M, VWID>;
+    using Run = RunMap<HB, R>;
+    __shared__ float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t voff = VG::base(tau) * 2u;
+    vu32x4 raw[2][NQ];
+    // issue the loads of tile blk into raw; false (nothing issued) for a
+    // partial tile, which the loop loads itself
+    auto issue = [&](uint32_t t) -> bool {
+        const uint32_t blk = outer_block<R>(t, ntiles);
+        const uint32_t hi = blk & ((1u << HB) - 1u);
+        if (tile_valid<A>(nvalid, hi) < (1u << A))
+            return false;   // uniform per workgroup
+        const __bf16 *base = x + (size_t)(blk >> HB) * nvalid + ((size_t)hi << A);
+        const __amdgpu_buffer_rsrc_t r0 = buffer(base, (1u << M) * 2u);
+        const __amdgpu_buffer_rsrc_t r1 = buffer(base + (1u << M), (1u << M) * 2u);
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+            raw[0][j] = __builtin_bit_cast(
+                vu32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                            r0, voff, VG::reg((uint32_t)(j * PER)) * 2u, kStreaming));
+            raw[1][j] = __builtin_bit_cast(
+                vu32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                            r1, voff, VG::reg((uint32_t)(j * PER)) * 2u, kStreaming));
+        }
+        return true;
+    };
+    // tile t is worked on XCD t mod 8, as in the one-tile-per-workgroup grid
+    // (the grid is a multiple of 8 or covers every tile), so outer_block's
+    // renumbering applies unchanged
+    uint32_t t = blockIdx.x;
+    bool have = t < ntiles && issue(t);
+    for (; t < ntiles; t += gridDim.x) {   // uniform per workgroup
+        const uint32_t blk = outer_block<R>(t, ntiles);
+        const uint32_t hi = blk & ((1u << HB) - 1u);
+        float v0[V], v1[V];
+        if (have) {
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t w0 = raw[0][j][e], w1 = raw[1][j][e];
+                    v0[j * PER + 2 * e] = __builtin_bit_cast(float, w0 << 16);
+                    v0[j * PER + 2 * e + 1] = __builtin_bit_cast(float, w0 & 0xffff0000u);
+                    v1[j * PER + 2 * e] = __builtin_bit_cast(float, w1 << 16);
+                    v1[j * PER + 2 * e + 1] = __builtin_bit_cast(float, w1 & 0xffff0000u);
+                }
+            }
+        } else {
+            const uint32_t valid = tile_valid<A>(nvalid, hi);
+            const __bf16 *base = x + (size_t)(blk >> HB) * nvalid + ((size_t)hi << A);
+            load_tile_vec<M, VWID, __bf16>(v0, base, min(valid, 1u << M), tau);
+            load_tile_vec<M, VWID, __bf16>(v1, base + (1u << M),
+                                           valid > (1u << M) ? valid - (1u << M) : 0u, tau);
+        }
+        have = t + gridDim.x < ntiles && issue(t + gridDim.x);
+        const __amdgpu_buffer_rsrc_t r =
+            buffer(ws + ((size_t)(blk >> HB) << (A + HB)) + ((size_t)hi << R),
+                   extent_bytes<Run, A, float>());
+        cross_butterflies(v0, v1);
+        butterflies<0, VB>(v0);
+        butterflies<0, VB>(v1);
+        vforward_groups<M, VWID, 0, true>(lds, v0, tau);
+        store_layout<VG::SL, Run, float>(v0, r, tau);
+        vforward_groups<M, VWID, 0, true>(lds, v1, tau);
+        store_layout<VG::SL, Run, float>(v1, r, tau, Run::at(1u << M) * 4u);
+    }
+}
+
 // Two operands in one launch (as outer_fwd2_kernel).
 template <int HB, int R, typename T, int VWID>
 __global__ void __launch_bounds__(1 << (15 - VB))
@@ -882,6 +963,15 @@ hipError_t launch_outer_fwd(const T *x, float *ws, int64_t B, uint32_t nvalid, h
     const bool vec = use_vec<sp.A, T>(nvalid);
     if constexpr (sp.A == 16) {
         const dim3 block(1u << (15 - VB));
+        if constexpr (sizeof(T) == 2 && VW == 3) {
+            if (vec) {
+                const uint32_t ntiles = (uint32_t)(B << sp.HB);
+                hipLaunchKernelGGL((outer_fwd_kernel2_pf<sp.HB, sp.R>),
+                                   dim3(ntiles < 256u ? ntiles : 256u), block, 0, st, x, ws,
+                                   nvalid, ntiles);
+                return hipGetLastError();
+            }
+        }
         if (vec)
             hipLaunchKernelGGL((outer_fwd_kernel2<sp.HB, sp.R, T, VW>), grid, block, 0, st, x, ws,
                                nvalid);
