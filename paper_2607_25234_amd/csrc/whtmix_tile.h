@@ -805,10 +805,12 @@ outer_fwd_kernel2(const T *__restrict__ x, float *__restrict__ ws, uint32_t nval
 // gridDim.x, ...: the next tile's x (both register sets, 32 words per
 // thread, when the tile is whole) is loaded while this tile is transformed
 // and stored, since one 1024-thread workgroup per CU leaves no other
-// workgroup to cover the load latency.
+// workgroup to cover the load latency.  With two operands (x1, ws1 not
+// null) tiles ntiles.. 2 ntiles - 1 are those of x1, as in outer_fwd2_kernel2.
 template <int HB, int R>
 __global__ void __launch_bounds__(1 << (15 - VB))
-outer_fwd_kernel2_pf(const __bf16 *__restrict__ x, float *__restrict__ ws, uint32_t nvalid,
+outer_fwd_kernel2_pf(const __bf16 *__restrict__ x0, float *__restrict__ ws0,
+                     const __bf16 *__restrict__ x1, float *__restrict__ ws1, uint32_t nvalid,
                      uint32_t ntiles)
 {
     constexpr int A = 16, M = 15, VWID = 3, PER = 8, NQ = V / PER;
@@ -820,12 +822,20 @@ outer_fwd_kernel2_pf(const __bf16 *__restrict__ x, float *__restrict__ ws, uint3
     vu32x4 raw[2][NQ];
     // issue the loads of tile blk into raw; false (nothing issued) for a
     // partial tile, which the loop loads itself
+    const uint32_t total = x1 ? 2u * ntiles : ntiles;
+    // operand and tile of grid-wide tile t
+    auto locate = [&](uint32_t t, bool &second) -> uint32_t {
+        second = t >= ntiles;
+        return outer_block<R>(second ? t - ntiles : t, ntiles);
+    };
     auto issue = [&](uint32_t t) -> bool {
-        const uint32_t blk = outer_block<R>(t, ntiles);
+        bool second;
+        const uint32_t blk = locate(t, second);
         const uint32_t hi = blk & ((1u << HB) - 1u);
         if (tile_valid<A>(nvalid, hi) < (1u << A))
             return false;   // uniform per workgroup
-        const __bf16 *base = x + (size_t)(blk >> HB) * nvalid + ((size_t)hi << A);
+        const __bf16 *base =
+            (second ? x1 : x0) + (size_t)(blk >> HB) * nvalid + ((size_t)hi << A);
         const __amdgpu_buffer_rsrc_t r0 = buffer(base, (1u << M) * 2u);
         const __amdgpu_buffer_rsrc_t r1 = buffer(base + (1u << M), (1u << M) * 2u);
 #pragma unroll
@@ -843,10 +853,13 @@ outer_fwd_kernel2_pf(const __bf16 *__restrict__ x, float *__restrict__ ws, uint3
     // (the grid is a multiple of 8 or covers every tile), so outer_block's
     // renumbering applies unchanged
     uint32_t t = blockIdx.x;
-    bool have = t < ntiles && issue(t);
-    for (; t < ntiles; t += gridDim.x) {   // uniform per workgroup
-        const uint32_t blk = outer_block<R>(t, ntiles);
+    bool have = t < total && issue(t);
+    for (; t < total; t += gridDim.x) {   // uniform per workgroup
+        bool second;
+        const uint32_t blk = locate(t, second);
         const uint32_t hi = blk & ((1u << HB) - 1u);
+        const __bf16 *x = second ? x1 : x0;
+        float *ws = second ? ws1 : ws0;
         float v0[V], v1[V];
         if (have) {
 #pragma unroll
@@ -867,7 +880,7 @@ outer_fwd_kernel2_pf(const __bf16 *__restrict__ x, float *__restrict__ ws, uint3
             load_tile_vec<M, VWID, __bf16>(v1, base + (1u << M),
                                            valid > (1u << M) ? valid - (1u << M) : 0u, tau);
         }
-        have = t + gridDim.x < ntiles && issue(t + gridDim.x);
+        have = t + gridDim.x < total && issue(t + gridDim.x);
         const __amdgpu_buffer_rsrc_t r =
             buffer(ws + ((size_t)(blk >> HB) << (A + HB)) + ((size_t)hi << R),
                    extent_bytes<Run, A, float>());
@@ -968,7 +981,7 @@ hipError_t launch_outer_fwd(const T *x, float *ws, int64_t B, uint32_t nvalid, h
                 const uint32_t ntiles = (uint32_t)(B << sp.HB);
                 hipLaunchKernelGGL((outer_fwd_kernel2_pf<sp.HB, sp.R>),
                                    dim3(ntiles < 256u ? ntiles : 256u), block, 0, st, x, ws,
-                                   nvalid, ntiles);
+                                   (const __bf16 *)nullptr, (float *)nullptr, nvalid, ntiles);
                 return hipGetLastError();
             }
         }
@@ -1000,6 +1013,15 @@ hipError_t launch_outer_fwd2(const T *x, const T *dy, float *wsx, float *wsd, in
     const bool vec = use_vec<sp.A, T>(nvalid);
     if constexpr (sp.A == 16) {
         const dim3 block(1u << (15 - VB));
+        if constexpr (sizeof(T) == 2 && VW == 3) {
+            if (vec) {
+                const uint32_t ntiles = (uint32_t)(B << sp.HB);
+                hipLaunchKernelGGL((outer_fwd_kernel2_pf<sp.HB, sp.R>),
+                                   dim3(2u * ntiles < 256u ? 2u * ntiles : 256u), block, 0, st, x,
+                                   wsx, dy, wsd, nvalid, ntiles);
+                return hipGetLastError();
+            }
+        }
         if (vec)
             hipLaunchKernelGGL((outer_fwd2_kernel2<sp.HB, sp.R, T, VW>), grid, block, 0, st, x, dy,
                                wsx, wsd, nvalid);
