@@ -1120,6 +1120,88 @@ module_outer_inv_pair_kernel(const float *__restrict__ ws, const __bf16 *__restr
     project_out_pair(zh, zl, lds, y + b * nvalid + ((size_t)hi << A), valid, tau);
 }
 
+// The same pass as a grid of one resident workgroup per CU (the kernel's LDS
+// holds W_out or the exchange, 128 KiB, so no second workgroup fits) taking
+// tiles t, t + grid, ...: the first NPF of the 32 registers of the next
+// tile's first set are read from the workspace while this tile's projection
+// runs on the matrix cores, which otherwise leave the CU's memory path idle
+// (more spill beside the projection's operands).  The read is issued after W_out
+// has landed in LDS (the wait for it would also wait for the read) and kept
+// ahead of the MFMAs by a scheduling barrier.
+template <int HB, int R>
+__global__ void __launch_bounds__(kPairThreads)
+module_outer_inv_pair_pf_kernel(const float *__restrict__ ws, const __bf16 *__restrict__ w_out,
+                                __bf16 *__restrict__ y, uint32_t nvalid, uint32_t ntiles)
+{
+    constexpr int A = 16, M = 15, NPF = 8;
+    using Run = RunMap<HB, R>;
+    using SetMap = DropBit5<Run>;
+    __shared__ __attribute__((aligned(16))) float lds[pad(1u << M)];
+    const uint32_t tau = threadIdx.x;
+    const uint32_t voff = SetMap::at(layout_base<M - 5>(tau)) * 4u;
+    auto tile_ws = [&](uint32_t blk) {
+        return buffer(ws + ((size_t)(blk >> HB) << (A + HB)) +
+                          ((size_t)(blk & ((1u << HB) - 1u)) << R),
+                      extent_bytes<Run, A, float>());
+    };
+    // register k of set s (as load_layout<M - 5, SetMap> with the set's offset)
+    auto read = [&](__amdgpu_buffer_rsrc_t r, int k, uint32_t s) {
+        return Elt<float>::load<kTemporal>(
+            r, voff, s * Run::at(1u << 5) * 4u + SetMap::at((uint32_t)k << (M - 5)) * 4u);
+    };
+    float nx[NPF];
+    uint32_t t = blockIdx.x;
+    if (t < ntiles) {
+        const __amdgpu_buffer_rsrc_t r = tile_ws(outer_block<R>(t, ntiles));
+#pragma unroll
+        for (int k = 0; k < NPF; ++k)
+            nx[k] = read(r, k, 0u);
+    }
+    for (; t < ntiles; t += gridDim.x) {   // uniform per workgroup
+        const uint32_t blk = outer_block<R>(t, ntiles);
+        const size_t b = blk >> HB;
+        const uint32_t hi = blk & ((1u << HB) - 1u);
+        const uint32_t valid = tile_valid<A>(nvalid, hi);
+        const bool more = t + gridDim.x < ntiles;
+        const __amdgpu_buffer_rsrc_t rn =
+            tile_ws(more ? outer_block<R>(t + gridDim.x, ntiles) : blk);
+        if (valid == 0) {   // wholly padding: nothing to store
+            if (more) {
+#pragma unroll
+                for (int k = 0; k < NPF; ++k)
+                    nx[k] = read(rn, k, 0u);
+            }
+            continue;
+        }
+        float v0[V], v1[V];
+        {
+            const __amdgpu_buffer_rsrc_t r = tile_ws(blk);
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                v0[k] = k < NPF ? nx[k] : read(r, k, 0u);
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                v1[k] = read(r, k, 1u);
+        }
+        cross_butterflies(v0, v1);   // t bit 5 (the bit groups commute)
+        inverse_to_epilogue<M, 7, true>(lds, v0, tau);   // the last tile's W_out readers first
+        inverse_to_epilogue<M, 7, true>(lds, v1, tau);
+        __syncthreads();             // every thread has read its epilogue-layout values
+        stage_weights_dma<kPairWChunks, kPairThreads>(lds, w_out, tau);
+        bf16x8 zh[kPairKs], zl[kPairKs];
+        split_pair(v0, v1, zh, zl);  // while W_out arrives
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (more) {
+#pragma unroll
+            for (int k = 0; k < NPF; ++k)
+                nx[k] = read(rn, k, 0u);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        project_out_pair(zh, zl, lds, y + b * nvalid + ((size_t)hi << A), valid, tau);
+    }
+}
+
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(__bf16 v) { return (float)v; }
 
@@ -1454,8 +1536,10 @@ hipError_t launch_module_pair(const ModuleArgs &m)
     if ((e = record(m.events[1], st)) != hipSuccess) return e;
     if ((e = launch_middle(middle_args(m, true))) != hipSuccess) return e;
     if ((e = record(m.events[2], st)) != hipSuccess) return e;
-    hipLaunchKernelGGL((module_outer_inv_pair_kernel<HB, R>), grid, block, 0, st, m.ws,
-                       pin + kPairC * kPairC, static_cast<__bf16 *>(m.y), nullptr, m.nvalid);
+    const uint32_t ntiles = (uint32_t)(m.B << HB);
+    hipLaunchKernelGGL((module_outer_inv_pair_pf_kernel<HB, R>),
+                       dim3(ntiles < 256u ? ntiles : 256u), block, 0, st, m.ws,
+                       pin + kPairC * kPairC, static_cast<__bf16 *>(m.y), m.nvalid, ntiles);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return record(m.events[3], st);
 }
