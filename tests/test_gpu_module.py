@@ -184,11 +184,15 @@ def test_module_identity_weights_reduce_to_the_mixer(dev):
     assert errors(y, ym)[0] < 1e-6
 
 
-@pytest.mark.parametrize("shape", [(1, 1 << 19, 256), (1, 139872, 256)],
+@pytest.mark.parametrize("shape", [(1, 1 << 19, 256), (1, 139872, 256), (3, 32768, 256),
+                                   (5, 20000, 256)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_module_c256_large_identity_weights(shape, dev):
     """bf16 C = 256 at 2^27 elements (runs of 16 floats, renumbered outer
-    blocks) and at 2^26 with padding: W_in = W_out = I gives the mixer alone.
+    blocks) and at 2^26 with padding; 3 and 5 slices of 2^23 (384 and 640
+    outer tiles over the inverse pass's 256 persistent workgroups, so some
+    take one tile more than others; the 5 slices padded, with wholly padded
+    tiles stepped over): W_in = W_out = I gives the mixer alone.
     Each output is the nearest bf16 of a float32 value, and the two float32
     values differ by rounding only, so an element may differ by one bf16 ulp
     (2^-7 of its magnitude at most): the bar is 2^-7 normwise."""
