@@ -157,6 +157,32 @@ def test_fused_2_16_large_batch(dev, orc):
     check("2^16 x 64", run_gpu(x, g, "f32", dev), orc.whtmix(x, g), "f32")
 
 
+def test_pair_tiles_two_padded_slices(dev, orc):
+    """Two bf16 slices of 100000 x 512, padded to 2^26: 2048 outer tiles of
+    2^16 over the forward outer pass's 256 persistent workgroups (8 each),
+    among them tiles that straddle the last token and tiles wholly in the
+    padding; the backward takes x and dy in one such launch."""
+    import torch
+    B, N, C, dtype = 2, 100000, 512, "bf16"
+    d = whtmix.plan_describe(B, N, C, dtype)
+    assert (d["plan"], d["log2_slice"]) == ("three_pass", 26)
+    P = whtmix.padded_tokens(N)
+    x, _ = workloads.draw(B, N, C, dtype, seed=71)
+    _, g = workloads.draw(1, P, C, "f32", seed=72)
+    g = g.reshape(P, C)
+    say(f"pair tiles {(B, N, C)} {dtype}")
+    check("forward", run_gpu(x, g, dtype, dev), orc.whtmix(x, g), dtype)
+    dy, _ = workloads.draw(B, N, C, dtype, seed=73)
+    dx, dg = whtmix.backward(to_device(x, dtype, dev), to_device(dy, dtype, dev),
+                             torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize(dev)
+    dx_ref, dg_ref = orc.whtmix_grad(x, dy, g)
+    check("dx", to_host(dx), dx_ref, dtype)
+    e, _ = errors(to_host(dg), dg_ref)
+    say(f"  dG: normwise-max {e:.3e}")
+    assert e <= 1e-5, e
+
+
 SEPARABLE = [(1, 1, 1), (2, 32, 32), (3, 64, 128), (2, 4096, 64), (1, 9216, 64),
              (2, 16384, 128), (1, 1000, 16), (2, 1000, 64)]
 
