@@ -820,14 +820,14 @@ outer_fwd_kernel2_pf(const __bf16 *__restrict__ x0, float *__restrict__ ws0,
     const uint32_t tau = threadIdx.x;
     const uint32_t voff = VG::base(tau) * 2u;
     vu32x4 raw[2][NQ];
-    // issue the loads of tile blk into raw; false (nothing issued) for a
-    // partial tile, which the loop loads itself
     const uint32_t total = x1 ? 2u * ntiles : ntiles;
     // operand and tile of grid-wide tile t
     auto locate = [&](uint32_t t, bool &second) -> uint32_t {
         second = t >= ntiles;
         return outer_block<R>(second ? t - ntiles : t, ntiles);
     };
+    // issue the loads of grid-wide tile t into raw; false (nothing issued)
+    // for a partial tile, which the loop loads itself
     auto issue = [&](uint32_t t) -> bool {
         bool second;
         const uint32_t blk = locate(t, second);
